@@ -1,0 +1,254 @@
+"""Benchmark: one partition's DIGEST GCN rounds on one MI355X.
+
+A step is one round r of Algorithm 1 for the partition: every layer's
+forward (with the pull / push the schedule asks for in that round), the loss
+head, and every layer's backward, all in libdigest.so, replayed from HIP
+graphs with inputs resident in HBM.  Default workload: the Flickr-shaped
+synthetic graph (90,000 nodes in 8 blocks, partition 0, GCN 500 -> 256 -> 7,
+sync interval 10).
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--sync N]
+
+Prints one JSON line: whole-round throughput in GTEPS (aggregation edges of
+the forward and backward per round / time), the roofline of the dominant
+kernel (from a second, instrumented pass with HIP events on the launch
+stream) and the CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GCN layer fwd+bwd GTEPS on one partition; % of HBM / MFMA roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
+
+
+def round_model(st, widths, splits):
+    """Algorithmic bytes / flops per round for each kernel kind.
+
+    Returns {kind: (bytes, flops, launches)} for the kinds that run every
+    round, and per-launch figures for pull/push (their launches depend on
+    the schedule).
+    """
+    n, nh, nnz, nnz_in, nb = st["n_own"], st["n_halo"], st["nnz"], st["nnz_in"], st["n_boundary"]
+    L = len(widths) - 1
+    m = {k: [0.0, 0.0, 0] for k in ("spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
+                                      "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed",
+                                      "softmax_xent")}
+
+    def add(k, b, f=0.0):
+        m[k][0] += b
+        m[k][1] += f
+        m[k][2] += 1
+
+    for l in range(1, L + 1):
+        di, do = widths[l - 1], widths[l]
+        relu = l < L
+        add("spmm_fwd", 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)
+        add("gemm_fwd_relu", 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
+        add("gemm_dw_splitk", 4 * (n * di + n * do * (2 if relu else 1) + di * do),
+            2.0 * n * di * do)
+        if splits[l] > 1:
+            add("splitk_reduce_dw", 4 * (splits[l] + 1) * di * do)
+        if l > 1:
+            narrow = (not relu) and do < di
+            w = do if narrow else di
+            add("spmm_bwd_transposed", 4 * (n + 1) + 8 * nnz_in + 8 * n * w)
+            add("gemm_dgrad", 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
+                2.0 * n * di * do)
+    add("softmax_xent", 4 * (2 * n * widths[-1] + n))
+    per_launch = {
+        "pull_gather": {l: 8.0 * nh * widths[l] + 4 * nh for l in range(L)},
+        "push_scatter": {l: 8.0 * nb * widths[l] + 8 * nb for l in range(1, L)},
+    }
+    return {k: tuple(v) for k, v in m.items()}, per_launch
+
+
+def splitk_factors(n, widths):
+    """Mirror of the library's split-K choice (for the byte model only)."""
+    out = {}
+    for l in range(1, len(widths)):
+        M, N = widths[l - 1], widths[l]
+        tiles = -(-M // 64) * -(-N // 64)
+        s = max(1, min(-(-2048 // max(tiles, 1)), max(1, n // 256), 256))
+        chunk = -(-n // s)
+        chunk = -(-chunk // 16) * 16 or 16
+        out[l] = max(1, -(-n // chunk))
+    return out
+
+
+def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
+    """The oracle as it stands, timed on this host's cores on whole rounds."""
+    import oracle
+    L = cfg.layers
+    op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
+                                part.halo, cfg.widths)
+    stores = [X] + [np.maximum(np.random.default_rng(70 + l).standard_normal(
+        (g.n, cfg.widths[l]), dtype=np.float32), 0) for l in range(1, L)]
+    for lev in range(L):
+        op.pull(lev, stores[lev])
+    x = X[part.owned]
+    t0 = time.perf_counter()
+    rounds = 0
+    while True:
+        rounds += 1
+        do_pull, do_push = oracle.sync_period(K, rounds)
+        h, outs = x, []
+        for l in range(1, L + 1):
+            if do_pull and l >= 2:
+                op.pull(l - 1, stores[l - 1])
+            act = oracle.RELU if l < L else oracle.IDENTITY
+            outs.append((h, op.forward(l, h, Ws[l - 1], act)))
+            h = outs[-1][1]
+            if do_push and l < L:
+                op.push(l, h, stores[l])
+        _, dh = oracle.softmax_xent(h, y)
+        for l in range(L, 0, -1):
+            act = oracle.RELU if l < L else oracle.IDENTITY
+            _, dh = op.backward(l, outs[l - 1][0], Ws[l - 1], outs[l - 1][1], dh, act,
+                                want_dh_in=l > 1)
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    return rounds, time.perf_counter() - t0, oracle.num_threads()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="medium")
+    ap.add_argument("--sync", type=int, default=0, help="sync interval (default: the workload's)")
+    ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graph replay")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one partition on one GPU; runs on more than one GPU are not "
+              "part of this build (--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2206_00057_amd import digest as D
+    from paper_2206_00057_amd import step, synth
+
+    cfg = synth.CONFIGS[args.config]
+    K = args.sync or cfg.sync_periods[-1 if args.config == "halo" else 0]
+    t0 = time.time()
+    g = synth.make_graph(cfg)
+    part = synth.make_partition(cfg, g, 0)
+    st = synth.shape_stats(cfg, g, part)
+    X, Ws, y = synth.features(cfg), synth.weights(cfg), synth.labels(cfg)[part.owned]
+    print(f"[bench] workload {cfg.name}: {st} (inputs {time.time() - t0:.1f}s)",
+          file=sys.stderr, flush=True)
+
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    L = cfg.layers
+    dX, dWs, dy = dev(X), [dev(w) for w in Ws], dev(y)
+    # stores initialised by one full-graph forward at the initial weights (library, no halo)
+    full = step.GpuPartition(g.n, synth.extract_partition(g, np.arange(g.n)), cfg.widths)
+    full.forward(dX, dWs)
+    stores = [dX] + [full.H[l].clone() for l in range(1, L)]
+    del full
+    torch.cuda.synchronize()
+    gp = step.GpuPartition(g.n, part, cfg.widths)
+    x_own = dev(X[part.owned])
+    gp.pull_all(stores)
+
+    def run(r):
+        if args.eager:
+            gp.round(r, K, x_own, dWs, stores, dy)
+        else:
+            gp.replay(r, K)
+
+    if not args.eager:
+        gp.capture(K, x_own, dWs, stores, dy)
+    for r in range(1, args.warmup + 1):
+        run(r)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rounds = range(args.warmup + 1, args.warmup + args.steps + 1)
+    e0.record()
+    for r in rounds:
+        run(r)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    edges = sum(st["nnz"] + (st["nnz_in"] if l > 1 else 0) for l in range(1, L + 1))
+    value = edges * args.steps / (ms * 1e-3) / 1e9
+    print(f"[bench] timed {args.steps} rounds: {ms:.3f} ms", file=sys.stderr, flush=True)
+
+    # instrumented pass over the same rounds: per-kernel durations from HIP events
+    D.digest_profile_enable(gp.p, True)
+    for r in rounds:
+        gp.round(r, K, x_own, dWs, stores, dy)
+    prof = D.digest_profile_read(gp.p)
+    D.digest_profile_enable(gp.p, False)
+    model, per_launch = round_model(st, cfg.widths, splitk_factors(st["n_own"], cfg.widths))
+    kernels = {}
+    for kind, (tot_ms, n_l) in prof.items():
+        if n_l == 0:
+            continue
+        entry = {"launches": n_l, "avg_us": 1e3 * tot_ms / n_l, "total_ms": tot_ms}
+        if kind in model:
+            b, f, per_round = model[kind]
+            b_tot, f_tot = b * args.steps, f * args.steps
+            entry["gbs"] = b_tot / (tot_ms * 1e-3) / 1e9
+            if f:
+                entry["tflops"] = f_tot / (tot_ms * 1e-3) / 1e12
+        elif kind in per_launch:
+            # launches follow the schedule; bytes of one launch averaged over the levels used
+            levels = list(per_launch[kind].values())
+            entry["gbs"] = np.mean(levels) * n_l / (tot_ms * 1e-3) / 1e9
+        kernels[kind] = entry
+    dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+    d = kernels[dom]
+    if "tflops" in d and model[dom][1] / max(model[dom][0], 1) > FP32_MFMA_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3:
+        roof = {"bound": "mfma", "achieved": round(d["tflops"], 3), "peak": FP32_MFMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(d["gbs"] / HBM_PEAK_GBS, 4)}
+    roof.update({"kernel": dom, "avg_launch_us": round(d["avg_us"], 3), "traffic": None})
+
+    cpu = None
+    if not args.no_cpu:
+        nr, secs, cores = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds)
+        cpu = {"value": edges * nr / secs / 1e9, "unit": "GTEPS", "cores": cores, "kind": "oracle",
+               "sample": f"{nr} whole rounds of the same partition (forward, loss, backward, "
+                         f"scheduled pull/push) in {secs:.1f}s, float64 oracle, {cores} threads"}
+
+    out = {
+        "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms / args.steps, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: synthetic block graph, N={g.n:,}, partition 0 "
+                         f"({st['n_own']:,} owned + {st['n_halo']:,} halo rows), "
+                         f"GCN {'->'.join(map(str, cfg.widths))}, sync interval {K}"),
+            "n_global": g.n, "n_own": st["n_own"], "n_halo": st["n_halo"],
+            "n_boundary": st["n_boundary"], "nnz": st["nnz"], "nnz_in": st["nnz_in"],
+            "widths": list(cfg.widths), "sync_interval": K, "edges_per_step": edges,
+            "launch": "eager" if args.eager else "hip-graph replay",
+        },
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
+                        for kk, vv in v.items()} for k, v in kernels.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,227 @@
+/*
+ * digest.h -- C ABI of the MI355X (gfx950) hot path of DIGEST:
+ * one graph partition's GCN layer with stale halo representations, plus the
+ * periodic push/pull of representations through a representation store.
+ *
+ * Paper: "Distributed Graph Neural Network Training with Periodic Stale
+ * Representation Synchronization" (DIGEST), arXiv 2206.00057.
+ *
+ * Model of one partition m (Sec. 2 Eq. 2, Sec. 3.1 Eq. 4-5):
+ *   H^{l} = sigma( P_in H_in^{l-1} W^l + P_out H~_out^{l-1} W^l ),
+ * where P_in / P_out are the columns of the GCN propagation matrix P_m
+ * (rows = the partition's own nodes) that point inside / outside the
+ * partition, H_in are fresh own rows and H~_out are stale rows of the
+ * out-of-partition neighbours ("halo") pulled from the store (Sec. 3.2).
+ *
+ * Conventions for every call below
+ *   - Status: 0 (DIGEST_OK) or a negative digest_status.  On error nothing
+ *     has been enqueued, outputs are untouched and the handle stays valid;
+ *     digest_last_error() returns a message (thread-local).
+ *   - Device pointers are caller-owned (e.g. PyTorch tensors), fp32,
+ *     row-major, contiguous, 4-byte aligned (16-byte aligned rows run
+ *     faster); node ids are int64 at the ABI.
+ *   - hip_stream is a hipStream_t (NULL = the default stream); every device
+ *     call only enqueues work on it and never synchronises the host, except
+ *     digest_profile_read.
+ *   - A handle is not thread-safe; distinct handles are independent.
+ *   - Terminology: "level" l is the representation H^{l} (width d_l);
+ *     layer l (1..L) maps level l-1 to level l.  Level 0 is the feature
+ *     matrix X.  The store of level l is an [n_global, d_l] array.
+ */
+#ifndef DIGEST_H
+#define DIGEST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct digest_partition digest_partition;
+
+typedef enum {
+    DIGEST_OK = 0,
+    DIGEST_EINVAL = -1,  /* malformed argument (ids, CSR, widths, layer/level, NULL) */
+    DIGEST_ENOMEM = -2,  /* host allocation failed, or workspace too small */
+    DIGEST_EHIP = -3,    /* HIP runtime error (message in digest_last_error) */
+    DIGEST_ESTATE = -4   /* call out of order (see each call) */
+} digest_status;
+
+enum { DIGEST_ACT_RELU = 0, DIGEST_ACT_IDENTITY = 1 };
+enum { DIGEST_PUSH_BOUNDARY = 0, DIGEST_PUSH_ALL_OWNED = 1 };
+
+/* Message describing the last non-OK status returned on this thread. */
+const char *digest_last_error(void);
+
+/*
+ * Build one partition (host only: no HIP call is made here).
+ *
+ * Eq. 2 splits a node's neighbours into in-subgraph and out-of-subgraph
+ * sets; Sec. 3.2 defines the out-of-subgraph set of a partition as every
+ * neighbour of an owned node that is not owned ("halo").
+ *
+ *   n_global       number of nodes of the whole graph, 1 <= n_global < 2^31.
+ *   indptr         [n_owned+1] CSR row pointers of P_m: row i belongs to
+ *                  owned[i]; indptr[0] == 0, non-decreasing, nnz < 2^31.
+ *   indices        [nnz] GLOBAL column ids; each must be owned or halo.
+ *                  Repeated (row, column) entries are allowed and summed.
+ *   values         [nnz] entries of P (the GCN-normalised adjacency with
+ *                  self loops, computed by the caller; not renormalised).
+ *   owned          [n_owned] distinct ids in [0, n_global) (n_owned >= 0).
+ *   halo           [n_halo] distinct ids in [0, n_global), disjoint from
+ *                  owned; unreferenced halo ids are allowed.  Halo slot j
+ *                  gets local column n_owned + j.
+ *   n_layers, widths  L >= 1 and d_0..d_L (each in [1, 65536]).
+ *   out            receives the handle.
+ * All host arrays are copied; the caller may free them on return.
+ * Derived here: the local CSR, the boundary rows (owned rows with at least
+ * one halo column, ascending: the rows the push writes), and the CSR of
+ * P_in^T (row c lists the owned rows i with an entry in column c, i
+ * ascending).
+ * Errors: DIGEST_EINVAL for any violation above, DIGEST_ENOMEM.
+ */
+digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
+                                      const int64_t *indices, const float *values,
+                                      const int64_t *owned, int64_t n_owned,
+                                      const int64_t *halo, int64_t n_halo,
+                                      int32_t n_layers, const int32_t *widths,
+                                      digest_partition **out);
+
+/* Release a handle (NULL is ignored).  The bound workspace is the caller's. */
+void digest_partition_destroy(digest_partition *p);
+
+/* Sizes: boundary rows, nnz of P_m, nnz of the owned block P_in, and the
+ * device workspace bytes the handle needs.  Any output pointer may be NULL. */
+digest_status digest_partition_query(const digest_partition *p, int64_t *n_boundary,
+                                     int64_t *nnz, int64_t *nnz_in,
+                                     size_t *workspace_bytes);
+
+/*
+ * Bind caller-allocated device memory (>= workspace_bytes, 256-byte
+ * aligned) and upload the partition's index structures into it on
+ * hip_stream.  The library owns the layout of this memory (local CSR,
+ * P_in^T, id lists, one halo buffer per level, the aggregated input AH of
+ * each layer kept for the backward, reduction scratch) until the next bind
+ * or destroy.  Re-binding resets the pull/forward state.
+ * Errors: DIGEST_EINVAL (NULL, misaligned), DIGEST_ENOMEM (too small),
+ * DIGEST_EHIP.
+ */
+digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr,
+                                              size_t bytes, void *hip_stream);
+
+/* Test hook (host arrays, host-side copy of the maps; any may be NULL):
+ * col_local[nnz] local column numbers, boundary_gid / boundary_local
+ * [n_boundary] global ids and owned-row numbers of the pushed rows. */
+digest_status digest_partition_export_maps(const digest_partition *p, int32_t *col_local,
+                                           int64_t *boundary_gid,
+                                           int32_t *boundary_local);
+
+/* Test hook: CSR of P_in^T (t_indptr[n_owned+1], t_src[nnz_in], t_vals[nnz_in]). */
+digest_status digest_partition_export_transpose(const digest_partition *p,
+                                                int64_t *t_indptr, int32_t *t_src,
+                                                float *t_vals);
+
+/* Test hook: copy the halo buffer of `level` ([n_halo, d_level], filled by
+ * digest_pull) into the caller's device array `out` on hip_stream.
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP. */
+digest_status digest_partition_read_halo(const digest_partition *p, int32_t level, float *out,
+                                         void *hip_stream);
+
+/*
+ * Pull (Sec. 3.2; Algorithm 1 pulls when r mod N == 0): gather the stale
+ * rows of the halo nodes of level `level` out of the store into the
+ * handle's halo buffer of that level:  halo_buf[j, :] = store[halo[j], :].
+ *   level  0..L-1 (level 0 = the static features X, pulled once).
+ *   store  device [n_global, d_level].
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace bound), DIGEST_EHIP.
+ */
+digest_status digest_pull(digest_partition *p, int32_t level, const float *store,
+                          void *hip_stream);
+
+/*
+ * Push (Sec. 3.2; Algorithm 1 pushes when (r-1) mod N == 0): write freshly
+ * computed own rows of level `level` into the store:
+ *   store[owned[b], :] = h_own[b, :]  for b in the boundary rows
+ *   (mode DIGEST_PUSH_BOUNDARY, the only rows another partition reads), or
+ *   for every owned row (mode DIGEST_PUSH_ALL_OWNED, the paper's wording).
+ * Other store rows are untouched.
+ *   level  1..L-1 (the stale levels; level 0 is static, level L is never
+ *          stored).   h_own  device [n_owned, d_level].
+ *   store  device [n_global, d_level].
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP.
+ */
+digest_status digest_push(digest_partition *p, int32_t level, const float *h_own,
+                          float *store, int32_t mode, void *hip_stream);
+
+/*
+ * Layer forward (Eq. 5):  AH = P_in h_in + P_out halo_buf[layer-1]
+ * (two-source sparse aggregation), then h_out = act(AH W).  AH is kept in
+ * the workspace for digest_layer_backward of the same layer.
+ *   layer  1..L.   h_in  device [n_owned, d_{layer-1}] (fresh own rows).
+ *   w      device [d_{layer-1}, d_layer].   h_out device [n_owned, d_layer].
+ *   act    DIGEST_ACT_RELU or DIGEST_ACT_IDENTITY (the paper uses ReLU on
+ *          hidden layers and raw logits at the last layer).
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace, or level layer-1 never
+ * pulled while the partition has halo nodes), DIGEST_EHIP.
+ */
+digest_status digest_layer_forward(digest_partition *p, int32_t layer, const float *h_in,
+                                   const float *w, float *h_out, int32_t act,
+                                   void *hip_stream);
+
+/*
+ * Layer backward (Eq. 6 with the upstream gradient; GCN backward of
+ * Appendix A.3), using the AH saved by the last forward of `layer`:
+ *   D     = dh_out * 1[h_out > 0]  (ReLU) or dh_out (identity)
+ *   dw    = AH^T D                              (overwritten)
+ *   dh_in = P_in^T (D W^T)   if dh_in != NULL   (overwritten)
+ * The stale halo rows are constants of the layer: they get no gradient.
+ *   h_out, dh_out device [n_owned, d_layer];  w device [d_{layer-1}, d_layer];
+ *   dw device [d_{layer-1}, d_layer];  dh_in device [n_owned, d_{layer-1}].
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no forward of this layer since the
+ * workspace was bound), DIGEST_EHIP.
+ */
+digest_status digest_layer_backward(digest_partition *p, int32_t layer,
+                                    const float *h_out, const float *dh_out,
+                                    const float *w, float *dw, float *dh_in,
+                                    void *hip_stream);
+
+/*
+ * Local loss head (Eq. 3 with cross entropy), over all n_owned rows:
+ *   loss    = -(1/n) sum_i log softmax(logits_i)[labels_i]   (device, 1 float)
+ *   dlogits = (softmax(logits) - onehot(labels)) / n          [n_owned, d_L]
+ *   labels  device int32 [n_owned]; a label outside [0, d_L) makes that
+ *           row's dlogits zero and the loss NaN (checked on the device).
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP.
+ */
+digest_status digest_softmax_xent(digest_partition *p, const float *logits,
+                                  const int32_t *labels, float *dlogits, float *loss,
+                                  void *hip_stream);
+
+/*
+ * Synchronisation schedule of Algorithm 1 (pure, host only): in round
+ * iter (1-based) with interval K >= 1, *do_pull = (iter mod K == 0) and
+ * *do_push = ((iter-1) mod K == 0); both apply to levels 1..L-1.
+ * Errors: DIGEST_EINVAL (K < 1, iter < 1, NULL).
+ */
+digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull,
+                                 int32_t *do_push);
+
+/*
+ * Instrumentation: while enabled, every kernel the handle launches is
+ * bracketed by HIP events on its own stream.  digest_profile_read
+ * synchronises on those events and returns, per kernel kind, the summed
+ * duration (ms) and launch count since the last read (then clears them).
+ * Kernel kinds are numbered 0..digest_profile_kernel_count()-1.
+ */
+digest_status digest_profile_enable(digest_partition *p, int32_t on);
+digest_status digest_profile_read(digest_partition *p, double *total_ms /*[count]*/,
+                                  int64_t *launches /*[count]*/);
+int32_t digest_profile_kernel_count(void);
+const char *digest_profile_kernel_name(int32_t kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DIGEST_H */

@@ -1,0 +1,786 @@
+// Host side of the DIGEST per-partition library: argument validation, the
+// partition's index maps (Eq. 2; halo and push sets of Sec. 3.2), the
+// workspace layout, and the launch sequence of each C-ABI call.
+#include "digest.h"
+#include "kernels.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using digest::FixupItem;
+using digest::SpmmItem;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+digest_status fail(digest_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+// Kernel kinds reported by the instrumentation.
+enum Kind : int32_t {
+    K_PULL = 0,
+    K_PUSH,
+    K_SPMM_FWD,
+    K_FIXUP_FWD,
+    K_GEMM_FWD,
+    K_GEMM_DW,
+    K_REDUCE_DW,
+    K_GEMM_DH,
+    K_SPMM_BWD,
+    K_FIXUP_BWD,
+    K_LOSS,
+    K_COUNT
+};
+const char *const kKindNames[K_COUNT] = {
+    "pull_gather", "push_scatter", "spmm_fwd", "spmm_fwd_fixup", "gemm_fwd_relu",
+    "gemm_dw_splitk", "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed",
+    "spmm_bwd_fixup", "softmax_xent"};
+
+// Largest number of CSR entries one aggregation work item takes; longer
+// rows are cut into several items whose partial sums a fixup pass adds.
+constexpr int32_t kSegment = 256;
+constexpr size_t kAlign = 256;
+constexpr int32_t kMaxWidth = 65536;
+constexpr int32_t kMaxLayers = 64;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Split-K factor for a contraction with an M x N result over K.
+void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchunk)
+{
+    const int64_t tiles = ((M + digest::kGemmBM - 1) / digest::kGemmBM) *
+                          ((N + digest::kGemmBN - 1) / digest::kGemmBN);
+    int64_t s = (2048 + tiles - 1) / std::max<int64_t>(tiles, 1);
+    const int64_t max_by_k = std::max<int64_t>(1, K / 256);   // at least 256 rows per split
+    s = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s, max_by_k), 256));
+    int64_t chunk = (K + s - 1) / std::max<int64_t>(s, 1);
+    chunk = (chunk + digest::kGemmBK - 1) / digest::kGemmBK * digest::kGemmBK;
+    if (chunk <= 0)
+        chunk = digest::kGemmBK;
+    s = std::max<int64_t>(1, (K + chunk - 1) / chunk);
+    splits = (int32_t)s;
+    kchunk = (int32_t)chunk;
+}
+
+void build_items(const std::vector<int32_t> &rowptr, int32_t n_rows, std::vector<SpmmItem> &items,
+                 std::vector<FixupItem> &fix, int32_t &n_slots)
+{
+    items.clear();
+    fix.clear();
+    n_slots = 0;
+    // Long rows first (their segments start early), then rows in order.
+    for (int32_t r = 0; r < n_rows; ++r) {
+        const int32_t kb = rowptr[r], ke = rowptr[r + 1];
+        if (ke - kb > kSegment) {
+            const int32_t nseg = (ke - kb + kSegment - 1) / kSegment;
+            fix.push_back({r, n_slots, nseg, 0});
+            for (int32_t s = 0; s < nseg; ++s) {
+                const int32_t a = kb + s * kSegment;
+                items.push_back({r, a, std::min(ke, a + kSegment), -(n_slots + s) - 1});
+            }
+            n_slots += nseg;
+        }
+    }
+    for (int32_t r = 0; r < n_rows; ++r) {
+        const int32_t kb = rowptr[r], ke = rowptr[r + 1];
+        if (ke - kb <= kSegment)
+            items.push_back({r, kb, ke, r});
+    }
+}
+
+}  // namespace
+
+struct digest_partition {
+    int64_t n_global = 0;
+    int32_t n_own = 0, n_halo = 0, n_bnd = 0;
+    int64_t nnz = 0, nnz_in = 0;
+    int32_t L = 0;
+    std::vector<int32_t> widths;
+
+    // host copies of everything uploaded at bind time
+    std::vector<int32_t> rowptr, col, t_rowptr, t_src, halo_gid, bnd_local, bnd_gid, owned_gid;
+    std::vector<float> val, t_val;
+    std::vector<SpmmItem> items_f, items_t;
+    std::vector<FixupItem> fix_f, fix_t;
+    int32_t slots_f = 0, slots_t = 0;
+
+    struct Layout {
+        size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
+        size_t items_f, items_t, fix_f, fix_t;
+        std::vector<size_t> halo_buf;   // per level 0..L-1
+        std::vector<size_t> ah;         // per layer 1..L (index 0 unused)
+        size_t tmp, spmm_part, gemm_part, loss_part;
+        size_t total;
+    } lay{};
+
+    char *ws = nullptr;
+    std::vector<char> pulled;     // per level
+    std::vector<char> fwd_done;   // per layer
+    std::vector<int32_t> act;     // per layer
+
+    bool prof = false;
+    struct Rec {
+        int32_t kind;
+        hipEvent_t a, b;
+    };
+    std::vector<Rec> recs;
+    std::vector<hipEvent_t> pool;
+
+    template <class T>
+    T *at(size_t off) const
+    {
+        return reinterpret_cast<T *>(ws + off);
+    }
+};
+
+namespace {
+
+void plan_layout(digest_partition &p)
+{
+    auto &l = p.lay;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t r = o;
+        o += align_up(std::max<size_t>(bytes, 1));
+        return r;
+    };
+    l.rowptr = take(sizeof(int32_t) * (p.n_own + 1));
+    l.col = take(sizeof(int32_t) * p.nnz);
+    l.val = take(sizeof(float) * p.nnz);
+    l.t_rowptr = take(sizeof(int32_t) * (p.n_own + 1));
+    l.t_src = take(sizeof(int32_t) * p.nnz_in);
+    l.t_val = take(sizeof(float) * p.nnz_in);
+    l.halo_gid = take(sizeof(int32_t) * p.n_halo);
+    l.bnd_local = take(sizeof(int32_t) * p.n_bnd);
+    l.bnd_gid = take(sizeof(int32_t) * p.n_bnd);
+    l.owned_gid = take(sizeof(int32_t) * p.n_own);
+    l.items_f = take(sizeof(SpmmItem) * p.items_f.size());
+    l.items_t = take(sizeof(SpmmItem) * p.items_t.size());
+    l.fix_f = take(sizeof(FixupItem) * p.fix_f.size());
+    l.fix_t = take(sizeof(FixupItem) * p.fix_t.size());
+    l.halo_buf.assign(p.L, 0);
+    for (int32_t lev = 0; lev < p.L; ++lev)
+        l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * p.widths[lev]);
+    l.ah.assign(p.L + 1, 0);
+    for (int32_t k = 1; k <= p.L; ++k)
+        l.ah[k] = take(sizeof(float) * (size_t)p.n_own * p.widths[k - 1]);
+    int64_t wmax = 0, din_max = 0, gemm_part = 0;
+    for (int32_t k = 1; k <= p.L; ++k) {
+        const int64_t di = p.widths[k - 1], dout = p.widths[k];
+        wmax = std::max({wmax, di, dout});
+        din_max = std::max(din_max, di);
+        int32_t splits, kchunk;
+        splitk_plan(di, dout, p.n_own, splits, kchunk);
+        if (splits > 1)
+            gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
+    }
+    l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
+    const int64_t part = std::max<int64_t>((int64_t)p.slots_f * din_max, (int64_t)p.slots_t * wmax);
+    l.spmm_part = take(sizeof(float) * (size_t)part);
+    l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
+    l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own));
+    l.total = o;
+}
+
+// RAII bracket of one kernel launch for the instrumentation.
+struct Timed {
+    digest_partition *p;
+    hipStream_t s;
+    hipEvent_t b = nullptr;
+    Timed(digest_partition *p_, int32_t kind, hipStream_t s_) : p(p_), s(s_)
+    {
+        if (!p->prof)
+            return;
+        auto get = [&]() {
+            hipEvent_t e = nullptr;
+            if (!p->pool.empty()) {
+                e = p->pool.back();
+                p->pool.pop_back();
+            } else if (hipEventCreate(&e) != hipSuccess) {
+                e = nullptr;
+            }
+            return e;
+        };
+        hipEvent_t a = get();
+        b = get();
+        if (!a || !b) {
+            if (a)
+                p->pool.push_back(a);
+            if (b)
+                p->pool.push_back(b);
+            b = nullptr;
+            return;
+        }
+        (void)hipEventRecord(a, s);
+        p->recs.push_back({kind, a, b});
+    }
+    ~Timed()
+    {
+        if (b)
+            (void)hipEventRecord(b, s);
+    }
+};
+
+digest_status hip_check(hipError_t e, const char *what)
+{
+    if (e != hipSuccess)
+        return fail(DIGEST_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return DIGEST_OK;
+}
+
+digest_status need_bound(const digest_partition *p)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    if (!p->ws)
+        return fail(DIGEST_ESTATE, "no workspace bound");
+    return DIGEST_OK;
+}
+
+// Sparse aggregation with its long-row fixup.
+digest_status run_spmm(digest_partition *p, bool transposed, const float *src0,
+                       const float *src1, int32_t d, float *out, hipStream_t s)
+{
+    const auto &items = transposed ? p->items_t : p->items_f;
+    const auto &fix = transposed ? p->fix_t : p->fix_f;
+    const int32_t *colp = p->at<int32_t>(transposed ? p->lay.t_src : p->lay.col);
+    const float *valp = p->at<float>(transposed ? p->lay.t_val : p->lay.val);
+    float *part = p->at<float>(p->lay.spmm_part);
+    {
+        Timed t(p, transposed ? K_SPMM_BWD : K_SPMM_FWD, s);
+        digest_status st = hip_check(
+            digest::launch_spmm(p->at<SpmmItem>(transposed ? p->lay.items_t : p->lay.items_f),
+                                (int32_t)items.size(), colp, valp, src0, src1, p->n_own, d, out,
+                                part, s),
+            "spmm");
+        if (st)
+            return st;
+    }
+    if (!fix.empty()) {
+        Timed t(p, transposed ? K_FIXUP_BWD : K_FIXUP_FWD, s);
+        return hip_check(
+            digest::launch_spmm_fixup(p->at<FixupItem>(transposed ? p->lay.fix_t : p->lay.fix_f),
+                                      (int32_t)fix.size(), d, part, out, s),
+            "spmm fixup");
+    }
+    return DIGEST_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *digest_last_error(void) { return g_last_error.c_str(); }
+
+digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
+                                      const int64_t *indices, const float *values,
+                                      const int64_t *owned, int64_t n_owned,
+                                      const int64_t *halo, int64_t n_halo,
+                                      int32_t n_layers, const int32_t *widths,
+                                      digest_partition **out)
+{
+    if (!out)
+        return fail(DIGEST_EINVAL, "out is NULL");
+    if (n_global < 1 || n_global >= INT32_MAX)
+        return fail(DIGEST_EINVAL, "n_global must be in [1, 2^31-1)");
+    if (n_owned < 0 || n_owned > n_global || n_halo < 0 || n_halo > n_global ||
+        n_owned + n_halo > n_global)
+        return fail(DIGEST_EINVAL, "n_owned / n_halo out of range");
+    if (!indptr || (n_owned > 0 && !owned) || (n_halo > 0 && !halo))
+        return fail(DIGEST_EINVAL, "NULL id or indptr array");
+    if (n_layers < 1 || n_layers > kMaxLayers || !widths)
+        return fail(DIGEST_EINVAL, "n_layers must be in [1, %d] and widths non-NULL", kMaxLayers);
+    for (int32_t k = 0; k <= n_layers; ++k)
+        if (widths[k] < 1 || widths[k] > kMaxWidth)
+            return fail(DIGEST_EINVAL, "widths[%d] = %d outside [1, %d]", k, widths[k], kMaxWidth);
+    if (indptr[0] != 0)
+        return fail(DIGEST_EINVAL, "indptr[0] must be 0");
+    for (int64_t i = 0; i < n_owned; ++i)
+        if (indptr[i + 1] < indptr[i])
+            return fail(DIGEST_EINVAL, "indptr decreases at row %lld", (long long)i);
+    const int64_t nnz = indptr[n_owned];
+    if (nnz >= INT32_MAX)
+        return fail(DIGEST_EINVAL, "nnz must be < 2^31");
+    if (nnz > 0 && (!indices || !values))
+        return fail(DIGEST_EINVAL, "NULL indices or values");
+
+    digest_partition *p = new (std::nothrow) digest_partition();
+    if (!p)
+        return fail(DIGEST_ENOMEM, "out of host memory");
+    try {
+        p->n_global = n_global;
+        p->n_own = (int32_t)n_owned;
+        p->n_halo = (int32_t)n_halo;
+        p->nnz = nnz;
+        p->L = n_layers;
+        p->widths.assign(widths, widths + n_layers + 1);
+
+        // global id -> local number (owned i -> i, halo j -> n_own + j)
+        std::vector<int32_t> local((size_t)n_global, -1);
+        p->owned_gid.resize(n_owned);
+        for (int64_t i = 0; i < n_owned; ++i) {
+            const int64_t g = owned[i];
+            if (g < 0 || g >= n_global || local[g] != -1) {
+                delete p;
+                return fail(DIGEST_EINVAL, "owned[%lld] = %lld is out of range or repeated",
+                            (long long)i, (long long)g);
+            }
+            local[g] = (int32_t)i;
+            p->owned_gid[i] = (int32_t)g;
+        }
+        p->halo_gid.resize(n_halo);
+        for (int64_t j = 0; j < n_halo; ++j) {
+            const int64_t g = halo[j];
+            if (g < 0 || g >= n_global || local[g] != -1) {
+                delete p;
+                return fail(DIGEST_EINVAL,
+                            "halo[%lld] = %lld is out of range, repeated or owned",
+                            (long long)j, (long long)g);
+            }
+            local[g] = (int32_t)(n_owned + j);
+            p->halo_gid[j] = (int32_t)g;
+        }
+
+        // local CSR and the boundary (rows that read at least one halo column)
+        p->rowptr.resize(n_owned + 1);
+        p->col.resize(nnz);
+        p->val.assign(values, values + nnz);
+        p->rowptr[0] = 0;
+        for (int64_t i = 0; i < n_owned; ++i) {
+            bool reads_halo = false;
+            for (int64_t k = indptr[i]; k < indptr[i + 1]; ++k) {
+                const int64_t g = indices[k];
+                if (g < 0 || g >= n_global || local[g] < 0) {
+                    delete p;
+                    return fail(DIGEST_EINVAL,
+                                "column %lld of row %lld is neither owned nor halo",
+                                (long long)g, (long long)i);
+                }
+                const int32_t c = local[g];
+                p->col[k] = c;
+                reads_halo |= c >= n_owned;
+            }
+            p->rowptr[i + 1] = (int32_t)indptr[i + 1];
+            if (reads_halo) {
+                p->bnd_local.push_back((int32_t)i);
+                p->bnd_gid.push_back((int32_t)owned[i]);
+            }
+        }
+        p->n_bnd = (int32_t)p->bnd_local.size();
+
+        // CSR of P_in^T by a stable counting sort on the owned column
+        p->t_rowptr.assign(n_owned + 1, 0);
+        for (int64_t k = 0; k < nnz; ++k)
+            if (p->col[k] < n_owned)
+                p->t_rowptr[p->col[k] + 1] += 1;
+        for (int64_t c = 0; c < n_owned; ++c)
+            p->t_rowptr[c + 1] += p->t_rowptr[c];
+        p->nnz_in = p->t_rowptr[n_owned];
+        p->t_src.resize(p->nnz_in);
+        p->t_val.resize(p->nnz_in);
+        std::vector<int32_t> next(p->t_rowptr.begin(), p->t_rowptr.end() - 1);
+        for (int32_t i = 0; i < (int32_t)n_owned; ++i)
+            for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k) {
+                const int32_t c = p->col[k];
+                if (c < n_owned) {
+                    p->t_src[next[c]] = i;
+                    p->t_val[next[c]] = p->val[k];
+                    ++next[c];
+                }
+            }
+
+        build_items(p->rowptr, p->n_own, p->items_f, p->fix_f, p->slots_f);
+        build_items(p->t_rowptr, p->n_own, p->items_t, p->fix_t, p->slots_t);
+        plan_layout(*p);
+        p->pulled.assign(p->L, 0);
+        p->fwd_done.assign(p->L + 1, 0);
+        p->act.assign(p->L + 1, DIGEST_ACT_RELU);
+    } catch (const std::bad_alloc &) {
+        delete p;
+        return fail(DIGEST_ENOMEM, "out of host memory");
+    }
+    *out = p;
+    return DIGEST_OK;
+}
+
+void digest_partition_destroy(digest_partition *p)
+{
+    if (!p)
+        return;
+    for (auto &r : p->recs) {
+        (void)hipEventDestroy(r.a);
+        (void)hipEventDestroy(r.b);
+    }
+    for (auto e : p->pool)
+        (void)hipEventDestroy(e);
+    delete p;
+}
+
+digest_status digest_partition_query(const digest_partition *p, int64_t *n_boundary,
+                                     int64_t *nnz, int64_t *nnz_in, size_t *workspace_bytes)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    if (n_boundary)
+        *n_boundary = p->n_bnd;
+    if (nnz)
+        *nnz = p->nnz;
+    if (nnz_in)
+        *nnz_in = p->nnz_in;
+    if (workspace_bytes)
+        *workspace_bytes = p->lay.total;
+    return DIGEST_OK;
+}
+
+digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr, size_t bytes,
+                                              void *hip_stream)
+{
+    if (!p || !dev_ptr)
+        return fail(DIGEST_EINVAL, "NULL handle or workspace");
+    if ((uintptr_t)dev_ptr % kAlign)
+        return fail(DIGEST_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+    if (bytes < p->lay.total)
+        return fail(DIGEST_ENOMEM, "workspace has %zu bytes, needs %zu", bytes, p->lay.total);
+    hipStream_t s = (hipStream_t)hip_stream;
+    char *ws = (char *)dev_ptr;
+    struct Up {
+        size_t off;
+        const void *src;
+        size_t bytes;
+    };
+    const auto &l = p->lay;
+    const Up ups[] = {
+        {l.rowptr, p->rowptr.data(), sizeof(int32_t) * p->rowptr.size()},
+        {l.col, p->col.data(), sizeof(int32_t) * p->col.size()},
+        {l.val, p->val.data(), sizeof(float) * p->val.size()},
+        {l.t_rowptr, p->t_rowptr.data(), sizeof(int32_t) * p->t_rowptr.size()},
+        {l.t_src, p->t_src.data(), sizeof(int32_t) * p->t_src.size()},
+        {l.t_val, p->t_val.data(), sizeof(float) * p->t_val.size()},
+        {l.halo_gid, p->halo_gid.data(), sizeof(int32_t) * p->halo_gid.size()},
+        {l.bnd_local, p->bnd_local.data(), sizeof(int32_t) * p->bnd_local.size()},
+        {l.bnd_gid, p->bnd_gid.data(), sizeof(int32_t) * p->bnd_gid.size()},
+        {l.owned_gid, p->owned_gid.data(), sizeof(int32_t) * p->owned_gid.size()},
+        {l.items_f, p->items_f.data(), sizeof(SpmmItem) * p->items_f.size()},
+        {l.items_t, p->items_t.data(), sizeof(SpmmItem) * p->items_t.size()},
+        {l.fix_f, p->fix_f.data(), sizeof(FixupItem) * p->fix_f.size()},
+        {l.fix_t, p->fix_t.data(), sizeof(FixupItem) * p->fix_t.size()},
+    };
+    for (const Up &u : ups) {
+        if (!u.bytes)
+            continue;
+        digest_status st = hip_check(
+            hipMemcpyAsync(ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s), "upload");
+        if (st)
+            return st;
+    }
+    p->ws = ws;
+    std::fill(p->pulled.begin(), p->pulled.end(), 0);
+    std::fill(p->fwd_done.begin(), p->fwd_done.end(), 0);
+    return DIGEST_OK;
+}
+
+digest_status digest_partition_export_maps(const digest_partition *p, int32_t *col_local,
+                                           int64_t *boundary_gid, int32_t *boundary_local)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    if (col_local)
+        std::copy(p->col.begin(), p->col.end(), col_local);
+    if (boundary_gid)
+        for (int32_t b = 0; b < p->n_bnd; ++b)
+            boundary_gid[b] = p->bnd_gid[b];
+    if (boundary_local)
+        std::copy(p->bnd_local.begin(), p->bnd_local.end(), boundary_local);
+    return DIGEST_OK;
+}
+
+digest_status digest_partition_export_transpose(const digest_partition *p, int64_t *t_indptr,
+                                                int32_t *t_src, float *t_vals)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    if (t_indptr)
+        for (size_t c = 0; c < p->t_rowptr.size(); ++c)
+            t_indptr[c] = p->t_rowptr[c];
+    if (t_src)
+        std::copy(p->t_src.begin(), p->t_src.end(), t_src);
+    if (t_vals)
+        std::copy(p->t_val.begin(), p->t_val.end(), t_vals);
+    return DIGEST_OK;
+}
+
+digest_status digest_partition_read_halo(const digest_partition *p, int32_t level, float *out,
+                                         void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (level < 0 || level >= p->L || !out)
+        return fail(DIGEST_EINVAL, "bad level %d or NULL output", level);
+    const size_t bytes = sizeof(float) * (size_t)p->n_halo * p->widths[level];
+    if (!bytes)
+        return DIGEST_OK;
+    return hip_check(hipMemcpyAsync(out, p->at<float>(p->lay.halo_buf[level]), bytes,
+                                    hipMemcpyDeviceToDevice, (hipStream_t)hip_stream),
+                     "read halo");
+}
+
+digest_status digest_pull(digest_partition *p, int32_t level, const float *store,
+                          void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (level < 0 || level >= p->L)
+        return fail(DIGEST_EINVAL, "pull level %d outside [0, %d)", level, p->L);
+    if (!store)
+        return fail(DIGEST_EINVAL, "store is NULL");
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (p->n_halo > 0) {
+        Timed t(p, K_PULL, s);
+        digest_status st = hip_check(
+            digest::launch_copy_rows(p->at<int32_t>(p->lay.halo_gid), nullptr, p->n_halo,
+                                     p->widths[level], store,
+                                     p->at<float>(p->lay.halo_buf[level]), s),
+            "pull");
+        if (st)
+            return st;
+    }
+    p->pulled[level] = 1;
+    return DIGEST_OK;
+}
+
+digest_status digest_push(digest_partition *p, int32_t level, const float *h_own, float *store,
+                          int32_t mode, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (level < 1 || level >= p->L)
+        return fail(DIGEST_EINVAL, "push level %d outside [1, %d)", level, p->L);
+    if (!h_own || !store)
+        return fail(DIGEST_EINVAL, "h_own or store is NULL");
+    if (mode != DIGEST_PUSH_BOUNDARY && mode != DIGEST_PUSH_ALL_OWNED)
+        return fail(DIGEST_EINVAL, "unknown push mode %d", mode);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const bool all = mode == DIGEST_PUSH_ALL_OWNED;
+    const int32_t rows = all ? p->n_own : p->n_bnd;
+    if (rows == 0)
+        return DIGEST_OK;
+    Timed t(p, K_PUSH, s);
+    return hip_check(digest::launch_copy_rows(
+                         all ? nullptr : p->at<int32_t>(p->lay.bnd_local),
+                         p->at<int32_t>(all ? p->lay.owned_gid : p->lay.bnd_gid), rows,
+                         p->widths[level], h_own, store, s),
+                     "push");
+}
+
+digest_status digest_layer_forward(digest_partition *p, int32_t layer, const float *h_in,
+                                   const float *w, float *h_out, int32_t act, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    if (act != DIGEST_ACT_RELU && act != DIGEST_ACT_IDENTITY)
+        return fail(DIGEST_EINVAL, "unknown activation %d", act);
+    if (p->n_own > 0 && (!h_in || !w || !h_out))
+        return fail(DIGEST_EINVAL, "NULL h_in, w or h_out");
+    if (p->n_halo > 0 && !p->pulled[layer - 1])
+        return fail(DIGEST_ESTATE, "level %d was never pulled", layer - 1);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    float *ah = p->at<float>(p->lay.ah[layer]);
+    if (p->n_own > 0) {
+        digest_status st = run_spmm(p, false, h_in,
+                                    p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1])
+                                                  : nullptr,
+                                    d_in, ah, s);
+        if (st)
+            return st;
+        digest::GemmArgs g{};
+        g.M = p->n_own;
+        g.N = d_out;
+        g.K = d_in;
+        g.A = ah;
+        g.lda = d_in;
+        g.B = w;
+        g.ldb = d_out;
+        g.C = h_out;
+        g.ldc = d_out;
+        g.relu = act == DIGEST_ACT_RELU;
+        g.splits = 1;
+        g.kchunk = d_in;
+        Timed t(p, K_GEMM_FWD, s);
+        st = hip_check(digest::launch_gemm(g, s), "forward gemm");
+        if (st)
+            return st;
+    }
+    p->fwd_done[layer] = 1;
+    p->act[layer] = act;
+    return DIGEST_OK;
+}
+
+digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_out,
+                                    const float *dh_out, const float *w, float *dw,
+                                    float *dh_in, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    if (!dw || !w || (p->n_own > 0 && (!h_out || !dh_out)))
+        return fail(DIGEST_EINVAL, "NULL h_out, dh_out, w or dw");
+    if (!p->fwd_done[layer])
+        return fail(DIGEST_ESTATE, "no forward of layer %d since the workspace was bound",
+                    layer);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const bool relu = p->act[layer] == DIGEST_ACT_RELU;
+    const float *ah = p->at<float>(p->lay.ah[layer]);
+
+    // dW = AH^T D, D = dh_out (masked by h_out > 0 for ReLU), split over rows.
+    digest::GemmArgs g{};
+    g.M = d_in;
+    g.N = d_out;
+    g.K = p->n_own;
+    g.A = ah;
+    g.lda = d_in;
+    g.a_trans = true;
+    g.B = dh_out;
+    g.ldb = d_out;
+    g.b_mask = relu ? h_out : nullptr;
+    splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
+    float *gpart = p->at<float>(p->lay.gemm_part);
+    g.C = g.splits > 1 ? gpart : dw;
+    g.ldc = d_out;
+    {
+        Timed t(p, K_GEMM_DW, s);
+        if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
+            return st;
+    }
+    if (g.splits > 1) {
+        Timed t(p, K_REDUCE_DW, s);
+        if (digest_status st = hip_check(
+                digest::launch_splitk_reduce(gpart, g.splits, (int64_t)d_in * d_out, dw, s),
+                "dW reduce"))
+            return st;
+    }
+    if (!dh_in || p->n_own == 0)
+        return DIGEST_OK;
+
+    float *tmp = p->at<float>(p->lay.tmp);
+    digest::GemmArgs h{};
+    h.M = p->n_own;
+    h.N = d_in;
+    h.K = d_out;
+    h.B = w;
+    h.ldb = d_out;
+    h.b_trans = true;
+    h.ldc = d_in;
+    h.splits = 1;
+    h.kchunk = d_out;
+    if (!relu && d_out < d_in) {
+        // Narrow output: aggregate D first (width d_out), then (P_in^T D) W^T.
+        if (digest_status st = run_spmm(p, true, dh_out, nullptr, d_out, tmp, s))
+            return st;
+        h.A = tmp;
+        h.lda = d_out;
+        h.C = dh_in;
+        Timed t(p, K_GEMM_DH, s);
+        return hip_check(digest::launch_gemm(h, s), "dgrad gemm");
+    }
+    // Otherwise G = D W^T (mask fused into the operand load), then P_in^T G.
+    h.A = dh_out;
+    h.lda = d_out;
+    h.a_mask = relu ? h_out : nullptr;
+    h.C = tmp;
+    {
+        Timed t(p, K_GEMM_DH, s);
+        if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
+            return st;
+    }
+    return run_spmm(p, true, tmp, nullptr, d_in, dh_in, s);
+}
+
+digest_status digest_softmax_xent(digest_partition *p, const float *logits,
+                                  const int32_t *labels, float *dlogits, float *loss,
+                                  void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (!loss || (p->n_own > 0 && (!logits || !labels || !dlogits)))
+        return fail(DIGEST_EINVAL, "NULL logits, labels, dlogits or loss");
+    hipStream_t s = (hipStream_t)hip_stream;
+    Timed t(p, K_LOSS, s);
+    return hip_check(digest::launch_softmax_xent(logits, labels, p->n_own, p->widths[p->L],
+                                                 dlogits, p->at<float>(p->lay.loss_part), loss,
+                                                 s),
+                     "softmax xent");
+}
+
+digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull, int32_t *do_push)
+{
+    if (K < 1 || iter < 1 || !do_pull || !do_push)
+        return fail(DIGEST_EINVAL, "need K >= 1, iter >= 1 and non-NULL outputs");
+    *do_pull = (iter % K) == 0;
+    *do_push = ((iter - 1) % K) == 0;
+    return DIGEST_OK;
+}
+
+digest_status digest_profile_enable(digest_partition *p, int32_t on)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    p->prof = on != 0;
+    return DIGEST_OK;
+}
+
+digest_status digest_profile_read(digest_partition *p, double *total_ms, int64_t *launches)
+{
+    if (!p || !total_ms || !launches)
+        return fail(DIGEST_EINVAL, "NULL argument");
+    for (int32_t k = 0; k < K_COUNT; ++k) {
+        total_ms[k] = 0.0;
+        launches[k] = 0;
+    }
+    digest_status st = DIGEST_OK;
+    for (auto &r : p->recs) {
+        if (!st) {
+            hipError_t e = hipEventSynchronize(r.b);
+            float ms = 0.f;
+            if (e == hipSuccess)
+                e = hipEventElapsedTime(&ms, r.a, r.b);
+            if (e != hipSuccess)
+                st = hip_check(e, "profile read");
+            total_ms[r.kind] += ms;
+            launches[r.kind] += 1;
+        }
+        p->pool.push_back(r.a);
+        p->pool.push_back(r.b);
+    }
+    p->recs.clear();
+    return st;
+}
+
+int32_t digest_profile_kernel_count(void) { return K_COUNT; }
+
+const char *digest_profile_kernel_name(int32_t kind)
+{
+    return (kind >= 0 && kind < K_COUNT) ? kKindNames[kind] : "";
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Internal interface between the host library (digest_host.cpp) and the
+// gfx950 kernels (digest_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace digest {
+
+// One unit of sparse-aggregation work: CSR entries [kb, ke) of row `row`.
+// dst >= 0: the result is row `dst` of the output; dst < 0: the result is a
+// partial sum stored in scratch slot (-dst - 1) and summed by a fixup pass.
+struct SpmmItem {
+    int32_t row, kb, ke, dst;
+};
+
+// A row whose entries were split into `nseg` items with consecutive scratch
+// slots starting at `slot`: out[row] = sum of those slots, in slot order.
+struct FixupItem {
+    int32_t row, slot, nseg, pad;
+};
+
+// dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows.
+hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                            int32_t d, const float *src, float *dst, hipStream_t s);
+
+// Two-source CSR aggregation.  Column c < n_src0 reads row c of src0,
+// otherwise row (c - n_src0) of src1.  Every output row (and every scratch
+// slot) named by an item is fully written.
+hipError_t launch_spmm(const SpmmItem *items, int32_t n_items, const int32_t *col,
+                       const float *val, const float *src0, const float *src1,
+                       int32_t n_src0, int32_t d, float *out, float *partial,
+                       hipStream_t s);
+
+hipError_t launch_spmm_fixup(const FixupItem *items, int32_t n_items, int32_t d,
+                             const float *partial, float *out, hipStream_t s);
+
+// C = op(A) op(B) in fp32 on MFMA, K-range split over grid.z when splits > 1.
+//   op(A)(m,k) = a_trans ? A[k*lda + m] : A[m*lda + k]      (M x K)
+//   op(B)(k,n) = b_trans ? B[n*ldb + k] : B[k*ldb + n]      (K x N)
+//   a_mask / b_mask (optional, same layout as A / B): operand element is
+//   zeroed unless the mask element is > 0 (the ReLU derivative).
+//   splits > 1: split z writes C + z*M*ldc (a [splits, M, ldc] scratch).
+//   relu: epilogue max(x, 0).
+struct GemmArgs {
+    int32_t M, N, K;
+    const float *A;
+    int32_t lda;
+    bool a_trans;
+    const float *a_mask;
+    const float *B;
+    int32_t ldb;
+    bool b_trans;
+    const float *b_mask;
+    float *C;
+    int32_t ldc;
+    bool relu;
+    int32_t splits;
+    int32_t kchunk;
+};
+
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
+
+// out[e] = sum_{z < splits} part[z*count + e], in z order.
+hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count, float *out,
+                                hipStream_t s);
+
+// Row-wise softmax cross entropy; block_loss needs softmax_xent_blocks(n) floats.
+int32_t softmax_xent_blocks(int32_t n);
+hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
+                               int32_t C, float *dlogits, float *block_loss, float *loss,
+                               hipStream_t s);
+
+// GEMM tile sizes (rows of C per workgroup, cols of C per workgroup, K step).
+constexpr int kGemmBM = 64;
+constexpr int kGemmBN = 64;
+constexpr int kGemmBK = 16;
+
+}  // namespace digest

@@ -1,0 +1,281 @@
+"""Thin Python binding of ``libdigest.so`` (the C ABI declared in include/digest.h).
+
+Functions carry the C names.  They only marshal arguments: tensors become
+device pointers (after dtype/device/size checks that keep every kernel
+inside the buffers it is given), the stream defaults to torch's current
+stream, and a negative status raises ``DigestError``.  All computation runs
+in the HIP library; if it is not built, importing this module fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdigest.so")
+
+OK, EINVAL, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4
+ACT_RELU, ACT_IDENTITY = 0, 1
+PUSH_BOUNDARY, PUSH_ALL_OWNED = 0, 1
+
+_lib = None
+
+
+class DigestError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"digest status {status}: {message}")
+        self.status = status
+
+
+def lib():
+    """Load libdigest.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2206_00057_amd.build` "
+                               "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        st = ctypes.c_int
+        sig = {
+            "digest_last_error": ([], ctypes.c_char_p),
+            "digest_partition_create": ([i64, P, P, P, P, i64, P, i64, i32, P, P], st),
+            "digest_partition_destroy": ([P], None),
+            "digest_partition_query": ([P, P, P, P, P], st),
+            "digest_partition_bind_workspace": ([P, P, sz, P], st),
+            "digest_partition_export_maps": ([P, P, P, P], st),
+            "digest_partition_export_transpose": ([P, P, P, P], st),
+            "digest_partition_read_halo": ([P, i32, P, P], st),
+            "digest_pull": ([P, i32, P, P], st),
+            "digest_push": ([P, i32, P, P, i32, P], st),
+            "digest_layer_forward": ([P, i32, P, P, P, i32, P], st),
+            "digest_layer_backward": ([P, i32, P, P, P, P, P, P], st),
+            "digest_softmax_xent": ([P, P, P, P, P, P], st),
+            "digest_sync_period": ([i32, i64, P, P], st),
+            "digest_profile_enable": ([P, i32], st),
+            "digest_profile_read": ([P, P, P], st),
+            "digest_profile_kernel_count": ([], i32),
+            "digest_profile_kernel_name": ([i32], ctypes.c_char_p),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != OK:
+        raise DigestError(status, lib().digest_last_error().decode())
+
+
+def _np(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, dtype, numel, name):
+    """Device pointer of a contiguous CUDA tensor with exactly ``numel`` elements."""
+    import torch
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Partition:
+    """Handle of one partition (wraps ``digest_partition*``)."""
+
+    def __init__(self, handle, n_global, n_own, n_halo, widths):
+        self.handle = ctypes.c_void_p(handle)
+        self.n_global = n_global
+        self.n_own = n_own
+        self.n_halo = n_halo
+        self.widths = list(widths)
+        self.L = len(self.widths) - 1
+        self.workspace = None
+        q = digest_partition_query(self)
+        self.n_boundary = q["n_boundary"]
+        self.nnz = q["nnz"]
+        self.nnz_in = q["nnz_in"]
+        self.workspace_bytes = q["workspace_bytes"]
+
+    def __del__(self):
+        try:
+            digest_partition_destroy(self)
+        except Exception:
+            pass
+
+
+def digest_partition_create(n_global, indptr, indices, values, owned, halo, widths):
+    indptr, p_indptr = _np(indptr, np.int64)
+    indices, p_indices = _np(indices, np.int64)
+    values, p_values = _np(values, np.float32)
+    owned, p_owned = _np(owned, np.int64)
+    halo, p_halo = _np(halo, np.int64)
+    widths, p_widths = _np(widths, np.int32)
+    if indptr.shape[0] != owned.shape[0] + 1:
+        raise ValueError("indptr must have n_owned + 1 entries")
+    nnz = int(indptr[-1]) if indptr.size else 0
+    if indices.shape[0] < nnz or values.shape[0] < nnz:
+        raise ValueError("indices/values shorter than indptr[-1]")
+    out = ctypes.c_void_p()
+    _check(lib().digest_partition_create(int(n_global), p_indptr, p_indices, p_values, p_owned,
+                                         owned.shape[0], p_halo, halo.shape[0],
+                                         widths.shape[0] - 1, p_widths, ctypes.byref(out)))
+    return Partition(out.value, int(n_global), owned.shape[0], halo.shape[0], widths.tolist())
+
+
+def digest_partition_destroy(p):
+    if p.handle:
+        lib().digest_partition_destroy(p.handle)
+        p.handle = ctypes.c_void_p()
+
+
+def digest_partition_query(p):
+    nb, nnz, nnz_in = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    ws = ctypes.c_size_t()
+    _check(lib().digest_partition_query(p.handle, ctypes.byref(nb), ctypes.byref(nnz),
+                                        ctypes.byref(nnz_in), ctypes.byref(ws)))
+    return {"n_boundary": nb.value, "nnz": nnz.value, "nnz_in": nnz_in.value,
+            "workspace_bytes": ws.value}
+
+
+def digest_partition_bind_workspace(p, workspace, stream=None):
+    """Bind a CUDA uint8 tensor of at least ``p.workspace_bytes`` bytes."""
+    import torch
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda:
+        raise TypeError("workspace must be a CUDA tensor")
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib().digest_partition_bind_workspace(p.handle, ctypes.c_void_p(workspace.data_ptr()),
+                                                 nbytes, _stream(stream)))
+    p.workspace = workspace
+
+
+def digest_partition_export_maps(p):
+    col = np.empty(p.nnz, np.int32)
+    bgid = np.empty(p.n_boundary, np.int64)
+    bloc = np.empty(p.n_boundary, np.int32)
+    _check(lib().digest_partition_export_maps(p.handle, col.ctypes.data_as(ctypes.c_void_p),
+                                              bgid.ctypes.data_as(ctypes.c_void_p),
+                                              bloc.ctypes.data_as(ctypes.c_void_p)))
+    return col, bgid, bloc
+
+
+def digest_partition_export_transpose(p):
+    ptr = np.empty(p.n_own + 1, np.int64)
+    src = np.empty(p.nnz_in, np.int32)
+    val = np.empty(p.nnz_in, np.float32)
+    _check(lib().digest_partition_export_transpose(p.handle, ptr.ctypes.data_as(ctypes.c_void_p),
+                                                   src.ctypes.data_as(ctypes.c_void_p),
+                                                   val.ctypes.data_as(ctypes.c_void_p)))
+    return ptr, src, val
+
+
+def digest_partition_read_halo(p, level, out, stream=None):
+    import torch
+    _check_level(p, level, 0)
+    ptr = _dev(out, torch.float32, p.n_halo * p.widths[level], "out")
+    _check(lib().digest_partition_read_halo(p.handle, int(level), ptr, _stream(stream)))
+
+
+def _check_level(p, level, lo):
+    if not (lo <= level < p.L):
+        raise DigestError(EINVAL, f"level {level} outside [{lo}, {p.L})")
+
+
+def _check_layer(p, layer):
+    if not (1 <= layer <= p.L):
+        raise DigestError(EINVAL, f"layer {layer} outside [1, {p.L}]")
+
+
+def digest_pull(p, level, store, stream=None):
+    import torch
+    _check_level(p, level, 0)
+    ptr = _dev(store, torch.float32, p.n_global * p.widths[level], "store")
+    _check(lib().digest_pull(p.handle, int(level), ptr, _stream(stream)))
+
+
+def digest_push(p, level, h_own, store, mode=PUSH_BOUNDARY, stream=None):
+    import torch
+    _check_level(p, level, 1)
+    d = p.widths[level]
+    ph = _dev(h_own, torch.float32, p.n_own * d, "h_own")
+    ps = _dev(store, torch.float32, p.n_global * d, "store")
+    _check(lib().digest_push(p.handle, int(level), ph, ps, int(mode), _stream(stream)))
+
+
+def digest_layer_forward(p, layer, h_in, w, h_out, act, stream=None):
+    import torch
+    _check_layer(p, layer)
+    di, do = p.widths[layer - 1], p.widths[layer]
+    a = _dev(h_in, torch.float32, p.n_own * di, "h_in")
+    b = _dev(w, torch.float32, di * do, "w")
+    c = _dev(h_out, torch.float32, p.n_own * do, "h_out")
+    _check(lib().digest_layer_forward(p.handle, int(layer), a, b, c, int(act), _stream(stream)))
+
+
+def digest_layer_backward(p, layer, h_out, dh_out, w, dw, dh_in=None, stream=None):
+    import torch
+    _check_layer(p, layer)
+    di, do = p.widths[layer - 1], p.widths[layer]
+    a = _dev(h_out, torch.float32, p.n_own * do, "h_out")
+    b = _dev(dh_out, torch.float32, p.n_own * do, "dh_out")
+    c = _dev(w, torch.float32, di * do, "w")
+    e = _dev(dw, torch.float32, di * do, "dw")
+    f = _dev(dh_in, torch.float32, p.n_own * di, "dh_in") if dh_in is not None else None
+    _check(lib().digest_layer_backward(p.handle, int(layer), a, b, c, e, f, _stream(stream)))
+
+
+def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):
+    import torch
+    C = p.widths[-1]
+    a = _dev(logits, torch.float32, p.n_own * C, "logits")
+    b = _dev(labels, torch.int32, p.n_own, "labels")
+    c = _dev(dlogits, torch.float32, p.n_own * C, "dlogits")
+    d = _dev(loss, torch.float32, 1, "loss")
+    _check(lib().digest_softmax_xent(p.handle, a, b, c, d, _stream(stream)))
+
+
+def digest_sync_period(K, iteration):
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().digest_sync_period(int(K), int(iteration), ctypes.byref(a), ctypes.byref(b)))
+    return bool(a.value), bool(b.value)
+
+
+def digest_profile_enable(p, on=True):
+    _check(lib().digest_profile_enable(p.handle, 1 if on else 0))
+
+
+def kernel_names():
+    L = lib()
+    return [L.digest_profile_kernel_name(i).decode() for i in range(L.digest_profile_kernel_count())]
+
+
+def digest_profile_read(p):
+    """Per kernel kind: (total ms, launches) since the last read (synchronises)."""
+    n = lib().digest_profile_kernel_count()
+    ms = np.zeros(n, np.float64)
+    cnt = np.zeros(n, np.int64)
+    _check(lib().digest_profile_read(p.handle, ms.ctypes.data_as(ctypes.c_void_p),
+                                     cnt.ctypes.data_as(ctypes.c_void_p)))
+    return {name: (float(ms[i]), int(cnt[i])) for i, name in enumerate(kernel_names())}

@@ -1,0 +1,94 @@
+"""One DIGEST training round of one partition on the GPU, as a sequence of
+library calls (Algorithm 1's inner loop for a single subgraph):
+
+    for l = 1..L:   pull level l-1 if the schedule says so (levels >= 1),
+                    layer forward, push level l if the schedule says so
+                    (levels 1..L-1)
+    loss head
+    for l = L..1:   layer backward
+
+All arithmetic runs in libdigest.so; this module only owns the device
+buffers (PyTorch tensors) and orders the calls on one stream.  ``capture``
+records the round into a HIP graph (one graph per distinct pull/push
+pattern of the schedule) so that replays cost one launch.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import digest as D
+
+
+class GpuPartition:
+    def __init__(self, n_global, part, widths, device="cuda"):
+        self.widths = [int(w) for w in widths]
+        self.L = len(self.widths) - 1
+        self.device = device
+        self.p = D.digest_partition_create(n_global, part.indptr, part.indices, part.values,
+                                           part.owned, part.halo, self.widths)
+        n = self.p.n_own
+        self.n_own = n
+        self.workspace = torch.empty(max(self.p.workspace_bytes, 256), dtype=torch.uint8,
+                                     device=device)
+        D.digest_partition_bind_workspace(self.p, self.workspace)
+        f32 = dict(dtype=torch.float32, device=device)
+        # H[l]: output of layer l (H[0] is the caller's input rows); dH[l] its gradient
+        self.H = [None] + [torch.empty(n, self.widths[l], **f32) for l in range(1, self.L + 1)]
+        self.dH = [None] + [torch.empty(n, self.widths[l], **f32) for l in range(1, self.L + 1)]
+        self.dW = [None] + [torch.empty(self.widths[l - 1], self.widths[l], **f32)
+                            for l in range(1, self.L + 1)]
+        self.loss = torch.zeros(1, **f32)
+        self.graphs = {}
+
+    def act(self, layer):
+        return D.ACT_RELU if layer < self.L else D.ACT_IDENTITY
+
+    def pull_all(self, stores):
+        """Initial pull of every level (level 0 = features)."""
+        for lev in range(self.L):
+            D.digest_pull(self.p, lev, stores[lev])
+
+    def forward(self, x_own, Ws, stores=None, do_pull=False, do_push=False):
+        h = x_own
+        for l in range(1, self.L + 1):
+            if do_pull and l >= 2:
+                D.digest_pull(self.p, l - 1, stores[l - 1])
+            D.digest_layer_forward(self.p, l, h, Ws[l - 1], self.H[l], self.act(l))
+            if do_push and l <= self.L - 1:
+                D.digest_push(self.p, l, self.H[l], stores[l])
+            h = self.H[l]
+        return self.H[self.L]
+
+    def backward(self, Ws, labels):
+        D.digest_softmax_xent(self.p, self.H[self.L], labels, self.dH[self.L], self.loss)
+        for l in range(self.L, 0, -1):
+            dh_in = self.dH[l - 1] if l > 1 else None
+            D.digest_layer_backward(self.p, l, self.H[l], self.dH[l], Ws[l - 1], self.dW[l], dh_in)
+
+    def round(self, r, K, x_own, Ws, stores, labels):
+        """Round r (1-based) with sync interval K, eagerly."""
+        do_pull, do_push = D.digest_sync_period(K, r)
+        self.forward(x_own, Ws, stores, do_pull, do_push)
+        self.backward(Ws, labels)
+
+    def capture(self, K, x_own, Ws, stores, labels):
+        """Record one HIP graph per pull/push pattern that the schedule uses."""
+        patterns = sorted({D.digest_sync_period(K, r) for r in range(1, 2 * K + 1)})
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):   # warm-up outside capture
+            for pat in patterns:
+                self.forward(x_own, Ws, stores, *pat)
+                self.backward(Ws, labels)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        for pat in patterns:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.forward(x_own, Ws, stores, *pat)
+                self.backward(Ws, labels)
+            self.graphs[(K, pat)] = g
+        torch.cuda.synchronize()
+
+    def replay(self, r, K):
+        self.graphs[(K, D.digest_sync_period(K, r))].replay()

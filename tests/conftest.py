@@ -29,3 +29,13 @@ def read_golden(name):
 @pytest.fixture
 def golden():
     return read_golden
+
+
+@pytest.fixture(scope="session", autouse=True)
+def _built_libraries():
+    """Build the oracle and libdigest.so only if nothing is built yet."""
+    import oracle
+    oracle.build()
+    from paper_2206_00057_amd import build as B
+    if not os.path.exists(B.LIB):
+        B.build()

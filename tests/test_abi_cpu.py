@@ -1,0 +1,147 @@
+"""Host-side checks of libdigest.so that need no GPU: every symbol of
+include/digest.h is exported, the index maps built by digest_partition_create
+match the oracle bit for bit, malformed inputs are rejected with the
+documented status, calls before a workspace is bound fail with
+DIGEST_ESTATE, and the schedule matches Algorithm 1.  No kernel is launched."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import ROOT
+from paper_2206_00057_amd import digest as D
+from paper_2206_00057_amd import synth
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "digest.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(digest_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_header_symbol():
+    names = header_functions()
+    assert len(names) >= 16
+    L = D.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _tiny_partition(part=0, cfg=None):
+    cfg = cfg or synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    return cfg, g, synth.make_partition(cfg, g, part)
+
+
+@pytest.mark.parametrize("part", [0, 3])
+def test_maps_bit_exact_vs_oracle(part):
+    cfg, g, p = _tiny_partition(part)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    col, bgid, bloc = D.digest_partition_export_maps(h)
+    o_col, o_bnd = oracle.partition_maps(g.n, p.indptr, p.indices, p.owned, p.halo)
+    np.testing.assert_array_equal(col, o_col)
+    np.testing.assert_array_equal(bloc, o_bnd)
+    np.testing.assert_array_equal(bgid, p.owned[o_bnd])
+    t_ptr, t_src, t_val = D.digest_partition_export_transpose(h)
+    o_ptr, o_src, o_val = oracle.owned_transpose(p.n_own, p.indptr, o_col, p.values)
+    np.testing.assert_array_equal(t_ptr, o_ptr)
+    np.testing.assert_array_equal(t_src, o_src)
+    np.testing.assert_array_equal(t_val.view(np.uint32), o_val.view(np.uint32))
+    assert h.nnz == p.nnz and h.nnz_in == o_ptr[-1] and h.n_boundary == o_bnd.size
+    assert h.workspace_bytes > 0 and h.workspace_bytes % 256 == 0
+
+
+def test_maps_with_duplicates_and_unreferenced_halo():
+    # row 0: owned 0 twice (summed), halo 5; row 1: owned 0; halo 7 unreferenced
+    indptr = np.array([0, 3, 4])
+    indices = np.array([0, 0, 5, 0])
+    values = np.array([0.5, 0.25, 1.0, 2.0], np.float32)
+    owned, halo = np.array([0, 3]), np.array([5, 7])
+    h = D.digest_partition_create(8, indptr, indices, values, owned, halo, [4, 4])
+    col, bgid, bloc = D.digest_partition_export_maps(h)
+    assert col.tolist() == [0, 0, 2, 0]
+    assert bloc.tolist() == [0] and bgid.tolist() == [0]
+    o_col, o_bnd = oracle.partition_maps(8, indptr, indices, owned, halo)
+    assert o_col.tolist() == col.tolist() and o_bnd.tolist() == bloc.tolist()
+    t_ptr, t_src, t_val = D.digest_partition_export_transpose(h)
+    assert t_ptr.tolist() == [0, 3, 3] and t_src.tolist() == [0, 0, 1]
+    assert t_val.tolist() == [0.5, 0.25, 2.0]
+
+
+def test_empty_partition_is_valid():
+    h = D.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
+                                  np.zeros(0), np.zeros(0), [3, 2])
+    assert h.nnz == 0 and h.n_boundary == 0 and h.nnz_in == 0
+
+
+def expect_status(status, fn, *a, **kw):
+    with pytest.raises(D.DigestError) as e:
+        fn(*a, **kw)
+    assert e.value.status == status, str(e.value)
+
+
+def test_create_rejects_malformed_input():
+    cfg, g, p = _tiny_partition()
+    mk = lambda **kw: D.digest_partition_create(
+        kw.get("n", g.n), kw.get("indptr", p.indptr), kw.get("indices", p.indices),
+        kw.get("values", p.values), kw.get("owned", p.owned), kw.get("halo", p.halo),
+        kw.get("widths", cfg.widths))
+    mk()
+    E = D.EINVAL
+    expect_status(E, mk, halo=p.halo[1:])                              # column not owned/halo
+    expect_status(E, mk, halo=np.append(p.halo, p.owned[3]))           # owned and halo overlap
+    expect_status(E, mk, owned=np.append(p.owned[:-1], p.owned[0]))    # repeated owned id
+    expect_status(E, mk, halo=np.append(p.halo[:-1], p.halo[0]))       # repeated halo id
+    expect_status(E, mk, n=int(max(p.halo.max(), p.owned.max())))      # id out of range
+    bad = p.indptr.copy()
+    bad[5] = bad[4] - 1
+    expect_status(E, mk, indptr=bad)                                   # decreasing indptr
+    bad = p.indptr.copy()
+    bad[0] = 1
+    expect_status(E, mk, indptr=bad)                                   # indptr[0] != 0
+    expect_status(E, mk, widths=[64, 0, 16])                           # width 0
+    expect_status(E, mk, widths=[64])                                  # no layer
+    neg = p.indices.copy()
+    neg[7] = -3
+    expect_status(E, mk, indices=neg)                                  # negative id
+    expect_status(E, mk, n=0)
+
+
+def test_device_calls_without_workspace_fail_with_estate():
+    cfg, g, p = _tiny_partition()
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    L = D.lib()
+    fake = ctypes.c_void_p(256)   # never dereferenced: the state check comes first
+    assert L.digest_pull(h.handle, 0, fake, None) == D.ESTATE
+    assert L.digest_push(h.handle, 1, fake, fake, 0, None) == D.ESTATE
+    assert L.digest_layer_forward(h.handle, 1, fake, fake, fake, 0, None) == D.ESTATE
+    assert L.digest_layer_backward(h.handle, 1, fake, fake, fake, fake, None, None) == D.ESTATE
+    assert L.digest_softmax_xent(h.handle, fake, fake, fake, fake, None) == D.ESTATE
+    assert L.digest_pull(None, 0, fake, None) == D.EINVAL
+    assert b"workspace" in L.digest_last_error() or b"handle" in L.digest_last_error()
+    # binding rejects misaligned or short workspaces before touching the device
+    assert L.digest_partition_bind_workspace(h.handle, ctypes.c_void_p(4), 1 << 30, None) == D.EINVAL
+    assert L.digest_partition_bind_workspace(h.handle, ctypes.c_void_p(256), 16, None) == D.ENOMEM
+
+
+def test_sync_period_matches_algorithm_and_oracle(golden):
+    f = os.path.join(ROOT, "tests", "golden", "alg1_schedule.txt")
+    for line in open(f):
+        line = line.split("#", 1)[0].split()
+        if line:
+            K, r, pull, push = map(int, line)
+            assert D.digest_sync_period(K, r) == (bool(pull), bool(push))
+    for K in (1, 2, 3, 7, 10, 20):
+        for r in range(1, 3 * K + 2):
+            assert D.digest_sync_period(K, r) == oracle.sync_period(K, r)
+    expect_status(D.EINVAL, D.digest_sync_period, 0, 1)
+    expect_status(D.EINVAL, D.digest_sync_period, 4, 0)
+
+
+def test_profile_kernel_names():
+    names = D.kernel_names()
+    assert len(names) == D.lib().digest_profile_kernel_count()
+    assert "spmm_fwd" in names and "gemm_fwd_relu" in names and "pull_gather" in names

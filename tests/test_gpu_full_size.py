@@ -1,0 +1,59 @@
+"""GPU parity at the full sizes of the four large workloads (Flickr-, Reddit-
+and OGB-Products-shaped synthetic graphs, and the halo-dominated permutation
+partition), in the same library calls the benchmark times: pull and push
+contents bit-exact; every layer's forward and backward and the loss head
+within rtol 1e-4 / atol 1e-5 plus the scale-aware bound, over all outputs
+(the oracle finishes these in seconds with its threads)."""
+import time
+
+import numpy as np
+import pytest
+
+from paper_2206_00057_amd import synth
+from test_gpu_parity import Case, check_layer, check_loss, check_pull, check_push, torch
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+_graphs = {}
+
+
+def graph_for(cfg):
+    key = (cfg.n, cfg.blocks, cfg.degree, cfg.shape, cfg.cap, cfg.p_intra, cfg.c)
+    if key not in _graphs:
+        _graphs.clear()
+        t = time.time()
+        _graphs[key] = synth.make_graph(cfg)
+        print(f"[graph {cfg.name}: {time.time() - t:.1f}s]", flush=True)
+    return _graphs[key]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["medium", "dense", "large", "halo"])
+def test_full_size_workload(name):
+    cfg = synth.CONFIGS[name]
+    g = graph_for(cfg)
+    part = synth.make_partition(cfg, g, 0)
+    c = Case(cfg, g, part, label=name)
+    print(f"[{name}] {synth.shape_stats(cfg, g, part)}", flush=True)
+    for level in range(c.L):
+        t = time.time()
+        check_pull(c, level)
+        print(f"[{name}] pull level {level} ok {time.time() - t:.1f}s", flush=True)
+    for level in range(1, c.L):
+        t = time.time()
+        check_push(c, level)
+        print(f"[{name}] push level {level} ok {time.time() - t:.1f}s", flush=True)
+    for layer in range(1, c.L + 1):
+        t = time.time()
+        check_layer(c, layer)
+        print(f"[{name}] layer {layer} fwd+bwd ok {time.time() - t:.1f}s", flush=True)
+    check_loss(c)
+    print(f"[{name}] loss ok", flush=True)
+    del c
+    torch.cuda.empty_cache()

@@ -1,0 +1,476 @@
+"""GPU parity of every library call against the CPU oracle, on identical
+seeded inputs from ``paper_2206_00057_amd.synth`` (no oracle input ever comes
+from the GPU).
+
+Bars: index maps, pull and push contents bit-exact; activations, gradients
+and the loss within rtol 1e-4 / atol 1e-5 element-wise, plus a scale-aware
+bound max|gpu - oracle| / max|oracle| (gradients scale like 1/n_own, where
+atol alone says little).  Cases span several tiles with ragged tails, odd
+widths, rows longer than one aggregation work item, an empty partition, a
+partition without halo, and the small GCN workload end to end over several
+rounds of Algorithm 1 with sync intervals 1 and 5.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2206_00057_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 1e-4, 1e-5
+SCALE_TOL = 2e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def D():
+    from paper_2206_00057_amd import digest
+    return digest
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def assert_close(gpu, ref, name, rtol=RTOL, atol=ATOL, scale_tol=SCALE_TOL):
+    g = np.asarray(gpu, np.float64)
+    r = np.asarray(ref, np.float64)
+    assert g.shape == r.shape, name
+    assert np.all(np.isfinite(g)), f"{name}: non-finite GPU values"
+    err = np.abs(g - r)
+    bad = err > atol + rtol * np.abs(r)
+    peak = float(np.abs(r).max()) if r.size else 0.0
+    scale = float(err.max()) / peak if r.size and peak > 0 else 0.0
+    assert not bad.any(), (f"{name}: {int(bad.sum())}/{bad.size} outside rtol/atol, "
+                           f"max err {err.max():.3e}, scale err {scale:.3e}")
+    assert scale <= scale_tol, f"{name}: scale err {scale:.3e} > {scale_tol}"
+    return scale
+
+
+def assert_bits(gpu, ref, name):
+    g = np.ascontiguousarray(gpu)
+    r = np.ascontiguousarray(ref)
+    assert g.shape == r.shape, name
+    np.testing.assert_array_equal(g.view(np.uint32), r.view(np.uint32), err_msg=name)
+
+
+class Case:
+    """A partition with its library handle, oracle twin and seeded inputs."""
+
+    def __init__(self, cfg, g, part, label=""):
+        self.cfg, self.g, self.part = cfg, g, part
+        self.label = label or cfg.name
+        self.widths = list(cfg.widths)
+        self.L = len(self.widths) - 1
+        Dm = D()
+        self.h = Dm.digest_partition_create(g.n, part.indptr, part.indices, part.values,
+                                            part.owned, part.halo, self.widths)
+        self.ws = torch.empty(max(self.h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+        Dm.digest_partition_bind_workspace(self.h, self.ws)
+        self.op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values,
+                                         part.owned, part.halo, self.widths)
+        self.n = part.n_own
+
+    def store(self, level):
+        if level == 0:
+            return synth.features(self.cfg)
+        return synth.relu_normal((self.g.n, self.widths[level]), seed=20 + level)
+
+    def layer_input(self, layer):
+        if layer == 1:
+            return synth.features(self.cfg)[self.part.owned]
+        return synth.relu_normal((self.n, self.widths[layer - 1]), seed=10 + layer)
+
+    def upstream(self, layer):
+        return synth.normal((self.n, self.widths[layer]), seed=30 + layer,
+                            scale=1.0 / max(self.n, 1))
+
+    def act(self, layer):
+        return oracle.RELU if layer < self.L else oracle.IDENTITY
+
+
+def check_pull(c, level, store=None):
+    Dm = D()
+    store = c.store(level) if store is None else store
+    Dm.digest_pull(c.h, level, dev(store))
+    out = torch.empty(c.part.n_halo, c.widths[level], device="cuda")
+    Dm.digest_partition_read_halo(c.h, level, out)
+    assert_bits(host(out), c.op.pull(level, store), f"{c.label} pull level {level}")
+
+
+def check_push(c, level):
+    Dm = D()
+    base = synth.normal((c.g.n, c.widths[level]), seed=40 + level)
+    h_own = synth.normal((c.n, c.widths[level]), seed=50 + level)
+    for mode, all_owned in ((Dm.PUSH_BOUNDARY, False), (Dm.PUSH_ALL_OWNED, True)):
+        s = dev(base)
+        Dm.digest_push(c.h, level, dev(h_own), s, mode)
+        ref = c.op.push(level, h_own, base.copy(), all_owned=all_owned)
+        assert_bits(host(s), ref, f"{c.label} push level {level} mode {mode}")
+
+
+def check_layer(c, layer, check_dh_in=True):
+    """Forward and backward of one layer on seeded inputs, vs the oracle."""
+    Dm = D()
+    if c.part.n_halo:
+        store = c.store(layer - 1)
+        Dm.digest_pull(c.h, layer - 1, dev(store))
+        c.op.pull(layer - 1, store)
+    h_in = c.layer_input(layer)
+    W = synth.weights(c.cfg)[layer - 1]
+    act = c.act(layer)
+    out = torch.empty(c.n, c.widths[layer], device="cuda")
+    Dm.digest_layer_forward(c.h, layer, dev(h_in), dev(W), out, act)
+    ref_out = c.op.forward(layer, h_in, W, act)
+    assert_close(host(out), ref_out, f"{c.label} forward layer {layer}")
+    # backward: mask and upstream gradient from the oracle / the generator
+    dh = c.upstream(layer)
+    dw = torch.empty(W.shape, device="cuda")
+    want = check_dh_in and layer > 1
+    dh_in = torch.empty(c.n, c.widths[layer - 1], device="cuda") if want else None
+    Dm.digest_layer_backward(c.h, layer, dev(ref_out), dev(dh), dev(W), dw, dh_in)
+    ref_dw, ref_dh_in = c.op.backward(layer, h_in, W, ref_out, dh, act, want_dh_in=want)
+    assert_close(host(dw), ref_dw, f"{c.label} dW layer {layer}")
+    if want:
+        assert_close(host(dh_in), ref_dh_in, f"{c.label} dH_in layer {layer}")
+
+
+def check_loss(c, seed=60):
+    Dm = D()
+    C = c.widths[-1]
+    logits = synth.normal((c.n, C), seed=seed, scale=3.0)
+    y = synth.labels(c.cfg)[c.part.owned]
+    dl = torch.empty(c.n, C, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    Dm.digest_softmax_xent(c.h, dev(logits), dev(y), dl, loss)
+    ref_loss, ref_dl = oracle.softmax_xent(logits, y)
+    assert_close(host(dl), ref_dl, f"{c.label} dlogits")
+    assert abs(float(host(loss)[0]) - ref_loss) <= ATOL + RTOL * abs(ref_loss)
+
+
+# ---------------------------------------------------------------------------
+# the small GCN workload (2,000 nodes, 64 -> 64 -> 16), every call
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def tiny_graph():
+    cfg = synth.CONFIGS["tiny"]
+    return cfg, synth.make_graph(cfg)
+
+
+@pytest.fixture(scope="module", params=[0, 3])
+def tiny(request, tiny_graph):
+    cfg, g = tiny_graph
+    return Case(cfg, g, synth.make_partition(cfg, g, request.param),
+                label=f"tiny/part{request.param}")
+
+
+def test_tiny_pull_push_bit_exact(tiny):
+    for level in range(tiny.L):
+        check_pull(tiny, level)
+    for level in range(1, tiny.L):
+        check_push(tiny, level)
+
+
+@pytest.mark.parametrize("layer", [1, 2])
+def test_tiny_layer(tiny, layer):
+    check_layer(tiny, layer)
+
+
+def test_tiny_loss(tiny):
+    check_loss(tiny)
+
+
+def test_tiny_bad_label_gives_nan_and_zero_rows(tiny):
+    Dm = D()
+    C = tiny.widths[-1]
+    logits = synth.normal((tiny.n, C), seed=61)
+    y = synth.labels(tiny.cfg)[tiny.part.owned].copy()
+    y[5] = C
+    dl = torch.full((tiny.n, C), 7.0, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    Dm.digest_softmax_xent(tiny.h, dev(logits), dev(y), dl, loss)
+    assert np.isnan(host(loss)[0])
+    out = host(dl)
+    assert np.all(out[5] == 0)
+    ref_loss, ref_dl = oracle.softmax_xent(logits[np.arange(tiny.n) != 5],
+                                           y[np.arange(tiny.n) != 5])
+    # the other rows keep their value (normalised by the full row count)
+    assert_close(out[np.arange(tiny.n) != 5] * tiny.n,
+                 ref_dl * (tiny.n - 1), "dlogits with one bad label")
+
+
+def test_determinism_bitwise(tiny):
+    Dm = D()
+    store = tiny.store(0)
+    Dm.digest_pull(tiny.h, 0, dev(store))
+    x = dev(tiny.layer_input(1))
+    W = dev(synth.weights(tiny.cfg)[0])
+    outs, dws = [], []
+    for _ in range(2):
+        out = torch.empty(tiny.n, tiny.widths[1], device="cuda")
+        Dm.digest_layer_forward(tiny.h, 1, x, W, out, Dm.ACT_RELU)
+        dw = torch.empty(W.shape, device="cuda")
+        Dm.digest_layer_backward(tiny.h, 1, out, dev(tiny.upstream(1)), W, dw, None)
+        outs.append(host(out))
+        dws.append(host(dw))
+    assert_bits(outs[0], outs[1], "forward run twice")
+    assert_bits(dws[0], dws[1], "dW run twice")
+
+
+# ---------------------------------------------------------------------------
+# shapes: odd widths, ragged tiles, long rows, empty and halo-free partitions
+# ---------------------------------------------------------------------------
+
+WIDTHS = [(1, 1, 1), (3, 5, 2), (7, 41, 47), (602, 47, 7), (100, 256, 41), (64, 64, 16),
+          (33, 130, 9), (500, 256, 7)]
+
+
+@pytest.mark.parametrize("widths", WIDTHS, ids=lambda w: "x".join(map(str, w)))
+def test_widths(widths):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=1)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 1), label=f"widths{widths}")
+    for level in range(c.L):
+        check_pull(c, level)
+    for layer in (1, 2):
+        check_layer(c, layer)
+    check_loss(c)
+
+
+def test_long_rows_split_into_items():
+    """Rows with more entries than one work item (lognormal, mean ~490)."""
+    cfg = synth.scaled(synth.CONFIGS["dense"], 8000, widths=(96, 40, 5), classes=5)
+    g = synth.make_graph(cfg, seed=2)
+    part = synth.make_partition(cfg, g, 0)
+    assert np.diff(part.indptr).max() > 1000
+    c = Case(cfg, g, part, label="long-rows")
+    for layer in (1, 2):
+        check_layer(c, layer)
+
+
+def test_relu_narrowing_layer_uses_masked_dgrad():
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=(48, 20, 3), classes=3)
+    g = synth.make_graph(cfg, seed=4)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 2), label="relu-narrow")
+    check_layer(c, 1, check_dh_in=True)
+    # dh_in of layer 1 (ReLU, narrowing) is also defined by the API
+    Dm = D()
+    h_in = c.layer_input(1)
+    W = synth.weights(cfg)[0]
+    out = torch.empty(c.n, 20, device="cuda")
+    Dm.digest_layer_forward(c.h, 1, dev(h_in), dev(W), out, Dm.ACT_RELU)
+    ref_out = c.op.forward(1, h_in, W, oracle.RELU)
+    dh = c.upstream(1)
+    dw = torch.empty(W.shape, device="cuda")
+    dh_in = torch.empty(c.n, 48, device="cuda")
+    Dm.digest_layer_backward(c.h, 1, dev(ref_out), dev(dh), dev(W), dw, dh_in)
+    ref_dw, ref_dh = c.op.backward(1, h_in, W, ref_out, dh, oracle.RELU, want_dh_in=True)
+    assert_close(host(dh_in), ref_dh, "relu-narrow dH_in")
+
+
+def test_single_partition_no_halo():
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 900, widths=(16, 24, 5), classes=5)
+    g = synth.make_graph(cfg, seed=6)
+    part = synth.extract_partition(g, np.arange(g.n, dtype=np.int64))
+    assert part.n_halo == 0
+    c = Case(cfg, g, part, label="no-halo")
+    assert c.h.n_boundary == 0
+    for layer in (1, 2):
+        check_layer(c, layer)
+
+
+def test_empty_partition():
+    Dm = D()
+    h = Dm.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
+                                   np.zeros(0), np.zeros(0), [3, 2])
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    Dm.digest_partition_bind_workspace(h, ws)
+    Dm.digest_pull(h, 0, torch.zeros(10, 3, device="cuda"))
+    e = torch.empty(0, 3, device="cuda")
+    out = torch.empty(0, 2, device="cuda")
+    W = torch.ones(3, 2, device="cuda")
+    Dm.digest_layer_forward(h, 1, e, W, out, Dm.ACT_IDENTITY)
+    dw = torch.full((3, 2), 5.0, device="cuda")
+    Dm.digest_layer_backward(h, 1, out, out, W, dw, e)
+    assert np.all(host(dw) == 0)
+    loss = torch.full((1,), 3.0, device="cuda")
+    Dm.digest_softmax_xent(h, out, torch.empty(0, dtype=torch.int32, device="cuda"), out, loss)
+    assert host(loss)[0] == 0
+
+
+def test_state_errors_on_device():
+    Dm = D()
+    cfg = synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    part = synth.make_partition(cfg, g, 0)
+    c = Case(cfg, g, part)
+    W = dev(synth.weights(cfg)[1])
+    x = torch.zeros(c.n, 64, device="cuda")
+    out = torch.empty(c.n, 16, device="cuda")
+    with pytest.raises(Dm.DigestError) as e:       # level 1 never pulled
+        Dm.digest_layer_forward(c.h, 2, x, W, out, Dm.ACT_IDENTITY)
+    assert e.value.status == Dm.ESTATE
+    with pytest.raises(Dm.DigestError) as e:       # no forward of layer 2 yet
+        Dm.digest_layer_backward(c.h, 2, out, out, W, torch.empty(64, 16, device="cuda"), None)
+    assert e.value.status == Dm.ESTATE
+    with pytest.raises(Dm.DigestError) as e:       # push of level 0 is not a stale level
+        Dm.digest_push(c.h, 0, x, torch.zeros(g.n, 64, device="cuda"))
+    assert e.value.status == Dm.EINVAL
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1 over several rounds (the small workload), sync interval 1 and 5
+# ---------------------------------------------------------------------------
+
+def _full_forward_oracle(g, X, Ws, L):
+    allp = oracle.OraclePartition(g.n, g.indptr, g.indices, g.values,
+                                  np.arange(g.n, dtype=np.int64), np.zeros(0, np.int64),
+                                  [X.shape[1]] + [w.shape[1] for w in Ws])
+    hs = [X]
+    for l in range(1, L + 1):
+        hs.append(allp.forward(l, hs[-1], Ws[l - 1], oracle.RELU if l < L else oracle.IDENTITY))
+    return hs
+
+
+@pytest.mark.parametrize("K", [1, 5])
+def test_rounds_of_algorithm1(tiny_graph, K):
+    """Each side runs its own rounds: the other partitions are played by a
+    full-graph forward at the current weights whose boundary rows are pushed
+    at every push round; the partition itself pulls/pushes per the schedule
+    and applies SGD.  Compared round by round."""
+    from paper_2206_00057_amd import step
+    Dm = D()
+    cfg, g = tiny_graph
+    part = synth.make_partition(cfg, g, 0)
+    L = cfg.layers
+    X = synth.features(cfg)
+    Ws = synth.weights(cfg)
+    y = synth.labels(cfg)[part.owned]
+    lr = 0.5
+    # shared start: stores initialised by one full-graph forward at the initial W
+    init = _full_forward_oracle(g, X, Ws, L)
+    o_stores = [X] + [init[l].copy() for l in range(1, L)]
+    g_stores = [dev(X)] + [dev(init[l]) for l in range(1, L)]
+    op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
+                                part.halo, cfg.widths)
+    gp = step.GpuPartition(g.n, part, cfg.widths)
+    for lev in range(L):
+        op.pull(lev, o_stores[lev])
+    gp.pull_all(g_stores)
+    oW = [w.copy() for w in Ws]
+    gW = [dev(w) for w in Ws]
+    x_own = X[part.owned]
+    gx = dev(x_own)
+    gy = dev(y)
+    others = np.setdiff1d(np.arange(g.n), part.owned)
+    for r in range(1, 3 * K + 2):
+        do_pull, do_push = Dm.digest_sync_period(K, r)
+        assert (do_pull, do_push) == oracle.sync_period(K, r)
+        if do_push:   # the other partitions push their rows computed at the current W
+            o_full = _full_forward_oracle(g, X, oW, L)
+            for l in range(1, L):
+                o_stores[l][others] = o_full[l][others]
+            # the GPU side gets the same emulated rows from its own weights, via the library
+            gfull = step.GpuPartition(g.n, synth.extract_partition(g, np.arange(g.n)), cfg.widths)
+            gfull.pull_all([dev(X)] + [torch.zeros(g.n, cfg.widths[l], device="cuda")
+                                       for l in range(1, L)])
+            gfull.forward(dev(X), gW)
+            idx = torch.from_numpy(others).cuda()
+            for l in range(1, L):
+                g_stores[l][idx] = gfull.H[l][idx]
+        # oracle round
+        h = x_own
+        outs = []
+        for l in range(1, L + 1):
+            if do_pull and l >= 2:
+                op.pull(l - 1, o_stores[l - 1])
+            act = oracle.RELU if l < L else oracle.IDENTITY
+            outs.append((h, op.forward(l, h, oW[l - 1], act)))
+            h = outs[-1][1]
+            if do_push and l <= L - 1:
+                op.push(l, h, o_stores[l])
+        o_loss, dh = oracle.softmax_xent(h, y)
+        o_dw = [None] * L
+        for l in range(L, 0, -1):
+            act = oracle.RELU if l < L else oracle.IDENTITY
+            o_dw[l - 1], dh_in = op.backward(l, outs[l - 1][0], oW[l - 1], outs[l - 1][1], dh,
+                                             act, want_dh_in=l > 1)
+            dh = dh_in
+        # GPU round
+        gp.round(r, K, gx, gW, g_stores, gy)
+        assert_close(host(gp.H[L]), outs[-1][1], f"K={K} round {r} logits")
+        assert abs(float(host(gp.loss)[0]) - o_loss) <= ATOL + RTOL * abs(o_loss)
+        for l in range(1, L + 1):
+            assert_close(host(gp.dW[l]), o_dw[l - 1], f"K={K} round {r} dW{l}",
+                         scale_tol=1e-4)
+        for l in range(1, L):
+            assert_close(host(g_stores[l]), o_stores[l], f"K={K} round {r} store level {l}")
+        # SGD on both sides
+        for l in range(L):
+            oW[l] = (oW[l] - np.float32(lr) * o_dw[l]).astype(np.float32)
+            gW[l].sub_(lr * gp.dW[l + 1])
+
+
+def test_graph_replay_matches_eager(tiny_graph):
+    from paper_2206_00057_amd import step
+    cfg, g = tiny_graph
+    part = synth.make_partition(cfg, g, 1)
+    L = cfg.layers
+    X = synth.features(cfg)
+    stores = [dev(X)] + [dev(synth.relu_normal((g.n, cfg.widths[l]), 20 + l))
+                         for l in range(1, L)]
+    Ws = [dev(w) for w in synth.weights(cfg)]
+    y = dev(synth.labels(cfg)[part.owned])
+    x = dev(X[part.owned])
+    gp = step.GpuPartition(g.n, part, cfg.widths)
+    gp.pull_all(stores)
+    K = 3
+    eager = {}
+    for r in (1, 2, 3):
+        gp.round(r, K, x, Ws, stores, y)
+        eager[r] = (host(gp.H[L]).copy(), [host(gp.dW[l]).copy() for l in range(1, L + 1)])
+    gp.capture(K, x, Ws, stores, y)
+    for rep in range(3):
+        for r in (1, 2, 3):
+            gp.H[L].zero_()
+            for l in range(1, L + 1):
+                gp.dW[l].zero_()
+            gp.replay(r, K)
+            torch.cuda.synchronize()
+            _ = torch.ones(1000, device="cuda").sum().item()   # eager work between replays
+            assert_bits(host(gp.H[L]), eager[r][0], f"replay {rep} round {r} logits")
+            for l in range(1, L + 1):
+                assert_bits(host(gp.dW[l]), eager[r][1][l - 1], f"replay {rep} round {r} dW{l}")
+
+
+def test_profile_instrumentation(tiny_graph):
+    from paper_2206_00057_amd import step
+    Dm = D()
+    cfg, g = tiny_graph
+    part = synth.make_partition(cfg, g, 0)
+    gp = step.GpuPartition(g.n, part, cfg.widths)
+    stores = [dev(synth.features(cfg))] + [dev(synth.relu_normal((g.n, 64), 21))]
+    gp.pull_all(stores)
+    Ws = [dev(w) for w in synth.weights(cfg)]
+    Dm.digest_profile_enable(gp.p, True)
+    gp.round(1, 1, dev(synth.features(cfg)[part.owned]), Ws, stores,
+             dev(synth.labels(cfg)[part.owned]))
+    prof = Dm.digest_profile_read(gp.p)
+    Dm.digest_profile_enable(gp.p, False)
+    assert prof["spmm_fwd"][1] == 2 and prof["gemm_fwd_relu"][1] == 2
+    assert prof["pull_gather"][1] == 1 and prof["push_scatter"][1] == 1
+    assert prof["softmax_xent"][1] == 1 and prof["gemm_dw_splitk"][1] == 2
+    assert all(ms >= 0 for ms, _ in prof.values())
+    assert Dm.digest_profile_read(gp.p)["spmm_fwd"][1] == 0
