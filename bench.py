@@ -79,9 +79,9 @@ def splitk_factors(n, widths):
     for l in range(1, len(widths)):
         M, N = widths[l - 1], widths[l]
         tiles = -(-M // 64) * -(-N // 64)
-        s = max(1, min(-(-2048 // max(tiles, 1)), max(1, n // 256), 256))
+        s = max(1, min(-(-768 // max(tiles, 1)), max(1, n // 256), 256))
         chunk = -(-n // s)
-        chunk = -(-chunk // 16) * 16 or 16
+        chunk = -(-chunk // 32) * 32 or 32
         out[l] = max(1, -(-n // chunk))
     return out
 

@@ -14,8 +14,7 @@
 #include <string>
 #include <vector>
 
-using digest::FixupItem;
-using digest::SpmmItem;
+using digest::SpmmBlock;
 
 namespace {
 
@@ -37,39 +36,37 @@ enum Kind : int32_t {
     K_PULL = 0,
     K_PUSH,
     K_SPMM_FWD,
-    K_FIXUP_FWD,
     K_GEMM_FWD,
     K_GEMM_DW,
     K_REDUCE_DW,
     K_GEMM_DH,
     K_SPMM_BWD,
-    K_FIXUP_BWD,
     K_LOSS,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
-    "pull_gather", "push_scatter", "spmm_fwd", "spmm_fwd_fixup", "gemm_fwd_relu",
-    "gemm_dw_splitk", "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed",
-    "spmm_bwd_fixup", "softmax_xent"};
+    "pull_gather", "push_scatter", "spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
+    "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent"};
 
-// Largest number of CSR entries one aggregation work item takes; longer
-// rows are cut into several items whose partial sums a fixup pass adds.
-constexpr int32_t kSegment = 256;
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
 constexpr int32_t kMaxLayers = 64;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Split-K factor for a contraction with an M x N result over K.
+// Split-K factor for a contraction with an M x N result over K: about
+// kSplitTarget workgroups in all, at least kSplitMinRows rows of K per split,
+// split starts on GEMM K-tile boundaries.
+constexpr int64_t kSplitTarget = 768;
+constexpr int64_t kSplitMinRows = 256;
+
 void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchunk)
 {
     const int64_t tiles = ((M + digest::kGemmBM - 1) / digest::kGemmBM) *
                           ((N + digest::kGemmBN - 1) / digest::kGemmBN);
-    int64_t s = (2048 + tiles - 1) / std::max<int64_t>(tiles, 1);
-    const int64_t max_by_k = std::max<int64_t>(1, K / 256);   // at least 256 rows per split
-    s = std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(s, max_by_k), 256));
-    int64_t chunk = (K + s - 1) / std::max<int64_t>(s, 1);
+    int64_t s = (kSplitTarget + tiles - 1) / std::max<int64_t>(tiles, 1);
+    s = std::max<int64_t>(1, std::min<int64_t>({s, std::max<int64_t>(1, K / kSplitMinRows), 256}));
+    int64_t chunk = (K + s - 1) / s;
     chunk = (chunk + digest::kGemmBK - 1) / digest::kGemmBK * digest::kGemmBK;
     if (chunk <= 0)
         chunk = digest::kGemmBK;
@@ -78,29 +75,29 @@ void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchu
     kchunk = (int32_t)chunk;
 }
 
-void build_items(const std::vector<int32_t> &rowptr, int32_t n_rows, std::vector<SpmmItem> &items,
-                 std::vector<FixupItem> &fix, int32_t &n_slots)
+// Aggregation blocks of a CSR: every long row gets a block of its own (those
+// come first, so they start early); runs of consecutive short rows are
+// packed one per wave.
+void build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
+                  std::vector<SpmmBlock> &blocks)
 {
-    items.clear();
-    fix.clear();
-    n_slots = 0;
-    // Long rows first (their segments start early), then rows in order.
-    for (int32_t r = 0; r < n_rows; ++r) {
-        const int32_t kb = rowptr[r], ke = rowptr[r + 1];
-        if (ke - kb > kSegment) {
-            const int32_t nseg = (ke - kb + kSegment - 1) / kSegment;
-            fix.push_back({r, n_slots, nseg, 0});
-            for (int32_t s = 0; s < nseg; ++s) {
-                const int32_t a = kb + s * kSegment;
-                items.push_back({r, a, std::min(ke, a + kSegment), -(n_slots + s) - 1});
-            }
-            n_slots += nseg;
+    const int32_t waves = digest::kSpmmThreads / 64;
+    blocks.clear();
+    for (int32_t r = 0; r < n_rows; ++r)
+        if (rowptr[r + 1] - rowptr[r] > digest::kSpmmLongRow)
+            blocks.push_back({r, 0, rowptr[r], rowptr[r + 1]});
+    int32_t first = -1, count = 0;
+    for (int32_t r = 0; r <= n_rows; ++r) {
+        const bool short_row = r < n_rows && rowptr[r + 1] - rowptr[r] <= digest::kSpmmLongRow;
+        if (short_row) {
+            if (count == 0)
+                first = r;
+            ++count;
         }
-    }
-    for (int32_t r = 0; r < n_rows; ++r) {
-        const int32_t kb = rowptr[r], ke = rowptr[r + 1];
-        if (ke - kb <= kSegment)
-            items.push_back({r, kb, ke, r});
+        if (count > 0 && (!short_row || count == waves || r == n_rows - 1)) {
+            blocks.push_back({first, count, 0, 0});
+            count = 0;
+        }
     }
 }
 
@@ -116,16 +113,14 @@ struct digest_partition {
     // host copies of everything uploaded at bind time
     std::vector<int32_t> rowptr, col, t_rowptr, t_src, halo_gid, bnd_local, bnd_gid, owned_gid;
     std::vector<float> val, t_val;
-    std::vector<SpmmItem> items_f, items_t;
-    std::vector<FixupItem> fix_f, fix_t;
-    int32_t slots_f = 0, slots_t = 0;
+    std::vector<SpmmBlock> blocks_f, blocks_t;
 
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
-        size_t items_f, items_t, fix_f, fix_t;
+        size_t blocks_f, blocks_t;
         std::vector<size_t> halo_buf;   // per level 0..L-1
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused)
-        size_t tmp, spmm_part, gemm_part, loss_part;
+        size_t tmp, gemm_part, loss_part;
         size_t total;
     } lay{};
 
@@ -170,29 +165,24 @@ void plan_layout(digest_partition &p)
     l.bnd_local = take(sizeof(int32_t) * p.n_bnd);
     l.bnd_gid = take(sizeof(int32_t) * p.n_bnd);
     l.owned_gid = take(sizeof(int32_t) * p.n_own);
-    l.items_f = take(sizeof(SpmmItem) * p.items_f.size());
-    l.items_t = take(sizeof(SpmmItem) * p.items_t.size());
-    l.fix_f = take(sizeof(FixupItem) * p.fix_f.size());
-    l.fix_t = take(sizeof(FixupItem) * p.fix_t.size());
+    l.blocks_f = take(sizeof(SpmmBlock) * p.blocks_f.size());
+    l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
     l.halo_buf.assign(p.L, 0);
     for (int32_t lev = 0; lev < p.L; ++lev)
         l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * p.widths[lev]);
     l.ah.assign(p.L + 1, 0);
     for (int32_t k = 1; k <= p.L; ++k)
         l.ah[k] = take(sizeof(float) * (size_t)p.n_own * p.widths[k - 1]);
-    int64_t wmax = 0, din_max = 0, gemm_part = 0;
+    int64_t wmax = 0, gemm_part = 0;
     for (int32_t k = 1; k <= p.L; ++k) {
         const int64_t di = p.widths[k - 1], dout = p.widths[k];
         wmax = std::max({wmax, di, dout});
-        din_max = std::max(din_max, di);
         int32_t splits, kchunk;
         splitk_plan(di, dout, p.n_own, splits, kchunk);
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
     }
     l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
-    const int64_t part = std::max<int64_t>((int64_t)p.slots_f * din_max, (int64_t)p.slots_t * wmax);
-    l.spmm_part = take(sizeof(float) * (size_t)part);
     l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
     l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own));
     l.total = o;
@@ -253,33 +243,20 @@ digest_status need_bound(const digest_partition *p)
     return DIGEST_OK;
 }
 
-// Sparse aggregation with its long-row fixup.
+// Sparse aggregation over the local CSR (forward) or the CSR of P_in^T.
 digest_status run_spmm(digest_partition *p, bool transposed, const float *src0,
                        const float *src1, int32_t d, float *out, hipStream_t s)
 {
-    const auto &items = transposed ? p->items_t : p->items_f;
-    const auto &fix = transposed ? p->fix_t : p->fix_f;
-    const int32_t *colp = p->at<int32_t>(transposed ? p->lay.t_src : p->lay.col);
-    const float *valp = p->at<float>(transposed ? p->lay.t_val : p->lay.val);
-    float *part = p->at<float>(p->lay.spmm_part);
-    {
-        Timed t(p, transposed ? K_SPMM_BWD : K_SPMM_FWD, s);
-        digest_status st = hip_check(
-            digest::launch_spmm(p->at<SpmmItem>(transposed ? p->lay.items_t : p->lay.items_f),
-                                (int32_t)items.size(), colp, valp, src0, src1, p->n_own, d, out,
-                                part, s),
-            "spmm");
-        if (st)
-            return st;
-    }
-    if (!fix.empty()) {
-        Timed t(p, transposed ? K_FIXUP_BWD : K_FIXUP_FWD, s);
-        return hip_check(
-            digest::launch_spmm_fixup(p->at<FixupItem>(transposed ? p->lay.fix_t : p->lay.fix_f),
-                                      (int32_t)fix.size(), d, part, out, s),
-            "spmm fixup");
-    }
-    return DIGEST_OK;
+    const auto &blocks = transposed ? p->blocks_t : p->blocks_f;
+    Timed t(p, transposed ? K_SPMM_BWD : K_SPMM_FWD, s);
+    return hip_check(
+        digest::launch_spmm(p->at<SpmmBlock>(transposed ? p->lay.blocks_t : p->lay.blocks_f),
+                            (int32_t)blocks.size(),
+                            p->at<int32_t>(transposed ? p->lay.t_rowptr : p->lay.rowptr),
+                            p->at<int32_t>(transposed ? p->lay.t_src : p->lay.col),
+                            p->at<float>(transposed ? p->lay.t_val : p->lay.val), src0, src1,
+                            p->n_own, d, out, s),
+        "spmm");
 }
 
 }  // namespace
@@ -405,8 +382,8 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
                 }
             }
 
-        build_items(p->rowptr, p->n_own, p->items_f, p->fix_f, p->slots_f);
-        build_items(p->t_rowptr, p->n_own, p->items_t, p->fix_t, p->slots_t);
+        build_blocks(p->rowptr, p->n_own, p->blocks_f);
+        build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
         plan_layout(*p);
         p->pulled.assign(p->L, 0);
         p->fwd_done.assign(p->L + 1, 0);
@@ -476,10 +453,8 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.bnd_local, p->bnd_local.data(), sizeof(int32_t) * p->bnd_local.size()},
         {l.bnd_gid, p->bnd_gid.data(), sizeof(int32_t) * p->bnd_gid.size()},
         {l.owned_gid, p->owned_gid.data(), sizeof(int32_t) * p->owned_gid.size()},
-        {l.items_f, p->items_f.data(), sizeof(SpmmItem) * p->items_f.size()},
-        {l.items_t, p->items_t.data(), sizeof(SpmmItem) * p->items_t.size()},
-        {l.fix_f, p->fix_f.data(), sizeof(FixupItem) * p->fix_f.size()},
-        {l.fix_t, p->fix_t.data(), sizeof(FixupItem) * p->fix_t.size()},
+        {l.blocks_f, p->blocks_f.data(), sizeof(SpmmBlock) * p->blocks_f.size()},
+        {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
     };
     for (const Up &u : ups) {
         if (!u.bytes)

@@ -4,14 +4,14 @@
 //                  (scatter boundary rows into it), Sec. 3.2: one row per
 //                  lane group, 16-byte vectors when the width allows.
 //   k_spmm         two-source CSR aggregation P_in H_in + P_out H~_out of
-//                  Eq. 5 (and P_in^T G of the backward): one wave per work
-//                  item of at most a fixed number of entries, lanes split
-//                  into groups over entries x feature vectors, entry
-//                  indices fetched 64 at a time and broadcast across the
-//                  wave, wave-level segmented reduction across groups.
-//                  Long rows are split into several items whose partial
-//                  sums are added by k_spmm_fixup in a fixed order, so
-//                  results are deterministic and no float atomics are used.
+//                  Eq. 5 (and P_in^T G of the backward).  Short rows take
+//                  one wave each; a long row takes a whole 8-wave block
+//                  whose waves split its entries and add their sums in LDS
+//                  in a fixed order.  Inside a wave, lanes split into groups
+//                  over entries x feature vectors, entry indices are fetched
+//                  64 at a time and broadcast, many gathers are kept in
+//                  flight, and groups are combined by a butterfly.  Results
+//                  are deterministic; no float atomics, no global fences.
 //   k_gemm         fp32 MFMA (v_mfma_f32_32x32x2f32) GEMM with optional
 //                  transposed operands, ReLU-derivative operand masks, a
 //                  ReLU epilogue and split-K over grid.z: the dense
@@ -103,132 +103,164 @@ __global__ __launch_bounds__(256) void k_copy_rows(const int32_t *__restrict__ s
 // Sparse aggregation
 // ---------------------------------------------------------------------------
 
-template <int VEC, int GL, bool TWO>
-__global__ __launch_bounds__(256) void k_spmm(const SpmmItem *__restrict__ items,
-                                              int32_t n_items, const int32_t *__restrict__ col,
-                                              const float *__restrict__ val,
-                                              const float *__restrict__ src0,
-                                              const float *__restrict__ src1, int32_t n_src0,
-                                              int32_t d, float *__restrict__ out,
-                                              float *__restrict__ partial)
+constexpr int kSpmmWaves = kSpmmThreads / kWave;
+
+// Entries in flight per lane group: a register budget of ~48 gathered floats
+// when the whole wave shares one entry (scalar addresses), ~32 when every
+// group has its own (per-lane 64-bit addresses).
+constexpr int spmm_inflight(int groups, int nch, int vec)
 {
-    constexpr int G = kWave / GL;   // entry groups per wave
-    constexpr int U = 4;            // entries in flight per group
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (w >= n_items)
-        return;   // uniform per wave
-    const SpmmItem it = items[w];
+    const int budget = groups == 1 ? 48 : 32;
+    const int cap = groups == 1 ? 12 : 8;
+    const int u = budget / (nch * vec);
+    return u < 2 ? 2 : (u > cap ? cap : u);
+}
+
+// One block of kSpmmWaves waves.  A short-row block gives wave w the row
+// b.row + w (w < b.nrows); a long-row block splits the entries [b.kb, b.ke)
+// of row b.row into kSpmmWaves contiguous parts, one per wave, and adds the
+// per-wave sums in LDS in wave order.  Inside a wave the lanes form 64/GL
+// groups: group g takes the entries j = g, g + G, ... of its range, lane gl
+// of a group accumulates the feature vectors gl, gl + GL, ... (NCH of them
+// per column pass).  Entry ids and weights are fetched 64 at a time (one per
+// lane) and broadcast; up to U entries per group are in flight.
+template <int VEC, int GL, int NCH, bool TWO>
+__global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restrict__ blocks,
+                                                       const int32_t *__restrict__ rowptr,
+                                                       const int32_t *__restrict__ col,
+                                                       const float *__restrict__ val,
+                                                       const float *__restrict__ src0,
+                                                       const float *__restrict__ src1,
+                                                       int32_t n_src0, int32_t d,
+                                                       float *__restrict__ out)
+{
+    constexpr int G = kWave / GL;
+    constexpr int U = spmm_inflight(G, NCH, VEC);
+    constexpr int SPAN = NCH * GL;   // feature vectors per column pass
+    __shared__ float red[kSpmmWaves][SPAN * VEC];
+
+    const SpmmBlock b = blocks[blockIdx.x];
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
     const int g = lane / GL;
     const int gl = lane % GL;
     const int dv = d / VEC;
-    float *dst = it.dst >= 0 ? out + (int64_t)it.dst * d
-                             : partial + (int64_t)(-(it.dst + 1)) * d;
+    const bool long_row = b.nrows == 0;   // uniform over the block
+    int row, kb, ke;
+    if (long_row) {
+        row = b.row;
+        const int per = (b.ke - b.kb + kSpmmWaves - 1) / kSpmmWaves;
+        kb = min(b.ke, b.kb + wave * per);
+        ke = min(b.ke, kb + per);
+    } else {
+        row = b.row + wave;
+        if (wave < b.nrows) {
+            kb = rowptr[row];
+            ke = rowptr[row + 1];
+        } else {
+            kb = ke = 0;
+        }
+    }
 
-    for (int c0 = 0; c0 < dv; c0 += GL) {
-        const int c = c0 + gl;
-        const bool active = c < dv;
-        float acc[VEC];
+    for (int c0 = 0; c0 < dv; c0 += SPAN) {
+        float acc[NCH][VEC];
 #pragma unroll
-        for (int v = 0; v < VEC; ++v)
-            acc[v] = 0.f;
+        for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                acc[ch][v] = 0.f;
 
-        for (int kb = it.kb; kb < it.ke; kb += kWave) {
-            const int nb = min(kWave, it.ke - kb);
+        for (int k0 = kb; k0 < ke; k0 += kWave) {
+            const int nb = min(kWave, ke - k0);
             int mc = 0;
             float mv = 0.f;
             if (lane < nb) {
-                mc = col[kb + lane];
-                mv = val[kb + lane];
+                mc = col[k0 + lane];
+                mv = val[k0 + lane];
             }
             const int steps = (nb + G - 1) / G;
-            int s = 0;
-            for (; s + U <= steps; s += U) {
+            for (int s = 0; s < steps; s += U) {
                 int cc[U];
                 float aa[U];
-                float x[U][VEC];
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    if constexpr (G == 1) {
-                        cc[u] = readlane_i(mc, s + u);
-                        aa[u] = readlane_f(mv, s + u);
-                    } else {
-                        const int j = (s + u) * G + g;
-                        cc[u] = __shfl(mc, j & (kWave - 1));
-                        aa[u] = __shfl(mv, j & (kWave - 1));
-                        if (j >= nb)
-                            aa[u] = 0.f;
-                    }
-                }
+                bool ok[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int j = (s + u) * G + g;
-                    if (active && j < nb) {
-                        const float *sp = (TWO && cc[u] >= n_src0)
-                                              ? src1 + (int64_t)(cc[u] - n_src0) * d
-                                              : src0 + (int64_t)cc[u] * d;
-                        load_vec<VEC>(sp + c * VEC, x[u]);
+                    if constexpr (G == 1) {
+                        cc[u] = readlane_i(mc, (s + u) & (kWave - 1));
+                        aa[u] = readlane_f(mv, (s + u) & (kWave - 1));
                     } else {
+                        cc[u] = __shfl(mc, j & (kWave - 1));
+                        aa[u] = __shfl(mv, j & (kWave - 1));
+                    }
+                    ok[u] = j < nb;
+                }
+                float x[U][NCH][VEC];
 #pragma unroll
-                        for (int v = 0; v < VEC; ++v)
-                            x[u][v] = 0.f;
+                for (int u = 0; u < U; ++u) {
+                    const float *sp = (TWO && cc[u] >= n_src0)
+                                          ? src1 + (int64_t)(cc[u] - n_src0) * d
+                                          : src0 + (int64_t)cc[u] * d;
+#pragma unroll
+                    for (int ch = 0; ch < NCH; ++ch) {
+                        const int c = c0 + ch * GL + gl;
+                        if (ok[u] && c < dv) {
+                            load_vec<VEC>(sp + c * VEC, x[u][ch]);
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < VEC; ++v)
+                                x[u][ch][v] = 0.f;
+                        }
                     }
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u)
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v)
-                        acc[v] = fmaf(aa[u], x[u][v], acc[v]);
-            }
-            for (; s < steps; ++s) {
-                int cj;
-                float aj;
-                const int j = s * G + g;
-                if constexpr (G == 1) {
-                    cj = readlane_i(mc, s);
-                    aj = readlane_f(mv, s);
-                } else {
-                    cj = __shfl(mc, j & (kWave - 1));
-                    aj = __shfl(mv, j & (kWave - 1));
-                }
-                if (active && j < nb) {
-                    const float *sp = (TWO && cj >= n_src0) ? src1 + (int64_t)(cj - n_src0) * d
-                                                            : src0 + (int64_t)cj * d;
-                    float x[VEC];
-                    load_vec<VEC>(sp + c * VEC, x);
+                    for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v)
-                        acc[v] = fmaf(aj, x[v], acc[v]);
-                }
+                        for (int v = 0; v < VEC; ++v)
+                            acc[ch][v] = fmaf(aa[u], x[u][ch][v], acc[ch][v]);
             }
         }
         if constexpr (G > 1) {
 #pragma unroll
             for (int off = GL; off < kWave; off <<= 1)
 #pragma unroll
-                for (int v = 0; v < VEC; ++v)
-                    acc[v] += __shfl_xor(acc[v], off);
+                for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        acc[ch][v] += __shfl_xor(acc[ch][v], off);
         }
-        if (g == 0 && active)
-            store_vec<VEC>(dst + c * VEC, acc);
-    }
-}
-
-__global__ __launch_bounds__(256) void k_spmm_fixup(const FixupItem *__restrict__ items,
-                                                    int32_t n_items, int32_t d,
-                                                    const float *__restrict__ partial,
-                                                    float *__restrict__ out)
-{
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (w >= n_items)
-        return;
-    const FixupItem it = items[w];
-    for (int c = lane; c < d; c += kWave) {
-        float acc = 0.f;
-        for (int s = 0; s < it.nseg; ++s)
-            acc += partial[(int64_t)(it.slot + s) * d + c];
-        out[(int64_t)it.row * d + c] = acc;
+        if (!long_row) {
+            if (wave < b.nrows && g == 0) {
+#pragma unroll
+                for (int ch = 0; ch < NCH; ++ch) {
+                    const int c = c0 + ch * GL + gl;
+                    if (c < dv)
+                        store_vec<VEC>(out + (int64_t)row * d + c * VEC, acc[ch]);
+                }
+            }
+        } else {
+            if (g == 0) {
+#pragma unroll
+                for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        red[wave][(ch * GL + gl) * VEC + v] = acc[ch][v];
+            }
+            __syncthreads();
+            for (int t = threadIdx.x; t < SPAN * VEC; t += kSpmmThreads) {
+                const int c = c0 + t / VEC;
+                if (c < dv) {
+                    float sum = 0.f;
+#pragma unroll
+                    for (int w = 0; w < kSpmmWaves; ++w)
+                        sum += red[w][t];
+                    out[(int64_t)row * d + (int64_t)c * VEC + t % VEC] = sum;
+                }
+            }
+            __syncthreads();
+        }
     }
 }
 
@@ -238,12 +270,68 @@ __global__ __launch_bounds__(256) void k_spmm_fixup(const FixupItem *__restrict_
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-// 64x64 tile of C per workgroup, 4 waves in a 2x2 arrangement, each wave one
-// 32x32 block accumulated with v_mfma_f32_32x32x2f32.  Operand tiles are
-// staged through LDS as [k][m] / [k][n] so that the fragment reads (lane l
-// takes row l%32 at k = l/32) are contiguous; the next K tile is fetched into
-// registers while the current one is multiplied.
-template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU>
+// One operand quad in flight: 4 consecutive elements of a row-major operand
+// (and of its mask) as loaded, plus whether they lie inside the operand.
+// The loads are issued unconditionally (an out-of-range quad reads the
+// operand's first element instead) so that the number of loads in flight is
+// static; the zero fill and the mask are applied only when the quad is
+// written to LDS, so no wait on the loads sits between fetch and compute.
+// With VEC the contiguous extent is a multiple of 4 and a quad is one
+// aligned 16-byte load.
+template <bool VEC, bool MASK>
+struct Quad {
+    float v[4];
+    float m[4];
+    uint32_t ok;   // bit j: element j is inside the operand
+
+    __device__ __forceinline__ void load(const float *__restrict__ base,
+                                         const float *__restrict__ mbase, int64_t off, int pos,
+                                         int lim, bool row_ok)
+    {
+        if constexpr (VEC) {
+            const bool in = row_ok && pos < lim;
+            const int64_t o = in ? off : 0;
+            const float4 a = *reinterpret_cast<const float4 *>(base + o);
+            v[0] = a.x;
+            v[1] = a.y;
+            v[2] = a.z;
+            v[3] = a.w;
+            if constexpr (MASK) {
+                const float4 b = *reinterpret_cast<const float4 *>(mbase + o);
+                m[0] = b.x;
+                m[1] = b.y;
+                m[2] = b.z;
+                m[3] = b.w;
+            }
+            ok = in ? 0xFu : 0u;
+        } else {
+            ok = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const bool in = row_ok && pos + j < lim;
+                const int64_t o = in ? off + j : 0;
+                v[j] = base[o];
+                if constexpr (MASK)
+                    m[j] = mbase[o];
+                ok |= in ? (1u << j) : 0u;
+            }
+        }
+    }
+
+    __device__ __forceinline__ float get(int j) const
+    {
+        const bool keep = ((ok >> j) & 1u) && (!MASK || m[j] > 0.f);
+        return keep ? v[j] : 0.f;
+    }
+};
+
+// 64x64 tile of C per workgroup; 4 waves in a 2x2 arrangement, each owning a
+// 32x32 block accumulated with v_mfma_f32_32x32x2f32.  K advances 32 at a
+// time through two LDS buffers ([k][m] and [k][n], so that the fragment read
+// of lane l -- row l%32 at k = l/32 -- is contiguous); the two following K
+// tiles are in flight in registers while the current one is multiplied (16
+// MFMAs per wave); one barrier per K step.
+template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
 __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, int32_t kchunk,
                                               const float *__restrict__ A, int32_t lda,
                                               const float *__restrict__ Am,
@@ -252,11 +340,12 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
                                               float *__restrict__ C, int32_t ldc,
                                               int64_t c_split_stride)
 {
-    constexpr int BM = kGemmBM, BN = kGemmBN, BK = kGemmBK, PAD = 4;
-    constexpr int PER = BM * BK / 256;   // elements per thread and operand
-    static_assert(BM * BK == BN * BK, "square operand tiles");
-    __shared__ float As[BK][BM + PAD];
-    __shared__ float Bs[BK][BN + PAD];
+    constexpr int BM = kGemmBM, BN = kGemmBN, BK = kGemmBK;
+    constexpr int PA = AT ? 4 : 1;   // [k][m] rows written as float4 when m is contiguous
+    constexpr int PB = BT ? 1 : 4;
+    static_assert(BM == 64 && BN == 64 && BK == 32, "tile shape assumed below");
+    __shared__ float As[2][BK][BM + PA];
+    __shared__ float Bs[2][BK][BN + PB];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -273,78 +362,95 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     for (int i = 0; i < 16; ++i)
         acc[i] = 0.f;
 
-    float ra[PER], rb[PER];
-    auto a_coord = [](int e, int &m, int &k) {
-        if (AT) {
-            m = e % BM;
-            k = e / BM;
-        } else {
-            k = e % BK;
-            m = e / BK;
-        }
-    };
-    auto b_coord = [](int e, int &n, int &k) {
-        if (BT) {
-            k = e % BK;
-            n = e / BK;
-        } else {
-            n = e % BN;
-            k = e / BN;
-        }
-    };
-    auto fetch = [&](int k0) {
+    // Each thread moves two quads (4 consecutive elements) of each operand
+    // tile per K step: quad q = tid + 256*i.  Two register sets hold the next
+    // two K tiles, so every global load has two compute phases to land.
+    using QA = Quad<VA, AMASK>;
+    using QB = Quad<VB, BMASK>;
+    QA qa0[2], qa1[2];
+    QB qb0[2], qb1[2];
+    auto fetch = [&](int k0, QA (&qa)[2], QB (&qb)[2]) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int e = tid + i * 256;
-            int m, n, k;
-            a_coord(e, m, k);
-            float v = 0.f;
-            if (m0 + m < M && k0 + k < ke) {
-                const int64_t idx = AT ? (int64_t)(k0 + k) * lda + (m0 + m)
-                                       : (int64_t)(m0 + m) * lda + (k0 + k);
-                v = A[idx];
-                if (AMASK && !(Am[idx] > 0.f))
-                    v = 0.f;
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + 256 * i;
+            if (AT) {   // A(m,k) = A[k*lda + m]; quad along m
+                const int k = q / (BM / 4), m = (q % (BM / 4)) * 4;
+                qa[i].load(A, Am, (int64_t)(k0 + k) * lda + (m0 + m), m0 + m, M, k0 + k < ke);
+            } else {    // A(m,k) = A[m*lda + k]; quad along k
+                const int m = q / (BK / 4), k = (q % (BK / 4)) * 4;
+                qa[i].load(A, Am, (int64_t)(m0 + m) * lda + (k0 + k), k0 + k, ke, m0 + m < M);
             }
-            ra[i] = v;
-            b_coord(e, n, k);
-            float u = 0.f;
-            if (n0 + n < N && k0 + k < ke) {
-                const int64_t idx = BT ? (int64_t)(n0 + n) * ldb + (k0 + k)
-                                       : (int64_t)(k0 + k) * ldb + (n0 + n);
-                u = B[idx];
-                if (BMASK && !(Bm[idx] > 0.f))
-                    u = 0.f;
+            if (BT) {   // B(k,n) = B[n*ldb + k]; quad along k
+                const int n = q / (BK / 4), k = (q % (BK / 4)) * 4;
+                qb[i].load(B, Bm, (int64_t)(n0 + n) * ldb + (k0 + k), k0 + k, ke, n0 + n < N);
+            } else {    // B(k,n) = B[k*ldb + n]; quad along n
+                const int k = q / (BN / 4), n = (q % (BN / 4)) * 4;
+                qb[i].load(B, Bm, (int64_t)(k0 + k) * ldb + (n0 + n), n0 + n, N, k0 + k < ke);
             }
-            rb[i] = u;
         }
     };
-    auto stash = [&]() {
+    auto stash = [&](int buf, const QA (&qa)[2], const QB (&qb)[2]) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int e = tid + i * 256;
-            int m, n, k;
-            a_coord(e, m, k);
-            As[k][m] = ra[i];
-            b_coord(e, n, k);
-            Bs[k][n] = rb[i];
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + 256 * i;
+            if (AT) {
+                const int k = q / (BM / 4), m = (q % (BM / 4)) * 4;
+                *reinterpret_cast<float4 *>(&As[buf][k][m]) =
+                    make_float4(qa[i].get(0), qa[i].get(1), qa[i].get(2), qa[i].get(3));
+            } else {
+                const int m = q / (BK / 4), k = (q % (BK / 4)) * 4;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    As[buf][k + j][m] = qa[i].get(j);
+            }
+            if (BT) {
+                const int n = q / (BK / 4), k = (q % (BK / 4)) * 4;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    Bs[buf][k + j][n] = qb[i].get(j);
+            } else {
+                const int k = q / (BN / 4), n = (q % (BN / 4)) * 4;
+                *reinterpret_cast<float4 *>(&Bs[buf][k][n]) =
+                    make_float4(qb[i].get(0), qb[i].get(1), qb[i].get(2), qb[i].get(3));
+            }
         }
+    };
+    // All fragment reads of a K step are issued before its MFMAs, so LDS
+    // latency is paid once per step instead of once per MFMA.
+    auto compute = [&](int buf) {
+        float fa[BK / 2], fb[BK / 2];
+#pragma unroll
+        for (int s = 0; s < BK / 2; ++s) {
+            fa[s] = As[buf][2 * s + (lane >> 5)][wm + (lane & 31)];
+            fb[s] = Bs[buf][2 * s + (lane >> 5)][wn + (lane & 31)];
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep every read ahead of the MFMAs
+#pragma unroll
+        for (int s = 0; s < BK / 2; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[s], fb[s], acc, 0, 0, 0);
     };
 
-    if (kb < ke)
-        fetch(kb);
-    for (int k0 = kb; k0 < ke; k0 += BK) {
+    // Tile t sits in LDS buffer t % 2; tile t+1 is in flight in one register
+    // set while tile t+2 is requested into the other.  The loop body is
+    // straight-line (tiles past the end load as zeros and add nothing), so
+    // the compiler can wait on exactly the older register set.
+    const int ntiles = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    if (ntiles > 0) {
+        fetch(kb, qa0, qb0);
+        stash(0, qa0, qb0);
+        fetch(kb + BK, qa1, qb1);
+    }
+    __syncthreads();
+    for (int t = 0; t < ntiles; t += 2) {
+        const int k0 = kb + t * BK;
+        fetch(k0 + 2 * BK, qa0, qb0);
+        compute(0);
+        stash(1, qa1, qb1);
         __syncthreads();
-        stash();
+        fetch(k0 + 3 * BK, qa1, qb1);
+        compute(1);
+        stash(0, qa0, qb0);
         __syncthreads();
-        if (k0 + BK < ke)
-            fetch(k0 + BK);
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            const float a = As[kk + (lane >> 5)][wm + (lane & 31)];
-            const float b = Bs[kk + (lane >> 5)][wn + (lane & 31)];
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
-        }
     }
 
     float *Cz = C + (int64_t)blockIdx.z * c_split_stride;
@@ -361,6 +467,8 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     }
 }
 
+// out[e] = sum over z of part[z][e], z ascending; one element per thread,
+// eight slices in flight.
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__ part,
                                                        int32_t splits, int64_t count,
                                                        float *__restrict__ out)
@@ -369,7 +477,17 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__
     if (e >= count)
         return;
     float acc = 0.f;
-    for (int z = 0; z < splits; ++z)
+    int z = 0;
+    for (; z + 8 <= splits; z += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = part[(int64_t)(z + u) * count + e];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            acc += v[u];
+    }
+    for (; z < splits; ++z)
         acc += part[(int64_t)z * count + e];
     out[e] = acc;
 }
@@ -495,53 +613,93 @@ hipError_t copy_rows_v(int gl, const int32_t *sidx, const int32_t *didx, int32_t
     }
 }
 
-template <int VEC, int GL, bool TWO>
-hipError_t spmm_t(const SpmmItem *items, int32_t n_items, const int32_t *col, const float *val,
-                  const float *src0, const float *src1, int32_t n_src0, int32_t d, float *out,
-                  float *partial, hipStream_t s)
+template <int VEC, int GL, int NCH, bool TWO>
+hipError_t spmm_t(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
+                  const int32_t *col, const float *val, const float *src0, const float *src1,
+                  int32_t n_src0, int32_t d, float *out, hipStream_t s)
 {
-    const int64_t blocks = ((int64_t)n_items + 3) / 4;
-    hipLaunchKernelGGL((k_spmm<VEC, GL, TWO>), dim3((unsigned)blocks), dim3(256), 0, s, items,
-                       n_items, col, val, src0, src1, n_src0, d, out, partial);
+    hipLaunchKernelGGL((k_spmm<VEC, GL, NCH, TWO>), dim3((unsigned)n_blocks), dim3(kSpmmThreads),
+                       0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, out);
     return hipGetLastError();
 }
 
+#define DIGEST_SPMM_ARGS blocks, n_blocks, rowptr, col, val, src0, src1, n_src0, d, out, s
+
 template <int VEC, bool TWO>
-hipError_t spmm_g(int gl, const SpmmItem *items, int32_t n_items, const int32_t *col,
-                  const float *val, const float *src0, const float *src1, int32_t n_src0,
-                  int32_t d, float *out, float *partial, hipStream_t s)
+hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
+                  const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
+                  const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
 {
     switch (gl) {
-    case 4: return spmm_t<VEC, 4, TWO>(items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    case 8: return spmm_t<VEC, 8, TWO>(items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    case 16: return spmm_t<VEC, 16, TWO>(items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    case 32: return spmm_t<VEC, 32, TWO>(items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    default: return spmm_t<VEC, 64, TWO>(items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
+    case 4: return spmm_t<VEC, 4, 1, TWO>(DIGEST_SPMM_ARGS);
+    case 8: return spmm_t<VEC, 8, 1, TWO>(DIGEST_SPMM_ARGS);
+    case 16: return spmm_t<VEC, 16, 1, TWO>(DIGEST_SPMM_ARGS);
+    case 32: return spmm_t<VEC, 32, 1, TWO>(DIGEST_SPMM_ARGS);
+    default: break;
+    }
+    if constexpr (VEC == 4) {
+        return nch >= 2 ? spmm_t<4, 64, 2, TWO>(DIGEST_SPMM_ARGS)
+                        : spmm_t<4, 64, 1, TWO>(DIGEST_SPMM_ARGS);
+    } else if constexpr (VEC == 2) {
+        switch (nch) {
+        case 1: return spmm_t<2, 64, 1, TWO>(DIGEST_SPMM_ARGS);
+        case 2: return spmm_t<2, 64, 2, TWO>(DIGEST_SPMM_ARGS);
+        case 3: return spmm_t<2, 64, 3, TWO>(DIGEST_SPMM_ARGS);
+        case 4: return spmm_t<2, 64, 4, TWO>(DIGEST_SPMM_ARGS);
+        default: return spmm_t<2, 64, 5, TWO>(DIGEST_SPMM_ARGS);
+        }
+    } else {
+        switch (nch) {
+        case 1: return spmm_t<1, 64, 1, TWO>(DIGEST_SPMM_ARGS);
+        case 2: return spmm_t<1, 64, 2, TWO>(DIGEST_SPMM_ARGS);
+        default: return spmm_t<1, 64, 4, TWO>(DIGEST_SPMM_ARGS);
+        }
     }
 }
 
 template <bool TWO>
-hipError_t spmm_v(int vec, int gl, const SpmmItem *items, int32_t n_items, const int32_t *col,
-                  const float *val, const float *src0, const float *src1, int32_t n_src0,
-                  int32_t d, float *out, float *partial, hipStream_t s)
+hipError_t spmm_v(int vec, int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
+                  const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
+                  const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
 {
     switch (vec) {
-    case 4: return spmm_g<4, TWO>(gl, items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    case 2: return spmm_g<2, TWO>(gl, items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
-    default: return spmm_g<1, TWO>(gl, items, n_items, col, val, src0, src1, n_src0, d, out, partial, s);
+    case 4: return spmm_g<4, TWO>(gl, nch, DIGEST_SPMM_ARGS);
+    case 2: return spmm_g<2, TWO>(gl, nch, DIGEST_SPMM_ARGS);
+    default: return spmm_g<1, TWO>(gl, nch, DIGEST_SPMM_ARGS);
     }
 }
 
-template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU>
+template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
 hipError_t gemm_t(const GemmArgs &a, hipStream_t s)
 {
     const dim3 grid((unsigned)((a.M + kGemmBM - 1) / kGemmBM),
                     (unsigned)((a.N + kGemmBN - 1) / kGemmBN), (unsigned)a.splits);
     const int64_t split_stride = a.splits > 1 ? (int64_t)a.M * a.ldc : 0;
-    hipLaunchKernelGGL((k_gemm<AT, BT, AMASK, BMASK, RELU>), grid, dim3(256), 0, s, a.M, a.N,
-                       a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb, a.b_mask, a.C, a.ldc,
-                       split_stride);
+    hipLaunchKernelGGL((k_gemm<AT, BT, AMASK, BMASK, RELU, VA, VB>), grid, dim3(256), 0, s, a.M,
+                       a.N, a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb, a.b_mask, a.C,
+                       a.ldc, split_stride);
     return hipGetLastError();
+}
+
+// 16-byte operand loads need a 16-byte aligned base (and mask) and a leading
+// dimension that keeps every row 16-byte aligned.
+bool quad_ok(const float *p, const float *mask, int32_t ld)
+{
+    auto al = [](const float *q) { return q == nullptr || ((uintptr_t)q % 16) == 0; };
+    return al(p) && al(mask) && ld % 4 == 0;
+}
+
+template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU>
+hipError_t gemm_q(const GemmArgs &a, hipStream_t s)
+{
+    const bool va = quad_ok(a.A, a.a_mask, a.lda), vb = quad_ok(a.B, a.b_mask, a.ldb);
+    if (va && vb)
+        return gemm_t<AT, BT, AMASK, BMASK, RELU, true, true>(a, s);
+    if (va)
+        return gemm_t<AT, BT, AMASK, BMASK, RELU, true, false>(a, s);
+    if (vb)
+        return gemm_t<AT, BT, AMASK, BMASK, RELU, false, true>(a, s);
+    return gemm_t<AT, BT, AMASK, BMASK, RELU, false, false>(a, s);
 }
 
 }  // namespace
@@ -560,52 +718,47 @@ hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_
     }
 }
 
-hipError_t launch_spmm(const SpmmItem *items, int32_t n_items, const int32_t *col,
-                       const float *val, const float *src0, const float *src1,
-                       int32_t n_src0, int32_t d, float *out, float *partial, hipStream_t s)
+hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const float *src0,
+                       const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
 {
-    if (n_items <= 0 || d <= 0)
+    if (n_blocks <= 0 || d <= 0)
         return hipSuccess;
     int vec = pick_vec(d, src0, out);
-    if (src1 && pick_vec(d, src1, partial) < vec)
-        vec = pick_vec(d, src1, partial);
-    const int gl = pick_group(d / vec);
+    if (src1 && pick_vec(d, src1, nullptr) < vec)
+        vec = pick_vec(d, src1, nullptr);
+    const int dv = d / vec;
+    const int gl = pick_group(dv);
+    const int max_nch = vec == 4 ? 2 : (vec == 2 ? 5 : 4);
+    int nch = (dv + kWave - 1) / kWave;
+    if (vec == 1 && nch == 3)
+        nch = 4;
+    nch = nch < 1 ? 1 : (nch > max_nch ? max_nch : nch);
     if (src1)
-        return spmm_v<true>(vec, gl, items, n_items, col, val, src0, src1, n_src0, d, out,
-                            partial, s);
-    return spmm_v<false>(vec, gl, items, n_items, col, val, src0, src1, n_src0, d, out, partial,
-                         s);
-}
-
-hipError_t launch_spmm_fixup(const FixupItem *items, int32_t n_items, int32_t d,
-                             const float *partial, float *out, hipStream_t s)
-{
-    if (n_items <= 0 || d <= 0)
-        return hipSuccess;
-    const int64_t blocks = ((int64_t)n_items + 3) / 4;
-    hipLaunchKernelGGL(k_spmm_fixup, dim3((unsigned)blocks), dim3(256), 0, s, items, n_items, d,
-                       partial, out);
-    return hipGetLastError();
+        return spmm_v<true>(vec, gl, nch, DIGEST_SPMM_ARGS);
+    return spmm_v<false>(vec, gl, nch, DIGEST_SPMM_ARGS);
 }
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
 {
     if (a.M <= 0 || a.N <= 0)
         return hipSuccess;
+    if (a.splits > 1 && a.kchunk % kGemmBK != 0)
+        return hipErrorInvalidValue;   // split starts must stay quad aligned
     const bool am = a.a_mask != nullptr, bm = a.b_mask != nullptr;
     // The instantiations the layer needs:
     //   forward      A.B        (+ReLU epilogue)
     //   dW           A^T.B      (B optionally masked)
     //   D.W^T        A.B^T      (A optionally masked)
     if (!a.a_trans && !a.b_trans && !am && !bm)
-        return a.relu ? gemm_t<false, false, false, false, true>(a, s)
-                      : gemm_t<false, false, false, false, false>(a, s);
+        return a.relu ? gemm_q<false, false, false, false, true>(a, s)
+                      : gemm_q<false, false, false, false, false>(a, s);
     if (a.a_trans && !a.b_trans && !am && !a.relu)
-        return bm ? gemm_t<true, false, false, true, false>(a, s)
-                  : gemm_t<true, false, false, false, false>(a, s);
+        return bm ? gemm_q<true, false, false, true, false>(a, s)
+                  : gemm_q<true, false, false, false, false>(a, s);
     if (!a.a_trans && a.b_trans && !bm && !a.relu)
-        return am ? gemm_t<false, true, true, false, false>(a, s)
-                  : gemm_t<false, true, false, false, false>(a, s);
+        return am ? gemm_q<false, true, true, false, false>(a, s)
+                  : gemm_q<false, true, false, false, false>(a, s);
     return hipErrorInvalidValue;
 }
 

@@ -8,33 +8,29 @@
 
 namespace digest {
 
-// One unit of sparse-aggregation work: CSR entries [kb, ke) of row `row`.
-// dst >= 0: the result is row `dst` of the output; dst < 0: the result is a
-// partial sum stored in scratch slot (-dst - 1) and summed by a fixup pass.
-struct SpmmItem {
-    int32_t row, kb, ke, dst;
+// One block of sparse-aggregation work (kSpmmThreads threads = 8 waves).
+//   nrows > 0: the short rows [row, row + nrows), one per wave (nrows <= 8);
+//   nrows == 0: the single long row `row`, whose entries [kb, ke) the waves
+//               split among themselves.
+struct SpmmBlock {
+    int32_t row, nrows, kb, ke;
 };
 
-// A row whose entries were split into `nseg` items with consecutive scratch
-// slots starting at `slot`: out[row] = sum of those slots, in slot order.
-struct FixupItem {
-    int32_t row, slot, nseg, pad;
-};
+constexpr int kSpmmThreads = 512;
+// Rows with more entries than this get a whole block.
+constexpr int32_t kSpmmLongRow = 64;
 
 // dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows.
 hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
                             int32_t d, const float *src, float *dst, hipStream_t s);
 
-// Two-source CSR aggregation.  Column c < n_src0 reads row c of src0,
-// otherwise row (c - n_src0) of src1.  Every output row (and every scratch
-// slot) named by an item is fully written.
-hipError_t launch_spmm(const SpmmItem *items, int32_t n_items, const int32_t *col,
-                       const float *val, const float *src0, const float *src1,
-                       int32_t n_src0, int32_t d, float *out, float *partial,
+// Two-source CSR aggregation out[r] = sum_k val[k] * src(col[k]) over the
+// rows named by the blocks.  Column c < n_src0 reads row c of src0,
+// otherwise row (c - n_src0) of src1.  Every named row is fully written.
+hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const float *src0,
+                       const float *src1, int32_t n_src0, int32_t d, float *out,
                        hipStream_t s);
-
-hipError_t launch_spmm_fixup(const FixupItem *items, int32_t n_items, int32_t d,
-                             const float *partial, float *out, hipStream_t s);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split over grid.z when splits > 1.
 //   op(A)(m,k) = a_trans ? A[k*lda + m] : A[m*lda + k]      (M x K)
@@ -75,6 +71,6 @@ hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32
 // GEMM tile sizes (rows of C per workgroup, cols of C per workgroup, K step).
 constexpr int kGemmBM = 64;
 constexpr int kGemmBN = 64;
-constexpr int kGemmBK = 16;
+constexpr int kGemmBK = 32;
 
 }  // namespace digest
