@@ -32,12 +32,36 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 
 
-def round_model(st, widths, splits):
+def transform_first(l, widths):
+    """Mirror of the library's choice: identity layers at least 4x narrowing."""
+    return l == len(widths) - 1 and 4 * widths[l] <= widths[l - 1]
+
+
+def splitk(M, N, K):
+    """Mirror of the library's split-K plan: (splits, rows per split)."""
+    tiles = -(-M // 64) * -(-N // 64)
+    s = max(1, min(-(-768 // max(tiles, 1)), max(1, K // 256), 256))
+    chunk = -(-K // s)
+    chunk = -(-chunk // 32) * 32 or 32
+    return max(1, -(-K // chunk)), chunk
+
+
+def tf_slices(n, nh, di, do):
+    if do <= 16:
+        R = n + nh
+        target = 512 // max(1, -(-di // 256))
+        chunk = max(64, -(-R // max(target, 1)))
+        return max(1, -(-R // chunk))
+    return splitk(di, do, n)[0] + (splitk(di, do, nh)[0] if nh else 0)
+
+
+def round_model(st, widths):
     """Algorithmic bytes / flops per round for each kernel kind.
 
     Returns {kind: (bytes, flops, launches)} for the kinds that run every
-    round, and per-launch figures for pull/push (their launches depend on
-    the schedule).
+    round, and per-launch bytes for pull/push (their launches depend on the
+    schedule).  The layer order (aggregate-first or transform-first) follows
+    the library's rule.
     """
     n, nh, nnz, nnz_in, nb = st["n_own"], st["n_halo"], st["nnz"], st["nnz_in"], st["n_boundary"]
     L = len(widths) - 1
@@ -53,12 +77,23 @@ def round_model(st, widths, splits):
     for l in range(1, L + 1):
         di, do = widths[l - 1], widths[l]
         relu = l < L
+        if transform_first(l, widths):
+            R = n + nh
+            add("gemm_fwd_relu", 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
+            add("spmm_fwd", 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)
+            add("spmm_bwd_transposed", 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do)
+            add("gemm_dw_splitk", 4 * (R * di + R * do), 2.0 * R * di * do)
+            add("splitk_reduce_dw", 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
+            if l > 1:
+                add("gemm_dgrad", 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
+            continue
         add("spmm_fwd", 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)
         add("gemm_fwd_relu", 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
         add("gemm_dw_splitk", 4 * (n * di + n * do * (2 if relu else 1) + di * do),
             2.0 * n * di * do)
-        if splits[l] > 1:
-            add("splitk_reduce_dw", 4 * (splits[l] + 1) * di * do)
+        s = splitk(di, do, n)[0]
+        if s > 1:
+            add("splitk_reduce_dw", 4 * (s + 1) * di * do)
         if l > 1:
             narrow = (not relu) and do < di
             w = do if narrow else di
@@ -71,19 +106,6 @@ def round_model(st, widths, splits):
         "push_scatter": {l: 8.0 * nb * widths[l] + 8 * nb for l in range(1, L)},
     }
     return {k: tuple(v) for k, v in m.items()}, per_launch
-
-
-def splitk_factors(n, widths):
-    """Mirror of the library's split-K choice (for the byte model only)."""
-    out = {}
-    for l in range(1, len(widths)):
-        M, N = widths[l - 1], widths[l]
-        tiles = -(-M // 64) * -(-N // 64)
-        s = max(1, min(-(-768 // max(tiles, 1)), max(1, n // 256), 256))
-        chunk = -(-n // s)
-        chunk = -(-chunk // 32) * 32 or 32
-        out[l] = max(1, -(-n // chunk))
-    return out
 
 
 def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
@@ -194,7 +216,7 @@ def main():
         gp.round(r, K, x_own, dWs, stores, dy)
     prof = D.digest_profile_read(gp.p)
     D.digest_profile_enable(gp.p, False)
-    model, per_launch = round_model(st, cfg.widths, splitk_factors(st["n_own"], cfg.widths))
+    model, per_launch = round_model(st, cfg.widths)
     kernels = {}
     for kind, (tot_ms, n_l) in prof.items():
         if n_l == 0:

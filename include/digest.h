@@ -117,7 +117,8 @@ digest_status digest_partition_export_maps(const digest_partition *p, int32_t *c
                                            int64_t *boundary_gid,
                                            int32_t *boundary_local);
 
-/* Test hook: CSR of P_in^T (t_indptr[n_owned+1], t_src[nnz_in], t_vals[nnz_in]). */
+/* Test hook: CSR of P_in^T (t_indptr[n_owned+1], t_src[nnz_in], t_vals[nnz_in]);
+ * row c lists the owned rows with an entry in owned column c, ascending. */
 digest_status digest_partition_export_transpose(const digest_partition *p,
                                                 int64_t *t_indptr, int32_t *t_src,
                                                 float *t_vals);
@@ -155,13 +156,18 @@ digest_status digest_push(digest_partition *p, int32_t level, const float *h_own
                           float *store, int32_t mode, void *hip_stream);
 
 /*
- * Layer forward (Eq. 5):  AH = P_in h_in + P_out halo_buf[layer-1]
- * (two-source sparse aggregation), then h_out = act(AH W).  AH is kept in
- * the workspace for digest_layer_backward of the same layer.
+ * Layer forward (Eq. 5):  h_out = act(P_in h_in W + P_out halo_buf[layer-1] W)
  *   layer  1..L.   h_in  device [n_owned, d_{layer-1}] (fresh own rows).
  *   w      device [d_{layer-1}, d_layer].   h_out device [n_owned, d_layer].
  *   act    DIGEST_ACT_RELU or DIGEST_ACT_IDENTITY (the paper uses ReLU on
  *          hidden layers and raw logits at the last layer).
+ * Order of the two products (the same result up to float rounding): a
+ * layer with the identity activation whose output is at least 4x narrower
+ * than its input is computed transform-first, T = [h_in; halo] W over all
+ * n_owned + n_halo local rows, then h_out = P_m T, so that the sparse
+ * aggregation runs at the narrow width; every other layer aggregates first,
+ * AH = P_m [h_in; halo], then h_out = act(AH W), keeping AH in the
+ * workspace for the backward.
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace, or level layer-1 never
  * pulled while the partition has halo nodes), DIGEST_EHIP.
  */
@@ -171,17 +177,20 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
 
 /*
  * Layer backward (Eq. 6 with the upstream gradient; GCN backward of
- * Appendix A.3), using the AH saved by the last forward of `layer`:
+ * Appendix A.3) of the last forward of `layer`:
  *   D     = dh_out * 1[h_out > 0]  (ReLU) or dh_out (identity)
- *   dw    = AH^T D                              (overwritten)
- *   dh_in = P_in^T (D W^T)   if dh_in != NULL   (overwritten)
+ *   dw    = (P_m [h_in; halo])^T D                      (overwritten)
+ *   dh_in = P_in^T D W^T           if dh_in != NULL    (overwritten)
  * The stale halo rows are constants of the layer: they get no gradient.
- *   h_out, dh_out device [n_owned, d_layer];  w device [d_{layer-1}, d_layer];
- *   dw device [d_{layer-1}, d_layer];  dh_in device [n_owned, d_{layer-1}].
+ *   h_in   the same device array the forward of this layer read (it must
+ *          be unchanged); h_out, dh_out device [n_owned, d_layer];
+ *   w device [d_{layer-1}, d_layer];  dw device [d_{layer-1}, d_layer];
+ *   dh_in device [n_owned, d_{layer-1}].
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no forward of this layer since the
- * workspace was bound), DIGEST_EHIP.
+ * workspace was bound, or level layer-1 pulled again since that forward:
+ * the halo rows the forward used are gone), DIGEST_EHIP.
  */
-digest_status digest_layer_backward(digest_partition *p, int32_t layer,
+digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_in,
                                     const float *h_out, const float *dh_out,
                                     const float *w, float *dw, float *dh_in,
                                     void *hip_stream);

@@ -75,6 +75,16 @@ void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchu
     kchunk = (int32_t)chunk;
 }
 
+// Workgroup tile of C for a GEMM (see GemmArgs::tile): 64x64 keeps enough
+// workgroups for the partition-sized products; very tall forward products
+// and long split-K contractions run slightly faster on larger tiles.
+int32_t gemm_tile_for(int64_t M, int64_t N, int64_t K, bool contraction_over_rows)
+{
+    if (contraction_over_rows)
+        return (K >= 100000 && M >= 128) ? 2 : 0;
+    return (M >= 100000 && N >= 128) ? 3 : 0;
+}
+
 // Aggregation blocks of a CSR: every long row gets a block of its own (those
 // come first, so they start early); runs of consecutive short rows are
 // packed one per wave.
@@ -113,21 +123,26 @@ struct digest_partition {
     // host copies of everything uploaded at bind time
     std::vector<int32_t> rowptr, col, t_rowptr, t_src, halo_gid, bnd_local, bnd_gid, owned_gid;
     std::vector<float> val, t_val;
-    std::vector<SpmmBlock> blocks_f, blocks_t;
+    // blocks_t covers the first n_own rows of the transpose (P_in^T),
+    // blocks_tf all n_own + n_halo rows (P_m^T).
+    std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf;
 
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
-        size_t blocks_f, blocks_t;
+        size_t blocks_f, blocks_t, blocks_tf;
         std::vector<size_t> halo_buf;   // per level 0..L-1
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused)
-        size_t tmp, gemm_part, loss_part;
+        size_t tmp, tbuf, gemm_part, loss_part;
         size_t total;
     } lay{};
 
     char *ws = nullptr;
-    std::vector<char> pulled;     // per level
-    std::vector<char> fwd_done;   // per layer
-    std::vector<int32_t> act;     // per layer
+    std::vector<char> pulled;       // per level
+    std::vector<int64_t> pull_gen;  // per level: number of pulls since bind
+    std::vector<char> fwd_done;     // per layer
+    std::vector<int32_t> act;       // per layer
+    std::vector<char> tf;           // per layer: forward ran transform-first
+    std::vector<int64_t> fwd_gen;   // per layer: pull_gen of level layer-1 at forward
 
     bool prof = false;
     struct Rec {
@@ -146,6 +161,51 @@ struct digest_partition {
 
 namespace {
 
+// A layer whose output is at least 4x narrower than its input: with the
+// identity activation it runs transform-first, Z = P_m ([H_in; H~_out] W),
+// aggregating at the narrow width (the same product, associated the other
+// way).
+bool narrow_layer(int64_t d_in, int64_t d_out) { return 4 * d_out <= d_in; }
+
+// The kernels for a narrow side (<= kNarrow columns); the dgrad one stages
+// W (d_in x 16 floats) in LDS, which bounds d_in.
+bool narrow_valu(int64_t d_in, int64_t d_out)
+{
+    return d_out <= digest::kNarrow && d_in <= 1024;
+}
+
+// Split-K slices of the transform-first weight gradient H_mix^T G over the
+// n_own + n_halo rows.  Narrow outputs (<= kNarrow) use the VALU kernel with
+// `chunk` rows per slice; wider ones use the MFMA GEMM twice (owned rows,
+// then halo rows) with their own split plans.
+struct TfPlan {
+    bool valu;
+    int32_t chunk, slices;           // VALU: rows per slice, number of slices
+    int32_t s_own, k_own, s_halo, k_halo;   // MFMA: splits and chunks
+};
+
+TfPlan tf_plan(int64_t n_own, int64_t n_halo, int64_t d_in, int64_t d_out)
+{
+    TfPlan t{};
+    const int64_t R = n_own + n_halo;
+    t.valu = d_out <= digest::kNarrow;
+    if (t.valu) {
+        // about 2,048 waves: (d_in / 64) feature blocks x slices of >= 32 rows
+        const int64_t fblocks = (d_in + 63) / 64;
+        const int64_t target = std::max<int64_t>(1, 2048 / fblocks);
+        int64_t chunk = std::max<int64_t>(32, (R + target - 1) / target);
+        chunk = (chunk + 31) / 32 * 32;
+        t.chunk = (int32_t)chunk;
+        t.slices = (int32_t)std::max<int64_t>(1, (R + chunk - 1) / chunk);
+    } else {
+        splitk_plan(d_in, d_out, n_own, t.s_own, t.k_own);
+        if (n_halo > 0)
+            splitk_plan(d_in, d_out, n_halo, t.s_halo, t.k_halo);
+        t.slices = t.s_own + (n_halo > 0 ? t.s_halo : 0);
+    }
+    return t;
+}
+
 void plan_layout(digest_partition &p)
 {
     auto &l = p.lay;
@@ -158,22 +218,23 @@ void plan_layout(digest_partition &p)
     l.rowptr = take(sizeof(int32_t) * (p.n_own + 1));
     l.col = take(sizeof(int32_t) * p.nnz);
     l.val = take(sizeof(float) * p.nnz);
-    l.t_rowptr = take(sizeof(int32_t) * (p.n_own + 1));
-    l.t_src = take(sizeof(int32_t) * p.nnz_in);
-    l.t_val = take(sizeof(float) * p.nnz_in);
+    l.t_rowptr = take(sizeof(int32_t) * ((size_t)p.n_own + p.n_halo + 1));
+    l.t_src = take(sizeof(int32_t) * p.nnz);
+    l.t_val = take(sizeof(float) * p.nnz);
     l.halo_gid = take(sizeof(int32_t) * p.n_halo);
     l.bnd_local = take(sizeof(int32_t) * p.n_bnd);
     l.bnd_gid = take(sizeof(int32_t) * p.n_bnd);
     l.owned_gid = take(sizeof(int32_t) * p.n_own);
     l.blocks_f = take(sizeof(SpmmBlock) * p.blocks_f.size());
     l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
+    l.blocks_tf = take(sizeof(SpmmBlock) * p.blocks_tf.size());
     l.halo_buf.assign(p.L, 0);
     for (int32_t lev = 0; lev < p.L; ++lev)
         l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * p.widths[lev]);
     l.ah.assign(p.L + 1, 0);
     for (int32_t k = 1; k <= p.L; ++k)
         l.ah[k] = take(sizeof(float) * (size_t)p.n_own * p.widths[k - 1]);
-    int64_t wmax = 0, gemm_part = 0;
+    int64_t wmax = 0, gemm_part = 0, tbuf = 0;
     for (int32_t k = 1; k <= p.L; ++k) {
         const int64_t di = p.widths[k - 1], dout = p.widths[k];
         wmax = std::max({wmax, di, dout});
@@ -181,8 +242,14 @@ void plan_layout(digest_partition &p)
         splitk_plan(di, dout, p.n_own, splits, kchunk);
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
+        if (narrow_layer(di, dout)) {
+            tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + p.n_halo) * dout);
+            const TfPlan t = tf_plan(p.n_own, p.n_halo, di, dout);
+            gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
+        }
     }
     l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
+    l.tbuf = take(sizeof(float) * (size_t)tbuf);
     l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
     l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own));
     l.total = o;
@@ -243,19 +310,23 @@ digest_status need_bound(const digest_partition *p)
     return DIGEST_OK;
 }
 
-// Sparse aggregation over the local CSR (forward) or the CSR of P_in^T.
-digest_status run_spmm(digest_partition *p, bool transposed, const float *src0,
-                       const float *src1, int32_t d, float *out, hipStream_t s)
+// Sparse aggregation over the local CSR (P_m), the CSR of P_in^T (the first
+// n_own rows of the transpose) or of P_m^T (all of it).
+enum class Csr { Fwd, InT, FullT };
+
+digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
+                       int32_t n_src0, int32_t d, float *out, hipStream_t s)
 {
-    const auto &blocks = transposed ? p->blocks_t : p->blocks_f;
-    Timed t(p, transposed ? K_SPMM_BWD : K_SPMM_FWD, s);
+    const bool fwd = which == Csr::Fwd;
+    const auto &blocks = fwd ? p->blocks_f : (which == Csr::InT ? p->blocks_t : p->blocks_tf);
+    const size_t boff = fwd ? p->lay.blocks_f : (which == Csr::InT ? p->lay.blocks_t : p->lay.blocks_tf);
+    Timed t(p, fwd ? K_SPMM_FWD : K_SPMM_BWD, s);
     return hip_check(
-        digest::launch_spmm(p->at<SpmmBlock>(transposed ? p->lay.blocks_t : p->lay.blocks_f),
-                            (int32_t)blocks.size(),
-                            p->at<int32_t>(transposed ? p->lay.t_rowptr : p->lay.rowptr),
-                            p->at<int32_t>(transposed ? p->lay.t_src : p->lay.col),
-                            p->at<float>(transposed ? p->lay.t_val : p->lay.val), src0, src1,
-                            p->n_own, d, out, s),
+        digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks.size(),
+                            p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr),
+                            p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
+                            p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1, n_src0, d,
+                            out, s),
         "spmm");
 }
 
@@ -361,32 +432,36 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
         }
         p->n_bnd = (int32_t)p->bnd_local.size();
 
-        // CSR of P_in^T by a stable counting sort on the owned column
-        p->t_rowptr.assign(n_owned + 1, 0);
+        // CSR of P_m^T by a stable counting sort on the local column: row c
+        // lists the owned rows i with an entry in column c, i ascending.  Its
+        // first n_own rows are P_in^T.
+        const int64_t n_loc = n_owned + n_halo;
+        p->t_rowptr.assign(n_loc + 1, 0);
         for (int64_t k = 0; k < nnz; ++k)
-            if (p->col[k] < n_owned)
-                p->t_rowptr[p->col[k] + 1] += 1;
-        for (int64_t c = 0; c < n_owned; ++c)
+            p->t_rowptr[p->col[k] + 1] += 1;
+        for (int64_t c = 0; c < n_loc; ++c)
             p->t_rowptr[c + 1] += p->t_rowptr[c];
         p->nnz_in = p->t_rowptr[n_owned];
-        p->t_src.resize(p->nnz_in);
-        p->t_val.resize(p->nnz_in);
+        p->t_src.resize(nnz);
+        p->t_val.resize(nnz);
         std::vector<int32_t> next(p->t_rowptr.begin(), p->t_rowptr.end() - 1);
         for (int32_t i = 0; i < (int32_t)n_owned; ++i)
             for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k) {
                 const int32_t c = p->col[k];
-                if (c < n_owned) {
-                    p->t_src[next[c]] = i;
-                    p->t_val[next[c]] = p->val[k];
-                    ++next[c];
-                }
+                p->t_src[next[c]] = i;
+                p->t_val[next[c]] = p->val[k];
+                ++next[c];
             }
 
         build_blocks(p->rowptr, p->n_own, p->blocks_f);
         build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
+        build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
         plan_layout(*p);
         p->pulled.assign(p->L, 0);
+        p->pull_gen.assign(p->L, 0);
         p->fwd_done.assign(p->L + 1, 0);
+        p->tf.assign(p->L + 1, 0);
+        p->fwd_gen.assign(p->L + 1, 0);
         p->act.assign(p->L + 1, DIGEST_ACT_RELU);
     } catch (const std::bad_alloc &) {
         delete p;
@@ -455,6 +530,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.owned_gid, p->owned_gid.data(), sizeof(int32_t) * p->owned_gid.size()},
         {l.blocks_f, p->blocks_f.data(), sizeof(SpmmBlock) * p->blocks_f.size()},
         {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
+        {l.blocks_tf, p->blocks_tf.data(), sizeof(SpmmBlock) * p->blocks_tf.size()},
     };
     for (const Up &u : ups) {
         if (!u.bytes)
@@ -466,6 +542,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
     }
     p->ws = ws;
     std::fill(p->pulled.begin(), p->pulled.end(), 0);
+    std::fill(p->pull_gen.begin(), p->pull_gen.end(), 0);
     std::fill(p->fwd_done.begin(), p->fwd_done.end(), 0);
     return DIGEST_OK;
 }
@@ -491,12 +568,12 @@ digest_status digest_partition_export_transpose(const digest_partition *p, int64
     if (!p)
         return fail(DIGEST_EINVAL, "NULL partition handle");
     if (t_indptr)
-        for (size_t c = 0; c < p->t_rowptr.size(); ++c)
+        for (int64_t c = 0; c <= p->n_own; ++c)
             t_indptr[c] = p->t_rowptr[c];
     if (t_src)
-        std::copy(p->t_src.begin(), p->t_src.end(), t_src);
+        std::copy(p->t_src.begin(), p->t_src.begin() + p->nnz_in, t_src);
     if (t_vals)
-        std::copy(p->t_val.begin(), p->t_val.end(), t_vals);
+        std::copy(p->t_val.begin(), p->t_val.begin() + p->nnz_in, t_vals);
     return DIGEST_OK;
 }
 
@@ -536,6 +613,7 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
             return st;
     }
     p->pulled[level] = 1;
+    p->pull_gen[level] += 1;
     return DIGEST_OK;
 }
 
@@ -578,52 +656,193 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         return fail(DIGEST_ESTATE, "level %d was never pulled", layer - 1);
     hipStream_t s = (hipStream_t)hip_stream;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    float *ah = p->at<float>(p->lay.ah[layer]);
-    if (p->n_own > 0) {
-        digest_status st = run_spmm(p, false, h_in,
-                                    p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1])
-                                                  : nullptr,
-                                    d_in, ah, s);
-        if (st)
+    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    const bool tf = act == DIGEST_ACT_IDENTITY && narrow_layer(d_in, d_out);
+    if (p->n_own > 0 && tf) {
+        // T = [h_in; halo] W over all local rows, then h_out = P_m T.
+        float *T = p->at<float>(p->lay.tbuf);
+        {
+            Timed t(p, K_GEMM_FWD, s);
+            if (narrow_valu(d_in, d_out)) {
+                if (digest_status st = hip_check(
+                        digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
+                                                halo, d_in, w, T, d_out, false, s),
+                        "transform"))
+                    return st;
+            } else {
+                digest::GemmArgs g{};
+                g.N = d_out;
+                g.K = d_in;
+                g.lda = d_in;
+                g.B = w;
+                g.ldb = d_out;
+                g.ldc = d_out;
+                g.splits = 1;
+                g.kchunk = d_in;
+                g.M = p->n_own;
+                g.A = h_in;
+                g.C = T;
+                g.tile = gemm_tile_for(g.M, d_out, d_in, false);
+                if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
+                    return st;
+                if (p->n_halo > 0) {
+                    g.M = p->n_halo;
+                    g.tile = gemm_tile_for(g.M, d_out, d_in, false);
+                    g.A = halo;
+                    g.C = T + (int64_t)p->n_own * d_out;
+                    if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
+                        return st;
+                }
+            }
+        }
+        if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, d_out,
+                                        h_out, s))
             return st;
-        digest::GemmArgs g{};
-        g.M = p->n_own;
-        g.N = d_out;
-        g.K = d_in;
-        g.A = ah;
-        g.lda = d_in;
-        g.B = w;
-        g.ldb = d_out;
-        g.C = h_out;
-        g.ldc = d_out;
-        g.relu = act == DIGEST_ACT_RELU;
-        g.splits = 1;
-        g.kchunk = d_in;
+    } else if (p->n_own > 0) {
+        // AH = P_in h_in + P_out halo (kept for the backward), then act(AH W).
+        float *ah = p->at<float>(p->lay.ah[layer]);
+        if (digest_status st = run_spmm(p, Csr::Fwd, h_in, halo, p->n_own, d_in, ah, s))
+            return st;
         Timed t(p, K_GEMM_FWD, s);
-        st = hip_check(digest::launch_gemm(g, s), "forward gemm");
-        if (st)
-            return st;
+        if (narrow_valu(d_in, d_out)) {
+            if (digest_status st = hip_check(
+                    digest::launch_narrow_n(p->n_own, p->n_own, d_in, d_out, ah, nullptr, d_in, w,
+                                            h_out, d_out, act == DIGEST_ACT_RELU, s),
+                    "forward transform"))
+                return st;
+        } else {
+            digest::GemmArgs g{};
+            g.M = p->n_own;
+            g.N = d_out;
+            g.K = d_in;
+            g.A = ah;
+            g.lda = d_in;
+            g.B = w;
+            g.ldb = d_out;
+            g.C = h_out;
+            g.ldc = d_out;
+            g.relu = act == DIGEST_ACT_RELU;
+            g.splits = 1;
+            g.kchunk = d_in;
+            g.tile = gemm_tile_for(g.M, d_out, d_in, false);
+            if (digest_status st = hip_check(digest::launch_gemm(g, s), "forward gemm"))
+                return st;
+        }
     }
     p->fwd_done[layer] = 1;
     p->act[layer] = act;
+    p->tf[layer] = tf;
+    p->fwd_gen[layer] = p->pull_gen[layer - 1];
     return DIGEST_OK;
 }
 
-digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_out,
-                                    const float *dh_out, const float *w, float *dw,
-                                    float *dh_in, void *hip_stream)
+namespace {
+
+// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer, with
+// G = P_m^T D over all local rows (halo rows of G only feed dW).
+digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
+                                       const float *dh_out, const float *w, float *dw,
+                                       float *dh_in, hipStream_t s)
+{
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    float *G = p->at<float>(p->lay.tbuf);
+    float *gpart = p->at<float>(p->lay.gemm_part);
+    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, s))
+        return st;
+    const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
+    {
+        Timed tm(p, K_GEMM_DW, s);
+        if (t.valu) {
+            if (digest_status st = hip_check(
+                    digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
+                                             halo, d_in, G, t.chunk, t.slices, gpart, s),
+                    "dW narrow"))
+                return st;
+        } else {
+            digest::GemmArgs g{};
+            g.M = d_in;
+            g.N = d_out;
+            g.lda = d_in;
+            g.a_trans = true;
+            g.ldb = d_out;
+            g.ldc = d_out;
+            g.K = p->n_own;
+            g.A = h_in;
+            g.B = G;
+            g.splits = t.s_own;
+            g.kchunk = t.k_own;
+            g.tile = gemm_tile_for(d_in, d_out, g.K, true);
+            g.C = gpart;
+            if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
+                return st;
+            if (p->n_halo > 0) {
+                g.K = p->n_halo;
+                g.A = halo;
+                g.B = G + (int64_t)p->n_own * d_out;
+                g.splits = t.s_halo;
+                g.kchunk = t.k_halo;
+                g.tile = gemm_tile_for(d_in, d_out, g.K, true);
+                g.C = gpart + (int64_t)t.s_own * d_in * d_out;
+                if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
+                    return st;
+            }
+        }
+    }
+    {
+        Timed tm(p, K_REDUCE_DW, s);
+        if (digest_status st = hip_check(
+                digest::launch_splitk_reduce(gpart, t.slices, (int64_t)d_in * d_out, dw, s),
+                "dW reduce"))
+            return st;
+    }
+    if (!dh_in)
+        return DIGEST_OK;
+    Timed tm(p, K_GEMM_DH, s);
+    if (narrow_valu(d_in, d_out))
+        return hip_check(
+            digest::launch_narrow_k(p->n_own, d_in, d_out, G, d_out, w, dh_in, d_in, s),
+            "dgrad narrow");
+    digest::GemmArgs h{};
+    h.M = p->n_own;
+    h.N = d_in;
+    h.K = d_out;
+    h.A = G;
+    h.lda = d_out;
+    h.B = w;
+    h.ldb = d_out;
+    h.b_trans = true;
+    h.C = dh_in;
+    h.ldc = d_in;
+    h.splits = 1;
+    h.kchunk = d_out;
+    h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
+    return hip_check(digest::launch_gemm(h, s), "dgrad gemm");
+}
+
+}  // namespace
+
+digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_in,
+                                    const float *h_out, const float *dh_out, const float *w,
+                                    float *dw, float *dh_in, void *hip_stream)
 {
     if (digest_status st = need_bound(p))
         return st;
     if (layer < 1 || layer > p->L)
         return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
-    if (!dw || !w || (p->n_own > 0 && (!h_out || !dh_out)))
-        return fail(DIGEST_EINVAL, "NULL h_out, dh_out, w or dw");
+    if (!dw || !w || (p->n_own > 0 && (!h_in || !h_out || !dh_out)))
+        return fail(DIGEST_EINVAL, "NULL h_in, h_out, dh_out, w or dw");
     if (!p->fwd_done[layer])
         return fail(DIGEST_ESTATE, "no forward of layer %d since the workspace was bound",
                     layer);
+    if (p->fwd_gen[layer] != p->pull_gen[layer - 1])
+        return fail(DIGEST_ESTATE,
+                    "level %d was pulled again between the forward and backward of layer %d",
+                    layer - 1, layer);
     hipStream_t s = (hipStream_t)hip_stream;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    if (p->tf[layer] && p->n_own > 0)
+        return backward_transform_first(p, layer, h_in, dh_out, w, dw, dh_in, s);
     const bool relu = p->act[layer] == DIGEST_ACT_RELU;
     const float *ah = p->at<float>(p->lay.ah[layer]);
 
@@ -639,6 +858,7 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     g.ldb = d_out;
     g.b_mask = relu ? h_out : nullptr;
     splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
+    g.tile = gemm_tile_for(d_in, d_out, p->n_own, true);
     float *gpart = p->at<float>(p->lay.gemm_part);
     g.C = g.splits > 1 ? gpart : dw;
     g.ldc = d_out;
@@ -668,9 +888,10 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     h.ldc = d_in;
     h.splits = 1;
     h.kchunk = d_out;
+    h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
     if (!relu && d_out < d_in) {
-        // Narrow output: aggregate D first (width d_out), then (P_in^T D) W^T.
-        if (digest_status st = run_spmm(p, true, dh_out, nullptr, d_out, tmp, s))
+        // Narrower output: aggregate D first (width d_out), then (P_in^T D) W^T.
+        if (digest_status st = run_spmm(p, Csr::InT, dh_out, nullptr, p->n_own, d_out, tmp, s))
             return st;
         h.A = tmp;
         h.lda = d_out;
@@ -688,7 +909,7 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
         if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
             return st;
     }
-    return run_spmm(p, true, tmp, nullptr, d_in, dh_in, s);
+    return run_spmm(p, Csr::InT, tmp, nullptr, p->n_own, d_in, dh_in, s);
 }
 
 digest_status digest_softmax_xent(digest_partition *p, const float *logits,

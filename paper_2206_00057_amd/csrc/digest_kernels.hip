@@ -20,6 +20,8 @@
 //   k_softmax_xent / k_loss_reduce  the mean cross-entropy loss head.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace digest {
@@ -325,13 +327,15 @@ struct Quad {
     }
 };
 
-// 64x64 tile of C per workgroup; 4 waves in a 2x2 arrangement, each owning a
-// 32x32 block accumulated with v_mfma_f32_32x32x2f32.  K advances 32 at a
-// time through two LDS buffers ([k][m] and [k][n], so that the fragment read
-// of lane l -- row l%32 at k = l/32 -- is contiguous); the two following K
-// tiles are in flight in registers while the current one is multiplied (16
-// MFMAs per wave); one barrier per K step.
-template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
+// BM x BN tile of C per workgroup; 4 waves in a 2x2 arrangement, each owning
+// (BM/2) x (BN/2) as TM x TN blocks of 32x32 accumulated with
+// v_mfma_f32_32x32x2f32 (the A fragment of a k step is shared by the TN
+// blocks of a row, the B fragment by the TM blocks of a column).  K advances
+// BK = 32 at a time through two LDS buffers ([k][m] and [k][n], so that the
+// fragment read of lane l -- row l%32 at k = l/32 -- is contiguous); the two
+// following K tiles are in flight in registers while the current one is
+// multiplied; one barrier per K step.
+template <int BM, int BN, bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
 __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, int32_t kchunk,
                                               const float *__restrict__ A, int32_t lda,
                                               const float *__restrict__ Am,
@@ -340,10 +344,13 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
                                               float *__restrict__ C, int32_t ldc,
                                               int64_t c_split_stride)
 {
-    constexpr int BM = kGemmBM, BN = kGemmBN, BK = kGemmBK;
+    constexpr int BK = kGemmBK;
+    constexpr int TM = BM / 64, TN = BN / 64;     // 32x32 blocks per wave
+    constexpr int QA = BM * BK / 4 / 256;         // operand quads per thread
+    constexpr int QB = BN * BK / 4 / 256;
     constexpr int PA = AT ? 4 : 1;   // [k][m] rows written as float4 when m is contiguous
     constexpr int PB = BT ? 1 : 4;
-    static_assert(BM == 64 && BN == 64 && BK == 32, "tile shape assumed below");
+    static_assert(BK == 32 && (BM == 64 || BM == 128) && (BN == 64 || BN == 128), "tile");
     __shared__ float As[2][BK][BM + PA];
     __shared__ float Bs[2][BK][BN + PB];
 
@@ -354,24 +361,25 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     const int n0 = blockIdx.y * BN;
     const int kb = blockIdx.z * kchunk;
     const int ke = min(K, kb + kchunk);
-    const int wm = (wid >> 1) * 32;
-    const int wn = (wid & 1) * 32;
+    const int wm = (wid >> 1) * (BM / 2);
+    const int wn = (wid & 1) * (BN / 2);
 
-    floatx16 acc;
+    floatx16 acc[TM][TN];
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-        acc[i] = 0.f;
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[i][j][e] = 0.f;
 
-    // Each thread moves two quads (4 consecutive elements) of each operand
-    // tile per K step: quad q = tid + 256*i.  Two register sets hold the next
-    // two K tiles, so every global load has two compute phases to land.
-    using QA = Quad<VA, AMASK>;
-    using QB = Quad<VB, BMASK>;
-    QA qa0[2], qa1[2];
-    QB qb0[2], qb1[2];
-    auto fetch = [&](int k0, QA (&qa)[2], QB (&qb)[2]) {
+    using QAt = Quad<VA, AMASK>;
+    using QBt = Quad<VB, BMASK>;
+    QAt qa0[QA], qa1[QA];
+    QBt qb0[QB], qb1[QB];
+    auto fetch = [&](int k0, QAt (&qa)[QA], QBt (&qb)[QB]) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < QA; ++i) {
             const int q = tid + 256 * i;
             if (AT) {   // A(m,k) = A[k*lda + m]; quad along m
                 const int k = q / (BM / 4), m = (q % (BM / 4)) * 4;
@@ -380,6 +388,10 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
                 const int m = q / (BK / 4), k = (q % (BK / 4)) * 4;
                 qa[i].load(A, Am, (int64_t)(m0 + m) * lda + (k0 + k), k0 + k, ke, m0 + m < M);
             }
+        }
+#pragma unroll
+        for (int i = 0; i < QB; ++i) {
+            const int q = tid + 256 * i;
             if (BT) {   // B(k,n) = B[n*ldb + k]; quad along k
                 const int n = q / (BK / 4), k = (q % (BK / 4)) * 4;
                 qb[i].load(B, Bm, (int64_t)(n0 + n) * ldb + (k0 + k), k0 + k, ke, n0 + n < N);
@@ -389,9 +401,9 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
             }
         }
     };
-    auto stash = [&](int buf, const QA (&qa)[2], const QB (&qb)[2]) {
+    auto stash = [&](int buf, const QAt (&qa)[QA], const QBt (&qb)[QB]) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < QA; ++i) {
             const int q = tid + 256 * i;
             if (AT) {
                 const int k = q / (BM / 4), m = (q % (BM / 4)) * 4;
@@ -403,6 +415,10 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
                 for (int j = 0; j < 4; ++j)
                     As[buf][k + j][m] = qa[i].get(j);
             }
+        }
+#pragma unroll
+        for (int i = 0; i < QB; ++i) {
+            const int q = tid + 256 * i;
             if (BT) {
                 const int n = q / (BK / 4), k = (q % (BK / 4)) * 4;
 #pragma unroll
@@ -418,16 +434,25 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     // All fragment reads of a K step are issued before its MFMAs, so LDS
     // latency is paid once per step instead of once per MFMA.
     auto compute = [&](int buf) {
-        float fa[BK / 2], fb[BK / 2];
+        float fa[BK / 2][TM], fb[BK / 2][TN];
 #pragma unroll
-        for (int s = 0; s < BK / 2; ++s) {
-            fa[s] = As[buf][2 * s + (lane >> 5)][wm + (lane & 31)];
-            fb[s] = Bs[buf][2 * s + (lane >> 5)][wn + (lane & 31)];
+        for (int st = 0; st < BK / 2; ++st) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[st][i] = As[buf][2 * st + (lane >> 5)][wm + 32 * i + (lane & 31)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                fb[st][j] = Bs[buf][2 * st + (lane >> 5)][wn + 32 * j + (lane & 31)];
         }
         __builtin_amdgcn_sched_barrier(0);   // keep every read ahead of the MFMAs
 #pragma unroll
-        for (int s = 0; s < BK / 2; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[s], fb[s], acc, 0, 0, 0);
+        for (int st = 0; st < BK / 2; ++st)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[st][i], fb[st][j],
+                                                                     acc[i][j], 0, 0, 0);
     };
 
     // Tile t sits in LDS buffer t % 2; tile t+1 is in flight in one register
@@ -454,21 +479,26 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     }
 
     float *Cz = C + (int64_t)blockIdx.z * c_split_stride;
-    const int cn = n0 + wn + (lane & 31);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int r = m0 + wm + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-        if (r < M && cn < N) {
-            float v = acc[i];
-            if (RELU)
-                v = fmaxf(v, 0.f);
-            Cz[(int64_t)r * ldc + cn] = v;
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int cn = n0 + wn + 32 * j + (lane & 31);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int r = m0 + wm + 32 * i + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+                if (r < M && cn < N) {
+                    float v = acc[i][j][e];
+                    if (RELU)
+                        v = fmaxf(v, 0.f);
+                    Cz[(int64_t)r * ldc + cn] = v;
+                }
+            }
         }
-    }
 }
 
-// out[e] = sum over z of part[z][e], z ascending; one element per thread,
-// eight slices in flight.
+// out[e] = sum over z of part[z][e], z ascending: one element per thread,
+// eight slices in flight (many elements, few slices).
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__ part,
                                                        int32_t splits, int64_t count,
                                                        float *__restrict__ out)
@@ -490,6 +520,245 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__
     for (; z < splits; ++z)
         acc += part[(int64_t)z * count + e];
     out[e] = acc;
+}
+
+// The same sum for few elements and many slices: a block takes 8 consecutive
+// elements; its 32 slice lanes per element sum the slices z = lane,
+// lane + 32, ... in order and the 32 partial sums are added in a fixed tree
+// in LDS.
+__global__ __launch_bounds__(256) void k_splitk_reduce_wide(const float *__restrict__ part,
+                                                            int32_t splits, int64_t count,
+                                                            float *__restrict__ out)
+{
+    constexpr int EPB = 8, SL = 32;   // elements per block, slice lanes
+    __shared__ float red[SL][EPB + 1];
+    const int el = threadIdx.x % EPB, sl = threadIdx.x / EPB;
+    const int64_t e = (int64_t)blockIdx.x * EPB + el;
+    float acc = 0.f;
+    if (e < count) {
+#pragma unroll 4
+        for (int z = sl; z < splits; z += SL)
+            acc += part[(int64_t)z * count + e];
+    }
+    red[sl][el] = acc;
+    __syncthreads();
+    for (int off = SL / 2; off > 0; off >>= 1) {
+        if (sl < off)
+            red[sl][el] += red[sl + off][el];
+        __syncthreads();
+    }
+    if (sl == 0 && e < count)
+        out[e] = red[0][el];
+}
+
+// ---------------------------------------------------------------------------
+// Narrow dense products (one side <= kNarrow = 16)
+// ---------------------------------------------------------------------------
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Fill an LDS array of `count` floats, value(i) for i < count, with the
+// block's threads: loads are issued in batches of 16 per thread before their
+// stores, so staging costs one round trip per batch rather than per element.
+template <class F>
+__device__ __forceinline__ void stage_lds(float *dst, int count, F value)
+{
+    constexpr int BATCH = 16;
+    const int stride = blockDim.x;
+    for (int base = threadIdx.x; base < count; base += BATCH * stride) {
+        float v[BATCH];
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            const int i = base + b * stride;
+            v[b] = i < count ? value(i) : 0.f;
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            const int i = base + b * stride;
+            if (i < count)
+                dst[i] = v[b];
+        }
+    }
+}
+
+// C[r][n] = sum_k A(r)[k] B[k][n] for n < N <= 16, on v_mfma_f32_16x16x4f32.
+// Row r of A is row r of A0 (r < m0) or row r - m0 of A1 (leading dim lda).
+// B is staged once per block in LDS (zero-padded to 16 columns); a wave owns
+// 16 rows.  The contraction order is permuted so that a lane feeds its own
+// 16-byte load: in MFMA step (j, v) lane group h = lane/16 contributes
+// k = 16 j + 4 h + v for row lane%16 (A) and column lane%16 (B), and every k
+// is covered once.  All A loads of a K chunk are issued before its MFMAs.
+template <bool VEC>
+__global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N,
+                                                  const float *__restrict__ A0,
+                                                  const float *__restrict__ A1, int32_t lda,
+                                                  const float *__restrict__ B,
+                                                  float *__restrict__ C, int32_t ldc, bool relu)
+{
+    constexpr int KC = 256;          // k per chunk
+    constexpr int J = KC / 16;       // 16-k steps per chunk
+    extern __shared__ float Bs[];    // [K][16]
+    stage_lds(Bs, K * 16, [&](int i) {
+        const int k = i >> 4, n = i & 15;
+        return n < N ? B[k * N + n] : 0.f;
+    });
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
+    const int row0 = (blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * 16;
+    if (row0 >= M)
+        return;   // uniform per wave (after the barrier)
+    const int m = lane & 15, h = lane >> 4;
+    const int r = row0 + m;
+    const bool row_ok = r < M;
+    const float *a = !row_ok ? A0 : (r < m0 ? A0 + (int64_t)r * lda : A1 + (int64_t)(r - m0) * lda);
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int kc = 0; kc < K; kc += KC) {
+        float av[J][4];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int k = kc + 16 * j + 4 * h;
+            if (VEC) {
+                const bool ok = row_ok && k < K;   // K % 4 == 0: quads are all in or all out
+                const float4 q = *reinterpret_cast<const float4 *>(ok ? a + k : A0);
+                av[j][0] = ok ? q.x : 0.f;
+                av[j][1] = ok ? q.y : 0.f;
+                av[j][2] = ok ? q.z : 0.f;
+                av[j][3] = ok ? q.w : 0.f;
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const bool ok = row_ok && k + v < K;
+                    const float q = *(ok ? a + k + v : A0);
+                    av[j][v] = ok ? q : 0.f;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int k = kc + 16 * j + 4 * h + v;
+                const float b = k < K ? Bs[k * 16 + m] : 0.f;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j][v], b, acc, 0, 0, 0);
+            }
+    }
+    // lane holds C[row0 + 4h + i][m] for i < 4
+    if (m < N) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int rr = row0 + 4 * h + i;
+            if (rr < M)
+                C[(int64_t)rr * ldc + m] = relu ? fmaxf(acc[i], 0.f) : acc[i];
+        }
+    }
+}
+
+// C[r][n] = sum_{k < K} A[r][k] W[n][k] (W row-major [N][K], i.e. A W^T) for
+// K <= KK.  W is staged once per block in LDS as [k][n4] (16-byte reads,
+// neighbouring threads on neighbouring addresses); blocks then stride over
+// the rows, each thread producing four consecutive columns of a row.
+template <int KK>
+__global__ __launch_bounds__(256) void k_narrow_k(int32_t M, int32_t N, int32_t K,
+                                                  const float *__restrict__ A, int32_t lda,
+                                                  const float *__restrict__ W,
+                                                  float *__restrict__ C, int32_t ldc, bool vec_out)
+{
+    extern __shared__ float Ws[];   // [KK][N4], N4 = N rounded up to 4
+    const int N4 = (N + 3) & ~3;
+    stage_lds(Ws, KK * N4, [&](int i) {
+        const int k = i / N4, n = i % N4;
+        return (k < K && n < N) ? W[(int64_t)n * K + k] : 0.f;
+    });
+    __syncthreads();
+    const uint32_t nq = (uint32_t)N4 / 4;
+    const uint32_t total = (uint32_t)M * nq;   // < 2^31, checked by the launcher
+    for (uint32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += gridDim.x * blockDim.x) {
+        const int64_t r = t / nq;
+        const int n0 = (int)(t % nq) * 4;
+        float s[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < KK; ++k) {
+            if (k < K) {
+                const float a = A[r * lda + k];
+                const float4 w = *reinterpret_cast<const float4 *>(Ws + k * N4 + n0);
+                s[0] = fmaf(a, w.x, s[0]);
+                s[1] = fmaf(a, w.y, s[1]);
+                s[2] = fmaf(a, w.z, s[2]);
+                s[3] = fmaf(a, w.w, s[3]);
+            }
+        }
+        if (vec_out) {
+            *reinterpret_cast<float4 *>(C + r * ldc + n0) = make_float4(s[0], s[1], s[2], s[3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (n0 + j < N)
+                    C[r * ldc + n0 + j] = s[j];
+        }
+    }
+}
+
+// Split-K partial of dW = H^T G for N <= 16, on v_mfma_f32_16x16x4f32:
+//   part[z][f][n] = sum over the rows r of slice z of H(r)[f] G[r][n],
+// row r of H from H0 (r < m0) or H1 (leading dim ldh); G row-major [R][N].
+// A wave owns 64 features (four 16-feature MFMA blocks sharing every G
+// load) and one slice of rows; in MFMA step s lane group h contributes row
+// rb + 4 s + h.  The 4 waves of a block take 4 consecutive slices.
+__global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N,
+                                                   const float *__restrict__ H0,
+                                                   const float *__restrict__ H1, int32_t ldh,
+                                                   const float *__restrict__ G, int32_t chunk,
+                                                   int32_t splits, float *__restrict__ part)
+{
+    constexpr int SB = 8;   // MFMA steps (32 rows) per batch of loads
+    const int lane = threadIdx.x & (kWave - 1);
+    const int z = blockIdx.y * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (z >= splits)
+        return;   // uniform per wave
+    const int f0 = blockIdx.x * 64;
+    const int rb = z * chunk;
+    const int re = min(R, rb + chunk);
+    const int m = lane & 15, h = lane >> 4;
+    floatx4 acc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int r0 = rb; r0 < re; r0 += 4 * SB) {
+        float av[SB][4], bv[SB];
+#pragma unroll
+        for (int s = 0; s < SB; ++s) {
+            const int r = r0 + 4 * s + h;
+            const bool ok = r < re;
+            const float *hp = r < m0 ? H0 + (int64_t)r * ldh : H1 + (int64_t)(r - m0) * ldh;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int f = f0 + 16 * q + m;
+                const bool okf = ok && f < F;
+                const float v = *(okf ? hp + f : H0);
+                av[s][q] = okf ? v : 0.f;
+            }
+            const bool okg = ok && m < N;
+            const float g = *(okg ? G + (int64_t)r * N + m : G);
+            bv[s] = okg ? g : 0.f;
+        }
+#pragma unroll
+        for (int s = 0; s < SB; ++s)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][q], bv[s], acc[q], 0, 0, 0);
+    }
+    // acc[q] lane holds D[f0 + 16 q + 4 h + i][m]
+    if (m < N) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int f = f0 + 16 * q + 4 * h + i;
+                if (f < F)
+                    part[((int64_t)z * F + f) * N + m] = acc[q][i];
+            }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -669,16 +938,27 @@ hipError_t spmm_v(int vec, int gl, int nch, const SpmmBlock *blocks, int32_t n_b
     }
 }
 
-template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
+template <int BM, int BN, bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
 hipError_t gemm_t(const GemmArgs &a, hipStream_t s)
 {
-    const dim3 grid((unsigned)((a.M + kGemmBM - 1) / kGemmBM),
-                    (unsigned)((a.N + kGemmBN - 1) / kGemmBN), (unsigned)a.splits);
+    const dim3 grid((unsigned)((a.M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN),
+                    (unsigned)a.splits);
     const int64_t split_stride = a.splits > 1 ? (int64_t)a.M * a.ldc : 0;
-    hipLaunchKernelGGL((k_gemm<AT, BT, AMASK, BMASK, RELU, VA, VB>), grid, dim3(256), 0, s, a.M,
-                       a.N, a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb, a.b_mask, a.C,
-                       a.ldc, split_stride);
+    hipLaunchKernelGGL((k_gemm<BM, BN, AT, BT, AMASK, BMASK, RELU, VA, VB>), grid, dim3(256), 0,
+                       s, a.M, a.N, a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb, a.b_mask,
+                       a.C, a.ldc, split_stride);
     return hipGetLastError();
+}
+
+template <bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
+hipError_t gemm_tile(const GemmArgs &a, hipStream_t s)
+{
+    switch (a.tile) {
+    case 1: return gemm_t<64, 128, AT, BT, AMASK, BMASK, RELU, VA, VB>(a, s);
+    case 2: return gemm_t<128, 64, AT, BT, AMASK, BMASK, RELU, VA, VB>(a, s);
+    case 3: return gemm_t<128, 128, AT, BT, AMASK, BMASK, RELU, VA, VB>(a, s);
+    default: return gemm_t<64, 64, AT, BT, AMASK, BMASK, RELU, VA, VB>(a, s);
+    }
 }
 
 // 16-byte operand loads need a 16-byte aligned base (and mask) and a leading
@@ -694,12 +974,12 @@ hipError_t gemm_q(const GemmArgs &a, hipStream_t s)
 {
     const bool va = quad_ok(a.A, a.a_mask, a.lda), vb = quad_ok(a.B, a.b_mask, a.ldb);
     if (va && vb)
-        return gemm_t<AT, BT, AMASK, BMASK, RELU, true, true>(a, s);
+        return gemm_tile<AT, BT, AMASK, BMASK, RELU, true, true>(a, s);
     if (va)
-        return gemm_t<AT, BT, AMASK, BMASK, RELU, true, false>(a, s);
+        return gemm_tile<AT, BT, AMASK, BMASK, RELU, true, false>(a, s);
     if (vb)
-        return gemm_t<AT, BT, AMASK, BMASK, RELU, false, true>(a, s);
-    return gemm_t<AT, BT, AMASK, BMASK, RELU, false, false>(a, s);
+        return gemm_tile<AT, BT, AMASK, BMASK, RELU, false, true>(a, s);
+    return gemm_tile<AT, BT, AMASK, BMASK, RELU, false, false>(a, s);
 }
 
 }  // namespace
@@ -743,6 +1023,8 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
 {
     if (a.M <= 0 || a.N <= 0)
         return hipSuccess;
+    if (a.tile < 0 || a.tile > 3)
+        return hipErrorInvalidValue;
     if (a.splits > 1 && a.kchunk % kGemmBK != 0)
         return hipErrorInvalidValue;   // split starts must stay quad aligned
     const bool am = a.a_mask != nullptr, bm = a.b_mask != nullptr;
@@ -767,9 +1049,15 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
 {
     if (count <= 0)
         return hipSuccess;
-    const int64_t blocks = (count + 255) / 256;
-    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0, s, part, splits,
-                       count, out);
+    if (splits >= 64 && count < 64 * 1024) {
+        const int64_t blocks = (count + 7) / 8;
+        hipLaunchKernelGGL(k_splitk_reduce_wide, dim3((unsigned)blocks), dim3(256), 0, s, part,
+                           splits, count, out);
+    } else {
+        const int64_t blocks = (count + 255) / 256;
+        hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)blocks), dim3(256), 0, s, part, splits,
+                           count, out);
+    }
     return hipGetLastError();
 }
 
@@ -792,6 +1080,67 @@ hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32
             return e;
     }
     hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, s, block_loss, nb, inv_n, loss);
+    return hipGetLastError();
+}
+
+
+hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
+                           const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
+                           bool relu, hipStream_t s)
+{
+    if (M <= 0 || N <= 0)
+        return hipSuccess;
+    if (N > kNarrow || K <= 0 || (size_t)K * 16 * sizeof(float) > 64 * 1024)
+        return hipErrorInvalidValue;
+    const bool v4 = K % 4 == 0 && lda % 4 == 0 && ((uintptr_t)A0 % 16) == 0 &&
+                    (A1 == nullptr || ((uintptr_t)A1 % 16) == 0);
+    const int64_t waves = ((int64_t)M + 15) / 16;
+    const int64_t blocks = (waves + 3) / 4;
+    const size_t lds = sizeof(float) * (size_t)K * 16;
+    if (v4)
+        hipLaunchKernelGGL((k_narrow_n<true>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0,
+                           K, N, A0, A1, lda, B, C, ldc, relu);
+    else
+        hipLaunchKernelGGL((k_narrow_n<false>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0,
+                           K, N, A0, A1, lda, B, C, ldc, relu);
+    return hipGetLastError();
+}
+
+hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
+                           const float *W, float *C, int32_t ldc, hipStream_t s)
+{
+    if (M <= 0 || N <= 0)
+        return hipSuccess;
+    const int n4 = (N + 3) & ~3;
+    if (K <= 0 || K > kNarrow || (size_t)n4 * kNarrow * sizeof(float) > 64 * 1024)
+        return hipErrorInvalidValue;
+    const int64_t threads = (int64_t)M * (n4 / 4);
+    if (threads >= INT32_MAX)
+        return hipErrorInvalidValue;
+    const int64_t blocks = std::min<int64_t>((threads + 255) / 256, 2048);
+    const bool vec_out = N % 4 == 0 && ldc % 4 == 0 && ((uintptr_t)C % 16) == 0;
+    const int kk = K <= 8 ? 8 : 16;
+    const size_t lds = sizeof(float) * (size_t)n4 * kk;
+    if (kk == 8)
+        hipLaunchKernelGGL((k_narrow_k<8>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K, A,
+                           lda, W, C, ldc, vec_out);
+    else
+        hipLaunchKernelGGL((k_narrow_k<16>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K,
+                           A, lda, W, C, ldc, vec_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
+                            const float *H1, int32_t ldh, const float *G, int32_t chunk,
+                            int32_t splits, float *part, hipStream_t s)
+{
+    if (F <= 0 || N <= 0)
+        return hipSuccess;
+    if (N > kNarrow || splits < 1 || chunk < 1)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((F + 63) / 64), (unsigned)((splits + 3) / 4));
+    hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, G, chunk,
+                       splits, part);
     return hipGetLastError();
 }
 

@@ -54,6 +54,7 @@ struct GemmArgs {
     bool relu;
     int32_t splits;
     int32_t kchunk;
+    int32_t tile = 0;   // workgroup tile of C: 0 = 64x64, 1 = 64x128, 2 = 128x64, 3 = 128x128
 };
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
@@ -62,13 +63,34 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count, float *out,
                                 hipStream_t s);
 
+// Narrow dense products (VALU) for one side at most kNarrow wide.
+constexpr int kNarrow = 16;
+
+// C[r][n] = sum_k A(r)[k] B[k][n], n < N <= kNarrow, B row-major [K][N];
+// A(r) is row r of A0 for r < m0, else row r - m0 of A1 (leading dim lda);
+// relu: epilogue max(x, 0).
+hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
+                           const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
+                           bool relu, hipStream_t s);
+
+// C[r][n] = sum_{k < K} A[r][k] W[n][k] with K <= kNarrow, W row-major [N][K].
+hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
+                           const float *W, float *C, int32_t ldc, hipStream_t s);
+
+// part[z][f][n] = sum over rows r in [z*chunk, (z+1)*chunk) of H(r)[f] G[r][n]
+// (f < F, n < N <= kNarrow; H(r) from H0 for r < m0 else H1, leading dim
+// ldh; G row-major [R][N]).  Sum the slices with launch_splitk_reduce.
+hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
+                            const float *H1, int32_t ldh, const float *G, int32_t chunk,
+                            int32_t splits, float *part, hipStream_t s);
+
 // Row-wise softmax cross entropy; block_loss needs softmax_xent_blocks(n) floats.
 int32_t softmax_xent_blocks(int32_t n);
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
                                int32_t C, float *dlogits, float *block_loss, float *loss,
                                hipStream_t s);
 
-// GEMM tile sizes (rows of C per workgroup, cols of C per workgroup, K step).
+// GEMM K step; the smallest workgroup tile of C is kGemmBM x kGemmBN.
 constexpr int kGemmBM = 64;
 constexpr int kGemmBN = 64;
 constexpr int kGemmBK = 32;

@@ -51,7 +51,7 @@ def lib():
             "digest_pull": ([P, i32, P, P], st),
             "digest_push": ([P, i32, P, P, i32, P], st),
             "digest_layer_forward": ([P, i32, P, P, P, i32, P], st),
-            "digest_layer_backward": ([P, i32, P, P, P, P, P, P], st),
+            "digest_layer_backward": ([P, i32, P, P, P, P, P, P, P], st),
             "digest_softmax_xent": ([P, P, P, P, P, P], st),
             "digest_sync_period": ([i32, i64, P, P], st),
             "digest_profile_enable": ([P, i32], st),
@@ -234,16 +234,17 @@ def digest_layer_forward(p, layer, h_in, w, h_out, act, stream=None):
     _check(lib().digest_layer_forward(p.handle, int(layer), a, b, c, int(act), _stream(stream)))
 
 
-def digest_layer_backward(p, layer, h_out, dh_out, w, dw, dh_in=None, stream=None):
+def digest_layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in=None, stream=None):
     import torch
     _check_layer(p, layer)
     di, do = p.widths[layer - 1], p.widths[layer]
+    x = _dev(h_in, torch.float32, p.n_own * di, "h_in")
     a = _dev(h_out, torch.float32, p.n_own * do, "h_out")
     b = _dev(dh_out, torch.float32, p.n_own * do, "dh_out")
     c = _dev(w, torch.float32, di * do, "w")
     e = _dev(dw, torch.float32, di * do, "dw")
     f = _dev(dh_in, torch.float32, p.n_own * di, "dh_in") if dh_in is not None else None
-    _check(lib().digest_layer_backward(p.handle, int(layer), a, b, c, e, f, _stream(stream)))
+    _check(lib().digest_layer_backward(p.handle, int(layer), x, a, b, c, e, f, _stream(stream)))
 
 
 def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):

@@ -49,6 +49,7 @@ class GpuPartition:
             D.digest_pull(self.p, lev, stores[lev])
 
     def forward(self, x_own, Ws, stores=None, do_pull=False, do_push=False):
+        self.x_own = x_own
         h = x_own
         for l in range(1, self.L + 1):
             if do_pull and l >= 2:
@@ -63,7 +64,9 @@ class GpuPartition:
         D.digest_softmax_xent(self.p, self.H[self.L], labels, self.dH[self.L], self.loss)
         for l in range(self.L, 0, -1):
             dh_in = self.dH[l - 1] if l > 1 else None
-            D.digest_layer_backward(self.p, l, self.H[l], self.dH[l], Ws[l - 1], self.dW[l], dh_in)
+            h_in = self.H[l - 1] if l > 1 else self.x_own
+            D.digest_layer_backward(self.p, l, h_in, self.H[l], self.dH[l], Ws[l - 1], self.dW[l],
+                                    dh_in)
 
     def round(self, r, K, x_own, Ws, stores, labels):
         """Round r (1-based) with sync interval K, eagerly."""

@@ -118,7 +118,7 @@ def test_device_calls_without_workspace_fail_with_estate():
     assert L.digest_pull(h.handle, 0, fake, None) == D.ESTATE
     assert L.digest_push(h.handle, 1, fake, fake, 0, None) == D.ESTATE
     assert L.digest_layer_forward(h.handle, 1, fake, fake, fake, 0, None) == D.ESTATE
-    assert L.digest_layer_backward(h.handle, 1, fake, fake, fake, fake, None, None) == D.ESTATE
+    assert L.digest_layer_backward(h.handle, 1, fake, fake, fake, fake, fake, None, None) == D.ESTATE
     assert L.digest_softmax_xent(h.handle, fake, fake, fake, fake, None) == D.ESTATE
     assert L.digest_pull(None, 0, fake, None) == D.EINVAL
     assert b"workspace" in L.digest_last_error() or b"handle" in L.digest_last_error()

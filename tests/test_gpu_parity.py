@@ -139,7 +139,7 @@ def check_layer(c, layer, check_dh_in=True):
     dw = torch.empty(W.shape, device="cuda")
     want = check_dh_in and layer > 1
     dh_in = torch.empty(c.n, c.widths[layer - 1], device="cuda") if want else None
-    Dm.digest_layer_backward(c.h, layer, dev(ref_out), dev(dh), dev(W), dw, dh_in)
+    Dm.digest_layer_backward(c.h, layer, dev(h_in), dev(ref_out), dev(dh), dev(W), dw, dh_in)
     ref_dw, ref_dh_in = c.op.backward(layer, h_in, W, ref_out, dh, act, want_dh_in=want)
     assert_close(host(dw), ref_dw, f"{c.label} dW layer {layer}")
     if want:
@@ -222,7 +222,7 @@ def test_determinism_bitwise(tiny):
         out = torch.empty(tiny.n, tiny.widths[1], device="cuda")
         Dm.digest_layer_forward(tiny.h, 1, x, W, out, Dm.ACT_RELU)
         dw = torch.empty(W.shape, device="cuda")
-        Dm.digest_layer_backward(tiny.h, 1, out, dev(tiny.upstream(1)), W, dw, None)
+        Dm.digest_layer_backward(tiny.h, 1, x, out, dev(tiny.upstream(1)), W, dw, None)
         outs.append(host(out))
         dws.append(host(dw))
     assert_bits(outs[0], outs[1], "forward run twice")
@@ -275,7 +275,7 @@ def test_relu_narrowing_layer_uses_masked_dgrad():
     dh = c.upstream(1)
     dw = torch.empty(W.shape, device="cuda")
     dh_in = torch.empty(c.n, 48, device="cuda")
-    Dm.digest_layer_backward(c.h, 1, dev(ref_out), dev(dh), dev(W), dw, dh_in)
+    Dm.digest_layer_backward(c.h, 1, dev(h_in), dev(ref_out), dev(dh), dev(W), dw, dh_in)
     ref_dw, ref_dh = c.op.backward(1, h_in, W, ref_out, dh, oracle.RELU, want_dh_in=True)
     assert_close(host(dh_in), ref_dh, "relu-narrow dH_in")
 
@@ -303,7 +303,7 @@ def test_empty_partition():
     W = torch.ones(3, 2, device="cuda")
     Dm.digest_layer_forward(h, 1, e, W, out, Dm.ACT_IDENTITY)
     dw = torch.full((3, 2), 5.0, device="cuda")
-    Dm.digest_layer_backward(h, 1, out, out, W, dw, e)
+    Dm.digest_layer_backward(h, 1, e, out, out, W, dw, e)
     assert np.all(host(dw) == 0)
     loss = torch.full((1,), 3.0, device="cuda")
     Dm.digest_softmax_xent(h, out, torch.empty(0, dtype=torch.int32, device="cuda"), out, loss)
@@ -323,7 +323,17 @@ def test_state_errors_on_device():
         Dm.digest_layer_forward(c.h, 2, x, W, out, Dm.ACT_IDENTITY)
     assert e.value.status == Dm.ESTATE
     with pytest.raises(Dm.DigestError) as e:       # no forward of layer 2 yet
-        Dm.digest_layer_backward(c.h, 2, out, out, W, torch.empty(64, 16, device="cuda"), None)
+        Dm.digest_layer_backward(c.h, 2, x, out, out, W, torch.empty(64, 16, device="cuda"), None)
+    assert e.value.status == Dm.ESTATE
+    # a pull of level 1 between the forward and the backward of layer 2
+    store1 = torch.zeros(g.n, 64, device="cuda")
+    Dm.digest_pull(c.h, 1, store1)
+    Dm.digest_layer_forward(c.h, 2, x, W, out, Dm.ACT_IDENTITY)
+    dw = torch.empty(64, 16, device="cuda")
+    Dm.digest_layer_backward(c.h, 2, x, out, out, W, dw, None)   # fine
+    Dm.digest_pull(c.h, 1, store1)
+    with pytest.raises(Dm.DigestError) as e:
+        Dm.digest_layer_backward(c.h, 2, x, out, out, W, dw, None)
     assert e.value.status == Dm.ESTATE
     with pytest.raises(Dm.DigestError) as e:       # push of level 0 is not a stale level
         Dm.digest_push(c.h, 0, x, torch.zeros(g.n, 64, device="cuda"))
