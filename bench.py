@@ -55,57 +55,70 @@ def tf_slices(n, nh, di, do):
     return splitk(di, do, n)[0] + (splitk(di, do, nh)[0] if nh else 0)
 
 
-def round_model(st, widths):
-    """Algorithmic bytes / flops per round for each kernel kind.
+def launch_model(st, widths):
+    """Algorithmic bytes and flops of one launch of each (kernel kind, layer).
 
-    Returns {kind: (bytes, flops, launches)} for the kinds that run every
-    round, and per-launch bytes for pull/push (their launches depend on the
-    schedule).  The layer order (aggregate-first or transform-first) follows
-    the library's rule.
+    Keys follow the library's instrumentation: "kind.lN" with N the layer
+    (the level for pull/push, L for the loss head).  The layer order
+    (aggregate-first or transform-first) follows the library's rule.
     """
     n, nh, nnz, nnz_in, nb = st["n_own"], st["n_halo"], st["nnz"], st["nnz_in"], st["n_boundary"]
     L = len(widths) - 1
-    m = {k: [0.0, 0.0, 0] for k in ("spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
-                                      "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed",
-                                      "softmax_xent")}
+    m = {}
 
-    def add(k, b, f=0.0):
-        m[k][0] += b
-        m[k][1] += f
-        m[k][2] += 1
+    def put(kind, l, b, f=0.0):
+        m[f"{kind}.l{l}"] = (float(b), float(f))
 
     for l in range(1, L + 1):
         di, do = widths[l - 1], widths[l]
         relu = l < L
         if transform_first(l, widths):
             R = n + nh
-            add("gemm_fwd_relu", 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
-            add("spmm_fwd", 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)
-            add("spmm_bwd_transposed", 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do)
-            add("gemm_dw_splitk", 4 * (R * di + R * do), 2.0 * R * di * do)
-            add("splitk_reduce_dw", 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
+            put("gemm_fwd_relu", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
+            put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)
+            put("spmm_bwd_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do)
+            put("gemm_dw_splitk", l, 4 * (R * di + R * do), 2.0 * R * di * do)
+            put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
             if l > 1:
-                add("gemm_dgrad", 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
+                put("gemm_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
             continue
-        add("spmm_fwd", 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)
-        add("gemm_fwd_relu", 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
-        add("gemm_dw_splitk", 4 * (n * di + n * do * (2 if relu else 1) + di * do),
+        put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)
+        put("gemm_fwd_relu", l, 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
+        put("gemm_dw_splitk", l, 4 * (n * di + n * do * (2 if relu else 1) + di * do),
             2.0 * n * di * do)
         s = splitk(di, do, n)[0]
         if s > 1:
-            add("splitk_reduce_dw", 4 * (s + 1) * di * do)
+            put("splitk_reduce_dw", l, 4 * (s + 1) * di * do)
         if l > 1:
             narrow = (not relu) and do < di
             w = do if narrow else di
-            add("spmm_bwd_transposed", 4 * (n + 1) + 8 * nnz_in + 8 * n * w)
-            add("gemm_dgrad", 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
+            put("spmm_bwd_transposed", l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w)
+            put("gemm_dgrad", l, 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
                 2.0 * n * di * do)
-    add("softmax_xent", 4 * (2 * n * widths[-1] + n))
-    per_launch = {
-        "pull_gather": {l: 8.0 * nh * widths[l] + 4 * nh for l in range(L)},
-        "push_scatter": {l: 8.0 * nb * widths[l] + 8 * nb for l in range(1, L)},
-    }
-    return {k: tuple(v) for k, v in m.items()}, per_launch
+    put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
+    for lev in range(L):
+        put("pull_gather", lev, 8.0 * nh * widths[lev] + 4 * nh)
+    for lev in range(1, L):
+        put("push_scatter", lev, 8.0 * nb * widths[lev] + 8 * nb)
+    return m
+
+
+def measured_traffic(workload, key):
+    """HBM bytes per launch of `key` from the committed counter summary, or
+    None when there is none for this kernel or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        line = line.split("#", 1)[0].strip()
+        if "=" in line:
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    from paper_2206_00057_amd.pmc import kernel_source_hash
+    if kv.get("kernel") != key or kv.get("source_sha") != kernel_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
@@ -153,6 +166,9 @@ def main():
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graph replay")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="before the rounds, copy a float32 buffer of this many MiB once "
+                         "(a plain copy kernel of known size for counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one partition on one GPU; runs on more than one GPU are not "
@@ -186,6 +202,14 @@ def main():
     gp = step.GpuPartition(g.n, part, cfg.widths)
     x_own = dev(X[part.owned])
     gp.pull_all(stores)
+    if args.calibration_copy_mib:
+        n_cal = args.calibration_copy_mib * (1 << 20) // 4
+        src_cal = torch.ones(n_cal, device="cuda")
+        dst_cal = torch.empty_like(src_cal)
+        torch.cuda.synchronize()
+        dst_cal.copy_(src_cal)
+        torch.cuda.synchronize()
+        del src_cal, dst_cal
 
     def run(r):
         if args.eager:
@@ -216,32 +240,28 @@ def main():
         gp.round(r, K, x_own, dWs, stores, dy)
     prof = D.digest_profile_read(gp.p)
     D.digest_profile_enable(gp.p, False)
-    model, per_launch = round_model(st, cfg.widths)
+    model = launch_model(st, cfg.widths)
     kernels = {}
-    for kind, (tot_ms, n_l) in prof.items():
-        if n_l == 0:
-            continue
+    for key, (tot_ms, n_l) in prof.items():
         entry = {"launches": n_l, "avg_us": 1e3 * tot_ms / n_l, "total_ms": tot_ms}
-        if kind in model:
-            b, f, per_round = model[kind]
-            b_tot, f_tot = b * args.steps, f * args.steps
-            entry["gbs"] = b_tot / (tot_ms * 1e-3) / 1e9
+        if key in model:
+            b, f = model[key]
+            entry["gbs"] = b / (entry["avg_us"] * 1e-6) / 1e9
             if f:
-                entry["tflops"] = f_tot / (tot_ms * 1e-3) / 1e12
-        elif kind in per_launch:
-            # launches follow the schedule; bytes of one launch averaged over the levels used
-            levels = list(per_launch[kind].values())
-            entry["gbs"] = np.mean(levels) * n_l / (tot_ms * 1e-3) / 1e9
-        kernels[kind] = entry
+                entry["tflops"] = f / (entry["avg_us"] * 1e-6) / 1e12
+        kernels[key] = entry
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
     d = kernels[dom]
-    if "tflops" in d and model[dom][1] / max(model[dom][0], 1) > FP32_MFMA_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3:
+    b_l, f_l = model.get(dom, (0.0, 0.0))
+    if f_l and f_l / max(b_l, 1.0) > FP32_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": round(d["tflops"], 3), "peak": FP32_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4)}
     else:
         roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(d["gbs"] / HBM_PEAK_GBS, 4)}
-    roof.update({"kernel": dom, "avg_launch_us": round(d["avg_us"], 3), "traffic": None})
+    roof.update({"traffic": measured_traffic(cfg.name, dom), "kernel": dom,
+                 "algorithmic_bytes_per_launch": b_l, "algorithmic_flops_per_launch": f_l,
+                 "avg_launch_us": round(d["avg_us"], 3)})
 
     cpu = None
     if not args.no_cpu:

@@ -219,13 +219,15 @@ digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull,
 /*
  * Instrumentation: while enabled, every kernel the handle launches is
  * bracketed by HIP events on its own stream.  digest_profile_read
- * synchronises on those events and returns, per kernel kind, the summed
- * duration (ms) and launch count since the last read (then clears them).
- * Kernel kinds are numbered 0..digest_profile_kernel_count()-1.
+ * synchronises on those events and returns the summed duration (ms) and
+ * launch count of each (kernel kind, layer) since the last read, then
+ * clears them.  Both arrays hold digest_profile_kernel_count() * (L + 1)
+ * entries; entry kind * (L + 1) + slot, where slot is the layer (1..L) for
+ * the layer kernels, the level (0..L-1) for pull and push, and L for the
+ * loss head.  Kernel kinds are numbered 0..digest_profile_kernel_count()-1.
  */
 digest_status digest_profile_enable(digest_partition *p, int32_t on);
-digest_status digest_profile_read(digest_partition *p, double *total_ms /*[count]*/,
-                                  int64_t *launches /*[count]*/);
+digest_status digest_profile_read(digest_partition *p, double *total_ms, int64_t *launches);
 int32_t digest_profile_kernel_count(void);
 const char *digest_profile_kernel_name(int32_t kind);
 

@@ -146,7 +146,7 @@ struct digest_partition {
 
     bool prof = false;
     struct Rec {
-        int32_t kind;
+        int32_t kind, layer;
         hipEvent_t a, b;
     };
     std::vector<Rec> recs;
@@ -260,7 +260,7 @@ struct Timed {
     digest_partition *p;
     hipStream_t s;
     hipEvent_t b = nullptr;
-    Timed(digest_partition *p_, int32_t kind, hipStream_t s_) : p(p_), s(s_)
+    Timed(digest_partition *p_, int32_t kind, int32_t layer, hipStream_t s_) : p(p_), s(s_)
     {
         if (!p->prof)
             return;
@@ -285,7 +285,7 @@ struct Timed {
             return;
         }
         (void)hipEventRecord(a, s);
-        p->recs.push_back({kind, a, b});
+        p->recs.push_back({kind, layer, a, b});
     }
     ~Timed()
     {
@@ -315,12 +315,12 @@ digest_status need_bound(const digest_partition *p)
 enum class Csr { Fwd, InT, FullT };
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
-                       int32_t n_src0, int32_t d, float *out, hipStream_t s)
+                       int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s)
 {
     const bool fwd = which == Csr::Fwd;
     const auto &blocks = fwd ? p->blocks_f : (which == Csr::InT ? p->blocks_t : p->blocks_tf);
     const size_t boff = fwd ? p->lay.blocks_f : (which == Csr::InT ? p->lay.blocks_t : p->lay.blocks_tf);
-    Timed t(p, fwd ? K_SPMM_FWD : K_SPMM_BWD, s);
+    Timed t(p, fwd ? K_SPMM_FWD : K_SPMM_BWD, layer, s);
     return hip_check(
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks.size(),
                             p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr),
@@ -603,7 +603,7 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
         return fail(DIGEST_EINVAL, "store is NULL");
     hipStream_t s = (hipStream_t)hip_stream;
     if (p->n_halo > 0) {
-        Timed t(p, K_PULL, s);
+        Timed t(p, K_PULL, level, s);
         digest_status st = hip_check(
             digest::launch_copy_rows(p->at<int32_t>(p->lay.halo_gid), nullptr, p->n_halo,
                                      p->widths[level], store,
@@ -633,7 +633,7 @@ digest_status digest_push(digest_partition *p, int32_t level, const float *h_own
     const int32_t rows = all ? p->n_own : p->n_bnd;
     if (rows == 0)
         return DIGEST_OK;
-    Timed t(p, K_PUSH, s);
+    Timed t(p, K_PUSH, level, s);
     return hip_check(digest::launch_copy_rows(
                          all ? nullptr : p->at<int32_t>(p->lay.bnd_local),
                          p->at<int32_t>(all ? p->lay.owned_gid : p->lay.bnd_gid), rows,
@@ -662,7 +662,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         // T = [h_in; halo] W over all local rows, then h_out = P_m T.
         float *T = p->at<float>(p->lay.tbuf);
         {
-            Timed t(p, K_GEMM_FWD, s);
+            Timed t(p, K_GEMM_FWD, layer, s);
             if (narrow_valu(d_in, d_out)) {
                 if (digest_status st = hip_check(
                         digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
@@ -696,14 +696,14 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             }
         }
         if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, d_out,
-                                        h_out, s))
+                                        h_out, layer, s))
             return st;
     } else if (p->n_own > 0) {
         // AH = P_in h_in + P_out halo (kept for the backward), then act(AH W).
         float *ah = p->at<float>(p->lay.ah[layer]);
-        if (digest_status st = run_spmm(p, Csr::Fwd, h_in, halo, p->n_own, d_in, ah, s))
+        if (digest_status st = run_spmm(p, Csr::Fwd, h_in, halo, p->n_own, d_in, ah, layer, s))
             return st;
-        Timed t(p, K_GEMM_FWD, s);
+        Timed t(p, K_GEMM_FWD, layer, s);
         if (narrow_valu(d_in, d_out)) {
             if (digest_status st = hip_check(
                     digest::launch_narrow_n(p->n_own, p->n_own, d_in, d_out, ah, nullptr, d_in, w,
@@ -748,11 +748,11 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
     float *G = p->at<float>(p->lay.tbuf);
     float *gpart = p->at<float>(p->lay.gemm_part);
-    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, s))
+    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s))
         return st;
     const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
     {
-        Timed tm(p, K_GEMM_DW, s);
+        Timed tm(p, K_GEMM_DW, layer, s);
         if (t.valu) {
             if (digest_status st = hip_check(
                     digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
@@ -790,7 +790,7 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
         }
     }
     {
-        Timed tm(p, K_REDUCE_DW, s);
+        Timed tm(p, K_REDUCE_DW, layer, s);
         if (digest_status st = hip_check(
                 digest::launch_splitk_reduce(gpart, t.slices, (int64_t)d_in * d_out, dw, s),
                 "dW reduce"))
@@ -798,7 +798,7 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
     }
     if (!dh_in)
         return DIGEST_OK;
-    Timed tm(p, K_GEMM_DH, s);
+    Timed tm(p, K_GEMM_DH, layer, s);
     if (narrow_valu(d_in, d_out))
         return hip_check(
             digest::launch_narrow_k(p->n_own, d_in, d_out, G, d_out, w, dh_in, d_in, s),
@@ -863,12 +863,12 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     g.C = g.splits > 1 ? gpart : dw;
     g.ldc = d_out;
     {
-        Timed t(p, K_GEMM_DW, s);
+        Timed t(p, K_GEMM_DW, layer, s);
         if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
             return st;
     }
     if (g.splits > 1) {
-        Timed t(p, K_REDUCE_DW, s);
+        Timed t(p, K_REDUCE_DW, layer, s);
         if (digest_status st = hip_check(
                 digest::launch_splitk_reduce(gpart, g.splits, (int64_t)d_in * d_out, dw, s),
                 "dW reduce"))
@@ -891,12 +891,12 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
     if (!relu && d_out < d_in) {
         // Narrower output: aggregate D first (width d_out), then (P_in^T D) W^T.
-        if (digest_status st = run_spmm(p, Csr::InT, dh_out, nullptr, p->n_own, d_out, tmp, s))
+        if (digest_status st = run_spmm(p, Csr::InT, dh_out, nullptr, p->n_own, d_out, tmp, layer, s))
             return st;
         h.A = tmp;
         h.lda = d_out;
         h.C = dh_in;
-        Timed t(p, K_GEMM_DH, s);
+        Timed t(p, K_GEMM_DH, layer, s);
         return hip_check(digest::launch_gemm(h, s), "dgrad gemm");
     }
     // Otherwise G = D W^T (mask fused into the operand load), then P_in^T G.
@@ -905,11 +905,11 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     h.a_mask = relu ? h_out : nullptr;
     h.C = tmp;
     {
-        Timed t(p, K_GEMM_DH, s);
+        Timed t(p, K_GEMM_DH, layer, s);
         if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
             return st;
     }
-    return run_spmm(p, Csr::InT, tmp, nullptr, p->n_own, d_in, dh_in, s);
+    return run_spmm(p, Csr::InT, tmp, nullptr, p->n_own, d_in, dh_in, layer, s);
 }
 
 digest_status digest_softmax_xent(digest_partition *p, const float *logits,
@@ -921,7 +921,7 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
     if (!loss || (p->n_own > 0 && (!logits || !labels || !dlogits)))
         return fail(DIGEST_EINVAL, "NULL logits, labels, dlogits or loss");
     hipStream_t s = (hipStream_t)hip_stream;
-    Timed t(p, K_LOSS, s);
+    Timed t(p, K_LOSS, p->L, s);
     return hip_check(digest::launch_softmax_xent(logits, labels, p->n_own, p->widths[p->L],
                                                  dlogits, p->at<float>(p->lay.loss_part), loss,
                                                  s),
@@ -949,7 +949,8 @@ digest_status digest_profile_read(digest_partition *p, double *total_ms, int64_t
 {
     if (!p || !total_ms || !launches)
         return fail(DIGEST_EINVAL, "NULL argument");
-    for (int32_t k = 0; k < K_COUNT; ++k) {
+    const int32_t slots = p->L + 1;
+    for (int32_t k = 0; k < K_COUNT * slots; ++k) {
         total_ms[k] = 0.0;
         launches[k] = 0;
     }
@@ -962,8 +963,8 @@ digest_status digest_profile_read(digest_partition *p, double *total_ms, int64_t
                 e = hipEventElapsedTime(&ms, r.a, r.b);
             if (e != hipSuccess)
                 st = hip_check(e, "profile read");
-            total_ms[r.kind] += ms;
-            launches[r.kind] += 1;
+            total_ms[r.kind * slots + r.layer] += ms;
+            launches[r.kind * slots + r.layer] += 1;
         }
         p->pool.push_back(r.a);
         p->pool.push_back(r.b);

@@ -14,7 +14,8 @@
 //                  are deterministic; no float atomics, no global fences.
 //   k_gemm         fp32 MFMA (v_mfma_f32_32x32x2f32) GEMM with optional
 //                  transposed operands, ReLU-derivative operand masks, a
-//                  ReLU epilogue and split-K over grid.z: the dense
+//                  ReLU epilogue and split-K; tiles are dealt to the XCDs in
+//                  contiguous runs (shared operand strips share an L2): the dense
 //                  transform AH W, the weight gradient AH^T D and D W^T.
 //   k_splitk_reduce  deterministic sum of split-K partial products.
 //   k_softmax_xent / k_loss_reduce  the mean cross-entropy loss head.
@@ -28,6 +29,20 @@ namespace digest {
 namespace {
 
 constexpr int kWave = 64;
+
+// The dispatcher deals workgroups to the 8 XCDs (each with its own L2) in
+// turn by linear id.  xcd_contiguous maps the linear id p of an n-workgroup
+// grid to a logical id such that every XCD receives one contiguous run of
+// logical ids, in increasing order; it is a bijection of [0, n).  Kernels
+// order their logical work so that neighbours share operand data.
+constexpr uint32_t kXcds = 8;
+
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t p, uint32_t n)
+{
+    const uint32_t q = n / kXcds, rem = n % kXcds;
+    const uint32_t x = p % kXcds, slot = p / kXcds;
+    return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + slot;
+}
 
 template <int VEC>
 __device__ __forceinline__ void load_vec(const float *p, float (&x)[VEC])
@@ -342,7 +357,7 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
                                               const float *__restrict__ B, int32_t ldb,
                                               const float *__restrict__ Bm,
                                               float *__restrict__ C, int32_t ldc,
-                                              int64_t c_split_stride)
+                                              int64_t c_split_stride, int32_t gm, int32_t gn)
 {
     constexpr int BK = kGemmBK;
     constexpr int TM = BM / 64, TN = BN / 64;     // 32x32 blocks per wave
@@ -357,9 +372,15 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wid = tid / kWave;
-    const int m0 = blockIdx.x * BM;
-    const int n0 = blockIdx.y * BN;
-    const int kb = blockIdx.z * kchunk;
+    // Logical tiles: split-major, then M strip, then N tile, so that an XCD
+    // holds whole K slices and the N tiles of an M strip (shared operands).
+    const uint32_t logical = xcd_contiguous(blockIdx.x, gridDim.x);
+    const uint32_t per_split = (uint32_t)gm * (uint32_t)gn;
+    const int z = (int)(logical / per_split);
+    const uint32_t t = logical % per_split;
+    const int m0 = (int)(t / (uint32_t)gn) * BM;
+    const int n0 = (int)(t % (uint32_t)gn) * BN;
+    const int kb = z * kchunk;
     const int ke = min(K, kb + kchunk);
     const int wm = (wid >> 1) * (BM / 2);
     const int wn = (wid & 1) * (BN / 2);
@@ -478,7 +499,7 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
         __syncthreads();
     }
 
-    float *Cz = C + (int64_t)blockIdx.z * c_split_stride;
+    float *Cz = C + (int64_t)z * c_split_stride;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -941,12 +962,14 @@ hipError_t spmm_v(int vec, int gl, int nch, const SpmmBlock *blocks, int32_t n_b
 template <int BM, int BN, bool AT, bool BT, bool AMASK, bool BMASK, bool RELU, bool VA, bool VB>
 hipError_t gemm_t(const GemmArgs &a, hipStream_t s)
 {
-    const dim3 grid((unsigned)((a.M + BM - 1) / BM), (unsigned)((a.N + BN - 1) / BN),
-                    (unsigned)a.splits);
+    const int64_t gm = (a.M + BM - 1) / BM, gn = (a.N + BN - 1) / BN;
+    const int64_t grid = gm * gn * a.splits;
+    if (grid > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
     const int64_t split_stride = a.splits > 1 ? (int64_t)a.M * a.ldc : 0;
-    hipLaunchKernelGGL((k_gemm<BM, BN, AT, BT, AMASK, BMASK, RELU, VA, VB>), grid, dim3(256), 0,
-                       s, a.M, a.N, a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb, a.b_mask,
-                       a.C, a.ldc, split_stride);
+    hipLaunchKernelGGL((k_gemm<BM, BN, AT, BT, AMASK, BMASK, RELU, VA, VB>), dim3((unsigned)grid),
+                       dim3(256), 0, s, a.M, a.N, a.K, a.kchunk, a.A, a.lda, a.a_mask, a.B, a.ldb,
+                       a.b_mask, a.C, a.ldc, split_stride, (int32_t)gm, (int32_t)gn);
     return hipGetLastError();
 }
 

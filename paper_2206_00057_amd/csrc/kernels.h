@@ -32,7 +32,8 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t 
                        const float *src1, int32_t n_src0, int32_t d, float *out,
                        hipStream_t s);
 
-// C = op(A) op(B) in fp32 on MFMA, K-range split over grid.z when splits > 1.
+// C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
+// slices (each its own grid part) when splits > 1.
 //   op(A)(m,k) = a_trans ? A[k*lda + m] : A[m*lda + k]      (M x K)
 //   op(B)(k,n) = b_trans ? B[n*ldb + k] : B[k*ldb + n]      (K x N)
 //   a_mask / b_mask (optional, same layout as A / B): operand element is

@@ -273,10 +273,19 @@ def kernel_names():
 
 
 def digest_profile_read(p):
-    """Per kernel kind: (total ms, launches) since the last read (synchronises)."""
+    """Per (kernel kind, layer slot): {"kind.lN": (total ms, launches)} since the
+    last read (synchronises).  Slot = layer for layer kernels, level for
+    pull/push, L for the loss head; entries without launches are omitted."""
     n = lib().digest_profile_kernel_count()
-    ms = np.zeros(n, np.float64)
-    cnt = np.zeros(n, np.int64)
+    slots = p.L + 1
+    ms = np.zeros(n * slots, np.float64)
+    cnt = np.zeros(n * slots, np.int64)
     _check(lib().digest_profile_read(p.handle, ms.ctypes.data_as(ctypes.c_void_p),
                                      cnt.ctypes.data_as(ctypes.c_void_p)))
-    return {name: (float(ms[i]), int(cnt[i])) for i, name in enumerate(kernel_names())}
+    out = {}
+    for i, name in enumerate(kernel_names()):
+        for sl in range(slots):
+            j = i * slots + sl
+            if cnt[j]:
+                out[f"{name}.l{sl}"] = (float(ms[j]), int(cnt[j]))
+    return out

@@ -1,0 +1,133 @@
+"""Text summaries of rocprofv3 output for the kernels of libdigest.so.
+
+Kernel durations (from a ``rocprofv3 --kernel-trace --stats`` run):
+
+    python -m paper_2206_00057_amd.pmc stats --csv <dir>/<name>_kernel_stats.csv \\
+        --title "..." --command "..." --out profiles/<kernel-or-workload>_kernel_stats.txt
+
+HBM traffic of one kernel, from two counter passes over the same command:
+
+    python -m paper_2206_00057_amd.pmc traffic \\
+        --fetch gpurun_out/pmc_fetch/fetch_counter_collection.csv \\
+        --write gpurun_out/pmc_write/write_counter_collection.csv \\
+        --kernel-name "k_gemm<64, 64, true, false, false, true" --key gemm_dw_splitk.l1 \\
+        --copy-bytes 268435456 --workload medium --out profiles/medium_hbm_traffic.txt
+
+FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel's dispatches are
+averaged, then each is divided by what the same counter reads, per byte, for
+a plain copy kernel of known size (the largest "copyBuffer" dispatch of the
+run, a device-to-device copy of --copy-bytes bytes).  The summary records the
+hash of the kernel sources; bench.py reports the figure only while that hash
+still matches.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import os
+import re
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def kernel_source_hash() -> str:
+    """Hash of the sources that define the kernels and their launches."""
+    h = hashlib.sha256()
+    for f in ("digest_kernels.hip", "kernels.h", "digest_host.cpp"):
+        with open(os.path.join(ROOT, "paper_2206_00057_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _rows(path, counter):
+    out = []
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r.get("Counter_Name", counter) == counter:
+                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def summarize(fetch_csv, write_csv, kernel_name, copy_name, copy_bytes):
+    f = _rows(fetch_csv, "FETCH_SIZE")
+    w = _rows(write_csv, "WRITE_SIZE")
+    kf = [v for n, v in f if kernel_name in n]
+    kw = [v for n, v in w if kernel_name in n]
+    cf = max(v for n, v in f if copy_name in n)
+    cw = max(v for n, v in w if copy_name in n)
+    if not kf or not kw:
+        raise SystemExit(f"no dispatch of {kernel_name!r} in the counter files")
+    fetch_kib = sum(kf) / len(kf)
+    write_kib = sum(kw) / len(kw)
+    fetch_scale = cf * 1024.0 / copy_bytes
+    write_scale = cw * 1024.0 / copy_bytes
+    traffic = fetch_kib * 1024.0 / fetch_scale + write_kib * 1024.0 / write_scale
+    names = sorted({n for n, _ in f if kernel_name in n})
+    return {
+        "rocprof_kernel": names[0] if names else kernel_name,
+        "dispatches": len(kf),
+        "fetch_kib_per_dispatch": round(fetch_kib, 1),
+        "write_kib_per_dispatch": round(write_kib, 1),
+        "calibration_copy_bytes": copy_bytes,
+        "calibration_fetch_kib": round(cf, 1),
+        "calibration_write_kib": round(cw, 1),
+        "fetch_scale": round(fetch_scale, 4),
+        "write_scale": round(write_scale, 4),
+        "traffic_bytes_per_launch": round(traffic),
+    }
+
+
+def stats_table(path):
+    """Per-kernel rows of a rocprofv3 kernel_stats.csv, as fixed-width text."""
+    out = [f"# {'kernel':70s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} "
+           f"{'total_ms':>9s} {'pct':>6s}"]
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            name = re.sub(r"\(anonymous namespace\)::", "", r["Name"])
+            name = re.sub(r"\((.*)\)$", "", name).replace("void ", "")
+            out.append(f"  {name[:70]:70s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.2f} "
+                       f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} "
+                       f"{float(r['TotalDurationNs']) / 1e6:9.3f} {float(r['Percentage']):6.2f}")
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    st = sub.add_parser("stats", help="format a kernel_stats.csv")
+    st.add_argument("--csv", required=True)
+    st.add_argument("--title", required=True)
+    st.add_argument("--command", action="append", default=[])
+    st.add_argument("--out", required=True)
+    tr = sub.add_parser("traffic", help="HBM bytes per launch of one kernel")
+    tr.add_argument("--fetch", required=True)
+    tr.add_argument("--write", required=True)
+    tr.add_argument("--kernel-name", required=True, help="substring of the rocprof kernel name")
+    tr.add_argument("--key", required=True, help="bench.py kernel key, e.g. gemm_dw_splitk.l1")
+    tr.add_argument("--copy-name", default="copyBuffer")
+    tr.add_argument("--copy-bytes", type=int, required=True)
+    tr.add_argument("--workload", required=True)
+    tr.add_argument("--command", action="append", default=[])
+    tr.add_argument("--out", required=True)
+    a = ap.parse_args()
+    if a.cmd == "stats":
+        lines = [f"# {a.title}"] + [f"# command: {c}" for c in a.command]
+        lines += [f"# source: rocprofv3 --kernel-trace --stats ({os.path.basename(a.csv)})", "#"]
+        lines += stats_table(a.csv)
+    else:
+        s = summarize(a.fetch, a.write, a.kernel_name, a.copy_name, a.copy_bytes)
+        lines = [f"# HBM traffic of one launch of {a.key} on the {a.workload} workload,",
+                 "# from rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by",
+                 "# the counter's reading per byte of a plain device-to-device copy of known size.",
+                 "# commands:"]
+        lines += [f"#   {c}" for c in a.command]
+        lines += [f"kernel = {a.key}", f"source_sha = {kernel_source_hash()}"]
+        lines += [f"{k} = {v}" for k, v in s.items()]
+    with open(a.out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+if __name__ == "__main__":
+    main()
