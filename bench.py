@@ -47,10 +47,12 @@ def splitk(M, N, K):
 
 
 def tf_slices(n, nh, di, do):
+    """Mirror of the library's slice plan for the transform-first dW."""
     if do <= 16:
         R = n + nh
-        target = 512 // max(1, -(-di // 256))
-        chunk = max(64, -(-R // max(target, 1)))
+        target = max(1, 2048 // -(-di // 64))
+        chunk = max(32, -(-R // target))
+        chunk = -(-chunk // 32) * 32
         return max(1, -(-R // chunk))
     return splitk(di, do, n)[0] + (splitk(di, do, nh)[0] if nh else 0)
 
@@ -76,10 +78,12 @@ def launch_model(st, widths):
             R = n + nh
             put("gemm_fwd_relu", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
             put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)
-            put("spmm_bwd_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do)
+            fused = l > 1 and do <= 16 and di <= 1024 and di % 4 == 0
+            put("spmm_bwd_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do
+                + (4 * (n * di + di * do) if fused else 0))
             put("gemm_dw_splitk", l, 4 * (R * di + R * do), 2.0 * R * di * do)
             put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
-            if l > 1:
+            if l > 1 and not fused:
                 put("gemm_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
             continue
         put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)

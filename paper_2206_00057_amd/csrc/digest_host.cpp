@@ -87,15 +87,16 @@ int32_t gemm_tile_for(int64_t M, int64_t N, int64_t K, bool contraction_over_row
 
 // Aggregation blocks of a CSR: every long row gets a block of its own (those
 // come first, so they start early); runs of consecutive short rows are
-// packed one per wave.
-void build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
-                  std::vector<SpmmBlock> &blocks)
+// packed one per wave.  Returns the number of long-row blocks.
+int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
+                     std::vector<SpmmBlock> &blocks)
 {
     const int32_t waves = digest::kSpmmThreads / 64;
     blocks.clear();
     for (int32_t r = 0; r < n_rows; ++r)
         if (rowptr[r + 1] - rowptr[r] > digest::kSpmmLongRow)
             blocks.push_back({r, 0, rowptr[r], rowptr[r + 1]});
+    const int32_t n_long = (int32_t)blocks.size();
     int32_t first = -1, count = 0;
     for (int32_t r = 0; r <= n_rows; ++r) {
         const bool short_row = r < n_rows && rowptr[r + 1] - rowptr[r] <= digest::kSpmmLongRow;
@@ -109,6 +110,7 @@ void build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
             count = 0;
         }
     }
+    return n_long;
 }
 
 }  // namespace
@@ -126,6 +128,7 @@ struct digest_partition {
     // blocks_t covers the first n_own rows of the transpose (P_in^T),
     // blocks_tf all n_own + n_halo rows (P_m^T).
     std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf;
+    int32_t long_f = 0, long_t = 0, long_tf = 0;   // leading long-row blocks of each
 
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
@@ -251,7 +254,7 @@ void plan_layout(digest_partition &p)
     l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
     l.tbuf = take(sizeof(float) * (size_t)tbuf);
     l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
-    l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own));
+    l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own, p.widths[p.L]));
     l.total = o;
 }
 
@@ -315,18 +318,20 @@ digest_status need_bound(const digest_partition *p)
 enum class Csr { Fwd, InT, FullT };
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
-                       int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s)
+                       int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
+                       const digest::SpmmEpilogue *ep = nullptr)
 {
     const bool fwd = which == Csr::Fwd;
     const auto &blocks = fwd ? p->blocks_f : (which == Csr::InT ? p->blocks_t : p->blocks_tf);
     const size_t boff = fwd ? p->lay.blocks_f : (which == Csr::InT ? p->lay.blocks_t : p->lay.blocks_tf);
+    const int32_t n_long = fwd ? p->long_f : (which == Csr::InT ? p->long_t : p->long_tf);
     Timed t(p, fwd ? K_SPMM_FWD : K_SPMM_BWD, layer, s);
     return hip_check(
-        digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks.size(),
+        digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks.size(), n_long,
                             p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr),
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
                             p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1, n_src0, d,
-                            out, s),
+                            out, s, ep),
         "spmm");
 }
 
@@ -453,9 +458,9 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
                 ++next[c];
             }
 
-        build_blocks(p->rowptr, p->n_own, p->blocks_f);
-        build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
-        build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
+        p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
+        p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
+        p->long_tf = build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
         plan_layout(*p);
         p->pulled.assign(p->L, 0);
         p->pull_gen.assign(p->L, 0);
@@ -748,7 +753,13 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
     float *G = p->at<float>(p->lay.tbuf);
     float *gpart = p->at<float>(p->lay.gemm_part);
-    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s))
+    // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
+    // same launch also writes dh_in = G_own W^T for the owned rows.
+    const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
+                          digest::spmm_epilogue_ok(d_out, d_in, dh_in);
+    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in};
+    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
+                                    fused_dh ? &ep : nullptr))
         return st;
     const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
     {
@@ -796,7 +807,7 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                 "dW reduce"))
             return st;
     }
-    if (!dh_in)
+    if (!dh_in || fused_dh)
         return DIGEST_OK;
     Timed tm(p, K_GEMM_DH, layer, s);
     if (narrow_valu(d_in, d_out))

@@ -18,6 +18,8 @@
 //                  contiguous runs (shared operand strips share an L2): the dense
 //                  transform AH W, the weight gradient AH^T D and D W^T.
 //   k_splitk_reduce  deterministic sum of split-K partial products.
+//   k_narrow_n / k_narrow_k / k_dw_narrow  products with one side at most
+//                  16 wide (the transform-first last layer).
 //   k_softmax_xent / k_loss_reduce  the mean cross-entropy loss head.
 #include <hip/hip_runtime.h>
 
@@ -84,6 +86,30 @@ __device__ __forceinline__ float readlane_f(float v, int lane)
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
+// Fill an LDS array of `count` floats, value(i) for i < count, with the
+// block's threads: loads are issued in batches of 16 per thread before their
+// stores, so staging costs one round trip per batch rather than per element.
+template <class F>
+__device__ __forceinline__ void stage_lds(float *dst, int count, F value)
+{
+    constexpr int BATCH = 16;
+    const int stride = blockDim.x;
+    for (int base = threadIdx.x; base < count; base += BATCH * stride) {
+        float v[BATCH];
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            const int i = base + b * stride;
+            v[b] = i < count ? value(i) : 0.f;
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            const int i = base + b * stride;
+            if (i < count)
+                dst[i] = v[b];
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Row copy (pull / push)
 // ---------------------------------------------------------------------------
@@ -142,21 +168,18 @@ constexpr int spmm_inflight(int groups, int nch, int vec)
 // per column pass).  Entry ids and weights are fetched 64 at a time (one per
 // lane) and broadcast; up to U entries per group are in flight.
 template <int VEC, int GL, int NCH, bool TWO>
-__global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restrict__ blocks,
-                                                       const int32_t *__restrict__ rowptr,
-                                                       const int32_t *__restrict__ col,
-                                                       const float *__restrict__ val,
-                                                       const float *__restrict__ src0,
-                                                       const float *__restrict__ src1,
-                                                       int32_t n_src0, int32_t d,
-                                                       float *__restrict__ out)
+__device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__restrict__ rowptr,
+                                           const int32_t *__restrict__ col,
+                                           const float *__restrict__ val,
+                                           const float *__restrict__ src0,
+                                           const float *__restrict__ src1, int32_t n_src0,
+                                           int32_t d, float *__restrict__ out,
+                                           float (*red)[NCH * GL * VEC])
 {
     constexpr int G = kWave / GL;
     constexpr int U = spmm_inflight(G, NCH, VEC);
     constexpr int SPAN = NCH * GL;   // feature vectors per column pass
-    __shared__ float red[kSpmmWaves][SPAN * VEC];
 
-    const SpmmBlock b = blocks[blockIdx.x];
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
     const int g = lane / GL;
@@ -277,6 +300,158 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restri
                 }
             }
             __syncthreads();
+        }
+    }
+}
+
+// out2[4 n4 .. 4 n4 + 3] = sum_{k < d} gk[k] w[k][4 n4 ..], w in LDS as [k][n2].
+__device__ __forceinline__ void narrow_ep_store(const float (&gk)[kNarrow], int d,
+                                                const float *ws, int n2, int n4, float *out2)
+{
+    float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < kNarrow; ++k) {
+        if (k < d) {
+            const float4 w = *reinterpret_cast<const float4 *>(ws + k * n2 + 4 * n4);
+            o[0] = fmaf(gk[k], w.x, o[0]);
+            o[1] = fmaf(gk[k], w.y, o[1]);
+            o[2] = fmaf(gk[k], w.z, o[2]);
+            o[3] = fmaf(gk[k], w.w, o[3]);
+        }
+    }
+    *reinterpret_cast<float4 *>(out2 + 4 * n4) = make_float4(o[0], o[1], o[2], o[3]);
+}
+
+template <int VEC, int GL, int NCH, bool TWO>
+__global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restrict__ blocks,
+                                                       const int32_t *__restrict__ rowptr,
+                                                       const int32_t *__restrict__ col,
+                                                       const float *__restrict__ val,
+                                                       const float *__restrict__ src0,
+                                                       const float *__restrict__ src1,
+                                                       int32_t n_src0, int32_t d,
+                                                       float *__restrict__ out)
+{
+    __shared__ float red[kSpmmWaves][NCH * GL * VEC];
+    spmm_block<VEC, GL, NCH, TWO>(blocks[blockIdx.x], rowptr, col, val, src0, src1, n_src0, d,
+                                  out, red);
+}
+
+// Aggregation for rows at most GL * VEC <= 16 wide, where one row per wave
+// would leave most lanes idle: the n_long long-row blocks (first in the
+// list) run as in k_spmm, one per workgroup; every wave of the remaining
+// workgroups takes one short-row block (up to kSpmmWaves consecutive rows)
+// and gives each of its lane groups a row of its own.  A group fetches
+// kNarrowBatch * GL entry ids and weights at a time (kNarrowBatch per lane),
+// broadcasts them inside the group and keeps all of their gathers in flight,
+// so a row of up to that many entries costs one dependent round trip; the
+// entries of a row are added in CSR order, so results do not depend on the
+// launch shape.
+// With EP, rows r < ep.rows also get out2[r][n] = sum_k out[r][k] w[n][k]
+// (w row-major [n2][d], staged in LDS as [k][n2]); a lane group shares its
+// row by shuffles and writes it out in float4 pieces.
+constexpr int kNarrowBatch = 4;
+
+template <int VEC, int GL, bool TWO, bool EP>
+__global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
+    const SpmmBlock *__restrict__ blocks, int32_t n_long, int32_t n_blocks,
+    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+    const float *__restrict__ val, const float *__restrict__ src0, const float *__restrict__ src1,
+    int32_t n_src0, int32_t d, float *__restrict__ out, SpmmEpilogue ep)
+{
+    __shared__ float red[kSpmmWaves][GL * VEC];
+    extern __shared__ float ws[];   // EP: w as [k][n2]
+    if constexpr (EP) {
+        stage_lds(ws, d * ep.n2, [&](int i) {
+            const int k = i / ep.n2, n = i % ep.n2;
+            return ep.w[(int64_t)n * d + k];
+        });
+        __syncthreads();
+    }
+    if ((int32_t)blockIdx.x < n_long) {   // uniform over the block
+        const SpmmBlock b = blocks[blockIdx.x];
+        spmm_block<VEC, GL, 1, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, out, red);
+        if constexpr (EP) {
+            // the row was written by this block before spmm_block's last barrier
+            if (b.row < ep.rows) {
+                float gk[kNarrow];
+#pragma unroll
+                for (int k = 0; k < kNarrow; ++k)
+                    gk[k] = k < d ? out[(int64_t)b.row * d + k] : 0.f;
+                for (int n4 = threadIdx.x; n4 < ep.n2 / 4; n4 += kSpmmThreads)
+                    narrow_ep_store(gk, d, ws, ep.n2, n4, ep.out2 + (int64_t)b.row * ep.n2);
+            }
+        }
+        return;
+    }
+    constexpr int G = kWave / GL;
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const int g = lane / GL;
+    const int gl = lane % GL;
+    const int bi = n_long + ((int)blockIdx.x - n_long) * kSpmmWaves + wave;
+    if (bi >= n_blocks)
+        return;
+    const SpmmBlock b = blocks[bi];
+    const int dv = d / VEC;
+    const bool lane_ok = gl < dv;   // GL * VEC >= d, so one vector per lane covers the row
+    for (int i = g; i < b.nrows; i += G) {
+        const int row = b.row + i;
+        const int kb = rowptr[row], ke = rowptr[row + 1];
+        float acc[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            acc[v] = 0.f;
+        constexpr int E = kNarrowBatch * GL;   // entries per batch
+        for (int k0 = kb; k0 < ke; k0 += E) {
+            const int nb = min(E, ke - k0);
+            int mc[kNarrowBatch];
+            float mv[kNarrowBatch];
+#pragma unroll
+            for (int j = 0; j < kNarrowBatch; ++j) {   // entry k0 + j*GL + gl
+                const bool ok = j * GL + gl < nb;
+                mc[j] = ok ? col[k0 + j * GL + gl] : 0;
+                mv[j] = ok ? val[k0 + j * GL + gl] : 0.f;
+            }
+            float x[kNarrowBatch][GL][VEC];
+            float aa[kNarrowBatch][GL];
+#pragma unroll
+            for (int j = 0; j < kNarrowBatch; ++j)
+#pragma unroll
+                for (int u = 0; u < GL; ++u) {
+                    const int cc = __shfl(mc[j], g * GL + u);
+                    aa[j][u] = __shfl(mv[j], g * GL + u);
+                    const float *sp = (TWO && cc >= n_src0) ? src1 + (int64_t)(cc - n_src0) * d
+                                                            : src0 + (int64_t)cc * d;
+                    if (j * GL + u < nb && lane_ok) {
+                        load_vec<VEC>(sp + gl * VEC, x[j][u]);
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v)
+                            x[j][u][v] = 0.f;
+                    }
+                }
+#pragma unroll
+            for (int j = 0; j < kNarrowBatch; ++j)
+#pragma unroll
+                for (int u = 0; u < GL; ++u)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        acc[v] = fmaf(aa[j][u], x[j][u][v], acc[v]);
+        }
+        if (lane_ok)
+            store_vec<VEC>(out + (int64_t)row * d + gl * VEC, acc);
+        if constexpr (EP) {
+            if (row < ep.rows) {
+                float gk[kNarrow];
+#pragma unroll
+                for (int k = 0; k < kNarrow; ++k) {
+                    const float v = __shfl(acc[k % VEC], (g * GL + k / VEC) & (kWave - 1));
+                    gk[k] = k < d ? v : 0.f;
+                }
+                for (int n4 = gl; n4 < ep.n2 / 4; n4 += GL)
+                    narrow_ep_store(gk, d, ws, ep.n2, n4, ep.out2 + (int64_t)row * ep.n2);
+            }
         }
     }
 }
@@ -578,30 +753,6 @@ __global__ __launch_bounds__(256) void k_splitk_reduce_wide(const float *__restr
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// Fill an LDS array of `count` floats, value(i) for i < count, with the
-// block's threads: loads are issued in batches of 16 per thread before their
-// stores, so staging costs one round trip per batch rather than per element.
-template <class F>
-__device__ __forceinline__ void stage_lds(float *dst, int count, F value)
-{
-    constexpr int BATCH = 16;
-    const int stride = blockDim.x;
-    for (int base = threadIdx.x; base < count; base += BATCH * stride) {
-        float v[BATCH];
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b) {
-            const int i = base + b * stride;
-            v[b] = i < count ? value(i) : 0.f;
-        }
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b) {
-            const int i = base + b * stride;
-            if (i < count)
-                dst[i] = v[b];
-        }
-    }
-}
-
 // C[r][n] = sum_k A(r)[k] B[k][n] for n < N <= 16, on v_mfma_f32_16x16x4f32.
 // Row r of A is row r of A0 (r < m0) or row r - m0 of A1 (leading dim lda).
 // B is staged once per block in LDS (zero-padded to 16 columns); a wave owns
@@ -619,22 +770,15 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
     constexpr int KC = 256;          // k per chunk
     constexpr int J = KC / 16;       // 16-k steps per chunk
     extern __shared__ float Bs[];    // [K][16]
-    stage_lds(Bs, K * 16, [&](int i) {
-        const int k = i >> 4, n = i & 15;
-        return n < N ? B[k * N + n] : 0.f;
-    });
-    __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
     const int row0 = (blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * 16;
-    if (row0 >= M)
-        return;   // uniform per wave (after the barrier)
     const int m = lane & 15, h = lane >> 4;
     const int r = row0 + m;
-    const bool row_ok = r < M;
+    const bool row_ok = r < M;   // a wave past M loads the first element and stores nothing
     const float *a = !row_ok ? A0 : (r < m0 ? A0 + (int64_t)r * lda : A1 + (int64_t)(r - m0) * lda);
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int kc = 0; kc < K; kc += KC) {
-        float av[J][4];
+    float av[J][4];
+    auto load_chunk = [&](int kc) {
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int k = kc + 16 * j + 4 * h;
@@ -654,6 +798,14 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
                 }
             }
         }
+    };
+    stage_lds(Bs, K * 16, [&](int i) {
+        const int k = i >> 4, n = i & 15;
+        return n < N ? B[k * N + n] : 0.f;
+    });
+    __syncthreads();
+    for (int kc = 0; kc < K; kc += KC) {
+        load_chunk(kc);
 #pragma unroll
         for (int j = 0; j < J; ++j)
 #pragma unroll
@@ -675,47 +827,66 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
 }
 
 // C[r][n] = sum_{k < K} A[r][k] W[n][k] (W row-major [N][K], i.e. A W^T) for
-// K <= KK.  W is staged once per block in LDS as [k][n4] (16-byte reads,
-// neighbouring threads on neighbouring addresses); blocks then stride over
-// the rows, each thread producing four consecutive columns of a row.
+// K <= KK.  A wave owns a slice of 256 columns, four per lane, and keeps
+// that slice of W in registers for the whole launch; it then strides over
+// the rows, RU at a time: the K inputs of a row are read at a wave-uniform
+// address (scalar loads) and every lane writes its four outputs.
+constexpr int kNarrowKRows = 4;
+
 template <int KK>
 __global__ __launch_bounds__(256) void k_narrow_k(int32_t M, int32_t N, int32_t K,
                                                   const float *__restrict__ A, int32_t lda,
                                                   const float *__restrict__ W,
-                                                  float *__restrict__ C, int32_t ldc, bool vec_out)
+                                                  float *__restrict__ C, int32_t ldc,
+                                                  bool vec_out, int32_t slices)
 {
-    extern __shared__ float Ws[];   // [KK][N4], N4 = N rounded up to 4
-    const int N4 = (N + 3) & ~3;
-    stage_lds(Ws, KK * N4, [&](int i) {
-        const int k = i / N4, n = i % N4;
-        return (k < K && n < N) ? W[(int64_t)n * K + k] : 0.f;
-    });
-    __syncthreads();
-    const uint32_t nq = (uint32_t)N4 / 4;
-    const uint32_t total = (uint32_t)M * nq;   // < 2^31, checked by the launcher
-    for (uint32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < total;
-         t += gridDim.x * blockDim.x) {
-        const int64_t r = t / nq;
-        const int n0 = (int)(t % nq) * 4;
-        float s[4] = {0.f, 0.f, 0.f, 0.f};
+    constexpr int RU = kNarrowKRows;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int gw = __builtin_amdgcn_readfirstlane(
+        (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave));
+    const int nw = (int)(gridDim.x * (blockDim.x / kWave)) / slices;   // waves per slice
+    const int slice = gw % slices;
+    const int first = gw / slices;
+    if (first >= nw)
+        return;   // surplus waves (the launcher makes none)
+    const int n0 = slice * 256 + lane * 4;
+    float w[KK][4];
 #pragma unroll
-        for (int k = 0; k < KK; ++k) {
-            if (k < K) {
-                const float a = A[r * lda + k];
-                const float4 w = *reinterpret_cast<const float4 *>(Ws + k * N4 + n0);
-                s[0] = fmaf(a, w.x, s[0]);
-                s[1] = fmaf(a, w.y, s[1]);
-                s[2] = fmaf(a, w.z, s[2]);
-                s[3] = fmaf(a, w.w, s[3]);
-            }
+    for (int k = 0; k < KK; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[k][j] = (k < K && n0 + j < N) ? W[(int64_t)(n0 + j) * K + k] : 0.f;
+    for (int r0 = first * RU; r0 < M; r0 += nw * RU) {
+        float a[RU][KK];
+#pragma unroll
+        for (int u = 0; u < RU; ++u) {
+            const int r = min(r0 + u, M - 1);   // rows past M recompute row M-1, not stored
+            const float *ar = A + (int64_t)r * lda;
+#pragma unroll
+            for (int k = 0; k < KK; ++k)
+                a[u][k] = k < K ? ar[k] : 0.f;
         }
-        if (vec_out) {
-            *reinterpret_cast<float4 *>(C + r * ldc + n0) = make_float4(s[0], s[1], s[2], s[3]);
-        } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (n0 + j < N)
-                    C[r * ldc + n0 + j] = s[j];
+        for (int u = 0; u < RU; ++u) {
+            const int r = r0 + u;
+            if (r >= M)
+                break;
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < KK; ++k)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[j] = fmaf(a[u][k], w[k][j], acc[j]);
+            float *cr = C + (int64_t)r * ldc + n0;
+            if (vec_out) {
+                if (n0 < N)
+                    *reinterpret_cast<float4 *>(cr) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (n0 + j < N)
+                        cr[j] = acc[j];
+            }
         }
     }
 }
@@ -786,18 +957,22 @@ __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_
 // Softmax cross entropy
 // ---------------------------------------------------------------------------
 
-constexpr int kLossRowsPerBlock = 4;   // one row per wave
+constexpr int kLossThreads = 256;
 
-__global__ __launch_bounds__(256) void k_softmax_xent(const float *__restrict__ logits,
-                                                      const int32_t *__restrict__ labels,
-                                                      int32_t n, int32_t C, float inv_n,
-                                                      float *__restrict__ dlogits,
-                                                      float *__restrict__ block_loss)
+// Row-wise softmax cross entropy.  A row belongs to a group of GL lanes
+// (class c to lane c mod GL), so a wave holds 64/GL rows; each block writes
+// the sum of its rows' losses (in a fixed order) for k_loss_reduce.
+template <int GL>
+__global__ __launch_bounds__(kLossThreads) void k_softmax_xent(
+    const float *__restrict__ logits, const int32_t *__restrict__ labels, int32_t n, int32_t C,
+    float inv_n, float *__restrict__ dlogits, float *__restrict__ block_loss)
 {
-    __shared__ float wave_loss[kLossRowsPerBlock];
+    constexpr int G = kWave / GL;
+    __shared__ float part[kLossThreads / kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x / kWave;
-    const int r = blockIdx.x * kLossRowsPerBlock + wid;
+    const int g = lane / GL, gl = lane % GL;
+    const int r = (blockIdx.x * (kLossThreads / kWave) + wid) * G + g;
     float row_loss = 0.f;
     if (r < n) {
         const float *z = logits + (int64_t)r * C;
@@ -805,51 +980,55 @@ __global__ __launch_bounds__(256) void k_softmax_xent(const float *__restrict__ 
         const int y = labels[r];
         const bool bad = y < 0 || y >= C;
         float m = -INFINITY;
-        for (int c = lane; c < C; c += kWave)
+        for (int c = gl; c < C; c += GL)
             m = fmaxf(m, z[c]);
-        for (int off = kWave / 2; off > 0; off >>= 1)
+#pragma unroll
+        for (int off = GL / 2; off > 0; off >>= 1)
             m = fmaxf(m, __shfl_xor(m, off));
-        float s = 0.f;
-        for (int c = lane; c < C; c += kWave)
-            s += expf(z[c] - m);
-        for (int off = kWave / 2; off > 0; off >>= 1)
-            s += __shfl_xor(s, off);
-        const float log_s = logf(s);
-        for (int c = lane; c < C; c += kWave) {
+        float sum = 0.f;
+        for (int c = gl; c < C; c += GL)
+            sum += expf(z[c] - m);
+#pragma unroll
+        for (int off = GL / 2; off > 0; off >>= 1)
+            sum += __shfl_xor(sum, off);
+        const float log_s = logf(sum);
+        for (int c = gl; c < C; c += GL) {
             const float p = expf(z[c] - m - log_s);
             dz[c] = bad ? 0.f : (p - (c == y ? 1.f : 0.f)) * inv_n;
         }
         const int ys = bad ? 0 : y;   // never index with a bad label
-        row_loss = bad ? NAN : -(z[ys] - m - log_s);
+        if (gl == 0)
+            row_loss = bad ? NAN : -(z[ys] - m - log_s);
     }
+    // block sum: butterfly inside each wave, then the waves in order
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
+        row_loss += __shfl_xor(row_loss, off);
     if (lane == 0)
-        wave_loss[wid] = row_loss;
+        part[wid] = row_loss;
     __syncthreads();
     if (threadIdx.x == 0) {
         float t = 0.f;
-        for (int i = 0; i < kLossRowsPerBlock; ++i)
-            t += wave_loss[i];
+        for (int i = 0; i < kLossThreads / kWave; ++i)
+            t += part[i];
         block_loss[blockIdx.x] = t;
     }
 }
 
-__global__ __launch_bounds__(256) void k_loss_reduce(const float *__restrict__ block_loss,
+// loss = inv_n * sum of the block sums: one wave, lane j adding the block
+// sums j, j + 64, ... in order, then a butterfly (a fixed order).
+__global__ __launch_bounds__(kWave) void k_loss_reduce(const float *__restrict__ block_loss,
                                                      int32_t nb, float inv_n,
                                                      float *__restrict__ loss)
 {
-    __shared__ float part[256];
     float t = 0.f;
-    for (int i = threadIdx.x; i < nb; i += blockDim.x)
+    for (int i = threadIdx.x; i < nb; i += kWave)
         t += block_loss[i];
-    part[threadIdx.x] = t;
-    __syncthreads();
-    for (int off = 128; off > 0; off >>= 1) {
-        if ((int)threadIdx.x < off)
-            part[threadIdx.x] += part[threadIdx.x + off];
-        __syncthreads();
-    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
+        t += __shfl_xor(t, off);
     if (threadIdx.x == 0)
-        loss[0] = part[0] * inv_n;
+        loss[0] = t * inv_n;
 }
 
 // ---------------------------------------------------------------------------
@@ -901,6 +1080,26 @@ hipError_t copy_rows_v(int gl, const int32_t *sidx, const int32_t *didx, int32_t
     case 32: return copy_rows_t<VEC, 32>(sidx, didx, n_rows, d, src, dst, s);
     default: return copy_rows_t<VEC, 64>(sidx, didx, n_rows, d, src, dst, s);
     }
+}
+
+template <int VEC, int GL, bool TWO>
+hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_blocks,
+                         const int32_t *rowptr, const int32_t *col, const float *val,
+                         const float *src0, const float *src1, int32_t n_src0, int32_t d,
+                         float *out, const SpmmEpilogue *ep, hipStream_t s)
+{
+    const int64_t grid = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
+    if (ep) {
+        const size_t lds = sizeof(float) * (size_t)d * ep->n2;
+        hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, TWO, true>), dim3((unsigned)grid),
+                           dim3(kSpmmThreads), lds, s, blocks, n_long, n_blocks, rowptr, col, val,
+                           src0, src1, n_src0, d, out, *ep);
+    } else {
+        hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, TWO, false>), dim3((unsigned)grid),
+                           dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val,
+                           src0, src1, n_src0, d, out, SpmmEpilogue{});
+    }
+    return hipGetLastError();
 }
 
 template <int VEC, int GL, int NCH, bool TWO>
@@ -1021,10 +1220,19 @@ hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_
     }
 }
 
-hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
-                       const int32_t *col, const float *val, const float *src0,
-                       const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
+bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2)
 {
+    return d >= 1 && d <= kNarrow && n2 >= 4 && n2 % 4 == 0 &&
+           (size_t)d * n2 * sizeof(float) <= 64 * 1024 && ((uintptr_t)out2 % 16) == 0;
+}
+
+hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
+                       const int32_t *rowptr, const int32_t *col, const float *val,
+                       const float *src0, const float *src1, int32_t n_src0, int32_t d,
+                       float *out, hipStream_t s, const SpmmEpilogue *ep)
+{
+    if (ep && !spmm_epilogue_ok(d, ep->n2, ep->out2))
+        return hipErrorInvalidValue;
     if (n_blocks <= 0 || d <= 0)
         return hipSuccess;
     int vec = pick_vec(d, src0, out);
@@ -1032,6 +1240,31 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t 
         vec = pick_vec(d, src1, nullptr);
     const int dv = d / vec;
     const int gl = pick_group(dv);
+    if (ep && gl > 16)
+        return hipErrorInvalidValue;
+    if (gl <= 16) {   // narrow rows: a row per lane group
+        if (n_long < 0 || n_long > n_blocks)
+            return hipErrorInvalidValue;
+#define DIGEST_NARROW(V, L)                                                                      \
+    return src1 ? spmm_narrow_t<V, L, true>(blocks, n_long, n_blocks, rowptr, col, val, src0,   \
+                                            src1, n_src0, d, out, ep, s)                       \
+                : spmm_narrow_t<V, L, false>(blocks, n_long, n_blocks, rowptr, col, val, src0,  \
+                                             src1, n_src0, d, out, ep, s)
+        if (vec == 4) {
+            if (gl == 4) DIGEST_NARROW(4, 4);
+            if (gl == 8) DIGEST_NARROW(4, 8);
+            DIGEST_NARROW(4, 16);
+        } else if (vec == 2) {
+            if (gl == 4) DIGEST_NARROW(2, 4);
+            if (gl == 8) DIGEST_NARROW(2, 8);
+            DIGEST_NARROW(2, 16);
+        } else {
+            if (gl == 4) DIGEST_NARROW(1, 4);
+            if (gl == 8) DIGEST_NARROW(1, 8);
+            DIGEST_NARROW(1, 16);
+        }
+#undef DIGEST_NARROW
+    }
     const int max_nch = vec == 4 ? 2 : (vec == 2 ? 5 : 4);
     int nch = (dv + kWave - 1) / kWave;
     if (vec == 1 && nch == 3)
@@ -1084,25 +1317,41 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
     return hipGetLastError();
 }
 
-int32_t softmax_xent_blocks(int32_t n)
+// Lanes per row of the loss head: the class count rounded up to 8, 16 or 64.
+int loss_group(int32_t C) { return C <= 8 ? 8 : (C <= 16 ? 16 : 64); }
+
+int32_t softmax_xent_blocks(int32_t n, int32_t C)
 {
-    return (n + kLossRowsPerBlock - 1) / kLossRowsPerBlock;
+    const int32_t rows_per_block = (kLossThreads / kWave) * (kWave / loss_group(C));
+    return std::max<int32_t>(1, (n + rows_per_block - 1) / rows_per_block);
 }
 
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
                                int32_t C, float *dlogits, float *block_loss, float *loss,
                                hipStream_t s)
 {
-    const int32_t nb = softmax_xent_blocks(n);
+    if (C <= 0)
+        return hipErrorInvalidValue;
+    const int32_t nb = softmax_xent_blocks(n, C);
     const float inv_n = n > 0 ? 1.0f / (float)n : 0.f;
-    if (nb > 0) {
-        hipLaunchKernelGGL(k_softmax_xent, dim3((unsigned)nb), dim3(256), 0, s, logits, labels, n,
-                           C, inv_n, dlogits, block_loss);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess)
-            return e;
+    switch (loss_group(C)) {
+    case 8:
+        hipLaunchKernelGGL((k_softmax_xent<8>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
+                           logits, labels, n, C, inv_n, dlogits, block_loss);
+        break;
+    case 16:
+        hipLaunchKernelGGL((k_softmax_xent<16>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
+                           logits, labels, n, C, inv_n, dlogits, block_loss);
+        break;
+    default:
+        hipLaunchKernelGGL((k_softmax_xent<64>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
+                           logits, labels, n, C, inv_n, dlogits, block_loss);
+        break;
     }
-    hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(256), 0, s, block_loss, nb, inv_n, loss);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(kWave), 0, s, block_loss, nb, inv_n, loss);
     return hipGetLastError();
 }
 
@@ -1134,22 +1383,23 @@ hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int3
 {
     if (M <= 0 || N <= 0)
         return hipSuccess;
-    const int n4 = (N + 3) & ~3;
-    if (K <= 0 || K > kNarrow || (size_t)n4 * kNarrow * sizeof(float) > 64 * 1024)
+    if (K <= 0 || K > kNarrow)
         return hipErrorInvalidValue;
-    const int64_t threads = (int64_t)M * (n4 / 4);
-    if (threads >= INT32_MAX)
+    // per column slice: enough waves to give each at least kNarrowKRows
+    // rows, at most 4096 in all
+    const int64_t slices = (N + 255) / 256;
+    const int64_t row_groups = ((int64_t)M + kNarrowKRows - 1) / kNarrowKRows;
+    const int64_t per_slice = std::min<int64_t>(row_groups, std::max<int64_t>(1, 4096 / slices));
+    const int64_t blocks = (per_slice * slices + 3) / 4;   // the kernel idles any surplus wave
+    if (blocks * 4 * 64 > INT32_MAX)
         return hipErrorInvalidValue;
-    const int64_t blocks = std::min<int64_t>((threads + 255) / 256, 2048);
     const bool vec_out = N % 4 == 0 && ldc % 4 == 0 && ((uintptr_t)C % 16) == 0;
-    const int kk = K <= 8 ? 8 : 16;
-    const size_t lds = sizeof(float) * (size_t)n4 * kk;
-    if (kk == 8)
-        hipLaunchKernelGGL((k_narrow_k<8>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K, A,
-                           lda, W, C, ldc, vec_out);
+    if (K <= 8)
+        hipLaunchKernelGGL((k_narrow_k<8>), dim3((unsigned)blocks), dim3(256), 0, s, M, N, K, A,
+                           lda, W, C, ldc, vec_out, (int32_t)slices);
     else
-        hipLaunchKernelGGL((k_narrow_k<16>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K,
-                           A, lda, W, C, ldc, vec_out);
+        hipLaunchKernelGGL((k_narrow_k<16>), dim3((unsigned)blocks), dim3(256), 0, s, M, N, K, A,
+                           lda, W, C, ldc, vec_out, (int32_t)slices);
     return hipGetLastError();
 }
 

@@ -17,6 +17,8 @@ struct SpmmBlock {
 };
 
 constexpr int kSpmmThreads = 512;
+// Widest side handled by the narrow kernels.
+constexpr int kNarrow = 16;
 // Rows with more entries than this get a whole block.
 constexpr int32_t kSpmmLongRow = 64;
 
@@ -27,10 +29,22 @@ hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_
 // Two-source CSR aggregation out[r] = sum_k val[k] * src(col[k]) over the
 // rows named by the blocks.  Column c < n_src0 reads row c of src0,
 // otherwise row (c - n_src0) of src1.  Every named row is fully written.
-hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
-                       const int32_t *col, const float *val, const float *src0,
-                       const float *src1, int32_t n_src0, int32_t d, float *out,
-                       hipStream_t s);
+// Optional epilogue of a narrow aggregation (d <= kNarrow): rows r < rows
+// also get out2[r][n] = sum_k out[r][k] w[n][k] for n < n2, w row-major
+// [n2][d] (out times w^T).  Needs spmm_epilogue_ok(d, n2, out2).
+struct SpmmEpilogue {
+    const float *w;
+    int32_t rows, n2;
+    float *out2;
+};
+bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2);
+
+// The first n_long blocks are the long-row blocks (nrows == 0), the rest
+// short-row blocks.
+hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
+                       const int32_t *rowptr, const int32_t *col, const float *val,
+                       const float *src0, const float *src1, int32_t n_src0, int32_t d,
+                       float *out, hipStream_t s, const SpmmEpilogue *ep = nullptr);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
 // slices (each its own grid part) when splits > 1.
@@ -65,7 +79,6 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
                                 hipStream_t s);
 
 // Narrow dense products (VALU) for one side at most kNarrow wide.
-constexpr int kNarrow = 16;
 
 // C[r][n] = sum_k A(r)[k] B[k][n], n < N <= kNarrow, B row-major [K][N];
 // A(r) is row r of A0 for r < m0, else row r - m0 of A1 (leading dim lda);
@@ -85,8 +98,9 @@ hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const f
                             const float *H1, int32_t ldh, const float *G, int32_t chunk,
                             int32_t splits, float *part, hipStream_t s);
 
-// Row-wise softmax cross entropy; block_loss needs softmax_xent_blocks(n) floats.
-int32_t softmax_xent_blocks(int32_t n);
+// Row-wise softmax cross entropy and the mean loss; block_loss needs
+// softmax_xent_blocks(n, C) floats.
+int32_t softmax_xent_blocks(int32_t n, int32_t C);
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
                                int32_t C, float *dlogits, float *block_loss, float *loss,
                                hipStream_t s);
