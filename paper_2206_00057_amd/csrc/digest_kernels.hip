@@ -959,48 +959,13 @@ __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_
 
 constexpr int kLossThreads = 256;
 
-// Row-wise softmax cross entropy.  A row belongs to a group of GL lanes
-// (class c to lane c mod GL), so a wave holds 64/GL rows; each block writes
-// the sum of its rows' losses (in a fixed order) for k_loss_reduce.
-template <int GL>
-__global__ __launch_bounds__(kLossThreads) void k_softmax_xent(
-    const float *__restrict__ logits, const int32_t *__restrict__ labels, int32_t n, int32_t C,
-    float inv_n, float *__restrict__ dlogits, float *__restrict__ block_loss)
+// Block sum of the rows' losses into block_loss[blockIdx.x]: a butterfly
+// inside each wave, then the waves in order (a fixed order).
+__device__ __forceinline__ void loss_block_sum(float row_loss, float *__restrict__ block_loss)
 {
-    constexpr int G = kWave / GL;
     __shared__ float part[kLossThreads / kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x / kWave;
-    const int g = lane / GL, gl = lane % GL;
-    const int r = (blockIdx.x * (kLossThreads / kWave) + wid) * G + g;
-    float row_loss = 0.f;
-    if (r < n) {
-        const float *z = logits + (int64_t)r * C;
-        float *dz = dlogits + (int64_t)r * C;
-        const int y = labels[r];
-        const bool bad = y < 0 || y >= C;
-        float m = -INFINITY;
-        for (int c = gl; c < C; c += GL)
-            m = fmaxf(m, z[c]);
-#pragma unroll
-        for (int off = GL / 2; off > 0; off >>= 1)
-            m = fmaxf(m, __shfl_xor(m, off));
-        float sum = 0.f;
-        for (int c = gl; c < C; c += GL)
-            sum += expf(z[c] - m);
-#pragma unroll
-        for (int off = GL / 2; off > 0; off >>= 1)
-            sum += __shfl_xor(sum, off);
-        const float log_s = logf(sum);
-        for (int c = gl; c < C; c += GL) {
-            const float p = expf(z[c] - m - log_s);
-            dz[c] = bad ? 0.f : (p - (c == y ? 1.f : 0.f)) * inv_n;
-        }
-        const int ys = bad ? 0 : y;   // never index with a bad label
-        if (gl == 0)
-            row_loss = bad ? NAN : -(z[ys] - m - log_s);
-    }
-    // block sum: butterfly inside each wave, then the waves in order
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1)
         row_loss += __shfl_xor(row_loss, off);
@@ -1015,20 +980,123 @@ __global__ __launch_bounds__(kLossThreads) void k_softmax_xent(
     }
 }
 
-// loss = inv_n * sum of the block sums: one wave, lane j adding the block
-// sums j, j + 64, ... in order, then a butterfly (a fixed order).
+// loss = inv_n * sum of the block sums: one wave; lane j adds the block sums
+// j, j + 64, ... in order (loaded eight at a time), then a butterfly.
 __global__ __launch_bounds__(kWave) void k_loss_reduce(const float *__restrict__ block_loss,
                                                      int32_t nb, float inv_n,
                                                      float *__restrict__ loss)
 {
+    constexpr int U = 8;
     float t = 0.f;
-    for (int i = threadIdx.x; i < nb; i += kWave)
-        t += block_loss[i];
+    for (int i0 = threadIdx.x; i0 < nb; i0 += U * kWave) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kWave;
+            v[u] = i < nb ? block_loss[i] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            t += v[u];
+    }
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1)
         t += __shfl_xor(t, off);
     if (threadIdx.x == 0)
         loss[0] = t * inv_n;
+}
+
+// Row-wise softmax cross entropy.  A row belongs to a group of GL lanes;
+// lane gl of the group holds the classes gl, gl + GL, ... (NJ of them) in
+// registers, so each logit is read once; a wave holds 64/GL rows.
+template <int GL, int NJ>
+__global__ __launch_bounds__(kLossThreads) void k_softmax_xent(
+    const float *__restrict__ logits, const int32_t *__restrict__ labels, int32_t n, int32_t C,
+    float inv_n, float *__restrict__ dlogits, float *__restrict__ block_loss)
+{
+    constexpr int G = kWave / GL;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int g = lane / GL, gl = lane % GL;
+    const int r = (blockIdx.x * (kLossThreads / kWave) + threadIdx.x / kWave) * G + g;
+    float row_loss = 0.f;
+    if (r < n) {
+        const float *z = logits + (int64_t)r * C;
+        float *dz = dlogits + (int64_t)r * C;
+        const int y = labels[r];
+        const bool bad = y < 0 || y >= C;
+        float v[NJ];
+        float m = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int c = gl + j * GL;
+            v[j] = c < C ? z[c] : -INFINITY;
+            m = fmaxf(m, v[j]);
+        }
+#pragma unroll
+        for (int off = GL / 2; off > 0; off >>= 1)
+            m = fmaxf(m, __shfl_xor(m, off));
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            if (gl + j * GL < C)
+                sum += expf(v[j] - m);
+#pragma unroll
+        for (int off = GL / 2; off > 0; off >>= 1)
+            sum += __shfl_xor(sum, off);
+        const float log_s = logf(sum);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int c = gl + j * GL;
+            if (c < C) {
+                const float lp = v[j] - m - log_s;
+                dz[c] = bad ? 0.f : (expf(lp) - (c == y ? 1.f : 0.f)) * inv_n;
+                if (c == y)
+                    row_loss = -lp;
+            }
+        }
+        if (bad && gl == 0)
+            row_loss = NAN;
+    }
+    loss_block_sum(row_loss, block_loss);
+}
+
+// The same loss for any class count: a wave per row, lane c holding the
+// classes c, c + 64, ... read from memory in three passes.
+__global__ __launch_bounds__(kLossThreads) void k_softmax_xent_wide(
+    const float *__restrict__ logits, const int32_t *__restrict__ labels, int32_t n, int32_t C,
+    float inv_n, float *__restrict__ dlogits, float *__restrict__ block_loss)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int r = blockIdx.x * (kLossThreads / kWave) + threadIdx.x / kWave;
+    float row_loss = 0.f;
+    if (r < n) {
+        const float *z = logits + (int64_t)r * C;
+        float *dz = dlogits + (int64_t)r * C;
+        const int y = labels[r];
+        const bool bad = y < 0 || y >= C;
+        float m = -INFINITY;
+        for (int c = lane; c < C; c += kWave)
+            m = fmaxf(m, z[c]);
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1)
+            m = fmaxf(m, __shfl_xor(m, off));
+        float sum = 0.f;
+        for (int c = lane; c < C; c += kWave)
+            sum += expf(z[c] - m);
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1)
+            sum += __shfl_xor(sum, off);
+        const float log_s = logf(sum);
+        for (int c = lane; c < C; c += kWave) {
+            const float lp = z[c] - m - log_s;
+            dz[c] = bad ? 0.f : (expf(lp) - (c == y ? 1.f : 0.f)) * inv_n;
+            if (c == y)
+                row_loss = -lp;
+        }
+        if (bad && lane == 0)
+            row_loss = NAN;
+    }
+    loss_block_sum(row_loss, block_loss);
 }
 
 // ---------------------------------------------------------------------------
@@ -1317,8 +1385,11 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
     return hipGetLastError();
 }
 
-// Lanes per row of the loss head: the class count rounded up to 8, 16 or 64.
-int loss_group(int32_t C) { return C <= 8 ? 8 : (C <= 16 ? 16 : 64); }
+// Lanes per row of the loss head and class slots per lane: up to 128
+// classes every logit of a row sits in a register of its group; wider rows
+// take a wave each.
+int loss_group(int32_t C) { return C <= 8 ? 8 : (C <= 64 ? 16 : (C <= 128 ? 32 : 64)); }
+int loss_slots(int32_t C) { return (C + loss_group(C) - 1) / loss_group(C); }
 
 int32_t softmax_xent_blocks(int32_t n, int32_t C)
 {
@@ -1334,20 +1405,28 @@ hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32
         return hipErrorInvalidValue;
     const int32_t nb = softmax_xent_blocks(n, C);
     const float inv_n = n > 0 ? 1.0f / (float)n : 0.f;
-    switch (loss_group(C)) {
-    case 8:
-        hipLaunchKernelGGL((k_softmax_xent<8>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
+#define DIGEST_LOSS(GL, NJ)                                                                     \
+    hipLaunchKernelGGL((k_softmax_xent<GL, NJ>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,  \
+                       logits, labels, n, C, inv_n, dlogits, block_loss)
+    const int gl = loss_group(C), nj = loss_slots(C);
+    if (gl == 8)
+        DIGEST_LOSS(8, 1);
+    else if (gl == 16 && nj == 1)
+        DIGEST_LOSS(16, 1);
+    else if (gl == 16 && nj == 2)
+        DIGEST_LOSS(16, 2);
+    else if (gl == 16 && nj == 3)
+        DIGEST_LOSS(16, 3);
+    else if (gl == 16)
+        DIGEST_LOSS(16, 4);
+    else if (gl == 32 && nj == 3)
+        DIGEST_LOSS(32, 3);
+    else if (gl == 32)
+        DIGEST_LOSS(32, 4);
+    else
+        hipLaunchKernelGGL(k_softmax_xent_wide, dim3((unsigned)nb), dim3(kLossThreads), 0, s,
                            logits, labels, n, C, inv_n, dlogits, block_loss);
-        break;
-    case 16:
-        hipLaunchKernelGGL((k_softmax_xent<16>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
-                           logits, labels, n, C, inv_n, dlogits, block_loss);
-        break;
-    default:
-        hipLaunchKernelGGL((k_softmax_xent<64>), dim3((unsigned)nb), dim3(kLossThreads), 0, s,
-                           logits, labels, n, C, inv_n, dlogits, block_loss);
-        break;
-    }
+#undef DIGEST_LOSS
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;

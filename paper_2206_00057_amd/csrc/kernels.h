@@ -98,8 +98,8 @@ hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const f
                             const float *H1, int32_t ldh, const float *G, int32_t chunk,
                             int32_t splits, float *part, hipStream_t s);
 
-// Row-wise softmax cross entropy and the mean loss; block_loss needs
-// softmax_xent_blocks(n, C) floats.
+// Row-wise softmax cross entropy (C >= 1) and the mean loss; block_loss
+// needs softmax_xent_blocks(n, C) floats.
 int32_t softmax_xent_blocks(int32_t n, int32_t C);
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
                                int32_t C, float *dlogits, float *block_loss, float *loss,

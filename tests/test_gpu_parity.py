@@ -189,7 +189,9 @@ def test_tiny_layer(tiny, layer):
 
 
 def test_tiny_loss(tiny):
-    check_loss(tiny)
+    # repeated calls on one handle reuse its loss partials
+    for seed in (60, 62, 63):
+        check_loss(tiny, seed)
 
 
 def test_tiny_bad_label_gives_nan_and_zero_rows(tiny):
@@ -234,7 +236,7 @@ def test_determinism_bitwise(tiny):
 # ---------------------------------------------------------------------------
 
 WIDTHS = [(1, 1, 1), (3, 5, 2), (7, 41, 47), (602, 47, 7), (100, 256, 41), (64, 64, 16),
-          (33, 130, 9), (500, 256, 7)]
+          (33, 130, 9), (500, 256, 7), (16, 24, 70), (20, 40, 100), (8, 12, 130)]
 
 
 @pytest.mark.parametrize("widths", WIDTHS, ids=lambda w: "x".join(map(str, w)))
