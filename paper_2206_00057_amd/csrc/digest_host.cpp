@@ -76,13 +76,14 @@ void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchu
 }
 
 // Workgroup tile of C for a GEMM (see GemmArgs::tile): 64x64 keeps enough
-// workgroups for the partition-sized products; very tall forward products
-// and long split-K contractions run slightly faster on larger tiles.
+// workgroups for the partition-sized products and for every split-K weight
+// gradient; tall products (>= 20,000 rows) run faster on 128x128 tiles,
+// whose waves each own a 64x64 block (one LDS fragment read per MFMA).
 int32_t gemm_tile_for(int64_t M, int64_t N, int64_t K, bool contraction_over_rows)
 {
     if (contraction_over_rows)
-        return (K >= 100000 && M >= 128) ? 2 : 0;
-    return (M >= 100000 && N >= 128) ? 3 : 0;
+        return 0;
+    return (M >= 20000 && N >= 128) ? 3 : 0;
 }
 
 // Aggregation blocks of a CSR: every long row gets a block of its own (those

@@ -627,8 +627,6 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
             }
         }
     };
-    // All fragment reads of a K step are issued before its MFMAs, so LDS
-    // latency is paid once per step instead of once per MFMA.
     auto compute = [&](int buf) {
         float fa[BK / 2][TM], fb[BK / 2][TN];
 #pragma unroll
@@ -640,7 +638,6 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
             for (int j = 0; j < TN; ++j)
                 fb[st][j] = Bs[buf][2 * st + (lane >> 5)][wn + 32 * j + (lane & 31)];
         }
-        __builtin_amdgcn_sched_barrier(0);   // keep every read ahead of the MFMAs
 #pragma unroll
         for (int st = 0; st < BK / 2; ++st)
 #pragma unroll
