@@ -37,6 +37,11 @@ def transform_first(l, widths):
     return l == len(widths) - 1 and 4 * widths[l] <= widths[l - 1]
 
 
+def loss_group(C):
+    """Mirror of the library's lanes per row of the loss head."""
+    return 8 if C <= 8 else (16 if C <= 64 else (32 if C <= 128 else 64))
+
+
 def splitk(M, N, K):
     """Mirror of the library's split-K plan: (splits, rows per split)."""
     tiles = -(-M // 64) * -(-N // 64)
@@ -100,6 +105,7 @@ def launch_model(st, widths):
             put("gemm_dgrad", l, 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
                 2.0 * n * di * do)
     put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
+    put("loss_mean", L, 4 * -(-n // (4 * (64 // loss_group(widths[-1])))) + 4)
     for lev in range(L):
         put("pull_gather", lev, 8.0 * nh * widths[lev] + 4 * nh)
     for lev in range(1, L):
@@ -168,6 +174,8 @@ def main():
     ap.add_argument("--config", default="medium")
     ap.add_argument("--sync", type=int, default=0, help="sync interval (default: the workload's)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graph replay")
+    ap.add_argument("--overlap-io", action="store_true",
+                    help="pulls and pushes on a second stream next to the layers")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
@@ -203,7 +211,7 @@ def main():
     stores = [dX] + [full.H[l].clone() for l in range(1, L)]
     del full
     torch.cuda.synchronize()
-    gp = step.GpuPartition(g.n, part, cfg.widths)
+    gp = step.GpuPartition(g.n, part, cfg.widths, overlap_io=args.overlap_io)
     x_own = dev(X[part.owned])
     gp.pull_all(stores)
     if args.calibration_copy_mib:
@@ -287,6 +295,7 @@ def main():
             "n_boundary": st["n_boundary"], "nnz": st["nnz"], "nnz_in": st["nnz_in"],
             "widths": list(cfg.widths), "sync_interval": K, "edges_per_step": edges,
             "launch": "eager" if args.eager else "hip-graph replay",
+            "pull_push": "overlapped on a second stream" if args.overlap_io else "in line",
         },
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -42,11 +42,12 @@ enum Kind : int32_t {
     K_GEMM_DH,
     K_SPMM_BWD,
     K_LOSS,
+    K_LOSS_MEAN,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "pull_gather", "push_scatter", "spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
-    "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent"};
+    "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent", "loss_mean"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -933,11 +934,17 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
     if (!loss || (p->n_own > 0 && (!logits || !labels || !dlogits)))
         return fail(DIGEST_EINVAL, "NULL logits, labels, dlogits or loss");
     hipStream_t s = (hipStream_t)hip_stream;
-    Timed t(p, K_LOSS, p->L, s);
-    return hip_check(digest::launch_softmax_xent(logits, labels, p->n_own, p->widths[p->L],
-                                                 dlogits, p->at<float>(p->lay.loss_part), loss,
-                                                 s),
-                     "softmax xent");
+    const int32_t C = p->widths[p->L];
+    float *part = p->at<float>(p->lay.loss_part);
+    {
+        Timed t(p, K_LOSS, p->L, s);
+        if (digest_status st = hip_check(
+                digest::launch_softmax_xent(logits, labels, p->n_own, C, dlogits, part, s),
+                "softmax xent"))
+            return st;
+    }
+    Timed t(p, K_LOSS_MEAN, p->L, s);
+    return hip_check(digest::launch_loss_mean(part, p->n_own, C, loss, s), "loss mean");
 }
 
 digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull, int32_t *do_push)

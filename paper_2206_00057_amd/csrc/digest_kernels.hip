@@ -1395,8 +1395,7 @@ int32_t softmax_xent_blocks(int32_t n, int32_t C)
 }
 
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
-                               int32_t C, float *dlogits, float *block_loss, float *loss,
-                               hipStream_t s)
+                               int32_t C, float *dlogits, float *block_loss, hipStream_t s)
 {
     if (C <= 0)
         return hipErrorInvalidValue;
@@ -1424,9 +1423,16 @@ hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32
         hipLaunchKernelGGL(k_softmax_xent_wide, dim3((unsigned)nb), dim3(kLossThreads), 0, s,
                            logits, labels, n, C, inv_n, dlogits, block_loss);
 #undef DIGEST_LOSS
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
+    return hipGetLastError();
+}
+
+hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float *loss,
+                            hipStream_t s)
+{
+    if (C <= 0)
+        return hipErrorInvalidValue;
+    const int32_t nb = softmax_xent_blocks(n, C);
+    const float inv_n = n > 0 ? 1.0f / (float)n : 0.f;
     hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(kWave), 0, s, block_loss, nb, inv_n, loss);
     return hipGetLastError();
 }

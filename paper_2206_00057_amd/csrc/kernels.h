@@ -98,12 +98,14 @@ hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const f
                             const float *H1, int32_t ldh, const float *G, int32_t chunk,
                             int32_t splits, float *part, hipStream_t s);
 
-// Row-wise softmax cross entropy (C >= 1) and the mean loss; block_loss
-// needs softmax_xent_blocks(n, C) floats.
+// Row-wise softmax cross entropy (C >= 1): dlogits and the per-block loss
+// sums (softmax_xent_blocks(n, C) floats); launch_loss_mean then writes
+// their mean over the n rows.
 int32_t softmax_xent_blocks(int32_t n, int32_t C);
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
-                               int32_t C, float *dlogits, float *block_loss, float *loss,
-                               hipStream_t s);
+                               int32_t C, float *dlogits, float *block_loss, hipStream_t s);
+hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float *loss,
+                            hipStream_t s);
 
 // GEMM K step; the smallest workgroup tile of C is kGemmBM x kGemmBN.
 constexpr int kGemmBM = 64;

@@ -8,7 +8,14 @@ library calls (Algorithm 1's inner loop for a single subgraph):
     for l = L..1:   layer backward
 
 All arithmetic runs in libdigest.so; this module only owns the device
-buffers (PyTorch tensors) and orders the calls on one stream.  ``capture``
+buffers (PyTorch tensors) and orders the calls.  With overlap_io, pulls and
+pushes run on a second stream next to the layer computation, as the paper's
+system design overlaps representation I/O with the forward pass (Sec. 3.2):
+a pull of level l-1 only has to finish before layer l starts, and a push of
+level l only has to start after layer l.  With the store in the same HBM as
+the layers' operands both sides are bandwidth-bound and the overlap does not
+shorten a round, so the default keeps them in line on the caller's stream.
+``capture``
 records the round into a HIP graph (one graph per distinct pull/push
 pattern of the schedule) so that replays cost one launch.
 """
@@ -20,7 +27,7 @@ from . import digest as D
 
 
 class GpuPartition:
-    def __init__(self, n_global, part, widths, device="cuda"):
+    def __init__(self, n_global, part, widths, device="cuda", overlap_io=False):
         self.widths = [int(w) for w in widths]
         self.L = len(self.widths) - 1
         self.device = device
@@ -39,6 +46,11 @@ class GpuPartition:
                             for l in range(1, self.L + 1)]
         self.loss = torch.zeros(1, **f32)
         self.graphs = {}
+        # pulls and pushes: on their own stream (default priority) next to the
+        # layers, or in line on the caller's stream
+        self.overlap_io = overlap_io
+        self.io = torch.cuda.Stream(device=device) if overlap_io else None
+        self.pull_done = [torch.cuda.Event() for _ in range(self.L)]
 
     def act(self, layer):
         return D.ACT_RELU if layer < self.L else D.ACT_IDENTITY
@@ -50,6 +62,32 @@ class GpuPartition:
 
     def forward(self, x_own, Ws, stores=None, do_pull=False, do_push=False):
         self.x_own = x_own
+        if not self.overlap_io:
+            return self._forward_in_line(x_own, Ws, stores, do_pull, do_push)
+        main = torch.cuda.current_stream()
+        pulled = do_pull and self.L >= 2
+        if pulled:
+            # every scheduled pull starts now, on the I/O stream
+            self.io.wait_stream(main)
+            with torch.cuda.stream(self.io):
+                for lev in range(1, self.L):
+                    D.digest_pull(self.p, lev, stores[lev], stream=self.io)
+                    self.pull_done[lev].record(self.io)
+        h = x_own
+        for l in range(1, self.L + 1):
+            if pulled and l >= 2:
+                main.wait_event(self.pull_done[l - 1])
+            D.digest_layer_forward(self.p, l, h, Ws[l - 1], self.H[l], self.act(l))
+            if do_push and l <= self.L - 1:
+                self.io.wait_stream(main)
+                with torch.cuda.stream(self.io):
+                    D.digest_push(self.p, l, self.H[l], stores[l], stream=self.io)
+            h = self.H[l]
+        if pulled or do_push:
+            main.wait_stream(self.io)
+        return self.H[self.L]
+
+    def _forward_in_line(self, x_own, Ws, stores, do_pull, do_push):
         h = x_own
         for l in range(1, self.L + 1):
             if do_pull and l >= 2:

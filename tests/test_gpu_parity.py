@@ -356,8 +356,9 @@ def _full_forward_oracle(g, X, Ws, L):
     return hs
 
 
+@pytest.mark.parametrize("overlap_io", [False, True], ids=["in-line-io", "overlapped-io"])
 @pytest.mark.parametrize("K", [1, 5])
-def test_rounds_of_algorithm1(tiny_graph, K):
+def test_rounds_of_algorithm1(tiny_graph, K, overlap_io):
     """Each side runs its own rounds: the other partitions are played by a
     full-graph forward at the current weights whose boundary rows are pushed
     at every push round; the partition itself pulls/pushes per the schedule
@@ -377,7 +378,7 @@ def test_rounds_of_algorithm1(tiny_graph, K):
     g_stores = [dev(X)] + [dev(init[l]) for l in range(1, L)]
     op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
                                 part.halo, cfg.widths)
-    gp = step.GpuPartition(g.n, part, cfg.widths)
+    gp = step.GpuPartition(g.n, part, cfg.widths, overlap_io=overlap_io)
     for lev in range(L):
         op.pull(lev, o_stores[lev])
     gp.pull_all(g_stores)
@@ -435,7 +436,8 @@ def test_rounds_of_algorithm1(tiny_graph, K):
             gW[l].sub_(lr * gp.dW[l + 1])
 
 
-def test_graph_replay_matches_eager(tiny_graph):
+@pytest.mark.parametrize("overlap_io", [False, True], ids=["in-line-io", "overlapped-io"])
+def test_graph_replay_matches_eager(tiny_graph, overlap_io):
     from paper_2206_00057_amd import step
     cfg, g = tiny_graph
     part = synth.make_partition(cfg, g, 1)
@@ -446,7 +448,7 @@ def test_graph_replay_matches_eager(tiny_graph):
     Ws = [dev(w) for w in synth.weights(cfg)]
     y = dev(synth.labels(cfg)[part.owned])
     x = dev(X[part.owned])
-    gp = step.GpuPartition(g.n, part, cfg.widths)
+    gp = step.GpuPartition(g.n, part, cfg.widths, overlap_io=overlap_io)
     gp.pull_all(stores)
     K = 3
     eager = {}
@@ -485,7 +487,7 @@ def test_profile_instrumentation(tiny_graph):
     assert prof["spmm_fwd.l1"][1] == 1 and prof["spmm_fwd.l2"][1] == 1
     assert prof["gemm_fwd_relu.l1"][1] == 1 and prof["gemm_fwd_relu.l2"][1] == 1
     assert prof["pull_gather.l1"][1] == 1 and prof["push_scatter.l1"][1] == 1
-    assert prof["softmax_xent.l2"][1] == 1
+    assert prof["softmax_xent.l2"][1] == 1 and prof["loss_mean.l2"][1] == 1
     assert prof["gemm_dw_splitk.l1"][1] == 1 and prof["gemm_dw_splitk.l2"][1] == 1
     assert prof["spmm_bwd_transposed.l2"][1] == 1 and "spmm_bwd_transposed.l1" not in prof
     assert all(ms >= 0 for ms, _ in prof.values())
