@@ -977,19 +977,23 @@ __device__ __forceinline__ void loss_block_sum(float row_loss, float *__restrict
     }
 }
 
-// loss = inv_n * sum of the block sums: one wave; lane j adds the block sums
-// j, j + 64, ... in order (loaded eight at a time), then a butterfly.
-__global__ __launch_bounds__(kWave) void k_loss_reduce(const float *__restrict__ block_loss,
-                                                     int32_t nb, float inv_n,
-                                                     float *__restrict__ loss)
+// loss = inv_n * sum of the block sums, in a fixed order: thread j of one
+// kLossReduceThreads block adds the block sums j, j + T, ... (loaded eight at
+// a time), then the threads' sums are added by a butterfly inside each wave
+// and the waves' in wave order.
+constexpr int kLossReduceThreads = 1024;
+
+__global__ __launch_bounds__(kLossReduceThreads) void k_loss_reduce(
+    const float *__restrict__ block_loss, int32_t nb, float inv_n, float *__restrict__ loss)
 {
-    constexpr int U = 8;
+    constexpr int U = 8, T = kLossReduceThreads;
+    __shared__ float part[T / kWave];
     float t = 0.f;
-    for (int i0 = threadIdx.x; i0 < nb; i0 += U * kWave) {
+    for (int i0 = threadIdx.x; i0 < nb; i0 += U * T) {
         float v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int i = i0 + u * kWave;
+            const int i = i0 + u * T;
             v[u] = i < nb ? block_loss[i] : 0.f;
         }
 #pragma unroll
@@ -999,8 +1003,15 @@ __global__ __launch_bounds__(kWave) void k_loss_reduce(const float *__restrict__
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1)
         t += __shfl_xor(t, off);
-    if (threadIdx.x == 0)
-        loss[0] = t * inv_n;
+    if ((threadIdx.x & (kWave - 1)) == 0)
+        part[threadIdx.x / kWave] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float sum = 0.f;
+        for (int w = 0; w < T / kWave; ++w)
+            sum += part[w];
+        loss[0] = sum * inv_n;
+    }
 }
 
 // Row-wise softmax cross entropy.  A row belongs to a group of GL lanes;
@@ -1433,7 +1444,8 @@ hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float
         return hipErrorInvalidValue;
     const int32_t nb = softmax_xent_blocks(n, C);
     const float inv_n = n > 0 ? 1.0f / (float)n : 0.f;
-    hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(kWave), 0, s, block_loss, nb, inv_n, loss);
+    hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(kLossReduceThreads), 0, s, block_loss, nb,
+                       inv_n, loss);
     return hipGetLastError();
 }
 
