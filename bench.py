@@ -32,9 +32,20 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 
 
-def transform_first(l, widths):
-    """Mirror of the library's choice: identity layers at least 4x narrowing."""
-    return l == len(widths) - 1 and 4 * widths[l] <= widths[l - 1]
+def transform_first(l, widths, st):
+    """Mirror of the library's choice for the identity (last) layer: the
+    cheaper order under its cost model of gathered bytes and GEMM flops."""
+    if l != len(widths) - 1:
+        return False
+    di, do = widths[l - 1], widths[l]
+    n, R, nnz, nnz_in = st["n_own"], st["n_own"] + st["n_halo"], st["nnz"], st["nnz_in"]
+    gather, flops = 7.0e12, 80.0e12
+    dgrad = l > 1
+    af = ((nnz * di + (nnz_in * min(di, do) if dgrad else 0)) * 4.0 / gather
+          + 2.0 * n * di * do * (3.0 if dgrad else 2.0) / flops)
+    tf = (2.0 * nnz * do * 4.0 / gather
+          + (4.0 * R * di * do + (2.0 * n * di * do if dgrad else 0.0)) / flops)
+    return tf < af
 
 
 def loss_group(C):
@@ -79,7 +90,7 @@ def launch_model(st, widths):
     for l in range(1, L + 1):
         di, do = widths[l - 1], widths[l]
         relu = l < L
-        if transform_first(l, widths):
+        if transform_first(l, widths, st):
             R = n + nh
             put("gemm_fwd_relu", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
             put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)

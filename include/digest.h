@@ -162,12 +162,15 @@ digest_status digest_push(digest_partition *p, int32_t level, const float *h_own
  *   act    DIGEST_ACT_RELU or DIGEST_ACT_IDENTITY (the paper uses ReLU on
  *          hidden layers and raw logits at the last layer).
  * Order of the two products (the same result up to float rounding): a
- * layer with the identity activation whose output is at least 4x narrower
- * than its input is computed transform-first, T = [h_in; halo] W over all
- * n_owned + n_halo local rows, then h_out = P_m T, so that the sparse
- * aggregation runs at the narrow width; every other layer aggregates first,
- * AH = P_m [h_in; halo], then h_out = act(AH W), keeping AH in the
- * workspace for the backward.
+ * layer with the identity activation is computed transform-first,
+ * T = [h_in; halo] W over all n_owned + n_halo local rows, then
+ * h_out = P_m T, when a cost model of the layer's forward and backward says
+ * that is cheaper: it weighs the gathered bytes of the sparse aggregations
+ * (nnz rows at width d_out twice, against nnz rows at width d_in plus the
+ * input-gradient aggregation) and the GEMM flops (over n_owned + n_halo rows
+ * against n_owned rows) at measured MI355X rates.  Every other layer
+ * aggregates first, AH = P_m [h_in; halo], then h_out = act(AH W), keeping AH
+ * in the workspace for the backward.
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace, or level layer-1 never
  * pulled while the partition has halo nodes), DIGEST_EHIP.
  */

@@ -166,11 +166,31 @@ struct digest_partition {
 
 namespace {
 
-// A layer whose output is at least 4x narrower than its input: with the
-// identity activation it runs transform-first, Z = P_m ([H_in; H~_out] W),
-// aggregating at the narrow width (the same product, associated the other
-// way).
-bool narrow_layer(int64_t d_in, int64_t d_out) { return 4 * d_out <= d_in; }
+// Order of the two products of a layer with the identity activation (the
+// same result, associated the other way).  Aggregate-first gathers nnz rows
+// of width d_in (and, for layers > 1, nnz_in rows of width min(d_in, d_out)
+// for the input gradient) and multiplies the n_own aggregated rows;
+// transform-first, Z = P_m ([H_in; H~_out] W), multiplies all n_own + n_halo
+// local rows and gathers 2 nnz rows of width d_out (P_m and P_m^T).  The
+// rates are those measured for the aggregation kernels (random row gathers)
+// and the fp32 MFMA GEMM on MI355X.
+constexpr double kGatherBytesPerS = 7.0e12;
+constexpr double kGemmFlopsPerS = 80.0e12;
+
+bool transform_first_cheaper(const digest_partition &p, int32_t layer)
+{
+    const double di = p.widths[layer - 1], dout = p.widths[layer];
+    const double n = p.n_own, R = (double)p.n_own + (double)p.n_halo;
+    const bool dgrad = layer > 1;
+    const double af =
+        ((double)p.nnz * di + (dgrad ? (double)p.nnz_in * std::min(di, dout) : 0.0)) * 4.0 /
+            kGatherBytesPerS +
+        2.0 * n * di * dout * (dgrad ? 3.0 : 2.0) / kGemmFlopsPerS;
+    const double tf = 2.0 * (double)p.nnz * dout * 4.0 / kGatherBytesPerS +
+                      (4.0 * R * di * dout + (dgrad ? 2.0 * n * di * dout : 0.0)) /
+                          kGemmFlopsPerS;
+    return tf < af;
+}
 
 // The kernels for a narrow side (<= kNarrow columns); the dgrad one stages
 // W (d_in x 16 floats) in LDS, which bounds d_in.
@@ -247,7 +267,7 @@ void plan_layout(digest_partition &p)
         splitk_plan(di, dout, p.n_own, splits, kchunk);
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
-        if (narrow_layer(di, dout)) {
+        if (transform_first_cheaper(p, k)) {
             tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + p.n_halo) * dout);
             const TfPlan t = tf_plan(p.n_own, p.n_halo, di, dout);
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
@@ -664,7 +684,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
     hipStream_t s = (hipStream_t)hip_stream;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
-    const bool tf = act == DIGEST_ACT_IDENTITY && narrow_layer(d_in, d_out);
+    const bool tf = act == DIGEST_ACT_IDENTITY && transform_first_cheaper(*p, layer);
     if (p->n_own > 0 && tf) {
         // T = [h_in; halo] W over all local rows, then h_out = P_m T.
         float *T = p->at<float>(p->lay.tbuf);
