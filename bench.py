@@ -177,6 +177,55 @@ def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
     return rounds, time.perf_counter() - t0, oracle.num_threads()
 
 
+def train_bench(args):
+    """Algorithm 1 over every subgraph of the workload's graph on this GPU:
+    whole rounds (all subgraphs' forward, loss and backward, scheduled
+    pulls/pushes, parameter averaging) replayed from HIP graphs."""
+    import torch
+
+    from paper_2206_00057_amd import synth
+    from paper_2206_00057_amd.train import DigestTrainer
+
+    cfg = synth.CONFIGS[args.config]
+    K = args.sync or cfg.sync_periods[-1 if args.config == "halo" else 0]
+    t0 = time.time()
+    g = synth.make_graph(cfg)
+    M = synth.num_partitions(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(M)]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
+    tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws],
+                       args.lr, K)
+    print(f"[bench] training {cfg.name}: {M} subgraphs, inputs {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    tr.init_stores()
+    tr.capture()
+    for r in range(1, args.warmup + 1):
+        tr.replay(r)
+    torch.cuda.synchronize()
+    first_loss = tr.mean_loss()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for r in range(args.warmup + 1, args.warmup + args.steps + 1):
+        tr.replay(r)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    out = {
+        "metric": "DIGEST training GTEPS, all subgraphs of the graph on one GPU",
+        "value": round(tr.edges_per_round * args.steps / (ms * 1e-3) / 1e9, 4), "unit": "GTEPS",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms / args.steps, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: all {M} subgraphs, Algorithm 1 rounds with "
+                               f"sync interval {K}, SGD lr {args.lr}",
+                   "n_global": g.n, "subgraphs": M, "widths": list(cfg.widths),
+                   "edges_per_round": tr.edges_per_round, "launch": "hip-graph replay"},
+        "loss": {"after_warmup": round(first_loss, 6), "last": round(tr.mean_loss(), 6)},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,11 +241,17 @@ def main():
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="before the rounds, copy a float32 buffer of this many MiB once "
                          "(a plain copy kernel of known size for counter calibration)")
+    ap.add_argument("--train", action="store_true",
+                    help="Algorithm 1 rounds over every subgraph of the graph instead of one")
+    ap.add_argument("--lr", type=float, default=0.1, help="SGD learning rate for --train")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one partition on one GPU; runs on more than one GPU are not "
               "part of this build (--gpus 1).", file=sys.stderr)
         sys.exit(2)
+
+    if args.train:
+        return train_bench(args)
 
     import torch
 

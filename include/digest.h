@@ -211,6 +211,23 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
                                   void *hip_stream);
 
 /*
+ * Global parameter update of Algorithm 1 (AGG): each of the M subgraphs
+ * took one local SGD step from the same global parameters, W_m = W -
+ * lr * grad_m, and the new global parameters are their average (the
+ * convergence analysis of Appendix A.3 averages the local gradients):
+ *   w[e] <- w[e] - lr * (1/M) * sum_{m < M} grads[m][e]   for e < count,
+ * the sum taken in m order (deterministic).
+ *   w      device, count floats (updated in place).
+ *   grads  HOST array of M device pointers, each to count floats (e.g. the
+ *          dw of one subgraph's digest_layer_backward); not modified.
+ *   n_grads M, 1 <= M <= 64.   count >= 0.
+ * Not tied to a partition handle; enqueued on hip_stream.
+ * Errors: DIGEST_EINVAL (M out of range, negative count, NULL), DIGEST_EHIP.
+ */
+digest_status digest_sgd_average(float *w, const float *const *grads, int32_t n_grads,
+                                 int64_t count, float lr, void *hip_stream);
+
+/*
  * Synchronisation schedule of Algorithm 1 (pure, host only): in round
  * iter (1-based) with interval K >= 1, *do_pull = (iter mod K == 0) and
  * *do_push = ((iter-1) mod K == 0); both apply to levels 1..L-1.

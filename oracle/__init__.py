@@ -77,6 +77,8 @@ def _load():
                                                   ctypes.c_int, P, P]
             lib.oracle_sync_period.argtypes = [i32, i64, ctypes.POINTER(i32), ctypes.POINTER(i32)]
             lib.oracle_sync_period.restype = ctypes.c_int
+            lib.oracle_sgd_average.argtypes = [P, P, i32, i64, f32]
+            lib.oracle_sgd_average.restype = ctypes.c_int
             del f32
             _lib = lib
     return _lib
@@ -224,6 +226,21 @@ def sync_period(K, r):
     return bool(a.value), bool(b.value)
 
 
+def sgd_average(w, grads, lr):
+    """Algorithm 1's global update (AGG): the average of the M local models
+    ``w - lr * grads[m]``; returns the new float32 ``w``."""
+    w = _c(w, np.float32).copy()
+    gs = [_c(g, np.float32) for g in grads]
+    for g in gs:
+        if g.shape != w.shape:
+            raise OracleError("gradient shape differs from the parameter's")
+    ptrs = (ctypes.c_void_p * max(len(gs), 1))(*[g.ctypes.data for g in gs])
+    rc = _load().oracle_sgd_average(_p(w), ptrs, len(gs), w.size, float(lr))
+    if rc != 0:
+        raise OracleError("need at least one gradient")
+    return w
+
+
 class OraclePartition:
     """One partition's state, mirroring the library's call sequence.
 
@@ -276,3 +293,73 @@ class OraclePartition:
         return layer_backward(self.indptr, self.col_local, self.values, h_in,
                               self.halo_buf.get(layer - 1), w, h_out, dh_out, act,
                               want_dh_in=want_dh_in)
+
+
+class OracleTrainer:
+    """Algorithm 1 (synchronous mode) over every subgraph, one after another
+    at each layer: in round r every subgraph starts from the global W; for
+    each layer l, if r mod K == 0 and l >= 2 every subgraph pulls level l-1,
+    then every subgraph computes layer l, then, if (r-1) mod K == 0 and
+    l < L, every subgraph pushes level l; then every subgraph computes its
+    local loss (Eq. 3) and gradients, and AGG averages the M locally updated
+    models.  ``parts`` carry owned / halo / CSR rows (global columns)."""
+
+    def __init__(self, n_global, parts, widths, X, labels, Ws, lr, K):
+        self.widths = [int(x) for x in widths]
+        self.L = len(self.widths) - 1
+        self.lr, self.K = float(lr), int(K)
+        self.ops = [OraclePartition(n_global, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                    widths) for p in parts]
+        self.X = _c(X, np.float32)
+        self.x_own = [self.X[p.owned] for p in parts]
+        self.y_own = [_c(labels, np.int32)[p.owned] for p in parts]
+        self.W = [_c(w, np.float32).copy() for w in Ws]
+        self.stores = [self.X] + [np.zeros((int(n_global), self.widths[l]), np.float32)
+                                  for l in range(1, self.L)]
+        self.logits = [None] * len(parts)
+        self.losses = [None] * len(parts)
+
+    def act(self, layer):
+        return RELU if layer < self.L else IDENTITY
+
+    def init_stores(self):
+        """One forward of every subgraph at the current W, pulling before and
+        pushing after every layer, then every halo level pulled."""
+        for op in self.ops:
+            op.pull(0, self.stores[0])
+        h = list(self.x_own)
+        for l in range(1, self.L):
+            if l >= 2:
+                for op in self.ops:
+                    op.pull(l - 1, self.stores[l - 1])
+            h = [op.forward(l, h[m], self.W[l - 1], self.act(l)) for m, op in enumerate(self.ops)]
+            for m, op in enumerate(self.ops):
+                self.stores[l] = op.push(l, h[m], self.stores[l])
+        for op in self.ops:
+            for lev in range(1, self.L):
+                op.pull(lev, self.stores[lev])
+
+    def round(self, r):
+        do_pull, do_push = sync_period(self.K, r)
+        outs = [[None] * (self.L + 1) for _ in self.ops]
+        for m in range(len(self.ops)):
+            outs[m][0] = self.x_own[m]
+        for l in range(1, self.L + 1):
+            if do_pull and l >= 2:
+                for op in self.ops:
+                    op.pull(l - 1, self.stores[l - 1])
+            for m, op in enumerate(self.ops):
+                outs[m][l] = op.forward(l, outs[m][l - 1], self.W[l - 1], self.act(l))
+            if do_push and l <= self.L - 1:
+                for m, op in enumerate(self.ops):
+                    self.stores[l] = op.push(l, outs[m][l], self.stores[l])
+        grads = [[None] * len(self.ops) for _ in range(self.L)]
+        for m, op in enumerate(self.ops):
+            self.logits[m] = outs[m][self.L]
+            self.losses[m], dh = softmax_xent(outs[m][self.L], self.y_own[m])
+            for l in range(self.L, 0, -1):
+                grads[l - 1][m], dh = op.backward(l, outs[m][l - 1], self.W[l - 1], outs[m][l],
+                                                  dh, self.act(l), want_dh_in=l > 1)
+        self.W = [sgd_average(self.W[l], grads[l], self.lr) for l in range(self.L)]
+        return float(np.mean(self.losses))
+

@@ -22,7 +22,11 @@
  *   - the layer backward by the chain rule (Sec. 3.1 Eq. 6 and the GCN
  *     backward of Appendix A.3), with the stale halo rows held constant;
  *   - the synchronisation schedule of Algorithm 1 (pull when r mod N == 0,
- *     push when (r-1) mod N == 0, for layers other than the last).
+ *     push when (r-1) mod N == 0, for layers other than the last);
+ *   - the global parameter update of Algorithm 1 (AGG of the M locally
+ *     updated models; each took one SGD step from the same global W, so
+ *     the average is W minus the learning rate times the mean gradient,
+ *     as the convergence proof of Appendix A.3 averages local gradients).
  *
  * Precision: every sum is accumulated in double; a value is rounded to float
  * only where a tensor is written out (AH, H_out, dW, dH_in, dlogits).
@@ -385,3 +389,24 @@ int oracle_sync_period(int32_t K, int64_t r, int32_t *do_pull, int32_t *do_push)
     *do_push = ((r - 1) % K) == 0;
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Global parameter update (Algorithm 1, AGG)                               */
+/* ------------------------------------------------------------------------ */
+
+/* w[e] <- w[e] - lr * (1/M) * sum_m grads[m][e] for e < count: the average of
+ * the M local models W - lr * grad_m.  The sum runs over m in order, in
+ * double.  Returns -1 for M < 1. */
+int oracle_sgd_average(float *w, const float *const *grads, int32_t M, int64_t count, float lr)
+{
+    if (M < 1)
+        return -1;
+    for (int64_t e = 0; e < count; ++e) {
+        double g = 0.0;
+        for (int32_t m = 0; m < M; ++m)
+            g += (double)grads[m][e];
+        w[e] = (float)((double)w[e] - (double)lr * (g / (double)M));
+    }
+    return 0;
+}
+

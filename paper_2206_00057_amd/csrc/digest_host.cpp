@@ -967,6 +967,27 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
     return hip_check(digest::launch_loss_mean(part, p->n_own, C, loss, s), "loss mean");
 }
 
+digest_status digest_sgd_average(float *w, const float *const *grads, int32_t n_grads,
+                                 int64_t count, float lr, void *hip_stream)
+{
+    if (n_grads < 1 || n_grads > digest::kMaxAverage)
+        return fail(DIGEST_EINVAL, "need 1 <= n_grads <= %d, got %d", digest::kMaxAverage,
+                    n_grads);
+    if (count < 0)
+        return fail(DIGEST_EINVAL, "negative count");
+    if (count > 0 && (!w || !grads))
+        return fail(DIGEST_EINVAL, "NULL w or grads");
+    digest::GradList g{};
+    for (int32_t m = 0; m < n_grads && count > 0; ++m) {
+        if (!grads[m])
+            return fail(DIGEST_EINVAL, "grads[%d] is NULL", m);
+        g.g[m] = grads[m];
+    }
+    return hip_check(digest::launch_sgd_average(w, g, n_grads, count, lr,
+                                                (hipStream_t)hip_stream),
+                     "sgd average");
+}
+
 digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull, int32_t *do_push)
 {
     if (K < 1 || iter < 1 || !do_pull || !do_push)

@@ -21,6 +21,8 @@
 //   k_narrow_n / k_narrow_k / k_dw_narrow  products with one side at most
 //                  16 wide (the transform-first last layer).
 //   k_softmax_xent / k_loss_reduce  the mean cross-entropy loss head.
+//   k_sgd_average  Algorithm 1's global update: the average of the M
+//                  locally updated models, W - lr * mean of the gradients.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -1108,6 +1110,24 @@ __global__ __launch_bounds__(kLossThreads) void k_softmax_xent_wide(
 }
 
 // ---------------------------------------------------------------------------
+// Global parameter update
+// ---------------------------------------------------------------------------
+
+// w[e] -= lr * (1/n) * sum over m of g.g[m][e], m ascending; a thread per
+// element.
+__global__ __launch_bounds__(256) void k_sgd_average(float *__restrict__ w, GradList g,
+                                                     int32_t n, int64_t count, float lr)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= count)
+        return;
+    float sum = 0.f;
+    for (int m = 0; m < n; ++m)
+        sum += g.g[m][e];
+    w[e] = w[e] - lr * (sum / (float)n);
+}
+
+// ---------------------------------------------------------------------------
 // dispatch helpers
 // ---------------------------------------------------------------------------
 
@@ -1508,6 +1528,20 @@ hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const f
     const dim3 grid((unsigned)((F + 63) / 64), (unsigned)((splits + 3) / 4));
     hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, G, chunk,
                        splits, part);
+    return hipGetLastError();
+}
+
+hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t count, float lr,
+                              hipStream_t s)
+{
+    if (n < 1 || n > kMaxAverage || count < 0)
+        return hipErrorInvalidValue;
+    if (count == 0)
+        return hipSuccess;
+    const int64_t blocks = (count + 255) / 256;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_sgd_average, dim3((unsigned)blocks), dim3(256), 0, s, w, g, n, count, lr);
     return hipGetLastError();
 }
 

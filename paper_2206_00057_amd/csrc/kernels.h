@@ -107,6 +107,15 @@ hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32
 hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float *loss,
                             hipStream_t s);
 
+// w[e] -= lr * (1/n) * sum_{m < n} g[m][e], the sum in m order, for
+// 1 <= n <= kMaxAverage device arrays of count floats.
+constexpr int kMaxAverage = 64;
+struct GradList {
+    const float *g[kMaxAverage];
+};
+hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t count, float lr,
+                              hipStream_t s);
+
 // GEMM K step; the smallest workgroup tile of C is kGemmBM x kGemmBN.
 constexpr int kGemmBM = 64;
 constexpr int kGemmBN = 64;

@@ -53,6 +53,7 @@ def lib():
             "digest_layer_forward": ([P, i32, P, P, P, i32, P], st),
             "digest_layer_backward": ([P, i32, P, P, P, P, P, P, P], st),
             "digest_softmax_xent": ([P, P, P, P, P, P], st),
+            "digest_sgd_average": ([P, P, i32, i64, ctypes.c_float, P], st),
             "digest_sync_period": ([i32, i64, P, P], st),
             "digest_profile_enable": ([P, i32], st),
             "digest_profile_read": ([P, P, P], st),
@@ -255,6 +256,18 @@ def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):
     c = _dev(dlogits, torch.float32, p.n_own * C, "dlogits")
     d = _dev(loss, torch.float32, 1, "loss")
     _check(lib().digest_softmax_xent(p.handle, a, b, c, d, _stream(stream)))
+
+
+def digest_sgd_average(w, grads, lr, stream=None):
+    """w -= lr * mean(grads), the average of the local models (Algorithm 1, AGG)."""
+    import torch
+    if not grads:
+        raise ValueError("need at least one gradient")
+    n = w.numel()
+    pw = _dev(w, torch.float32, n, "w")
+    ptrs = (ctypes.c_void_p * len(grads))(*[_dev(g, torch.float32, n, f"grads[{m}]").value
+                                            for m, g in enumerate(grads)])
+    _check(lib().digest_sgd_average(pw, ptrs, len(grads), n, float(lr), _stream(stream)))
 
 
 def digest_sync_period(K, iteration):

@@ -1,0 +1,134 @@
+"""DIGEST training of every subgraph of a graph on one GPU (Algorithm 1,
+synchronous mode), the subgraphs taking turns on one stream and sharing one
+device-resident representation store per stale level.
+
+Round r (1-based), sync interval K, M subgraphs:
+
+    every subgraph starts from the global parameters W
+    for l = 1..L:
+        if r mod K == 0 and l >= 2: every subgraph pulls level l-1
+        every subgraph runs the forward of layer l
+        if (r-1) mod K == 0 and l <= L-1: every subgraph pushes level l
+    every subgraph: loss head, backward of layers L..1 -> dW_m
+    W <- W - lr * (1/M) sum_m dW_m        (AGG of the M local models)
+
+The subgraphs advance layer by layer together (all forwards of layer l, then
+all pushes of level l, then the pulls of level l before layer l+1), the
+synchronous barrier of Algorithm 1 at layer granularity.  With K = 1 every
+halo row a subgraph reads was pushed by its owner earlier in the same round,
+so each subgraph's forward equals the full-graph GCN forward on its rows
+(P_m = P_in + P_out with fresh halo rows).  With K > 1 the halo rows are the
+stale ones of the last push round.
+
+All arithmetic runs in libdigest.so (the layers, pulls, pushes, loss heads
+and the parameter averaging); this module owns the buffers and orders the
+calls.  ``capture`` records one round per pull/push pattern into a HIP graph.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import digest as D
+from .step import GpuPartition
+
+
+class DigestTrainer:
+    def __init__(self, n_global, parts, widths, x, labels, weights, lr, K, device="cuda"):
+        """parts: synth-style partitions (owned, halo, CSR rows) covering the
+        graph; x: device [n_global, d_0] features; labels: device int32
+        [n_global]; weights: device float32 tensors W_1..W_L (the global
+        parameters, updated in place by every round)."""
+        if not 1 <= len(parts) <= 64:
+            raise ValueError("between 1 and 64 subgraphs")
+        self.widths = [int(w) for w in widths]
+        self.L = len(self.widths) - 1
+        self.n_global = int(n_global)
+        self.lr, self.K = float(lr), int(K)
+        self.W = weights
+        self.gps = [GpuPartition(n_global, p, widths, device=device) for p in parts]
+        idx = [torch.from_numpy(p.owned).to(device) for p in parts]
+        self.x_own = [x.index_select(0, i).contiguous() for i in idx]
+        self.y_own = [labels.index_select(0, i).contiguous() for i in idx]
+        f32 = dict(dtype=torch.float32, device=device)
+        # the shared store: level 0 is the static features, levels 1..L-1 stale
+        self.stores = [x] + [torch.zeros(n_global, self.widths[l], **f32)
+                             for l in range(1, self.L)]
+        self.losses = torch.zeros(len(parts), **f32)
+        self.graphs = {}
+        self.edges_per_round = sum(gp.p.nnz + (gp.p.nnz_in if l > 1 else 0)
+                                   for gp in self.gps for l in range(1, self.L + 1))
+
+    def act(self, layer):
+        return D.ACT_RELU if layer < self.L else D.ACT_IDENTITY
+
+    def init_stores(self):
+        """Fill the store with one forward of all subgraphs at the current W
+        with fresh halo rows (a round-0 pass that pulls before and pushes
+        after every layer), then give every subgraph all its halo levels."""
+        for gp in self.gps:
+            D.digest_pull(gp.p, 0, self.stores[0])
+        h = list(self.x_own)
+        for l in range(1, self.L):
+            for m, gp in enumerate(self.gps):
+                if l >= 2:
+                    D.digest_pull(gp.p, l - 1, self.stores[l - 1])
+                D.digest_layer_forward(gp.p, l, h[m], self.W[l - 1], gp.H[l], self.act(l))
+            for gp in self.gps:
+                D.digest_push(gp.p, l, gp.H[l], self.stores[l])
+            h = [gp.H[l] for gp in self.gps]
+        for gp in self.gps:
+            for lev in range(1, self.L):
+                D.digest_pull(gp.p, lev, self.stores[lev])
+
+    def _round(self, do_pull, do_push):
+        h = list(self.x_own)
+        for l in range(1, self.L + 1):
+            if do_pull and l >= 2:
+                for gp in self.gps:
+                    D.digest_pull(gp.p, l - 1, self.stores[l - 1])
+            for m, gp in enumerate(self.gps):
+                D.digest_layer_forward(gp.p, l, h[m], self.W[l - 1], gp.H[l], self.act(l))
+            if do_push and l <= self.L - 1:
+                for gp in self.gps:
+                    D.digest_push(gp.p, l, gp.H[l], self.stores[l])
+            h = [gp.H[l] for gp in self.gps]
+        for m, gp in enumerate(self.gps):
+            D.digest_softmax_xent(gp.p, gp.H[self.L], self.y_own[m], gp.dH[self.L],
+                                  self.losses[m:m + 1])
+            for l in range(self.L, 0, -1):
+                dh_in = gp.dH[l - 1] if l > 1 else None
+                h_in = gp.H[l - 1] if l > 1 else self.x_own[m]
+                D.digest_layer_backward(gp.p, l, h_in, gp.H[l], gp.dH[l], self.W[l - 1],
+                                        gp.dW[l], dh_in)
+        for l in range(1, self.L + 1):
+            D.digest_sgd_average(self.W[l - 1], [gp.dW[l] for gp in self.gps], self.lr)
+
+    def round(self, r):
+        """Round r (1-based), eagerly."""
+        self._round(*D.digest_sync_period(self.K, r))
+
+    def capture(self):
+        """Record one HIP graph per pull/push pattern of the schedule.  The
+        warm-up and the captures run rounds, so they also train: the caller
+        restores W (and the store) afterwards if it needs a fixed start."""
+        patterns = sorted({D.digest_sync_period(self.K, r) for r in range(1, 2 * self.K + 1)})
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for pat in patterns:
+                self._round(*pat)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        for pat in patterns:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self._round(*pat)
+            self.graphs[pat] = g
+        torch.cuda.synchronize()
+
+    def replay(self, r):
+        self.graphs[D.digest_sync_period(self.K, r)].replay()
+
+    def mean_loss(self):
+        """Average of the subgraphs' local losses of the last round (Eq. 3)."""
+        return float(self.losses.mean())

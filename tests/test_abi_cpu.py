@@ -127,6 +127,21 @@ def test_device_calls_without_workspace_fail_with_estate():
     assert L.digest_partition_bind_workspace(h.handle, ctypes.c_void_p(256), 16, None) == D.ENOMEM
 
 
+def test_sgd_average_rejects_bad_arguments_before_any_device_work():
+    L = D.lib()
+    fake = ctypes.c_void_p(256)   # never dereferenced: the checks come first
+    ptrs = (ctypes.c_void_p * 65)(*([256] * 65))
+    assert L.digest_sgd_average(fake, ptrs, 0, 10, ctypes.c_float(0.1), None) == D.EINVAL
+    assert L.digest_sgd_average(fake, ptrs, 65, 10, ctypes.c_float(0.1), None) == D.EINVAL
+    assert L.digest_sgd_average(fake, ptrs, 2, -1, ctypes.c_float(0.1), None) == D.EINVAL
+    assert L.digest_sgd_average(None, ptrs, 2, 10, ctypes.c_float(0.1), None) == D.EINVAL
+    nulls = (ctypes.c_void_p * 2)(256, None)
+    assert L.digest_sgd_average(fake, nulls, 2, 10, ctypes.c_float(0.1), None) == D.EINVAL
+    assert b"NULL" in L.digest_last_error()
+    # nothing to update: no device work, OK
+    assert L.digest_sgd_average(None, None, 1, 0, ctypes.c_float(0.1), None) == D.OK
+
+
 def test_sync_period_matches_algorithm_and_oracle(golden):
     f = os.path.join(ROOT, "tests", "golden", "alg1_schedule.txt")
     for line in open(f):

@@ -1,0 +1,160 @@
+"""Pins for the oracle's multi-subgraph training round (Algorithm 1,
+synchronous mode) and its global update (AGG), against what the paper and
+the mathematics fix, never against the oracle itself:
+
+  * AGG of one model is plain SGD; of M equal gradients it is one of them;
+    it is linear in the gradients (exact small cases);
+  * one subgraph covering the whole graph (no halo) trains exactly like
+    full-graph GCN with SGD on the mean cross entropy (torch float64
+    autograd);
+  * sync interval 1: every subgraph's logits equal the full-graph GCN rows
+    at the current W (P_m = P_in + P_out with fresh halo rows), round after
+    round;
+  * sync interval 3: before the first pull round the halo rows are those of
+    the initial store, so after one SGD step the logits differ from the
+    full-graph ones at the new W exactly by P_out (H~ - H) W on the rows.
+"""
+import numpy as np
+import pytest
+import scipy.sparse as sp
+import torch
+
+import oracle
+from paper_2206_00057_amd import synth
+
+
+def cfg_small(n=96, blocks=4, widths=(6, 5, 3), classes=3):
+    return synth.scaled(synth.CONFIGS["tiny"], n, blocks=blocks, cap=8, widths=widths,
+                        classes=classes)
+
+
+def dense(g):
+    return sp.csr_matrix((g.values.astype(np.float64), g.indices, g.indptr),
+                         shape=(g.n, g.n)).toarray()
+
+
+def full_forward(A, X, Ws):
+    """Full-graph GCN in float64: ReLU hidden layers, identity logits."""
+    h = X.astype(np.float64)
+    hs = [h]
+    for l, W in enumerate(Ws):
+        z = A @ h @ W.astype(np.float64)
+        h = np.maximum(z, 0.0) if l < len(Ws) - 1 else z
+        hs.append(h)
+    return hs
+
+
+# --------------------------------------------------------------------------
+# AGG
+# --------------------------------------------------------------------------
+
+def test_sgd_average_closed_forms():
+    rng = np.random.default_rng(0)
+    w = rng.standard_normal((4, 3)).astype(np.float32)
+    g1 = rng.standard_normal((4, 3)).astype(np.float32)
+    g2 = rng.standard_normal((4, 3)).astype(np.float32)
+    lr = 0.25
+    # one local model: plain SGD (float64 then rounded)
+    np.testing.assert_array_equal(oracle.sgd_average(w, [g1], lr),
+                                  (w.astype(np.float64) - lr * g1.astype(np.float64))
+                                  .astype(np.float32))
+    # M equal gradients: the same as one of them
+    np.testing.assert_array_equal(oracle.sgd_average(w, [g1] * 5, lr),
+                                  oracle.sgd_average(w, [g1], lr))
+    # the average of two local models W - lr g1 and W - lr g2
+    two = oracle.sgd_average(w, [g1, g2], lr)
+    ref = 0.5 * ((w.astype(np.float64) - lr * g1) + (w.astype(np.float64) - lr * g2))
+    np.testing.assert_allclose(two, ref, rtol=1e-6, atol=1e-7)
+    # exact small case
+    np.testing.assert_array_equal(
+        oracle.sgd_average(np.ones(3, np.float32), [np.full(3, 2, np.float32),
+                                                    np.full(3, 4, np.float32)], 0.5),
+        np.full(3, -0.5, np.float32))
+    with pytest.raises(oracle.OracleError):
+        oracle.sgd_average(w, [], lr)
+
+
+# --------------------------------------------------------------------------
+# one subgraph = full-graph training
+# --------------------------------------------------------------------------
+
+def test_single_subgraph_trains_like_full_graph_gcn():
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=5)
+    A = dense(g)
+    X = synth.features(cfg)
+    y = synth.labels(cfg)
+    Ws = synth.weights(cfg)
+    lr = 0.5
+    tr = oracle.OracleTrainer(g.n, [synth.extract_partition(g, np.arange(g.n))], cfg.widths,
+                              X, y, Ws, lr, K=2)
+    tr.init_stores()
+    # torch float64 autograd, SGD on the mean cross entropy over all nodes
+    At = torch.tensor(A)
+    Xt = torch.tensor(X, dtype=torch.float64)
+    Wt = [torch.tensor(w, dtype=torch.float64, requires_grad=True) for w in Ws]
+    yt = torch.tensor(y, dtype=torch.int64)
+    for r in (1, 2, 3):
+        loss = tr.round(r)
+        h = Xt
+        for l, W in enumerate(Wt):
+            z = At @ h @ W
+            h = torch.relu(z) if l < len(Wt) - 1 else z
+        ref_loss = torch.nn.functional.cross_entropy(h, yt)
+        grads = torch.autograd.grad(ref_loss, Wt)
+        with torch.no_grad():
+            Wt = [(W - lr * gW).requires_grad_(True) for W, gW in zip(Wt, grads)]
+        assert abs(loss - float(ref_loss)) < 1e-5 * abs(float(ref_loss))
+        for l in range(len(Ws)):
+            np.testing.assert_allclose(tr.W[l], Wt[l].detach().numpy(), rtol=1e-5, atol=1e-6)
+
+
+# --------------------------------------------------------------------------
+# several subgraphs: fresh halo rows at K = 1, stale ones before a pull
+# --------------------------------------------------------------------------
+
+def test_sync_interval_one_gives_full_graph_logits_every_round():
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=6)
+    A = dense(g)
+    X = synth.features(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    assert all(p.n_halo > 0 for p in parts)
+    tr = oracle.OracleTrainer(g.n, parts, cfg.widths, X, synth.labels(cfg), synth.weights(cfg),
+                              lr=0.5, K=1)
+    tr.init_stores()
+    for r in (1, 2, 3):
+        W_round = [w.copy() for w in tr.W]
+        tr.round(r)
+        full = full_forward(A, X, W_round)[-1]
+        for p, logits in zip(parts, tr.logits):
+            np.testing.assert_allclose(logits, full[p.owned], rtol=1e-5, atol=1e-6)
+
+
+def test_stale_halo_rows_before_the_first_pull():
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=7)
+    A = dense(g)
+    X = synth.features(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    tr = oracle.OracleTrainer(g.n, parts, cfg.widths, X, synth.labels(cfg), synth.weights(cfg),
+                              lr=0.5, K=3)
+    W1 = [w.copy() for w in tr.W]
+    tr.init_stores()
+    tr.round(1)          # no pull (1 mod 3 != 0); push ((1-1) mod 3 == 0)
+    # round 1 ran at W1 with halo rows from the initial store, also at W1: exact
+    full1 = full_forward(A, X, W1)
+    for p, logits in zip(parts, tr.logits):
+        np.testing.assert_allclose(logits, full1[-1][p.owned], rtol=1e-5, atol=1e-6)
+    W2 = [w.copy() for w in tr.W]
+    tr.round(2)          # no pull, no push: layer-2 halo rows still from W1's level 1
+    full2 = full_forward(A, X, W2)
+    H1_stale = full1[1]              # level-1 store: pushed in round 1 at W1
+    for m, (p, logits) in enumerate(zip(parts, tr.logits)):
+        mine = np.zeros(g.n, bool)
+        mine[p.owned] = True
+        Pout = A[p.owned] * (~mine)[None, :]
+        # logits = P_m [H1_own(W2); H1_halo(W1)] W2_2 = full2 rows + P_out (H1~ - H1) W2_2
+        ref = full2[-1][p.owned] + Pout @ (H1_stale - full2[1]) @ W2[1].astype(np.float64)
+        np.testing.assert_allclose(logits, ref, rtol=1e-5, atol=1e-6)
+        assert np.abs(logits - full2[-1][p.owned]).max() > 1e-6   # staleness is visible
