@@ -195,7 +195,7 @@ def train_bench(args):
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
     tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws],
-                       args.lr, K)
+                       args.lr, K, grad_exchange=args.grad_exchange)
     print(f"[bench] training {cfg.name}: {M} subgraphs, inputs {time.time() - t0:.1f}s",
           file=sys.stderr, flush=True)
     tr.init_stores()
@@ -218,7 +218,8 @@ def train_bench(args):
         "ms_per_step": round(ms / args.steps, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: all {M} subgraphs, Algorithm 1 rounds with "
-                               f"sync interval {K}, SGD lr {args.lr}",
+                               f"sync interval {K}, SGD lr {args.lr}, halo-gradient "
+                               f"exchange {args.grad_exchange}",
                    "n_global": g.n, "subgraphs": M, "widths": list(cfg.widths),
                    "edges_per_round": tr.edges_per_round, "launch": "hip-graph replay"},
         "loss": {"after_warmup": round(first_loss, 6), "last": round(tr.mean_loss(), 6)},
@@ -244,10 +245,13 @@ def main():
     ap.add_argument("--train", action="store_true",
                     help="Algorithm 1 rounds over every subgraph of the graph instead of one")
     ap.add_argument("--lr", type=float, default=0.1, help="SGD learning rate for --train")
+    ap.add_argument("--grad-exchange", default="none", choices=("none", "fresh", "stale"),
+                    help="--train: exchange the halo gradients P_out^T D W^T between "
+                         "subgraphs (same round or one round late)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one partition on one GPU; runs on more than one GPU are not "
-              "part of this build (--gpus 1).", file=sys.stderr)
+              "implemented (--gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     if args.train:

@@ -199,6 +199,48 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
                                     void *hip_stream);
 
 /*
+ * Halo gradient (the stale-gradient term of the appendix's DIGEST backward,
+ * P_out^T D W^T): the gradient of this subgraph's loss with respect to the
+ * rows of its halo nodes at level layer-1, from the last forward of
+ * `layer` (2..L):
+ *   D       = dh_out * 1[h_out > 0] (ReLU) or dh_out (identity)
+ *   dh_halo = P_out^T D W^T          [n_halo, d_{layer-1}], halo slot order
+ * (row j belongs to halo node halo[j]).  digest_layer_backward drops this
+ * term (halo rows are constants of the iteration); exchanging it through
+ * digest_push_add / digest_pull_add gives the owners of the halo nodes the
+ * gradient of the other subgraphs' losses.
+ *   h_out, dh_out device [n_owned, d_layer]; w device [d_{layer-1}, d_layer].
+ * Errors: DIGEST_EINVAL (layer < 2, NULL), DIGEST_ESTATE (no forward of the
+ * layer, no workspace), DIGEST_EHIP.
+ */
+digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const float *h_out,
+                                   const float *dh_out, const float *w, float *dh_halo,
+                                   void *hip_stream);
+
+/*
+ * Gradient push: add this subgraph's halo gradient of level `level` into a
+ * gradient store indexed by node id, gstore[halo[j], :] += dh_halo[j, :]
+ * (float32 adds; the halo ids are distinct, so one call never adds twice to
+ * a row; calls for different subgraphs on one stream add in call order).
+ *   level 1..L-1;  dh_halo device [n_halo, d_level];  gstore device
+ *   [n_global, d_level].
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP.
+ */
+digest_status digest_push_add(digest_partition *p, int32_t level, const float *dh_halo,
+                              float *gstore, void *hip_stream);
+
+/*
+ * Gradient pull: add what the other subgraphs pushed for this subgraph's
+ * own nodes to its gradient and clear those store rows for the next use:
+ *   dh_own[i, :] += gstore[owned[i], :];  gstore[owned[i], :] = 0.
+ *   level 1..L-1;  gstore device [n_global, d_level];  dh_own device
+ *   [n_owned, d_level] (e.g. the dh_in of the next layer's backward).
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP.
+ */
+digest_status digest_pull_add(digest_partition *p, int32_t level, float *gstore, float *dh_own,
+                              void *hip_stream);
+
+/*
  * Local loss head (Eq. 3 with cross entropy), over all n_owned rows:
  *   loss    = -(1/n) sum_i log softmax(logits_i)[labels_i]   (device, 1 float)
  *   dlogits = (softmax(logits) - onehot(labels)) / n          [n_owned, d_L]

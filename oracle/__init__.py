@@ -78,6 +78,8 @@ def _load():
             lib.oracle_sync_period.argtypes = [i32, i64, ctypes.POINTER(i32), ctypes.POINTER(i32)]
             lib.oracle_sync_period.restype = ctypes.c_int
             lib.oracle_sgd_average.argtypes = [P, P, i32, i64, f32]
+            lib.oracle_halo_gradient.argtypes = [i64, i64, P, P, P, i64, i64, P, P, P,
+                                                 ctypes.c_int, P]
             lib.oracle_sgd_average.restype = ctypes.c_int
             del f32
             _lib = lib
@@ -226,6 +228,37 @@ def sync_period(K, r):
     return bool(a.value), bool(b.value)
 
 
+def halo_gradient(indptr, col_local, values, n_halo, w, h_out, dh_out, act):
+    """The appendix's stale-gradient term P_out^T D W^T: float32 [n_halo, d_in]."""
+    indptr = _c(indptr, np.int64)
+    col_local = _c(col_local, np.int32)
+    values = _c(values, np.float32)
+    w = _c(w, np.float32)
+    h_out = _c(h_out, np.float32)
+    dh_out = _c(dh_out, np.float32)
+    n_own = indptr.shape[0] - 1
+    d_in, d_out = w.shape
+    out = np.empty((int(n_halo), d_in), np.float32)
+    _load().oracle_halo_gradient(n_own, int(n_halo), _p(indptr), _p(col_local), _p(values),
+                                 d_in, d_out, _p(w), _p(h_out), _p(dh_out), int(act), _p(out))
+    return out
+
+
+def push_add(gstore, halo, dh_halo):
+    """gstore[halo[j]] += dh_halo[j] (float32 adds; ``halo`` ids distinct)."""
+    halo = _c(halo, np.int64)
+    gstore[halo] = gstore[halo] + _c(dh_halo, np.float32)
+    return gstore
+
+
+def pull_add(gstore, owned, dh_own):
+    """dh_own += gstore[owned]; gstore[owned] = 0.  Returns the new dh_own."""
+    owned = _c(owned, np.int64)
+    out = _c(dh_own, np.float32) + gstore[owned]
+    gstore[owned] = 0.0
+    return out
+
+
 def sgd_average(w, grads, lr):
     """Algorithm 1's global update (AGG): the average of the M local models
     ``w - lr * grads[m]``; returns the new float32 ``w``."""
@@ -294,6 +327,10 @@ class OraclePartition:
                               self.halo_buf.get(layer - 1), w, h_out, dh_out, act,
                               want_dh_in=want_dh_in)
 
+    def halo_gradient(self, layer, w, h_out, dh_out, act):
+        return halo_gradient(self.indptr, self.col_local, self.values, self.n_halo, w, h_out,
+                             dh_out, act)
+
 
 class OracleTrainer:
     """Algorithm 1 (synchronous mode) over every subgraph, one after another
@@ -302,12 +339,24 @@ class OracleTrainer:
     then every subgraph computes layer l, then, if (r-1) mod K == 0 and
     l < L, every subgraph pushes level l; then every subgraph computes its
     local loss (Eq. 3) and gradients, and AGG averages the M locally updated
-    models.  ``parts`` carry owned / halo / CSR rows (global columns)."""
+    models.  ``parts`` carry owned / halo / CSR rows (global columns).
 
-    def __init__(self, n_global, parts, widths, X, labels, Ws, lr, K):
+    grad_exchange adds the appendix's stale-gradient term: after the
+    backward of layer l >= 2 (all subgraphs, layer by layer), every subgraph's
+    halo gradient P_out^T D W^T is added into a per-level gradient store and
+    each owner adds its rows to its input gradient -- in the same round
+    ("fresh") or one round later ("stale", the t-1 of the appendix).  With
+    "none" (reading A8) halo rows get no gradient."""
+
+    def __init__(self, n_global, parts, widths, X, labels, Ws, lr, K, grad_exchange="none"):
+        if grad_exchange not in ("none", "fresh", "stale"):
+            raise OracleError("grad_exchange is none, fresh or stale")
         self.widths = [int(x) for x in widths]
         self.L = len(self.widths) - 1
         self.lr, self.K = float(lr), int(K)
+        self.grad_exchange = grad_exchange
+        self.gstores = [None] + [np.zeros((int(n_global), self.widths[l]), np.float32)
+                                 for l in range(1, self.L)]
         self.ops = [OraclePartition(n_global, p.indptr, p.indices, p.values, p.owned, p.halo,
                                     widths) for p in parts]
         self.X = _c(X, np.float32)
@@ -354,12 +403,31 @@ class OracleTrainer:
                 for m, op in enumerate(self.ops):
                     self.stores[l] = op.push(l, outs[m][l], self.stores[l])
         grads = [[None] * len(self.ops) for _ in range(self.L)]
-        for m, op in enumerate(self.ops):
+        dh = [None] * len(self.ops)
+        for m in range(len(self.ops)):
             self.logits[m] = outs[m][self.L]
-            self.losses[m], dh = softmax_xent(outs[m][self.L], self.y_own[m])
-            for l in range(self.L, 0, -1):
-                grads[l - 1][m], dh = op.backward(l, outs[m][l - 1], self.W[l - 1], outs[m][l],
-                                                  dh, self.act(l), want_dh_in=l > 1)
+            self.losses[m], dh[m] = softmax_xent(outs[m][self.L], self.y_own[m])
+        for l in range(self.L, 0, -1):
+            dh_in = [None] * len(self.ops)
+            for m, op in enumerate(self.ops):
+                grads[l - 1][m], dh_in[m] = op.backward(l, outs[m][l - 1], self.W[l - 1],
+                                                        outs[m][l], dh[m], self.act(l),
+                                                        want_dh_in=l > 1)
+            if l > 1 and self.grad_exchange != "none":
+                hg = [op.halo_gradient(l, self.W[l - 1], outs[m][l], dh[m], self.act(l))
+                      for m, op in enumerate(self.ops)]
+                gs = self.gstores[l - 1]
+                if self.grad_exchange == "fresh":
+                    for m, op in enumerate(self.ops):
+                        push_add(gs, op.halo, hg[m])
+                    for m, op in enumerate(self.ops):
+                        dh_in[m] = pull_add(gs, op.owned, dh_in[m])
+                else:   # last round's halo gradients, then this round's for the next
+                    for m, op in enumerate(self.ops):
+                        dh_in[m] = pull_add(gs, op.owned, dh_in[m])
+                    for m, op in enumerate(self.ops):
+                        push_add(gs, op.halo, hg[m])
+            dh = dh_in
         self.W = [sgd_average(self.W[l], grads[l], self.lr) for l in range(self.L)]
         return float(np.mean(self.losses))
 

@@ -23,6 +23,9 @@
  *     backward of Appendix A.3), with the stale halo rows held constant;
  *   - the synchronisation schedule of Algorithm 1 (pull when r mod N == 0,
  *     push when (r-1) mod N == 0, for layers other than the last);
+ *   - the halo gradient P_out^T D W^T, the stale-gradient term of the DIGEST
+ *     backward in Appendix A.3 (what a subgraph's rows contribute to the
+ *     gradient of its halo nodes' representations);
  *   - the global parameter update of Algorithm 1 (AGG of the M locally
  *     updated models; each took one SGD step from the same global W, so
  *     the average is W minus the learning rate times the mean gradient,
@@ -408,5 +411,45 @@ int oracle_sgd_average(float *w, const float *const *grads, int32_t M, int64_t c
         w[e] = (float)((double)w[e] - (double)lr * (g / (double)M));
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Halo gradient (Appendix A.3, the P_out^T term)                           */
+/* ------------------------------------------------------------------------ */
+
+/* dh_halo[j] = sum over entries (i, n_own + j) of P of a_ij * (D W^T)[i],
+ * D = dh_out masked by h_out > 0 for ReLU; entries in CSR order, double. */
+void oracle_halo_gradient(int64_t n_own, int64_t n_halo, const int64_t *indptr,
+                          const int32_t *col_local, const float *values, int64_t d_in,
+                          int64_t d_out, const float *w, const float *h_out,
+                          const float *dh_out, int act, float *dh_halo)
+{
+    double *acc = (double *)calloc((size_t)(n_halo * d_in > 0 ? n_halo * d_in : 1), sizeof(double));
+    double *g = (double *)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+    for (int64_t i = 0; i < n_own; ++i) {
+        /* G[i] = D[i] W^T */
+        for (int64_t f = 0; f < d_in; ++f) {
+            double s = 0.0;
+            for (int64_t o = 0; o < d_out; ++o) {
+                double dz = (double)dh_out[i * d_out + o];
+                if (act == ORACLE_RELU && !(h_out[i * d_out + o] > 0.0f))
+                    dz = 0.0;
+                s += dz * (double)w[f * d_out + o];
+            }
+            g[f] = s;
+        }
+        for (int64_t k = indptr[i]; k < indptr[i + 1]; ++k) {
+            int64_t c = col_local[k];
+            if (c < n_own)
+                continue; /* in-subgraph column: the ordinary backward */
+            double a = (double)values[k];
+            for (int64_t f = 0; f < d_in; ++f)
+                acc[(c - n_own) * d_in + f] += a * g[f];
+        }
+    }
+    for (int64_t e = 0; e < n_halo * d_in; ++e)
+        dh_halo[e] = (float)acc[e];
+    free(g);
+    free(acc);
 }
 

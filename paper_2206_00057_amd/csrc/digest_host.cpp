@@ -43,11 +43,15 @@ enum Kind : int32_t {
     K_SPMM_BWD,
     K_LOSS,
     K_LOSS_MEAN,
+    K_HALO_GRAD,
+    K_GRAD_PUSH,
+    K_GRAD_PULL,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "pull_gather", "push_scatter", "spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
-    "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent", "loss_mean"};
+    "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent", "loss_mean",
+    "halo_gradient", "grad_push_add", "grad_pull_add"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -128,16 +132,17 @@ struct digest_partition {
     std::vector<int32_t> rowptr, col, t_rowptr, t_src, halo_gid, bnd_local, bnd_gid, owned_gid;
     std::vector<float> val, t_val;
     // blocks_t covers the first n_own rows of the transpose (P_in^T),
-    // blocks_tf all n_own + n_halo rows (P_m^T).
-    std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf;
-    int32_t long_f = 0, long_t = 0, long_tf = 0;   // leading long-row blocks of each
+    // blocks_tf all n_own + n_halo rows (P_m^T), blocks_th its n_halo halo rows
+    // (P_out^T, numbered from 0).
+    std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf, blocks_th;
+    int32_t long_f = 0, long_t = 0, long_tf = 0, long_th = 0;   // leading long-row blocks
 
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
-        size_t blocks_f, blocks_t, blocks_tf;
+        size_t blocks_f, blocks_t, blocks_tf, blocks_th;
         std::vector<size_t> halo_buf;   // per level 0..L-1
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused)
-        size_t tmp, tbuf, gemm_part, loss_part;
+        size_t tmp, tmp_halo, tbuf, gemm_part, loss_part;
         size_t total;
     } lay{};
 
@@ -253,6 +258,7 @@ void plan_layout(digest_partition &p)
     l.blocks_f = take(sizeof(SpmmBlock) * p.blocks_f.size());
     l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
     l.blocks_tf = take(sizeof(SpmmBlock) * p.blocks_tf.size());
+    l.blocks_th = take(sizeof(SpmmBlock) * p.blocks_th.size());
     l.halo_buf.assign(p.L, 0);
     for (int32_t lev = 0; lev < p.L; ++lev)
         l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * p.widths[lev]);
@@ -274,6 +280,7 @@ void plan_layout(digest_partition &p)
         }
     }
     l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
+    l.tmp_halo = take(sizeof(float) * (size_t)p.n_halo * wmax);
     l.tbuf = take(sizeof(float) * (size_t)tbuf);
     l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
     l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own, p.widths[p.L]));
@@ -336,21 +343,31 @@ digest_status need_bound(const digest_partition *p)
 }
 
 // Sparse aggregation over the local CSR (P_m), the CSR of P_in^T (the first
-// n_own rows of the transpose) or of P_m^T (all of it).
-enum class Csr { Fwd, InT, FullT };
+// n_own rows of the transpose), of P_m^T (all of it) or of P_out^T (its
+// n_halo halo rows, numbered from 0).
+enum class Csr { Fwd, InT, FullT, HaloT };
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
-                       const digest::SpmmEpilogue *ep = nullptr)
+                       const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1)
 {
     const bool fwd = which == Csr::Fwd;
-    const auto &blocks = fwd ? p->blocks_f : (which == Csr::InT ? p->blocks_t : p->blocks_tf);
-    const size_t boff = fwd ? p->lay.blocks_f : (which == Csr::InT ? p->lay.blocks_t : p->lay.blocks_tf);
-    const int32_t n_long = fwd ? p->long_f : (which == Csr::InT ? p->long_t : p->long_tf);
-    Timed t(p, fwd ? K_SPMM_FWD : K_SPMM_BWD, layer, s);
+    const std::vector<SpmmBlock> *blocks = &p->blocks_f;
+    size_t boff = p->lay.blocks_f;
+    int32_t n_long = p->long_f;
+    if (which == Csr::InT) {
+        blocks = &p->blocks_t, boff = p->lay.blocks_t, n_long = p->long_t;
+    } else if (which == Csr::FullT) {
+        blocks = &p->blocks_tf, boff = p->lay.blocks_tf, n_long = p->long_tf;
+    } else if (which == Csr::HaloT) {
+        blocks = &p->blocks_th, boff = p->lay.blocks_th, n_long = p->long_th;
+    }
+    const int32_t *rowptr = p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr);
+    if (which == Csr::HaloT)
+        rowptr += p->n_own;
+    Timed t(p, kind >= 0 ? kind : (fwd ? K_SPMM_FWD : K_SPMM_BWD), layer, s);
     return hip_check(
-        digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks.size(), n_long,
-                            p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr),
+        digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
                             p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1, n_src0, d,
                             out, s, ep),
@@ -483,6 +500,11 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
         p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
         p->long_tf = build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
+        {
+            const std::vector<int32_t> halo_rows(p->t_rowptr.begin() + n_owned,
+                                                 p->t_rowptr.end());
+            p->long_th = build_blocks(halo_rows, p->n_halo, p->blocks_th);
+        }
         plan_layout(*p);
         p->pulled.assign(p->L, 0);
         p->pull_gen.assign(p->L, 0);
@@ -558,6 +580,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.blocks_f, p->blocks_f.data(), sizeof(SpmmBlock) * p->blocks_f.size()},
         {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
         {l.blocks_tf, p->blocks_tf.data(), sizeof(SpmmBlock) * p->blocks_tf.size()},
+        {l.blocks_th, p->blocks_th.data(), sizeof(SpmmBlock) * p->blocks_th.size()},
     };
     for (const Up &u : ups) {
         if (!u.bytes)
@@ -965,6 +988,105 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
     }
     Timed t(p, K_LOSS_MEAN, p->L, s);
     return hip_check(digest::launch_loss_mean(part, p->n_own, C, loss, s), "loss mean");
+}
+
+digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const float *h_out,
+                                   const float *dh_out, const float *w, float *dh_halo,
+                                   void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (layer < 2 || layer > p->L)
+        return fail(DIGEST_EINVAL, "halo gradient of layer %d outside [2, %d]", layer, p->L);
+    if (!w || (p->n_own > 0 && (!h_out || !dh_out)) || (p->n_halo > 0 && !dh_halo))
+        return fail(DIGEST_EINVAL, "NULL h_out, dh_out, w or dh_halo");
+    if (!p->fwd_done[layer])
+        return fail(DIGEST_ESTATE, "no forward of layer %d since the workspace was bound",
+                    layer);
+    if (p->n_halo == 0)
+        return DIGEST_OK;
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const bool relu = p->act[layer] == DIGEST_ACT_RELU;
+    digest::GemmArgs h{};
+    h.N = d_in;
+    h.K = d_out;
+    h.B = w;
+    h.ldb = d_out;
+    h.b_trans = true;
+    h.ldc = d_in;
+    h.splits = 1;
+    h.kchunk = d_out;
+    if (!relu && d_out < d_in) {
+        // narrower output: (P_out^T D) W^T, the aggregation at width d_out
+        float *gh = p->at<float>(p->lay.tmp_halo);
+        if (digest_status st = run_spmm(p, Csr::HaloT, dh_out, nullptr, p->n_own, d_out, gh,
+                                        layer, s, nullptr, K_HALO_GRAD))
+            return st;
+        Timed t(p, K_HALO_GRAD, layer, s);
+        if (narrow_valu(d_in, d_out))
+            return hip_check(digest::launch_narrow_k(p->n_halo, d_in, d_out, gh, d_out, w,
+                                                     dh_halo, d_in, s),
+                             "halo gradient");
+        h.M = p->n_halo;
+        h.A = gh;
+        h.lda = d_out;
+        h.C = dh_halo;
+        h.tile = gemm_tile_for(p->n_halo, d_in, d_out, false);
+        return hip_check(digest::launch_gemm(h, s), "halo gradient");
+    }
+    // otherwise P_out^T (D W^T), with the ReLU mask fused into the GEMM
+    float *tmp = p->at<float>(p->lay.tmp);
+    h.M = p->n_own;
+    h.A = dh_out;
+    h.lda = d_out;
+    h.a_mask = relu ? h_out : nullptr;
+    h.C = tmp;
+    h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
+    {
+        Timed t(p, K_HALO_GRAD, layer, s);
+        if (digest_status st = hip_check(digest::launch_gemm(h, s), "halo gradient"))
+            return st;
+    }
+    return run_spmm(p, Csr::HaloT, tmp, nullptr, p->n_own, d_in, dh_halo, layer, s, nullptr,
+                    K_HALO_GRAD);
+}
+
+digest_status digest_push_add(digest_partition *p, int32_t level, const float *dh_halo,
+                              float *gstore, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (level < 1 || level >= p->L)
+        return fail(DIGEST_EINVAL, "gradient level %d outside [1, %d)", level, p->L);
+    if (!gstore || (p->n_halo > 0 && !dh_halo))
+        return fail(DIGEST_EINVAL, "NULL dh_halo or gradient store");
+    if (p->n_halo == 0)
+        return DIGEST_OK;
+    hipStream_t s = (hipStream_t)hip_stream;
+    Timed t(p, K_GRAD_PUSH, level, s);
+    return hip_check(digest::launch_add_rows(nullptr, p->at<int32_t>(p->lay.halo_gid),
+                                             p->n_halo, p->widths[level], dh_halo, gstore, s),
+                     "gradient push");
+}
+
+digest_status digest_pull_add(digest_partition *p, int32_t level, float *gstore, float *dh_own,
+                              void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (level < 1 || level >= p->L)
+        return fail(DIGEST_EINVAL, "gradient level %d outside [1, %d)", level, p->L);
+    if (!gstore || (p->n_own > 0 && !dh_own))
+        return fail(DIGEST_EINVAL, "NULL gradient store or dh_own");
+    if (p->n_own == 0)
+        return DIGEST_OK;
+    hipStream_t s = (hipStream_t)hip_stream;
+    Timed t(p, K_GRAD_PULL, level, s);
+    return hip_check(digest::launch_add_clear_rows(p->at<int32_t>(p->lay.owned_gid), nullptr,
+                                                   p->n_own, p->widths[level], gstore, dh_own,
+                                                   s),
+                     "gradient pull");
 }
 
 digest_status digest_sgd_average(float *w, const float *const *grads, int32_t n_grads,

@@ -116,13 +116,17 @@ __device__ __forceinline__ void stage_lds(float *dst, int count, F value)
 // Row copy (pull / push)
 // ---------------------------------------------------------------------------
 
-// A wave holds 64/GL groups of GL lanes; each group copies one row, lane j of
-// the group moving vectors j, j+GL, ...
-template <int VEC, int GL>
+// A wave holds 64/GL groups of GL lanes; each group moves one row, lane j of
+// the group handling vectors j, j+GL, ...  MODE: kCopy dst = src, kAdd
+// dst += src, kAddClear dst += src then src = 0 (each row of src and of
+// dst is touched by one group only, so no two lanes race).
+enum RowMode { kCopy = 0, kAdd = 1, kAddClear = 2 };
+
+template <int VEC, int GL, int MODE>
 __global__ __launch_bounds__(256) void k_copy_rows(const int32_t *__restrict__ sidx,
                                                    const int32_t *__restrict__ didx,
                                                    int32_t n_rows, int32_t d,
-                                                   const float *__restrict__ src,
+                                                   float *__restrict__ src,
                                                    float *__restrict__ dst)
 {
     constexpr int G = kWave / GL;
@@ -134,13 +138,27 @@ __global__ __launch_bounds__(256) void k_copy_rows(const int32_t *__restrict__ s
     const int gl = lane % GL;
     const int64_t sr = sidx ? sidx[r] : r;
     const int64_t dr = didx ? didx[r] : r;
-    const float *s = src + sr * d;
+    float *sp = src + sr * d;
     float *t = dst + dr * d;
     const int dv = d / VEC;
     for (int c = gl; c < dv; c += GL) {
         float x[VEC];
-        load_vec<VEC>(s + c * VEC, x);
+        load_vec<VEC>(sp + c * VEC, x);
+        if constexpr (MODE != kCopy) {
+            float y[VEC];
+            load_vec<VEC>(t + c * VEC, y);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                x[v] += y[v];
+        }
         store_vec<VEC>(t + c * VEC, x);
+        if constexpr (MODE == kAddClear) {
+            float z[VEC];
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                z[v] = 0.f;
+            store_vec<VEC>(sp + c * VEC, z);
+        }
     }
 }
 
@@ -1155,26 +1173,34 @@ int pick_group(int32_t dv)
 }
 
 template <int VEC, int GL>
-hipError_t copy_rows_t(const int32_t *sidx, const int32_t *didx, int32_t n_rows, int32_t d,
-                       const float *src, float *dst, hipStream_t s)
+hipError_t copy_rows_t(int mode, const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                       int32_t d, float *src, float *dst, hipStream_t s)
 {
     constexpr int rows_per_block = 4 * (kWave / GL);
     const int64_t blocks = ((int64_t)n_rows + rows_per_block - 1) / rows_per_block;
-    hipLaunchKernelGGL((k_copy_rows<VEC, GL>), dim3((unsigned)blocks), dim3(256), 0, s, sidx,
-                       didx, n_rows, d, src, dst);
+    const dim3 grid((unsigned)blocks), block(256);
+    if (mode == kAdd)
+        hipLaunchKernelGGL((k_copy_rows<VEC, GL, kAdd>), grid, block, 0, s, sidx, didx, n_rows, d,
+                           src, dst);
+    else if (mode == kAddClear)
+        hipLaunchKernelGGL((k_copy_rows<VEC, GL, kAddClear>), grid, block, 0, s, sidx, didx,
+                           n_rows, d, src, dst);
+    else
+        hipLaunchKernelGGL((k_copy_rows<VEC, GL, kCopy>), grid, block, 0, s, sidx, didx, n_rows,
+                           d, src, dst);
     return hipGetLastError();
 }
 
 template <int VEC>
-hipError_t copy_rows_v(int gl, const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                       int32_t d, const float *src, float *dst, hipStream_t s)
+hipError_t copy_rows_v(int gl, int mode, const int32_t *sidx, const int32_t *didx,
+                       int32_t n_rows, int32_t d, float *src, float *dst, hipStream_t s)
 {
     switch (gl) {
-    case 4: return copy_rows_t<VEC, 4>(sidx, didx, n_rows, d, src, dst, s);
-    case 8: return copy_rows_t<VEC, 8>(sidx, didx, n_rows, d, src, dst, s);
-    case 16: return copy_rows_t<VEC, 16>(sidx, didx, n_rows, d, src, dst, s);
-    case 32: return copy_rows_t<VEC, 32>(sidx, didx, n_rows, d, src, dst, s);
-    default: return copy_rows_t<VEC, 64>(sidx, didx, n_rows, d, src, dst, s);
+    case 4: return copy_rows_t<VEC, 4>(mode, sidx, didx, n_rows, d, src, dst, s);
+    case 8: return copy_rows_t<VEC, 8>(mode, sidx, didx, n_rows, d, src, dst, s);
+    case 16: return copy_rows_t<VEC, 16>(mode, sidx, didx, n_rows, d, src, dst, s);
+    case 32: return copy_rows_t<VEC, 32>(mode, sidx, didx, n_rows, d, src, dst, s);
+    default: return copy_rows_t<VEC, 64>(mode, sidx, didx, n_rows, d, src, dst, s);
     }
 }
 
@@ -1302,18 +1328,40 @@ hipError_t gemm_q(const GemmArgs &a, hipStream_t s)
 
 }  // namespace
 
-hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                            int32_t d, const float *src, float *dst, hipStream_t s)
+namespace {
+
+hipError_t move_rows(int mode, const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                     int32_t d, float *src, float *dst, hipStream_t s)
 {
     if (n_rows <= 0 || d <= 0)
         return hipSuccess;
     const int vec = pick_vec(d, src, dst);
     const int gl = pick_group(d / vec);
     switch (vec) {
-    case 4: return copy_rows_v<4>(gl, sidx, didx, n_rows, d, src, dst, s);
-    case 2: return copy_rows_v<2>(gl, sidx, didx, n_rows, d, src, dst, s);
-    default: return copy_rows_v<1>(gl, sidx, didx, n_rows, d, src, dst, s);
+    case 4: return copy_rows_v<4>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
+    case 2: return copy_rows_v<2>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
+    default: return copy_rows_v<1>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
     }
+}
+
+}  // namespace
+
+hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                            int32_t d, const float *src, float *dst, hipStream_t s)
+{
+    return move_rows(kCopy, sidx, didx, n_rows, d, const_cast<float *>(src), dst, s);
+}
+
+hipError_t launch_add_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows, int32_t d,
+                           const float *src, float *dst, hipStream_t s)
+{
+    return move_rows(kAdd, sidx, didx, n_rows, d, const_cast<float *>(src), dst, s);
+}
+
+hipError_t launch_add_clear_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                                 int32_t d, float *src, float *dst, hipStream_t s)
+{
+    return move_rows(kAddClear, sidx, didx, n_rows, d, src, dst, s);
 }
 
 bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2)

@@ -25,6 +25,13 @@ constexpr int32_t kSpmmLongRow = 64;
 // dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows.
 hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
                             int32_t d, const float *src, float *dst, hipStream_t s);
+// The same with dst += src; the listed destination rows must be distinct.
+hipError_t launch_add_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows, int32_t d,
+                           const float *src, float *dst, hipStream_t s);
+// dst += src, then the source rows are set to zero; the listed source rows
+// and the listed destination rows must each be distinct.
+hipError_t launch_add_clear_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
+                                 int32_t d, float *src, float *dst, hipStream_t s);
 
 // Two-source CSR aggregation out[r] = sum_k val[k] * src(col[k]) over the
 // rows named by the blocks.  Column c < n_src0 reads row c of src0,

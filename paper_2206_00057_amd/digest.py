@@ -54,6 +54,9 @@ def lib():
             "digest_layer_backward": ([P, i32, P, P, P, P, P, P, P], st),
             "digest_softmax_xent": ([P, P, P, P, P, P], st),
             "digest_sgd_average": ([P, P, i32, i64, ctypes.c_float, P], st),
+            "digest_halo_gradient": ([P, i32, P, P, P, P, P], st),
+            "digest_push_add": ([P, i32, P, P, P], st),
+            "digest_pull_add": ([P, i32, P, P, P], st),
             "digest_sync_period": ([i32, i64, P, P], st),
             "digest_profile_enable": ([P, i32], st),
             "digest_profile_read": ([P, P, P], st),
@@ -256,6 +259,40 @@ def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):
     c = _dev(dlogits, torch.float32, p.n_own * C, "dlogits")
     d = _dev(loss, torch.float32, 1, "loss")
     _check(lib().digest_softmax_xent(p.handle, a, b, c, d, _stream(stream)))
+
+
+def digest_halo_gradient(p, layer, h_out, dh_out, w, dh_halo, stream=None):
+    """dh_halo = P_out^T D W^T for the halo rows of level layer-1."""
+    import torch
+    _check_layer(p, layer)
+    d_in, d_out = p.widths[layer - 1], p.widths[layer]
+    _check(lib().digest_halo_gradient(
+        p.handle, int(layer), _dev(h_out, torch.float32, p.n_own * d_out, "h_out"),
+        _dev(dh_out, torch.float32, p.n_own * d_out, "dh_out"),
+        _dev(w, torch.float32, d_in * d_out, "w"),
+        _dev(dh_halo, torch.float32, p.n_halo * d_in, "dh_halo"), _stream(stream)))
+
+
+def digest_push_add(p, level, dh_halo, gstore, stream=None):
+    """gstore[halo] += dh_halo (level 1..L-1)."""
+    import torch
+    _check_level(p, level, 1)
+    d = p.widths[level]
+    _check(lib().digest_push_add(p.handle, int(level),
+                                 _dev(dh_halo, torch.float32, p.n_halo * d, "dh_halo"),
+                                 _dev(gstore, torch.float32, p.n_global * d, "gstore"),
+                                 _stream(stream)))
+
+
+def digest_pull_add(p, level, gstore, dh_own, stream=None):
+    """dh_own += gstore[owned]; gstore[owned] = 0 (level 1..L-1)."""
+    import torch
+    _check_level(p, level, 1)
+    d = p.widths[level]
+    _check(lib().digest_pull_add(p.handle, int(level),
+                                 _dev(gstore, torch.float32, p.n_global * d, "gstore"),
+                                 _dev(dh_own, torch.float32, p.n_own * d, "dh_own"),
+                                 _stream(stream)))
 
 
 def digest_sgd_average(w, grads, lr, stream=None):

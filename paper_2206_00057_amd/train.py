@@ -13,12 +13,21 @@ Round r (1-based), sync interval K, M subgraphs:
     W <- W - lr * (1/M) sum_m dW_m        (AGG of the M local models)
 
 The subgraphs advance layer by layer together (all forwards of layer l, then
-all pushes of level l, then the pulls of level l before layer l+1), the
-synchronous barrier of Algorithm 1 at layer granularity.  With K = 1 every
+all pushes of level l, then the pulls of level l before layer l+1; the
+backward likewise, layer L down to 1), the synchronous barrier of
+Algorithm 1 at layer granularity.  With K = 1 every
 halo row a subgraph reads was pushed by its owner earlier in the same round,
 so each subgraph's forward equals the full-graph GCN forward on its rows
 (P_m = P_in + P_out with fresh halo rows).  With K > 1 the halo rows are the
 stale ones of the last push round.
+
+grad_exchange adds the appendix's stale-gradient term: after the backward of
+layer l >= 2, every subgraph's halo gradient P_out^T D W^T goes into a
+per-level gradient store (digest_push_add) and each owner adds its rows to
+its input gradient (digest_pull_add) -- in the same round ("fresh": with
+K = 1 the mean of the subgraphs' gradients is then the full-graph gradient)
+or one round later ("stale", the t-1 of the appendix).  "none" keeps halo
+rows as constants.
 
 All arithmetic runs in libdigest.so (the layers, pulls, pushes, loss heads
 and the parameter averaging); this module owns the buffers and orders the
@@ -33,13 +42,17 @@ from .step import GpuPartition
 
 
 class DigestTrainer:
-    def __init__(self, n_global, parts, widths, x, labels, weights, lr, K, device="cuda"):
+    def __init__(self, n_global, parts, widths, x, labels, weights, lr, K, device="cuda",
+                 grad_exchange="none"):
         """parts: synth-style partitions (owned, halo, CSR rows) covering the
         graph; x: device [n_global, d_0] features; labels: device int32
         [n_global]; weights: device float32 tensors W_1..W_L (the global
         parameters, updated in place by every round)."""
         if not 1 <= len(parts) <= 64:
             raise ValueError("between 1 and 64 subgraphs")
+        if grad_exchange not in ("none", "fresh", "stale"):
+            raise ValueError("grad_exchange is none, fresh or stale")
+        self.grad_exchange = grad_exchange
         self.widths = [int(w) for w in widths]
         self.L = len(self.widths) - 1
         self.n_global = int(n_global)
@@ -54,6 +67,12 @@ class DigestTrainer:
         self.stores = [x] + [torch.zeros(n_global, self.widths[l], **f32)
                              for l in range(1, self.L)]
         self.losses = torch.zeros(len(parts), **f32)
+        if grad_exchange != "none":
+            # gradient stores (levels 1..L-1) and each subgraph's halo gradients
+            self.gstores = [None] + [torch.zeros(n_global, self.widths[l], **f32)
+                                     for l in range(1, self.L)]
+            self.dh_halo = [[None] + [torch.empty(p.n_halo, self.widths[l], **f32)
+                                      for l in range(1, self.L)] for p in parts]
         self.graphs = {}
         self.edges_per_round = sum(gp.p.nnz + (gp.p.nnz_in if l > 1 else 0)
                                    for gp in self.gps for l in range(1, self.L + 1))
@@ -95,13 +114,34 @@ class DigestTrainer:
         for m, gp in enumerate(self.gps):
             D.digest_softmax_xent(gp.p, gp.H[self.L], self.y_own[m], gp.dH[self.L],
                                   self.losses[m:m + 1])
-            for l in range(self.L, 0, -1):
+        for l in range(self.L, 0, -1):
+            for m, gp in enumerate(self.gps):
                 dh_in = gp.dH[l - 1] if l > 1 else None
                 h_in = gp.H[l - 1] if l > 1 else self.x_own[m]
                 D.digest_layer_backward(gp.p, l, h_in, gp.H[l], gp.dH[l], self.W[l - 1],
                                         gp.dW[l], dh_in)
+            if l > 1 and self.grad_exchange != "none":
+                self._exchange(l)
         for l in range(1, self.L + 1):
             D.digest_sgd_average(self.W[l - 1], [gp.dW[l] for gp in self.gps], self.lr)
+
+    def _exchange(self, l):
+        """Halo gradients of layer l into the level l-1 store and back to the
+        owners' input gradients (fresh: this round's; stale: last round's)."""
+        gs = self.gstores[l - 1]
+        for m, gp in enumerate(self.gps):
+            D.digest_halo_gradient(gp.p, l, gp.H[l], gp.dH[l], self.W[l - 1],
+                                   self.dh_halo[m][l - 1])
+        if self.grad_exchange == "fresh":
+            for m, gp in enumerate(self.gps):
+                D.digest_push_add(gp.p, l - 1, self.dh_halo[m][l - 1], gs)
+            for gp in self.gps:
+                D.digest_pull_add(gp.p, l - 1, gs, gp.dH[l - 1])
+        else:
+            for gp in self.gps:
+                D.digest_pull_add(gp.p, l - 1, gs, gp.dH[l - 1])
+            for m, gp in enumerate(self.gps):
+                D.digest_push_add(gp.p, l - 1, self.dh_halo[m][l - 1], gs)
 
     def round(self, r):
         """Round r (1-based), eagerly."""

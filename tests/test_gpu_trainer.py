@@ -51,20 +51,24 @@ def test_sgd_average_matches_oracle(M, count):
     np.testing.assert_allclose(host(gw), ref, rtol=1e-5, atol=1e-6)
 
 
-def _setup(cfg, seed=0, K=2, lr=0.5):
+def _setup(cfg, seed=0, K=2, lr=0.5, grad_exchange="none"):
     from paper_2206_00057_amd.train import DigestTrainer
     g = synth.make_graph(cfg, seed=seed)
     parts = [synth.make_partition(cfg, g, m) for m in range(synth.num_partitions(cfg))]
     X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
-    tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws], lr, K)
-    ot = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, lr, K)
+    tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws], lr, K,
+                       grad_exchange=grad_exchange)
+    ot = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, lr, K,
+                              grad_exchange=grad_exchange)
     return g, parts, tr, ot
 
 
-@pytest.mark.parametrize("K", [1, 3])
-def test_trainer_rounds_match_oracle(K):
+@pytest.mark.parametrize("K,mode", [(1, "none"), (3, "none"), (1, "fresh"), (2, "stale")])
+def test_trainer_rounds_match_oracle(K, mode):
     cfg = synth.CONFIGS["tiny"]
-    g, parts, tr, ot = _setup(cfg, K=K)
+    if mode != "none":   # a 3-layer model: the exchange runs at two levels
+        cfg = synth.scaled(cfg, 2000, widths=(64, 48, 32, 16))
+    g, parts, tr, ot = _setup(cfg, K=K, grad_exchange=mode)
     tr.init_stores()
     ot.init_stores()
     for lev in range(1, cfg.layers):
@@ -125,3 +129,95 @@ def test_trainer_graph_replay_matches_eager():
             np.testing.assert_array_equal(host(tr.W[l]).view(np.uint32),
                                           eager[r - 1][l].view(np.uint32),
                                           err_msg=f"replay round {r} W{l + 1}")
+
+
+@pytest.mark.parametrize("widths", [(24, 40, 6), (24, 200, 48), (24, 40, 48)],
+                         ids=["narrow-out", "gemm-out", "wide-out"])
+def test_halo_gradient_matches_oracle(widths):
+    """Each case runs ReLU (GEMM with the mask, then the transposed halo
+    aggregation) and identity; identity with d_out < d_in aggregates first,
+    then contracts by the narrow-output VALU kernel (6) or the MFMA GEMM (48
+    of 200); with d_out >= d_in it takes the GEMM-first order."""
+    from paper_2206_00057_amd import digest as D
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=4)
+    p = synth.make_partition(cfg, g, 2)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                  cfg.widths)
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    D.digest_partition_bind_workspace(h, ws)
+    op = oracle.OraclePartition(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    store = synth.relu_normal((g.n, widths[1]), seed=5)
+    D.digest_pull(h, 1, dev(store))
+    op.pull(1, store)
+    h_in = synth.relu_normal((p.n_own, widths[1]), seed=6)
+    W = synth.weights(cfg)[1]
+    for act in (oracle.RELU, oracle.IDENTITY):
+        out = torch.empty(p.n_own, widths[2], device="cuda")
+        D.digest_layer_forward(h, 2, dev(h_in), dev(W), out, act)
+        h_out = op.forward(2, h_in, W, act)
+        dh = synth.normal((p.n_own, widths[2]), seed=7, scale=1.0 / p.n_own)
+        got = torch.empty(p.n_halo, widths[1], device="cuda")
+        D.digest_halo_gradient(h, 2, dev(h_out), dev(dh), dev(W), got)
+        ref = op.halo_gradient(2, W, h_out, dh, act)
+        assert_close(host(got), ref, f"halo gradient {widths} act {act}", scale_tol=2e-5)
+
+
+def test_gradient_push_add_and_pull_add_bit_exact():
+    from paper_2206_00057_amd import digest as D
+    cfg = synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    hs, bufs = [], []
+    for p in parts:
+        h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                      cfg.widths)
+        bufs.append(torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda"))
+        D.digest_partition_bind_workspace(h, bufs[-1])
+        hs.append(h)
+    d = cfg.widths[1]
+    gs = np.zeros((g.n, d), np.float32)
+    ggs = dev(gs)
+    for m, (p, h) in enumerate(zip(parts, hs)):
+        dh = synth.normal((p.n_halo, d), seed=80 + m)
+        D.digest_push_add(h, 1, dev(dh), ggs)
+        oracle.push_add(gs, p.halo, dh)
+    np.testing.assert_array_equal(host(ggs).view(np.uint32), gs.view(np.uint32))
+    for m, (p, h) in enumerate(zip(parts, hs)):
+        own = synth.normal((p.n_own, d), seed=90 + m)
+        gown = dev(own)
+        D.digest_pull_add(h, 1, ggs, gown)
+        ref = oracle.pull_add(gs, p.owned, own)
+        np.testing.assert_array_equal(host(gown).view(np.uint32), ref.view(np.uint32))
+    assert not host(ggs).any()   # every row was pulled and cleared by its owner
+
+
+def test_gradient_exchange_calls_check_level_and_order():
+    """Halo gradients exist for layers 2..L only and need that layer's
+    forward first; gradient stores have levels 1..L-1.  Every rejected call
+    returns before a launch."""
+    import ctypes
+    from paper_2206_00057_amd import digest as D
+    cfg = synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    p = synth.make_partition(cfg, g, 0)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                  cfg.widths)
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    D.digest_partition_bind_workspace(h, ws)
+    torch.cuda.synchronize()
+    L = D.lib()
+    buf = torch.zeros(g.n * 64, device="cuda")
+    a = ctypes.c_void_p(buf.data_ptr())
+    for layer in (0, 1, cfg.layers + 1):
+        assert L.digest_halo_gradient(h.handle, layer, a, a, a, a, None) == D.EINVAL
+    assert L.digest_halo_gradient(h.handle, 2, a, a, None, a, None) == D.EINVAL
+    assert L.digest_halo_gradient(h.handle, 2, a, a, a, a, None) == D.ESTATE
+    assert b"forward" in L.digest_last_error()
+    for level in (0, cfg.layers):
+        assert L.digest_push_add(h.handle, level, a, a, None) == D.EINVAL
+        assert L.digest_pull_add(h.handle, level, a, a, None) == D.EINVAL
+    assert L.digest_push_add(h.handle, 1, a, None, None) == D.EINVAL
+    assert L.digest_pull_add(h.handle, 1, None, a, None) == D.EINVAL
+    torch.cuda.synchronize()
+

@@ -12,7 +12,13 @@ the mathematics fix, never against the oracle itself:
     round;
   * sync interval 3: before the first pull round the halo rows are those of
     the initial store, so after one SGD step the logits differ from the
-    full-graph ones at the new W exactly by P_out (H~ - H) W on the rows.
+    full-graph ones at the new W exactly by P_out (H~ - H) W on the rows;
+  * the halo gradient P_out^T D W^T against the dense formula;
+  * with the halo gradients exchanged in the same round and sync interval 1,
+    the mean of the equal-sized subgraphs' gradients is the full-graph
+    gradient, so M subgraphs train exactly like full-graph GCN (torch float64
+    autograd); exchanged one round late, the first round equals the one
+    without exchange (the gradient store starts empty).
 """
 import numpy as np
 import pytest
@@ -158,3 +164,90 @@ def test_stale_halo_rows_before_the_first_pull():
         ref = full2[-1][p.owned] + Pout @ (H1_stale - full2[1]) @ W2[1].astype(np.float64)
         np.testing.assert_allclose(logits, ref, rtol=1e-5, atol=1e-6)
         assert np.abs(logits - full2[-1][p.owned]).max() > 1e-6   # staleness is visible
+
+
+# --------------------------------------------------------------------------
+# halo gradients (the appendix's P_out^T term)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("act", [oracle.RELU, oracle.IDENTITY])
+def test_halo_gradient_matches_dense_formula(act):
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=8)
+    A = dense(g)
+    p = synth.make_partition(cfg, g, 1)
+    rng = np.random.default_rng(3)
+    d_in, d_out = 5, 4
+    w = rng.standard_normal((d_in, d_out)).astype(np.float32)
+    h_out = rng.standard_normal((p.n_own, d_out)).astype(np.float32)
+    dh_out = rng.standard_normal((p.n_own, d_out)).astype(np.float32)
+    op = oracle.OraclePartition(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                (d_in, d_out))
+    got = op.halo_gradient(1, w, h_out, dh_out, act)
+    D = dh_out.astype(np.float64) * ((h_out > 0) if act == oracle.RELU else 1.0)
+    ref = A[np.ix_(p.owned, p.halo)].T @ D @ w.astype(np.float64).T
+    np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-7)
+
+
+def _torch_full_graph_sgd(A, X, y, Ws, lr, rounds):
+    At = torch.tensor(A)
+    Xt = torch.tensor(X, dtype=torch.float64)
+    yt = torch.tensor(y, dtype=torch.int64)
+    Wt = [torch.tensor(w, dtype=torch.float64, requires_grad=True) for w in Ws]
+    traj = []
+    for _ in range(rounds):
+        h = Xt
+        for l, W in enumerate(Wt):
+            z = At @ h @ W
+            h = torch.relu(z) if l < len(Wt) - 1 else z
+        loss = torch.nn.functional.cross_entropy(h, yt)
+        grads = torch.autograd.grad(loss, Wt)
+        with torch.no_grad():
+            Wt = [(W - lr * gW).requires_grad_(True) for W, gW in zip(Wt, grads)]
+        traj.append([W.detach().numpy().copy() for W in Wt])
+    return traj
+
+
+@pytest.mark.parametrize("widths", [(6, 5, 3), (6, 5, 4, 3)])
+def test_fresh_gradient_exchange_trains_like_full_graph(widths):
+    cfg = cfg_small(widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=9)
+    A = dense(g)
+    X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    assert len({p.n_own for p in parts}) == 1      # equal sizes: mean of local means
+    lr = 0.5
+    tr = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, lr, K=1, grad_exchange="fresh")
+    tr.init_stores()
+    ref = _torch_full_graph_sgd(A, X, y, Ws, lr, 3)
+    for r in (1, 2, 3):
+        tr.round(r)
+        for l in range(len(Ws)):
+            np.testing.assert_allclose(tr.W[l], ref[r - 1][l], rtol=1e-5, atol=1e-6)
+    # without the exchange the same rounds do not follow full-graph SGD
+    plain = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, lr, K=1)
+    plain.init_stores()
+    plain.round(1)
+    assert max(np.abs(plain.W[l] - ref[0][l]).max() for l in range(len(Ws))) > 1e-4
+
+
+def test_stale_gradient_exchange_first_round_has_nothing_to_add():
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=10)
+    X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    runs = {}
+    for mode in ("none", "stale", "fresh"):
+        tr = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, 0.5, K=2, grad_exchange=mode)
+        tr.init_stores()
+        tr.round(1)
+        w1 = [w.copy() for w in tr.W]
+        tr.round(2)
+        runs[mode] = (w1, [w.copy() for w in tr.W])
+    for l in range(cfg.layers):
+        np.testing.assert_array_equal(runs["stale"][0][l], runs["none"][0][l])
+    assert max(np.abs(runs["stale"][1][l] - runs["none"][1][l]).max()
+               for l in range(cfg.layers)) > 1e-6
+    assert max(np.abs(runs["fresh"][0][l] - runs["none"][0][l]).max()
+               for l in range(cfg.layers)) > 1e-6
+
