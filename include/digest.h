@@ -218,6 +218,25 @@ digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const flo
                                    void *hip_stream);
 
 /*
+ * Layer backward with the halo gradient (the appendix's DIGEST backward
+ * with its stale-gradient term): the outputs of digest_layer_backward
+ * (dw, dh_in) and the dh_halo of digest_halo_gradient, from shared
+ * products.  The transposed aggregation runs over all of P_m^T, so D W^T
+ * (or P_m^T D) is formed once for the owned and the halo rows.
+ *   layer 2..L;  dh_in device [n_owned, d_{layer-1}] (required when
+ *   n_owned > 0);  dh_halo device [n_halo, d_{layer-1}] (required when
+ *   n_halo > 0); other arguments as for digest_layer_backward.
+ * Results equal those of the two separate calls up to float32 rounding
+ * order.
+ * Errors: those of digest_layer_backward; DIGEST_EINVAL for layer 1 or a
+ * NULL dh_in / dh_halo.
+ */
+digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, const float *h_in,
+                                         const float *h_out, const float *dh_out,
+                                         const float *w, float *dw, float *dh_in,
+                                         float *dh_halo, void *hip_stream);
+
+/*
  * Gradient push: add this subgraph's halo gradient of level `level` into a
  * gradient store indexed by node id, gstore[halo[j], :] += dh_halo[j, :]
  * (float32 adds; the halo ids are distinct, so one call never adds twice to

@@ -349,7 +349,8 @@ enum class Csr { Fwd, InT, FullT, HaloT };
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
-                       const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1)
+                       const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
+                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX)
 {
     const bool fwd = which == Csr::Fwd;
     const std::vector<SpmmBlock> *blocks = &p->blocks_f;
@@ -370,7 +371,7 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
                             p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1, n_src0, d,
-                            out, s, ep),
+                            out, s, ep, out1, n_out0),
         "spmm");
 }
 
@@ -788,11 +789,37 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
 
 namespace {
 
+// C[rows][d_in] = A[rows][d_out] W^T (W row-major [d_in][d_out]): the VALU
+// kernel for outputs of narrow contractions, else the MFMA GEMM.
+digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A, const float *w,
+                       float *C, hipStream_t s)
+{
+    if (narrow_valu(d_in, d_out))
+        return hip_check(digest::launch_narrow_k(rows, d_in, d_out, A, d_out, w, C, d_in, s),
+                         "times W^T (narrow)");
+    digest::GemmArgs h{};
+    h.M = rows;
+    h.N = d_in;
+    h.K = d_out;
+    h.A = A;
+    h.lda = d_out;
+    h.B = w;
+    h.ldb = d_out;
+    h.b_trans = true;
+    h.C = C;
+    h.ldc = d_in;
+    h.splits = 1;
+    h.kchunk = d_out;
+    h.tile = gemm_tile_for(rows, d_in, d_out, false);
+    return hip_check(digest::launch_gemm(h, s), "times W^T");
+}
+
 // dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer, with
-// G = P_m^T D over all local rows (halo rows of G only feed dW).
+// G = P_m^T D over all local rows.  The halo rows of G feed dW and, when
+// dh_halo is given, the halo gradient G_halo W^T.
 digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
                                        const float *dh_out, const float *w, float *dw,
-                                       float *dh_in, hipStream_t s)
+                                       float *dh_in, float *dh_halo, hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
@@ -801,8 +828,9 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
     // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
     // same launch also writes dh_in = G_own W^T for the owned rows.
     const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
-                          digest::spmm_epilogue_ok(d_out, d_in, dh_in);
-    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in};
+                          digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
+                          (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
+    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
     if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
                                     fused_dh ? &ep : nullptr))
         return st;
@@ -852,53 +880,39 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                 "dW reduce"))
             return st;
     }
-    if (!dh_in || fused_dh)
+    if (fused_dh)
         return DIGEST_OK;
-    Timed tm(p, K_GEMM_DH, layer, s);
-    if (narrow_valu(d_in, d_out))
-        return hip_check(
-            digest::launch_narrow_k(p->n_own, d_in, d_out, G, d_out, w, dh_in, d_in, s),
-            "dgrad narrow");
-    digest::GemmArgs h{};
-    h.M = p->n_own;
-    h.N = d_in;
-    h.K = d_out;
-    h.A = G;
-    h.lda = d_out;
-    h.B = w;
-    h.ldb = d_out;
-    h.b_trans = true;
-    h.C = dh_in;
-    h.ldc = d_in;
-    h.splits = 1;
-    h.kchunk = d_out;
-    h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
-    return hip_check(digest::launch_gemm(h, s), "dgrad gemm");
+    if (dh_in) {
+        Timed tm(p, K_GEMM_DH, layer, s);
+        if (digest_status st = times_wt(p->n_own, d_in, d_out, G, w, dh_in, s))
+            return st;
+    }
+    if (!dh_halo || p->n_halo == 0)
+        return DIGEST_OK;
+    Timed tm(p, K_HALO_GRAD, layer, s);
+    return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * d_out, w, dh_halo, s);
 }
 
 }  // namespace
 
-digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_in,
-                                    const float *h_out, const float *dh_out, const float *w,
-                                    float *dw, float *dh_in, void *hip_stream)
+}  // extern "C"
+
+namespace {
+
+// The layer backward of both entry points.  With dh_halo (layer >= 2, dh_in
+// given) the halo rows' gradient P_out^T D W^T comes out of the same
+// products: the transposed aggregation runs over all of P_m^T, its owned
+// rows into dh_in and its halo rows into dh_halo (or, aggregating first,
+// into the halo scratch that one more product by W^T finishes).
+digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_in,
+                             const float *h_out, const float *dh_out, const float *w, float *dw,
+                             float *dh_in, float *dh_halo, hipStream_t s)
 {
-    if (digest_status st = need_bound(p))
-        return st;
-    if (layer < 1 || layer > p->L)
-        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
-    if (!dw || !w || (p->n_own > 0 && (!h_in || !h_out || !dh_out)))
-        return fail(DIGEST_EINVAL, "NULL h_in, h_out, dh_out, w or dw");
-    if (!p->fwd_done[layer])
-        return fail(DIGEST_ESTATE, "no forward of layer %d since the workspace was bound",
-                    layer);
-    if (p->fwd_gen[layer] != p->pull_gen[layer - 1])
-        return fail(DIGEST_ESTATE,
-                    "level %d was pulled again between the forward and backward of layer %d",
-                    layer - 1, layer);
-    hipStream_t s = (hipStream_t)hip_stream;
+    if (p->n_halo == 0)
+        dh_halo = nullptr;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     if (p->tf[layer] && p->n_own > 0)
-        return backward_transform_first(p, layer, h_in, dh_out, w, dw, dh_in, s);
+        return backward_transform_first(p, layer, h_in, dh_out, w, dw, dh_in, dh_halo, s);
     const bool relu = p->act[layer] == DIGEST_ACT_RELU;
     const float *ah = p->at<float>(p->lay.ah[layer]);
 
@@ -933,7 +947,28 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     if (!dh_in || p->n_own == 0)
         return DIGEST_OK;
 
+    // P_in^T alone, or P_m^T with its halo rows split off
+    const Csr tr = dh_halo ? Csr::FullT : Csr::InT;
+    const int32_t split = dh_halo ? p->n_own : INT32_MAX;
     float *tmp = p->at<float>(p->lay.tmp);
+    if (!relu && d_out < d_in) {
+        // Narrower output: aggregate D first (width d_out), then times W^T.
+        float *gh = p->at<float>(p->lay.tmp_halo);
+        if (digest_status st = run_spmm(p, tr, dh_out, nullptr, p->n_own, d_out, tmp, layer, s,
+                                        nullptr, -1, dh_halo ? gh : nullptr, split))
+            return st;
+        {
+            Timed t(p, K_GEMM_DH, layer, s);
+            if (digest_status st = times_wt(p->n_own, d_in, d_out, tmp, w, dh_in, s))
+                return st;
+        }
+        if (!dh_halo)
+            return DIGEST_OK;
+        Timed t(p, K_HALO_GRAD, layer, s);
+        return times_wt(p->n_halo, d_in, d_out, gh, w, dh_halo, s);
+    }
+    // Otherwise G = D W^T (mask fused into the operand load), then the
+    // transposed aggregation of G.
     digest::GemmArgs h{};
     h.M = p->n_own;
     h.N = d_in;
@@ -945,17 +980,6 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
     h.splits = 1;
     h.kchunk = d_out;
     h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
-    if (!relu && d_out < d_in) {
-        // Narrower output: aggregate D first (width d_out), then (P_in^T D) W^T.
-        if (digest_status st = run_spmm(p, Csr::InT, dh_out, nullptr, p->n_own, d_out, tmp, layer, s))
-            return st;
-        h.A = tmp;
-        h.lda = d_out;
-        h.C = dh_in;
-        Timed t(p, K_GEMM_DH, layer, s);
-        return hip_check(digest::launch_gemm(h, s), "dgrad gemm");
-    }
-    // Otherwise G = D W^T (mask fused into the operand load), then P_in^T G.
     h.A = dh_out;
     h.lda = d_out;
     h.a_mask = relu ? h_out : nullptr;
@@ -965,7 +989,60 @@ digest_status digest_layer_backward(digest_partition *p, int32_t layer, const fl
         if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
             return st;
     }
-    return run_spmm(p, Csr::InT, tmp, nullptr, p->n_own, d_in, dh_in, layer, s);
+    return run_spmm(p, tr, tmp, nullptr, p->n_own, d_in, dh_in, layer, s, nullptr, -1, dh_halo,
+                    split);
+}
+
+// Argument and state checks shared by both backward entry points.
+digest_status check_backward(const digest_partition *p, int32_t layer, const float *h_in,
+                             const float *h_out, const float *dh_out, const float *w,
+                             const float *dw)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    if (!dw || !w || (p->n_own > 0 && (!h_in || !h_out || !dh_out)))
+        return fail(DIGEST_EINVAL, "NULL h_in, h_out, dh_out, w or dw");
+    if (!p->fwd_done[layer])
+        return fail(DIGEST_ESTATE, "no forward of layer %d since the workspace was bound",
+                    layer);
+    if (p->fwd_gen[layer] != p->pull_gen[layer - 1])
+        return fail(DIGEST_ESTATE,
+                    "level %d was pulled again between the forward and backward of layer %d",
+                    layer - 1, layer);
+    return DIGEST_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+digest_status digest_layer_backward(digest_partition *p, int32_t layer, const float *h_in,
+                                    const float *h_out, const float *dh_out, const float *w,
+                                    float *dw, float *dh_in, void *hip_stream)
+{
+    if (digest_status st = check_backward(p, layer, h_in, h_out, dh_out, w, dw))
+        return st;
+    return layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in, nullptr,
+                          (hipStream_t)hip_stream);
+}
+
+digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, const float *h_in,
+                                         const float *h_out, const float *dh_out,
+                                         const float *w, float *dw, float *dh_in,
+                                         float *dh_halo, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (layer < 2 || layer > p->L)
+        return fail(DIGEST_EINVAL, "halo gradient of layer %d outside [2, %d]", layer, p->L);
+    if ((p->n_own > 0 && !dh_in) || (p->n_halo > 0 && !dh_halo))
+        return fail(DIGEST_EINVAL, "NULL dh_in or dh_halo");
+    if (digest_status st = check_backward(p, layer, h_in, h_out, dh_out, w, dw))
+        return st;
+    return layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_halo,
+                          (hipStream_t)hip_stream);
 }
 
 digest_status digest_softmax_xent(digest_partition *p, const float *logits,

@@ -187,13 +187,28 @@ constexpr int spmm_inflight(int groups, int nch, int vec)
 // of a group accumulates the feature vectors gl, gl + GL, ... (NCH of them
 // per column pass).  Entry ids and weights are fetched 64 at a time (one per
 // lane) and broadcast; up to U entries per group are in flight.
+// Destination of an aggregation's rows: row r < n0 is out0 + r d, row
+// r >= n0 is out1 + (r - n0) d.  n0 = INT32_MAX makes one contiguous output;
+// a split lets one launch over P_m^T write the owned rows and the halo rows
+// to buffers of their own.
+struct SpmmOut {
+    float *out0;
+    float *out1;
+    int32_t n0;
+
+    __device__ __forceinline__ float *row(int32_t r, int32_t d) const
+    {
+        return r < n0 ? out0 + (int64_t)r * d : out1 + (int64_t)(r - n0) * d;
+    }
+};
+
 template <int VEC, int GL, int NCH, bool TWO>
 __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__restrict__ rowptr,
                                            const int32_t *__restrict__ col,
                                            const float *__restrict__ val,
                                            const float *__restrict__ src0,
                                            const float *__restrict__ src1, int32_t n_src0,
-                                           int32_t d, float *__restrict__ out,
+                                           int32_t d, const SpmmOut out,
                                            float (*red)[NCH * GL * VEC])
 {
     constexpr int G = kWave / GL;
@@ -297,7 +312,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
                 for (int ch = 0; ch < NCH; ++ch) {
                     const int c = c0 + ch * GL + gl;
                     if (c < dv)
-                        store_vec<VEC>(out + (int64_t)row * d + c * VEC, acc[ch]);
+                        store_vec<VEC>(out.row(row, d) + c * VEC, acc[ch]);
                 }
             }
         } else {
@@ -316,7 +331,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
 #pragma unroll
                     for (int w = 0; w < kSpmmWaves; ++w)
                         sum += red[w][t];
-                    out[(int64_t)row * d + (int64_t)c * VEC + t % VEC] = sum;
+                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = sum;
                 }
             }
             __syncthreads();
@@ -350,11 +365,19 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restri
                                                        const float *__restrict__ src0,
                                                        const float *__restrict__ src1,
                                                        int32_t n_src0, int32_t d,
-                                                       float *__restrict__ out)
+                                                       SpmmOut out)
 {
     __shared__ float red[kSpmmWaves][NCH * GL * VEC];
     spmm_block<VEC, GL, NCH, TWO>(blocks[blockIdx.x], rowptr, col, val, src0, src1, n_src0, d,
                                   out, red);
+}
+
+// Epilogue destination of row r: out2 for r < rows, out3 (if any) after.
+__device__ __forceinline__ float *ep_row(const SpmmEpilogue &ep, int32_t r)
+{
+    if (r < ep.rows)
+        return ep.out2 + (int64_t)r * ep.n2;
+    return ep.out3 ? ep.out3 + (int64_t)(r - ep.rows) * ep.n2 : nullptr;
 }
 
 // Aggregation for rows at most GL * VEC <= 16 wide, where one row per wave
@@ -377,7 +400,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     const SpmmBlock *__restrict__ blocks, int32_t n_long, int32_t n_blocks,
     const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
     const float *__restrict__ val, const float *__restrict__ src0, const float *__restrict__ src1,
-    int32_t n_src0, int32_t d, float *__restrict__ out, SpmmEpilogue ep)
+    int32_t n_src0, int32_t d, SpmmOut out, SpmmEpilogue ep)
 {
     __shared__ float red[kSpmmWaves][GL * VEC];
     extern __shared__ float ws[];   // EP: w as [k][n2]
@@ -393,13 +416,14 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
         spmm_block<VEC, GL, 1, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, out, red);
         if constexpr (EP) {
             // the row was written by this block before spmm_block's last barrier
-            if (b.row < ep.rows) {
+            if (float *o2 = ep_row(ep, b.row)) {
+                const float *orow = out.row(b.row, d);
                 float gk[kNarrow];
 #pragma unroll
                 for (int k = 0; k < kNarrow; ++k)
-                    gk[k] = k < d ? out[(int64_t)b.row * d + k] : 0.f;
+                    gk[k] = k < d ? orow[k] : 0.f;
                 for (int n4 = threadIdx.x; n4 < ep.n2 / 4; n4 += kSpmmThreads)
-                    narrow_ep_store(gk, d, ws, ep.n2, n4, ep.out2 + (int64_t)b.row * ep.n2);
+                    narrow_ep_store(gk, d, ws, ep.n2, n4, o2);
             }
         }
         return;
@@ -460,9 +484,9 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
                         acc[v] = fmaf(aa[j][u], x[j][u][v], acc[v]);
         }
         if (lane_ok)
-            store_vec<VEC>(out + (int64_t)row * d + gl * VEC, acc);
+            store_vec<VEC>(out.row(row, d) + gl * VEC, acc);
         if constexpr (EP) {
-            if (row < ep.rows) {
+            if (float *o2 = ep_row(ep, row)) {
                 float gk[kNarrow];
 #pragma unroll
                 for (int k = 0; k < kNarrow; ++k) {
@@ -470,7 +494,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
                     gk[k] = k < d ? v : 0.f;
                 }
                 for (int n4 = gl; n4 < ep.n2 / 4; n4 += GL)
-                    narrow_ep_store(gk, d, ws, ep.n2, n4, ep.out2 + (int64_t)row * ep.n2);
+                    narrow_ep_store(gk, d, ws, ep.n2, n4, o2);
             }
         }
     }
@@ -1208,7 +1232,7 @@ template <int VEC, int GL, bool TWO>
 hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_blocks,
                          const int32_t *rowptr, const int32_t *col, const float *val,
                          const float *src0, const float *src1, int32_t n_src0, int32_t d,
-                         float *out, const SpmmEpilogue *ep, hipStream_t s)
+                         SpmmOut out, const SpmmEpilogue *ep, hipStream_t s)
 {
     const int64_t grid = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
     if (ep) {
@@ -1227,7 +1251,7 @@ hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_bloc
 template <int VEC, int GL, int NCH, bool TWO>
 hipError_t spmm_t(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
                   const int32_t *col, const float *val, const float *src0, const float *src1,
-                  int32_t n_src0, int32_t d, float *out, hipStream_t s)
+                  int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
 {
     hipLaunchKernelGGL((k_spmm<VEC, GL, NCH, TWO>), dim3((unsigned)n_blocks), dim3(kSpmmThreads),
                        0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, out);
@@ -1239,7 +1263,7 @@ hipError_t spmm_t(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowp
 template <int VEC, bool TWO>
 hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
                   const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
-                  const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
+                  const float *src1, int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
 {
     switch (gl) {
     case 4: return spmm_t<VEC, 4, 1, TWO>(DIGEST_SPMM_ARGS);
@@ -1271,7 +1295,7 @@ hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
 template <bool TWO>
 hipError_t spmm_v(int vec, int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
                   const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
-                  const float *src1, int32_t n_src0, int32_t d, float *out, hipStream_t s)
+                  const float *src1, int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
 {
     switch (vec) {
     case 4: return spmm_g<4, TWO>(gl, nch, DIGEST_SPMM_ARGS);
@@ -1373,15 +1397,22 @@ bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2)
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
-                       float *out, hipStream_t s, const SpmmEpilogue *ep)
+                       float *out0, hipStream_t s, const SpmmEpilogue *ep, float *out1,
+                       int32_t n_out0)
 {
-    if (ep && !spmm_epilogue_ok(d, ep->n2, ep->out2))
+    if (ep && (!spmm_epilogue_ok(d, ep->n2, ep->out2) ||
+               (ep->out3 && !spmm_epilogue_ok(d, ep->n2, ep->out3))))
+        return hipErrorInvalidValue;
+    if (n_out0 < 0 || (n_out0 != INT32_MAX && !out1))
         return hipErrorInvalidValue;
     if (n_blocks <= 0 || d <= 0)
         return hipSuccess;
-    int vec = pick_vec(d, src0, out);
+    const SpmmOut out{out0, out1, n_out0};
+    int vec = pick_vec(d, src0, out0);
     if (src1 && pick_vec(d, src1, nullptr) < vec)
         vec = pick_vec(d, src1, nullptr);
+    if (out1 && pick_vec(d, out1, nullptr) < vec)
+        vec = pick_vec(d, out1, nullptr);
     const int dv = d / vec;
     const int gl = pick_group(dv);
     if (ep && gl > 16)

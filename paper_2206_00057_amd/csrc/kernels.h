@@ -35,14 +35,17 @@ hipError_t launch_add_clear_rows(const int32_t *sidx, const int32_t *didx, int32
 
 // Two-source CSR aggregation out[r] = sum_k val[k] * src(col[k]) over the
 // rows named by the blocks.  Column c < n_src0 reads row c of src0,
-// otherwise row (c - n_src0) of src1.  Every named row is fully written.
+// otherwise row (c - n_src0) of src1.  Every named row is fully written:
+// row r < n_out0 to out0[r], row r >= n_out0 to out1[r - n_out0].
 // Optional epilogue of a narrow aggregation (d <= kNarrow): rows r < rows
 // also get out2[r][n] = sum_k out[r][k] w[n][k] for n < n2, w row-major
-// [n2][d] (out times w^T).  Needs spmm_epilogue_ok(d, n2, out2).
+// [n2][d] (out times w^T), and with out3 the rows r >= rows get the same
+// product in out3[r - rows].  Needs spmm_epilogue_ok(d, n2, out2 and out3).
 struct SpmmEpilogue {
     const float *w;
     int32_t rows, n2;
     float *out2;
+    float *out3 = nullptr;
 };
 bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2);
 
@@ -51,7 +54,8 @@ bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2);
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
-                       float *out, hipStream_t s, const SpmmEpilogue *ep = nullptr);
+                       float *out0, hipStream_t s, const SpmmEpilogue *ep = nullptr,
+                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
 // slices (each its own grid part) when splits > 1.

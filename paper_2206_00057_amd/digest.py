@@ -55,6 +55,7 @@ def lib():
             "digest_softmax_xent": ([P, P, P, P, P, P], st),
             "digest_sgd_average": ([P, P, i32, i64, ctypes.c_float, P], st),
             "digest_halo_gradient": ([P, i32, P, P, P, P, P], st),
+            "digest_layer_backward_halo": ([P, i32, P, P, P, P, P, P, P, P], st),
             "digest_push_add": ([P, i32, P, P, P], st),
             "digest_pull_add": ([P, i32, P, P, P], st),
             "digest_sync_period": ([i32, i64, P, P], st),
@@ -249,6 +250,21 @@ def digest_layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in=None, stre
     e = _dev(dw, torch.float32, di * do, "dw")
     f = _dev(dh_in, torch.float32, p.n_own * di, "dh_in") if dh_in is not None else None
     _check(lib().digest_layer_backward(p.handle, int(layer), x, a, b, c, e, f, _stream(stream)))
+
+
+def digest_layer_backward_halo(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_halo,
+                               stream=None):
+    """digest_layer_backward plus dh_halo = P_out^T D W^T (layer 2..L)."""
+    import torch
+    _check_layer(p, layer)
+    di, do = p.widths[layer - 1], p.widths[layer]
+    _check(lib().digest_layer_backward_halo(
+        p.handle, int(layer), _dev(h_in, torch.float32, p.n_own * di, "h_in"),
+        _dev(h_out, torch.float32, p.n_own * do, "h_out"),
+        _dev(dh_out, torch.float32, p.n_own * do, "dh_out"),
+        _dev(w, torch.float32, di * do, "w"), _dev(dw, torch.float32, di * do, "dw"),
+        _dev(dh_in, torch.float32, p.n_own * di, "dh_in"),
+        _dev(dh_halo, torch.float32, p.n_halo * di, "dh_halo"), _stream(stream)))
 
 
 def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):

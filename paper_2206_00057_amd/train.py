@@ -114,24 +114,29 @@ class DigestTrainer:
         for m, gp in enumerate(self.gps):
             D.digest_softmax_xent(gp.p, gp.H[self.L], self.y_own[m], gp.dH[self.L],
                                   self.losses[m:m + 1])
+        exch = self.grad_exchange != "none"
         for l in range(self.L, 0, -1):
             for m, gp in enumerate(self.gps):
                 dh_in = gp.dH[l - 1] if l > 1 else None
                 h_in = gp.H[l - 1] if l > 1 else self.x_own[m]
-                D.digest_layer_backward(gp.p, l, h_in, gp.H[l], gp.dH[l], self.W[l - 1],
-                                        gp.dW[l], dh_in)
-            if l > 1 and self.grad_exchange != "none":
+                if exch and l > 1:
+                    # the halo gradient comes out of the backward's own products
+                    D.digest_layer_backward_halo(gp.p, l, h_in, gp.H[l], gp.dH[l],
+                                                 self.W[l - 1], gp.dW[l], dh_in,
+                                                 self.dh_halo[m][l - 1])
+                else:
+                    D.digest_layer_backward(gp.p, l, h_in, gp.H[l], gp.dH[l], self.W[l - 1],
+                                            gp.dW[l], dh_in)
+            if exch and l > 1:
                 self._exchange(l)
         for l in range(1, self.L + 1):
             D.digest_sgd_average(self.W[l - 1], [gp.dW[l] for gp in self.gps], self.lr)
 
     def _exchange(self, l):
-        """Halo gradients of layer l into the level l-1 store and back to the
-        owners' input gradients (fresh: this round's; stale: last round's)."""
+        """The halo gradients of layer l (from the backward) into the level
+        l-1 store and back to the owners' input gradients (fresh: this
+        round's; stale: last round's)."""
         gs = self.gstores[l - 1]
-        for m, gp in enumerate(self.gps):
-            D.digest_halo_gradient(gp.p, l, gp.H[l], gp.dH[l], self.W[l - 1],
-                                   self.dh_halo[m][l - 1])
         if self.grad_exchange == "fresh":
             for m, gp in enumerate(self.gps):
                 D.digest_push_add(gp.p, l - 1, self.dh_halo[m][l - 1], gs)

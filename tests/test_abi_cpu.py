@@ -123,6 +123,8 @@ def test_device_calls_without_workspace_fail_with_estate():
     assert L.digest_halo_gradient(h.handle, 2, fake, fake, fake, fake, None) == D.ESTATE
     assert L.digest_push_add(h.handle, 1, fake, fake, None) == D.ESTATE
     assert L.digest_pull_add(h.handle, 1, fake, fake, None) == D.ESTATE
+    assert L.digest_layer_backward_halo(h.handle, 2, fake, fake, fake, fake, fake, fake, fake,
+                                        None) == D.ESTATE
     assert L.digest_halo_gradient(None, 2, fake, fake, fake, fake, None) == D.EINVAL
     assert L.digest_push_add(None, 1, fake, fake, None) == D.EINVAL
     assert L.digest_pull(None, 0, fake, None) == D.EINVAL

@@ -219,5 +219,56 @@ def test_gradient_exchange_calls_check_level_and_order():
         assert L.digest_pull_add(h.handle, level, a, a, None) == D.EINVAL
     assert L.digest_push_add(h.handle, 1, a, None, None) == D.EINVAL
     assert L.digest_pull_add(h.handle, 1, None, a, None) == D.EINVAL
+    # the fused backward: no halo gradient of layer 1, and both outputs needed
+    assert L.digest_layer_backward_halo(h.handle, 1, a, a, a, a, a, a, a, None) == D.EINVAL
+    assert L.digest_layer_backward_halo(h.handle, 2, a, a, a, a, a, a, a, None) == D.ESTATE
     torch.cuda.synchronize()
 
+
+
+# (widths, identity layer takes the transform-first order): transform-first
+# with the halo rows from the fused narrow epilogue (6 of 40) or from the
+# narrow VALU product (6 of 42, no 16-byte rows), transform-first with MFMA
+# products (48 of 200), aggregate-first (36 of 40) and GEMM-first (48 of 40).
+BACKWARD_HALO_CASES = [((24, 40, 6), True), ((24, 42, 6), True), ((24, 200, 48), True),
+                       ((24, 40, 36), False), ((24, 40, 48), False)]
+
+
+@pytest.mark.parametrize("widths,tf", BACKWARD_HALO_CASES,
+                         ids=[f"{w[1]}-{w[2]}" for w, _ in BACKWARD_HALO_CASES])
+def test_layer_backward_halo_matches_oracle(widths, tf):
+    """The fused backward gives the separate calls' dw and dh_in and the halo
+    gradient, for ReLU (GEMM-first with the mask) and identity."""
+    import bench
+    from paper_2206_00057_amd import digest as D
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=4)
+    p = synth.make_partition(cfg, g, 2)
+    assert bench.transform_first(2, widths, synth.shape_stats(cfg, g, p)) == tf
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                  cfg.widths)
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    D.digest_partition_bind_workspace(h, ws)
+    op = oracle.OraclePartition(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    store = synth.relu_normal((g.n, widths[1]), seed=5)
+    D.digest_pull(h, 1, dev(store))
+    op.pull(1, store)
+    h_in = synth.relu_normal((p.n_own, widths[1]), seed=6)
+    W = synth.weights(cfg)[1]
+    d_in, d_out = widths[1], widths[2]
+    for act in (oracle.RELU, oracle.IDENTITY):
+        out = torch.empty(p.n_own, d_out, device="cuda")
+        D.digest_layer_forward(h, 2, dev(h_in), dev(W), out, act)
+        h_out = op.forward(2, h_in, W, act)
+        dh = synth.normal((p.n_own, d_out), seed=7, scale=1.0 / p.n_own)
+        dw = torch.empty(d_in, d_out, device="cuda")
+        dh_in = torch.empty(p.n_own, d_in, device="cuda")
+        dh_halo = torch.full((p.n_halo, d_in), float("nan"), device="cuda")
+        D.digest_layer_backward_halo(h, 2, dev(h_in), dev(h_out), dev(dh), dev(W), dw, dh_in,
+                                     dh_halo)
+        ref_dw, ref_dh = op.backward(2, h_in, W, h_out, dh, act)
+        ref_halo = op.halo_gradient(2, W, h_out, dh, act)
+        name = f"{widths} act {act}"
+        assert_close(host(dw), ref_dw, f"dw {name}")
+        assert_close(host(dh_in), ref_dh, f"dh_in {name}", scale_tol=2e-5)
+        assert_close(host(dh_halo), ref_halo, f"dh_halo {name}", scale_tol=2e-5)
