@@ -197,15 +197,23 @@ bool transform_first_cheaper(const digest_partition &p, int32_t layer)
     return tf < af;
 }
 
-// The kernels for a narrow side (<= kNarrow columns); the dgrad one stages
-// W (d_in x 16 floats) in LDS, which bounds d_in.
+// The kernels for a narrow side (<= kNarrow columns): the dgrad one keeps a
+// 256-column slice of W per wave, the weight-gradient one 64 features per
+// wave; d_in is bounded to keep their launch shapes sane.
 bool narrow_valu(int64_t d_in, int64_t d_out)
 {
     return d_out <= digest::kNarrow && d_in <= 1024;
 }
 
+// The forward's product for outputs up to kNarrowN wide, with W in LDS.
+bool narrow_out(int64_t d_in, int64_t d_out)
+{
+    return d_out <= digest::kNarrowN &&
+           digest::narrow_n_lds((int32_t)d_in, (int32_t)d_out) <= digest::kNarrowNLds;
+}
+
 // Split-K slices of the transform-first weight gradient H_mix^T G over the
-// n_own + n_halo rows.  Narrow outputs (<= kNarrow) use the VALU kernel with
+// n_own + n_halo rows.  Narrow outputs (<= kNarrow) use the MFMA kernel with
 // `chunk` rows per slice; wider ones use the MFMA GEMM twice (owned rows,
 // then halo rows) with their own split plans.
 struct TfPlan {
@@ -714,7 +722,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         float *T = p->at<float>(p->lay.tbuf);
         {
             Timed t(p, K_GEMM_FWD, layer, s);
-            if (narrow_valu(d_in, d_out)) {
+            if (narrow_out(d_in, d_out)) {
                 if (digest_status st = hip_check(
                         digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
                                                 halo, d_in, w, T, d_out, false, s),
@@ -755,7 +763,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         if (digest_status st = run_spmm(p, Csr::Fwd, h_in, halo, p->n_own, d_in, ah, layer, s))
             return st;
         Timed t(p, K_GEMM_FWD, layer, s);
-        if (narrow_valu(d_in, d_out)) {
+        if (narrow_out(d_in, d_out)) {
             if (digest_status st = hip_check(
                     digest::launch_narrow_n(p->n_own, p->n_own, d_in, d_out, ah, nullptr, d_in, w,
                                             h_out, d_out, act == DIGEST_ACT_RELU, s),
@@ -790,13 +798,17 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
 namespace {
 
 // C[rows][d_in] = A[rows][d_out] W^T (W row-major [d_in][d_out]): the VALU
-// kernel for outputs of narrow contractions, else the MFMA GEMM.
+// kernel for contractions up to kNarrow long, the MFMA kernel with W in LDS
+// up to kTimesWtK, else the MFMA GEMM.
 digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A, const float *w,
                        float *C, hipStream_t s)
 {
     if (narrow_valu(d_in, d_out))
         return hip_check(digest::launch_narrow_k(rows, d_in, d_out, A, d_out, w, C, d_in, s),
                          "times W^T (narrow)");
+    if (d_out <= digest::kTimesWtK && digest::times_wt_lds(d_out, d_in) <= digest::kNarrowNLds)
+        return hip_check(digest::launch_times_wt(rows, d_in, d_out, A, d_out, w, C, d_in, s),
+                         "times W^T (short)");
     digest::GemmArgs h{};
     h.M = rows;
     h.N = d_in;
@@ -1101,16 +1113,7 @@ digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const flo
                                         layer, s, nullptr, K_HALO_GRAD))
             return st;
         Timed t(p, K_HALO_GRAD, layer, s);
-        if (narrow_valu(d_in, d_out))
-            return hip_check(digest::launch_narrow_k(p->n_halo, d_in, d_out, gh, d_out, w,
-                                                     dh_halo, d_in, s),
-                             "halo gradient");
-        h.M = p->n_halo;
-        h.A = gh;
-        h.lda = d_out;
-        h.C = dh_halo;
-        h.tile = gemm_tile_for(p->n_halo, d_in, d_out, false);
-        return hip_check(digest::launch_gemm(h, s), "halo gradient");
+        return times_wt(p->n_halo, d_in, d_out, gh, w, dh_halo, s);
     }
     // otherwise P_out^T (D W^T), with the ReLU mask fused into the GEMM
     float *tmp = p->at<float>(p->lay.tmp);

@@ -794,14 +794,18 @@ __global__ __launch_bounds__(256) void k_splitk_reduce_wide(const float *__restr
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// C[r][n] = sum_k A(r)[k] B[k][n] for n < N <= 16, on v_mfma_f32_16x16x4f32.
+// C[r][n] = sum_k A(r)[k] B[k][n] for n < N <= 16 NB, on v_mfma_f32_16x16x4f32.
 // Row r of A is row r of A0 (r < m0) or row r - m0 of A1 (leading dim lda).
-// B is staged once per block in LDS (zero-padded to 16 columns); a wave owns
-// 16 rows.  The contraction order is permuted so that a lane feeds its own
-// 16-byte load: in MFMA step (j, v) lane group h = lane/16 contributes
-// k = 16 j + 4 h + v for row lane%16 (A) and column lane%16 (B), and every k
-// is covered once.  All A loads of a K chunk are issued before its MFMAs.
-template <bool VEC>
+// B is staged once per block in LDS, zero-padded to 16 NB columns, its rows
+// 16 NB + 4 floats apart so that the four k rows one MFMA step reads fall in
+// different banks.  The grid is sized to the chip and each wave takes 16-row
+// tiles in turn, so the staging is paid once per block, not per tile.  The
+// contraction order is permuted so that a lane feeds its own 16-byte load:
+// in MFMA step (j, v) lane group h = lane/16 contributes k = 16 j + 4 h + v
+// for row lane%16 (A) and column lane%16 of each column block (B), and every
+// k is covered once.  All A loads of a K chunk are issued before its MFMAs,
+// and the NB column blocks share them.
+template <bool VEC, int NB>
 __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N,
                                                   const float *__restrict__ A0,
                                                   const float *__restrict__ A1, int32_t lda,
@@ -810,59 +814,137 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
 {
     constexpr int KC = 256;          // k per chunk
     constexpr int J = KC / 16;       // 16-k steps per chunk
-    extern __shared__ float Bs[];    // [K][16]
+    constexpr int BS = 16 * NB + 4;  // LDS row stride of B
+    extern __shared__ float Bs[];    // [K][BS]
+    stage_lds(Bs, K * BS, [&](int i) {
+        const int k = i / BS, n = i % BS;
+        return n < N ? B[(int64_t)k * N + n] : 0.f;
+    });
+    __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
-    const int row0 = (blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * 16;
     const int m = lane & 15, h = lane >> 4;
-    const int r = row0 + m;
-    const bool row_ok = r < M;   // a wave past M loads the first element and stores nothing
-    const float *a = !row_ok ? A0 : (r < m0 ? A0 + (int64_t)r * lda : A1 + (int64_t)(r - m0) * lda);
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    float av[J][4];
-    auto load_chunk = [&](int kc) {
+    const int64_t tiles = ((int64_t)M + 15) / 16;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x / kWave);
+    for (int64_t t = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; t < tiles;
+         t += waves) {
+        const int64_t row0 = t * 16;
+        const int64_t r = row0 + m;
+        const bool row_ok = r < M;   // a lane past M loads the first element, stores nothing
+        const float *a =
+            !row_ok ? A0 : (r < m0 ? A0 + r * lda : A1 + (r - m0) * (int64_t)lda);
+        floatx4 acc[NB];
 #pragma unroll
-        for (int j = 0; j < J; ++j) {
-            const int k = kc + 16 * j + 4 * h;
-            if (VEC) {
-                const bool ok = row_ok && k < K;   // K % 4 == 0: quads are all in or all out
-                const float4 q = *reinterpret_cast<const float4 *>(ok ? a + k : A0);
-                av[j][0] = ok ? q.x : 0.f;
-                av[j][1] = ok ? q.y : 0.f;
-                av[j][2] = ok ? q.z : 0.f;
-                av[j][3] = ok ? q.w : 0.f;
-            } else {
+        for (int b = 0; b < NB; ++b)
+            acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+        float av[J][4];
+        for (int kc = 0; kc < K; kc += KC) {
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int k = kc + 16 * j + 4 * h;
+                if (VEC) {
+                    const bool ok = row_ok && k < K;   // K % 4 == 0: quads all in or all out
+                    const float4 q = *reinterpret_cast<const float4 *>(ok ? a + k : A0);
+                    av[j][0] = ok ? q.x : 0.f;
+                    av[j][1] = ok ? q.y : 0.f;
+                    av[j][2] = ok ? q.z : 0.f;
+                    av[j][3] = ok ? q.w : 0.f;
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const bool ok = row_ok && k + v < K;
+                        const float q = *(ok ? a + k + v : A0);
+                        av[j][v] = ok ? q : 0.f;
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < J; ++j)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const bool ok = row_ok && k + v < K;
-                    const float q = *(ok ? a + k + v : A0);
-                    av[j][v] = ok ? q : 0.f;
+                    const int k = kc + 16 * j + 4 * h + v;
+                    const float *brow = Bs + (k < K ? k : 0) * BS + m;
+#pragma unroll
+                    for (int b = 0; b < NB; ++b) {
+                        const float bv = k < K ? brow[16 * b] : 0.f;
+                        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j][v], bv, acc[b], 0, 0,
+                                                                      0);
+                    }
+                }
+        }
+        // lane holds C[row0 + 4h + i][16 b + m] for i < 4
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int n = 16 * b + m;
+            if (n < N) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t rr = row0 + 4 * h + i;
+                    if (rr < M)
+                        C[rr * ldc + n] = relu ? fmaxf(acc[b][i], 0.f) : acc[b][i];
                 }
             }
         }
-    };
-    stage_lds(Bs, K * 16, [&](int i) {
-        const int k = i >> 4, n = i & 15;
-        return n < N ? B[k * N + n] : 0.f;
+    }
+}
+
+// C[r][n] = sum_{k < K} A[r][k] W[n][k] (A W^T, W row-major [N][K]) for
+// 16 < K <= 4 KS <= 64, on v_mfma_f32_16x16x4f32: a product whose cost is
+// writing C.  W is staged once per block in LDS as [k][n] (k zero-padded to
+// 4 KS, rows bs floats apart with bs = 16 mod 64, so that the four k rows
+// of an MFMA step fall in different banks).  The grid is sized to the chip
+// and each wave takes 16-row tiles in turn: lane (m, h) = (lane % 16,
+// lane / 16) loads A[row m][4 j + h] for MFMA step j once per tile, and the
+// column blocks of C reuse them two at a time.
+template <int KS>
+__global__ __launch_bounds__(256) void k_times_wt(int32_t M, int32_t N, int32_t K,
+                                                  const float *__restrict__ A, int32_t lda,
+                                                  const float *__restrict__ W,
+                                                  float *__restrict__ C, int32_t ldc, int32_t bs)
+{
+    extern __shared__ float Ws[];   // [4 KS][bs]
+    stage_lds(Ws, 4 * KS * bs, [&](int i) {
+        const int k = i / bs, n = i % bs;
+        return (k < K && n < N) ? W[(int64_t)n * K + k] : 0.f;
     });
     __syncthreads();
-    for (int kc = 0; kc < K; kc += KC) {
-        load_chunk(kc);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int m = lane & 15, h = lane >> 4;
+    const int nb = (N + 15) / 16;
+    const int64_t tiles = ((int64_t)M + 15) / 16;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x / kWave);
+    for (int64_t t = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; t < tiles;
+         t += waves) {
+        const int64_t row0 = t * 16;
+        const int64_t r = row0 + m;
+        const float *ar = A + (r < M ? r : 0) * (int64_t)lda;
+        float a[KS];
 #pragma unroll
-        for (int j = 0; j < J; ++j)
+        for (int j = 0; j < KS; ++j) {
+            const int k = 4 * j + h;
+            a[j] = (r < M && k < K) ? ar[k] : 0.f;
+        }
+        for (int b = 0; b < nb; b += 2) {
+            // the second block of an odd last pair reads a valid column, stores nothing
+            const int c0 = 16 * b + m, c1 = min(16 * (b + 1) + m, bs - 1);
+            floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int k = kc + 16 * j + 4 * h + v;
-                const float b = k < K ? Bs[k * 16 + m] : 0.f;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j][v], b, acc, 0, 0, 0);
+            for (int j = 0; j < KS; ++j) {
+                const float *wr = Ws + (4 * j + h) * bs;
+                acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], wr[c0], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], wr[c1], acc1, 0, 0, 0);
             }
-    }
-    // lane holds C[row0 + 4h + i][m] for i < 4
-    if (m < N) {
+            // lane holds C[row0 + 4h + i][16 b + m] (acc0) and [16 (b+1) + m] (acc1)
+            const int n0 = 16 * b + m, n1 = n0 + 16;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int rr = row0 + 4 * h + i;
-            if (rr < M)
-                C[(int64_t)rr * ldc + m] = relu ? fmaxf(acc[i], 0.f) : acc[i];
+            for (int i = 0; i < 4; ++i) {
+                const int64_t rr = row0 + 4 * h + i;
+                if (rr < M) {
+                    if (n0 < N)
+                        C[rr * ldc + n0] = acc0[i];
+                    if (n1 < N)
+                        C[rr * ldc + n1] = acc1[i];
+                }
+            }
         }
     }
 }
@@ -1549,25 +1631,101 @@ hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float
 }
 
 
+namespace {
+
+// Blocks of a persistent launch: enough for every tile, at most what the
+// chip holds at once given the block's LDS (256 CUs, 160 KB each, at most 8
+// blocks per CU).
+int64_t persistent_blocks(int64_t tiles_per_block_work, size_t lds)
+{
+    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, (160 * 1024) / std::max<size_t>(lds, 1)));
+    return std::max<int64_t>(1, std::min<int64_t>(tiles_per_block_work, 256 * per_cu));
+}
+
+}  // namespace
+
+size_t narrow_n_lds(int32_t K, int32_t N)
+{
+    const int nb = (N + 15) / 16;
+    return sizeof(float) * (size_t)K * (16 * nb + 4);
+}
+
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
                            const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
                            bool relu, hipStream_t s)
 {
     if (M <= 0 || N <= 0)
         return hipSuccess;
-    if (N > kNarrow || K <= 0 || (size_t)K * 16 * sizeof(float) > 64 * 1024)
+    if (N > kNarrowN || K <= 0 || narrow_n_lds(K, N) > kNarrowNLds)
         return hipErrorInvalidValue;
     const bool v4 = K % 4 == 0 && lda % 4 == 0 && ((uintptr_t)A0 % 16) == 0 &&
                     (A1 == nullptr || ((uintptr_t)A1 % 16) == 0);
-    const int64_t waves = ((int64_t)M + 15) / 16;
-    const int64_t blocks = (waves + 3) / 4;
-    const size_t lds = sizeof(float) * (size_t)K * 16;
-    if (v4)
-        hipLaunchKernelGGL((k_narrow_n<true>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0,
-                           K, N, A0, A1, lda, B, C, ldc, relu);
+    const size_t lds = narrow_n_lds(K, N);
+    const int64_t blocks = persistent_blocks((((int64_t)M + 15) / 16 + 3) / 4, lds);
+    const int nb = (N + 15) / 16;
+#define DIGEST_NN(V, NB)                                                                       \
+    hipLaunchKernelGGL((k_narrow_n<V, NB>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0, K, \
+                       N, A0, A1, lda, B, C, ldc, relu)
+    if (v4) {
+        switch (nb) {
+        case 1: DIGEST_NN(true, 1); break;
+        case 2: DIGEST_NN(true, 2); break;
+        case 3: DIGEST_NN(true, 3); break;
+        default: DIGEST_NN(true, 4); break;
+        }
+    } else {
+        switch (nb) {
+        case 1: DIGEST_NN(false, 1); break;
+        case 2: DIGEST_NN(false, 2); break;
+        case 3: DIGEST_NN(false, 3); break;
+        default: DIGEST_NN(false, 4); break;
+        }
+    }
+#undef DIGEST_NN
+    return hipGetLastError();
+}
+
+namespace {
+
+// LDS row stride of W^T in k_times_wt (at least N, = 16 mod 64) and its MFMA
+// k-steps.
+int32_t times_wt_stride(int32_t N)
+{
+    int32_t bs = (N + 15) / 16 * 16;
+    while (bs % 64 != 16)
+        bs += 16;
+    return bs;
+}
+
+int times_wt_steps(int32_t K) { return K <= 32 ? 8 : (K <= 48 ? 12 : 16); }
+
+}  // namespace
+
+size_t times_wt_lds(int32_t K, int32_t N)
+{
+    return sizeof(float) * (size_t)(4 * times_wt_steps(K)) * times_wt_stride(N);
+}
+
+hipError_t launch_times_wt(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
+                           const float *W, float *C, int32_t ldc, hipStream_t s)
+{
+    if (M <= 0 || N <= 0)
+        return hipSuccess;
+    if (K <= kNarrow || K > kTimesWtK || times_wt_lds(K, N) > kNarrowNLds)
+        return hipErrorInvalidValue;
+    const int32_t bs = times_wt_stride(N);
+    const int ks = times_wt_steps(K);
+    const size_t lds = times_wt_lds(K, N);
+    const int64_t blocks = persistent_blocks((((int64_t)M + 15) / 16 + 3) / 4, lds);
+    if (ks == 8)
+        hipLaunchKernelGGL((k_times_wt<8>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K, A,
+                           lda, W, C, ldc, bs);
+    else if (ks == 12)
+        hipLaunchKernelGGL((k_times_wt<12>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K,
+                           A, lda, W, C, ldc, bs);
     else
-        hipLaunchKernelGGL((k_narrow_n<false>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0,
-                           K, N, A0, A1, lda, B, C, ldc, relu);
+        hipLaunchKernelGGL((k_times_wt<16>), dim3((unsigned)blocks), dim3(256), lds, s, M, N, K,
+                           A, lda, W, C, ldc, bs);
     return hipGetLastError();
 }
 

@@ -89,17 +89,28 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count, float *out,
                                 hipStream_t s);
 
-// Narrow dense products (VALU) for one side at most kNarrow wide.
+// Dense products with one narrow side, bound by streaming the wide operand.
 
-// C[r][n] = sum_k A(r)[k] B[k][n], n < N <= kNarrow, B row-major [K][N];
+// C[r][n] = sum_k A(r)[k] B[k][n], n < N <= kNarrowN, B row-major [K][N];
 // A(r) is row r of A0 for r < m0, else row r - m0 of A1 (leading dim lda);
-// relu: epilogue max(x, 0).
+// relu: epilogue max(x, 0).  B is held in LDS: needs
+// narrow_n_lds(K, N) <= kNarrowNLds.
+constexpr int kNarrowN = 64;
+constexpr size_t kNarrowNLds = 64 * 1024;
+size_t narrow_n_lds(int32_t K, int32_t N);
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
                            const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
                            bool relu, hipStream_t s);
 
 // C[r][n] = sum_{k < K} A[r][k] W[n][k] with K <= kNarrow, W row-major [N][K].
 hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
+                           const float *W, float *C, int32_t ldc, hipStream_t s);
+
+// The same product for kNarrow < K <= kTimesWtK on MFMA with W held in LDS:
+// needs times_wt_lds(K, N) <= kNarrowNLds.
+constexpr int kTimesWtK = 64;
+size_t times_wt_lds(int32_t K, int32_t N);
+hipError_t launch_times_wt(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
                            const float *W, float *C, int32_t ldc, hipStream_t s);
 
 // part[z][f][n] = sum over rows r in [z*chunk, (z+1)*chunk) of H(r)[f] G[r][n]

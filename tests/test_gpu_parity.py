@@ -236,7 +236,8 @@ def test_determinism_bitwise(tiny):
 # ---------------------------------------------------------------------------
 
 WIDTHS = [(1, 1, 1), (3, 5, 2), (7, 41, 47), (602, 47, 7), (100, 256, 41), (64, 64, 16),
-          (33, 130, 9), (500, 256, 7), (16, 24, 70), (20, 40, 100), (8, 12, 130)]
+          (33, 130, 9), (500, 256, 7), (16, 24, 70), (20, 40, 100), (8, 12, 130),
+          (8, 40, 24), (8, 100, 60)]
 
 
 @pytest.mark.parametrize("widths", WIDTHS, ids=lambda w: "x".join(map(str, w)))
