@@ -84,8 +84,8 @@ def launch_model(st, widths):
     L = len(widths) - 1
     m = {}
 
-    def put(kind, l, b, f=0.0):
-        m[f"{kind}.l{l}"] = (float(b), float(f))
+    def put(kind, l, b, f=0.0, e=0):
+        m[f"{kind}.l{l}"] = (float(b), float(f), int(e))
 
     for l in range(1, L + 1):
         di, do = widths[l - 1], widths[l]
@@ -93,16 +93,16 @@ def launch_model(st, widths):
         if transform_first(l, widths, st):
             R = n + nh
             put("gemm_fwd_relu", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
-            put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do)
+            put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do, e=nnz)
             fused = l > 1 and do <= 16 and di <= 1024 and di % 4 == 0
             put("spmm_bwd_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do
-                + (4 * (n * di + di * do) if fused else 0))
+                + (4 * (n * di + di * do) if fused else 0), e=nnz)
             put("gemm_dw_splitk", l, 4 * (R * di + R * do), 2.0 * R * di * do)
             put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
             if l > 1 and not fused:
                 put("gemm_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
             continue
-        put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di)
+        put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di, e=nnz)
         put("gemm_fwd_relu", l, 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
         put("gemm_dw_splitk", l, 4 * (n * di + n * do * (2 if relu else 1) + di * do),
             2.0 * n * di * do)
@@ -112,7 +112,7 @@ def launch_model(st, widths):
         if l > 1:
             narrow = (not relu) and do < di
             w = do if narrow else di
-            put("spmm_bwd_transposed", l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w)
+            put("spmm_bwd_transposed", l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w, e=nnz_in)
             put("gemm_dgrad", l, 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
                 2.0 * n * di * do)
     put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
@@ -327,14 +327,16 @@ def main():
     for key, (tot_ms, n_l) in prof.items():
         entry = {"launches": n_l, "avg_us": 1e3 * tot_ms / n_l, "total_ms": tot_ms}
         if key in model:
-            b, f = model[key]
+            b, f, e = model[key]
             entry["gbs"] = b / (entry["avg_us"] * 1e-6) / 1e9
             if f:
                 entry["tflops"] = f / (entry["avg_us"] * 1e-6) / 1e12
+            if e:   # aggregation kernels: entries of the sparse operand per second
+                entry["gteps"] = e / (entry["avg_us"] * 1e-6) / 1e9
         kernels[key] = entry
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
     d = kernels[dom]
-    b_l, f_l = model.get(dom, (0.0, 0.0))
+    b_l, f_l, _ = model.get(dom, (0.0, 0.0, 0))
     if f_l and f_l / max(b_l, 1.0) > FP32_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": round(d["tflops"], 3), "peak": FP32_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4)}
@@ -347,10 +349,18 @@ def main():
 
     cpu = None
     if not args.no_cpu:
+        import oracle
         nr, secs, cores = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds)
         cpu = {"value": edges * nr / secs / 1e9, "unit": "GTEPS", "cores": cores, "kind": "oracle",
                "sample": f"{nr} whole rounds of the same partition (forward, loss, backward, "
                          f"scheduled pull/push) in {secs:.1f}s, float64 oracle, {cores} threads"}
+        # the same oracle on one thread, beside the all-core figure
+        oracle.set_num_threads(1)
+        nr1, secs1, _ = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds / 2)
+        oracle.set_num_threads(cores)
+        cpu["single_thread"] = {
+            "value": edges * nr1 / secs1 / 1e9, "unit": "GTEPS", "cores": 1,
+            "sample": f"{nr1} whole rounds in {secs1:.1f}s, float64 oracle, 1 thread"}
 
     out = {
         "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1,

@@ -63,6 +63,8 @@ def _load():
             i64, i32, f32, f64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_double
             P = ctypes.c_void_p
             lib.oracle_num_threads.restype = ctypes.c_int
+            lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+            lib.oracle_set_num_threads.restype = ctypes.c_int
             lib.oracle_partition_maps.argtypes = [i64, P, P, i64, P, i64, P, P, P, P]
             lib.oracle_partition_maps.restype = ctypes.c_int
             lib.oracle_owned_transpose.argtypes = [i64, P, P, P, P, P, P]
@@ -88,6 +90,11 @@ def _load():
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> int:
+    """Thread count of the oracle's OpenMP loops from now on; returns it."""
+    return int(_load().oracle_set_num_threads(int(n)))
 
 
 def _c(a, dtype):

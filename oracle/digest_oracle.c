@@ -57,6 +57,20 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Thread count of the OpenMP loops from here on (n >= 1); returns the new
+   count.  Host plumbing for timing the oracle single-threaded. */
+int oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Partition maps (Eq. 2; halo set and push set of Sec. 3.2)                */
 /* ------------------------------------------------------------------------ */

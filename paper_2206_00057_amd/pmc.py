@@ -13,6 +13,11 @@ HBM traffic of one kernel, from two counter passes over the same command:
         --kernel-name "k_gemm<64, 64, true, false, false, true" --key gemm_dw_splitk.l1 \\
         --copy-bytes 268435456 --workload medium --out profiles/medium_hbm_traffic.txt
 
+Per-kernel counter averages from one counter pass (e.g. MFMA utilisation):
+
+    python -m paper_2206_00057_amd.pmc counters --csv <dir>/<name>_counter_collection.csv \
+        --kernel-name "k_gemm<64, 64" --title "..." --command "..." --out profiles/<name>.txt
+
 FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel's dispatches are
 averaged, then each is divided by what the same counter reads, per byte, for
 a plain copy kernel of known size (the largest "copyBuffer" dispatch of the
@@ -78,6 +83,38 @@ def summarize(fetch_csv, write_csv, kernel_name, copy_name, copy_bytes):
     }
 
 
+def counters_table(path, patterns):
+    """Average of every counter over the dispatches of each kernel whose name
+    contains one of the patterns, as fixed-width text."""
+    per = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            name = r["Kernel_Name"]
+            if not any(p in name for p in patterns):
+                continue
+            name = re.sub(r"\(anonymous namespace\)::", "", name)
+            name = re.sub(r"\((.*)\)$", "", name).replace("void ", "")
+            d = per.setdefault(name, {})
+            d.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            d.setdefault("_ns", {})[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) -
+                                                        int(r["Start_Timestamp"]))
+    out = []
+    for name, d in per.items():
+        ns = d.pop("_ns")
+        avg = {k: sum(v) / len(v) for k, v in d.items()}
+        out.append(f"{name}: {len(ns)} dispatches, {sum(ns.values()) / len(ns) / 1e3:.2f} us "
+                   "per dispatch")
+        for k in sorted(avg):
+            out.append(f"  {k:32s} {avg[k]:16.1f}")
+        if "SQ_INSTS_MFMA" in avg and "SQ_VALU_MFMA_BUSY_CYCLES" in avg and avg["SQ_INSTS_MFMA"]:
+            out.append(f"  {'busy cycles per MFMA':32s} "
+                       f"{avg['SQ_VALU_MFMA_BUSY_CYCLES'] / avg['SQ_INSTS_MFMA']:16.1f}")
+        if "SQ_WAIT_INST_ANY" in avg and avg.get("SQ_WAVE_CYCLES"):
+            out.append(f"  {'dependency-wait share of wave time':32s} "
+                       f"{avg['SQ_WAIT_INST_ANY'] / avg['SQ_WAVE_CYCLES']:16.3f}")
+    return out
+
+
 def stats_table(path):
     """Per-kernel rows of a rocprofv3 kernel_stats.csv, as fixed-width text."""
     out = [f"# {'kernel':70s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} "
@@ -100,6 +137,13 @@ def main():
     st.add_argument("--title", required=True)
     st.add_argument("--command", action="append", default=[])
     st.add_argument("--out", required=True)
+    co = sub.add_parser("counters", help="per-kernel averages of a counter pass")
+    co.add_argument("--csv", required=True)
+    co.add_argument("--kernel-name", action="append", required=True,
+                    help="substring of the rocprof kernel names to include (repeatable)")
+    co.add_argument("--title", required=True)
+    co.add_argument("--command", action="append", default=[])
+    co.add_argument("--out", required=True)
     tr = sub.add_parser("traffic", help="HBM bytes per launch of one kernel")
     tr.add_argument("--fetch", required=True)
     tr.add_argument("--write", required=True)
@@ -115,6 +159,11 @@ def main():
         lines = [f"# {a.title}"] + [f"# command: {c}" for c in a.command]
         lines += [f"# source: rocprofv3 --kernel-trace --stats ({os.path.basename(a.csv)})", "#"]
         lines += stats_table(a.csv)
+    elif a.cmd == "counters":
+        lines = [f"# {a.title}"] + [f"# command: {c}" for c in a.command]
+        lines += [f"# source: rocprofv3 --pmc ({os.path.basename(a.csv)})",
+                  f"# source_sha = {kernel_source_hash()}", "#"]
+        lines += counters_table(a.csv, a.kernel_name)
     else:
         s = summarize(a.fetch, a.write, a.kernel_name, a.copy_name, a.copy_bytes)
         lines = [f"# HBM traffic of one launch of {a.key} on the {a.workload} workload,",
