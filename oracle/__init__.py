@@ -17,6 +17,9 @@ What each function follows in the paper:
   - ``layer_backward``: Eq. 6 completed by the chain rule of the GCN backward
     (Appendix A.3), halo rows held constant.
   - ``sync_period``: the pull/push conditions of Algorithm 1.
+  - ``gat_forward`` / ``gat_backward``: the stale-representation layer of
+    Eq. 4 with the attention aggregation of the GAT model the experiments
+    train (single head), and its chain-rule backward, halo rows constant.
 
 Every function is pinned by ``tests/test_oracle_pins.py`` against
 brute-force set algebra, dense matrices, scipy/torch fp64 routines, closed
@@ -83,6 +86,10 @@ def _load():
             lib.oracle_halo_gradient.argtypes = [i64, i64, P, P, P, i64, i64, P, P, P,
                                                  ctypes.c_int, P]
             lib.oracle_sgd_average.restype = ctypes.c_int
+            lib.oracle_gat_forward.argtypes = [i64, i64, P, P, P, P, i64, i64, P, P, f64,
+                                               ctypes.c_int, P, P]
+            lib.oracle_gat_backward.argtypes = [i64, i64, P, P, P, P, i64, i64, P, P, f64,
+                                                ctypes.c_int, P, P, P, P, P]
             del f32
             _lib = lib
     return _lib
@@ -251,6 +258,56 @@ def halo_gradient(indptr, col_local, values, n_halo, w, h_out, dh_out, act):
     return out
 
 
+GAT_SLOPE = 0.2   # LeakyReLU slope of the attention scores (the GAT model's value)
+
+
+def _gat_common(indptr, col_local, h_own, halo_buf, w, att):
+    indptr = _c(indptr, np.int64)
+    col_local = _c(col_local, np.int32)
+    h_own = _c(h_own, np.float32)
+    w = _c(w, np.float32)
+    att = _c(att, np.float32)
+    d_in, d_out = w.shape
+    halo_buf = _c(halo_buf if halo_buf is not None else np.zeros((0, d_in), np.float32),
+                  np.float32)
+    if att.shape != (d_out, 2):
+        raise OracleError("att must be [d_out, 2] (source, target columns)")
+    return indptr, col_local, h_own, halo_buf, w, att, d_in, d_out
+
+
+def gat_forward(indptr, col_local, h_own, halo_buf, w, att, act, slope=GAT_SLOPE,
+                want_alpha=False):
+    """GAT layer forward with stale halo rows: float32 h_out [n_own, d_out]
+    (and the attention weights in CSR entry order with want_alpha)."""
+    indptr, col_local, h_own, halo_buf, w, att, d_in, d_out = _gat_common(
+        indptr, col_local, h_own, halo_buf, w, att)
+    n_own = indptr.shape[0] - 1
+    out = np.empty((n_own, d_out), np.float32)
+    alpha = np.empty(int(indptr[-1]), np.float32) if want_alpha else None
+    _load().oracle_gat_forward(n_own, halo_buf.shape[0], _p(indptr), _p(col_local), _p(h_own),
+                               _p(halo_buf), d_in, d_out, _p(w), _p(att), float(slope),
+                               int(act), _p(out), _p(alpha) if want_alpha else None)
+    return (out, alpha) if want_alpha else out
+
+
+def gat_backward(indptr, col_local, h_own, halo_buf, w, att, h_out, dh_out, act,
+                 slope=GAT_SLOPE, want_dh_in=True):
+    """Returns (dw [d_in, d_out], datt [d_out, 2], dh_in [n_own, d_in] or None)."""
+    indptr, col_local, h_own, halo_buf, w, att, d_in, d_out = _gat_common(
+        indptr, col_local, h_own, halo_buf, w, att)
+    n_own = indptr.shape[0] - 1
+    h_out = _c(h_out, np.float32)
+    dh_out = _c(dh_out, np.float32)
+    dw = np.empty((d_in, d_out), np.float32)
+    datt = np.empty((d_out, 2), np.float32)
+    dh_in = np.empty((n_own, d_in), np.float32) if want_dh_in else None
+    _load().oracle_gat_backward(n_own, halo_buf.shape[0], _p(indptr), _p(col_local), _p(h_own),
+                                _p(halo_buf), d_in, d_out, _p(w), _p(att), float(slope),
+                                int(act), _p(h_out), _p(dh_out), _p(dw), _p(datt),
+                                _p(dh_in) if want_dh_in else None)
+    return dw, datt, dh_in
+
+
 def push_add(gstore, halo, dh_halo):
     """gstore[halo[j]] += dh_halo[j] (float32 adds; ``halo`` ids distinct)."""
     halo = _c(halo, np.int64)
@@ -337,6 +394,17 @@ class OraclePartition:
     def halo_gradient(self, layer, w, h_out, dh_out, act):
         return halo_gradient(self.indptr, self.col_local, self.values, self.n_halo, w, h_out,
                              dh_out, act)
+
+    def gat_forward(self, layer, h_in, w, att, act, slope=GAT_SLOPE, want_alpha=False):
+        return gat_forward(self.indptr, self.col_local, h_in, self.halo_buf.get(layer - 1), w,
+                           att, act, slope, want_alpha)
+
+    def gat_backward(self, layer, h_in, w, att, h_out, dh_out, act, slope=GAT_SLOPE,
+                     want_dh_in=None):
+        if want_dh_in is None:
+            want_dh_in = layer > 1
+        return gat_backward(self.indptr, self.col_local, h_in, self.halo_buf.get(layer - 1), w,
+                            att, h_out, dh_out, act, slope, want_dh_in)
 
 
 class OracleTrainer:

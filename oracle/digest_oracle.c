@@ -393,6 +393,228 @@ void oracle_layer_backward(int64_t n_own, const int64_t *indptr,
 }
 
 /* ------------------------------------------------------------------------ */
+/* GAT layer with stale halo rows: the stale-representation layer of Eq. 4  */
+/* with an attention aggregation (the GAT model of the experiments,         */
+/* single head; formulas from the GAT model the paper cites)                */
+/* ------------------------------------------------------------------------ */
+
+/* z_v = x_v W for every local row v (owned rows from h_own, halo rows from
+   the stale halo buffer), in double: [(n_own + n_halo) x d_out]. */
+static double *gat_transform(int64_t n_own, int64_t n_halo, const float *h_own,
+                             const float *halo_buf, int64_t d_in, int64_t d_out,
+                             const float *w)
+{
+    int64_t R = n_own + n_halo;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(R * d_out > 0 ? R * d_out : 1));
+#pragma omp parallel for schedule(static)
+    for (int64_t v = 0; v < R; ++v) {
+        const float *x = v < n_own ? h_own + v * d_in : halo_buf + (v - n_own) * d_in;
+        for (int64_t o = 0; o < d_out; ++o) {
+            double acc = 0.0;
+            for (int64_t f = 0; f < d_in; ++f)
+                acc += (double)x[f] * (double)w[f * d_out + o];
+            z[v * d_out + o] = acc;
+        }
+    }
+    return z;
+}
+
+/* Source scores s_v = z_v . att[:,0] (every local row) and target scores
+   t_i = z_i . att[:,1] (owned rows); att is [d_out][2] row-major. */
+static void gat_scores(int64_t n_own, int64_t R, int64_t d_out, const double *z,
+                       const float *att, double *s, double *t)
+{
+    for (int64_t v = 0; v < R; ++v) {
+        double a = 0.0, b = 0.0;
+        for (int64_t o = 0; o < d_out; ++o) {
+            a += z[v * d_out + o] * (double)att[2 * o];
+            b += z[v * d_out + o] * (double)att[2 * o + 1];
+        }
+        s[v] = a;
+        if (v < n_own)
+            t[v] = b;
+    }
+}
+
+static double leaky(double x, double slope) { return x > 0.0 ? x : slope * x; }
+
+/* Attention weights of row i: alpha_k = softmax over the row's entries of
+   LeakyReLU(t_i + s_{col_k}); written to a[k - indptr[i]]. */
+static void gat_row_alpha(int64_t i, const int64_t *indptr, const int32_t *col_local,
+                          const double *s, const double *t, double slope, double *a)
+{
+    int64_t kb = indptr[i], ke = indptr[i + 1];
+    double m = -INFINITY;
+    for (int64_t k = kb; k < ke; ++k) {
+        double e = leaky(t[i] + s[col_local[k]], slope);
+        a[k - kb] = e;
+        if (e > m)
+            m = e;
+    }
+    double sum = 0.0;
+    for (int64_t k = kb; k < ke; ++k) {
+        a[k - kb] = exp(a[k - kb] - m);
+        sum += a[k - kb];
+    }
+    for (int64_t k = kb; k < ke; ++k)
+        a[k - kb] /= sum;
+}
+
+/*
+ * GAT forward on one partition:
+ *   z_v      = x_v W                              every local row
+ *   e_ik     = LeakyReLU(t_i + s_{col_k})         entries k of owned row i
+ *   alpha_ik = softmax over row i of e_ik
+ *   h_out_i  = act(sum_k alpha_ik z_{col_k})      (an empty row gives act(0))
+ * Optional alpha output: the weights in CSR entry order [nnz].
+ */
+void oracle_gat_forward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
+                        const int32_t *col_local, const float *h_own, const float *halo_buf,
+                        int64_t d_in, int64_t d_out, const float *w, const float *att,
+                        double slope, int act, float *h_out, float *alpha)
+{
+    int64_t R = n_own + n_halo;
+    double *z = gat_transform(n_own, n_halo, h_own, halo_buf, d_in, d_out, w);
+    double *s = (double *)malloc(sizeof(double) * (size_t)(R > 0 ? R : 1));
+    double *t = (double *)malloc(sizeof(double) * (size_t)(n_own > 0 ? n_own : 1));
+    gat_scores(n_own, R, d_out, z, att, s, t);
+#pragma omp parallel
+    {
+        int64_t maxrow = 1;
+        for (int64_t i = 0; i < n_own; ++i)
+            if (indptr[i + 1] - indptr[i] > maxrow)
+                maxrow = indptr[i + 1] - indptr[i];
+        double *a = (double *)malloc(sizeof(double) * (size_t)maxrow);
+        double *o = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n_own; ++i) {
+            gat_row_alpha(i, indptr, col_local, s, t, slope, a);
+            for (int64_t q = 0; q < d_out; ++q)
+                o[q] = 0.0;
+            for (int64_t k = indptr[i]; k < indptr[i + 1]; ++k) {
+                const double *zc = z + (int64_t)col_local[k] * d_out;
+                for (int64_t q = 0; q < d_out; ++q)
+                    o[q] += a[k - indptr[i]] * zc[q];
+                if (alpha)
+                    alpha[k] = (float)a[k - indptr[i]];
+            }
+            for (int64_t q = 0; q < d_out; ++q) {
+                double v = o[q];
+                if (act == ORACLE_RELU && v < 0.0)
+                    v = 0.0;
+                h_out[i * d_out + q] = (float)v;
+            }
+        }
+        free(o);
+        free(a);
+    }
+    free(t);
+    free(s);
+    free(z);
+}
+
+/*
+ * GAT backward on one partition, by the chain rule through the forward
+ * above (halo rows are constants: they get no gradient, but their z rows
+ * depend on W, so they contribute to dW and to the attention gradient):
+ *   D_i     = dh_out_i * act'(h_out_i)        (mask h_out > 0 for ReLU)
+ *   c_i     = D_i . o_i,  o_i = sum_k alpha_ik z_{col_k}
+ *   dpre_ik = alpha_ik (D_i . z_{col_k} - c_i) * LeakyReLU'(t_i + s_{col_k})
+ *   dz_{col_k} += alpha_ik D_i + dpre_ik att[:,0];   dz_i += dpre_ik att[:,1]
+ *   datt[:,0] = sum dpre_ik z_{col_k};  datt[:,1] = sum dpre_ik z_i
+ *   dW = sum over local rows v of x_v^T dz_v;  dh_in_i = dz_i W^T (owned i)
+ * att and datt are [d_out][2]; dh_in may be NULL.
+ */
+void oracle_gat_backward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
+                         const int32_t *col_local, const float *h_own, const float *halo_buf,
+                         int64_t d_in, int64_t d_out, const float *w, const float *att,
+                         double slope, int act, const float *h_out, const float *dh_out,
+                         float *dw, float *datt, float *dh_in)
+{
+    int64_t R = n_own + n_halo;
+    double *z = gat_transform(n_own, n_halo, h_own, halo_buf, d_in, d_out, w);
+    double *s = (double *)malloc(sizeof(double) * (size_t)(R > 0 ? R : 1));
+    double *t = (double *)malloc(sizeof(double) * (size_t)(n_own > 0 ? n_own : 1));
+    gat_scores(n_own, R, d_out, z, att, s, t);
+    double *dz = (double *)calloc((size_t)(R * d_out > 0 ? R * d_out : 1), sizeof(double));
+    double *da = (double *)calloc((size_t)(2 * d_out > 0 ? 2 * d_out : 1), sizeof(double));
+    int64_t maxrow = 1;
+    for (int64_t i = 0; i < n_own; ++i)
+        if (indptr[i + 1] - indptr[i] > maxrow)
+            maxrow = indptr[i + 1] - indptr[i];
+    double *a = (double *)malloc(sizeof(double) * (size_t)maxrow);
+    double *D = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
+    double *o = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
+    /* rows in ascending order, entries in CSR order: a fixed summation order */
+    for (int64_t i = 0; i < n_own; ++i) {
+        int64_t kb = indptr[i], ke = indptr[i + 1];
+        gat_row_alpha(i, indptr, col_local, s, t, slope, a);
+        for (int64_t q = 0; q < d_out; ++q) {
+            double g = (double)dh_out[i * d_out + q];
+            if (act == ORACLE_RELU && !(h_out[i * d_out + q] > 0.0f))
+                g = 0.0;
+            D[q] = g;
+            o[q] = 0.0;
+        }
+        for (int64_t k = kb; k < ke; ++k) {
+            const double *zc = z + (int64_t)col_local[k] * d_out;
+            for (int64_t q = 0; q < d_out; ++q)
+                o[q] += a[k - kb] * zc[q];
+        }
+        double c = 0.0;
+        for (int64_t q = 0; q < d_out; ++q)
+            c += D[q] * o[q];
+        for (int64_t k = kb; k < ke; ++k) {
+            int64_t col = col_local[k];
+            const double *zc = z + col * d_out;
+            double dalpha = 0.0;
+            for (int64_t q = 0; q < d_out; ++q)
+                dalpha += D[q] * zc[q];
+            double pre = t[i] + s[col];
+            double dpre = a[k - kb] * (dalpha - c) * (pre > 0.0 ? 1.0 : slope);
+            double *dzc = dz + col * d_out, *dzi = dz + i * d_out;
+            for (int64_t q = 0; q < d_out; ++q) {
+                dzc[q] += a[k - kb] * D[q] + dpre * (double)att[2 * q];
+                dzi[q] += dpre * (double)att[2 * q + 1];
+                da[2 * q] += dpre * zc[q];
+                da[2 * q + 1] += dpre * z[i * d_out + q];
+            }
+        }
+    }
+    for (int64_t e = 0; e < 2 * d_out; ++e)
+        datt[e] = (float)da[e];
+    /* dW[f][q] = sum over local rows v of x_v[f] dz_v[q] */
+#pragma omp parallel for schedule(static)
+    for (int64_t f = 0; f < d_in; ++f)
+        for (int64_t q = 0; q < d_out; ++q) {
+            double acc = 0.0;
+            for (int64_t v = 0; v < R; ++v) {
+                const float *x = v < n_own ? h_own + v * d_in : halo_buf + (v - n_own) * d_in;
+                acc += (double)x[f] * dz[v * d_out + q];
+            }
+            dw[f * d_out + q] = (float)acc;
+        }
+    if (dh_in) {
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < n_own; ++i)
+            for (int64_t f = 0; f < d_in; ++f) {
+                double acc = 0.0;
+                for (int64_t q = 0; q < d_out; ++q)
+                    acc += dz[i * d_out + q] * (double)w[f * d_out + q];
+                dh_in[i * d_in + f] = (float)acc;
+            }
+    }
+    free(o);
+    free(D);
+    free(a);
+    free(da);
+    free(dz);
+    free(t);
+    free(s);
+    free(z);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Synchronisation schedule (Algorithm 1)                                   */
 /* ------------------------------------------------------------------------ */
 
