@@ -260,6 +260,69 @@ digest_status digest_pull_add(digest_partition *p, int32_t level, float *gstore,
                               void *hip_stream);
 
 /*
+ * GAT layer over stale halo rows: the stale-representation layer of Eq. 4
+ * with the attention aggregation of the GAT model the paper's experiments
+ * train (single head; the paper cites the model and gives no formulas):
+ *   z_v     = x_v W          for every local row v: owned rows from h_in,
+ *                            halo rows from the stale halo buffer of level
+ *                            layer-1 (digest_pull)
+ *   s_v     = z_v . att[:,0] (source score),  t_i = z_i . att[:,1] (target)
+ *   e_ik    = LeakyReLU(t_i + s_{col k}, negative_slope)
+ *             over the entries k of owned row i (the CSR given at create;
+ *             its values are not used, only its structure)
+ *   alpha   = softmax of e over each row's entries
+ *   h_out_i = act(sum_k alpha_ik z_{col k})   (an empty row gives act(0))
+ * The GAT calls need a second workspace, bound once after
+ * digest_partition_bind_workspace; it keeps z, the scores and alpha of
+ * every layer from the forward for the backward.  The GCN calls are
+ * unaffected by it.
+ */
+
+/* Bytes of the GAT workspace (256-byte aligned device memory). */
+digest_status digest_gat_query(const digest_partition *p, size_t *workspace_bytes);
+
+/* Bind the GAT workspace (caller-owned device memory, at least the queried
+ * size, 256-byte aligned); uploads the transposed-entry permutation and
+ * waits for the upload.  Errors: DIGEST_EINVAL, DIGEST_ENOMEM (too small),
+ * DIGEST_EHIP. */
+digest_status digest_gat_bind_workspace(digest_partition *p, void *dev_ptr, size_t bytes,
+                                        void *hip_stream);
+
+/*
+ * GAT forward of `layer` (1..L):
+ *   h_in  device [n_owned, d_{layer-1}];  w device [d_{layer-1}, d_layer];
+ *   att   device [d_layer, 2] row-major (column 0 source, column 1 target);
+ *   negative_slope in [0, 1] (the GAT model uses 0.2);
+ *   h_out device [n_owned, d_layer];  act DIGEST_ACT_RELU or _IDENTITY.
+ *   d_layer <= 512.
+ * Errors: DIGEST_EINVAL (range, NULL, width), DIGEST_ESTATE (no workspace
+ * or GAT workspace, level layer-1 never pulled), DIGEST_EHIP.
+ */
+digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float *h_in,
+                                 const float *w, const float *att, float negative_slope,
+                                 float *h_out, int32_t act, void *hip_stream);
+
+/*
+ * GAT backward of `layer`, by the chain rule through the forward; halo rows
+ * are constants (no gradient), but their z rows depend on W, so they
+ * contribute to dw and datt:
+ *   D_i      = dh_out_i * act'(h_out_i)
+ *   dpre_ik  = alpha_ik (D_i . z_{col k} - D_i . o_i) LeakyReLU'(t_i + s_{col k})
+ *   dz_{col k} += alpha_ik D_i + dpre_ik att[:,0];  dz_i += dpre_ik att[:,1]
+ *   datt     = [sum dpre_ik z_{col k}, sum dpre_ik z_i]      [d_layer, 2]
+ *   dw       = sum over local rows v of x_v^T dz_v           [d_{layer-1}, d_layer]
+ *   dh_in_i  = dz_i W^T (owned rows; NULL skips it)
+ *   h_in, h_out, dh_out, w, att: as in and out of the forward of the layer.
+ * Sums run in a fixed order (no float atomics).
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no GAT forward of the layer since
+ * the GAT bind, or level layer-1 pulled again since it), DIGEST_EHIP.
+ */
+digest_status digest_gat_backward(digest_partition *p, int32_t layer, const float *h_in,
+                                  const float *h_out, const float *dh_out, const float *w,
+                                  const float *att, float *dw, float *datt, float *dh_in,
+                                  void *hip_stream);
+
+/*
  * Local loss head (Eq. 3 with cross entropy), over all n_owned rows:
  *   loss    = -(1/n) sum_i log softmax(logits_i)[labels_i]   (device, 1 float)
  *   dlogits = (softmax(logits) - onehot(labels)) / n          [n_owned, d_L]

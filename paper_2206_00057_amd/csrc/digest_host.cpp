@@ -46,12 +46,25 @@ enum Kind : int32_t {
     K_HALO_GRAD,
     K_GRAD_PUSH,
     K_GRAD_PULL,
+    K_GAT_TRANSFORM,
+    K_GAT_SCORES,
+    K_GAT_SOFTMAX,
+    K_GAT_AGG,
+    K_GAT_EDGE_GRAD,
+    K_GAT_PERM,
+    K_GAT_AGG_T,
+    K_GAT_SCORE_GRAD,
+    K_GAT_DATT,
+    K_GAT_DW,
+    K_GAT_DGRAD,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "pull_gather", "push_scatter", "spmm_fwd", "gemm_fwd_relu", "gemm_dw_splitk",
     "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent", "loss_mean",
-    "halo_gradient", "grad_push_add", "grad_pull_add"};
+    "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
+    "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
+    "gat_aggregate_transposed", "gat_score_grad", "gat_datt", "gat_dw", "gat_dgrad"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -154,6 +167,26 @@ struct digest_partition {
     std::vector<char> tf;           // per layer: forward ran transform-first
     std::vector<int64_t> fwd_gen;   // per layer: pull_gen of level layer-1 at forward
 
+    // GAT state, in a workspace of its own (digest_gat_bind_workspace)
+    std::vector<int32_t> t_perm;    // entry k of P_m^T is entry t_perm[k] of P_m
+    struct GatLayout {
+        size_t t_perm, ones;
+        std::vector<size_t> z, s, alpha;   // per layer 1..L (index 0 unused)
+        size_t alpha_t, dpre, dpre_t, d_o, dz, ds_src, g2, part;
+        size_t total;
+    } glay{};
+    char *gws = nullptr;
+    std::vector<char> gat_done;      // per layer: a GAT forward since the GAT bind
+    std::vector<int64_t> gat_gen;    // per layer: pull_gen of level layer-1 at that forward
+    std::vector<int32_t> gat_act;
+    std::vector<float> gat_slope;
+
+    template <class T>
+    T *gat(size_t off) const
+    {
+        return reinterpret_cast<T *>(gws + off);
+    }
+
     bool prof = false;
     struct Rec {
         int32_t kind, layer;
@@ -212,6 +245,19 @@ bool narrow_out(int64_t d_in, int64_t d_out)
            digest::narrow_n_lds((int32_t)d_in, (int32_t)d_out) <= digest::kNarrowNLds;
 }
 
+// Split-K slices of a narrow-output weight gradient over R rows, F features
+// (about 2,048 waves: F / 64 feature blocks x slices of >= 32 rows): rows
+// per slice and the number of slices.
+void narrow_rows_plan(int64_t R, int64_t F, int32_t &chunk, int32_t &slices)
+{
+    const int64_t fblocks = (F + 63) / 64;
+    const int64_t target = std::max<int64_t>(1, 2048 / fblocks);
+    int64_t c = std::max<int64_t>(32, (R + target - 1) / target);
+    c = (c + 31) / 32 * 32;
+    chunk = (int32_t)c;
+    slices = (int32_t)std::max<int64_t>(1, (R + c - 1) / c);
+}
+
 // Split-K slices of the transform-first weight gradient H_mix^T G over the
 // n_own + n_halo rows.  Narrow outputs (<= kNarrow) use the MFMA kernel with
 // `chunk` rows per slice; wider ones use the MFMA GEMM twice (owned rows,
@@ -228,13 +274,7 @@ TfPlan tf_plan(int64_t n_own, int64_t n_halo, int64_t d_in, int64_t d_out)
     const int64_t R = n_own + n_halo;
     t.valu = d_out <= digest::kNarrow;
     if (t.valu) {
-        // about 2,048 waves: (d_in / 64) feature blocks x slices of >= 32 rows
-        const int64_t fblocks = (d_in + 63) / 64;
-        const int64_t target = std::max<int64_t>(1, 2048 / fblocks);
-        int64_t chunk = std::max<int64_t>(32, (R + target - 1) / target);
-        chunk = (chunk + 31) / 32 * 32;
-        t.chunk = (int32_t)chunk;
-        t.slices = (int32_t)std::max<int64_t>(1, (R + chunk - 1) / chunk);
+        narrow_rows_plan(R, d_in, t.chunk, t.slices);
     } else {
         splitk_plan(d_in, d_out, n_own, t.s_own, t.k_own);
         if (n_halo > 0)
@@ -295,6 +335,49 @@ void plan_layout(digest_partition &p)
     l.total = o;
 }
 
+// The GAT workspace: the transposed-entry permutation, a column of ones,
+// per layer the transformed rows z, their scores and the attention
+// weights (kept from the forward for the backward), and the backward's
+// scratch, sized for the widest layer.
+void plan_gat_layout(digest_partition &p)
+{
+    auto &l = p.glay;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t r = o;
+        o += align_up(std::max<size_t>(bytes, 1));
+        return r;
+    };
+    const int64_t R = (int64_t)p.n_own + p.n_halo;
+    l.t_perm = take(sizeof(int32_t) * p.nnz);
+    l.ones = take(sizeof(float) * p.n_own);
+    l.z.assign(p.L + 1, 0);
+    l.s.assign(p.L + 1, 0);
+    l.alpha.assign(p.L + 1, 0);
+    int64_t dmax = 0, part = 0;
+    for (int32_t k = 1; k <= p.L; ++k) {
+        const int64_t di = p.widths[k - 1], dout = p.widths[k];
+        l.z[k] = take(sizeof(float) * (size_t)(R * dout));
+        l.s[k] = take(sizeof(float) * (size_t)(R * 2));
+        l.alpha[k] = take(sizeof(float) * (size_t)p.nnz);
+        dmax = std::max(dmax, dout);
+        const TfPlan t = tf_plan(p.n_own, p.n_halo, di, dout);
+        part = std::max<int64_t>(part, (int64_t)t.slices * di * dout);
+        int32_t chunk, slices;
+        narrow_rows_plan(R, dout, chunk, slices);
+        part = std::max<int64_t>(part, (int64_t)slices * dout * 2);
+    }
+    l.alpha_t = take(sizeof(float) * p.nnz);
+    l.dpre = take(sizeof(float) * p.nnz);
+    l.dpre_t = take(sizeof(float) * p.nnz);
+    l.d_o = take(sizeof(float) * (size_t)(p.n_own * dmax));
+    l.dz = take(sizeof(float) * (size_t)(R * dmax));
+    l.ds_src = take(sizeof(float) * (size_t)R);
+    l.g2 = take(sizeof(float) * (size_t)(R * 2));
+    l.part = take(sizeof(float) * (size_t)part);
+    l.total = o;
+}
+
 // RAII bracket of one kernel launch for the instrumentation.
 struct Timed {
     digest_partition *p;
@@ -352,13 +435,15 @@ digest_status need_bound(const digest_partition *p)
 
 // Sparse aggregation over the local CSR (P_m), the CSR of P_in^T (the first
 // n_own rows of the transpose), of P_m^T (all of it) or of P_out^T (its
-// n_halo halo rows, numbered from 0).
+// n_halo halo rows, numbered from 0).  `val` replaces the matrix's values
+// (edge weights in the same entry order); relu stores max(x, 0).
 enum class Csr { Fwd, InT, FullT, HaloT };
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
                        const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
-                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX)
+                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX,
+                       const float *val = nullptr, bool relu = false)
 {
     const bool fwd = which == Csr::Fwd;
     const std::vector<SpmmBlock> *blocks = &p->blocks_f;
@@ -378,9 +463,48 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     return hip_check(
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
-                            p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1, n_src0, d,
-                            out, s, ep, out1, n_out0),
+                            val ? val : p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1,
+                            n_src0, d, out, s, ep, out1, n_out0, relu),
         "spmm");
+}
+
+// T = [h_own; halo] W over the n_own + n_halo local rows (T row-major
+// [n_own + n_halo][d_out]): the narrow-output kernel with W in LDS when the
+// widths allow, else the MFMA GEMM for the owned and for the halo rows.
+digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_own,
+                             const float *halo, const float *w, float *T, hipStream_t s)
+{
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    if (narrow_out(d_in, d_out))
+        return hip_check(digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out,
+                                                 h_own, halo, d_in, w, T, d_out, false, s),
+                         "transform");
+    digest::GemmArgs g{};
+    g.N = d_out;
+    g.K = d_in;
+    g.lda = d_in;
+    g.B = w;
+    g.ldb = d_out;
+    g.ldc = d_out;
+    g.splits = 1;
+    g.kchunk = d_in;
+    if (p->n_own > 0) {
+        g.M = p->n_own;
+        g.A = h_own;
+        g.C = T;
+        g.tile = gemm_tile_for(g.M, d_out, d_in, false);
+        if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
+            return st;
+    }
+    if (p->n_halo > 0) {
+        g.M = p->n_halo;
+        g.tile = gemm_tile_for(g.M, d_out, d_in, false);
+        g.A = halo;
+        g.C = T + (int64_t)p->n_own * d_out;
+        if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
+            return st;
+    }
+    return DIGEST_OK;
 }
 
 }  // namespace
@@ -497,12 +621,14 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
         p->nnz_in = p->t_rowptr[n_owned];
         p->t_src.resize(nnz);
         p->t_val.resize(nnz);
+        p->t_perm.resize(nnz);
         std::vector<int32_t> next(p->t_rowptr.begin(), p->t_rowptr.end() - 1);
         for (int32_t i = 0; i < (int32_t)n_owned; ++i)
             for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k) {
                 const int32_t c = p->col[k];
                 p->t_src[next[c]] = i;
                 p->t_val[next[c]] = p->val[k];
+                p->t_perm[next[c]] = k;
                 ++next[c];
             }
 
@@ -515,6 +641,11 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
             p->long_th = build_blocks(halo_rows, p->n_halo, p->blocks_th);
         }
         plan_layout(*p);
+        plan_gat_layout(*p);
+        p->gat_done.assign(p->L + 1, 0);
+        p->gat_gen.assign(p->L + 1, 0);
+        p->gat_act.assign(p->L + 1, 0);
+        p->gat_slope.assign(p->L + 1, 0.f);
         p->pulled.assign(p->L, 0);
         p->pull_gen.assign(p->L, 0);
         p->fwd_done.assign(p->L + 1, 0);
@@ -722,37 +853,8 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         float *T = p->at<float>(p->lay.tbuf);
         {
             Timed t(p, K_GEMM_FWD, layer, s);
-            if (narrow_out(d_in, d_out)) {
-                if (digest_status st = hip_check(
-                        digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
-                                                halo, d_in, w, T, d_out, false, s),
-                        "transform"))
-                    return st;
-            } else {
-                digest::GemmArgs g{};
-                g.N = d_out;
-                g.K = d_in;
-                g.lda = d_in;
-                g.B = w;
-                g.ldb = d_out;
-                g.ldc = d_out;
-                g.splits = 1;
-                g.kchunk = d_in;
-                g.M = p->n_own;
-                g.A = h_in;
-                g.C = T;
-                g.tile = gemm_tile_for(g.M, d_out, d_in, false);
-                if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
-                    return st;
-                if (p->n_halo > 0) {
-                    g.M = p->n_halo;
-                    g.tile = gemm_tile_for(g.M, d_out, d_in, false);
-                    g.A = halo;
-                    g.C = T + (int64_t)p->n_own * d_out;
-                    if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
-                        return st;
-                }
-            }
+            if (digest_status st = transform_rows(p, layer, h_in, halo, w, T, s))
+                return st;
         }
         if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, d_out,
                                         h_out, layer, s))
@@ -826,29 +928,18 @@ digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A
     return hip_check(digest::launch_gemm(h, s), "times W^T");
 }
 
-// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer, with
-// G = P_m^T D over all local rows.  The halo rows of G feed dW and, when
-// dh_halo is given, the halo gradient G_halo W^T.
-digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
-                                       const float *dh_out, const float *w, float *dw,
-                                       float *dh_in, float *dh_halo, hipStream_t s)
+// dw = [h_own; halo]^T G over the n_own + n_halo local rows (G row-major
+// [n_own + n_halo][d_out]): split-K slices in `part`, summed in slice order.
+// Outputs up to kNarrow wide use the narrow MFMA kernel, wider ones the
+// GEMM over the owned rows and over the halo rows.
+digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *h_in,
+                               const float *halo, const float *G, float *gpart, float *dw,
+                               hipStream_t s, int32_t kind_dw, int32_t kind_reduce)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
-    float *G = p->at<float>(p->lay.tbuf);
-    float *gpart = p->at<float>(p->lay.gemm_part);
-    // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
-    // same launch also writes dh_in = G_own W^T for the owned rows.
-    const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
-                          digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
-                          (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
-    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
-    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
-                                    fused_dh ? &ep : nullptr))
-        return st;
     const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
     {
-        Timed tm(p, K_GEMM_DW, layer, s);
+        Timed tm(p, kind_dw, layer, s);
         if (t.valu) {
             if (digest_status st = hip_check(
                     digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
@@ -886,12 +977,38 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
         }
     }
     {
-        Timed tm(p, K_REDUCE_DW, layer, s);
+        Timed tm(p, kind_reduce, layer, s);
         if (digest_status st = hip_check(
                 digest::launch_splitk_reduce(gpart, t.slices, (int64_t)d_in * d_out, dw, s),
                 "dW reduce"))
             return st;
     }
+    return DIGEST_OK;
+}
+
+// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer, with
+// G = P_m^T D over all local rows.  The halo rows of G feed dW and, when
+// dh_halo is given, the halo gradient G_halo W^T.
+digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
+                                       const float *dh_out, const float *w, float *dw,
+                                       float *dh_in, float *dh_halo, hipStream_t s)
+{
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    float *G = p->at<float>(p->lay.tbuf);
+    float *gpart = p->at<float>(p->lay.gemm_part);
+    // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
+    // same launch also writes dh_in = G_own W^T for the owned rows.
+    const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
+                          digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
+                          (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
+    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
+    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
+                                    fused_dh ? &ep : nullptr))
+        return st;
+    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, G, gpart, dw, s, K_GEMM_DW,
+                                            K_REDUCE_DW))
+        return st;
     if (fused_dh)
         return DIGEST_OK;
     if (dh_in) {
@@ -1188,6 +1305,204 @@ digest_status digest_sgd_average(float *w, const float *const *grads, int32_t n_
     return hip_check(digest::launch_sgd_average(w, g, n_grads, count, lr,
                                                 (hipStream_t)hip_stream),
                      "sgd average");
+}
+
+digest_status digest_gat_query(const digest_partition *p, size_t *workspace_bytes)
+{
+    if (!p || !workspace_bytes)
+        return fail(DIGEST_EINVAL, "NULL handle or output");
+    *workspace_bytes = p->glay.total;
+    return DIGEST_OK;
+}
+
+digest_status digest_gat_bind_workspace(digest_partition *p, void *dev_ptr, size_t bytes,
+                                        void *hip_stream)
+{
+    if (!p || !dev_ptr)
+        return fail(DIGEST_EINVAL, "NULL handle or workspace");
+    if ((uintptr_t)dev_ptr % kAlign)
+        return fail(DIGEST_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+    if (bytes < p->glay.total)
+        return fail(DIGEST_ENOMEM, "GAT workspace has %zu bytes, needs %zu", bytes,
+                    p->glay.total);
+    hipStream_t s = (hipStream_t)hip_stream;
+    char *ws = (char *)dev_ptr;
+    if (p->nnz > 0)
+        if (digest_status st = hip_check(
+                hipMemcpyAsync(ws + p->glay.t_perm, p->t_perm.data(), sizeof(int32_t) * p->nnz,
+                               hipMemcpyHostToDevice, s),
+                "GAT upload"))
+            return st;
+    if (p->n_own > 0) {
+        const std::vector<float> ones((size_t)p->n_own, 1.0f);
+        if (digest_status st = hip_check(
+                hipMemcpyAsync(ws + p->glay.ones, ones.data(), sizeof(float) * p->n_own,
+                               hipMemcpyHostToDevice, s),
+                "GAT upload"))
+            return st;
+        // the host vector dies here: wait for the copy
+        if (digest_status st = hip_check(hipStreamSynchronize(s), "GAT upload"))
+            return st;
+    }
+    p->gws = ws;
+    std::fill(p->gat_done.begin(), p->gat_done.end(), 0);
+    return DIGEST_OK;
+}
+
+digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float *h_in,
+                                 const float *w, const float *att, float negative_slope,
+                                 float *h_out, int32_t act, void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (!p->gws)
+        return fail(DIGEST_ESTATE, "no GAT workspace bound");
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    if (act != DIGEST_ACT_RELU && act != DIGEST_ACT_IDENTITY)
+        return fail(DIGEST_EINVAL, "unknown activation %d", act);
+    if (!(negative_slope >= 0.f && negative_slope <= 1.f))
+        return fail(DIGEST_EINVAL, "negative slope must be in [0, 1]");
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    if (d_out > digest::kGatMaxWidth)
+        return fail(DIGEST_EINVAL, "GAT layer width %d above %d", d_out, digest::kGatMaxWidth);
+    if (!w || !att || (p->n_own > 0 && (!h_in || !h_out)))
+        return fail(DIGEST_EINVAL, "NULL h_in, w, att or h_out");
+    if (p->n_halo > 0 && !p->pulled[layer - 1])
+        return fail(DIGEST_ESTATE, "level %d was never pulled", layer - 1);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    const int32_t R = p->n_own + p->n_halo;
+    float *Z = p->gat<float>(p->glay.z[layer]);
+    float *S = p->gat<float>(p->glay.s[layer]);
+    float *alpha = p->gat<float>(p->glay.alpha[layer]);
+    {
+        Timed t(p, K_GAT_TRANSFORM, layer, s);
+        if (digest_status st = transform_rows(p, layer, h_in, halo, w, Z, s))
+            return st;
+    }
+    {
+        // scores: S = Z att, [R][2] (source, target)
+        Timed t(p, K_GAT_SCORES, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_narrow_n(R, R, d_out, 2, Z, nullptr, d_out, att, S, 2, false, s),
+                "GAT scores"))
+            return st;
+    }
+    if (p->n_own > 0) {
+        {
+            Timed t(p, K_GAT_SOFTMAX, layer, s);
+            if (digest_status st = hip_check(
+                    digest::launch_gat_softmax(p->n_own, p->at<int32_t>(p->lay.rowptr),
+                                               p->at<int32_t>(p->lay.col), S, negative_slope,
+                                               alpha, s),
+                    "GAT softmax"))
+                return st;
+        }
+        if (digest_status st = run_spmm(p, Csr::Fwd, Z, nullptr, R, d_out, h_out, layer, s,
+                                        nullptr, K_GAT_AGG, nullptr, INT32_MAX, alpha,
+                                        act == DIGEST_ACT_RELU))
+            return st;
+    }
+    p->gat_done[layer] = 1;
+    p->gat_gen[layer] = p->pull_gen[layer - 1];
+    p->gat_act[layer] = act;
+    p->gat_slope[layer] = negative_slope;
+    return DIGEST_OK;
+}
+
+digest_status digest_gat_backward(digest_partition *p, int32_t layer, const float *h_in,
+                                  const float *h_out, const float *dh_out, const float *w,
+                                  const float *att, float *dw, float *datt, float *dh_in,
+                                  void *hip_stream)
+{
+    if (digest_status st = need_bound(p))
+        return st;
+    if (!p->gws)
+        return fail(DIGEST_ESTATE, "no GAT workspace bound");
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    if (!w || !att || !dw || !datt || (p->n_own > 0 && (!h_in || !h_out || !dh_out)))
+        return fail(DIGEST_EINVAL, "NULL h_in, h_out, dh_out, w, att, dw or datt");
+    if (!p->gat_done[layer])
+        return fail(DIGEST_ESTATE, "no GAT forward of layer %d since the GAT workspace was bound",
+                    layer);
+    if (p->gat_gen[layer] != p->pull_gen[layer - 1])
+        return fail(DIGEST_ESTATE,
+                    "level %d was pulled again between the GAT forward and backward of layer %d",
+                    layer - 1, layer);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const int32_t R = p->n_own + p->n_halo;
+    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    const float *Z = p->gat<float>(p->glay.z[layer]);
+    const float *S = p->gat<float>(p->glay.s[layer]);
+    const float *alpha = p->gat<float>(p->glay.alpha[layer]);
+    float *alpha_t = p->gat<float>(p->glay.alpha_t);
+    float *dpre = p->gat<float>(p->glay.dpre);
+    float *dpre_t = p->gat<float>(p->glay.dpre_t);
+    float *dO = p->gat<float>(p->glay.d_o);
+    float *dz = p->gat<float>(p->glay.dz);
+    float *ds_src = p->gat<float>(p->glay.ds_src);
+    float *g2 = p->gat<float>(p->glay.g2);
+    float *part = p->gat<float>(p->glay.part);
+    {
+        // dO, the per-edge score gradients and their row sums (g2[i][1])
+        Timed t(p, K_GAT_EDGE_GRAD, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_gat_edge_grad(p->n_own, d_out, p->at<int32_t>(p->lay.rowptr),
+                                             p->at<int32_t>(p->lay.col), alpha, S, Z, h_out,
+                                             dh_out, p->gat_act[layer] == DIGEST_ACT_RELU,
+                                             p->gat_slope[layer], dO, dpre, g2, s),
+                "GAT edge gradient"))
+            return st;
+    }
+    {
+        Timed t(p, K_GAT_PERM, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_gather_perm2(p->nnz, p->gat<int32_t>(p->glay.t_perm), alpha, dpre,
+                                            alpha_t, dpre_t, s),
+                "GAT transpose"))
+            return st;
+    }
+    // dz = (alpha-weighted P_m)^T dO over every local row
+    if (digest_status st = run_spmm(p, Csr::FullT, dO, nullptr, p->n_own, d_out, dz, layer, s,
+                                    nullptr, K_GAT_AGG_T, nullptr, INT32_MAX, alpha_t))
+        return st;
+    // source-score gradients: column sums of dpre, then the score terms of dz
+    if (digest_status st = run_spmm(p, Csr::FullT, p->gat<float>(p->glay.ones), nullptr,
+                                    p->n_own, 1, ds_src, layer, s, nullptr, K_GAT_SCORE_GRAD,
+                                    nullptr, INT32_MAX, dpre_t))
+        return st;
+    {
+        Timed t(p, K_GAT_SCORE_GRAD, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_gat_rank1(R, p->n_own, d_out, att, ds_src, g2, dz, s),
+                "GAT score terms"))
+            return st;
+    }
+    {
+        // datt = Z^T g2 ([d_out][2])
+        int32_t chunk, slices;
+        narrow_rows_plan(R, d_out, chunk, slices);
+        Timed t(p, K_GAT_DATT, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_dw_narrow(R, R, d_out, 2, Z, nullptr, d_out, g2, chunk, slices,
+                                         part, s),
+                "GAT datt"))
+            return st;
+        if (digest_status st = hip_check(
+                digest::launch_splitk_reduce(part, slices, (int64_t)d_out * 2, datt, s),
+                "GAT datt reduce"))
+            return st;
+    }
+    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, dz, part, dw, s, K_GAT_DW,
+                                            K_GAT_DW))
+        return st;
+    if (!dh_in || p->n_own == 0)
+        return DIGEST_OK;
+    Timed t(p, K_GAT_DGRAD, layer, s);
+    return times_wt(p->n_own, d_in, d_out, dz, w, dh_in, s);
 }
 
 digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull, int32_t *do_push)

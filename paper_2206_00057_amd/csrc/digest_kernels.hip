@@ -18,11 +18,14 @@
 //                  contiguous runs (shared operand strips share an L2): the dense
 //                  transform AH W, the weight gradient AH^T D and D W^T.
 //   k_splitk_reduce  deterministic sum of split-K partial products.
-//   k_narrow_n / k_narrow_k / k_dw_narrow  products with one side at most
-//                  16 wide (the transform-first last layer).
+//   k_narrow_n / k_narrow_k / k_times_wt / k_dw_narrow  products with one
+//                  narrow side (the transform-first last layer).
 //   k_softmax_xent / k_loss_reduce  the mean cross-entropy loss head.
 //   k_sgd_average  Algorithm 1's global update: the average of the M
 //                  locally updated models, W - lr * mean of the gradients.
+//   k_gat_*        the GAT layer over stale halo rows (Eq. 4 with an
+//                  attention aggregation): edge softmax, the per-edge
+//                  gradient, and the helpers of its backward.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -195,10 +198,21 @@ struct SpmmOut {
     float *out0;
     float *out1;
     int32_t n0;
+    bool relu;   // store max(x, 0)
 
     __device__ __forceinline__ float *row(int32_t r, int32_t d) const
     {
         return r < n0 ? out0 + (int64_t)r * d : out1 + (int64_t)(r - n0) * d;
+    }
+    template <int VEC>
+    __device__ __forceinline__ void put(int32_t r, int32_t d, int32_t off, float (&v)[VEC]) const
+    {
+        if (relu) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i)
+                v[i] = fmaxf(v[i], 0.f);
+        }
+        store_vec<VEC>(row(r, d) + off, v);
     }
 };
 
@@ -312,7 +326,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
                 for (int ch = 0; ch < NCH; ++ch) {
                     const int c = c0 + ch * GL + gl;
                     if (c < dv)
-                        store_vec<VEC>(out.row(row, d) + c * VEC, acc[ch]);
+                        out.put<VEC>(row, d, c * VEC, acc[ch]);
                 }
             }
         } else {
@@ -331,7 +345,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
 #pragma unroll
                     for (int w = 0; w < kSpmmWaves; ++w)
                         sum += red[w][t];
-                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = sum;
+                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = out.relu ? fmaxf(sum, 0.f) : sum;
                 }
             }
             __syncthreads();
@@ -484,7 +498,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
                         acc[v] = fmaf(aa[j][u], x[j][u][v], acc[v]);
         }
         if (lane_ok)
-            store_vec<VEC>(out.row(row, d) + gl * VEC, acc);
+            out.put<VEC>(row, d, gl * VEC, acc);
         if constexpr (EP) {
             if (float *o2 = ep_row(ep, row)) {
                 float gk[kNarrow];
@@ -1234,6 +1248,195 @@ __global__ __launch_bounds__(kLossThreads) void k_softmax_xent_wide(
 }
 
 // ---------------------------------------------------------------------------
+// GAT layer
+// ---------------------------------------------------------------------------
+
+constexpr int kGatGroup = 16;   // lanes per row in the edge softmax
+constexpr int kGatCache = 4;    // scores a lane keeps between the passes
+
+__device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? x : slope * x; }
+
+// alpha[k] = softmax over the entries k of row i of
+// LeakyReLU(s[i][1] + s[col[k]][0]), s [rows][2] (source, target score).
+// A group of kGatGroup lanes takes a row and strides over its entries three
+// times: the maximum, the sum of exponentials, the weights; the group
+// combines its lanes by a fixed butterfly, so results are deterministic.
+// The first kGatCache scores of each lane stay in registers between passes.
+__global__ __launch_bounds__(256) void k_gat_softmax(int32_t n_rows,
+                                                     const int32_t *__restrict__ rowptr,
+                                                     const int32_t *__restrict__ col,
+                                                     const float *__restrict__ s, float slope,
+                                                     float *__restrict__ alpha)
+{
+    const int gl = threadIdx.x % kGatGroup;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kGatGroup;
+    if (row >= n_rows)
+        return;   // whole groups leave together; the butterflies stay inside a group
+    const int kb = rowptr[row], ke = rowptr[row + 1];
+    const float t = s[2 * row + 1];
+    float ec[kGatCache];
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kGatCache; ++u) {
+        const int k = kb + gl + u * kGatGroup;
+        ec[u] = k < ke ? leaky(t + s[2 * (int64_t)col[k]], slope) : -INFINITY;
+        m = fmaxf(m, ec[u]);
+    }
+    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
+        m = fmaxf(m, leaky(t + s[2 * (int64_t)col[k]], slope));
+#pragma unroll
+    for (int off = kGatGroup / 2; off > 0; off >>= 1)
+        m = fmaxf(m, __shfl_xor(m, off));
+    float l = 0.f;
+#pragma unroll
+    for (int u = 0; u < kGatCache; ++u)
+        l += kb + gl + u * kGatGroup < ke ? expf(ec[u] - m) : 0.f;
+    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
+        l += expf(leaky(t + s[2 * (int64_t)col[k]], slope) - m);
+#pragma unroll
+    for (int off = kGatGroup / 2; off > 0; off >>= 1)
+        l += __shfl_xor(l, off);
+    const float inv = 1.f / l;
+#pragma unroll
+    for (int u = 0; u < kGatCache; ++u) {
+        const int k = kb + gl + u * kGatGroup;
+        if (k < ke)
+            alpha[k] = expf(ec[u] - m) * inv;
+    }
+    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
+        alpha[k] = expf(leaky(t + s[2 * (int64_t)col[k]], slope) - m) * inv;
+}
+
+// Per-edge gradient of the GAT layer, one wave per owned row i:
+//   D_i     = dh_out_i * 1[h_out_i > 0] (relu) or dh_out_i    -> dO_i
+//   c_i     = D_i . h_out_i  (= D_i . o_i: the mask zeroes D where o <= 0)
+//   dpre[k] = alpha[k] (D_i . z_{col k} - c_i) * LeakyReLU'(t_i + s_{col k})
+//   g2[i][1] = sum_k dpre[k]
+// The wave's G = 64 / GL lane groups split the row's entries; inside a group
+// GL lanes hold D_i as NCH vectors of VEC features (every group the same)
+// and gather the matching features of z; a group's dot product and the row
+// sum are fixed butterflies.
+template <int VEC, int GL, int NCH>
+__global__ __launch_bounds__(256) void k_gat_edge_grad(
+    int32_t n_own, int32_t d, const int32_t *__restrict__ rowptr,
+    const int32_t *__restrict__ col, const float *__restrict__ alpha,
+    const float *__restrict__ s, const float *__restrict__ z, const float *__restrict__ h_out,
+    const float *__restrict__ dh_out, bool relu, float slope, float *__restrict__ dO,
+    float *__restrict__ dpre, float *__restrict__ g2)
+{
+    constexpr int G = kWave / GL;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int g = lane / GL, gl = lane % GL;
+    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (row >= n_own)
+        return;   // uniform per wave
+    const int dv = d / VEC;
+    float D[NCH][VEC];
+    float c = 0.f;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+        const int cv = ch * GL + gl;
+        if (cv < dv) {
+            float dh[VEC], h[VEC];
+            load_vec<VEC>(dh_out + row * d + cv * VEC, dh);
+            load_vec<VEC>(h_out + row * d + cv * VEC, h);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                D[ch][v] = (!relu || h[v] > 0.f) ? dh[v] : 0.f;
+                c = fmaf(D[ch][v], h[v], c);
+            }
+            if (g == 0)
+                store_vec<VEC>(dO + row * d + cv * VEC, D[ch]);
+        } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                D[ch][v] = 0.f;
+        }
+    }
+#pragma unroll
+    for (int off = GL / 2; off > 0; off >>= 1)
+        c += __shfl_xor(c, off);
+    const float t = s[2 * row + 1];
+    const int kb = rowptr[row], ke = rowptr[row + 1];
+    float rowsum = 0.f;
+    for (int k0 = kb; k0 < ke; k0 += G) {
+        const int k = k0 + g;
+        const bool ok = k < ke;
+        const int64_t j = ok ? col[k] : 0;
+        float dot = 0.f;
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            const int cv = ch * GL + gl;
+            if (ok && cv < dv) {
+                float zv[VEC];
+                load_vec<VEC>(z + j * d + cv * VEC, zv);
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+                    dot = fmaf(D[ch][v], zv[v], dot);
+            }
+        }
+#pragma unroll
+        for (int off = GL / 2; off > 0; off >>= 1)
+            dot += __shfl_xor(dot, off);
+        if (ok) {
+            const float pre = t + s[2 * j];
+            const float dp = alpha[k] * (dot - c) * (pre > 0.f ? 1.f : slope);
+            if (gl == 0) {
+                dpre[k] = dp;
+                rowsum += dp;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
+        rowsum += __shfl_xor(rowsum, off);
+    if (lane == 0)
+        g2[2 * row + 1] = rowsum;
+}
+
+// a_t[k] = a[perm[k]], b_t[k] = b[perm[k]]: edge values into the entry order
+// of the transposed CSR.
+__global__ __launch_bounds__(256) void k_gather_perm2(int64_t n, const int32_t *__restrict__ perm,
+                                                      const float *__restrict__ a,
+                                                      const float *__restrict__ b,
+                                                      float *__restrict__ a_t,
+                                                      float *__restrict__ b_t)
+{
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < n) {
+        const int32_t p = perm[k];
+        a_t[k] = a[p];
+        b_t[k] = b[p];
+    }
+}
+
+// Score terms of the GAT backward over the local rows v < R:
+//   dz[v] += ds_src[v] att[:,0] + (v < n_own ? g2[v][1] att[:,1] : 0)
+//   g2[v][0] = ds_src[v];  g2[v][1] = 0 for the halo rows
+// (g2 then holds the gradient of the scores, [R][2]).  A thread per element
+// of dz; the thread of column 0 writes g2.
+__global__ __launch_bounds__(256) void k_gat_rank1(int64_t R, int32_t n_own, int32_t d,
+                                                   const float *__restrict__ att,
+                                                   const float *__restrict__ ds_src,
+                                                   float *__restrict__ g2,
+                                                   float *__restrict__ dz)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= R * d)
+        return;
+    const int64_t v = e / d;
+    const int q = (int)(e % d);
+    const float a = ds_src[v];
+    const float b = v < n_own ? g2[2 * v + 1] : 0.f;
+    dz[e] += a * att[2 * q] + b * att[2 * q + 1];
+    if (q == 0) {
+        g2[2 * v] = a;
+        if (v >= n_own)
+            g2[2 * v + 1] = 0.f;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Global parameter update
 // ---------------------------------------------------------------------------
 
@@ -1480,7 +1683,7 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep, float *out1,
-                       int32_t n_out0)
+                       int32_t n_out0, bool relu)
 {
     if (ep && (!spmm_epilogue_ok(d, ep->n2, ep->out2) ||
                (ep->out3 && !spmm_epilogue_ok(d, ep->n2, ep->out3))))
@@ -1489,7 +1692,9 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         return hipErrorInvalidValue;
     if (n_blocks <= 0 || d <= 0)
         return hipSuccess;
-    const SpmmOut out{out0, out1, n_out0};
+    if (relu && ep)
+        return hipErrorInvalidValue;   // the epilogue reads the stored row back
+    const SpmmOut out{out0, out1, n_out0, relu};
     int vec = pick_vec(d, src0, out0);
     if (src1 && pick_vec(d, src1, nullptr) < vec)
         vec = pick_vec(d, src1, nullptr);
@@ -1779,6 +1984,106 @@ hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t co
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(k_sgd_average, dim3((unsigned)blocks), dim3(256), 0, s, w, g, n, count, lr);
+    return hipGetLastError();
+}
+
+hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32_t *col,
+                              const float *s, float slope, float *alpha, hipStream_t st)
+{
+    if (n_rows <= 0)
+        return hipSuccess;
+    const int64_t blocks = ((int64_t)n_rows * kGatGroup + 255) / 256;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_gat_softmax, dim3((unsigned)blocks), dim3(256), 0, st, n_rows, rowptr,
+                       col, s, slope, alpha);
+    return hipGetLastError();
+}
+
+namespace {
+
+template <int VEC, int GL, int NCH>
+hipError_t gat_edge_grad_t(int32_t n_own, int32_t d, const int32_t *rowptr, const int32_t *col,
+                           const float *alpha, const float *s, const float *z,
+                           const float *h_out, const float *dh_out, bool relu, float slope,
+                           float *dO, float *dpre, float *g2, hipStream_t st)
+{
+    const int64_t blocks = ((int64_t)n_own + 3) / 4;
+    hipLaunchKernelGGL((k_gat_edge_grad<VEC, GL, NCH>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu, slope, dO, dpre,
+                       g2);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
+                                const int32_t *col, const float *alpha, const float *s,
+                                const float *z, const float *h_out, const float *dh_out,
+                                bool relu, float slope, float *dO, float *dpre, float *g2,
+                                hipStream_t st)
+{
+    if (n_own <= 0)
+        return hipSuccess;
+    if (d < 1 || d > kGatMaxWidth)
+        return hipErrorInvalidValue;
+    // vectors of 4/2/1 floats as width and alignment allow; a group wide
+    // enough for the row, at most a wave; up to 8 vectors per lane
+    int vec = 1;
+    auto al = [](const void *q, uintptr_t n) { return ((uintptr_t)q % n) == 0; };
+    if (d % 4 == 0 && al(z, 16) && al(h_out, 16) && al(dh_out, 16) && al(dO, 16))
+        vec = 4;
+    else if (d % 2 == 0 && al(z, 8) && al(h_out, 8) && al(dh_out, 8) && al(dO, 8))
+        vec = 2;
+    const int dv = d / vec;
+    const int gl = dv <= 4 ? 4 : (dv <= 8 ? 8 : (dv <= 16 ? 16 : (dv <= 32 ? 32 : 64)));
+    const int nch = (dv + gl - 1) / gl;
+#define DIGEST_GEG(V, L, C)                                                                     \
+    return gat_edge_grad_t<V, L, C>(n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu,    \
+                                    slope, dO, dpre, g2, st)
+#define DIGEST_GEG_V(V)                                                                         \
+    do {                                                                                        \
+        if (gl == 4) DIGEST_GEG(V, 4, 1);                                                       \
+        if (gl == 8) DIGEST_GEG(V, 8, 1);                                                       \
+        if (gl == 16) DIGEST_GEG(V, 16, 1);                                                     \
+        if (gl == 32) DIGEST_GEG(V, 32, 1);                                                     \
+        if (nch <= 1) DIGEST_GEG(V, 64, 1);                                                     \
+        if (nch <= 2) DIGEST_GEG(V, 64, 2);                                                     \
+        if (nch <= 4) DIGEST_GEG(V, 64, 4);                                                     \
+        DIGEST_GEG(V, 64, 8);                                                                   \
+    } while (0)
+    if (vec == 4)
+        DIGEST_GEG_V(4);
+    if (vec == 2)
+        DIGEST_GEG_V(2);
+    DIGEST_GEG_V(1);
+#undef DIGEST_GEG_V
+#undef DIGEST_GEG
+}
+
+hipError_t launch_gather_perm2(int64_t n, const int32_t *perm, const float *a, const float *b,
+                               float *a_t, float *b_t, hipStream_t st)
+{
+    if (n <= 0)
+        return hipSuccess;
+    const int64_t blocks = (n + 255) / 256;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_gather_perm2, dim3((unsigned)blocks), dim3(256), 0, st, n, perm, a, b,
+                       a_t, b_t);
+    return hipGetLastError();
+}
+
+hipError_t launch_gat_rank1(int64_t R, int32_t n_own, int32_t d, const float *att,
+                            const float *ds_src, float *g2, float *dz, hipStream_t st)
+{
+    if (R <= 0 || d <= 0)
+        return hipSuccess;
+    const int64_t blocks = (R * d + 255) / 256;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_gat_rank1, dim3((unsigned)blocks), dim3(256), 0, st, R, n_own, d, att,
+                       ds_src, g2, dz);
     return hipGetLastError();
 }
 

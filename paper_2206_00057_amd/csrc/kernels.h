@@ -36,7 +36,8 @@ hipError_t launch_add_clear_rows(const int32_t *sidx, const int32_t *didx, int32
 // Two-source CSR aggregation out[r] = sum_k val[k] * src(col[k]) over the
 // rows named by the blocks.  Column c < n_src0 reads row c of src0,
 // otherwise row (c - n_src0) of src1.  Every named row is fully written:
-// row r < n_out0 to out0[r], row r >= n_out0 to out1[r - n_out0].
+// row r < n_out0 to out0[r], row r >= n_out0 to out1[r - n_out0]; relu
+// stores max(x, 0) (not with an epilogue).
 // Optional epilogue of a narrow aggregation (d <= kNarrow): rows r < rows
 // also get out2[r][n] = sum_k out[r][k] w[n][k] for n < n2, w row-major
 // [n2][d] (out times w^T), and with out3 the rows r >= rows get the same
@@ -55,7 +56,7 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep = nullptr,
-                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX);
+                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX, bool relu = false);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
 // slices (each its own grid part) when splits > 1.
@@ -137,6 +138,27 @@ struct GradList {
 };
 hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t count, float lr,
                               hipStream_t s);
+
+// GAT layer (attention aggregation over stale halo rows).  s is [rows][2]
+// (source score, target score); alpha, dpre are in CSR entry order.
+constexpr int kGatMaxWidth = 512;
+// alpha[k] = softmax over row i's entries of LeakyReLU(s[i][1] + s[col k][0]).
+hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32_t *col,
+                              const float *s, float slope, float *alpha, hipStream_t st);
+// dO = dh_out (masked by h_out > 0 with relu), dpre[k] the gradient of the
+// k-th pre-activation score, g2[i][1] = sum of row i's dpre; d <= kGatMaxWidth.
+hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
+                                const int32_t *col, const float *alpha, const float *s,
+                                const float *z, const float *h_out, const float *dh_out,
+                                bool relu, float slope, float *dO, float *dpre, float *g2,
+                                hipStream_t st);
+// a_t[k] = a[perm[k]], b_t[k] = b[perm[k]] for k < n.
+hipError_t launch_gather_perm2(int64_t n, const int32_t *perm, const float *a, const float *b,
+                               float *a_t, float *b_t, hipStream_t st);
+// dz[v] += ds_src[v] att[:,0] + (v < n_own ? g2[v][1] att[:,1] : 0) over
+// v < R; then g2[v][0] = ds_src[v], g2[v][1] = 0 for v >= n_own.
+hipError_t launch_gat_rank1(int64_t R, int32_t n_own, int32_t d, const float *att,
+                            const float *ds_src, float *g2, float *dz, hipStream_t st);
 
 // GEMM K step; the smallest workgroup tile of C is kGemmBM x kGemmBN.
 constexpr int kGemmBM = 64;

@@ -56,6 +56,10 @@ def lib():
             "digest_sgd_average": ([P, P, i32, i64, ctypes.c_float, P], st),
             "digest_halo_gradient": ([P, i32, P, P, P, P, P], st),
             "digest_layer_backward_halo": ([P, i32, P, P, P, P, P, P, P, P], st),
+            "digest_gat_query": ([P, P], st),
+            "digest_gat_bind_workspace": ([P, P, sz, P], st),
+            "digest_gat_forward": ([P, i32, P, P, P, ctypes.c_float, P, i32, P], st),
+            "digest_gat_backward": ([P, i32, P, P, P, P, P, P, P, P, P], st),
             "digest_push_add": ([P, i32, P, P, P], st),
             "digest_pull_add": ([P, i32, P, P, P], st),
             "digest_sync_period": ([i32, i64, P, P], st),
@@ -265,6 +269,53 @@ def digest_layer_backward_halo(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_h
         _dev(w, torch.float32, di * do, "w"), _dev(dw, torch.float32, di * do, "dw"),
         _dev(dh_in, torch.float32, p.n_own * di, "dh_in"),
         _dev(dh_halo, torch.float32, p.n_halo * di, "dh_halo"), _stream(stream)))
+
+
+GAT_SLOPE = 0.2   # the GAT model's LeakyReLU slope
+
+
+def digest_gat_query(p):
+    """Bytes of the partition's GAT workspace."""
+    n = ctypes.c_size_t(0)
+    _check(lib().digest_gat_query(p.handle, ctypes.byref(n)))
+    return int(n.value)
+
+
+def digest_gat_bind_workspace(p, workspace, stream=None):
+    """Bind a CUDA tensor of at least digest_gat_query(p) bytes."""
+    import torch
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda:
+        raise TypeError("GAT workspace must be a CUDA tensor")
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib().digest_gat_bind_workspace(p.handle, ctypes.c_void_p(workspace.data_ptr()),
+                                           nbytes, _stream(stream)))
+    p.gat_workspace = workspace   # kept alive with the handle
+
+
+def digest_gat_forward(p, layer, h_in, w, att, h_out, act, slope=GAT_SLOPE, stream=None):
+    import torch
+    _check_layer(p, layer)
+    di, do = p.widths[layer - 1], p.widths[layer]
+    _check(lib().digest_gat_forward(
+        p.handle, int(layer), _dev(h_in, torch.float32, p.n_own * di, "h_in"),
+        _dev(w, torch.float32, di * do, "w"), _dev(att, torch.float32, do * 2, "att"),
+        ctypes.c_float(slope), _dev(h_out, torch.float32, p.n_own * do, "h_out"), int(act),
+        _stream(stream)))
+
+
+def digest_gat_backward(p, layer, h_in, h_out, dh_out, w, att, dw, datt, dh_in=None,
+                        stream=None):
+    import torch
+    _check_layer(p, layer)
+    di, do = p.widths[layer - 1], p.widths[layer]
+    _check(lib().digest_gat_backward(
+        p.handle, int(layer), _dev(h_in, torch.float32, p.n_own * di, "h_in"),
+        _dev(h_out, torch.float32, p.n_own * do, "h_out"),
+        _dev(dh_out, torch.float32, p.n_own * do, "dh_out"),
+        _dev(w, torch.float32, di * do, "w"), _dev(att, torch.float32, do * 2, "att"),
+        _dev(dw, torch.float32, di * do, "dw"), _dev(datt, torch.float32, do * 2, "datt"),
+        _dev(dh_in, torch.float32, p.n_own * di, "dh_in") if dh_in is not None else None,
+        _stream(stream)))
 
 
 def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):

@@ -1,0 +1,171 @@
+"""GPU parity of the GAT layer over stale halo rows (libdigest's
+digest_gat_forward / digest_gat_backward) against the CPU oracle on the same
+seeded inputs: element by element at sizes the oracle finishes in seconds
+(several tiles, ragged tails, odd widths, no-halo and one-row edge cases),
+and on a Flickr-shaped partition with 500-entry rows."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2206_00057_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 1e-4, 1e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def assert_close(gpu, ref, name, scale_tol=1e-4):
+    g = np.asarray(gpu, np.float64)
+    r = np.asarray(ref, np.float64)
+    err = np.abs(g - r)
+    assert np.all(np.isfinite(g)), name
+    assert not (err > ATOL + RTOL * np.abs(r)).any(), f"{name}: max err {err.max():.3e}"
+    peak = float(np.abs(r).max())
+    assert peak == 0 or err.max() / peak <= scale_tol, f"{name}: scale err {err.max() / peak:.3e}"
+
+
+class Case:
+    """One partition bound on the GPU (both workspaces) beside its oracle."""
+
+    def __init__(self, n_global, part, widths, seed=0):
+        from paper_2206_00057_amd import digest as D
+        self.D, self.p, self.widths = D, part, list(widths)
+        self.h = D.digest_partition_create(n_global, part.indptr, part.indices, part.values,
+                                           part.owned, part.halo, widths)
+        self.ws = torch.empty(max(self.h.workspace_bytes, 256), dtype=torch.uint8,
+                              device="cuda")
+        D.digest_partition_bind_workspace(self.h, self.ws)
+        self.gws = torch.empty(max(D.digest_gat_query(self.h), 256), dtype=torch.uint8,
+                               device="cuda")
+        D.digest_gat_bind_workspace(self.h, self.gws)
+        self.op = oracle.OraclePartition(n_global, part.indptr, part.indices, part.values,
+                                         part.owned, part.halo, widths)
+        self.n_global = n_global
+        self.seed = seed
+
+    def pull(self, level, store):
+        self.D.digest_pull(self.h, level, dev(store))
+        self.op.pull(level, store)
+
+    def layer(self, layer, act, label):
+        """Forward and backward of one GAT layer on both sides, compared."""
+        D, p = self.D, self.p
+        di, do = self.widths[layer - 1], self.widths[layer]
+        s = self.seed + 10 * layer
+        h_in = synth.relu_normal((p.n_own, di), seed=s + 1)
+        W = synth.normal((di, do), seed=s + 2, scale=float(np.sqrt(2.0 / (di + do))))
+        # Glorot scale, the GAT model's initialisation of its attention
+        # vectors; much larger vectors make the softmax ill-conditioned (score
+        # rounding times alpha_a alpha_b |z_a - z_b| at near ties)
+        att = synth.normal((do, 2), seed=s + 3, scale=float(np.sqrt(2.0 / (do + 2))))
+        out = torch.empty(p.n_own, do, device="cuda")
+        D.digest_gat_forward(self.h, layer, dev(h_in), dev(W), dev(att), out, act)
+        ref = self.op.gat_forward(layer, h_in, W, att, act)
+        assert_close(host(out), ref, f"{label} h_out", scale_tol=2e-5)
+        dh = synth.normal((p.n_own, do), seed=s + 4, scale=1.0 / max(p.n_own, 1))
+        dw = torch.empty(di, do, device="cuda")
+        datt = torch.empty(do, 2, device="cuda")
+        dh_in = torch.full((p.n_own, di), float("nan"), device="cuda")
+        D.digest_gat_backward(self.h, layer, dev(h_in), dev(ref), dev(dh), dev(W), dev(att),
+                              dw, datt, dh_in)
+        rdw, rdatt, rdh = self.op.gat_backward(layer, h_in, W, att, ref, dh, act,
+                                               want_dh_in=True)
+        assert_close(host(dw), rdw, f"{label} dw")
+        assert_close(host(datt), rdatt, f"{label} datt")
+        assert_close(host(dh_in), rdh, f"{label} dh_in", scale_tol=2e-5)
+        return out, dw, datt, dh_in
+
+
+def tiny_case(widths, seed=1, part=1, n=1200):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], n, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=seed)
+    return Case(g.n, synth.make_partition(cfg, g, part), widths, seed=seed), cfg, g
+
+
+# (widths, what layer 2 exercises): edge-gradient vector width 4/2/1 and
+# chunks per lane, the narrow (W in LDS) and the GEMM transforms
+WIDTHS = [(24, 40, 6), (24, 40, 48), (8, 64, 300), (7, 41, 47), (3, 5, 2), (16, 100, 130),
+          (12, 33, 512)]
+
+
+@pytest.mark.parametrize("widths", WIDTHS, ids=lambda w: "x".join(map(str, w)))
+@pytest.mark.parametrize("act", [oracle.RELU, oracle.IDENTITY], ids=["relu", "identity"])
+def test_gat_layers_match_oracle(widths, act):
+    c, cfg, g = tiny_case(widths)
+    for level in range(c.op.L):
+        c.pull(level, synth.relu_normal((g.n, widths[level]), seed=40 + level))
+    for layer in (1, 2):
+        c.layer(layer, act, f"widths {widths} layer {layer} act {act}")
+
+
+def test_gat_without_halo_and_repeated_calls_are_bitwise_equal():
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=(24, 40, 6), classes=6)
+    g = synth.make_graph(cfg, seed=2)
+    c = Case(g.n, synth.extract_partition(g, np.arange(g.n)), cfg.widths, seed=2)
+    assert c.p.n_halo == 0
+    c.pull(0, synth.features(cfg))
+    first = [host(t).copy() for t in c.layer(1, oracle.RELU, "no halo")]
+    again = [host(t).copy() for t in c.layer(1, oracle.RELU, "no halo, again")]
+    for a, b in zip(first, again):
+        np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_gat_flickr_shaped_partition():
+    """Partition 0 of the Flickr-shaped graph (11,250 owned rows, rows up to
+    ~500 entries), layer 1 (500 -> 256), every output element."""
+    cfg = synth.CONFIGS["medium"]
+    g = synth.make_graph(cfg)
+    part = synth.make_partition(cfg, g, 0)
+    c = Case(g.n, part, (cfg.widths[0], 256), seed=5)
+    c.pull(0, synth.features(cfg))
+    assert int(np.diff(part.indptr).max()) > 64   # long rows: past the cached scores
+    c.layer(1, oracle.RELU, "flickr-shaped layer 1")
+
+
+def test_gat_call_order_and_arguments_are_checked():
+    from paper_2206_00057_amd import digest as D
+    cfg = synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    p = synth.make_partition(cfg, g, 0)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                  cfg.widths)
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    D.digest_partition_bind_workspace(h, ws)
+    torch.cuda.synchronize()
+    L = D.lib()
+    buf = torch.zeros(g.n * 64, device="cuda")
+    a = ctypes.c_void_p(buf.data_ptr())
+    f = ctypes.c_float(0.2)
+    # no GAT workspace yet
+    assert L.digest_gat_forward(h.handle, 1, a, a, a, f, a, 0, None) == D.ESTATE
+    gws = torch.empty(D.digest_gat_query(h), dtype=torch.uint8, device="cuda")
+    assert L.digest_gat_bind_workspace(h.handle, ctypes.c_void_p(gws.data_ptr()), 16,
+                                       None) == D.ENOMEM
+    D.digest_gat_bind_workspace(h, gws)
+    assert L.digest_gat_forward(h.handle, 0, a, a, a, f, a, 0, None) == D.EINVAL
+    assert L.digest_gat_forward(h.handle, 1, a, a, a, ctypes.c_float(1.5), a, 0, None) == D.EINVAL
+    assert L.digest_gat_forward(h.handle, 1, a, a, None, f, a, 0, None) == D.EINVAL
+    # level 0 never pulled
+    assert L.digest_gat_forward(h.handle, 1, a, a, a, f, a, 0, None) == D.ESTATE
+    # backward before any GAT forward
+    assert L.digest_gat_backward(h.handle, 1, a, a, a, a, a, a, a, None, None) == D.ESTATE
+    assert b"GAT forward" in L.digest_last_error()
+    torch.cuda.synchronize()
