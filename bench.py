@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "GCN layer fwd+bwd GTEPS on one partition; % of HBM / MFMA roofline"
+METRIC_GAT = "GAT layer fwd+bwd GTEPS on one partition; % of HBM / MFMA roofline"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 
@@ -71,6 +72,44 @@ def tf_slices(n, nh, di, do):
         chunk = -(-chunk // 32) * 32
         return max(1, -(-R // chunk))
     return splitk(di, do, n)[0] + (splitk(di, do, nh)[0] if nh else 0)
+
+
+def launch_model_gat(st, widths):
+    """Algorithmic bytes, flops and aggregation entries of one launch of each
+    GAT (kernel kind, layer): every operand row read once, every output
+    written once (R = owned + halo rows)."""
+    n, nh, nnz = st["n_own"], st["n_halo"], st["nnz"]
+    R = n + nh
+    L = len(widths) - 1
+    m = {}
+
+    def put(kind, l, b, f=0.0, e=0):
+        m[f"{kind}.l{l}"] = (float(b), float(f), int(e))
+
+    for l in range(1, L + 1):
+        di, do = widths[l - 1], widths[l]
+        put("gat_transform", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
+        put("gat_scores", l, 4 * (R * do + 2 * do + 2 * R), 4.0 * R * do)
+        put("gat_softmax", l, 4 * (n + 1) + 16 * nnz + 4 * n)
+        put("gat_aggregate", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do, e=nnz)
+        put("gat_edge_grad", l, 4 * (n + 1) + 12 * nnz + 12 * n * do + 4 * R * do + 8 * R + 4 * n,
+            e=nnz)
+        put("gat_transpose_edges", l, 20 * nnz)
+        put("gat_aggregate_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do, e=nnz)
+        put("gat_score_sums", l, 4 * (R + 1) + 8 * nnz + 4 * n + 4 * R)
+        put("gat_score_grad", l, 8 * R * do + 8 * do + 4 * R + 12 * R)
+        put("gat_datt", l, 4 * (R * do + 2 * R + 2 * do), 4.0 * R * do)
+        put("gat_dw", l, 4 * (R * di + R * do + di * do), 2.0 * R * di * do)
+        put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
+        if l > 1:
+            put("gat_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
+    put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
+    put("loss_mean", L, 4 * -(-n // (4 * (64 // loss_group(widths[-1])))) + 4)
+    for lev in range(L):
+        put("pull_gather", lev, 8.0 * nh * widths[lev] + 4 * nh)
+    for lev in range(1, L):
+        put("push_scatter", lev, 8.0 * st["n_boundary"] * widths[lev] + 8 * st["n_boundary"])
+    return m
 
 
 def launch_model(st, widths):
@@ -142,8 +181,9 @@ def measured_traffic(workload, key):
     return float(kv["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
-    """The oracle as it stands, timed on this host's cores on whole rounds."""
+def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s, atts=None):
+    """The oracle as it stands, timed on this host's cores on whole rounds
+    (GCN layers, or GAT layers when atts are given)."""
     import oracle
     L = cfg.layers
     op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
@@ -163,15 +203,22 @@ def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s):
             if do_pull and l >= 2:
                 op.pull(l - 1, stores[l - 1])
             act = oracle.RELU if l < L else oracle.IDENTITY
-            outs.append((h, op.forward(l, h, Ws[l - 1], act)))
+            if atts is not None:
+                outs.append((h, op.gat_forward(l, h, Ws[l - 1], atts[l - 1], act)))
+            else:
+                outs.append((h, op.forward(l, h, Ws[l - 1], act)))
             h = outs[-1][1]
             if do_push and l < L:
                 op.push(l, h, stores[l])
         _, dh = oracle.softmax_xent(h, y)
         for l in range(L, 0, -1):
             act = oracle.RELU if l < L else oracle.IDENTITY
-            _, dh = op.backward(l, outs[l - 1][0], Ws[l - 1], outs[l - 1][1], dh, act,
-                                want_dh_in=l > 1)
+            if atts is not None:
+                _, _, dh = op.gat_backward(l, outs[l - 1][0], Ws[l - 1], atts[l - 1],
+                                           outs[l - 1][1], dh, act, want_dh_in=l > 1)
+            else:
+                _, dh = op.backward(l, outs[l - 1][0], Ws[l - 1], outs[l - 1][1], dh, act,
+                                    want_dh_in=l > 1)
         if time.perf_counter() - t0 >= budget_s:
             break
     return rounds, time.perf_counter() - t0, oracle.num_threads()
@@ -242,6 +289,9 @@ def main():
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="before the rounds, copy a float32 buffer of this many MiB once "
                          "(a plain copy kernel of known size for counter calibration)")
+    ap.add_argument("--model", default="gcn", choices=("gcn", "gat"),
+                    help="layer type: the GCN layer of Eq. 5 or the GAT layer over stale halo "
+                         "rows")
     ap.add_argument("--train", action="store_true",
                     help="Algorithm 1 rounds over every subgraph of the graph instead of one")
     ap.add_argument("--lr", type=float, default=0.1, help="SGD learning rate for --train")
@@ -275,13 +325,18 @@ def main():
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     L = cfg.layers
     dX, dWs, dy = dev(X), [dev(w) for w in Ws], dev(y)
+    gat = args.model == "gat"
+    atts = synth.attentions(cfg) if gat else None
+    datts = [dev(a) for a in atts] if gat else None
     # stores initialised by one full-graph forward at the initial weights (library, no halo)
-    full = step.GpuPartition(g.n, synth.extract_partition(g, np.arange(g.n)), cfg.widths)
+    full = step.GpuPartition(g.n, synth.extract_partition(g, np.arange(g.n)), cfg.widths,
+                             model=args.model, atts=datts)
     full.forward(dX, dWs)
     stores = [dX] + [full.H[l].clone() for l in range(1, L)]
     del full
     torch.cuda.synchronize()
-    gp = step.GpuPartition(g.n, part, cfg.widths, overlap_io=args.overlap_io)
+    gp = step.GpuPartition(g.n, part, cfg.widths, overlap_io=args.overlap_io, model=args.model,
+                           atts=datts)
     x_own = dev(X[part.owned])
     gp.pull_all(stores)
     if args.calibration_copy_mib:
@@ -312,7 +367,10 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
-    edges = sum(st["nnz"] + (st["nnz_in"] if l > 1 else 0) for l in range(1, L + 1))
+    if gat:   # per layer: the forward aggregation and the transposed one of the backward
+        edges = 2 * L * st["nnz"]
+    else:
+        edges = sum(st["nnz"] + (st["nnz_in"] if l > 1 else 0) for l in range(1, L + 1))
     value = edges * args.steps / (ms * 1e-3) / 1e9
     print(f"[bench] timed {args.steps} rounds: {ms:.3f} ms", file=sys.stderr, flush=True)
 
@@ -322,7 +380,7 @@ def main():
         gp.round(r, K, x_own, dWs, stores, dy)
     prof = D.digest_profile_read(gp.p)
     D.digest_profile_enable(gp.p, False)
-    model = launch_model(st, cfg.widths)
+    model = launch_model_gat(st, cfg.widths) if gat else launch_model(st, cfg.widths)
     kernels = {}
     for key, (tot_ms, n_l) in prof.items():
         entry = {"launches": n_l, "avg_us": 1e3 * tot_ms / n_l, "total_ms": tot_ms}
@@ -350,27 +408,29 @@ def main():
     cpu = None
     if not args.no_cpu:
         import oracle
-        nr, secs, cores = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds)
+        nr, secs, cores = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds, atts)
         cpu = {"value": edges * nr / secs / 1e9, "unit": "GTEPS", "cores": cores, "kind": "oracle",
                "sample": f"{nr} whole rounds of the same partition (forward, loss, backward, "
                          f"scheduled pull/push) in {secs:.1f}s, float64 oracle, {cores} threads"}
         # the same oracle on one thread, beside the all-core figure
         oracle.set_num_threads(1)
-        nr1, secs1, _ = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds / 2)
+        nr1, secs1, _ = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds / 2, atts)
         oracle.set_num_threads(cores)
         cpu["single_thread"] = {
             "value": edges * nr1 / secs1 / 1e9, "unit": "GTEPS", "cores": 1,
             "sample": f"{nr1} whole rounds in {secs1:.1f}s, float64 oracle, 1 thread"}
 
     out = {
-        "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1,
+        "metric": METRIC_GAT if gat else METRIC, "value": round(value, 4), "unit": "GTEPS",
+        "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms / args.steps, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {
             "workload": (f"{cfg.name}: synthetic block graph, N={g.n:,}, partition 0 "
                          f"({st['n_own']:,} owned + {st['n_halo']:,} halo rows), "
-                         f"GCN {'->'.join(map(str, cfg.widths))}, sync interval {K}"),
+                         f"{args.model.upper()} {'->'.join(map(str, cfg.widths))}, "
+                         f"sync interval {K}"),
             "n_global": g.n, "n_own": st["n_own"], "n_halo": st["n_halo"],
             "n_boundary": st["n_boundary"], "nnz": st["nnz"], "nnz_in": st["nnz_in"],
             "widths": list(cfg.widths), "sync_interval": K, "edges_per_step": edges,

@@ -54,6 +54,7 @@ enum Kind : int32_t {
     K_GAT_PERM,
     K_GAT_AGG_T,
     K_GAT_SCORE_GRAD,
+    K_GAT_SCORE_SUMS,
     K_GAT_DATT,
     K_GAT_DW,
     K_GAT_DGRAD,
@@ -64,7 +65,8 @@ const char *const kKindNames[K_COUNT] = {
     "splitk_reduce_dw", "gemm_dgrad", "spmm_bwd_transposed", "softmax_xent", "loss_mean",
     "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
     "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
-    "gat_aggregate_transposed", "gat_score_grad", "gat_datt", "gat_dw", "gat_dgrad"};
+    "gat_aggregate_transposed", "gat_score_grad", "gat_score_sums", "gat_datt", "gat_dw",
+    "gat_dgrad"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -1471,7 +1473,7 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
         return st;
     // source-score gradients: column sums of dpre, then the score terms of dz
     if (digest_status st = run_spmm(p, Csr::FullT, p->gat<float>(p->glay.ones), nullptr,
-                                    p->n_own, 1, ds_src, layer, s, nullptr, K_GAT_SCORE_GRAD,
+                                    p->n_own, 1, ds_src, layer, s, nullptr, K_GAT_SCORE_SUMS,
                                     nullptr, INT32_MAX, dpre_t))
         return st;
     {
@@ -1497,7 +1499,7 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
             return st;
     }
     if (digest_status st = weight_grad_rows(p, layer, h_in, halo, dz, part, dw, s, K_GAT_DW,
-                                            K_GAT_DW))
+                                            K_REDUCE_DW))
         return st;
     if (!dh_in || p->n_own == 0)
         return DIGEST_OK;

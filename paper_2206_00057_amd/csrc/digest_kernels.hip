@@ -1251,60 +1251,96 @@ __global__ __launch_bounds__(kLossThreads) void k_softmax_xent_wide(
 // GAT layer
 // ---------------------------------------------------------------------------
 
-constexpr int kGatGroup = 16;   // lanes per row in the edge softmax
 constexpr int kGatCache = 4;    // scores a lane keeps between the passes
 
 __device__ __forceinline__ float leaky(float x, float slope) { return x > 0.f ? x : slope * x; }
 
 // alpha[k] = softmax over the entries k of row i of
 // LeakyReLU(s[i][1] + s[col[k]][0]), s [rows][2] (source, target score).
-// A group of kGatGroup lanes takes a row and strides over its entries three
-// times: the maximum, the sum of exponentials, the weights; the group
-// combines its lanes by a fixed butterfly, so results are deterministic.
-// The first kGatCache scores of each lane stay in registers between passes.
+// A wave takes a row and strides over its entries three times (the
+// maximum, the sum of exponentials, the weights), combining its lanes by a
+// fixed butterfly, so results are deterministic.  Each lane keeps its first
+// kGatCache scores in registers (rows up to 256 entries are read once);
+// beyond them the passes recompute the scores kGatCache entries at a time,
+// their loads all issued before use.
 __global__ __launch_bounds__(256) void k_gat_softmax(int32_t n_rows,
                                                      const int32_t *__restrict__ rowptr,
                                                      const int32_t *__restrict__ col,
                                                      const float *__restrict__ s, float slope,
                                                      float *__restrict__ alpha)
 {
-    const int gl = threadIdx.x % kGatGroup;
-    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kGatGroup;
+    constexpr int U = kGatCache;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
     if (row >= n_rows)
-        return;   // whole groups leave together; the butterflies stay inside a group
+        return;   // uniform per wave
     const int kb = rowptr[row], ke = rowptr[row + 1];
+    if (ke <= kb)
+        return;   // an empty row has no weights
     const float t = s[2 * row + 1];
-    float ec[kGatCache];
+    // scores of entries k0 + lane + u * 64, u < U (-inf past the row); the
+    // loads are unconditional (an entry past the row reads its last one)
+    auto scores = [&](int k0, float (&e)[U]) {
+        int c[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = k0 + lane + u * kWave;
+            c[u] = col[k < ke ? k : ke - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float v = leaky(t + s[2 * (int64_t)c[u]], slope);
+            e[u] = k0 + lane + u * kWave < ke ? v : -INFINITY;
+        }
+    };
+    constexpr int SPAN = U * kWave;
+    float ec[U];
+    scores(kb, ec);
     float m = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < kGatCache; ++u) {
-        const int k = kb + gl + u * kGatGroup;
-        ec[u] = k < ke ? leaky(t + s[2 * (int64_t)col[k]], slope) : -INFINITY;
+    for (int u = 0; u < U; ++u)
         m = fmaxf(m, ec[u]);
-    }
-    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
-        m = fmaxf(m, leaky(t + s[2 * (int64_t)col[k]], slope));
+    for (int k0 = kb + SPAN; k0 < ke; k0 += SPAN) {
+        float e[U];
+        scores(k0, e);
 #pragma unroll
-    for (int off = kGatGroup / 2; off > 0; off >>= 1)
+        for (int u = 0; u < U; ++u)
+            m = fmaxf(m, e[u]);
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
         m = fmaxf(m, __shfl_xor(m, off));
     float l = 0.f;
 #pragma unroll
-    for (int u = 0; u < kGatCache; ++u)
-        l += kb + gl + u * kGatGroup < ke ? expf(ec[u] - m) : 0.f;
-    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
-        l += expf(leaky(t + s[2 * (int64_t)col[k]], slope) - m);
+    for (int u = 0; u < U; ++u)
+        l += kb + lane + u * kWave < ke ? expf(ec[u] - m) : 0.f;
+    for (int k0 = kb + SPAN; k0 < ke; k0 += SPAN) {
+        float e[U];
+        scores(k0, e);
 #pragma unroll
-    for (int off = kGatGroup / 2; off > 0; off >>= 1)
+        for (int u = 0; u < U; ++u)
+            l += k0 + lane + u * kWave < ke ? expf(e[u] - m) : 0.f;
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1)
         l += __shfl_xor(l, off);
     const float inv = 1.f / l;
 #pragma unroll
-    for (int u = 0; u < kGatCache; ++u) {
-        const int k = kb + gl + u * kGatGroup;
+    for (int u = 0; u < U; ++u) {
+        const int k = kb + lane + u * kWave;
         if (k < ke)
             alpha[k] = expf(ec[u] - m) * inv;
     }
-    for (int k = kb + gl + kGatCache * kGatGroup; k < ke; k += kGatGroup)
-        alpha[k] = expf(leaky(t + s[2 * (int64_t)col[k]], slope) - m) * inv;
+    for (int k0 = kb + SPAN; k0 < ke; k0 += SPAN) {
+        float e[U];
+        scores(k0, e);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = k0 + lane + u * kWave;
+            if (k < ke)
+                alpha[k] = expf(e[u] - m) * inv;
+        }
+    }
 }
 
 // Per-edge gradient of the GAT layer, one wave per owned row i:
@@ -1312,12 +1348,15 @@ __global__ __launch_bounds__(256) void k_gat_softmax(int32_t n_rows,
 //   c_i     = D_i . h_out_i  (= D_i . o_i: the mask zeroes D where o <= 0)
 //   dpre[k] = alpha[k] (D_i . z_{col k} - c_i) * LeakyReLU'(t_i + s_{col k})
 //   g2[i][1] = sum_k dpre[k]
-// The wave's G = 64 / GL lane groups split the row's entries; inside a group
-// GL lanes hold D_i as NCH vectors of VEC features (every group the same)
-// and gather the matching features of z; a group's dot product and the row
-// sum are fixed butterflies.
-template <int VEC, int GL, int NCH>
-__global__ __launch_bounds__(256) void k_gat_edge_grad(
+// The wave's G = 64 / GL lane groups split the row's entries, U entries per
+// group in flight at once; inside a group GL lanes hold D_i as NCH vectors
+// of VEC features (every group the same) and gather the matching features
+// of z; the U dot products of a group go through one butterfly together.
+// All sums have a fixed order.  At most four waves per SIMD: left to
+// maximise occupancy the compiler reuses one register quad for every gather
+// and waits on each, which serialises the step.
+template <int VEC, int GL, int NCH, int U>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_gat_edge_grad(
     int32_t n_own, int32_t d, const int32_t *__restrict__ rowptr,
     const int32_t *__restrict__ col, const float *__restrict__ alpha,
     const float *__restrict__ s, const float *__restrict__ z, const float *__restrict__ h_out,
@@ -1359,31 +1398,57 @@ __global__ __launch_bounds__(256) void k_gat_edge_grad(
     const float t = s[2 * row + 1];
     const int kb = rowptr[row], ke = rowptr[row + 1];
     float rowsum = 0.f;
-    for (int k0 = kb; k0 < ke; k0 += G) {
-        const int k = k0 + g;
-        const bool ok = k < ke;
-        const int64_t j = ok ? col[k] : 0;
-        float dot = 0.f;
+    // Every load below is issued unconditionally from a valid address (an
+    // entry past the row reads the row's last entry, a vector past the width
+    // its first vector) and its result is ignored or multiplied by a zero of
+    // D, so all U x NCH gathers of a step are in flight together.
+    for (int k0 = kb; k0 < ke; k0 += G * U) {
+        int kk[U];
+        bool ok[U];
+        int64_t jj[U];
+        float al[U], sj[U], dot[U];
 #pragma unroll
-        for (int ch = 0; ch < NCH; ++ch) {
-            const int cv = ch * GL + gl;
-            if (ok && cv < dv) {
-                float zv[VEC];
-                load_vec<VEC>(z + j * d + cv * VEC, zv);
-#pragma unroll
-                for (int v = 0; v < VEC; ++v)
-                    dot = fmaf(D[ch][v], zv[v], dot);
-            }
+        for (int u = 0; u < U; ++u) {
+            kk[u] = k0 + u * G + g;
+            ok[u] = kk[u] < ke;
+            kk[u] = ok[u] ? kk[u] : ke - 1;
+            jj[u] = col[kk[u]];
         }
 #pragma unroll
+        for (int u = 0; u < U; ++u) {
+            al[u] = alpha[kk[u]];
+            sj[u] = s[2 * jj[u]];
+            dot[u] = 0.f;
+        }
+        float zv[U][NCH][VEC];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int ch = 0; ch < NCH; ++ch) {
+                const int cv = ch * GL + gl < dv ? ch * GL + gl : 0;
+                load_vec<VEC>(z + jj[u] * d + cv * VEC, zv[u][ch]);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+                    dot[u] = fmaf(D[ch][v], zv[u][ch][v], dot[u]);
+#pragma unroll
         for (int off = GL / 2; off > 0; off >>= 1)
-            dot += __shfl_xor(dot, off);
-        if (ok) {
-            const float pre = t + s[2 * j];
-            const float dp = alpha[k] * (dot - c) * (pre > 0.f ? 1.f : slope);
-            if (gl == 0) {
-                dpre[k] = dp;
-                rowsum += dp;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                dot[u] += __shfl_xor(dot[u], off);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (ok[u]) {
+                const float pre = t + sj[u];
+                const float dp = al[u] * (dot[u] - c) * (pre > 0.f ? 1.f : slope);
+                if (gl == 0) {
+                    dpre[kk[u]] = dp;
+                    rowsum += dp;
+                }
             }
         }
     }
@@ -1992,7 +2057,7 @@ hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32
 {
     if (n_rows <= 0)
         return hipSuccess;
-    const int64_t blocks = ((int64_t)n_rows * kGatGroup + 255) / 256;
+    const int64_t blocks = ((int64_t)n_rows + 3) / 4;   // a wave per row
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(k_gat_softmax, dim3((unsigned)blocks), dim3(256), 0, st, n_rows, rowptr,
@@ -2002,14 +2067,14 @@ hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32
 
 namespace {
 
-template <int VEC, int GL, int NCH>
+template <int VEC, int GL, int NCH, int U = 2>
 hipError_t gat_edge_grad_t(int32_t n_own, int32_t d, const int32_t *rowptr, const int32_t *col,
                            const float *alpha, const float *s, const float *z,
                            const float *h_out, const float *dh_out, bool relu, float slope,
                            float *dO, float *dpre, float *g2, hipStream_t st)
 {
     const int64_t blocks = ((int64_t)n_own + 3) / 4;
-    hipLaunchKernelGGL((k_gat_edge_grad<VEC, GL, NCH>), dim3((unsigned)blocks), dim3(256), 0, st,
+    hipLaunchKernelGGL((k_gat_edge_grad<VEC, GL, NCH, U>), dim3((unsigned)blocks), dim3(256), 0, st,
                        n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu, slope, dO, dpre,
                        g2);
     return hipGetLastError();
@@ -2027,8 +2092,9 @@ hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
         return hipSuccess;
     if (d < 1 || d > kGatMaxWidth)
         return hipErrorInvalidValue;
-    // vectors of 4/2/1 floats as width and alignment allow; a group wide
-    // enough for the row, at most a wave; up to 8 vectors per lane
+    // vectors of 4/2/1 floats as width and alignment allow; groups of at
+    // most 16 lanes (at least four entries per wave step) up to 128 vectors
+    // per row, whole-wave groups beyond; up to 8 vectors per lane
     int vec = 1;
     auto al = [](const void *q, uintptr_t n) { return ((uintptr_t)q % n) == 0; };
     if (d % 4 == 0 && al(z, 16) && al(h_out, 16) && al(dh_out, 16) && al(dO, 16))
@@ -2036,7 +2102,7 @@ hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
     else if (d % 2 == 0 && al(z, 8) && al(h_out, 8) && al(dh_out, 8) && al(dO, 8))
         vec = 2;
     const int dv = d / vec;
-    const int gl = dv <= 4 ? 4 : (dv <= 8 ? 8 : (dv <= 16 ? 16 : (dv <= 32 ? 32 : 64)));
+    const int gl = dv <= 4 ? 4 : (dv <= 8 ? 8 : (dv <= 128 ? 16 : 64));
     const int nch = (dv + gl - 1) / gl;
 #define DIGEST_GEG(V, L, C)                                                                     \
     return gat_edge_grad_t<V, L, C>(n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu,    \
@@ -2045,10 +2111,12 @@ hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
     do {                                                                                        \
         if (gl == 4) DIGEST_GEG(V, 4, 1);                                                       \
         if (gl == 8) DIGEST_GEG(V, 8, 1);                                                       \
-        if (gl == 16) DIGEST_GEG(V, 16, 1);                                                     \
-        if (gl == 32) DIGEST_GEG(V, 32, 1);                                                     \
-        if (nch <= 1) DIGEST_GEG(V, 64, 1);                                                     \
-        if (nch <= 2) DIGEST_GEG(V, 64, 2);                                                     \
+        if (gl == 16) {                                                                         \
+            if (nch <= 1) DIGEST_GEG(V, 16, 1);                                                 \
+            if (nch <= 2) DIGEST_GEG(V, 16, 2);                                                 \
+            if (nch <= 4) DIGEST_GEG(V, 16, 4);                                                 \
+            DIGEST_GEG(V, 16, 8);                                                               \
+        }                                                                                       \
         if (nch <= 4) DIGEST_GEG(V, 64, 4);                                                     \
         DIGEST_GEG(V, 64, 8);                                                                   \
     } while (0)

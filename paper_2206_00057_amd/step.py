@@ -1,5 +1,6 @@
 """One DIGEST training round of one partition on the GPU, as a sequence of
-library calls (Algorithm 1's inner loop for a single subgraph):
+library calls (Algorithm 1's inner loop for a single subgraph), for the GCN
+layer of Eq. 5 or the GAT layer over stale halo rows:
 
     for l = 1..L:   pull level l-1 if the schedule says so (levels >= 1),
                     layer forward, push level l if the schedule says so
@@ -27,7 +28,15 @@ from . import digest as D
 
 
 class GpuPartition:
-    def __init__(self, n_global, part, widths, device="cuda", overlap_io=False):
+    def __init__(self, n_global, part, widths, device="cuda", overlap_io=False, model="gcn",
+                 atts=None):
+        """model "gcn" (Eq. 5) or "gat" (the attention layer over stale halo
+        rows; atts are its per-layer [d_l, 2] attention matrices)."""
+        if model not in ("gcn", "gat"):
+            raise ValueError("model is gcn or gat")
+        if model == "gat" and (atts is None or len(atts) != len(widths) - 1):
+            raise ValueError("a GAT model needs one attention matrix per layer")
+        self.model, self.atts = model, atts
         self.widths = [int(w) for w in widths]
         self.L = len(self.widths) - 1
         self.device = device
@@ -38,12 +47,18 @@ class GpuPartition:
         self.workspace = torch.empty(max(self.p.workspace_bytes, 256), dtype=torch.uint8,
                                      device=device)
         D.digest_partition_bind_workspace(self.p, self.workspace)
+        if model == "gat":
+            self.gat_workspace = torch.empty(max(D.digest_gat_query(self.p), 256),
+                                             dtype=torch.uint8, device=device)
+            D.digest_gat_bind_workspace(self.p, self.gat_workspace)
         f32 = dict(dtype=torch.float32, device=device)
         # H[l]: output of layer l (H[0] is the caller's input rows); dH[l] its gradient
         self.H = [None] + [torch.empty(n, self.widths[l], **f32) for l in range(1, self.L + 1)]
         self.dH = [None] + [torch.empty(n, self.widths[l], **f32) for l in range(1, self.L + 1)]
         self.dW = [None] + [torch.empty(self.widths[l - 1], self.widths[l], **f32)
                             for l in range(1, self.L + 1)]
+        self.dAtt = ([None] + [torch.empty(self.widths[l], 2, **f32) for l in range(1, self.L + 1)]
+                     if model == "gat" else None)
         self.loss = torch.zeros(1, **f32)
         self.graphs = {}
         # pulls and pushes: on their own stream (default priority) next to the
@@ -54,6 +69,13 @@ class GpuPartition:
 
     def act(self, layer):
         return D.ACT_RELU if layer < self.L else D.ACT_IDENTITY
+
+    def _layer(self, l, h, W, stream=None):
+        if self.model == "gat":
+            D.digest_gat_forward(self.p, l, h, W, self.atts[l - 1], self.H[l], self.act(l),
+                                 stream=stream)
+        else:
+            D.digest_layer_forward(self.p, l, h, W, self.H[l], self.act(l), stream=stream)
 
     def pull_all(self, stores):
         """Initial pull of every level (level 0 = features)."""
@@ -77,7 +99,7 @@ class GpuPartition:
         for l in range(1, self.L + 1):
             if pulled and l >= 2:
                 main.wait_event(self.pull_done[l - 1])
-            D.digest_layer_forward(self.p, l, h, Ws[l - 1], self.H[l], self.act(l))
+            self._layer(l, h, Ws[l - 1])
             if do_push and l <= self.L - 1:
                 self.io.wait_stream(main)
                 with torch.cuda.stream(self.io):
@@ -92,7 +114,7 @@ class GpuPartition:
         for l in range(1, self.L + 1):
             if do_pull and l >= 2:
                 D.digest_pull(self.p, l - 1, stores[l - 1])
-            D.digest_layer_forward(self.p, l, h, Ws[l - 1], self.H[l], self.act(l))
+            self._layer(l, h, Ws[l - 1])
             if do_push and l <= self.L - 1:
                 D.digest_push(self.p, l, self.H[l], stores[l])
             h = self.H[l]
@@ -103,8 +125,12 @@ class GpuPartition:
         for l in range(self.L, 0, -1):
             dh_in = self.dH[l - 1] if l > 1 else None
             h_in = self.H[l - 1] if l > 1 else self.x_own
-            D.digest_layer_backward(self.p, l, h_in, self.H[l], self.dH[l], Ws[l - 1], self.dW[l],
-                                    dh_in)
+            if self.model == "gat":
+                D.digest_gat_backward(self.p, l, h_in, self.H[l], self.dH[l], Ws[l - 1],
+                                      self.atts[l - 1], self.dW[l], self.dAtt[l], dh_in)
+            else:
+                D.digest_layer_backward(self.p, l, h_in, self.H[l], self.dH[l], Ws[l - 1],
+                                        self.dW[l], dh_in)
 
     def round(self, r, K, x_own, Ws, stores, labels):
         """Round r (1-based) with sync interval K, eagerly."""

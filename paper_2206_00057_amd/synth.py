@@ -235,6 +235,14 @@ def weights(cfg: GraphConfig, seed: int = 3) -> list:
     return out
 
 
+def attentions(cfg: GraphConfig, seed: int = 5) -> list:
+    """GAT attention matrices, one [d_l, 2] per layer (source and target
+    columns), Glorot-normal: the GAT model's initialisation scale."""
+    rng = np.random.default_rng(seed)
+    return [(rng.standard_normal((d, 2)) * np.sqrt(2.0 / (d + 2))).astype(np.float32)
+            for d in cfg.widths[1:]]
+
+
 def labels(cfg: GraphConfig, seed: int = 4) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return rng.integers(0, cfg.classes, size=cfg.n).astype(np.int32)

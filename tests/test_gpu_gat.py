@@ -169,3 +169,45 @@ def test_gat_call_order_and_arguments_are_checked():
     assert L.digest_gat_backward(h.handle, 1, a, a, a, a, a, a, a, None, None) == D.ESTATE
     assert b"GAT forward" in L.digest_last_error()
     torch.cuda.synchronize()
+
+
+def test_gat_round_driver_matches_oracle_and_replays_bitwise():
+    """Two GAT layers through the round driver (pulls, layers, loss head,
+    backward), eagerly against the oracle, then replayed from HIP graphs
+    against the eager round bit for bit."""
+    from paper_2206_00057_amd import digest as D
+    from paper_2206_00057_amd import step
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=(24, 40, 6), classes=6)
+    g = synth.make_graph(cfg, seed=6)
+    part = synth.make_partition(cfg, g, 1)
+    X, Ws, atts = synth.features(cfg), synth.weights(cfg), synth.attentions(cfg)
+    y = synth.labels(cfg)[part.owned]
+    stores = [X, synth.relu_normal((g.n, cfg.widths[1]), seed=61)]
+    gp = step.GpuPartition(g.n, part, cfg.widths, model="gat", atts=[dev(a) for a in atts])
+    dstores = [dev(s) for s in stores]
+    gp.pull_all(dstores)
+    x_own, dWs, dy = dev(X[part.owned]), [dev(w) for w in Ws], dev(y)
+    gp.round(2, 2, x_own, dWs, dstores, dy)     # r = 2, K = 2: pull, no push
+    eager = [host(t).copy() for t in (gp.H[2], gp.dW[1], gp.dW[2], gp.dAtt[1], gp.dAtt[2])]
+
+    op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
+                                part.halo, cfg.widths)
+    op.pull(0, stores[0])
+    op.pull(1, stores[1])
+    h1 = op.gat_forward(1, X[part.owned], Ws[0], atts[0], oracle.RELU)
+    h2 = op.gat_forward(2, h1, Ws[1], atts[1], oracle.IDENTITY)
+    assert_close(eager[0], h2, "round logits", scale_tol=2e-5)
+    _, dl = oracle.softmax_xent(h2, y)
+    dw2, da2, dh1 = op.gat_backward(2, h1, Ws[1], atts[1], h2, dl, oracle.IDENTITY)
+    dw1, da1, _ = op.gat_backward(1, X[part.owned], Ws[0], atts[0], h1, dh1, oracle.RELU,
+                                  want_dh_in=False)
+    for got, ref, name in zip(eager[1:], (dw1, dw2, da1, da2), ("dW1", "dW2", "datt1", "datt2")):
+        assert_close(got, ref, f"round {name}")
+
+    gp.capture(2, x_own, dWs, dstores, dy)
+    for _ in range(3):
+        gp.replay(2, 2)
+        torch.cuda.synchronize()
+        _ = torch.ones(1000, device="cuda").sum().item()   # eager work between replays
+        for t, ref in zip((gp.H[2], gp.dW[1], gp.dW[2], gp.dAtt[1], gp.dAtt[2]), eager):
+            np.testing.assert_array_equal(host(t).view(np.uint32), ref.view(np.uint32))
