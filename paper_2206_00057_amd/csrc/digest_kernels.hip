@@ -1767,9 +1767,13 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         vec = pick_vec(d, out1, nullptr);
     const int dv = d / vec;
     const int gl = pick_group(dv);
-    if (ep && gl > 16)
+    // the row-per-lane-group kernel holds kNarrowBatch x GL x VEC gathered
+    // floats per lane: rows up to kNarrow floats; wider ones go to the
+    // row-per-wave kernel (with lane groups as narrow as the row)
+    const bool narrow = d <= kNarrow;
+    if (ep && !narrow)
         return hipErrorInvalidValue;
-    if (gl <= 16) {   // narrow rows: a row per lane group
+    if (narrow) {   // narrow rows: a row per lane group
         if (n_long < 0 || n_long > n_blocks)
             return hipErrorInvalidValue;
 #define DIGEST_NARROW(V, L)                                                                      \
