@@ -241,8 +241,10 @@ def train_bench(args):
     parts = [synth.make_partition(cfg, g, m) for m in range(M)]
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     X, y, Ws = synth.features(cfg), synth.labels(cfg), synth.weights(cfg)
+    gat = args.model == "gat"
+    atts = [dev(a) for a in synth.attentions(cfg)] if gat else None
     tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws],
-                       args.lr, K, grad_exchange=args.grad_exchange)
+                       args.lr, K, grad_exchange=args.grad_exchange, model=args.model, atts=atts)
     print(f"[bench] training {cfg.name}: {M} subgraphs, inputs {time.time() - t0:.1f}s",
           file=sys.stderr, flush=True)
     tr.init_stores()
@@ -259,12 +261,13 @@ def train_bench(args):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
     out = {
-        "metric": "DIGEST training GTEPS, all subgraphs of the graph on one GPU",
+        "metric": f"DIGEST {args.model.upper()} training GTEPS, all subgraphs of the graph on one GPU",
         "value": round(tr.edges_per_round * args.steps / (ms * 1e-3) / 1e9, 4), "unit": "GTEPS",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms / args.steps, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: all {M} subgraphs, Algorithm 1 rounds with "
+        "config": {"workload": f"{cfg.name}: all {M} subgraphs, {args.model.upper()}, "
+                               f"Algorithm 1 rounds with "
                                f"sync interval {K}, SGD lr {args.lr}, halo-gradient "
                                f"exchange {args.grad_exchange}",
                    "n_global": g.n, "subgraphs": M, "widths": list(cfg.widths),

@@ -421,11 +421,23 @@ class OracleTrainer:
     halo gradient P_out^T D W^T is added into a per-level gradient store and
     each owner adds its rows to its input gradient -- in the same round
     ("fresh") or one round later ("stale", the t-1 of the appendix).  With
-    "none" (reading A8) halo rows get no gradient."""
+    "none" (reading A8) halo rows get no gradient.
 
-    def __init__(self, n_global, parts, widths, X, labels, Ws, lr, K, grad_exchange="none"):
+    model="gat" runs the GAT layer over stale halo rows instead of Eq. 5;
+    AGG then averages the attention matrices ``atts`` as well as W."""
+
+    def __init__(self, n_global, parts, widths, X, labels, Ws, lr, K, grad_exchange="none",
+                 model="gcn", atts=None):
         if grad_exchange not in ("none", "fresh", "stale"):
             raise OracleError("grad_exchange is none, fresh or stale")
+        if model not in ("gcn", "gat"):
+            raise OracleError("model is gcn or gat")
+        if model == "gat" and (atts is None or len(atts) != len(widths) - 1):
+            raise OracleError("a GAT model needs one attention matrix per layer")
+        if model == "gat" and grad_exchange != "none":
+            raise OracleError("the halo-gradient exchange is defined for GCN layers")
+        self.model = model
+        self.att = [_c(a, np.float32).copy() for a in atts] if model == "gat" else None
         self.widths = [int(x) for x in widths]
         self.L = len(self.widths) - 1
         self.lr, self.K = float(lr), int(K)
@@ -446,6 +458,11 @@ class OracleTrainer:
     def act(self, layer):
         return RELU if layer < self.L else IDENTITY
 
+    def _forward(self, op, l, h):
+        if self.model == "gat":
+            return op.gat_forward(l, h, self.W[l - 1], self.att[l - 1], self.act(l))
+        return op.forward(l, h, self.W[l - 1], self.act(l))
+
     def init_stores(self):
         """One forward of every subgraph at the current W, pulling before and
         pushing after every layer, then every halo level pulled."""
@@ -456,7 +473,7 @@ class OracleTrainer:
             if l >= 2:
                 for op in self.ops:
                     op.pull(l - 1, self.stores[l - 1])
-            h = [op.forward(l, h[m], self.W[l - 1], self.act(l)) for m, op in enumerate(self.ops)]
+            h = [self._forward(op, l, h[m]) for m, op in enumerate(self.ops)]
             for m, op in enumerate(self.ops):
                 self.stores[l] = op.push(l, h[m], self.stores[l])
         for op in self.ops:
@@ -473,11 +490,12 @@ class OracleTrainer:
                 for op in self.ops:
                     op.pull(l - 1, self.stores[l - 1])
             for m, op in enumerate(self.ops):
-                outs[m][l] = op.forward(l, outs[m][l - 1], self.W[l - 1], self.act(l))
+                outs[m][l] = self._forward(op, l, outs[m][l - 1])
             if do_push and l <= self.L - 1:
                 for m, op in enumerate(self.ops):
                     self.stores[l] = op.push(l, outs[m][l], self.stores[l])
         grads = [[None] * len(self.ops) for _ in range(self.L)]
+        agrads = [[None] * len(self.ops) for _ in range(self.L)]
         dh = [None] * len(self.ops)
         for m in range(len(self.ops)):
             self.logits[m] = outs[m][self.L]
@@ -485,9 +503,14 @@ class OracleTrainer:
         for l in range(self.L, 0, -1):
             dh_in = [None] * len(self.ops)
             for m, op in enumerate(self.ops):
-                grads[l - 1][m], dh_in[m] = op.backward(l, outs[m][l - 1], self.W[l - 1],
-                                                        outs[m][l], dh[m], self.act(l),
-                                                        want_dh_in=l > 1)
+                if self.model == "gat":
+                    grads[l - 1][m], agrads[l - 1][m], dh_in[m] = op.gat_backward(
+                        l, outs[m][l - 1], self.W[l - 1], self.att[l - 1], outs[m][l], dh[m],
+                        self.act(l), want_dh_in=l > 1)
+                else:
+                    grads[l - 1][m], dh_in[m] = op.backward(l, outs[m][l - 1], self.W[l - 1],
+                                                            outs[m][l], dh[m], self.act(l),
+                                                            want_dh_in=l > 1)
             if l > 1 and self.grad_exchange != "none":
                 hg = [op.halo_gradient(l, self.W[l - 1], outs[m][l], dh[m], self.act(l))
                       for m, op in enumerate(self.ops)]
@@ -504,5 +527,7 @@ class OracleTrainer:
                         push_add(gs, op.halo, hg[m])
             dh = dh_in
         self.W = [sgd_average(self.W[l], grads[l], self.lr) for l in range(self.L)]
+        if self.model == "gat":   # AGG of the attention parameters too
+            self.att = [sgd_average(self.att[l], agrads[l], self.lr) for l in range(self.L)]
         return float(np.mean(self.losses))
 

@@ -29,6 +29,9 @@ K = 1 the mean of the subgraphs' gradients is then the full-graph gradient)
 or one round later ("stale", the t-1 of the appendix).  "none" keeps halo
 rows as constants.
 
+model="gat" trains GAT layers over stale halo rows instead of Eq. 5; AGG
+then averages the attention matrices as well as W.
+
 All arithmetic runs in libdigest.so (the layers, pulls, pushes, loss heads
 and the parameter averaging); this module owns the buffers and orders the
 calls.  ``capture`` records one round per pull/push pattern into a HIP graph.
@@ -43,7 +46,7 @@ from .step import GpuPartition
 
 class DigestTrainer:
     def __init__(self, n_global, parts, widths, x, labels, weights, lr, K, device="cuda",
-                 grad_exchange="none"):
+                 grad_exchange="none", model="gcn", atts=None):
         """parts: synth-style partitions (owned, halo, CSR rows) covering the
         graph; x: device [n_global, d_0] features; labels: device int32
         [n_global]; weights: device float32 tensors W_1..W_L (the global
@@ -52,13 +55,18 @@ class DigestTrainer:
             raise ValueError("between 1 and 64 subgraphs")
         if grad_exchange not in ("none", "fresh", "stale"):
             raise ValueError("grad_exchange is none, fresh or stale")
+        if model == "gat" and grad_exchange != "none":
+            raise ValueError("the halo-gradient exchange is defined for GCN layers")
         self.grad_exchange = grad_exchange
+        self.model = model
+        self.att = atts   # GAT: device [d_l, 2] attention matrices, updated in place
         self.widths = [int(w) for w in widths]
         self.L = len(self.widths) - 1
         self.n_global = int(n_global)
         self.lr, self.K = float(lr), int(K)
         self.W = weights
-        self.gps = [GpuPartition(n_global, p, widths, device=device) for p in parts]
+        self.gps = [GpuPartition(n_global, p, widths, device=device, model=model, atts=atts)
+                    for p in parts]
         idx = [torch.from_numpy(p.owned).to(device) for p in parts]
         self.x_own = [x.index_select(0, i).contiguous() for i in idx]
         self.y_own = [labels.index_select(0, i).contiguous() for i in idx]
@@ -74,11 +82,22 @@ class DigestTrainer:
             self.dh_halo = [[None] + [torch.empty(p.n_halo, self.widths[l], **f32)
                                       for l in range(1, self.L)] for p in parts]
         self.graphs = {}
-        self.edges_per_round = sum(gp.p.nnz + (gp.p.nnz_in if l > 1 else 0)
-                                   for gp in self.gps for l in range(1, self.L + 1))
+        # aggregation entries per round: GCN forward nnz and backward nnz_in
+        # (layers >= 2); GAT forward and transposed backward nnz per layer
+        if model == "gat":
+            self.edges_per_round = sum(2 * gp.p.nnz * self.L for gp in self.gps)
+        else:
+            self.edges_per_round = sum(gp.p.nnz + (gp.p.nnz_in if l > 1 else 0)
+                                       for gp in self.gps for l in range(1, self.L + 1))
 
     def act(self, layer):
         return D.ACT_RELU if layer < self.L else D.ACT_IDENTITY
+
+    def _fwd(self, gp, l, h):
+        if self.model == "gat":
+            D.digest_gat_forward(gp.p, l, h, self.W[l - 1], self.att[l - 1], gp.H[l], self.act(l))
+        else:
+            D.digest_layer_forward(gp.p, l, h, self.W[l - 1], gp.H[l], self.act(l))
 
     def init_stores(self):
         """Fill the store with one forward of all subgraphs at the current W
@@ -91,7 +110,7 @@ class DigestTrainer:
             for m, gp in enumerate(self.gps):
                 if l >= 2:
                     D.digest_pull(gp.p, l - 1, self.stores[l - 1])
-                D.digest_layer_forward(gp.p, l, h[m], self.W[l - 1], gp.H[l], self.act(l))
+                self._fwd(gp, l, h[m])
             for gp in self.gps:
                 D.digest_push(gp.p, l, gp.H[l], self.stores[l])
             h = [gp.H[l] for gp in self.gps]
@@ -106,7 +125,7 @@ class DigestTrainer:
                 for gp in self.gps:
                     D.digest_pull(gp.p, l - 1, self.stores[l - 1])
             for m, gp in enumerate(self.gps):
-                D.digest_layer_forward(gp.p, l, h[m], self.W[l - 1], gp.H[l], self.act(l))
+                self._fwd(gp, l, h[m])
             if do_push and l <= self.L - 1:
                 for gp in self.gps:
                     D.digest_push(gp.p, l, gp.H[l], self.stores[l])
@@ -119,7 +138,10 @@ class DigestTrainer:
             for m, gp in enumerate(self.gps):
                 dh_in = gp.dH[l - 1] if l > 1 else None
                 h_in = gp.H[l - 1] if l > 1 else self.x_own[m]
-                if exch and l > 1:
+                if self.model == "gat":
+                    D.digest_gat_backward(gp.p, l, h_in, gp.H[l], gp.dH[l], self.W[l - 1],
+                                          self.att[l - 1], gp.dW[l], gp.dAtt[l], dh_in)
+                elif exch and l > 1:
                     # the halo gradient comes out of the backward's own products
                     D.digest_layer_backward_halo(gp.p, l, h_in, gp.H[l], gp.dH[l],
                                                  self.W[l - 1], gp.dW[l], dh_in,
@@ -131,6 +153,8 @@ class DigestTrainer:
                 self._exchange(l)
         for l in range(1, self.L + 1):
             D.digest_sgd_average(self.W[l - 1], [gp.dW[l] for gp in self.gps], self.lr)
+            if self.model == "gat":
+                D.digest_sgd_average(self.att[l - 1], [gp.dAtt[l] for gp in self.gps], self.lr)
 
     def _exchange(self, l):
         """The halo gradients of layer l (from the backward) into the level

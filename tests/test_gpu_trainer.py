@@ -272,3 +272,32 @@ def test_layer_backward_halo_matches_oracle(widths, tf):
         assert_close(host(dw), ref_dw, f"dw {name}")
         assert_close(host(dh_in), ref_dh, f"dh_in {name}", scale_tol=2e-5)
         assert_close(host(dh_halo), ref_halo, f"dh_halo {name}", scale_tol=2e-5)
+
+
+@pytest.mark.parametrize("K", [1, 2])
+def test_gat_trainer_rounds_match_oracle(K):
+    """GAT layers in the multi-subgraph trainer: logits, loss, W, the
+    attention matrices (AGG averages both) and the stores round by round."""
+    from paper_2206_00057_amd.train import DigestTrainer
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 2000, widths=(64, 32, 16))
+    g = synth.make_graph(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(synth.num_partitions(cfg))]
+    X, y, Ws, atts = synth.features(cfg), synth.labels(cfg), synth.weights(cfg), \
+        synth.attentions(cfg)
+    tr = DigestTrainer(g.n, parts, cfg.widths, dev(X), dev(y), [dev(w) for w in Ws], 0.5, K,
+                       model="gat", atts=[dev(a) for a in atts])
+    ot = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, 0.5, K, model="gat", atts=atts)
+    tr.init_stores()
+    ot.init_stores()
+    for r in range(1, 2 * K + 2):
+        tr.round(r)
+        o_loss = ot.round(r)
+        for m, gp in enumerate(tr.gps):
+            assert_close(host(gp.H[cfg.layers]), ot.logits[m], f"GAT K={K} round {r} logits m={m}")
+        assert abs(tr.mean_loss() - o_loss) <= ATOL + RTOL * abs(o_loss)
+        for l in range(cfg.layers):
+            assert_close(host(tr.W[l]), ot.W[l], f"GAT K={K} round {r} W{l + 1}")
+            assert_close(host(tr.att[l]), ot.att[l], f"GAT K={K} round {r} att{l + 1}")
+        for lev in range(1, cfg.layers):
+            assert_close(host(tr.stores[lev]), ot.stores[lev], f"GAT K={K} round {r} store {lev}")
+

@@ -251,3 +251,89 @@ def test_stale_gradient_exchange_first_round_has_nothing_to_add():
     assert max(np.abs(runs["fresh"][0][l] - runs["none"][0][l]).max()
                for l in range(cfg.layers)) > 1e-6
 
+
+
+# --------------------------------------------------------------------------
+# GAT layers in the trainer
+# --------------------------------------------------------------------------
+
+def _torch_gat_full_sgd(g, X, y, Ws, atts, lr, rounds, slope=0.2):
+    """Full-graph GAT training by torch float64 autograd: dense masked
+    softmax attention, ReLU hidden / identity logits, mean cross entropy."""
+    import scipy.sparse as sp_
+    S = sp_.csr_matrix((np.ones_like(g.values, dtype=np.float64), g.indices, g.indptr),
+                       shape=(g.n, g.n)).toarray() > 0
+    mask = torch.from_numpy(S)
+    Xt = torch.tensor(X, dtype=torch.float64)
+    yt = torch.tensor(y, dtype=torch.int64)
+    Wt = [torch.tensor(w, dtype=torch.float64, requires_grad=True) for w in Ws]
+    At = [torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in atts]
+    traj = []
+    for _ in range(rounds):
+        h = Xt
+        for l, (W, a) in enumerate(zip(Wt, At)):
+            z = h @ W
+            e = torch.nn.functional.leaky_relu((z @ a[:, 1])[:, None] + (z @ a[:, 0])[None, :],
+                                               negative_slope=slope)
+            alpha = torch.softmax(e.masked_fill(~mask, float("-inf")), dim=1)
+            o = alpha @ z
+            h = torch.relu(o) if l < len(Wt) - 1 else o
+        loss = torch.nn.functional.cross_entropy(h, yt)
+        gW = torch.autograd.grad(loss, Wt + At)
+        with torch.no_grad():
+            Wt = [(W - lr * gw).requires_grad_(True) for W, gw in zip(Wt, gW[:len(Wt)])]
+            At = [(a - lr * ga).requires_grad_(True) for a, ga in zip(At, gW[len(Wt):])]
+        traj.append(([W.detach().numpy().copy() for W in Wt],
+                     [a.detach().numpy().copy() for a in At]))
+    return traj
+
+
+def test_gat_single_subgraph_trains_like_full_graph_gat():
+    cfg = cfg_small(widths=(6, 5, 3))
+    g = synth.make_graph(cfg, seed=11)
+    X, y, Ws, atts = synth.features(cfg), synth.labels(cfg), synth.weights(cfg), \
+        synth.attentions(cfg)
+    whole = synth.extract_partition(g, np.arange(g.n))
+    lr = 0.5
+    tr = oracle.OracleTrainer(g.n, [whole], cfg.widths, X, y, Ws, lr, K=1, model="gat",
+                              atts=atts)
+    tr.init_stores()
+    ref = _torch_gat_full_sgd(g, X, y, Ws, atts, lr, 3)
+    for r in (1, 2, 3):
+        tr.round(r)
+        for l in range(len(Ws)):
+            np.testing.assert_allclose(tr.W[l], ref[r - 1][0][l], rtol=1e-5, atol=1e-6)
+            np.testing.assert_allclose(tr.att[l], ref[r - 1][1][l], rtol=1e-5, atol=1e-6)
+
+
+def test_gat_sync_interval_one_gives_full_graph_logits():
+    cfg = cfg_small(widths=(6, 5, 3))
+    g = synth.make_graph(cfg, seed=12)
+    X, y, Ws, atts = synth.features(cfg), synth.labels(cfg), synth.weights(cfg), \
+        synth.attentions(cfg)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    tr = oracle.OracleTrainer(g.n, parts, cfg.widths, X, y, Ws, 0.5, K=1, model="gat",
+                              atts=atts)
+    full = oracle.OracleTrainer(g.n, [synth.extract_partition(g, np.arange(g.n))], cfg.widths,
+                                X, y, Ws, 0.5, K=1, model="gat", atts=atts)
+    tr.init_stores()
+    full.init_stores()
+    for r in (1, 2):
+        W_before = [w.copy() for w in tr.W]
+        A_before = [a.copy() for a in tr.att]
+        full.W, full.att = [w.copy() for w in W_before], [a.copy() for a in A_before]
+        full.round(r)
+        tr.round(r)
+        for m, p in enumerate(parts):
+            np.testing.assert_allclose(tr.logits[m], full.logits[0][p.owned], rtol=1e-5,
+                                       atol=1e-6)
+
+
+def test_gat_trainer_refuses_gradient_exchange():
+    cfg = cfg_small()
+    g = synth.make_graph(cfg, seed=13)
+    parts = [synth.make_partition(cfg, g, m) for m in range(cfg.blocks)]
+    with pytest.raises(oracle.OracleError):
+        oracle.OracleTrainer(g.n, parts, cfg.widths, synth.features(cfg), synth.labels(cfg),
+                             synth.weights(cfg), 0.5, K=1, model="gat",
+                             atts=synth.attentions(cfg), grad_exchange="fresh")
