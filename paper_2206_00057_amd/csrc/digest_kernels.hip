@@ -462,32 +462,39 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
             acc[v] = 0.f;
         constexpr int E = kNarrowBatch * GL;   // entries per batch
         for (int k0 = kb; k0 < ke; k0 += E) {
-            const int nb = min(E, ke - k0);
+            // Every load is unconditional so that all of a batch's gathers
+            // are in flight together: an entry past the row rereads the
+            // row's last entry with weight 0 (it adds nothing, and no other
+            // row's data can enter), a lane past the width rereads the row's
+            // first vector and stores nothing.
             int mc[kNarrowBatch];
             float mv[kNarrowBatch];
 #pragma unroll
             for (int j = 0; j < kNarrowBatch; ++j) {   // entry k0 + j*GL + gl
-                const bool ok = j * GL + gl < nb;
-                mc[j] = ok ? col[k0 + j * GL + gl] : 0;
-                mv[j] = ok ? val[k0 + j * GL + gl] : 0.f;
+                const int k = k0 + j * GL + gl;
+                const int kc = k < ke ? k : ke - 1;
+                mc[j] = col[kc];
+                mv[j] = val[kc] * (k < ke ? 1.f : 0.f);
             }
-            float x[kNarrowBatch][GL][VEC];
+            int cc[kNarrowBatch][GL];
             float aa[kNarrowBatch][GL];
 #pragma unroll
             for (int j = 0; j < kNarrowBatch; ++j)
 #pragma unroll
                 for (int u = 0; u < GL; ++u) {
-                    const int cc = __shfl(mc[j], g * GL + u);
+                    cc[j][u] = __shfl(mc[j], g * GL + u);
                     aa[j][u] = __shfl(mv[j], g * GL + u);
-                    const float *sp = (TWO && cc >= n_src0) ? src1 + (int64_t)(cc - n_src0) * d
-                                                            : src0 + (int64_t)cc * d;
-                    if (j * GL + u < nb && lane_ok) {
-                        load_vec<VEC>(sp + gl * VEC, x[j][u]);
-                    } else {
+                }
+            float x[kNarrowBatch][GL][VEC];
+            const int lv = (lane_ok ? gl : 0) * VEC;
 #pragma unroll
-                        for (int v = 0; v < VEC; ++v)
-                            x[j][u][v] = 0.f;
-                    }
+            for (int j = 0; j < kNarrowBatch; ++j)
+#pragma unroll
+                for (int u = 0; u < GL; ++u) {
+                    const int c = cc[j][u];
+                    const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * d
+                                                           : src0 + (int64_t)c * d;
+                    load_vec<VEC>(sp + lv, x[j][u]);
                 }
 #pragma unroll
             for (int j = 0; j < kNarrowBatch; ++j)
