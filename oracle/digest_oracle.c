@@ -409,11 +409,15 @@ static double *gat_transform(int64_t n_own, int64_t n_halo, const float *h_own,
 #pragma omp parallel for schedule(static)
     for (int64_t v = 0; v < R; ++v) {
         const float *x = v < n_own ? h_own + v * d_in : halo_buf + (v - n_own) * d_in;
-        for (int64_t o = 0; o < d_out; ++o) {
-            double acc = 0.0;
-            for (int64_t f = 0; f < d_in; ++f)
-                acc += (double)x[f] * (double)w[f * d_out + o];
-            z[v * d_out + o] = acc;
+        double *zv = z + v * d_out;
+        for (int64_t o = 0; o < d_out; ++o)
+            zv[o] = 0.0;
+        /* every z_v[o] sums over f in ascending order */
+        for (int64_t f = 0; f < d_in; ++f) {
+            double xf = (double)x[f];
+            const float *wf = w + f * d_out;
+            for (int64_t o = 0; o < d_out; ++o)
+                zv[o] += xf * (double)wf[o];
         }
     }
     return z;
@@ -520,10 +524,19 @@ void oracle_gat_forward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
  *   D_i     = dh_out_i * act'(h_out_i)        (mask h_out > 0 for ReLU)
  *   c_i     = D_i . o_i,  o_i = sum_k alpha_ik z_{col_k}
  *   dpre_ik = alpha_ik (D_i . z_{col_k} - c_i) * LeakyReLU'(t_i + s_{col_k})
- *   dz_{col_k} += alpha_ik D_i + dpre_ik att[:,0];   dz_i += dpre_ik att[:,1]
- *   datt[:,0] = sum dpre_ik z_{col_k};  datt[:,1] = sum dpre_ik z_i
+ *   dz_v    = sum over entries (i,k) with col_k = v of
+ *               (alpha_ik D_i + dpre_ik att[:,0])
+ *             + (v owned) (sum_k dpre_vk) att[:,1]
+ *   datt[:,0] = sum_v (sum over entries reading v of dpre) z_v
+ *   datt[:,1] = sum_i (sum_k dpre_ik) z_i
  *   dW = sum over local rows v of x_v^T dz_v;  dh_in_i = dz_i W^T (owned i)
  * att and datt are [d_out][2]; dh_in may be NULL.
+ *
+ * Every sum has one fixed order, whatever the thread count: the entries
+ * that feed a column in ascending (row, entry) order, rows and columns in
+ * ascending order.  Threads split independent rows (first pass), columns
+ * (the scatter: each thread scans every entry and applies those whose
+ * column it owns) and feature blocks of dW.
  */
 void oracle_gat_backward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
                          const int32_t *col_local, const float *h_own, const float *halo_buf,
@@ -532,68 +545,136 @@ void oracle_gat_backward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
                          float *dw, float *datt, float *dh_in)
 {
     int64_t R = n_own + n_halo;
+    int64_t nnz = n_own > 0 ? indptr[n_own] - indptr[0] : 0;
+    int64_t e0 = n_own > 0 ? indptr[0] : 0;
+    size_t one = 1;
     double *z = gat_transform(n_own, n_halo, h_own, halo_buf, d_in, d_out, w);
     double *s = (double *)malloc(sizeof(double) * (size_t)(R > 0 ? R : 1));
     double *t = (double *)malloc(sizeof(double) * (size_t)(n_own > 0 ? n_own : 1));
     gat_scores(n_own, R, d_out, z, att, s, t);
-    double *dz = (double *)calloc((size_t)(R * d_out > 0 ? R * d_out : 1), sizeof(double));
-    double *da = (double *)calloc((size_t)(2 * d_out > 0 ? 2 * d_out : 1), sizeof(double));
-    int64_t maxrow = 1;
-    for (int64_t i = 0; i < n_own; ++i)
-        if (indptr[i + 1] - indptr[i] > maxrow)
-            maxrow = indptr[i + 1] - indptr[i];
-    double *a = (double *)malloc(sizeof(double) * (size_t)maxrow);
-    double *D = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
-    double *o = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
-    /* rows in ascending order, entries in CSR order: a fixed summation order */
-    for (int64_t i = 0; i < n_own; ++i) {
-        int64_t kb = indptr[i], ke = indptr[i + 1];
-        gat_row_alpha(i, indptr, col_local, s, t, slope, a);
-        for (int64_t q = 0; q < d_out; ++q) {
-            double g = (double)dh_out[i * d_out + q];
-            if (act == ORACLE_RELU && !(h_out[i * d_out + q] > 0.0f))
-                g = 0.0;
-            D[q] = g;
-            o[q] = 0.0;
-        }
-        for (int64_t k = kb; k < ke; ++k) {
-            const double *zc = z + (int64_t)col_local[k] * d_out;
-            for (int64_t q = 0; q < d_out; ++q)
-                o[q] += a[k - kb] * zc[q];
-        }
-        double c = 0.0;
-        for (int64_t q = 0; q < d_out; ++q)
-            c += D[q] * o[q];
-        for (int64_t k = kb; k < ke; ++k) {
-            int64_t col = col_local[k];
-            const double *zc = z + col * d_out;
-            double dalpha = 0.0;
-            for (int64_t q = 0; q < d_out; ++q)
-                dalpha += D[q] * zc[q];
-            double pre = t[i] + s[col];
-            double dpre = a[k - kb] * (dalpha - c) * (pre > 0.0 ? 1.0 : slope);
-            double *dzc = dz + col * d_out, *dzi = dz + i * d_out;
+    double *D = (double *)malloc(sizeof(double) * (size_t)(n_own * d_out > 0 ? n_own * d_out : 1));
+    double *alpha = (double *)malloc(sizeof(double) * (nnz > 0 ? (size_t)nnz : one));
+    double *dpre = (double *)malloc(sizeof(double) * (nnz > 0 ? (size_t)nnz : one));
+    double *rsum = (double *)malloc(sizeof(double) * (size_t)(n_own > 0 ? n_own : 1));
+
+    /* First pass, owned rows independently: D_i, the row's weights, o_i,
+       c_i and every dpre_ik, and their sum over the row. */
+#pragma omp parallel
+    {
+        double *o = (double *)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n_own; ++i) {
+            int64_t kb = indptr[i], ke = indptr[i + 1];
+            double *a = alpha + (kb - e0);
+            double *Di = D + i * d_out;
+            gat_row_alpha(i, indptr, col_local, s, t, slope, a);
             for (int64_t q = 0; q < d_out; ++q) {
-                dzc[q] += a[k - kb] * D[q] + dpre * (double)att[2 * q];
-                dzi[q] += dpre * (double)att[2 * q + 1];
-                da[2 * q] += dpre * zc[q];
-                da[2 * q + 1] += dpre * z[i * d_out + q];
+                double g = (double)dh_out[i * d_out + q];
+                if (act == ORACLE_RELU && !(h_out[i * d_out + q] > 0.0f))
+                    g = 0.0;
+                Di[q] = g;
+                o[q] = 0.0;
+            }
+            for (int64_t k = kb; k < ke; ++k) {
+                const double *zc = z + (int64_t)col_local[k] * d_out;
+                for (int64_t q = 0; q < d_out; ++q)
+                    o[q] += a[k - kb] * zc[q];
+            }
+            double c = 0.0;
+            for (int64_t q = 0; q < d_out; ++q)
+                c += Di[q] * o[q];
+            double rs = 0.0;
+            for (int64_t k = kb; k < ke; ++k) {
+                int64_t col = col_local[k];
+                const double *zc = z + col * d_out;
+                double dalpha = 0.0;
+                for (int64_t q = 0; q < d_out; ++q)
+                    dalpha += Di[q] * zc[q];
+                double pre = t[i] + s[col];
+                double dp = a[k - kb] * (dalpha - c) * (pre > 0.0 ? 1.0 : slope);
+                dpre[k - e0] = dp;
+                rs += dp;
+            }
+            rsum[i] = rs;
+        }
+        free(o);
+    }
+
+    /* Scatter into the columns: the thread that owns a column (blocks of
+       64 columns dealt round robin) applies its entries in (row, entry)
+       order. */
+    double *dz = (double *)calloc((size_t)(R * d_out > 0 ? R * d_out : 1), sizeof(double));
+    double *csum = (double *)calloc((size_t)(R > 0 ? R : 1), sizeof(double));
+#pragma omp parallel
+    {
+        int64_t nt = 1, me = 0;
+#ifdef _OPENMP
+        nt = omp_get_num_threads();
+        me = omp_get_thread_num();
+#endif
+        for (int64_t i = 0; i < n_own; ++i) {
+            const double *Di = D + i * d_out;
+            for (int64_t k = indptr[i]; k < indptr[i + 1]; ++k) {
+                int64_t col = col_local[k];
+                if ((col / 64) % nt != me)
+                    continue;
+                double a = alpha[k - e0], dp = dpre[k - e0];
+                double *dzc = dz + col * d_out;
+                for (int64_t q = 0; q < d_out; ++q)
+                    dzc[q] += a * Di[q] + dp * (double)att[2 * q];
+                csum[col] += dp;
             }
         }
     }
+    for (int64_t i = 0; i < n_own; ++i)
+        for (int64_t q = 0; q < d_out; ++q)
+            dz[i * d_out + q] += rsum[i] * (double)att[2 * q + 1];
+
+    double *da = (double *)calloc((size_t)(2 * d_out > 0 ? 2 * d_out : 1), sizeof(double));
+    for (int64_t v = 0; v < R; ++v)
+        for (int64_t q = 0; q < d_out; ++q) {
+            da[2 * q] += csum[v] * z[v * d_out + q];
+            if (v < n_own)
+                da[2 * q + 1] += rsum[v] * z[v * d_out + q];
+        }
     for (int64_t e = 0; e < 2 * d_out; ++e)
         datt[e] = (float)da[e];
-    /* dW[f][q] = sum over local rows v of x_v[f] dz_v[q] */
-#pragma omp parallel for schedule(static)
-    for (int64_t f = 0; f < d_in; ++f)
-        for (int64_t q = 0; q < d_out; ++q) {
-            double acc = 0.0;
-            for (int64_t v = 0; v < R; ++v) {
-                const float *x = v < n_own ? h_own + v * d_in : halo_buf + (v - n_own) * d_in;
-                acc += (double)x[f] * dz[v * d_out + q];
+
+    /* dW[f][q] = sum over local rows v (ascending) of x_v[f] dz_v[q], a block
+       of features per task so that dz streams once per block. */
+    {
+        int64_t nt = 1;
+#ifdef _OPENMP
+        nt = omp_get_max_threads();
+#endif
+        int64_t fb = d_in / (2 * nt);
+        fb = fb < 1 ? 1 : (fb > 16 ? 16 : fb);
+        int64_t nblk = (d_in + fb - 1) / fb;
+#pragma omp parallel
+        {
+            double *acc = (double *)malloc(sizeof(double) * (size_t)(fb * d_out > 0 ? fb * d_out : 1));
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t b = 0; b < nblk; ++b) {
+                int64_t f0 = b * fb, fn = d_in - f0 < fb ? d_in - f0 : fb;
+                for (int64_t e = 0; e < fn * d_out; ++e)
+                    acc[e] = 0.0;
+                for (int64_t v = 0; v < R; ++v) {
+                    const float *x = v < n_own ? h_own + v * d_in : halo_buf + (v - n_own) * d_in;
+                    const double *dzv = dz + v * d_out;
+                    for (int64_t j = 0; j < fn; ++j) {
+                        double xf = (double)x[f0 + j];
+                        double *aj = acc + j * d_out;
+                        for (int64_t q = 0; q < d_out; ++q)
+                            aj[q] += xf * dzv[q];
+                    }
+                }
+                for (int64_t j = 0; j < fn; ++j)
+                    for (int64_t q = 0; q < d_out; ++q)
+                        dw[(f0 + j) * d_out + q] = (float)acc[j * d_out + q];
             }
-            dw[f * d_out + q] = (float)acc;
+            free(acc);
         }
+    }
     if (dh_in) {
 #pragma omp parallel for schedule(static)
         for (int64_t i = 0; i < n_own; ++i)
@@ -604,11 +685,13 @@ void oracle_gat_backward(int64_t n_own, int64_t n_halo, const int64_t *indptr,
                 dh_in[i * d_in + f] = (float)acc;
             }
     }
-    free(o);
-    free(D);
-    free(a);
     free(da);
+    free(csum);
     free(dz);
+    free(rsum);
+    free(dpre);
+    free(alpha);
+    free(D);
     free(t);
     free(s);
     free(z);

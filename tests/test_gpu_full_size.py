@@ -3,7 +3,9 @@ and OGB-Products-shaped synthetic graphs, and the halo-dominated permutation
 partition), in the same library calls the benchmark times: pull and push
 contents bit-exact; every layer's forward and backward and the loss head
 within rtol 1e-4 / atol 1e-5 plus the scale-aware bound, over all outputs
-(the oracle finishes these in seconds with its threads)."""
+(the oracle finishes these in seconds with its threads); and the GAT layer
+over stale halo rows on the three workloads the GAT benchmark times, every
+layer's forward and backward over all outputs."""
 import time
 
 import numpy as np
@@ -11,6 +13,8 @@ import pytest
 
 from paper_2206_00057_amd import synth
 from test_gpu_parity import Case, check_layer, check_loss, check_pull, check_push, torch
+import test_gpu_gat
+import oracle
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -55,5 +59,29 @@ def test_full_size_workload(name):
         print(f"[{name}] layer {layer} fwd+bwd ok {time.time() - t:.1f}s", flush=True)
     check_loss(c)
     print(f"[{name}] loss ok", flush=True)
+    del c
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["medium", "dense", "large"])
+def test_full_size_gat_workload(name):
+    """Every GAT layer of the workload, on the partition the benchmark times:
+    each level pulled from a seeded store, then the layer's forward and
+    backward (dW, datt, dH_in) on both sides, the inputs on the dyadic grid
+    that makes every LeakyReLU branch decision exact."""
+    cfg = synth.CONFIGS[name]
+    g = graph_for(cfg)
+    part = synth.make_partition(cfg, g, 0)
+    c = test_gpu_gat.Case(g.n, part, cfg.widths, seed=5)
+    L = len(cfg.widths) - 1
+    print(f"[{name} gat] {synth.shape_stats(cfg, g, part)}", flush=True)
+    for layer in range(1, L + 1):
+        t = time.time()
+        store = synth.relu_normal((g.n, cfg.widths[layer - 1]), seed=70 + layer)
+        c.pull(layer - 1, test_gpu_gat.dyadic(store, test_gpu_gat.X_BITS))
+        act = oracle.RELU if layer < L else oracle.IDENTITY
+        c.layer(layer, act, f"{name} gat layer {layer}", grid=True)
+        print(f"[{name} gat] layer {layer} fwd+bwd ok {time.time() - t:.1f}s", flush=True)
     del c
     torch.cuda.empty_cache()

@@ -40,6 +40,40 @@ def assert_close(gpu, ref, name, scale_tol=1e-4):
     assert not (err > ATOL + RTOL * np.abs(r)).any(), f"{name}: max err {err.max():.3e}"
     peak = float(np.abs(r).max())
     assert peak == 0 or err.max() / peak <= scale_tol, f"{name}: scale err {err.max() / peak:.3e}"
+    return 0.0 if peak == 0 else float(err.max()) / peak
+
+
+# The derivative of LeakyReLU jumps at 0, so an edge whose score sum
+# t_i + s_j lies within float32 rounding of 0 can take the other branch on
+# the GPU than in the float64 oracle (both are valid there).  On the large
+# workloads such edges exist (an OGB-Products-shaped layer has ~10 of its
+# 15.6M edges within 1e-6 relative of 0), so those cases draw their inputs
+# on a dyadic grid: x in units of 2^-2, W of 2^-5, att of 2^-6.  Every
+# partial sum of z = x W, s = z att[:,0], t = z att[:,1] and t + s is then a
+# multiple of one unit below 2^24 units, exact in float32 in any order, and
+# both sides take every branch on the same exact value.
+X_BITS, W_BITS, ATT_BITS = 2, 5, 6
+
+
+def dyadic(a, bits):
+    """a rounded to the nearest multiple of 2^-bits, as float32."""
+    return (np.round(np.asarray(a, np.float64) * 2.0 ** bits) / 2.0 ** bits).astype(np.float32)
+
+
+def scores_exact(x_own, halo, W, att, chunk=1 << 17):
+    """True when the bound above holds for these grid inputs: the sums of
+    absolute values (which bound every partial sum) stay below 2^24 units."""
+    zu = 2.0 ** -(X_BITS + W_BITS)
+    su = 2.0 ** -(X_BITS + W_BITS + ATT_BITS)
+    Wd, ad = W.astype(np.float64), np.abs(att.astype(np.float64))
+    for x in (x_own, halo):
+        for r in range(0, x.shape[0], chunk):
+            xb = x[r:r + chunk].astype(np.float64)
+            if (np.abs(xb) @ np.abs(Wd)).max(initial=0) >= 2.0 ** 24 * zu:
+                return False
+            if 2 * (np.abs(xb @ Wd) @ ad).max(initial=0) >= 2.0 ** 24 * su:
+                return False
+    return True
 
 
 class Case:
@@ -65,8 +99,10 @@ class Case:
         self.D.digest_pull(self.h, level, dev(store))
         self.op.pull(level, store)
 
-    def layer(self, layer, act, label):
-        """Forward and backward of one GAT layer on both sides, compared."""
+    def layer(self, layer, act, label, grid=False):
+        """Forward and backward of one GAT layer on both sides, compared.
+        grid: inputs on the dyadic grid (the level's pulled store must be on
+        it too), so that every LeakyReLU branch is decided on exact values."""
         D, p = self.D, self.p
         di, do = self.widths[layer - 1], self.widths[layer]
         s = self.seed + 10 * layer
@@ -76,10 +112,17 @@ class Case:
         # vectors; much larger vectors make the softmax ill-conditioned (score
         # rounding times alpha_a alpha_b |z_a - z_b| at near ties)
         att = synth.normal((do, 2), seed=s + 3, scale=float(np.sqrt(2.0 / (do + 2))))
+        if grid:
+            h_in, W, att = dyadic(h_in, X_BITS), dyadic(W, W_BITS), dyadic(att, ATT_BITS)
+            halo = self.op.halo_buf.get(layer - 1)
+            halo = np.zeros((0, di), np.float32) if halo is None else halo
+            assert np.array_equal(halo, dyadic(halo, X_BITS)), "halo rows off the grid"
+            assert scores_exact(h_in, halo, W, att), "grid inputs too large for exact scores"
         out = torch.empty(p.n_own, do, device="cuda")
         D.digest_gat_forward(self.h, layer, dev(h_in), dev(W), dev(att), out, act)
         ref = self.op.gat_forward(layer, h_in, W, att, act)
-        assert_close(host(out), ref, f"{label} h_out", scale_tol=2e-5)
+        st = {"h_out": 2e-5, "dw": 1e-4, "datt": 1e-4, "dh_in": 2e-5}
+        errs = {"h_out": assert_close(host(out), ref, f"{label} h_out", scale_tol=st["h_out"])}
         dh = synth.normal((p.n_own, do), seed=s + 4, scale=1.0 / max(p.n_own, 1))
         dw = torch.empty(di, do, device="cuda")
         datt = torch.empty(do, 2, device="cuda")
@@ -88,9 +131,11 @@ class Case:
                               dw, datt, dh_in)
         rdw, rdatt, rdh = self.op.gat_backward(layer, h_in, W, att, ref, dh, act,
                                                want_dh_in=True)
-        assert_close(host(dw), rdw, f"{label} dw")
-        assert_close(host(datt), rdatt, f"{label} datt")
-        assert_close(host(dh_in), rdh, f"{label} dh_in", scale_tol=2e-5)
+        errs["dw"] = assert_close(host(dw), rdw, f"{label} dw", scale_tol=st["dw"])
+        errs["datt"] = assert_close(host(datt), rdatt, f"{label} datt", scale_tol=st["datt"])
+        errs["dh_in"] = assert_close(host(dh_in), rdh, f"{label} dh_in", scale_tol=st["dh_in"])
+        print(f"[{label}] scale errors " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()),
+              flush=True)
         return out, dw, datt, dh_in
 
 
