@@ -744,9 +744,10 @@ void oracle_halo_gradient(int64_t n_own, int64_t n_halo, const int64_t *indptr,
                           const float *dh_out, int act, float *dh_halo)
 {
     double *acc = (double *)calloc((size_t)(n_halo * d_in > 0 ? n_halo * d_in : 1), sizeof(double));
-    double *g = (double *)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
-    for (int64_t i = 0; i < n_own; ++i) {
-        /* G[i] = D[i] W^T */
+    double *G = (double *)malloc(sizeof(double) * (size_t)(n_own * d_in > 0 ? n_own * d_in : 1));
+    /* G[i] = D[i] W^T, rows independent */
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n_own; ++i)
         for (int64_t f = 0; f < d_in; ++f) {
             double s = 0.0;
             for (int64_t o = 0; o < d_out; ++o) {
@@ -755,8 +756,11 @@ void oracle_halo_gradient(int64_t n_own, int64_t n_halo, const int64_t *indptr,
                     dz = 0.0;
                 s += dz * (double)w[f * d_out + o];
             }
-            g[f] = s;
+            G[i * d_in + f] = s;
         }
+    /* scatter into the halo rows, owned rows in ascending order */
+    for (int64_t i = 0; i < n_own; ++i) {
+        const double *g = G + i * d_in;
         for (int64_t k = indptr[i]; k < indptr[i + 1]; ++k) {
             int64_t c = col_local[k];
             if (c < n_own)
@@ -768,7 +772,7 @@ void oracle_halo_gradient(int64_t n_own, int64_t n_halo, const int64_t *indptr,
     }
     for (int64_t e = 0; e < n_halo * d_in; ++e)
         dh_halo[e] = (float)acc[e];
-    free(g);
+    free(G);
     free(acc);
 }
 

@@ -1,8 +1,9 @@
 """GPU parity at the full sizes of the four large workloads (Flickr-, Reddit-
 and OGB-Products-shaped synthetic graphs, and the halo-dominated permutation
 partition), in the same library calls the benchmark times: pull and push
-contents bit-exact; every layer's forward and backward and the loss head
-within rtol 1e-4 / atol 1e-5 plus the scale-aware bound, over all outputs
+contents bit-exact; every layer's forward and backward, the fused backward
+with the halo gradient, and the loss head within rtol 1e-4 / atol 1e-5 plus
+the scale-aware bound, over all outputs
 (the oracle finishes these in seconds with its threads); and the GAT layer
 over stale halo rows on the three workloads the GAT benchmark times, every
 layer's forward and backward over all outputs."""
@@ -12,13 +13,39 @@ import numpy as np
 import pytest
 
 from paper_2206_00057_amd import synth
-from test_gpu_parity import Case, check_layer, check_loss, check_pull, check_push, torch
+from test_gpu_parity import (Case, assert_close, check_layer, check_loss, check_pull, check_push,
+                             dev, host, torch)
 import test_gpu_gat
 import oracle
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 _graphs = {}
+
+
+def check_backward_halo(c, layer):
+    """The trainer's fused backward of a layer above the first, with the
+    halo gradient P_out^T D W^T (Appendix A.3's stale-gradient term): dW,
+    dH_in and dH_halo against the oracle."""
+    from paper_2206_00057_amd import digest as Dm
+    h_in = c.layer_input(layer)
+    W = synth.weights(c.cfg)[layer - 1]
+    act = c.act(layer)
+    d_in, d_out = c.widths[layer - 1], c.widths[layer]
+    out = torch.empty(c.n, d_out, device="cuda")
+    Dm.digest_layer_forward(c.h, layer, dev(h_in), dev(W), out, act)
+    ref_out = c.op.forward(layer, h_in, W, act)
+    dh = c.upstream(layer)
+    dw = torch.empty(d_in, d_out, device="cuda")
+    dh_in = torch.empty(c.n, d_in, device="cuda")
+    dh_halo = torch.full((c.part.n_halo, d_in), float("nan"), device="cuda")
+    Dm.digest_layer_backward_halo(c.h, layer, dev(h_in), dev(ref_out), dev(dh), dev(W), dw,
+                                  dh_in, dh_halo)
+    ref_dw, ref_dh = c.op.backward(layer, h_in, W, ref_out, dh, act)
+    ref_halo = c.op.halo_gradient(layer, W, ref_out, dh, act)
+    assert_close(host(dw), ref_dw, f"{c.label} fused dW layer {layer}")
+    assert_close(host(dh_in), ref_dh, f"{c.label} fused dH_in layer {layer}")
+    assert_close(host(dh_halo), ref_halo, f"{c.label} dH_halo layer {layer}")
 
 
 def graph_for(cfg):
@@ -57,6 +84,10 @@ def test_full_size_workload(name):
         t = time.time()
         check_layer(c, layer)
         print(f"[{name}] layer {layer} fwd+bwd ok {time.time() - t:.1f}s", flush=True)
+        if layer > 1 and c.part.n_halo:
+            t = time.time()
+            check_backward_halo(c, layer)   # level layer-1 as check_layer pulled it
+            print(f"[{name}] layer {layer} halo gradient ok {time.time() - t:.1f}s", flush=True)
     check_loss(c)
     print(f"[{name}] loss ok", flush=True)
     del c
