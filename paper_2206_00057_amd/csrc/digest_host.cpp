@@ -1452,7 +1452,9 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
         // dO, the per-edge score gradients and their row sums (g2[i][1])
         Timed t(p, K_GAT_EDGE_GRAD, layer, s);
         if (digest_status st = hip_check(
-                digest::launch_gat_edge_grad(p->n_own, d_out, p->at<int32_t>(p->lay.rowptr),
+                digest::launch_gat_edge_grad(p->at<SpmmBlock>(p->lay.blocks_f),
+                                             (int32_t)p->blocks_f.size(), d_out,
+                                             p->at<int32_t>(p->lay.rowptr),
                                              p->at<int32_t>(p->lay.col), alpha, S, Z, h_out,
                                              dh_out, p->gat_act[layer] == DIGEST_ACT_RELU,
                                              p->gat_slope[layer], dO, dpre, g2, s),

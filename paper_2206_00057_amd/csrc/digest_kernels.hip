@@ -1350,32 +1350,53 @@ __global__ __launch_bounds__(256) void k_gat_softmax(int32_t n_rows,
     }
 }
 
-// Per-edge gradient of the GAT layer, one wave per owned row i:
+// Per-edge gradient of the GAT layer over the owned rows i:
 //   D_i     = dh_out_i * 1[h_out_i > 0] (relu) or dh_out_i    -> dO_i
 //   c_i     = D_i . h_out_i  (= D_i . o_i: the mask zeroes D where o <= 0)
 //   dpre[k] = alpha[k] (D_i . z_{col k} - c_i) * LeakyReLU'(t_i + s_{col k})
 //   g2[i][1] = sum_k dpre[k]
-// The wave's G = 64 / GL lane groups split the row's entries, U entries per
-// group in flight at once; inside a group GL lanes hold D_i as NCH vectors
-// of VEC features (every group the same) and gather the matching features
-// of z; the U dot products of a group go through one butterfly together.
-// All sums have a fixed order.  At most four waves per SIMD: left to
-// maximise occupancy the compiler reuses one register quad for every gather
-// and waits on each, which serialises the step.
+// Work follows the aggregation's block plan: a short-row block gives wave w
+// the row b.row + w; a long-row block splits the entries of row b.row into
+// kSpmmWaves contiguous parts, one per wave, and adds the waves' row sums
+// in LDS in wave order (so a row of thousands of entries is not one wave's
+// serial loop).  Inside a wave the G = 64 / GL lane groups split the
+// entries, U per group in flight at once; inside a group GL lanes hold D_i
+// as NCH vectors of VEC features and gather the matching features of z; the
+// U dot products of a group go through one butterfly together.  All sums
+// have a fixed order.  At most four waves per SIMD: left to maximise
+// occupancy the compiler reuses one register quad for every gather and
+// waits on each, which serialises the step.
 template <int VEC, int GL, int NCH, int U>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_gat_edge_grad(
-    int32_t n_own, int32_t d, const int32_t *__restrict__ rowptr,
-    const int32_t *__restrict__ col, const float *__restrict__ alpha,
-    const float *__restrict__ s, const float *__restrict__ z, const float *__restrict__ h_out,
-    const float *__restrict__ dh_out, bool relu, float slope, float *__restrict__ dO,
-    float *__restrict__ dpre, float *__restrict__ g2)
+__global__ __launch_bounds__(kSpmmThreads) __attribute__((amdgpu_waves_per_eu(1, 4))) void
+k_gat_edge_grad(const SpmmBlock *__restrict__ blocks, int32_t d,
+                const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+                const float *__restrict__ alpha, const float *__restrict__ s,
+                const float *__restrict__ z, const float *__restrict__ h_out,
+                const float *__restrict__ dh_out, bool relu, float slope, float *__restrict__ dO,
+                float *__restrict__ dpre, float *__restrict__ g2)
 {
     constexpr int G = kWave / GL;
+    __shared__ float red[kSpmmWaves];
     const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
     const int g = lane / GL, gl = lane % GL;
-    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (row >= n_own)
-        return;   // uniform per wave
+    const SpmmBlock b = blocks[blockIdx.x];
+    const bool long_row = b.nrows == 0;   // uniform over the block
+    int64_t row;
+    int kb, ke;
+    if (long_row) {
+        row = b.row;
+        const int per = (b.ke - b.kb + kSpmmWaves - 1) / kSpmmWaves;
+        kb = min(b.ke, b.kb + wave * per);
+        ke = min(b.ke, kb + per);
+    } else {
+        if (wave >= b.nrows)
+            return;   // uniform per wave; short-row blocks have no barrier
+        row = b.row + wave;
+        kb = rowptr[row];
+        ke = rowptr[row + 1];
+    }
+    const bool writer = !long_row || wave == 0;   // stores dO and g2
     const int dv = d / VEC;
     float D[NCH][VEC];
     float c = 0.f;
@@ -1391,7 +1412,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) voi
                 D[ch][v] = (!relu || h[v] > 0.f) ? dh[v] : 0.f;
                 c = fmaf(D[ch][v], h[v], c);
             }
-            if (g == 0)
+            if (writer && g == 0)
                 store_vec<VEC>(dO + row * d + cv * VEC, D[ch]);
         } else {
 #pragma unroll
@@ -1403,12 +1424,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) voi
     for (int off = GL / 2; off > 0; off >>= 1)
         c += __shfl_xor(c, off);
     const float t = s[2 * row + 1];
-    const int kb = rowptr[row], ke = rowptr[row + 1];
     float rowsum = 0.f;
     // Every load below is issued unconditionally from a valid address (an
-    // entry past the row reads the row's last entry, a vector past the width
-    // its first vector) and its result is ignored or multiplied by a zero of
-    // D, so all U x NCH gathers of a step are in flight together.
+    // entry past the part reads the part's last entry, a vector past the
+    // width its first vector) and its result is ignored or multiplied by a
+    // zero of D, so all U x NCH gathers of a step are in flight together.
     for (int k0 = kb; k0 < ke; k0 += G * U) {
         int kk[U];
         bool ok[U];
@@ -1462,8 +1482,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) voi
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1)
         rowsum += __shfl_xor(rowsum, off);
-    if (lane == 0)
+    if (long_row) {
+        if (lane == 0)
+            red[wave] = rowsum;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            float r = 0.f;
+#pragma unroll
+            for (int w = 0; w < kSpmmWaves; ++w)
+                r += red[w];
+            g2[2 * row + 1] = r;
+        }
+    } else if (lane == 0) {
         g2[2 * row + 1] = rowsum;
+    }
 }
 
 // a_t[k] = a[perm[k]], b_t[k] = b[perm[k]]: edge values into the entry order
@@ -2079,27 +2111,27 @@ hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32
 namespace {
 
 template <int VEC, int GL, int NCH, int U = 2>
-hipError_t gat_edge_grad_t(int32_t n_own, int32_t d, const int32_t *rowptr, const int32_t *col,
-                           const float *alpha, const float *s, const float *z,
-                           const float *h_out, const float *dh_out, bool relu, float slope,
-                           float *dO, float *dpre, float *g2, hipStream_t st)
+hipError_t gat_edge_grad_t(const SpmmBlock *blocks, int32_t n_blocks, int32_t d,
+                           const int32_t *rowptr, const int32_t *col, const float *alpha,
+                           const float *s, const float *z, const float *h_out,
+                           const float *dh_out, bool relu, float slope, float *dO, float *dpre,
+                           float *g2, hipStream_t st)
 {
-    const int64_t blocks = ((int64_t)n_own + 3) / 4;
-    hipLaunchKernelGGL((k_gat_edge_grad<VEC, GL, NCH, U>), dim3((unsigned)blocks), dim3(256), 0, st,
-                       n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu, slope, dO, dpre,
-                       g2);
+    hipLaunchKernelGGL((k_gat_edge_grad<VEC, GL, NCH, U>), dim3((unsigned)n_blocks),
+                       dim3(kSpmmThreads), 0, st, blocks, d, rowptr, col, alpha, s, z, h_out,
+                       dh_out, relu, slope, dO, dpre, g2);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
-                                const int32_t *col, const float *alpha, const float *s,
-                                const float *z, const float *h_out, const float *dh_out,
-                                bool relu, float slope, float *dO, float *dpre, float *g2,
-                                hipStream_t st)
+hipError_t launch_gat_edge_grad(const SpmmBlock *blocks, int32_t n_blocks, int32_t d,
+                                const int32_t *rowptr, const int32_t *col, const float *alpha,
+                                const float *s, const float *z, const float *h_out,
+                                const float *dh_out, bool relu, float slope, float *dO,
+                                float *dpre, float *g2, hipStream_t st)
 {
-    if (n_own <= 0)
+    if (n_blocks <= 0)
         return hipSuccess;
     if (d < 1 || d > kGatMaxWidth)
         return hipErrorInvalidValue;
@@ -2116,8 +2148,8 @@ hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
     const int gl = dv <= 4 ? 4 : (dv <= 8 ? 8 : (dv <= 128 ? 16 : 64));
     const int nch = (dv + gl - 1) / gl;
 #define DIGEST_GEG(V, L, C)                                                                     \
-    return gat_edge_grad_t<V, L, C>(n_own, d, rowptr, col, alpha, s, z, h_out, dh_out, relu,    \
-                                    slope, dO, dpre, g2, st)
+    return gat_edge_grad_t<V, L, C>(blocks, n_blocks, d, rowptr, col, alpha, s, z, h_out,       \
+                                    dh_out, relu, slope, dO, dpre, g2, st)
 #define DIGEST_GEG_V(V)                                                                         \
     do {                                                                                        \
         if (gl == 4) DIGEST_GEG(V, 4, 1);                                                       \

@@ -147,11 +147,11 @@ hipError_t launch_gat_softmax(int32_t n_rows, const int32_t *rowptr, const int32
                               const float *s, float slope, float *alpha, hipStream_t st);
 // dO = dh_out (masked by h_out > 0 with relu), dpre[k] the gradient of the
 // k-th pre-activation score, g2[i][1] = sum of row i's dpre; d <= kGatMaxWidth.
-hipError_t launch_gat_edge_grad(int32_t n_own, int32_t d, const int32_t *rowptr,
-                                const int32_t *col, const float *alpha, const float *s,
-                                const float *z, const float *h_out, const float *dh_out,
-                                bool relu, float slope, float *dO, float *dpre, float *g2,
-                                hipStream_t st);
+hipError_t launch_gat_edge_grad(const SpmmBlock *blocks, int32_t n_blocks, int32_t d,
+                                const int32_t *rowptr, const int32_t *col, const float *alpha,
+                                const float *s, const float *z, const float *h_out,
+                                const float *dh_out, bool relu, float slope, float *dO,
+                                float *dpre, float *g2, hipStream_t st);
 // a_t[k] = a[perm[k]], b_t[k] = b[perm[k]] for k < n.
 hipError_t launch_gather_perm2(int64_t n, const int32_t *perm, const float *a, const float *b,
                                float *a_t, float *b_t, hipStream_t st);
