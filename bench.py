@@ -95,9 +95,10 @@ def launch_model_gat(st, widths):
         put("gat_edge_grad", l, 4 * (n + 1) + 12 * nnz + 12 * n * do + 4 * R * do + 8 * R + 4 * n,
             e=nnz)
         put("gat_transpose_edges", l, 20 * nnz)
-        put("gat_aggregate_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do, e=nnz)
+        put("gat_aggregate_transposed", l,
+            4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do + 4 * R + 4 * n + 8 * do, e=nnz)
         put("gat_score_sums", l, 4 * (R + 1) + 8 * nnz + 4 * n + 4 * R)
-        put("gat_score_grad", l, 8 * R * do + 8 * do + 4 * R + 12 * R)
+        put("gat_score_grad", l, 8 * R + 4 * nh)
         put("gat_datt", l, 4 * (R * do + 2 * R + 2 * do), 4.0 * R * do)
         put("gat_dw", l, 4 * (R * di + R * do + di * do), 2.0 * R * di * do)
         put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)

@@ -445,7 +445,8 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
                        const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
                        float *out1 = nullptr, int32_t n_out0 = INT32_MAX,
-                       const float *val = nullptr, bool relu = false)
+                       const float *val = nullptr, bool relu = false,
+                       const digest::SpmmRank1 *r1 = nullptr)
 {
     const bool fwd = which == Csr::Fwd;
     const std::vector<SpmmBlock> *blocks = &p->blocks_f;
@@ -466,7 +467,7 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
                             val ? val : p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1,
-                            n_src0, d, out, s, ep, out1, n_out0, relu),
+                            n_src0, d, out, s, ep, out1, n_out0, relu, r1),
         "spmm");
 }
 
@@ -1469,20 +1470,29 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
                 "GAT transpose"))
             return st;
     }
-    // dz = (alpha-weighted P_m)^T dO over every local row
-    if (digest_status st = run_spmm(p, Csr::FullT, dO, nullptr, p->n_own, d_out, dz, layer, s,
-                                    nullptr, K_GAT_AGG_T, nullptr, INT32_MAX, alpha_t))
-        return st;
-    // source-score gradients: column sums of dpre, then the score terms of dz
+    // source-score gradients: column sums of dpre
     if (digest_status st = run_spmm(p, Csr::FullT, p->gat<float>(p->glay.ones), nullptr,
                                     p->n_own, 1, ds_src, layer, s, nullptr, K_GAT_SCORE_SUMS,
                                     nullptr, INT32_MAX, dpre_t))
         return st;
+    // dz = (alpha-weighted P_m)^T dO over every local row, plus the score
+    // terms ds_src[v] att[:,0] + (owned v) g2[v][1] att[:,1] added in its store
     {
+        digest::SpmmRank1 r1;
+        r1.a = att;
+        r1.x = ds_src;
+        r1.y = g2;
+        r1.ny = p->n_own;
+        if (digest_status st = run_spmm(p, Csr::FullT, dO, nullptr, p->n_own, d_out, dz, layer,
+                                        s, nullptr, K_GAT_AGG_T, nullptr, INT32_MAX, alpha_t,
+                                        false, &r1))
+            return st;
+    }
+    {
+        // the datt operand [ds_src, row sums of the owned rows]
         Timed t(p, K_GAT_SCORE_GRAD, layer, s);
         if (digest_status st = hip_check(
-                digest::launch_gat_rank1(R, p->n_own, d_out, att, ds_src, g2, dz, s),
-                "GAT score terms"))
+                digest::launch_gat_score_cols(R, p->n_own, ds_src, g2, s), "GAT score columns"))
             return st;
     }
     {

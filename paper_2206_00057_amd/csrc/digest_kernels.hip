@@ -198,20 +198,29 @@ struct SpmmOut {
     float *out0;
     float *out1;
     int32_t n0;
-    bool relu;   // store max(x, 0)
+    bool relu;      // store max(x, 0)
+    SpmmRank1 r1;   // rank-one terms added first when r1.a is set
 
     __device__ __forceinline__ float *row(int32_t r, int32_t d) const
     {
         return r < n0 ? out0 + (int64_t)r * d : out1 + (int64_t)(r - n0) * d;
     }
+    // the stored value of feature f of row r whose sum is v
+    __device__ __forceinline__ float fin(int32_t r, int32_t f, float v) const
+    {
+        if (r1.a) {
+            const float xa = r1.x[r];
+            const float yb = r < r1.ny ? r1.y[2 * (int64_t)r + 1] : 0.f;
+            v += xa * r1.a[2 * f] + yb * r1.a[2 * f + 1];
+        }
+        return relu ? fmaxf(v, 0.f) : v;
+    }
     template <int VEC>
     __device__ __forceinline__ void put(int32_t r, int32_t d, int32_t off, float (&v)[VEC]) const
     {
-        if (relu) {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i)
-                v[i] = fmaxf(v[i], 0.f);
-        }
+        for (int i = 0; i < VEC; ++i)
+            v[i] = fin(r, off + i, v[i]);
         store_vec<VEC>(row(r, d) + off, v);
     }
 };
@@ -345,7 +354,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
 #pragma unroll
                     for (int w = 0; w < kSpmmWaves; ++w)
                         sum += red[w][t];
-                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = out.relu ? fmaxf(sum, 0.f) : sum;
+                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = out.fin(row, c * VEC + t % VEC, sum);
                 }
             }
             __syncthreads();
@@ -1519,25 +1528,16 @@ __global__ __launch_bounds__(256) void k_gather_perm2(int64_t n, const int32_t *
 //   g2[v][0] = ds_src[v];  g2[v][1] = 0 for the halo rows
 // (g2 then holds the gradient of the scores, [R][2]).  A thread per element
 // of dz; the thread of column 0 writes g2.
-__global__ __launch_bounds__(256) void k_gat_rank1(int64_t R, int32_t n_own, int32_t d,
-                                                   const float *__restrict__ att,
-                                                   const float *__restrict__ ds_src,
-                                                   float *__restrict__ g2,
-                                                   float *__restrict__ dz)
+__global__ __launch_bounds__(256) void k_gat_score_cols(int64_t R, int32_t n_own,
+                                                        const float *__restrict__ ds_src,
+                                                        float *__restrict__ g2)
 {
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= R * d)
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v >= R)
         return;
-    const int64_t v = e / d;
-    const int q = (int)(e % d);
-    const float a = ds_src[v];
-    const float b = v < n_own ? g2[2 * v + 1] : 0.f;
-    dz[e] += a * att[2 * q] + b * att[2 * q + 1];
-    if (q == 0) {
-        g2[2 * v] = a;
-        if (v >= n_own)
-            g2[2 * v + 1] = 0.f;
-    }
+    g2[2 * v] = ds_src[v];
+    if (v >= n_own)
+        g2[2 * v + 1] = 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -1787,7 +1787,7 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep, float *out1,
-                       int32_t n_out0, bool relu)
+                       int32_t n_out0, bool relu, const SpmmRank1 *r1)
 {
     if (ep && (!spmm_epilogue_ok(d, ep->n2, ep->out2) ||
                (ep->out3 && !spmm_epilogue_ok(d, ep->n2, ep->out3))))
@@ -1796,9 +1796,11 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         return hipErrorInvalidValue;
     if (n_blocks <= 0 || d <= 0)
         return hipSuccess;
-    if (relu && ep)
+    if ((relu || (r1 && r1->a)) && ep)
         return hipErrorInvalidValue;   // the epilogue reads the stored row back
-    const SpmmOut out{out0, out1, n_out0, relu};
+    if (r1 && r1->a && (!r1->x || (r1->ny > 0 && !r1->y)))
+        return hipErrorInvalidValue;
+    const SpmmOut out{out0, out1, n_out0, relu, r1 ? *r1 : SpmmRank1{}};
     int vec = pick_vec(d, src0, out0);
     if (src1 && pick_vec(d, src1, nullptr) < vec)
         vec = pick_vec(d, src1, nullptr);
@@ -2185,16 +2187,16 @@ hipError_t launch_gather_perm2(int64_t n, const int32_t *perm, const float *a, c
     return hipGetLastError();
 }
 
-hipError_t launch_gat_rank1(int64_t R, int32_t n_own, int32_t d, const float *att,
-                            const float *ds_src, float *g2, float *dz, hipStream_t st)
+hipError_t launch_gat_score_cols(int64_t R, int32_t n_own, const float *ds_src, float *g2,
+                                 hipStream_t st)
 {
-    if (R <= 0 || d <= 0)
+    if (R <= 0)
         return hipSuccess;
-    const int64_t blocks = (R * d + 255) / 256;
+    const int64_t blocks = (R + 255) / 256;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_gat_rank1, dim3((unsigned)blocks), dim3(256), 0, st, R, n_own, d, att,
-                       ds_src, g2, dz);
+    hipLaunchKernelGGL(k_gat_score_cols, dim3((unsigned)blocks), dim3(256), 0, st, R, n_own,
+                       ds_src, g2);
     return hipGetLastError();
 }
 

@@ -50,13 +50,24 @@ struct SpmmEpilogue {
 };
 bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2);
 
+// Rank-one terms an aggregation can add to its row r before the store:
+// out[r][f] += x[r] a[f][0] + (r < ny ? y[2r + 1] : 0) a[f][1], with a
+// row-major [d][2] and y [rows][2] (the GAT backward's score terms).
+struct SpmmRank1 {
+    const float *a = nullptr;
+    const float *x = nullptr;
+    const float *y = nullptr;
+    int32_t ny = 0;
+};
+
 // The first n_long blocks are the long-row blocks (nrows == 0), the rest
 // short-row blocks.
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep = nullptr,
-                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX, bool relu = false);
+                       float *out1 = nullptr, int32_t n_out0 = INT32_MAX, bool relu = false,
+                       const SpmmRank1 *r1 = nullptr);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
 // slices (each its own grid part) when splits > 1.
@@ -155,10 +166,10 @@ hipError_t launch_gat_edge_grad(const SpmmBlock *blocks, int32_t n_blocks, int32
 // a_t[k] = a[perm[k]], b_t[k] = b[perm[k]] for k < n.
 hipError_t launch_gather_perm2(int64_t n, const int32_t *perm, const float *a, const float *b,
                                float *a_t, float *b_t, hipStream_t st);
-// dz[v] += ds_src[v] att[:,0] + (v < n_own ? g2[v][1] att[:,1] : 0) over
-// v < R; then g2[v][0] = ds_src[v], g2[v][1] = 0 for v >= n_own.
-hipError_t launch_gat_rank1(int64_t R, int32_t n_own, int32_t d, const float *att,
-                            const float *ds_src, float *g2, float *dz, hipStream_t st);
+// The score-gradient operand of datt: g2[v][0] = ds_src[v] for v < R and
+// g2[v][1] = 0 for n_own <= v < R (the owned rows keep their row sums).
+hipError_t launch_gat_score_cols(int64_t R, int32_t n_own, const float *ds_src, float *g2,
+                                 hipStream_t st);
 
 // GEMM K step; the smallest workgroup tile of C is kGemmBM x kGemmBN.
 constexpr int kGemmBM = 64;
