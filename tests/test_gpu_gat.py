@@ -256,3 +256,40 @@ def test_gat_round_driver_matches_oracle_and_replays_bitwise():
         _ = torch.ones(1000, device="cuda").sum().item()   # eager work between replays
         for t, ref in zip((gp.H[2], gp.dW[1], gp.dW[2], gp.dAtt[1], gp.dAtt[2]), eager):
             np.testing.assert_array_equal(host(t).view(np.uint32), ref.view(np.uint32))
+
+
+def boundary_partition(seed=11):
+    """A hand-built partition whose owned rows have 0, 1, 7, 63, 64, 65, 66,
+    100 and 521 entries (the last five past the one-wave threshold of 64
+    entries at least once; 521 leaves the eighth wave a short part), columns
+    drawn without repeats from owned and halo nodes alike."""
+    rng = np.random.default_rng(seed)
+    n_global = 1400
+    owned = np.arange(200, 320, dtype=np.int64)
+    lengths = [0, 1, 7, 63, 64, 65, 66, 100, 521, 0] + list(rng.integers(0, 12, owned.size - 10))
+    rng.shuffle(lengths)
+    indptr = np.zeros(owned.size + 1, np.int64)
+    np.cumsum(lengths, out=indptr[1:])
+    indices = np.concatenate([np.sort(rng.choice(n_global, k, replace=False)) for k in lengths])
+    indices = indices.astype(np.int64)
+    values = rng.random(indices.size).astype(np.float32)
+    mine = np.zeros(n_global, bool)
+    mine[owned] = True
+    halo = np.unique(indices[~mine[indices]])
+    return n_global, synth.Partition(owned, halo, indptr, indices, values)
+
+
+@pytest.mark.parametrize("widths", [(16, 40, 6), (12, 256, 47)], ids=["40-6", "256-47"])
+def test_gat_empty_and_long_rows(widths):
+    """Empty rows give act(0) and no gradient; rows at and past the 64-entry
+    threshold (a block of 8 waves splitting the entries) match the oracle."""
+    n_global, part = boundary_partition()
+    assert (np.diff(part.indptr) == 0).sum() >= 2 and np.diff(part.indptr).max() == 521
+    c = Case(n_global, part, widths, seed=3)
+    for level in range(len(widths) - 1):
+        c.pull(level, synth.relu_normal((n_global, widths[level]), seed=90 + level))
+    for layer in (1, 2):
+        act = oracle.RELU if layer == 1 else oracle.IDENTITY
+        out, dw, datt, dh_in = c.layer(layer, act, f"boundary rows {widths} layer {layer}")
+        empty = np.diff(part.indptr) == 0
+        assert not host(out)[empty].any()
