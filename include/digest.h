@@ -313,7 +313,9 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
  *   dw       = sum over local rows v of x_v^T dz_v           [d_{layer-1}, d_layer]
  *   dh_in_i  = dz_i W^T (owned rows; NULL skips it)
  *   h_in, h_out, dh_out, w, att: as in and out of the forward of the layer.
- * Sums run in a fixed order (no float atomics).
+ * LeakyReLU'(x) is 1 for x > 0 and negative_slope otherwise (at 0 too), and
+ * act' is the ReLU mask h_out > 0.  Sums run in a fixed order (no float
+ * atomics).
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no GAT forward of the layer since
  * the GAT bind, or level layer-1 pulled again since it), DIGEST_EHIP.
  */
