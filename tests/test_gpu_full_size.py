@@ -3,7 +3,8 @@ and OGB-Products-shaped synthetic graphs, and the halo-dominated permutation
 partition), in the same library calls the benchmark times: pull and push
 contents bit-exact; every layer's forward and backward, the fused backward
 with the halo gradient, and the loss head within rtol 1e-4 / atol 1e-5 plus
-the scale-aware bound, over all outputs
+the scale-aware bound, over all outputs; Algorithm 1's rounds over all eight
+Flickr-shaped subgraphs against the oracle trainer
 (the oracle finishes these in seconds with its threads); and the GAT layer
 over stale halo rows on the three workloads the GAT benchmark times, every
 layer's forward and backward over all outputs."""
@@ -116,3 +117,36 @@ def test_full_size_gat_workload(name):
         print(f"[{name} gat] layer {layer} fwd+bwd ok {time.time() - t:.1f}s", flush=True)
     del c
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("mode,rounds", [("none", 11), ("fresh", 3)])
+def test_full_size_trainer_rounds(mode, rounds):
+    """Algorithm 1 over all eight subgraphs of the Flickr-shaped workload
+    (the configuration `bench.py --train` times), sync interval 10: rounds
+    1..11 take the initial push, the pull of round 10 and the push of round
+    11. Each round's logits of every subgraph, the global W and the stores
+    are checked against the oracle trainer running its own trajectory."""
+    from test_gpu_trainer import _setup
+    cfg = synth.CONFIGS["medium"]
+    K = cfg.sync_periods[0]
+    g, parts, tr, ot = _setup(cfg, K=K, lr=0.1, grad_exchange=mode)
+    tr.init_stores()
+    ot.init_stores()
+    for lev in range(1, cfg.layers):
+        assert_close(host(tr.stores[lev]), ot.stores[lev], f"initial store level {lev}")
+    for r in range(1, rounds + 1):
+        t = time.time()
+        tr.round(r)
+        o_loss = ot.round(r)
+        for m, gp in enumerate(tr.gps):
+            assert_close(host(gp.H[cfg.layers]), ot.logits[m], f"{mode} round {r} logits m={m}",
+                         scale_tol=1e-4)
+        assert abs(tr.mean_loss() - o_loss) <= 1e-5 + 1e-4 * abs(o_loss)
+        for l in range(cfg.layers):
+            assert_close(host(tr.W[l]), ot.W[l], f"{mode} round {r} W{l + 1}", scale_tol=1e-4)
+        for lev in range(1, cfg.layers):
+            assert_close(host(tr.stores[lev]), ot.stores[lev], f"{mode} round {r} store {lev}",
+                         scale_tol=1e-4)
+        print(f"[medium trainer {mode}] round {r} ok, loss {o_loss:.6f} {time.time() - t:.1f}s",
+              flush=True)
