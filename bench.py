@@ -363,14 +363,17 @@ def main():
     for r in range(1, args.warmup + 1):
         run(r)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # an event after every round (enqueued, no host wait) also gives the
+    # median round time beside the mean
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     rounds = range(args.warmup + 1, args.warmup + args.steps + 1)
-    e0.record()
-    for r in rounds:
+    ev[0].record()
+    for i, r in enumerate(rounds):
         run(r)
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
+    ms = ev[0].elapsed_time(ev[-1])
+    ms_median = float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]))
     if gat:   # per layer: the forward aggregation and the transposed one of the backward
         edges = 2 * L * st["nnz"]
     else:
@@ -428,6 +431,7 @@ def main():
         "metric": METRIC_GAT if gat else METRIC, "value": round(value, 4), "unit": "GTEPS",
         "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms / args.steps, 5),
+        "ms_per_step_median": round(ms_median, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {
