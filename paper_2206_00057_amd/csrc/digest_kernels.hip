@@ -403,29 +403,30 @@ __device__ __forceinline__ float *ep_row(const SpmmEpilogue &ep, int32_t r)
     return ep.out3 ? ep.out3 + (int64_t)(r - ep.rows) * ep.n2 : nullptr;
 }
 
-// Aggregation for rows at most GL * VEC <= 16 wide, where one row per wave
-// would leave most lanes idle: the n_long long-row blocks (first in the
-// list) run as in k_spmm, one per workgroup; every wave of the remaining
+// Aggregation for rows of at most kNarrowWide floats, where one row per
+// wave would leave most lanes idle: the n_long long-row blocks (first in
+// the list) run as in k_spmm, one per workgroup; every wave of the remaining
 // workgroups takes one short-row block (up to kSpmmWaves consecutive rows)
-// and gives each of its lane groups a row of its own.  A group fetches
-// kNarrowBatch * GL entry ids and weights at a time (kNarrowBatch per lane),
-// broadcasts them inside the group and keeps all of their gathers in flight,
-// so a row of up to that many entries costs one dependent round trip; the
-// entries of a row are added in CSR order, so results do not depend on the
-// launch shape.
-// With EP, rows r < ep.rows also get out2[r][n] = sum_k out[r][k] w[n][k]
-// (w row-major [n2][d], staged in LDS as [k][n2]); a lane group shares its
-// row by shuffles and writes it out in float4 pieces.
-constexpr int kNarrowBatch = 4;
-
-template <int VEC, int GL, bool TWO, bool EP>
+// and gives each of its lane groups a row of its own, GL lanes holding NCH
+// vectors of VEC floats each (GL * NCH * VEC >= the row width).  A group
+// fetches NB * GL entry ids and weights at a time (NB per lane), broadcasts
+// them inside the group and keeps all of their gathers in flight, so a row
+// of up to that many entries costs one dependent round trip; the entries
+// of a row are added in CSR order, so results do not depend on the launch
+// shape.  NB is chosen so that a lane holds at most 64 gathered floats.
+// With EP (rows of at most kNarrow floats, NCH = 1), rows r < ep.rows also
+// get out2[r][n] = sum_k out[r][k] w[n][k] (w row-major [n2][d], staged in
+// LDS as [k][n2]); a lane group shares its row by shuffles and writes it out
+// in float4 pieces.
+template <int VEC, int GL, int NCH, int NB, bool TWO, bool EP>
 __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     const SpmmBlock *__restrict__ blocks, int32_t n_long, int32_t n_blocks,
     const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
     const float *__restrict__ val, const float *__restrict__ src0, const float *__restrict__ src1,
     int32_t n_src0, int32_t d, SpmmOut out, SpmmEpilogue ep)
 {
-    __shared__ float red[kSpmmWaves][GL * VEC];
+    static_assert(!EP || (NCH == 1 && GL * VEC <= kNarrow), "epilogue rows are kNarrow wide");
+    __shared__ float red[kSpmmWaves][NCH * GL * VEC];
     extern __shared__ float ws[];   // EP: w as [k][n2]
     if constexpr (EP) {
         stage_lds(ws, d * ep.n2, [&](int i) {
@@ -436,7 +437,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     }
     if ((int32_t)blockIdx.x < n_long) {   // uniform over the block
         const SpmmBlock b = blocks[blockIdx.x];
-        spmm_block<VEC, GL, 1, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, out, red);
+        spmm_block<VEC, GL, NCH, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, out, red);
         if constexpr (EP) {
             // the row was written by this block before spmm_block's last barrier
             if (float *o2 = ep_row(ep, b.row)) {
@@ -461,66 +462,76 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
         return;
     const SpmmBlock b = blocks[bi];
     const int dv = d / VEC;
-    const bool lane_ok = gl < dv;   // GL * VEC >= d, so one vector per lane covers the row
     for (int i = g; i < b.nrows; i += G) {
         const int row = b.row + i;
         const int kb = rowptr[row], ke = rowptr[row + 1];
-        float acc[VEC];
+        float acc[NCH][VEC];
 #pragma unroll
-        for (int v = 0; v < VEC; ++v)
-            acc[v] = 0.f;
-        constexpr int E = kNarrowBatch * GL;   // entries per batch
+        for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                acc[ch][v] = 0.f;
+        constexpr int E = NB * GL;   // entries per batch
         for (int k0 = kb; k0 < ke; k0 += E) {
             // Every load is unconditional so that all of a batch's gathers
             // are in flight together: an entry past the row rereads the
             // row's last entry with weight 0 (it adds nothing, and no other
-            // row's data can enter), a lane past the width rereads the row's
-            // first vector and stores nothing.
-            int mc[kNarrowBatch];
-            float mv[kNarrowBatch];
+            // row's data can enter), a vector past the width rereads the
+            // row's first vector and is not stored.
+            int mc[NB];
+            float mv[NB];
 #pragma unroll
-            for (int j = 0; j < kNarrowBatch; ++j) {   // entry k0 + j*GL + gl
+            for (int j = 0; j < NB; ++j) {   // entry k0 + j*GL + gl
                 const int k = k0 + j * GL + gl;
                 const int kc = k < ke ? k : ke - 1;
                 mc[j] = col[kc];
                 mv[j] = val[kc] * (k < ke ? 1.f : 0.f);
             }
-            int cc[kNarrowBatch][GL];
-            float aa[kNarrowBatch][GL];
+            int cc[NB][GL];
+            float aa[NB][GL];
 #pragma unroll
-            for (int j = 0; j < kNarrowBatch; ++j)
+            for (int j = 0; j < NB; ++j)
 #pragma unroll
                 for (int u = 0; u < GL; ++u) {
                     cc[j][u] = __shfl(mc[j], g * GL + u);
                     aa[j][u] = __shfl(mv[j], g * GL + u);
                 }
-            float x[kNarrowBatch][GL][VEC];
-            const int lv = (lane_ok ? gl : 0) * VEC;
+            float x[NB][GL][NCH][VEC];
 #pragma unroll
-            for (int j = 0; j < kNarrowBatch; ++j)
+            for (int j = 0; j < NB; ++j)
 #pragma unroll
                 for (int u = 0; u < GL; ++u) {
                     const int c = cc[j][u];
                     const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * d
                                                            : src0 + (int64_t)c * d;
-                    load_vec<VEC>(sp + lv, x[j][u]);
+#pragma unroll
+                    for (int ch = 0; ch < NCH; ++ch) {
+                        const int cv = ch * GL + gl;
+                        load_vec<VEC>(sp + (cv < dv ? cv : 0) * VEC, x[j][u][ch]);
+                    }
                 }
 #pragma unroll
-            for (int j = 0; j < kNarrowBatch; ++j)
+            for (int j = 0; j < NB; ++j)
 #pragma unroll
                 for (int u = 0; u < GL; ++u)
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v)
-                        acc[v] = fmaf(aa[j][u], x[j][u][v], acc[v]);
+                    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v)
+                            acc[ch][v] = fmaf(aa[j][u], x[j][u][ch][v], acc[ch][v]);
         }
-        if (lane_ok)
-            out.put<VEC>(row, d, gl * VEC, acc);
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            const int cv = ch * GL + gl;
+            if (cv < dv)
+                out.put<VEC>(row, d, cv * VEC, acc[ch]);
+        }
         if constexpr (EP) {
             if (float *o2 = ep_row(ep, row)) {
                 float gk[kNarrow];
 #pragma unroll
                 for (int k = 0; k < kNarrow; ++k) {
-                    const float v = __shfl(acc[k % VEC], (g * GL + k / VEC) & (kWave - 1));
+                    const float v = __shfl(acc[0][k % VEC], (g * GL + k / VEC) & (kWave - 1));
                     gk[k] = k < d ? v : 0.f;
                 }
                 for (int n4 = gl; n4 < ep.n2 / 4; n4 += GL)
@@ -1617,23 +1628,37 @@ hipError_t copy_rows_v(int gl, int mode, const int32_t *sidx, const int32_t *did
     }
 }
 
-template <int VEC, int GL, bool TWO>
+// Gathered floats one lane of the narrow kernel holds per batch.
+constexpr int kNarrowLaneFloats = 64;
+constexpr int narrow_nb(int gl, int nch, int vec)
+{
+    const int nb = kNarrowLaneFloats / (gl * nch * vec);
+    return nb < 1 ? 1 : (nb > 4 ? 4 : nb);
+}
+
+template <int VEC, int GL, int NCH, bool TWO>
 hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_blocks,
                          const int32_t *rowptr, const int32_t *col, const float *val,
                          const float *src0, const float *src1, int32_t n_src0, int32_t d,
                          SpmmOut out, const SpmmEpilogue *ep, hipStream_t s)
 {
+    constexpr int NB = narrow_nb(GL, NCH, VEC);
     const int64_t grid = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
-    if (ep) {
-        const size_t lds = sizeof(float) * (size_t)d * ep->n2;
-        hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, TWO, true>), dim3((unsigned)grid),
-                           dim3(kSpmmThreads), lds, s, blocks, n_long, n_blocks, rowptr, col, val,
-                           src0, src1, n_src0, d, out, *ep);
+    if constexpr (NCH == 1 && GL * VEC <= kNarrow) {
+        if (ep) {
+            const size_t lds = sizeof(float) * (size_t)d * ep->n2;
+            hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, NCH, NB, TWO, true>), dim3((unsigned)grid),
+                               dim3(kSpmmThreads), lds, s, blocks, n_long, n_blocks, rowptr, col,
+                               val, src0, src1, n_src0, d, out, *ep);
+            return hipGetLastError();
+        }
     } else {
-        hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, TWO, false>), dim3((unsigned)grid),
-                           dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val,
-                           src0, src1, n_src0, d, out, SpmmEpilogue{});
+        if (ep)
+            return hipErrorInvalidValue;
     }
+    hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, NCH, NB, TWO, false>), dim3((unsigned)grid),
+                       dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val, src0,
+                       src1, n_src0, d, out, SpmmEpilogue{});
     return hipGetLastError();
 }
 
@@ -1808,32 +1833,38 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         vec = pick_vec(d, out1, nullptr);
     const int dv = d / vec;
     const int gl = pick_group(dv);
-    // the row-per-lane-group kernel holds kNarrowBatch x GL x VEC gathered
-    // floats per lane: rows up to kNarrow floats; wider ones go to the
-    // row-per-wave kernel (with lane groups as narrow as the row)
-    const bool narrow = d <= kNarrow;
-    if (ep && !narrow)
+    // rows of at most kNarrowWide floats: the row-per-lane-group kernel, in
+    // groups of at most 16 lanes holding NCH vectors each; wider rows: the
+    // row-per-wave kernel
+    const bool narrow = d <= kNarrowWide;
+    if (ep && d > kNarrow)
         return hipErrorInvalidValue;
     if (narrow) {   // narrow rows: a row per lane group
         if (n_long < 0 || n_long > n_blocks)
             return hipErrorInvalidValue;
-#define DIGEST_NARROW(V, L)                                                                      \
-    return src1 ? spmm_narrow_t<V, L, true>(blocks, n_long, n_blocks, rowptr, col, val, src0,   \
-                                            src1, n_src0, d, out, ep, s)                       \
-                : spmm_narrow_t<V, L, false>(blocks, n_long, n_blocks, rowptr, col, val, src0,  \
-                                             src1, n_src0, d, out, ep, s)
-        if (vec == 4) {
-            if (gl == 4) DIGEST_NARROW(4, 4);
-            if (gl == 8) DIGEST_NARROW(4, 8);
-            DIGEST_NARROW(4, 16);
-        } else if (vec == 2) {
-            if (gl == 4) DIGEST_NARROW(2, 4);
-            if (gl == 8) DIGEST_NARROW(2, 8);
-            DIGEST_NARROW(2, 16);
-        } else {
-            if (gl == 4) DIGEST_NARROW(1, 4);
-            if (gl == 8) DIGEST_NARROW(1, 8);
-            DIGEST_NARROW(1, 16);
+        const int ngl = gl > 16 ? 16 : gl;
+        const int nnch = (dv + ngl - 1) / ngl;
+#define DIGEST_NARROW(V, L, C)                                                                   \
+    return src1 ? spmm_narrow_t<V, L, C, true>(blocks, n_long, n_blocks, rowptr, col, val,      \
+                                               src0, src1, n_src0, d, out, ep, s)              \
+                : spmm_narrow_t<V, L, C, false>(blocks, n_long, n_blocks, rowptr, col, val,     \
+                                                src0, src1, n_src0, d, out, ep, s)
+        if (vec == 4) {   // dv <= 16
+            if (ngl == 4) DIGEST_NARROW(4, 4, 1);
+            if (ngl == 8) DIGEST_NARROW(4, 8, 1);
+            DIGEST_NARROW(4, 16, 1);
+        } else if (vec == 2) {   // dv <= 32
+            if (ngl == 4) DIGEST_NARROW(2, 4, 1);
+            if (ngl == 8) DIGEST_NARROW(2, 8, 1);
+            if (nnch <= 1) DIGEST_NARROW(2, 16, 1);
+            DIGEST_NARROW(2, 16, 2);
+        } else {   // dv <= 64
+            if (ngl == 4) DIGEST_NARROW(1, 4, 1);
+            if (ngl == 8) DIGEST_NARROW(1, 8, 1);
+            if (nnch <= 1) DIGEST_NARROW(1, 16, 1);
+            if (nnch <= 2) DIGEST_NARROW(1, 16, 2);
+            if (nnch <= 3) DIGEST_NARROW(1, 16, 3);
+            DIGEST_NARROW(1, 16, 4);
         }
 #undef DIGEST_NARROW
     }

@@ -19,6 +19,8 @@ struct SpmmBlock {
 constexpr int kSpmmThreads = 512;
 // Widest side handled by the narrow kernels.
 constexpr int kNarrow = 16;
+// Widest row the row-per-lane-group aggregation takes.
+constexpr int kNarrowWide = 64;
 // Rows with more entries than this get a whole block.
 constexpr int32_t kSpmmLongRow = 64;
 
