@@ -293,3 +293,25 @@ def test_gat_empty_and_long_rows(widths):
         out, dw, datt, dh_in = c.layer(layer, act, f"boundary rows {widths} layer {layer}")
         empty = np.diff(part.indptr) == 0
         assert not host(out)[empty].any()
+
+
+def test_gat_empty_partition():
+    """No owned rows (so no halo): both calls succeed, and dW and datt are
+    written as zeros."""
+    from paper_2206_00057_amd import digest as D
+    h = D.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
+                                  np.zeros(0), np.zeros(0), [3, 4])
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    D.digest_partition_bind_workspace(h, ws)
+    gws = torch.empty(max(D.digest_gat_query(h), 256), dtype=torch.uint8, device="cuda")
+    D.digest_gat_bind_workspace(h, gws)
+    D.digest_pull(h, 0, torch.zeros(10, 3, device="cuda"))
+    e = torch.empty(0, 3, device="cuda")
+    out = torch.empty(0, 4, device="cuda")
+    W = torch.ones(3, 4, device="cuda")
+    att = torch.ones(4, 2, device="cuda")
+    D.digest_gat_forward(h, 1, e, W, att, out, oracle.RELU)
+    dw = torch.full((3, 4), 5.0, device="cuda")
+    datt = torch.full((4, 2), 5.0, device="cuda")
+    D.digest_gat_backward(h, 1, e, out, out, W, att, dw, datt, e)
+    assert np.all(host(dw) == 0) and np.all(host(datt) == 0)
