@@ -183,3 +183,32 @@ def test_empty_row_gives_zero_and_no_gradient():
     # row 1 reads nothing and nobody reads it: its input gradient is zero
     assert not dh[1].any()
     assert np.abs(dh[0]).max() > 0
+
+
+def test_backward_does_not_depend_on_the_thread_count():
+    """Every sum of the GAT backward has one order whatever the thread count:
+    one thread and several give the same bits, on rows longer than one
+    column block of the parallel scatter."""
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1500, widths=(20, 24, 6), classes=6)
+    g = synth.make_graph(cfg, seed=9)
+    p = synth.make_partition(cfg, g, 1)
+    op = oracle.OraclePartition(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                cfg.widths)
+    assert np.diff(op.indptr).max() > 64 and op.n_own + op.n_halo > 4 * 64
+    h, halo = rand((op.n_own, 20), 30), rand((op.n_halo, 20), 31)
+    W, att = rand((20, 24), 32, 0.3), rand((24, 2), 33, 0.5)
+    G = rand((op.n_own, 24), 34)
+    out = oracle.gat_forward(op.indptr, op.col_local, h, halo, W, att, RELU)
+    before = oracle.num_threads()
+    try:
+        results = []
+        for n in (1, 3, max(before, 4)):
+            oracle.set_num_threads(n)
+            results.append(oracle.gat_backward(op.indptr, op.col_local, h, halo, W, att, out,
+                                               G, RELU))
+    finally:
+        oracle.set_num_threads(before)
+    for other in results[1:]:
+        for a, b in zip(results[0], other):
+            np.testing.assert_array_equal(np.asarray(a).view(np.uint32),
+                                          np.asarray(b).view(np.uint32))
