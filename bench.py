@@ -399,6 +399,8 @@ def main():
             if e:   # aggregation kernels: entries of the sparse operand per second
                 entry["gteps"] = e / (entry["avg_us"] * 1e-6) / 1e9
         kernels[key] = entry
+    pp_ms = sum(v["total_ms"] for k, v in kernels.items()
+                if k.startswith(("pull_gather.", "push_scatter."))) / args.steps
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
     d = kernels[dom]
     b_l, f_l, _ = model.get(dom, (0.0, 0.0, 0))
@@ -445,6 +447,12 @@ def main():
             "launch": "eager" if args.eager else "hip-graph replay",
             "pull_push": "overlapped on a second stream" if args.overlap_io else "in line",
         },
+        # the scheduled pulls and pushes of the timed rounds, per round (from
+        # the instrumented pass), and the rate with them taken out of the
+        # round time: edges over the forward and backward alone
+        "pull_push_ms_per_step": round(pp_ms, 5),
+        "gteps_excluding_pull_push": (None if args.overlap_io else
+                                      round(edges / ((ms / args.steps - pp_ms) * 1e-3) / 1e9, 4)),
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
