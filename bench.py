@@ -56,11 +56,25 @@ def loss_group(C):
 
 def splitk(M, N, K):
     """Mirror of the library's split-K plan: (splits, rows per split)."""
-    tiles = -(-M // 64) * -(-N // 64)
-    s = max(1, min(-(-768 // max(tiles, 1)), max(1, K // 256), 256))
-    chunk = -(-K // s)
-    chunk = -(-chunk // 32) * 32 or 32
-    return max(1, -(-K // chunk)), chunk
+    tiles = max(1, -(-M // 64) * -(-N // 64))
+    cap = min(256, max(1, K // 256))
+    lo = max(1, min(-(-768 // tiles), cap))
+
+    def realise(want):
+        chunk = -(-K // want)
+        chunk = -(-chunk // 32) * 32 or 32
+        return max(1, -(-K // chunk)), chunk
+
+    def fill(sp):
+        wg = tiles * sp
+        return wg / (-(-wg // 256) * 256)
+
+    best = realise(lo)
+    for want in range(lo + 1, min(cap, 2 * lo) + 1):
+        cand = realise(want)
+        if fill(cand[0]) > fill(best[0]) + 1e-9:
+            best = cand
+    return best
 
 
 def tf_slices(n, nh, di, do):

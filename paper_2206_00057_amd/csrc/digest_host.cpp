@@ -74,25 +74,46 @@ constexpr int32_t kMaxLayers = 64;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Split-K factor for a contraction with an M x N result over K: about
+// Split-K factor for a contraction with an M x N result over K: at least
 // kSplitTarget workgroups in all, at least kSplitMinRows rows of K per split,
-// split starts on GEMM K-tile boundaries.
+// split starts on GEMM K-tile boundaries.  From that count up to twice it,
+// the split whose workgroups fill whole rounds of the chip's kCUs compute
+// units best is taken (the fewest splits among equals): a round of 800
+// workgroups on 256 CUs leaves most CUs idle for its last quarter.
 constexpr int64_t kSplitTarget = 768;
 constexpr int64_t kSplitMinRows = 256;
+constexpr int64_t kCUs = 256;
 
 void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchunk)
 {
-    const int64_t tiles = ((M + digest::kGemmBM - 1) / digest::kGemmBM) *
-                          ((N + digest::kGemmBN - 1) / digest::kGemmBN);
-    int64_t s = (kSplitTarget + tiles - 1) / std::max<int64_t>(tiles, 1);
-    s = std::max<int64_t>(1, std::min<int64_t>({s, std::max<int64_t>(1, K / kSplitMinRows), 256}));
-    int64_t chunk = (K + s - 1) / s;
-    chunk = (chunk + digest::kGemmBK - 1) / digest::kGemmBK * digest::kGemmBK;
-    if (chunk <= 0)
-        chunk = digest::kGemmBK;
-    s = std::max<int64_t>(1, (K + chunk - 1) / chunk);
-    splits = (int32_t)s;
-    kchunk = (int32_t)chunk;
+    const int64_t tiles = std::max<int64_t>(1, ((M + digest::kGemmBM - 1) / digest::kGemmBM) *
+                                                   ((N + digest::kGemmBN - 1) / digest::kGemmBN));
+    const int64_t cap = std::min<int64_t>(256, std::max<int64_t>(1, K / kSplitMinRows));
+    const int64_t lo = std::max<int64_t>(1, std::min<int64_t>((kSplitTarget + tiles - 1) / tiles, cap));
+    // the split count and K-chunk that a requested count rounds to
+    auto realise = [&](int64_t want, int64_t &chunk) {
+        chunk = (K + want - 1) / want;
+        chunk = (chunk + digest::kGemmBK - 1) / digest::kGemmBK * digest::kGemmBK;
+        if (chunk <= 0)
+            chunk = digest::kGemmBK;
+        return std::max<int64_t>(1, (K + chunk - 1) / chunk);
+    };
+    int64_t best_chunk = 0;
+    int64_t best = realise(lo, best_chunk);
+    auto fill = [&](int64_t sp) {
+        const int64_t wg = tiles * sp;
+        return (double)wg / (double)(((wg + kCUs - 1) / kCUs) * kCUs);
+    };
+    for (int64_t want = lo + 1; want <= std::min<int64_t>(cap, 2 * lo); ++want) {
+        int64_t chunk = 0;
+        const int64_t sp = realise(want, chunk);
+        if (fill(sp) > fill(best) + 1e-9) {
+            best = sp;
+            best_chunk = chunk;
+        }
+    }
+    splits = (int32_t)best;
+    kchunk = (int32_t)best_chunk;
 }
 
 // Workgroup tile of C for a GEMM (see GemmArgs::tile): 64x64 keeps enough
