@@ -8,8 +8,8 @@ Kernel durations (from a ``rocprofv3 --kernel-trace --stats`` run):
 HBM traffic of one kernel, from two counter passes over the same command:
 
     python -m paper_2206_00057_amd.pmc traffic \\
-        --fetch gpurun_out/pmc_fetch/fetch_counter_collection.csv \\
-        --write gpurun_out/pmc_write/write_counter_collection.csv \\
+        --fetch <fetch-dir>/fetch_counter_collection.csv \\
+        --write <write-dir>/write_counter_collection.csv \\
         --kernel-name "k_gemm<64, 64, true, false, false, true" --key gemm_dw_splitk.l1 \\
         --copy-bytes 268435456 --workload medium --out profiles/medium_hbm_traffic.txt
 
