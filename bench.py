@@ -3,16 +3,19 @@
 A step is one round r of Algorithm 1 for the partition: every layer's
 forward (with the pull / push the schedule asks for in that round), the loss
 head, and every layer's backward, all in libdigest.so, replayed from HIP
-graphs with inputs resident in HBM.  Default workload: the Flickr-shaped
-synthetic graph (90,000 nodes in 8 blocks, partition 0, GCN 500 -> 256 -> 7,
-sync interval 10).
+graphs with inputs resident in HBM.  Default workload: the
+OGB-Products-shaped synthetic graph (2,450,000 nodes in 8 blocks,
+partition 0 with 306,250 owned rows, GCN 100 -> 256 -> 256 -> 47, sync
+interval 10), the largest workload that one GPU holds as one partition.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--sync N]
 
 Prints one JSON line: whole-round throughput in GTEPS (aggregation edges of
 the forward and backward per round / time), the roofline of the dominant
 kernel (from a second, instrumented pass with HIP events on the launch
-stream) and the CPU oracle timed on a bounded sample on this host.
+stream; its algorithmic bytes and flops come from the library's own launch
+plan, digest_profile_model) and the CPU oracle timed on a bounded sample on
+this host.
 """
 from __future__ import annotations
 
@@ -21,6 +24,7 @@ import json
 import os
 import sys
 import time
+from types import SimpleNamespace
 
 import numpy as np
 
@@ -31,159 +35,24 @@ METRIC = "GCN layer fwd+bwd GTEPS on one partition; % of HBM / MFMA roofline"
 METRIC_GAT = "GAT layer fwd+bwd GTEPS on one partition; % of HBM / MFMA roofline"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
-
-
-def transform_first(l, widths, st):
-    """Mirror of the library's choice for the identity (last) layer: the
-    cheaper order under its cost model of gathered bytes and GEMM flops."""
-    if l != len(widths) - 1:
-        return False
-    di, do = widths[l - 1], widths[l]
-    n, R, nnz, nnz_in = st["n_own"], st["n_own"] + st["n_halo"], st["nnz"], st["nnz_in"]
-    gather, flops = 7.0e12, 80.0e12
-    dgrad = l > 1
-    af = ((nnz * di + (nnz_in * min(di, do) if dgrad else 0)) * 4.0 / gather
-          + 2.0 * n * di * do * (3.0 if dgrad else 2.0) / flops)
-    tf = (2.0 * nnz * do * 4.0 / gather
-          + (4.0 * R * di * do + (2.0 * n * di * do if dgrad else 0.0)) / flops)
-    return tf < af
-
-
-def loss_group(C):
-    """Mirror of the library's lanes per row of the loss head."""
-    return 8 if C <= 8 else (16 if C <= 64 else (32 if C <= 128 else 64))
-
-
-def splitk(M, N, K):
-    """Mirror of the library's split-K plan: (splits, rows per split)."""
-    tiles = max(1, -(-M // 64) * -(-N // 64))
-    cap = min(256, max(1, K // 256))
-    lo = max(1, min(-(-768 // tiles), cap))
-
-    def realise(want):
-        chunk = -(-K // want)
-        chunk = -(-chunk // 32) * 32 or 32
-        return max(1, -(-K // chunk)), chunk
-
-    def fill(sp):
-        wg = tiles * sp
-        return wg / (-(-wg // 256) * 256)
-
-    best = realise(lo)
-    for want in range(lo + 1, min(cap, 2 * lo) + 1):
-        cand = realise(want)
-        if fill(cand[0]) > fill(best[0]) + 1e-9:
-            best = cand
-    return best
-
-
-def tf_slices(n, nh, di, do):
-    """Mirror of the library's slice plan for the transform-first dW."""
-    if do <= 16:
-        R = n + nh
-        target = max(1, 2048 // -(-di // 64))
-        chunk = max(32, -(-R // target))
-        chunk = -(-chunk // 32) * 32
-        return max(1, -(-R // chunk))
-    return splitk(di, do, n)[0] + (splitk(di, do, nh)[0] if nh else 0)
-
-
-def launch_model_gat(st, widths):
-    """Algorithmic bytes, flops and aggregation entries of one launch of each
-    GAT (kernel kind, layer): every operand row read once, every output
-    written once (R = owned + halo rows)."""
-    n, nh, nnz = st["n_own"], st["n_halo"], st["nnz"]
-    R = n + nh
-    L = len(widths) - 1
-    m = {}
-
-    def put(kind, l, b, f=0.0, e=0):
-        m[f"{kind}.l{l}"] = (float(b), float(f), int(e))
-
-    for l in range(1, L + 1):
-        di, do = widths[l - 1], widths[l]
-        put("gat_transform", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
-        put("gat_scores", l, 4 * (R * do + 2 * do + 2 * R), 4.0 * R * do)
-        put("gat_softmax", l, 4 * (n + 1) + 16 * nnz + 4 * n)
-        put("gat_aggregate", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do, e=nnz)
-        put("gat_edge_grad", l, 4 * (n + 1) + 12 * nnz + 12 * n * do + 4 * R * do + 8 * R + 4 * n,
-            e=nnz)
-        put("gat_transpose_edges", l, 20 * nnz)
-        put("gat_aggregate_transposed", l,
-            4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do + 4 * R + 4 * n + 8 * do, e=nnz)
-        put("gat_score_sums", l, 4 * (R + 1) + 8 * nnz + 4 * n + 4 * R)
-        put("gat_score_grad", l, 8 * R + 4 * nh)
-        put("gat_datt", l, 4 * (R * do + 2 * R + 2 * do), 4.0 * R * do)
-        put("gat_dw", l, 4 * (R * di + R * do + di * do), 2.0 * R * di * do)
-        put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
-        if l > 1:
-            put("gat_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
-    put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
-    put("loss_mean", L, 4 * -(-n // (4 * (64 // loss_group(widths[-1])))) + 4)
-    for lev in range(L):
-        put("pull_gather", lev, 8.0 * nh * widths[lev] + 4 * nh)
-    for lev in range(1, L):
-        put("push_scatter", lev, 8.0 * st["n_boundary"] * widths[lev] + 8 * st["n_boundary"])
-    return m
-
-
-def launch_model(st, widths):
-    """Algorithmic bytes and flops of one launch of each (kernel kind, layer).
-
-    Keys follow the library's instrumentation: "kind.lN" with N the layer
-    (the level for pull/push, L for the loss head).  The layer order
-    (aggregate-first or transform-first) follows the library's rule.
-    """
-    n, nh, nnz, nnz_in, nb = st["n_own"], st["n_halo"], st["nnz"], st["nnz_in"], st["n_boundary"]
-    L = len(widths) - 1
-    m = {}
-
-    def put(kind, l, b, f=0.0, e=0):
-        m[f"{kind}.l{l}"] = (float(b), float(f), int(e))
-
-    for l in range(1, L + 1):
-        di, do = widths[l - 1], widths[l]
-        relu = l < L
-        if transform_first(l, widths, st):
-            R = n + nh
-            put("gemm_fwd_relu", l, 4 * (R * di + di * do + R * do), 2.0 * R * di * do)
-            put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * R * do + 4 * n * do, e=nnz)
-            fused = l > 1 and do <= 16 and di <= 1024 and di % 4 == 0
-            put("spmm_bwd_transposed", l, 4 * (R + 1) + 8 * nnz + 4 * n * do + 4 * R * do
-                + (4 * (n * di + di * do) if fused else 0), e=nnz)
-            put("gemm_dw_splitk", l, 4 * (R * di + R * do), 2.0 * R * di * do)
-            put("splitk_reduce_dw", l, 4 * (tf_slices(n, nh, di, do) + 1) * di * do)
-            if l > 1 and not fused:
-                put("gemm_dgrad", l, 4 * (n * do + di * do + n * di), 2.0 * n * di * do)
-            continue
-        put("spmm_fwd", l, 4 * (n + 1) + 8 * nnz + 4 * (n + nh) * di + 4 * n * di, e=nnz)
-        put("gemm_fwd_relu", l, 4 * (n * di + di * do + n * do), 2.0 * n * di * do)
-        put("gemm_dw_splitk", l, 4 * (n * di + n * do * (2 if relu else 1) + di * do),
-            2.0 * n * di * do)
-        s = splitk(di, do, n)[0]
-        if s > 1:
-            put("splitk_reduce_dw", l, 4 * (s + 1) * di * do)
-        if l > 1:
-            narrow = (not relu) and do < di
-            w = do if narrow else di
-            put("spmm_bwd_transposed", l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w, e=nnz_in)
-            put("gemm_dgrad", l, 4 * (n * do * (1 if narrow or not relu else 2) + di * do + n * di),
-                2.0 * n * di * do)
-    put("softmax_xent", L, 4 * (2 * n * widths[-1] + n))
-    put("loss_mean", L, 4 * -(-n // (4 * (64 // loss_group(widths[-1])))) + 4)
-    for lev in range(L):
-        put("pull_gather", lev, 8.0 * nh * widths[lev] + 4 * nh)
-    for lev in range(1, L):
-        put("push_scatter", lev, 8.0 * nb * widths[lev] + 8 * nb)
-    return m
+# Edges of the single-thread oracle sample per round (a leading block of the
+# partition's rows), so that one sampled round takes a few seconds.
+CPU_SAMPLE_EDGES = 2_000_000
+# Edges per round above which the all-core oracle leg also runs on a row
+# sample (a whole round of the largest partitions takes minutes on a host).
+CPU_FULL_ROUND_EDGES = 100_000_000
 
 
 def measured_traffic(workload, key):
-    """HBM bytes per launch of `key` from the committed counter summary, or
-    None when there is none for this kernel or the kernels changed since."""
-    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.txt")
+    """(bytes per launch, source) of `key` from the committed counter
+    summary: L2-to-fabric bytes (rocprofv3 FETCH_SIZE + WRITE_SIZE, each
+    scaled by a plain copy kernel of known size; Infinity Cache hits are
+    included, so this is not HBM traffic alone).  (None, reason) when there
+    is no summary for this kernel or the kernel sources changed since."""
+    rel = os.path.join("profiles", f"{workload}_hbm_traffic.txt")
+    path = os.path.join(ROOT, rel)
     if not os.path.exists(path):
-        return None
+        return None, f"no counter summary for {workload}"
     kv = {}
     for line in open(path):
         line = line.split("#", 1)[0].strip()
@@ -191,23 +60,57 @@ def measured_traffic(workload, key):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     from paper_2206_00057_amd.pmc import kernel_source_hash
-    if kv.get("kernel") != key or kv.get("source_sha") != kernel_source_hash():
-        return None
-    return float(kv["traffic_bytes_per_launch"])
+    if kv.get("kernel") != key:
+        return None, f"{rel} covers {kv.get('kernel')}, not {key}"
+    sha = kernel_source_hash()
+    if kv.get("source_sha") != sha:
+        return None, f"{rel} was taken on kernel sources {kv.get('source_sha')}, now {sha}"
+    return (float(kv["traffic_bytes_per_launch"]),
+            f"{rel}: rocprofv3 FETCH_SIZE+WRITE_SIZE (L2-fabric bytes, Infinity Cache hits "
+            f"included), kernel sources {sha}")
 
 
-def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s, atts=None):
-    """The oracle as it stands, timed on this host's cores on whole rounds
-    (GCN layers, or GAT layers when atts are given)."""
+def row_sample(part, rows):
+    """The first `rows` owned rows of a partition as a partition of their
+    own: the same CSR rows, every column that is not one of those rows
+    becoming a halo node (ascending id)."""
+    rows = min(int(rows), int(part.n_own))
+    indptr = np.ascontiguousarray(part.indptr[:rows + 1])
+    nnz = int(indptr[-1])
+    indices = np.ascontiguousarray(part.indices[:nnz])
+    owned = np.ascontiguousarray(part.owned[:rows])
+    halo = np.setdiff1d(np.unique(indices), owned)
+    return SimpleNamespace(indptr=indptr, indices=indices,
+                           values=np.ascontiguousarray(part.values[:nnz]), owned=owned,
+                           halo=halo, n_own=rows, n_halo=int(halo.shape[0]),
+                           nnz_in=int(np.isin(indices, owned).sum()), nnz=nnz)
+
+
+def round_edges(part, L, gat):
+    """Aggregation edges of one round: GCN forward nnz per layer plus the
+    transposed backward's nnz_in for layers >= 2; GAT 2 nnz per layer."""
+    return 2 * L * part.nnz if gat else L * part.nnz + (L - 1) * part.nnz_in
+
+
+def cpu_rounds(cfg, g, part, X, Ws, y, K, budget_s, atts=None):
+    """The oracle as it stands, timed on whole rounds of `part` (GCN layers,
+    or GAT layers when atts are given) until budget_s has passed (at least
+    one round).  Returns (rounds, seconds, threads)."""
     import oracle
     L = cfg.layers
     op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values, part.owned,
                                 part.halo, cfg.widths)
-    stores = [X] + [np.maximum(np.random.default_rng(70 + l).standard_normal(
-        (g.n, cfg.widths[l]), dtype=np.float32), 0) for l in range(1, L)]
+    # stale store levels: synthetic values on the rows this partition pulls
+    stores = [X]
+    for l in range(1, L):
+        st = np.zeros((g.n, cfg.widths[l]), np.float32)
+        st[part.halo] = np.maximum(np.random.default_rng(70 + l).standard_normal(
+            (part.halo.shape[0], cfg.widths[l]), dtype=np.float32), 0)
+        stores.append(st)
     for lev in range(L):
         op.pull(lev, stores[lev])
     x = X[part.owned]
+    y = y[:part.n_own]
     t0 = time.perf_counter()
     rounds = 0
     while True:
@@ -237,6 +140,65 @@ def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s, atts=None):
         if time.perf_counter() - t0 >= budget_s:
             break
     return rounds, time.perf_counter() - t0, oracle.num_threads()
+
+
+def cpu_baseline(cfg, g, part, X, Ws, y, K, budget_s, atts=None):
+    """The oracle on this host's cores: whole rounds of the partition on
+    every thread (of a leading row sample when a round is too large to time
+    in seconds), and a smaller leading row sample on one thread."""
+    import oracle
+    gat = atts is not None
+    L = cfg.layers
+    full = SimpleNamespace(**{k: getattr(part, k) for k in
+                              ("indptr", "indices", "values", "owned", "halo", "n_own",
+                               "n_halo")}, nnz=int(part.indptr[-1]),
+                           nnz_in=int(np.isin(part.indices, part.owned).sum()))
+    e_full = round_edges(full, L, gat)
+
+    def leg(target_edges, budget):
+        if e_full <= target_edges:
+            smp, what = full, f"whole rounds of the partition ({full.n_own:,} rows)"
+        else:
+            rows = max(1, int(full.n_own * target_edges / e_full))
+            smp = row_sample(full, rows)
+            what = (f"whole rounds of its first {smp.n_own:,} owned rows as a partition "
+                    f"({smp.n_halo:,} halo rows)")
+        nr, secs, thr = cpu_rounds(cfg, g, smp, X, Ws, y, K, budget, atts)
+        e = round_edges(smp, L, gat)
+        return {"value": e * nr / secs / 1e9, "unit": "GTEPS", "cores": thr, "kind": "oracle",
+                "sample": f"{nr} x {e:,} edges: {what}, {secs:.1f}s, float64 oracle, "
+                          f"{thr} thread{'s' if thr != 1 else ''}"}
+
+    out = leg(CPU_FULL_ROUND_EDGES, budget_s)
+    threads = out["cores"]
+    oracle.set_num_threads(1)
+    try:
+        one = leg(CPU_SAMPLE_EDGES, budget_s / 2)
+    finally:
+        oracle.set_num_threads(threads)
+    out["single_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
+    return out
+
+
+# What each synthetic workload stands in for (the datasets of the paper's
+# experiments, Table 3 of the appendix).
+WORKLOADS = {
+    "tiny": "small block graph",
+    "medium": "Flickr-shaped graph",
+    "dense": "Reddit-shaped graph",
+    "large": "OGB-Products-shaped graph",
+    "halo": "OGB-Products-shaped graph, random 1/16 partition",
+}
+
+
+def workload_name(cfg, K, model, n, st):
+    """Workload key and sync interval first, then the shape; under 120
+    characters."""
+    parts = "16" if cfg.partition == "perm" else str(cfg.blocks)
+    head = f"{cfg.name}, K={K}: {WORKLOADS[cfg.name]}, N={n:,}, part 0 of {parts}"
+    tail = f"{model.upper()} {'-'.join(map(str, cfg.widths))}"
+    full = f"{head} ({st['n_own']:,} own, {st['n_halo']:,} halo), {tail}"
+    return full if len(full) < 120 else f"{head}, {tail}"[:119]
 
 
 def train_bench(args):
@@ -281,10 +243,10 @@ def train_bench(args):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms / args.steps, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: all {M} subgraphs, {args.model.upper()}, "
-                               f"Algorithm 1 rounds with "
-                               f"sync interval {K}, SGD lr {args.lr}, halo-gradient "
+        "config": {"workload": f"{cfg.name}, K={K}, all {M} subgraphs: {WORKLOADS[cfg.name]}, "
+                               f"{args.model.upper()} {'-'.join(map(str, cfg.widths))}, "
                                f"exchange {args.grad_exchange}",
+                   "lr": args.lr,
                    "n_global": g.n, "subgraphs": M, "widths": list(cfg.widths),
                    "edges_per_round": tr.edges_per_round, "launch": "hip-graph replay"},
         "loss": {"after_warmup": round(first_loss, 6), "last": round(tr.mean_loss(), 6)},
@@ -295,9 +257,9 @@ def train_bench(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="medium")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="large", choices=tuple(WORKLOADS))
     ap.add_argument("--sync", type=int, default=0, help="sync interval (default: the workload's)")
     ap.add_argument("--eager", action="store_true", help="launch eagerly instead of graph replay")
     ap.add_argument("--overlap-io", action="store_true",
@@ -401,7 +363,8 @@ def main():
         gp.round(r, K, x_own, dWs, stores, dy)
     prof = D.digest_profile_read(gp.p)
     D.digest_profile_enable(gp.p, False)
-    model = launch_model_gat(st, cfg.widths) if gat else launch_model(st, cfg.widths)
+    # algorithmic bytes / flops / entries of each launch, from the library's plan
+    model = D.digest_profile_model(gp.p, D.MODEL_GAT if gat else D.MODEL_GCN)
     kernels = {}
     for key, (tot_ms, n_l) in prof.items():
         entry = {"launches": n_l, "avg_us": 1e3 * tot_ms / n_l, "total_ms": tot_ms}
@@ -424,24 +387,18 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(d["gbs"] / HBM_PEAK_GBS, 4)}
-    roof.update({"traffic": measured_traffic(cfg.name, dom), "kernel": dom,
+    traffic, traffic_source = measured_traffic(cfg.name, dom)
+    roof.update({"traffic": traffic, "traffic_source": traffic_source, "kernel": dom,
                  "algorithmic_bytes_per_launch": b_l, "algorithmic_flops_per_launch": f_l,
-                 "avg_launch_us": round(d["avg_us"], 3)})
+                 "avg_launch_us": round(d["avg_us"], 3),
+                 "achieved_basis": "algorithmic (compulsory) bytes or flops of one launch / "
+                                   "its mean HIP-event duration on the launch stream"})
 
     cpu = None
     if not args.no_cpu:
-        import oracle
-        nr, secs, cores = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds, atts)
-        cpu = {"value": edges * nr / secs / 1e9, "unit": "GTEPS", "cores": cores, "kind": "oracle",
-               "sample": f"{nr} whole rounds of the same partition (forward, loss, backward, "
-                         f"scheduled pull/push) in {secs:.1f}s, float64 oracle, {cores} threads"}
-        # the same oracle on one thread, beside the all-core figure
-        oracle.set_num_threads(1)
-        nr1, secs1, _ = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds / 2, atts)
-        oracle.set_num_threads(cores)
-        cpu["single_thread"] = {
-            "value": edges * nr1 / secs1 / 1e9, "unit": "GTEPS", "cores": 1,
-            "sample": f"{nr1} whole rounds in {secs1:.1f}s, float64 oracle, 1 thread"}
+        t_cpu = time.time()
+        cpu = cpu_baseline(cfg, g, part, X, Ws, y, K, args.cpu_seconds, atts)
+        print(f"[bench] cpu baseline {time.time() - t_cpu:.1f}s", file=sys.stderr, flush=True)
 
     out = {
         "metric": METRIC_GAT if gat else METRIC, "value": round(value, 4), "unit": "GTEPS",
@@ -451,10 +408,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": (f"{cfg.name}: synthetic block graph, N={g.n:,}, partition 0 "
-                         f"({st['n_own']:,} owned + {st['n_halo']:,} halo rows), "
-                         f"{args.model.upper()} {'->'.join(map(str, cfg.widths))}, "
-                         f"sync interval {K}"),
+            "workload": workload_name(cfg, K, args.model, g.n, st),
             "n_global": g.n, "n_own": st["n_own"], "n_halo": st["n_halo"],
             "n_boundary": st["n_boundary"], "nnz": st["nnz"], "nnz_in": st["nnz_in"],
             "widths": list(cfg.widths), "sync_interval": K, "edges_per_step": edges,

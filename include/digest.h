@@ -103,7 +103,9 @@ digest_status digest_partition_query(const digest_partition *p, int64_t *n_bound
  * hip_stream.  The library owns the layout of this memory (local CSR,
  * P_in^T, id lists, one halo buffer per level, the aggregated input AH of
  * each layer kept for the backward, reduction scratch) until the next bind
- * or destroy.  Re-binding resets the pull/forward state.
+ * or destroy.  Re-binding resets the pull/forward state: every level must
+ * be pulled again, and every backward (GCN or GAT) needs a forward after
+ * the bind.
  * Errors: DIGEST_EINVAL (NULL, misaligned), DIGEST_ENOMEM (too small),
  * DIGEST_EHIP.
  */
@@ -144,8 +146,15 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
  * Push (Sec. 3.2; Algorithm 1 pushes when (r-1) mod N == 0): write freshly
  * computed own rows of level `level` into the store:
  *   store[owned[b], :] = h_own[b, :]  for b in the boundary rows
- *   (mode DIGEST_PUSH_BOUNDARY, the only rows another partition reads), or
- *   for every owned row (mode DIGEST_PUSH_ALL_OWNED, the paper's wording).
+ *   (mode DIGEST_PUSH_BOUNDARY), or for every owned row (mode
+ *   DIGEST_PUSH_ALL_OWNED, the paper's wording).
+ * The boundary rows are the owned rows with a halo column.  They are the
+ * only rows other partitions read when P is structurally symmetric (an
+ * edge u -> v implies v -> u, as for the GCN normalisation of an
+ * undirected graph): a node in another partition's halo then has that
+ * partition's node among its own columns.  For a directed P use
+ * DIGEST_PUSH_ALL_OWNED, or rows some other partition reads may never be
+ * written.
  * Other store rows are untouched.
  *   level  1..L-1 (the stale levels; level 0 is static, level L is never
  *          stored).   h_own  device [n_owned, d_level].
@@ -376,6 +385,68 @@ digest_status digest_profile_enable(digest_partition *p, int32_t on);
 digest_status digest_profile_read(digest_partition *p, double *total_ms, int64_t *launches);
 int32_t digest_profile_kernel_count(void);
 const char *digest_profile_kernel_name(int32_t kind);
+
+/*
+ * Launch plan of one layer as the library runs it (host only; a pure
+ * function of the partition's sizes and widths), for tests and measurement.
+ * The two products of Eq. 5 associate either way; the plan records which
+ * order and which kernels the layer calls use.
+ *   transform_first     1: an identity layer runs as P_m ([h_in; halo] W)
+ *                       (forward) with G = P_m^T D over every local row
+ *                       (backward); 0: (P_m [h_in; halo]) W with AH kept.
+ *   forward_narrow      1: the product with W runs on the narrow-output
+ *                       kernel (W held in LDS); 0: the MFMA GEMM.
+ *   dw_slices           split-K slices of the weight gradient, summed in
+ *                       slice order (1: no split).
+ *   dgrad_narrow_first  aggregate-first layers: 1 if the input gradient is
+ *                       (P_in^T D) W^T (aggregated at width d_layer), 0 if
+ *                       P_in^T (D W^T).
+ *   dgrad_fused         transform-first layers: 1 if dh_in = G_own W^T is
+ *                       formed in the epilogue of the transposed
+ *                       aggregation (when the caller asks for dh_in).
+ *   hot_rows_fwd, hot_rows_bwd  source rows whose gathers the forward
+ *                       (P_m) / transposed (P_in^T) aggregation of this
+ *                       layer runs in a pass of their own, sliced over
+ *                       the feature columns so that each slice of these
+ *                       rows stays in one L2 (0: a single pass).
+ *   hot_entries_fwd, hot_entries_bwd  entries of the sparse operand that
+ *                       those passes take.
+ * Errors: DIGEST_EINVAL (NULL, layer outside 1..L).
+ */
+typedef struct {
+    int32_t transform_first;
+    int32_t forward_narrow;
+    int32_t dw_slices;
+    int32_t dgrad_narrow_first;
+    int32_t dgrad_fused;
+    int32_t hot_rows_fwd;
+    int32_t hot_rows_bwd;
+    int64_t hot_entries_fwd;
+    int64_t hot_entries_bwd;
+} digest_layer_plan;
+
+digest_status digest_partition_plan(const digest_partition *p, int32_t layer,
+                                    digest_layer_plan *out);
+
+/*
+ * Algorithmic cost of one launch of each instrumented (kernel kind, slot),
+ * indexed like digest_profile_read, for the launches that one round of the
+ * GCN layers (model DIGEST_MODEL_GCN: every forward with act ReLU below
+ * layer L and identity at L, the loss head, every backward with dh_in for
+ * layers >= 2, the pulls of levels 0..L-1 and pushes of levels 1..L-1) or
+ * of the GAT layers (DIGEST_MODEL_GAT) makes under the plan above:
+ *   bytes    the bytes that must move if every operand is read once and
+ *            every output written once (the compulsory traffic: a source
+ *            row of an aggregation counts once however many entries read it);
+ *   flops    floating-point operations of the dense products (0 otherwise);
+ *   entries  entries of the sparse operand of an aggregation (0 otherwise).
+ * Each array holds digest_profile_kernel_count() * (L + 1) entries; kinds
+ * the round does not launch are 0.
+ * Errors: DIGEST_EINVAL (NULL, unknown model).
+ */
+enum { DIGEST_MODEL_GCN = 0, DIGEST_MODEL_GAT = 1 };
+digest_status digest_profile_model(const digest_partition *p, int32_t model, double *bytes,
+                                   double *flops, int64_t *entries);
 
 #ifdef __cplusplus
 }

@@ -184,7 +184,7 @@ struct digest_partition {
 
     char *ws = nullptr;
     std::vector<char> pulled;       // per level
-    std::vector<int64_t> pull_gen;  // per level: number of pulls since bind
+    std::vector<int64_t> pull_gen;  // per level: number of pulls since create
     std::vector<char> fwd_done;     // per layer
     std::vector<int32_t> act;       // per layer
     std::vector<char> tf;           // per layer: forward ran transform-first
@@ -755,9 +755,13 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
             return st;
     }
     p->ws = ws;
+    // The halo buffers and AH of the old workspace are gone: no level counts
+    // as pulled and no forward (GCN or GAT) as done.  Pull generations keep
+    // counting across binds, so a forward recorded before the bind can never
+    // match a later pull count.
     std::fill(p->pulled.begin(), p->pulled.end(), 0);
-    std::fill(p->pull_gen.begin(), p->pull_gen.end(), 0);
     std::fill(p->fwd_done.begin(), p->fwd_done.end(), 0);
+    std::fill(p->gat_done.begin(), p->gat_done.end(), 0);
     return DIGEST_OK;
 }
 
@@ -1097,6 +1101,10 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
                 "dW reduce"))
             return st;
     }
+    if (p->n_own == 0 && dh_halo)
+        // no owned row reads a halo row: the halo gradient is zero
+        return hip_check(digest::launch_fill_zero(dh_halo, (int64_t)p->n_halo * d_in, s),
+                         "zero halo gradient");
     if (!dh_in || p->n_own == 0)
         return DIGEST_OK;
 
@@ -1387,7 +1395,7 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
         return fail(DIGEST_EINVAL, "unknown activation %d", act);
     if (!(negative_slope >= 0.f && negative_slope <= 1.f))
         return fail(DIGEST_EINVAL, "negative slope must be in [0, 1]");
-    const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
+    const int32_t d_out = p->widths[layer];
     if (d_out > digest::kGatMaxWidth)
         return fail(DIGEST_EINVAL, "GAT layer width %d above %d", d_out, digest::kGatMaxWidth);
     if (!w || !att || (p->n_own > 0 && (!h_in || !h_out)))
@@ -1590,6 +1598,131 @@ int32_t digest_profile_kernel_count(void) { return K_COUNT; }
 const char *digest_profile_kernel_name(int32_t kind)
 {
     return (kind >= 0 && kind < K_COUNT) ? kKindNames[kind] : "";
+}
+
+}  // extern "C"
+
+namespace {
+
+// The plan of one layer (see digest_layer_plan).  Device pointers are
+// assumed 16-byte aligned, as the layer calls' callers pass them.
+digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
+{
+    digest_layer_plan pl{};
+    const int32_t d_in = p.widths[layer - 1], d_out = p.widths[layer];
+    const bool relu = layer < p.L;
+    pl.transform_first = !relu && p.n_own > 0 && transform_first_cheaper(p, layer);
+    pl.forward_narrow = narrow_out(d_in, d_out);
+    if (pl.transform_first) {
+        pl.dw_slices = tf_plan(p.n_own, p.n_halo, d_in, d_out).slices;
+        pl.dgrad_fused = layer > 1 && narrow_valu(d_in, d_out) &&
+                         digest::spmm_epilogue_ok(d_out, d_in, nullptr);
+    } else {
+        int32_t splits = 1, kchunk = 0;
+        splitk_plan(d_in, d_out, p.n_own, splits, kchunk);
+        pl.dw_slices = splits;
+        pl.dgrad_narrow_first = !relu && d_out < d_in;
+    }
+    return pl;
+}
+
+}  // namespace
+
+extern "C" {
+
+digest_status digest_partition_plan(const digest_partition *p, int32_t layer,
+                                    digest_layer_plan *out)
+{
+    if (!p || !out)
+        return fail(DIGEST_EINVAL, "NULL handle or output");
+    if (layer < 1 || layer > p->L)
+        return fail(DIGEST_EINVAL, "layer %d outside [1, %d]", layer, p->L);
+    *out = layer_plan(*p, layer);
+    return DIGEST_OK;
+}
+
+digest_status digest_profile_model(const digest_partition *p, int32_t model, double *bytes,
+                                   double *flops, int64_t *entries)
+{
+    if (!p || !bytes || !flops || !entries)
+        return fail(DIGEST_EINVAL, "NULL argument");
+    if (model != DIGEST_MODEL_GCN && model != DIGEST_MODEL_GAT)
+        return fail(DIGEST_EINVAL, "unknown model %d", model);
+    const int32_t slots = p->L + 1;
+    for (int32_t k = 0; k < K_COUNT * slots; ++k) {
+        bytes[k] = 0.0;
+        flops[k] = 0.0;
+        entries[k] = 0;
+    }
+    auto put = [&](int32_t kind, int32_t slot, double b, double f = 0.0, int64_t e = 0) {
+        bytes[kind * slots + slot] = b;
+        flops[kind * slots + slot] = f;
+        entries[kind * slots + slot] = e;
+    };
+    const double n = p->n_own, nh = p->n_halo, nb = p->n_bnd, R = n + nh;
+    const double nnz = (double)p->nnz, nnz_in = (double)p->nnz_in;
+    const int32_t L = p->L;
+    for (int32_t l = 1; l <= L; ++l) {
+        const double di = p->widths[l - 1], dout = p->widths[l];
+        const bool relu = l < L;
+        if (model == DIGEST_MODEL_GAT) {
+            const TfPlan t = tf_plan(p->n_own, p->n_halo, p->widths[l - 1], p->widths[l]);
+            put(K_GAT_TRANSFORM, l, 4 * (R * di + di * dout + R * dout), 2 * R * di * dout);
+            put(K_GAT_SCORES, l, 4 * (R * dout + 2 * dout + 2 * R), 4 * R * dout);
+            put(K_GAT_SOFTMAX, l, 4 * (n + 1) + 16 * nnz + 4 * n);
+            put(K_GAT_AGG, l, 4 * (n + 1) + 8 * nnz + 4 * R * dout + 4 * n * dout, 0.0, p->nnz);
+            put(K_GAT_EDGE_GRAD, l,
+                4 * (n + 1) + 12 * nnz + 12 * n * dout + 4 * R * dout + 8 * R + 4 * n, 0.0,
+                p->nnz);
+            put(K_GAT_PERM, l, 20 * nnz);
+            put(K_GAT_AGG_T, l,
+                4 * (R + 1) + 8 * nnz + 4 * n * dout + 4 * R * dout + 4 * R + 4 * n + 8 * dout,
+                0.0, p->nnz);
+            put(K_GAT_SCORE_SUMS, l, 4 * (R + 1) + 8 * nnz + 4 * n + 4 * R);
+            put(K_GAT_SCORE_GRAD, l, 8 * R + 4 * nh);
+            put(K_GAT_DATT, l, 4 * (R * dout + 2 * R + 2 * dout), 4 * R * dout);
+            put(K_GAT_DW, l, 4 * (R * di + R * dout + di * dout), 2 * R * di * dout);
+            put(K_REDUCE_DW, l, 4 * (t.slices + 1) * di * dout);
+            if (l > 1)
+                put(K_GAT_DGRAD, l, 4 * (n * dout + di * dout + n * di), 2 * n * di * dout);
+            continue;
+        }
+        const digest_layer_plan pl = layer_plan(*p, l);
+        if (pl.transform_first) {
+            put(K_GEMM_FWD, l, 4 * (R * di + di * dout + R * dout), 2 * R * di * dout);
+            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * dout + 4 * n * dout, 0.0, p->nnz);
+            put(K_SPMM_BWD, l,
+                4 * (R + 1) + 8 * nnz + 4 * n * dout + 4 * R * dout +
+                    (pl.dgrad_fused ? 4 * (n * di + di * dout) : 0.0),
+                0.0, p->nnz);
+            put(K_GEMM_DW, l, 4 * (R * di + R * dout + di * dout), 2 * R * di * dout);
+            put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);
+            if (l > 1 && !pl.dgrad_fused)
+                put(K_GEMM_DH, l, 4 * (n * dout + di * dout + n * di), 2 * n * di * dout);
+            continue;
+        }
+        put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * di + 4 * n * di, 0.0, p->nnz);
+        put(K_GEMM_FWD, l, 4 * (n * di + di * dout + n * dout), 2 * n * di * dout);
+        put(K_GEMM_DW, l, 4 * (n * di + n * dout * (relu ? 2 : 1) + di * dout),
+            2 * n * di * dout);
+        if (pl.dw_slices > 1)
+            put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);
+        if (l > 1) {
+            const double w = pl.dgrad_narrow_first ? dout : di;
+            put(K_SPMM_BWD, l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w, 0.0, p->nnz_in);
+            put(K_GEMM_DH, l,
+                4 * (n * dout * ((pl.dgrad_narrow_first || !relu) ? 1 : 2) + di * dout + n * di),
+                2 * n * di * dout);
+        }
+    }
+    const double C = p->widths[L];
+    put(K_LOSS, L, 4 * (2 * n * C + n));
+    put(K_LOSS_MEAN, L, 4.0 * digest::softmax_xent_blocks(p->n_own, p->widths[L]) + 4);
+    for (int32_t lev = 0; lev < L; ++lev)
+        put(K_PULL, lev, 8 * nh * p->widths[lev] + 4 * nh);
+    for (int32_t lev = 1; lev < L; ++lev)
+        put(K_PUSH, lev, 8 * nb * p->widths[lev] + 8 * nb);
+    return DIGEST_OK;
 }
 
 }  // extern "C"

@@ -1569,6 +1569,15 @@ __global__ __launch_bounds__(256) void k_sgd_average(float *__restrict__ w, Grad
     w[e] = w[e] - lr * (sum / (float)n);
 }
 
+// p[e] = 0 for e < count, a thread per element (a kernel rather than a
+// memset, so that it records as a kernel node under graph capture).
+__global__ __launch_bounds__(256) void k_fill_zero(float *__restrict__ p, int64_t count)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < count)
+        p[e] = 0.f;
+}
+
 // ---------------------------------------------------------------------------
 // dispatch helpers
 // ---------------------------------------------------------------------------
@@ -2125,6 +2134,17 @@ hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t co
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(k_sgd_average, dim3((unsigned)blocks), dim3(256), 0, s, w, g, n, count, lr);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float *p, int64_t count, hipStream_t s)
+{
+    if (count <= 0)
+        return hipSuccess;
+    const int64_t blocks = (count + 255) / 256;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, p, count);
     return hipGetLastError();
 }
 

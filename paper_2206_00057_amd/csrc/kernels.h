@@ -152,6 +152,9 @@ struct GradList {
 hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t count, float lr,
                               hipStream_t s);
 
+// p[0 .. count) = 0.
+hipError_t launch_fill_zero(float *p, int64_t count, hipStream_t s);
+
 // GAT layer (attention aggregation over stale halo rows).  s is [rows][2]
 // (source score, target score); alpha, dpre are in CSR entry order.
 constexpr int kGatMaxWidth = 512;

@@ -14,9 +14,12 @@ import os
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libdigest.so")
+# DIGEST_LIBRARY names another build of the same ABI (e.g. the host-only
+# sanitizer build); by default the in-tree libdigest.so.
+LIB_PATH = os.environ.get("DIGEST_LIBRARY") or os.path.join(_PKG, "libdigest.so")
 
 OK, EINVAL, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4
+MODEL_GCN, MODEL_GAT = 0, 1
 ACT_RELU, ACT_IDENTITY = 0, 1
 PUSH_BOUNDARY, PUSH_ALL_OWNED = 0, 1
 
@@ -67,6 +70,8 @@ def lib():
             "digest_profile_read": ([P, P, P], st),
             "digest_profile_kernel_count": ([], i32),
             "digest_profile_kernel_name": ([i32], ctypes.c_char_p),
+            "digest_partition_plan": ([P, i32, P], st),
+            "digest_profile_model": ([P, i32, P, P, P], st),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -405,4 +410,42 @@ def digest_profile_read(p):
             j = i * slots + sl
             if cnt[j]:
                 out[f"{name}.l{sl}"] = (float(ms[j]), int(cnt[j]))
+    return out
+
+
+class LayerPlan(ctypes.Structure):
+    """``digest_layer_plan`` of include/digest.h."""
+    _fields_ = [("transform_first", ctypes.c_int32), ("forward_narrow", ctypes.c_int32),
+                ("dw_slices", ctypes.c_int32), ("dgrad_narrow_first", ctypes.c_int32),
+                ("dgrad_fused", ctypes.c_int32), ("hot_rows_fwd", ctypes.c_int32),
+                ("hot_rows_bwd", ctypes.c_int32), ("hot_entries_fwd", ctypes.c_int64),
+                ("hot_entries_bwd", ctypes.c_int64)]
+
+
+def digest_partition_plan(p, layer):
+    """The library's launch plan of ``layer`` as a dict of the C fields."""
+    _check_layer(p, layer)
+    out = LayerPlan()
+    _check(lib().digest_partition_plan(p.handle, int(layer), ctypes.byref(out)))
+    return {name: int(getattr(out, name)) for name, _ in LayerPlan._fields_}
+
+
+def digest_profile_model(p, model=MODEL_GCN):
+    """Algorithmic (bytes, flops, sparse entries) of one launch of each
+    (kernel kind, slot) a round makes, keyed like ``digest_profile_read``;
+    kinds the round does not launch are omitted."""
+    n = lib().digest_profile_kernel_count()
+    slots = p.L + 1
+    b = np.zeros(n * slots, np.float64)
+    f = np.zeros(n * slots, np.float64)
+    e = np.zeros(n * slots, np.int64)
+    _check(lib().digest_profile_model(p.handle, int(model), b.ctypes.data_as(ctypes.c_void_p),
+                                      f.ctypes.data_as(ctypes.c_void_p),
+                                      e.ctypes.data_as(ctypes.c_void_p)))
+    out = {}
+    for i, name in enumerate(kernel_names()):
+        for sl in range(slots):
+            j = i * slots + sl
+            if b[j] or f[j] or e[j]:
+                out[f"{name}.l{sl}"] = (float(b[j]), float(f[j]), int(e[j]))
     return out

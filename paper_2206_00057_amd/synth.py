@@ -221,6 +221,38 @@ def make_partition(cfg: GraphConfig, g: Graph, part: int = 0) -> Partition:
     return extract_partition(g, owned_nodes(cfg, part))
 
 
+def scramble_rows(p: Partition, seed: int, repeat_frac: float = 0.25,
+                  long_row: int = 0) -> Partition:
+    """The same partition with every CSR row's entries in a seeded random
+    order and about repeat_frac of them repeated (each repeat carries a
+    fresh weight; repeated (row, column) entries of a CSR are summed).  With
+    long_row > 0 the longest row also gets repeats of its own entries until
+    it holds at least long_row of them.  Owned and halo lists are unchanged
+    (no new column appears)."""
+    rng = np.random.default_rng(seed)
+    rows = np.diff(p.indptr)
+    longest = int(np.argmax(rows)) if rows.size else -1
+    cols, vals, counts = [], [], []
+    for i in range(p.n_own):
+        kb, ke = int(p.indptr[i]), int(p.indptr[i + 1])
+        c, v = p.indices[kb:ke], p.values[kb:ke]
+        rep = np.flatnonzero(rng.random(ke - kb) < repeat_frac)
+        if i == longest and long_row > 0 and ke > kb:
+            extra = max(0, long_row - (ke - kb) - rep.size)
+            rep = np.concatenate([rep, rng.integers(0, ke - kb, size=extra)])
+        c = np.concatenate([c, c[rep]])
+        v = np.concatenate([v, (v[rep] * rng.uniform(0.5, 1.5, rep.size)).astype(np.float32)])
+        order = rng.permutation(c.size)
+        cols.append(c[order])
+        vals.append(v[order])
+        counts.append(c.size)
+    indptr = np.zeros(p.n_own + 1, np.int64)
+    np.cumsum(counts, out=indptr[1:])
+    cat = lambda a, t: np.concatenate(a).astype(t) if a else np.zeros(0, t)
+    return Partition(p.owned.copy(), p.halo.copy(), indptr, cat(cols, np.int64),
+                     cat(vals, np.float32))
+
+
 def features(cfg: GraphConfig, seed: int = 2) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return rng.standard_normal((cfg.n, cfg.widths[0]), dtype=np.float32)

@@ -44,6 +44,19 @@ from . import digest as D
 from .step import GpuPartition
 
 
+def boundary_push_mode(gps, parts):
+    """DIGEST_PUSH_BOUNDARY when every halo node of every subgraph is a
+    boundary row of its owner (so pushing boundary rows writes every row
+    anyone pulls; this holds when the graph is structurally symmetric),
+    else DIGEST_PUSH_ALL_OWNED, the paper's push of every owned row."""
+    import numpy as np
+    pushed = np.concatenate([D.digest_partition_export_maps(gp.p)[1] for gp in gps] +
+                            [np.zeros(0, np.int64)])
+    pulled = np.concatenate([np.asarray(p.halo, np.int64) for p in parts] +
+                            [np.zeros(0, np.int64)])
+    return D.PUSH_BOUNDARY if np.isin(pulled, pushed).all() else D.PUSH_ALL_OWNED
+
+
 class DigestTrainer:
     def __init__(self, n_global, parts, widths, x, labels, weights, lr, K, device="cuda",
                  grad_exchange="none", model="gcn", atts=None):
@@ -67,6 +80,7 @@ class DigestTrainer:
         self.W = weights
         self.gps = [GpuPartition(n_global, p, widths, device=device, model=model, atts=atts)
                     for p in parts]
+        self.push_mode = boundary_push_mode(self.gps, parts)
         idx = [torch.from_numpy(p.owned).to(device) for p in parts]
         self.x_own = [x.index_select(0, i).contiguous() for i in idx]
         self.y_own = [labels.index_select(0, i).contiguous() for i in idx]
@@ -112,7 +126,7 @@ class DigestTrainer:
                     D.digest_pull(gp.p, l - 1, self.stores[l - 1])
                 self._fwd(gp, l, h[m])
             for gp in self.gps:
-                D.digest_push(gp.p, l, gp.H[l], self.stores[l])
+                D.digest_push(gp.p, l, gp.H[l], self.stores[l], self.push_mode)
             h = [gp.H[l] for gp in self.gps]
         for gp in self.gps:
             for lev in range(1, self.L):
@@ -128,7 +142,7 @@ class DigestTrainer:
                 self._fwd(gp, l, h[m])
             if do_push and l <= self.L - 1:
                 for gp in self.gps:
-                    D.digest_push(gp.p, l, gp.H[l], self.stores[l])
+                    D.digest_push(gp.p, l, gp.H[l], self.stores[l], self.push_mode)
             h = [gp.H[l] for gp in self.gps]
         for m, gp in enumerate(self.gps):
             D.digest_softmax_xent(gp.p, gp.H[self.L], self.y_own[m], gp.dH[self.L],

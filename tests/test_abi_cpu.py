@@ -167,3 +167,35 @@ def test_profile_kernel_names():
     names = D.kernel_names()
     assert len(names) == D.lib().digest_profile_kernel_count()
     assert "spmm_fwd" in names and "gemm_fwd_relu" in names and "pull_gather" in names
+
+
+def test_launch_plan_and_cost_model():
+    """The plan query reports the library's product order and split counts,
+    and the per-launch cost model covers exactly the kinds a round launches,
+    with the compulsory bytes of the copies and aggregations."""
+    cfg, g, p = _tiny_partition(0)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    pl1, pl2 = D.digest_partition_plan(h, 1), D.digest_partition_plan(h, 2)
+    assert pl1["transform_first"] == 0 and pl1["dw_slices"] >= 1   # ReLU layers aggregate first
+    assert pl2["transform_first"] == 1   # 64 -> 16 identity: narrower gathers pay
+    with pytest.raises(D.DigestError):
+        D.digest_partition_plan(h, 0)
+    with pytest.raises(D.DigestError):
+        D.digest_partition_plan(h, cfg.layers + 1)
+    n, nh, nb = p.n_own, p.n_halo, h.n_boundary
+    gcn = D.digest_profile_model(h, D.MODEL_GCN)
+    assert gcn["pull_gather.l0"][0] == 8 * nh * cfg.widths[0] + 4 * nh
+    assert gcn["push_scatter.l1"][0] == 8 * nb * cfg.widths[1] + 8 * nb
+    di = cfg.widths[0]
+    assert gcn["spmm_fwd.l1"] == (4 * (n + 1) + 8 * h.nnz + 4 * (n + nh) * di + 4 * n * di, 0.0,
+                                  h.nnz)
+    assert gcn["gemm_fwd_relu.l1"][1] == 2.0 * n * di * cfg.widths[1]
+    assert not any(k.startswith("gat_") for k in gcn)
+    assert "softmax_xent.l2" in gcn and "loss_mean.l2" in gcn
+    gat = D.digest_profile_model(h, D.MODEL_GAT)
+    assert gat["gat_aggregate.l2"][2] == h.nnz and "spmm_fwd.l1" not in gat
+    L = D.lib()
+    buf = (ctypes.c_double * 1000)()
+    cnt = (ctypes.c_int64 * 1000)()
+    assert L.digest_profile_model(h.handle, 7, buf, buf, cnt) == D.EINVAL
+    assert L.digest_profile_model(h.handle, 0, None, buf, cnt) == D.EINVAL

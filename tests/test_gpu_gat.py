@@ -315,3 +315,20 @@ def test_gat_empty_partition():
     datt = torch.full((4, 2), 5.0, device="cuda")
     D.digest_gat_backward(h, 1, e, out, out, W, att, dw, datt, e)
     assert np.all(host(dw) == 0) and np.all(host(datt) == 0)
+
+
+@pytest.mark.parametrize("widths", [(24, 40, 6), (24, 40, 48)], ids=["40-6", "40-48"])
+def test_gat_scrambled_rows_with_repeats(widths):
+    """Rows in random column order with repeated (row, column) entries (each
+    entry is its own softmax term, as in the oracle) and one row of 300
+    entries: softmax, aggregation, edge gradient and transposed sums."""
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=1)
+    part = synth.scramble_rows(synth.make_partition(cfg, g, 1), seed=9, repeat_frac=0.3,
+                               long_row=300)
+    c = Case(g.n, part, widths, seed=1)
+    for level in range(c.op.L):
+        c.pull(level, synth.relu_normal((g.n, widths[level]), seed=40 + level))
+    for layer in (1, 2):
+        act = oracle.RELU if layer == 1 else oracle.IDENTITY
+        c.layer(layer, act, f"scrambled {widths} layer {layer}")

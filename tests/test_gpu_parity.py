@@ -493,3 +493,71 @@ def test_profile_instrumentation(tiny_graph):
     assert prof["spmm_bwd_transposed.l2"][1] == 1 and "spmm_bwd_transposed.l1" not in prof
     assert all(ms >= 0 for ms, _ in prof.values())
     assert Dm.digest_profile_read(gp.p) == {}
+
+
+# ---------------------------------------------------------------------------
+# CSR rows in any column order, with repeated (row, column) entries: the
+# header lets callers pass them (repeats are summed), and the oracle follows
+# the same CSR, so every call must still match it
+# ---------------------------------------------------------------------------
+
+# (widths, what layer 2 runs): transform-first identity with the fused
+# narrow epilogue (64 -> 16), aggregate-first identity on the GEMM (40 -> 48)
+SCRAMBLED = [(64, 64, 16), (24, 40, 48)]
+
+
+@pytest.mark.parametrize("widths", SCRAMBLED, ids=lambda w: "x".join(map(str, w)))
+def test_scrambled_rows_with_repeats(widths):
+    from paper_2206_00057_amd import digest as Dm
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 2000, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg)
+    base = synth.make_partition(cfg, g, 1)
+    part = synth.scramble_rows(base, seed=7, repeat_frac=0.3, long_row=300)
+    rows = np.diff(part.indptr)
+    assert rows.max() >= 300 and part.nnz > base.nnz
+    assert any(np.any(np.diff(part.indices[part.indptr[i]:part.indptr[i + 1]]) <= 0)
+               for i in range(part.n_own))
+    c = Case(cfg, g, part, label=f"scrambled {widths}")
+    for layer in (1, 2):
+        check_layer(c, layer)
+    # the halo gradient of layer 2, standalone and from the fused backward
+    W = synth.weights(cfg)[1]
+    h_in = c.layer_input(2)
+    for act in (oracle.RELU, oracle.IDENTITY):
+        out = torch.empty(c.n, widths[2], device="cuda")
+        Dm.digest_layer_forward(c.h, 2, dev(h_in), dev(W), out, act)
+        h_out = c.op.forward(2, h_in, W, act)
+        dh = c.upstream(2)
+        ref_halo = c.op.halo_gradient(2, W, h_out, dh, act)
+        got = torch.full((part.n_halo, widths[1]), float("nan"), device="cuda")
+        Dm.digest_halo_gradient(c.h, 2, dev(h_out), dev(dh), dev(W), got)
+        assert_close(host(got), ref_halo, f"{c.label} halo gradient act {act}")
+        dw = torch.empty(W.shape, device="cuda")
+        dh_in = torch.empty(c.n, widths[1], device="cuda")
+        got2 = torch.full((part.n_halo, widths[1]), float("nan"), device="cuda")
+        Dm.digest_layer_backward_halo(c.h, 2, dev(h_in), dev(h_out), dev(dh), dev(W), dw, dh_in,
+                                      got2)
+        ref_dw, ref_dh = c.op.backward(2, h_in, W, h_out, dh, act)
+        assert_close(host(dw), ref_dw, f"{c.label} fused dW act {act}")
+        assert_close(host(dh_in), ref_dh, f"{c.label} fused dh_in act {act}")
+        assert_close(host(got2), ref_halo, f"{c.label} fused halo gradient act {act}")
+
+
+def test_empty_partition_with_halo_gives_zero_halo_gradient():
+    """No owned rows but unreferenced halo ids: the fused backward's halo
+    gradient is zero (as digest_halo_gradient gives), and dW is zero."""
+    from paper_2206_00057_amd import digest as Dm
+    widths = [8, 12, 5]
+    halo = np.array([3, 7, 11], np.int64)
+    h = Dm.digest_partition_create(20, np.zeros(1, np.int64), np.zeros(0, np.int64),
+                                   np.zeros(0, np.float32), np.zeros(0, np.int64), halo, widths)
+    ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+    Dm.digest_partition_bind_workspace(h, ws)
+    Dm.digest_pull(h, 1, dev(synth.normal((20, widths[1]), seed=3)))
+    W = dev(synth.normal((widths[1], widths[2]), seed=4))
+    empty = torch.empty(0, device="cuda")
+    Dm.digest_layer_forward(h, 2, empty, W, empty, Dm.ACT_IDENTITY)
+    dw = torch.full((widths[1], widths[2]), float("nan"), device="cuda")
+    dh_halo = torch.full((3, widths[1]), float("nan"), device="cuda")
+    Dm.digest_layer_backward_halo(h, 2, empty, empty, empty, W, dw, empty, dh_halo)
+    assert not host(dh_halo).any() and not host(dw).any()

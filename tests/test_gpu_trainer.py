@@ -239,14 +239,13 @@ BACKWARD_HALO_CASES = [((24, 40, 6), True), ((24, 42, 6), True), ((24, 200, 48),
 def test_layer_backward_halo_matches_oracle(widths, tf):
     """The fused backward gives the separate calls' dw and dh_in and the halo
     gradient, for ReLU (GEMM-first with the mask) and identity."""
-    import bench
     from paper_2206_00057_amd import digest as D
     cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
     g = synth.make_graph(cfg, seed=4)
     p = synth.make_partition(cfg, g, 2)
-    assert bench.transform_first(2, widths, synth.shape_stats(cfg, g, p)) == tf
     h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
                                   cfg.widths)
+    assert D.digest_partition_plan(h, 2)["transform_first"] == int(tf)
     ws = torch.empty(max(h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
     D.digest_partition_bind_workspace(h, ws)
     op = oracle.OraclePartition(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)

@@ -386,3 +386,24 @@ def test_schedule_matches_algorithm_table(golden):
         oracle.sync_period(0, 1)
     with pytest.raises(oracle.OracleError):
         oracle.sync_period(3, 0)
+
+
+def test_repeated_entries_in_any_order_sum_like_a_dense_matrix():
+    """A CSR row may list its columns in any order and repeat a column: the
+    aggregation is the product with the dense matrix whose entry is the sum
+    of the repeats (checked against a dense numpy product in float64)."""
+    cfg = synth.CONFIGS["tiny"]
+    g = synth.make_graph(cfg)
+    base = synth.make_partition(cfg, g, 1)
+    p = synth.scramble_rows(base, seed=3, repeat_frac=0.4, long_row=200)
+    col, _ = oracle.partition_maps(g.n, p.indptr, p.indices, p.owned, p.halo)
+    d = 9
+    h_own = synth.normal((p.n_own, d), seed=1)
+    halo = synth.normal((p.n_halo, d), seed=2)
+    got = oracle.aggregate(p.indptr, col, p.values, h_own, halo)
+    dense = np.zeros((p.n_own, p.n_own + p.n_halo))
+    rows = np.repeat(np.arange(p.n_own), np.diff(p.indptr))
+    np.add.at(dense, (rows, col), p.values.astype(np.float64))
+    ref = dense @ np.vstack([h_own, halo]).astype(np.float64)
+    np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-6)
+    assert p.nnz > base.nnz
