@@ -346,6 +346,34 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
                                   void *hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the loss
+ * head of digest_softmax_xent without a partition handle or workspace.  It
+ * allocates nothing.  Its per-block partial sums go to a fixed device array
+ * of the library (DIGEST_STATIC_SCRATCH_FLOATS floats; each GPU the library
+ * runs on holds its own copy until the process ends); every block writes
+ * its sum before the final mean reads it, so nothing must start at zero.
+ * Every call on one GPU shares that array and leaves its contents there:
+ * calls that overlap on one GPU (on different streams, or from different
+ * host threads) race and must be ordered by the caller.
+ *   n_rows      0 <= n_rows <= DIGEST_STATIC_SCRATCH_FLOATS * r(n_classes),
+ *               with r(C) = 32 rows for C <= 8, 16 for C <= 64, 8 for
+ *               C <= 128 and 4 beyond (the rows one partial sum covers).
+ *   n_classes   1 .. 65536.
+ *   logits, dlogits  device [n_rows, n_classes];  labels device int32
+ *               [n_rows];  loss device, 1 float.  Results as for
+ *               digest_softmax_xent (a label outside [0, n_classes) gives
+ *               that row zero dlogits and the loss NaN).
+ *   hip_stream  a stream of the current device (NULL: its default stream).
+ * Errors: DIGEST_EINVAL (sizes, NULL, n_rows above the limit, a stream of
+ * another device), DIGEST_EHIP.
+ */
+#define DIGEST_STATIC_SCRATCH_FLOATS 262144
+digest_status digest_softmax_xent_static(int64_t n_rows, int32_t n_classes,
+                                         const float *logits, const int32_t *labels,
+                                         float *dlogits, float *loss, void *hip_stream);
+
+/*
  * Global parameter update of Algorithm 1 (AGG): each of the M subgraphs
  * took one local SGD step from the same global parameters, W_m = W -
  * lr * grad_m, and the new global parameters are their average (the

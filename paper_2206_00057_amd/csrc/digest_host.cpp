@@ -1228,6 +1228,49 @@ digest_status digest_softmax_xent(digest_partition *p, const float *logits,
     return hip_check(digest::launch_loss_mean(part, p->n_own, C, loss, s), "loss mean");
 }
 
+digest_status digest_softmax_xent_static(int64_t n_rows, int32_t n_classes,
+                                         const float *logits, const int32_t *labels,
+                                         float *dlogits, float *loss, void *hip_stream)
+{
+    static_assert(DIGEST_STATIC_SCRATCH_FLOATS == digest::kStaticScratchFloats,
+                  "the header's scratch size is the library's");
+    if (n_rows < 0 || n_rows >= INT32_MAX)
+        return fail(DIGEST_EINVAL, "n_rows %lld out of range", (long long)n_rows);
+    if (n_classes < 1 || n_classes > kMaxWidth)
+        return fail(DIGEST_EINVAL, "n_classes %d outside [1, %d]", n_classes, kMaxWidth);
+    if (!loss || (n_rows > 0 && (!logits || !labels || !dlogits)))
+        return fail(DIGEST_EINVAL, "NULL logits, labels, dlogits or loss");
+    const int64_t blocks = digest::softmax_xent_blocks((int32_t)n_rows, n_classes);
+    if (blocks > (int64_t)digest::kStaticScratchFloats)
+        return fail(DIGEST_EINVAL,
+                    "%lld rows of %d classes need %lld partial sums; the static scratch holds "
+                    "%zu (at most %lld rows)",
+                    (long long)n_rows, n_classes, (long long)blocks, digest::kStaticScratchFloats,
+                    (long long)digest::kStaticScratchFloats *
+                        digest::softmax_xent_rows_per_block(n_classes));
+    hipStream_t s = (hipStream_t)hip_stream;
+    int dev = -1;
+    if (digest_status st = hip_check(hipGetDevice(&dev), "current device"))
+        return st;
+    if (s) {
+        hipDevice_t sdev = -1;
+        if (digest_status st = hip_check(hipStreamGetDevice(s, &sdev), "stream device"))
+            return st;
+        if (sdev != dev)
+            return fail(DIGEST_EINVAL, "the stream belongs to device %d, the current device is %d",
+                        (int)sdev, dev);
+    }
+    float *part = nullptr;
+    if (digest_status st = hip_check(digest::static_scratch(&part), "static scratch"))
+        return st;
+    if (digest_status st = hip_check(digest::launch_softmax_xent(logits, labels, (int32_t)n_rows,
+                                                                 n_classes, dlogits, part, s),
+                                     "softmax xent"))
+        return st;
+    return hip_check(digest::launch_loss_mean(part, (int32_t)n_rows, n_classes, loss, s),
+                     "loss mean");
+}
+
 digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const float *h_out,
                                    const float *dh_out, const float *w, float *dh_halo,
                                    void *hip_stream)

@@ -29,8 +29,17 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "kernels.h"
+
+// The library's fixed scratch array for callers that cannot allocate
+// (digest_softmax_xent_static): every GPU the library runs on holds its own
+// copy until the process ends.  On the host this name is only a stand-in
+// for the symbol, not a device address; host code uses the address that
+// digest::static_scratch() looks up.
+static __device__ __align__(256) float scratch[digest::kStaticScratchFloats];
 
 namespace digest {
 namespace {
@@ -1935,9 +1944,14 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
 int loss_group(int32_t C) { return C <= 8 ? 8 : (C <= 64 ? 16 : (C <= 128 ? 32 : 64)); }
 int loss_slots(int32_t C) { return (C + loss_group(C) - 1) / loss_group(C); }
 
+int32_t softmax_xent_rows_per_block(int32_t C)
+{
+    return (kLossThreads / kWave) * (kWave / loss_group(C));
+}
+
 int32_t softmax_xent_blocks(int32_t n, int32_t C)
 {
-    const int32_t rows_per_block = (kLossThreads / kWave) * (kWave / loss_group(C));
+    const int32_t rows_per_block = softmax_xent_rows_per_block(C);
     return std::max<int32_t>(1, (n + rows_per_block - 1) / rows_per_block);
 }
 
@@ -2135,6 +2149,34 @@ hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t co
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(k_sgd_average, dim3((unsigned)blocks), dim3(256), 0, s, w, g, n, count, lr);
     return hipGetLastError();
+}
+
+hipError_t static_scratch(float **ptr)
+{
+    // device address of `scratch` per device, looked up once per device with
+    // that device current (the caller's current device)
+    static std::mutex mu;
+    static std::vector<float *> addr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if ((size_t)dev >= addr.size())
+        addr.resize((size_t)dev + 1, nullptr);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        if (!p)
+            return hipErrorInvalidSymbol;
+        addr[dev] = static_cast<float *>(p);
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_fill_zero(float *p, int64_t count, hipStream_t s)

@@ -138,6 +138,7 @@ hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const f
 // sums (softmax_xent_blocks(n, C) floats); launch_loss_mean then writes
 // their mean over the n rows.
 int32_t softmax_xent_blocks(int32_t n, int32_t C);
+int32_t softmax_xent_rows_per_block(int32_t C);
 hipError_t launch_softmax_xent(const float *logits, const int32_t *labels, int32_t n,
                                int32_t C, float *dlogits, float *block_loss, hipStream_t s);
 hipError_t launch_loss_mean(const float *block_loss, int32_t n, int32_t C, float *loss,
@@ -151,6 +152,12 @@ struct GradList {
 };
 hipError_t launch_sgd_average(float *w, const GradList &g, int32_t n, int64_t count, float lr,
                               hipStream_t s);
+
+// The library's fixed device scratch array (kStaticScratchFloats floats, one
+// copy per GPU, 256-byte aligned): its address on the current device,
+// looked up on the first call per device.
+constexpr size_t kStaticScratchFloats = 256 * 1024;
+hipError_t static_scratch(float **ptr);
 
 // p[0 .. count) = 0.
 hipError_t launch_fill_zero(float *p, int64_t count, hipStream_t s);

@@ -56,6 +56,7 @@ def lib():
             "digest_layer_forward": ([P, i32, P, P, P, i32, P], st),
             "digest_layer_backward": ([P, i32, P, P, P, P, P, P, P], st),
             "digest_softmax_xent": ([P, P, P, P, P, P], st),
+            "digest_softmax_xent_static": ([i64, i32, P, P, P, P, P], st),
             "digest_sgd_average": ([P, P, i32, i64, ctypes.c_float, P], st),
             "digest_halo_gradient": ([P, i32, P, P, P, P, P], st),
             "digest_layer_backward_halo": ([P, i32, P, P, P, P, P, P, P, P], st),
@@ -331,6 +332,20 @@ def digest_softmax_xent(p, logits, labels, dlogits, loss, stream=None):
     c = _dev(dlogits, torch.float32, p.n_own * C, "dlogits")
     d = _dev(loss, torch.float32, 1, "loss")
     _check(lib().digest_softmax_xent(p.handle, a, b, c, d, _stream(stream)))
+
+
+def digest_softmax_xent_static(logits, labels, dlogits, loss, stream=None):
+    """The loss head without a partition or workspace (for callers that
+    cannot allocate): logits [n, C], labels int32 [n], dlogits [n, C], loss
+    [1]; partial sums in the library's fixed device array."""
+    import torch
+    if logits.dim() != 2:
+        raise ValueError("logits must be [n, C]")
+    n, C = int(logits.shape[0]), int(logits.shape[1])
+    _check(lib().digest_softmax_xent_static(
+        n, C, _dev(logits, torch.float32, n * C, "logits"),
+        _dev(labels, torch.int32, n, "labels"), _dev(dlogits, torch.float32, n * C, "dlogits"),
+        _dev(loss, torch.float32, 1, "loss"), _stream(stream)))
 
 
 def digest_halo_gradient(p, layer, h_out, dh_out, w, dh_halo, stream=None):
