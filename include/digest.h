@@ -432,13 +432,24 @@ const char *digest_profile_kernel_name(int32_t kind);
  *   dgrad_fused         transform-first layers: 1 if dh_in = G_own W^T is
  *                       formed in the epilogue of the transposed
  *                       aggregation (when the caller asks for dh_in).
- *   hot_rows_fwd, hot_rows_bwd  source rows whose gathers the forward
- *                       (P_m) / transposed (P_in^T) aggregation of this
- *                       layer runs in a pass of their own, sliced over
- *                       the feature columns so that each slice of these
- *                       rows stays in one L2 (0: a single pass).
- *   hot_entries_fwd, hot_entries_bwd  entries of the sparse operand that
- *                       those passes take.
+ *   tiers_fwd, tiers_bwd  sliced passes of the forward aggregation (P_m)
+ *                       and of the transposed one (P_in^T) of this layer,
+ *                       which run before one pass over the remaining
+ *                       entries (0: a single pass).  The source rows are
+ *                       ranked by how many entries read them; tier t takes
+ *                       the entries that read the rows ranked
+ *                       [t R, (t+1) R), R = tier_rows_fwd / _bwd, and its
+ *                       pass gathers 32-float column slices of them, each
+ *                       slice on one XCD, so that one XCD's slices of the R
+ *                       rows stay in its L2.  Each pass adds into the
+ *                       output in tier order (a fixed summation order).
+ *                       Planned at create, and only when the environment
+ *                       variable DIGEST_SPMM_TIER_BYTES gives a per-XCD L2
+ *                       budget (unset or 0, the default: no tiers, which
+ *                       measured fastest on the workloads at hand); then a
+ *                       cost model picks the tier count, or
+ *                       DIGEST_SPMM_TIERS forces one.
+ *   tier_entries_fwd, tier_entries_bwd  entries the sliced passes take.
  * Errors: DIGEST_EINVAL (NULL, layer outside 1..L).
  */
 typedef struct {
@@ -447,10 +458,12 @@ typedef struct {
     int32_t dw_slices;
     int32_t dgrad_narrow_first;
     int32_t dgrad_fused;
-    int32_t hot_rows_fwd;
-    int32_t hot_rows_bwd;
-    int64_t hot_entries_fwd;
-    int64_t hot_entries_bwd;
+    int32_t tiers_fwd;
+    int32_t tiers_bwd;
+    int32_t tier_rows_fwd;
+    int32_t tier_rows_bwd;
+    int64_t tier_entries_fwd;
+    int64_t tier_entries_bwd;
 } digest_layer_plan;
 
 digest_status digest_partition_plan(const digest_partition *p, int32_t layer,

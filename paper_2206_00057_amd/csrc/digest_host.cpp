@@ -9,8 +9,10 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
+#include <numeric>
 #include <string>
 #include <vector>
 
@@ -131,17 +133,17 @@ int32_t gemm_tile_for(int64_t M, int64_t N, int64_t K, bool contraction_over_row
 // come first, so they start early); runs of consecutive short rows are
 // packed one per wave.  Returns the number of long-row blocks.
 int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
-                     std::vector<SpmmBlock> &blocks)
+                     std::vector<SpmmBlock> &blocks, int32_t long_row = digest::kSpmmLongRow)
 {
     const int32_t waves = digest::kSpmmThreads / 64;
     blocks.clear();
     for (int32_t r = 0; r < n_rows; ++r)
-        if (rowptr[r + 1] - rowptr[r] > digest::kSpmmLongRow)
+        if (rowptr[r + 1] - rowptr[r] > long_row)
             blocks.push_back({r, 0, rowptr[r], rowptr[r + 1]});
     const int32_t n_long = (int32_t)blocks.size();
     int32_t first = -1, count = 0;
     for (int32_t r = 0; r <= n_rows; ++r) {
-        const bool short_row = r < n_rows && rowptr[r + 1] - rowptr[r] <= digest::kSpmmLongRow;
+        const bool short_row = r < n_rows && rowptr[r + 1] - rowptr[r] <= long_row;
         if (short_row) {
             if (count == 0)
                 first = r;
@@ -153,6 +155,161 @@ int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
         }
     }
     return n_long;
+}
+
+// A tiered plan of one aggregation (one sparse operand at one width).  The
+// source rows (columns of the operand) are ranked by how many entries read
+// them; tier t holds the rows ranked [t H, (t+1) H), where H rows of one
+// XCD's share of the column slices fit the L2 budget of one XCD.  The
+// aggregation then runs as one sliced pass per tier (each XCD gathering its
+// column slices of the tier's rows, which stay in its L2) and one ordinary
+// pass over the remaining entries, each pass adding into the output, in
+// tier order.  The entries are split into T + 1 CSRs over the same rows,
+// stored one after another in `col` / `val` (row pointers are offsets into
+// them); a row's entries keep their order within each CSR.
+struct TierPlan {
+    int32_t which = 0;       // the sparse operand (Csr)
+    int32_t width = 0;       // aggregation width the plan is for
+    int32_t tiers = 0;       // sliced passes (the last CSR is the rest)
+    int32_t rows_per_tier = 0;
+    int64_t tier_entries = 0;   // entries in the sliced passes
+    std::vector<int32_t> rowptr;   // (tiers + 1) x (n_rows + 1), absolute offsets
+    std::vector<int32_t> col;
+    std::vector<float> val;
+    std::vector<SpmmBlock> blocks;   // per CSR: long-row blocks first
+    std::vector<int32_t> blk_off, blk_cnt, blk_long;   // per CSR
+    size_t off_rowptr = 0, off_col = 0, off_val = 0, off_blocks = 0;   // workspace
+};
+
+// Cost model of a tier: the gathers of its entries hit the L2 (kTierHitBytesPerS)
+// instead of going past it (the measured random-gather rate); in exchange
+// the pass re-reads the tier's index arrays once per column slice and the
+// output (and writes it) once more, and costs one more launch.
+constexpr double kTierHitBytesPerS = 18.0e12;
+constexpr double kTierMissBytesPerS = 7.0e12;
+constexpr double kStreamBytesPerS = 6.5e12;
+constexpr double kLaunchSeconds = 4.0e-6;
+constexpr int32_t kMaxTiers = 32;
+// Tiering is off unless DIGEST_SPMM_TIER_BYTES gives the per-XCD L2 budget
+// (about 3 MiB of the 4 MiB L2 suits it): on the measured workloads the
+// sliced passes do hit the L2 (82-84% of their requests), but the one-pass
+// kernel already finds the most-read rows in the Infinity Cache, the
+// remaining pass then runs at the lower rate of rows that miss it, and the
+// tiered aggregation was no faster (OGB-Products-shaped, 256 wide) or
+// slower (Reddit-shaped, 602 wide, 15 tiers).
+constexpr int64_t kTierBudgetBytes = 0;
+
+int64_t env_int(const char *name, int64_t dflt)
+{
+    const char *v = std::getenv(name);
+    if (!v || !*v)
+        return dflt;
+    char *end = nullptr;
+    const long long x = std::strtoll(v, &end, 10);
+    return (end && *end == 0) ? (int64_t)x : dflt;
+}
+
+// Plan the tiers of the CSR (rowptr, col, val) with n_rows rows over
+// n_cols source rows, aggregated at `width`.  DIGEST_SPMM_TIER_BYTES sets
+// the per-XCD L2 budget (unset or 0: no tiers) and DIGEST_SPMM_TIERS forces
+// that many tiers regardless of the cost model (tuning and tests).
+TierPlan plan_one_tier(int32_t which, const std::vector<int32_t> &rowptr,
+                       const std::vector<int32_t> &col, const std::vector<float> &val,
+                       int32_t n_rows, int64_t n_cols, int32_t width)
+{
+    TierPlan t;
+    t.which = which;
+    t.width = width;
+    const int64_t budget = env_int("DIGEST_SPMM_TIER_BYTES", kTierBudgetBytes);
+    const int64_t force = env_int("DIGEST_SPMM_TIERS", -1);
+    const int64_t slices = (width + digest::kSliceFloats - 1) / digest::kSliceFloats;
+    // a sliced pass needs a slice for every XCD and rows of an even width
+    if (budget <= 0 || force == 0 || slices < 8 || width % 2 != 0 || n_rows == 0)
+        return t;
+    const int64_t per_xcd = (slices + 7) / 8;
+    const int64_t H = std::max<int64_t>(1, budget / (per_xcd * digest::kSliceFloats * 4));
+    const int64_t nnz = rowptr[n_rows];
+    std::vector<int64_t> count((size_t)n_cols, 0);
+    for (int64_t k = 0; k < nnz; ++k)
+        count[col[k]] += 1;
+    std::vector<int32_t> order((size_t)n_cols);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int32_t a, int32_t b) { return count[a] > count[b]; });
+    // tier of each source row (-1: the rest); rows read once stay in the rest
+    std::vector<int32_t> tier_of((size_t)n_cols, -1);
+    const double row_bytes = 4.0 * width;
+    const double per_pass = 2.0 * n_rows * row_bytes / kStreamBytesPerS + kLaunchSeconds;
+    int32_t T = 0;
+    for (int64_t t0 = 0; t0 < n_cols && T < kMaxTiers; t0 += H) {
+        if (force > 0 && T >= force)
+            break;
+        const int64_t t1 = std::min<int64_t>(n_cols, t0 + H);
+        int64_t refs = 0;
+        for (int64_t r = t0; r < t1; ++r)
+            refs += count[order[r]] >= 2 ? count[order[r]] : 0;
+        if (refs == 0)
+            break;
+        const double saving =
+            refs * row_bytes * (1.0 / kTierMissBytesPerS - 1.0 / kTierHitBytesPerS);
+        const double cost = per_pass + refs * 8.0 * slices / kTierHitBytesPerS;
+        if (force < 0 && saving <= cost)
+            break;
+        for (int64_t r = t0; r < t1; ++r)
+            if (count[order[r]] >= 2)
+                tier_of[order[r]] = T;
+        t.tier_entries += refs;
+        ++T;
+    }
+    if (T == 0)
+        return t;
+    t.tiers = T;
+    t.rows_per_tier = (int32_t)H;
+    // split the entries into T + 1 CSRs (tiers, then the rest), each row's
+    // entries in their original order
+    const int32_t C = T + 1;
+    std::vector<int64_t> per((size_t)C * (n_rows + 1), 0);   // counts, then offsets
+    for (int32_t i = 0; i < n_rows; ++i)
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+            const int32_t c = tier_of[col[k]] < 0 ? T : tier_of[col[k]];
+            per[(size_t)c * (n_rows + 1) + i + 1] += 1;
+        }
+    t.rowptr.assign((size_t)C * (n_rows + 1), 0);
+    int64_t base = 0;
+    for (int32_t c = 0; c < C; ++c) {
+        int32_t *rp = &t.rowptr[(size_t)c * (n_rows + 1)];
+        rp[0] = (int32_t)base;
+        for (int32_t i = 0; i < n_rows; ++i)
+            rp[i + 1] = rp[i] + (int32_t)per[(size_t)c * (n_rows + 1) + i + 1];
+        base = rp[n_rows];
+    }
+    t.col.resize((size_t)nnz);
+    t.val.resize((size_t)nnz);
+    for (int32_t i = 0; i < n_rows; ++i) {
+        int32_t next[kMaxTiers + 1];
+        for (int32_t c = 0; c < C; ++c)
+            next[c] = t.rowptr[(size_t)c * (n_rows + 1) + i];
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k) {
+            const int32_t c = tier_of[col[k]] < 0 ? T : tier_of[col[k]];
+            t.col[next[c]] = col[k];
+            t.val[next[c]] = val[k];
+            ++next[c];
+        }
+    }
+    for (int32_t c = 0; c < C; ++c) {
+        std::vector<int32_t> rp(t.rowptr.begin() + (size_t)c * (n_rows + 1),
+                                t.rowptr.begin() + (size_t)(c + 1) * (n_rows + 1));
+        std::vector<SpmmBlock> b;
+        // the sliced passes' strip kernel takes every row up to
+        // kTierLongRow entries; only longer rows get a workgroup each
+        const int32_t n_long = build_blocks(rp, n_rows, b, c < T ? digest::kTierLongRow
+                                                                 : digest::kSpmmLongRow);
+        t.blk_off.push_back((int32_t)t.blocks.size());
+        t.blk_cnt.push_back((int32_t)b.size());
+        t.blk_long.push_back(n_long);
+        t.blocks.insert(t.blocks.end(), b.begin(), b.end());
+    }
+    return t;
 }
 
 }  // namespace
@@ -172,6 +329,10 @@ struct digest_partition {
     // (P_out^T, numbered from 0).
     std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf, blocks_th;
     int32_t long_f = 0, long_t = 0, long_tf = 0, long_th = 0;   // leading long-row blocks
+
+    // Tiered plans of the aggregations (see TierPlan), at most one per
+    // (sparse operand, width).
+    std::vector<TierPlan> tier_plans;
 
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
@@ -355,6 +516,12 @@ void plan_layout(digest_partition &p)
     l.tbuf = take(sizeof(float) * (size_t)tbuf);
     l.gemm_part = take(sizeof(float) * (size_t)gemm_part);
     l.loss_part = take(sizeof(float) * (size_t)digest::softmax_xent_blocks(p.n_own, p.widths[p.L]));
+    for (TierPlan &t : p.tier_plans) {
+        t.off_rowptr = take(sizeof(int32_t) * t.rowptr.size());
+        t.off_col = take(sizeof(int32_t) * t.col.size());
+        t.off_val = take(sizeof(float) * t.val.size());
+        t.off_blocks = take(sizeof(SpmmBlock) * t.blocks.size());
+    }
     l.total = o;
 }
 
@@ -462,6 +629,47 @@ digest_status need_bound(const digest_partition *p)
 // (edge weights in the same entry order); relu stores max(x, 0).
 enum class Csr { Fwd, InT, FullT, HaloT };
 
+// Tiered plans for the aggregations a standard round runs at widths where
+// slicing applies: the forward's P_m at d_in of every aggregate-first layer
+// and the backward's P_in^T at its width for layers >= 2 (the layer plan's
+// orders, ReLU below the last layer).  Operands or widths that gain nothing
+// get no plan and run as one pass.
+void plan_tiers(digest_partition &p)
+{
+    p.tier_plans.clear();
+    std::vector<std::pair<int32_t, int32_t>> tried;
+    auto want = [&](Csr which, int32_t w) {
+        for (const auto &tw : tried)
+            if (tw.first == (int32_t)which && tw.second == w)
+                return;
+        tried.push_back({(int32_t)which, w});
+        TierPlan t = which == Csr::Fwd
+                         ? plan_one_tier((int32_t)which, p.rowptr, p.col, p.val, p.n_own,
+                                         (int64_t)p.n_own + p.n_halo, w)
+                         : plan_one_tier((int32_t)which, p.t_rowptr, p.t_src, p.t_val, p.n_own,
+                                         p.n_own, w);
+        if (t.tiers > 0)
+            p.tier_plans.push_back(std::move(t));
+    };
+    for (int32_t l = 1; l <= p.L; ++l) {
+        const int32_t d_in = p.widths[l - 1], d_out = p.widths[l];
+        const bool relu = l < p.L;
+        if (!relu && p.n_own > 0 && transform_first_cheaper(p, l))
+            continue;
+        want(Csr::Fwd, d_in);
+        if (l > 1)
+            want(Csr::InT, (!relu && d_out < d_in) ? d_out : d_in);
+    }
+}
+
+const TierPlan *find_tiers(const digest_partition &p, Csr which, int32_t width)
+{
+    for (const TierPlan &t : p.tier_plans)
+        if (t.which == (int32_t)which && t.width == width)
+            return &t;
+    return nullptr;
+}
+
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
                        const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
@@ -484,6 +692,31 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     if (which == Csr::HaloT)
         rowptr += p->n_own;
     Timed t(p, kind >= 0 ? kind : (fwd ? K_SPMM_FWD : K_SPMM_BWD), layer, s);
+    const TierPlan *tp = find_tiers(*p, which, d);
+    if (tp && !ep && !val && !relu && !(r1 && r1->a) && n_out0 == INT32_MAX && !out1 &&
+        digest::spmm_sliced_ok(d, src0, src1, out)) {
+        // sliced passes over the tiers, then the rest, each adding into out
+        const int32_t n_rows = p->n_own;
+        const int32_t *trp = p->at<int32_t>(tp->off_rowptr);
+        const int32_t *tcol = p->at<int32_t>(tp->off_col);
+        const float *tval = p->at<float>(tp->off_val);
+        const SpmmBlock *tblk = p->at<SpmmBlock>(tp->off_blocks);
+        for (int32_t c = 0; c <= tp->tiers; ++c) {
+            const int32_t *rp = trp + (int64_t)c * (n_rows + 1);
+            const SpmmBlock *b = tblk + tp->blk_off[c];
+            const hipError_t e =
+                c < tp->tiers
+                    ? digest::launch_spmm_sliced(b, tp->blk_cnt[c], tp->blk_long[c], rp, tcol,
+                                                 tval, (int64_t)tp->col.size(), src0, src1,
+                                                 n_src0, n_rows, d, out, c > 0, s)
+                    : digest::launch_spmm(b, tp->blk_cnt[c], tp->blk_long[c], rp, tcol, tval,
+                                          src0, src1, n_src0, d, out, s, nullptr, nullptr,
+                                          INT32_MAX, false, nullptr, true);
+            if (digest_status st = hip_check(e, "tiered spmm"))
+                return st;
+        }
+        return DIGEST_OK;
+    }
     return hip_check(
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
@@ -664,6 +897,7 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
                                                  p->t_rowptr.end());
             p->long_th = build_blocks(halo_rows, p->n_halo, p->blocks_th);
         }
+        plan_tiers(*p);
         plan_layout(*p);
         plan_gat_layout(*p);
         p->gat_done.assign(p->L + 1, 0);
@@ -753,6 +987,22 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
             hipMemcpyAsync(ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s), "upload");
         if (st)
             return st;
+    }
+    for (const TierPlan &t : p->tier_plans) {
+        const Up tu[] = {
+            {t.off_rowptr, t.rowptr.data(), sizeof(int32_t) * t.rowptr.size()},
+            {t.off_col, t.col.data(), sizeof(int32_t) * t.col.size()},
+            {t.off_val, t.val.data(), sizeof(float) * t.val.size()},
+            {t.off_blocks, t.blocks.data(), sizeof(SpmmBlock) * t.blocks.size()},
+        };
+        for (const Up &u : tu) {
+            if (!u.bytes)
+                continue;
+            digest_status st = hip_check(
+                hipMemcpyAsync(ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s), "upload");
+            if (st)
+                return st;
+        }
     }
     p->ws = ws;
     // The halo buffers and AH of the old workspace are gone: no level counts
@@ -1665,6 +1915,18 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
         splitk_plan(d_in, d_out, p.n_own, splits, kchunk);
         pl.dw_slices = splits;
         pl.dgrad_narrow_first = !relu && d_out < d_in;
+        if (const TierPlan *t = find_tiers(p, Csr::Fwd, d_in)) {
+            pl.tiers_fwd = t->tiers;
+            pl.tier_rows_fwd = t->rows_per_tier;
+            pl.tier_entries_fwd = t->tier_entries;
+        }
+        if (layer > 1)
+            if (const TierPlan *t =
+                    find_tiers(p, Csr::InT, pl.dgrad_narrow_first ? d_out : d_in)) {
+                pl.tiers_bwd = t->tiers;
+                pl.tier_rows_bwd = t->rows_per_tier;
+                pl.tier_entries_bwd = t->tier_entries;
+            }
     }
     return pl;
 }

@@ -199,24 +199,29 @@ constexpr int spmm_inflight(int groups, int nch, int vec)
 // of a group accumulates the feature vectors gl, gl + GL, ... (NCH of them
 // per column pass).  Entry ids and weights are fetched 64 at a time (one per
 // lane) and broadcast; up to U entries per group are in flight.
-// Destination of an aggregation's rows: row r < n0 is out0 + r d, row
-// r >= n0 is out1 + (r - n0) d.  n0 = INT32_MAX makes one contiguous output;
+// Destination of an aggregation's rows: row r < n0 is out0 + r ld, row
+// r >= n0 is out1 + (r - n0) ld.  n0 = INT32_MAX makes one contiguous output;
 // a split lets one launch over P_m^T write the owned rows and the halo rows
-// to buffers of their own.
+// to buffers of their own.  With acc the row's sum is added to what the
+// output already holds (a later pass over more entries of the same rows).
 struct SpmmOut {
     float *out0;
     float *out1;
     int32_t n0;
     bool relu;      // store max(x, 0)
     SpmmRank1 r1;   // rank-one terms added first when r1.a is set
+    int32_t ld;     // row stride of out0 and out1 (floats)
+    bool acc;       // out = out + sum
 
-    __device__ __forceinline__ float *row(int32_t r, int32_t d) const
+    __device__ __forceinline__ float *row(int32_t r) const
     {
-        return r < n0 ? out0 + (int64_t)r * d : out1 + (int64_t)(r - n0) * d;
+        return r < n0 ? out0 + (int64_t)r * ld : out1 + (int64_t)(r - n0) * ld;
     }
     // the stored value of feature f of row r whose sum is v
     __device__ __forceinline__ float fin(int32_t r, int32_t f, float v) const
     {
+        if (acc)
+            v += row(r)[f];
         if (r1.a) {
             const float xa = r1.x[r];
             const float yb = r < r1.ny ? r1.y[2 * (int64_t)r + 1] : 0.f;
@@ -225,12 +230,28 @@ struct SpmmOut {
         return relu ? fmaxf(v, 0.f) : v;
     }
     template <int VEC>
-    __device__ __forceinline__ void put(int32_t r, int32_t d, int32_t off, float (&v)[VEC]) const
+    __device__ __forceinline__ void put(int32_t r, int32_t off, float (&v)[VEC]) const
     {
+        if (acc) {
+            float prev[VEC];
+            load_vec<VEC>(row(r) + off, prev);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i)
-            v[i] = fin(r, off + i, v[i]);
-        store_vec<VEC>(row(r, d) + off, v);
+            for (int i = 0; i < VEC; ++i)
+                v[i] += prev[i];
+        }
+        if (relu || r1.a) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+                float t = v[i];
+                if (r1.a) {
+                    const float xa = r1.x[r];
+                    const float yb = r < r1.ny ? r1.y[2 * (int64_t)r + 1] : 0.f;
+                    t += xa * r1.a[2 * (off + i)] + yb * r1.a[2 * (off + i) + 1];
+                }
+                v[i] = relu ? fmaxf(t, 0.f) : t;
+            }
+        }
+        store_vec<VEC>(row(r) + off, v);
     }
 };
 
@@ -240,7 +261,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
                                            const float *__restrict__ val,
                                            const float *__restrict__ src0,
                                            const float *__restrict__ src1, int32_t n_src0,
-                                           int32_t d, const SpmmOut out,
+                                           int32_t d, int32_t lds, const SpmmOut out,
                                            float (*red)[NCH * GL * VEC])
 {
     constexpr int G = kWave / GL;
@@ -306,8 +327,8 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const float *sp = (TWO && cc[u] >= n_src0)
-                                          ? src1 + (int64_t)(cc[u] - n_src0) * d
-                                          : src0 + (int64_t)cc[u] * d;
+                                          ? src1 + (int64_t)(cc[u] - n_src0) * lds
+                                          : src0 + (int64_t)cc[u] * lds;
 #pragma unroll
                     for (int ch = 0; ch < NCH; ++ch) {
                         const int c = c0 + ch * GL + gl;
@@ -344,7 +365,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
                 for (int ch = 0; ch < NCH; ++ch) {
                     const int c = c0 + ch * GL + gl;
                     if (c < dv)
-                        out.put<VEC>(row, d, c * VEC, acc[ch]);
+                        out.put<VEC>(row, c * VEC, acc[ch]);
                 }
             }
         } else {
@@ -363,7 +384,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
 #pragma unroll
                     for (int w = 0; w < kSpmmWaves; ++w)
                         sum += red[w][t];
-                    out.row(row, d)[(int64_t)c * VEC + t % VEC] = out.fin(row, c * VEC + t % VEC, sum);
+                    out.row(row)[(int64_t)c * VEC + t % VEC] = out.fin(row, c * VEC + t % VEC, sum);
                 }
             }
             __syncthreads();
@@ -397,11 +418,11 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm(const SpmmBlock *__restri
                                                        const float *__restrict__ src0,
                                                        const float *__restrict__ src1,
                                                        int32_t n_src0, int32_t d,
-                                                       SpmmOut out)
+                                                       int32_t lds, SpmmOut out)
 {
     __shared__ float red[kSpmmWaves][NCH * GL * VEC];
     spmm_block<VEC, GL, NCH, TWO>(blocks[blockIdx.x], rowptr, col, val, src0, src1, n_src0, d,
-                                  out, red);
+                                  lds, out, red);
 }
 
 // Epilogue destination of row r: out2 for r < rows, out3 (if any) after.
@@ -427,7 +448,13 @@ __device__ __forceinline__ float *ep_row(const SpmmEpilogue &ep, int32_t r)
 // get out2[r][n] = sum_k out[r][k] w[n][k] (w row-major [n2][d], staged in
 // LDS as [k][n2]); a lane group shares its row by shuffles and writes it out
 // in float4 pieces.
-template <int VEC, int GL, int NCH, int NB, bool TWO, bool EP>
+// With SL the rows are d floats wide (sources and output, stride d) and
+// the launch covers them in column slices of kSliceFloats: workgroup w
+// takes slice (w mod 8) + 8 ((w / 8) mod q) of work block w / (8 q), q the
+// slices per XCD, so every workgroup of one slice runs on one XCD (the
+// dispatcher deals workgroups to the 8 XCDs in turn) and the slice of the
+// rows a pass gathers stays in that XCD's L2.
+template <int VEC, int GL, int NCH, int NB, bool TWO, bool EP, bool SL = false>
 __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     const SpmmBlock *__restrict__ blocks, int32_t n_long, int32_t n_blocks,
     const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
@@ -435,7 +462,24 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     int32_t n_src0, int32_t d, SpmmOut out, SpmmEpilogue ep)
 {
     static_assert(!EP || (NCH == 1 && GL * VEC <= kNarrow), "epilogue rows are kNarrow wide");
+    static_assert(!SL || !EP, "no epilogue on a sliced pass");
     __shared__ float red[kSpmmWaves][NCH * GL * VEC];
+    int32_t wb = (int32_t)blockIdx.x;   // work block
+    int32_t lds = d;                    // source row stride
+    if constexpr (SL) {
+        const int32_t q = (d + kXcds * kSliceFloats - 1) / (kXcds * kSliceFloats);
+        const int32_t off = (wb % kXcds + kXcds * ((wb / kXcds) % q)) * kSliceFloats;
+        if (off >= d)
+            return;   // the whole workgroup: no slice here
+        wb /= kXcds * q;
+        src0 += off;
+        if (src1)
+            src1 += off;
+        out.out0 += off;
+        if (out.out1)
+            out.out1 += off;
+        d = min(kSliceFloats, d - off);
+    }
     extern __shared__ float ws[];   // EP: w as [k][n2]
     if constexpr (EP) {
         stage_lds(ws, d * ep.n2, [&](int i) {
@@ -444,13 +488,13 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
         });
         __syncthreads();
     }
-    if ((int32_t)blockIdx.x < n_long) {   // uniform over the block
-        const SpmmBlock b = blocks[blockIdx.x];
-        spmm_block<VEC, GL, NCH, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, out, red);
+    if (wb < n_long) {   // uniform over the block
+        const SpmmBlock b = blocks[wb];
+        spmm_block<VEC, GL, NCH, TWO>(b, rowptr, col, val, src0, src1, n_src0, d, lds, out, red);
         if constexpr (EP) {
             // the row was written by this block before spmm_block's last barrier
             if (float *o2 = ep_row(ep, b.row)) {
-                const float *orow = out.row(b.row, d);
+                const float *orow = out.row(b.row);
                 float gk[kNarrow];
 #pragma unroll
                 for (int k = 0; k < kNarrow; ++k)
@@ -466,7 +510,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     const int lane = threadIdx.x % kWave;
     const int g = lane / GL;
     const int gl = lane % GL;
-    const int bi = n_long + ((int)blockIdx.x - n_long) * kSpmmWaves + wave;
+    const int bi = n_long + (wb - n_long) * kSpmmWaves + wave;
     if (bi >= n_blocks)
         return;
     const SpmmBlock b = blocks[bi];
@@ -511,8 +555,8 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
 #pragma unroll
                 for (int u = 0; u < GL; ++u) {
                     const int c = cc[j][u];
-                    const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * d
-                                                           : src0 + (int64_t)c * d;
+                    const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * lds
+                                                           : src0 + (int64_t)c * lds;
 #pragma unroll
                     for (int ch = 0; ch < NCH; ++ch) {
                         const int cv = ch * GL + gl;
@@ -533,7 +577,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
         for (int ch = 0; ch < NCH; ++ch) {
             const int cv = ch * GL + gl;
             if (cv < dv)
-                out.put<VEC>(row, d, cv * VEC, acc[ch]);
+                out.put<VEC>(row, cv * VEC, acc[ch]);
         }
         if constexpr (EP) {
             if (float *o2 = ep_row(ep, row)) {
@@ -546,6 +590,143 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
                 for (int n4 = gl; n4 < ep.n2 / 4; n4 += GL)
                     narrow_ep_store(gk, d, ws, ep.n2, n4, o2);
             }
+        }
+    }
+}
+
+// Sliced pass of a tiered aggregation over its rows of at most
+// kTierLongRow entries (longer rows are left to the long-row blocks of
+// k_spmm_narrow).  Workgroups map to XCDs and column slices as in
+// k_spmm_narrow's sliced mode; each wave then walks a strip of rows_per_wave
+// consecutive rows with one lane group (GL lanes, one vector each) per row,
+// G rows at a time.  A group takes its rows' entries in batches of NB * GL,
+// and the loop is software-pipelined so that a batch's gathers are in
+// flight together with the index loads of the group's next batch and the
+// row pointers of its row after next: a step costs one gather round trip
+// (from the L2 that holds this XCD's slices of the tier's rows), not the
+// three dependent round trips of index, pointer and gather.  Every load
+// is unconditional (padding entries reread entry 0 with weight 0) so that
+// the wait counts stay static.  A row's entries are added in CSR order.
+constexpr int kTierNB = 2;
+
+template <int VEC, bool TWO>
+__global__ __launch_bounds__(256) void k_spmm_tier(
+    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+    const float *__restrict__ val, const float *__restrict__ src0,
+    const float *__restrict__ src1, int32_t n_src0, int32_t n_rows, int32_t d,
+    int32_t rows_per_wave, SpmmOut out)
+{
+    constexpr int GL = kSliceFloats / VEC;   // lanes per row slice
+    constexpr int G = kWave / GL;            // rows in flight per wave
+    constexpr int E = kTierNB * GL;          // entries per group batch
+    int32_t wb = (int32_t)blockIdx.x;
+    const int32_t lds = d;
+    {
+        const int32_t q = (d + kXcds * kSliceFloats - 1) / (kXcds * kSliceFloats);
+        const int32_t off = (wb % kXcds + kXcds * ((wb / kXcds) % q)) * kSliceFloats;
+        if (off >= d)
+            return;
+        wb /= kXcds * q;
+        src0 += off;
+        if (src1)
+            src1 += off;
+        out.out0 += off;
+        d = min(kSliceFloats, d - off);
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int g = lane / GL, gl = lane % GL;
+    const int64_t wave = (int64_t)wb * (256 / kWave) + threadIdx.x / kWave;
+    const int64_t rb = wave * rows_per_wave;
+    if (rb >= n_rows)
+        return;   // the whole wave (no barriers in this kernel)
+    const int32_t r_begin = (int32_t)rb;
+    const int32_t r_end = (int32_t)min<int64_t>(n_rows, rb + rows_per_wave);
+    const int dv = d / VEC;
+    const int cv = gl < dv ? gl : 0;   // lanes past the slice reread vector 0, store nothing
+
+    // entry range of row rr; rows past the strip and long rows (left to the
+    // long-row blocks, `lng` set) read as empty.  The pointer loads are
+    // clamped into the strip, so they are unconditional.
+    auto bounds = [&](int32_t rr, int32_t &kb, int32_t &ke, bool &lng) {
+        const int32_t rc = rr < r_end ? rr : r_end - 1;
+        kb = rowptr[rc];
+        ke = rowptr[rc + 1];
+        lng = ke - kb > kTierLongRow;
+        if (rr >= r_end || lng)
+            ke = kb;
+    };
+    int32_t r = r_begin + g;
+    int32_t k, ke, nk, nke;
+    bool lng, nlng;
+    bounds(r, k, ke, lng);
+    bounds(r + G, nk, nke, nlng);
+    int mc[kTierNB];
+    float mv[kTierNB];
+    auto fetch = [&](int32_t kk0, int32_t kke, bool live, int (&c)[kTierNB], float (&a)[kTierNB]) {
+#pragma unroll
+        for (int j = 0; j < kTierNB; ++j) {
+            const int32_t kk = kk0 + j * GL + gl;
+            const bool in = live && kk < kke;
+            c[j] = col[in ? kk : 0];
+            a[j] = val[in ? kk : 0] * (in ? 1.f : 0.f);
+        }
+    };
+    fetch(k, ke, r < r_end, mc, mv);
+    float acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v)
+        acc[v] = 0.f;
+    while (__any(r < r_end)) {
+        float x[kTierNB][GL][VEC];
+        float aa[kTierNB][GL];
+#pragma unroll
+        for (int j = 0; j < kTierNB; ++j)
+#pragma unroll
+            for (int u = 0; u < GL; ++u) {
+                const int c = __shfl(mc[j], g * GL + u);
+                aa[j][u] = __shfl(mv[j], g * GL + u);
+                const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * lds
+                                                       : src0 + (int64_t)c * lds;
+                load_vec<VEC>(sp + cv * VEC, x[j][u]);
+            }
+        // the next batch: more of this row, or the first of the group's next row
+        const bool row_end = k + E >= ke;
+        const int32_t k2 = row_end ? nk : k + E;
+        const int32_t ke2 = row_end ? nke : ke;
+        const int32_t r2 = row_end ? r + G : r;
+        int mc2[kTierNB];
+        float mv2[kTierNB];
+        fetch(k2, ke2, r2 < r_end, mc2, mv2);
+        int32_t nnk, nnke;
+        bool nnlng;
+        bounds(r + 2 * G, nnk, nnke, nnlng);   // used only when this row ends
+#pragma unroll
+        for (int j = 0; j < kTierNB; ++j)
+#pragma unroll
+            for (int u = 0; u < GL; ++u)
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+                    acc[v] = fmaf(aa[j][u], x[j][u][v], acc[v]);
+        if (row_end) {
+            if (r < r_end && gl < dv && !lng)
+                out.put<VEC>(r, gl * VEC, acc);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                acc[v] = 0.f;
+            r += G;
+            k = nk;
+            ke = nke;
+            lng = nlng;
+            nk = nnk;
+            nke = nnke;
+            nlng = nnlng;
+        } else {
+            k += E;
+        }
+#pragma unroll
+        for (int j = 0; j < kTierNB; ++j) {
+            mc[j] = mc2[j];
+            mv[j] = mv2[j];
         }
     }
 }
@@ -1662,6 +1843,8 @@ hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_bloc
 {
     constexpr int NB = narrow_nb(GL, NCH, VEC);
     const int64_t grid = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
+    if (grid > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
     if constexpr (NCH == 1 && GL * VEC <= kNarrow) {
         if (ep) {
             const size_t lds = sizeof(float) * (size_t)d * ep->n2;
@@ -1686,7 +1869,28 @@ hipError_t spmm_t(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowp
                   int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
 {
     hipLaunchKernelGGL((k_spmm<VEC, GL, NCH, TWO>), dim3((unsigned)n_blocks), dim3(kSpmmThreads),
-                       0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, out);
+                       0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, d, out);
+    return hipGetLastError();
+}
+
+// A sliced pass (kSliceFloats-column slices dealt to the XCDs) of the narrow
+// kernel over rows of d floats.
+template <int VEC, bool TWO>
+hipError_t spmm_sliced_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_blocks,
+                         const int32_t *rowptr, const int32_t *col, const float *val,
+                         const float *src0, const float *src1, int32_t n_src0, int32_t d,
+                         SpmmOut out, hipStream_t s)
+{
+    constexpr int GL = kSliceFloats / VEC;
+    constexpr int NB = narrow_nb(GL, 1, VEC);
+    const int64_t work = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
+    const int64_t q = (d + kXcds * kSliceFloats - 1) / (kXcds * kSliceFloats);
+    const int64_t grid = work * kXcds * q;
+    if (grid > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, 1, NB, TWO, false, true>), dim3((unsigned)grid),
+                       dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val, src0,
+                       src1, n_src0, d, out, SpmmEpilogue{});
     return hipGetLastError();
 }
 
@@ -1826,11 +2030,78 @@ bool spmm_epilogue_ok(int32_t d, int32_t n2, const float *out2)
            (size_t)d * n2 * sizeof(float) <= 64 * 1024 && ((uintptr_t)out2 % 16) == 0;
 }
 
+bool spmm_sliced_ok(int32_t d, const float *src0, const float *src1, const float *out0)
+{
+    return d > 0 && pick_vec(d, src0, out0) >= 2 && (!src1 || pick_vec(d, src1, nullptr) >= 2);
+}
+
+namespace {
+
+template <int VEC, bool TWO>
+hipError_t spmm_tier_t(const SpmmBlock *blocks, int32_t n_long, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const float *src0,
+                       const float *src1, int32_t n_src0, int32_t n_rows, int32_t d,
+                       SpmmOut out, hipStream_t s)
+{
+    // the long rows: whole workgroups, as in the unsliced kernel's plan
+    if (n_long > 0)
+        if (hipError_t e = spmm_sliced_t<VEC, TWO>(blocks, n_long, n_long, rowptr, col, val,
+                                                   src0, src1, n_src0, d, out, s))
+            return e;
+    // the short rows: strips of rows per wave, about four rounds of waves
+    // of the whole chip (256 CUs x 16 waves)
+    constexpr int G = kWave / (kSliceFloats / VEC);
+    const int64_t q = (d + kXcds * kSliceFloats - 1) / (kXcds * kSliceFloats);
+    int64_t rpw = kXcds * q * (int64_t)n_rows / (256 * 16 * 4);
+    rpw = std::min<int64_t>(256, std::max<int64_t>(G, (rpw + G - 1) / G * G));
+    const int64_t waves = (n_rows + rpw - 1) / rpw;
+    const int64_t grid = (waves + 3) / 4 * kXcds * q;
+    if (grid > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_spmm_tier<VEC, TWO>), dim3((unsigned)grid), dim3(256), 0, s, rowptr,
+                       col, val, src0, src1, n_src0, n_rows, d, (int32_t)rpw, out);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_spmm_sliced(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
+                              const int32_t *rowptr, const int32_t *col, const float *val,
+                              int64_t nnz, const float *src0, const float *src1, int32_t n_src0,
+                              int32_t n_rows, int32_t d, float *out0, bool acc, hipStream_t s)
+{
+    if (n_rows <= 0 || d <= 0)
+        return hipSuccess;
+    if (n_long < 0 || n_long > n_blocks || nnz < 1)
+        return hipErrorInvalidValue;   // padding entries reread entry 0
+    const SpmmOut out{out0, nullptr, INT32_MAX, false, SpmmRank1{}, d, acc};
+    // every slice starts on a multiple of kSliceFloats, so the vector width
+    // of the whole row is the slices' too
+    int vec = pick_vec(d, src0, out0);
+    if (src1 && pick_vec(d, src1, nullptr) < vec)
+        vec = pick_vec(d, src1, nullptr);
+#define DIGEST_TIER(V, T)                                                                       \
+    return spmm_tier_t<V, T>(blocks, n_long, rowptr, col, val, src0, src1, n_src0, n_rows, d,   \
+                             out, s)
+    if (vec == 4) {
+        if (src1)
+            DIGEST_TIER(4, true);
+        DIGEST_TIER(4, false);
+    }
+    if (vec == 2) {
+        if (src1)
+            DIGEST_TIER(2, true);
+        DIGEST_TIER(2, false);
+    }
+#undef DIGEST_TIER
+    return hipErrorInvalidValue;   // rows of odd width take the unsliced kernel
+}
+
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep, float *out1,
-                       int32_t n_out0, bool relu, const SpmmRank1 *r1)
+                       int32_t n_out0, bool relu, const SpmmRank1 *r1, bool acc)
 {
     if (ep && (!spmm_epilogue_ok(d, ep->n2, ep->out2) ||
                (ep->out3 && !spmm_epilogue_ok(d, ep->n2, ep->out3))))
@@ -1843,7 +2114,7 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         return hipErrorInvalidValue;   // the epilogue reads the stored row back
     if (r1 && r1->a && (!r1->x || (r1->ny > 0 && !r1->y)))
         return hipErrorInvalidValue;
-    const SpmmOut out{out0, out1, n_out0, relu, r1 ? *r1 : SpmmRank1{}};
+    const SpmmOut out{out0, out1, n_out0, relu, r1 ? *r1 : SpmmRank1{}, d, acc};
     int vec = pick_vec(d, src0, out0);
     if (src1 && pick_vec(d, src1, nullptr) < vec)
         vec = pick_vec(d, src1, nullptr);

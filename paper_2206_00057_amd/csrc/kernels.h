@@ -23,6 +23,8 @@ constexpr int kNarrow = 16;
 constexpr int kNarrowWide = 64;
 // Rows with more entries than this get a whole block.
 constexpr int32_t kSpmmLongRow = 64;
+// Rows with more entries than this get a whole block in a sliced pass.
+constexpr int32_t kTierLongRow = 1024;
 
 // dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows.
 hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
@@ -64,12 +66,27 @@ struct SpmmRank1 {
 
 // The first n_long blocks are the long-row blocks (nrows == 0), the rest
 // short-row blocks.
+// acc: add each row's sum to what out already holds.
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep = nullptr,
                        float *out1 = nullptr, int32_t n_out0 = INT32_MAX, bool relu = false,
-                       const SpmmRank1 *r1 = nullptr);
+                       const SpmmRank1 *r1 = nullptr, bool acc = false);
+
+// The same aggregation (one output, no epilogue) as one pass over column
+// slices of kSliceFloats floats, the slices dealt to the 8 XCDs so that each
+// XCD gathers only its slices of the source rows (a set of rows whose slices
+// fit one L2 stays resident there).  Needs rows of an even width with 8-byte
+// aligned sources and output (16-byte for float4 gathers).  acc as above.
+constexpr int kSliceFloats = 32;
+bool spmm_sliced_ok(int32_t d, const float *src0, const float *src1, const float *out0);
+// The rows are 0 .. n_rows-1 of the CSR; blocks lists its work blocks (the
+// n_long long-row blocks first); nnz >= 1 entries.
+hipError_t launch_spmm_sliced(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
+                              const int32_t *rowptr, const int32_t *col, const float *val,
+                              int64_t nnz, const float *src0, const float *src1, int32_t n_src0,
+                              int32_t n_rows, int32_t d, float *out0, bool acc, hipStream_t s);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`
 // slices (each its own grid part) when splits > 1.

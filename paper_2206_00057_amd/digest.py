@@ -432,9 +432,10 @@ class LayerPlan(ctypes.Structure):
     """``digest_layer_plan`` of include/digest.h."""
     _fields_ = [("transform_first", ctypes.c_int32), ("forward_narrow", ctypes.c_int32),
                 ("dw_slices", ctypes.c_int32), ("dgrad_narrow_first", ctypes.c_int32),
-                ("dgrad_fused", ctypes.c_int32), ("hot_rows_fwd", ctypes.c_int32),
-                ("hot_rows_bwd", ctypes.c_int32), ("hot_entries_fwd", ctypes.c_int64),
-                ("hot_entries_bwd", ctypes.c_int64)]
+                ("dgrad_fused", ctypes.c_int32), ("tiers_fwd", ctypes.c_int32),
+                ("tiers_bwd", ctypes.c_int32), ("tier_rows_fwd", ctypes.c_int32),
+                ("tier_rows_bwd", ctypes.c_int32), ("tier_entries_fwd", ctypes.c_int64),
+                ("tier_entries_bwd", ctypes.c_int64)]
 
 
 def digest_partition_plan(p, layer):

@@ -199,3 +199,27 @@ def test_launch_plan_and_cost_model():
     cnt = (ctypes.c_int64 * 1000)()
     assert L.digest_profile_model(h.handle, 7, buf, buf, cnt) == D.EINVAL
     assert L.digest_profile_model(h.handle, 0, None, buf, cnt) == D.EINVAL
+
+
+def test_tier_plan_follows_the_overrides(monkeypatch):
+    """Tiers are planned at create: a forced count with a small L2 budget
+    gives that many tiers of budget / 128 rows (256-wide rows: one 32-float
+    slice per XCD), a zero budget none; the tiers' entries are part of the
+    operand."""
+    widths = [256, 256, 7]
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 2000, widths=widths, classes=7)
+    g = synth.make_graph(cfg)
+    p = synth.make_partition(cfg, g, 0)
+    monkeypatch.setenv("DIGEST_SPMM_TIERS", "2")
+    monkeypatch.setenv("DIGEST_SPMM_TIER_BYTES", "4096")
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, widths)
+    pl = D.digest_partition_plan(h, 1)
+    assert pl["tiers_fwd"] == 2 and pl["tier_rows_fwd"] == 32
+    assert 0 < pl["tier_entries_fwd"] < h.nnz
+    pl2 = D.digest_partition_plan(h, 2)
+    if not pl2["transform_first"]:
+        assert pl2["tiers_bwd"] == 2 and 0 < pl2["tier_entries_bwd"] < h.nnz_in
+    monkeypatch.setenv("DIGEST_SPMM_TIER_BYTES", "0")
+    h0 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, widths)
+    assert D.digest_partition_plan(h0, 1)["tiers_fwd"] == 0
+    assert h0.workspace_bytes < h.workspace_bytes

@@ -561,3 +561,59 @@ def test_empty_partition_with_halo_gives_zero_halo_gradient():
     dh_halo = torch.full((3, widths[1]), float("nan"), device="cuda")
     Dm.digest_layer_backward_halo(h, 2, empty, empty, empty, W, dw, empty, dh_halo)
     assert not host(dh_halo).any() and not host(dw).any()
+
+
+# ---------------------------------------------------------------------------
+# tiered aggregation: sliced passes over the most-read source rows, then the
+# rest, each adding into the output (forced here on small graphs)
+# ---------------------------------------------------------------------------
+
+# (widths, what is tiered): float4 slices at 256 (one slice per XCD) and 264
+# (a partial second slice group), forward and transposed; float2 slices at
+# 602 (three slice groups per XCD)
+TIERED = [(256, 264, 258, 7), (602, 300, 41)]
+
+
+@pytest.mark.parametrize("widths", TIERED, ids=lambda w: "x".join(map(str, w)))
+def test_tiered_aggregation_matches_oracle(widths, monkeypatch):
+    from paper_2206_00057_amd import digest as Dm
+    monkeypatch.setenv("DIGEST_SPMM_TIERS", "3")
+    monkeypatch.setenv("DIGEST_SPMM_TIER_BYTES", "8192")
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 2000, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg)
+    part = synth.scramble_rows(synth.make_partition(cfg, g, 1), seed=5, repeat_frac=0.1,
+                               long_row=400)
+    c = Case(cfg, g, part, label=f"tiered {widths}")
+    plan = Dm.digest_partition_plan(c.h, 1)
+    assert plan["tiers_fwd"] == 3 and 0 < plan["tier_entries_fwd"] < part.nnz, plan
+    if len(widths) == 4:
+        plan2 = Dm.digest_partition_plan(c.h, 2)
+        assert plan2["tiers_fwd"] == 3 and plan2["tiers_bwd"] == 3, plan2
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+
+
+def test_tiering_off_gives_one_pass(monkeypatch):
+    """DIGEST_SPMM_TIER_BYTES=0 plans no tiers; the results agree with the
+    tiered plan's within the float32 bar (the sums are ordered differently)."""
+    from paper_2206_00057_amd import digest as Dm
+    widths = (256, 264, 7)
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 2000, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg)
+    part = synth.make_partition(cfg, g, 2)
+    outs = []
+    for env in ({"DIGEST_SPMM_TIER_BYTES": "0"},
+                {"DIGEST_SPMM_TIER_BYTES": "8192", "DIGEST_SPMM_TIERS": "2"}):
+        for k in ("DIGEST_SPMM_TIER_BYTES", "DIGEST_SPMM_TIERS"):
+            monkeypatch.delenv(k, raising=False)
+        for k, v in env.items():
+            monkeypatch.setenv(k, v)
+        c = Case(cfg, g, part, label=str(env))
+        assert (Dm.digest_partition_plan(c.h, 1)["tiers_fwd"] > 0) == ("DIGEST_SPMM_TIERS" in env)
+        x = c.layer_input(1)
+        W = synth.weights(cfg)[0]
+        Dm.digest_pull(c.h, 0, dev(c.store(0)))
+        out = torch.empty(c.n, widths[1], device="cuda")
+        Dm.digest_layer_forward(c.h, 1, dev(x), dev(W), out, Dm.ACT_RELU)
+        outs.append(host(out))
+    assert_close(outs[1], outs[0], "tiered vs one pass")
