@@ -76,6 +76,10 @@ constexpr int32_t kMaxLayers = 64;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Row stride of a library-owned buffer of rows `d` floats wide: a multiple
+// of 4 floats, so that its rows hold whole 16-byte vectors.
+int32_t padded_width(int32_t d) { return (d + 3) / 4 * 4; }
+
 // Split-K factor for a contraction with an M x N result over K: at least
 // kSplitTarget workgroups in all, at least kSplitMinRows rows of K per split,
 // split starts on GEMM K-tile boundaries.  From that count up to twice it,
@@ -506,7 +510,7 @@ void plan_layout(digest_partition &p)
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
         if (transform_first_cheaper(p, k)) {
-            tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + p.n_halo) * dout);
+            tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + p.n_halo) * padded_width(dout));
             const TfPlan t = tf_plan(p.n_own, p.n_halo, di, dout);
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
         }
@@ -675,7 +679,8 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
                        const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
                        float *out1 = nullptr, int32_t n_out0 = INT32_MAX,
                        const float *val = nullptr, bool relu = false,
-                       const digest::SpmmRank1 *r1 = nullptr)
+                       const digest::SpmmRank1 *r1 = nullptr, int32_t lds = 0,
+                       int32_t out_ld = 0, int32_t out_w = 0)
 {
     const bool fwd = which == Csr::Fwd;
     const std::vector<SpmmBlock> *blocks = &p->blocks_f;
@@ -694,6 +699,7 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     Timed t(p, kind >= 0 ? kind : (fwd ? K_SPMM_FWD : K_SPMM_BWD), layer, s);
     const TierPlan *tp = find_tiers(*p, which, d);
     if (tp && !ep && !val && !relu && !(r1 && r1->a) && n_out0 == INT32_MAX && !out1 &&
+        (lds == 0 || lds == d) && (out_ld == 0 || out_ld == d) && (out_w == 0 || out_w == d) &&
         digest::spmm_sliced_ok(d, src0, src1, out)) {
         // sliced passes over the tiers, then the rest, each adding into out
         const int32_t n_rows = p->n_own;
@@ -721,7 +727,8 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
                             p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
                             val ? val : p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1,
-                            n_src0, d, out, s, ep, out1, n_out0, relu, r1),
+                            n_src0, d, out, s, ep, out1, n_out0, relu, r1, false, lds, out_ld,
+                            out_w),
         "spmm");
 }
 
@@ -729,12 +736,13 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
 // [n_own + n_halo][d_out]): the narrow-output kernel with W in LDS when the
 // widths allow, else the MFMA GEMM for the owned and for the halo rows.
 digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_own,
-                             const float *halo, const float *w, float *T, hipStream_t s)
+                             const float *halo, const float *w, float *T, int32_t ldt,
+                             hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     if (narrow_out(d_in, d_out))
         return hip_check(digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out,
-                                                 h_own, halo, d_in, w, T, d_out, false, s),
+                                                 h_own, halo, d_in, w, T, ldt, false, s),
                          "transform");
     digest::GemmArgs g{};
     g.N = d_out;
@@ -742,7 +750,7 @@ digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_
     g.lda = d_in;
     g.B = w;
     g.ldb = d_out;
-    g.ldc = d_out;
+    g.ldc = ldt;
     g.splits = 1;
     g.kchunk = d_in;
     if (p->n_own > 0) {
@@ -757,7 +765,7 @@ digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_
         g.M = p->n_halo;
         g.tile = gemm_tile_for(g.M, d_out, d_in, false);
         g.A = halo;
-        g.C = T + (int64_t)p->n_own * d_out;
+        g.C = T + (int64_t)p->n_own * ldt;
         if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
             return st;
     }
@@ -1128,14 +1136,18 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
     const bool tf = act == DIGEST_ACT_IDENTITY && transform_first_cheaper(*p, layer);
     if (p->n_own > 0 && tf) {
         // T = [h_in; halo] W over all local rows, then h_out = P_m T.
+        // T's rows are padded to a multiple of 4 floats so that the
+        // aggregation gathers whole float4 vectors; it stores d_out columns
         float *T = p->at<float>(p->lay.tbuf);
+        const int32_t ldt = padded_width(d_out);
         {
             Timed t(p, K_GEMM_FWD, layer, s);
-            if (digest_status st = transform_rows(p, layer, h_in, halo, w, T, s))
+            if (digest_status st = transform_rows(p, layer, h_in, halo, w, T, ldt, s))
                 return st;
         }
-        if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, d_out,
-                                        h_out, layer, s))
+        if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, ldt,
+                                        h_out, layer, s, nullptr, -1, nullptr, INT32_MAX,
+                                        nullptr, false, nullptr, ldt, d_out, d_out))
             return st;
     } else if (p->n_own > 0) {
         // AH = P_in h_in + P_out halo (kept for the backward), then act(AH W).
@@ -1180,21 +1192,21 @@ namespace {
 // C[rows][d_in] = A[rows][d_out] W^T (W row-major [d_in][d_out]): the VALU
 // kernel for contractions up to kNarrow long, the MFMA kernel with W in LDS
 // up to kTimesWtK, else the MFMA GEMM.
-digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A, const float *w,
-                       float *C, hipStream_t s)
+digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A, int32_t lda,
+                       const float *w, float *C, hipStream_t s)
 {
     if (narrow_valu(d_in, d_out))
-        return hip_check(digest::launch_narrow_k(rows, d_in, d_out, A, d_out, w, C, d_in, s),
+        return hip_check(digest::launch_narrow_k(rows, d_in, d_out, A, lda, w, C, d_in, s),
                          "times W^T (narrow)");
     if (d_out <= digest::kTimesWtK && digest::times_wt_lds(d_out, d_in) <= digest::kNarrowNLds)
-        return hip_check(digest::launch_times_wt(rows, d_in, d_out, A, d_out, w, C, d_in, s),
+        return hip_check(digest::launch_times_wt(rows, d_in, d_out, A, lda, w, C, d_in, s),
                          "times W^T (short)");
     digest::GemmArgs h{};
     h.M = rows;
     h.N = d_in;
     h.K = d_out;
     h.A = A;
-    h.lda = d_out;
+    h.lda = lda;
     h.B = w;
     h.ldb = d_out;
     h.b_trans = true;
@@ -1207,12 +1219,13 @@ digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A
 }
 
 // dw = [h_own; halo]^T G over the n_own + n_halo local rows (G row-major
-// [n_own + n_halo][d_out]): split-K slices in `part`, summed in slice order.
+// [n_own + n_halo][d_out], leading dim ldg): split-K slices in `part`,
+// summed in slice order.
 // Outputs up to kNarrow wide use the narrow MFMA kernel, wider ones the
 // GEMM over the owned rows and over the halo rows.
 digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *h_in,
-                               const float *halo, const float *G, float *gpart, float *dw,
-                               hipStream_t s, int32_t kind_dw, int32_t kind_reduce)
+                               const float *halo, const float *G, int32_t ldg, float *gpart,
+                               float *dw, hipStream_t s, int32_t kind_dw, int32_t kind_reduce)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
@@ -1221,7 +1234,7 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
         if (t.valu) {
             if (digest_status st = hip_check(
                     digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
-                                             halo, d_in, G, t.chunk, t.slices, gpart, s),
+                                             halo, d_in, G, ldg, t.chunk, t.slices, gpart, s),
                     "dW narrow"))
                 return st;
         } else {
@@ -1230,7 +1243,7 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
             g.N = d_out;
             g.lda = d_in;
             g.a_trans = true;
-            g.ldb = d_out;
+            g.ldb = ldg;
             g.ldc = d_out;
             g.K = p->n_own;
             g.A = h_in;
@@ -1244,7 +1257,7 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
             if (p->n_halo > 0) {
                 g.K = p->n_halo;
                 g.A = halo;
-                g.B = G + (int64_t)p->n_own * d_out;
+                g.B = G + (int64_t)p->n_own * ldg;
                 g.splits = t.s_halo;
                 g.kchunk = t.k_halo;
                 g.tile = gemm_tile_for(d_in, d_out, g.K, true);
@@ -1273,7 +1286,10 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    // G's rows are padded like T's, so that the products that read it load
+    // whole vectors
     float *G = p->at<float>(p->lay.tbuf);
+    const int32_t ldg = padded_width(d_out);
     float *gpart = p->at<float>(p->lay.gemm_part);
     // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
     // same launch also writes dh_in = G_own W^T for the owned rows.
@@ -1282,22 +1298,23 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                           (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
     const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
     if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
-                                    fused_dh ? &ep : nullptr))
+                                    fused_dh ? &ep : nullptr, -1, nullptr, INT32_MAX, nullptr,
+                                    false, nullptr, d_out, ldg, d_out))
         return st;
-    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, G, gpart, dw, s, K_GEMM_DW,
-                                            K_REDUCE_DW))
+    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, G, ldg, gpart, dw, s,
+                                            K_GEMM_DW, K_REDUCE_DW))
         return st;
     if (fused_dh)
         return DIGEST_OK;
     if (dh_in) {
         Timed tm(p, K_GEMM_DH, layer, s);
-        if (digest_status st = times_wt(p->n_own, d_in, d_out, G, w, dh_in, s))
+        if (digest_status st = times_wt(p->n_own, d_in, d_out, G, ldg, w, dh_in, s))
             return st;
     }
     if (!dh_halo || p->n_halo == 0)
         return DIGEST_OK;
     Timed tm(p, K_HALO_GRAD, layer, s);
-    return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * d_out, w, dh_halo, s);
+    return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * ldg, ldg, w, dh_halo, s);
 }
 
 }  // namespace
@@ -1370,13 +1387,13 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
             return st;
         {
             Timed t(p, K_GEMM_DH, layer, s);
-            if (digest_status st = times_wt(p->n_own, d_in, d_out, tmp, w, dh_in, s))
+            if (digest_status st = times_wt(p->n_own, d_in, d_out, tmp, d_out, w, dh_in, s))
                 return st;
         }
         if (!dh_halo)
             return DIGEST_OK;
         Timed t(p, K_HALO_GRAD, layer, s);
-        return times_wt(p->n_halo, d_in, d_out, gh, w, dh_halo, s);
+        return times_wt(p->n_halo, d_in, d_out, gh, d_out, w, dh_halo, s);
     }
     // Otherwise G = D W^T (mask fused into the operand load), then the
     // transposed aggregation of G.
@@ -1555,7 +1572,7 @@ digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const flo
                                         layer, s, nullptr, K_HALO_GRAD))
             return st;
         Timed t(p, K_HALO_GRAD, layer, s);
-        return times_wt(p->n_halo, d_in, d_out, gh, w, dh_halo, s);
+        return times_wt(p->n_halo, d_in, d_out, gh, d_out, w, dh_halo, s);
     }
     // otherwise P_out^T (D W^T), with the ReLU mask fused into the GEMM
     float *tmp = p->at<float>(p->lay.tmp);
@@ -1703,7 +1720,7 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
     float *alpha = p->gat<float>(p->glay.alpha[layer]);
     {
         Timed t(p, K_GAT_TRANSFORM, layer, s);
-        if (digest_status st = transform_rows(p, layer, h_in, halo, w, Z, s))
+        if (digest_status st = transform_rows(p, layer, h_in, halo, w, Z, p->widths[layer], s))
             return st;
     }
     {
@@ -1823,7 +1840,7 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
         narrow_rows_plan(R, d_out, chunk, slices);
         Timed t(p, K_GAT_DATT, layer, s);
         if (digest_status st = hip_check(
-                digest::launch_dw_narrow(R, R, d_out, 2, Z, nullptr, d_out, g2, chunk, slices,
+                digest::launch_dw_narrow(R, R, d_out, 2, Z, nullptr, d_out, g2, 2, chunk, slices,
                                          part, s),
                 "GAT datt"))
             return st;
@@ -1832,13 +1849,13 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
                 "GAT datt reduce"))
             return st;
     }
-    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, dz, part, dw, s, K_GAT_DW,
+    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, dz, d_out, part, dw, s, K_GAT_DW,
                                             K_REDUCE_DW))
         return st;
     if (!dh_in || p->n_own == 0)
         return DIGEST_OK;
     Timed t(p, K_GAT_DGRAD, layer, s);
-    return times_wt(p->n_own, d_in, d_out, dz, w, dh_in, s);
+    return times_wt(p->n_own, d_in, d_out, dz, d_out, w, dh_in, s);
 }
 
 digest_status digest_sync_period(int32_t K, int64_t iter, int32_t *do_pull, int32_t *do_push)

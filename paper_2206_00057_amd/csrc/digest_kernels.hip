@@ -204,6 +204,9 @@ constexpr int spmm_inflight(int groups, int nch, int vec)
 // a split lets one launch over P_m^T write the owned rows and the halo rows
 // to buffers of their own.  With acc the row's sum is added to what the
 // output already holds (a later pass over more entries of the same rows).
+// Only the first w columns are stored (the gathered rows may be padded
+// wider); vst says whether a vector of the gather's width may be stored as
+// one (the output's rows are aligned for it), else the columns go one by one.
 struct SpmmOut {
     float *out0;
     float *out1;
@@ -212,6 +215,8 @@ struct SpmmOut {
     SpmmRank1 r1;   // rank-one terms added first when r1.a is set
     int32_t ld;     // row stride of out0 and out1 (floats)
     bool acc;       // out = out + sum
+    int32_t w;      // stored columns
+    bool vst;       // vector stores allowed
 
     __device__ __forceinline__ float *row(int32_t r) const
     {
@@ -232,9 +237,17 @@ struct SpmmOut {
     template <int VEC>
     __device__ __forceinline__ void put(int32_t r, int32_t off, float (&v)[VEC]) const
     {
+        float *p = row(r) + off;
+        const bool whole = vst && off + VEC <= w;
         if (acc) {
             float prev[VEC];
-            load_vec<VEC>(row(r) + off, prev);
+            if (whole) {
+                load_vec<VEC>(p, prev);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i)
+                    prev[i] = off + i < w ? p[i] : 0.f;
+            }
 #pragma unroll
             for (int i = 0; i < VEC; ++i)
                 v[i] += prev[i];
@@ -251,7 +264,14 @@ struct SpmmOut {
                 v[i] = relu ? fmaxf(t, 0.f) : t;
             }
         }
-        store_vec<VEC>(row(r) + off, v);
+        if (whole) {
+            store_vec<VEC>(p, v);
+        } else {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i)
+                if (off + i < w)
+                    p[i] = v[i];
+        }
     }
 };
 
@@ -379,7 +399,7 @@ __device__ __forceinline__ void spmm_block(const SpmmBlock b, const int32_t *__r
             __syncthreads();
             for (int t = threadIdx.x; t < SPAN * VEC; t += kSpmmThreads) {
                 const int c = c0 + t / VEC;
-                if (c < dv) {
+                if (c < dv && c * VEC + t % VEC < out.w) {
                     float sum = 0.f;
 #pragma unroll
                     for (int w = 0; w < kSpmmWaves; ++w)
@@ -459,13 +479,12 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
     const SpmmBlock *__restrict__ blocks, int32_t n_long, int32_t n_blocks,
     const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
     const float *__restrict__ val, const float *__restrict__ src0, const float *__restrict__ src1,
-    int32_t n_src0, int32_t d, SpmmOut out, SpmmEpilogue ep)
+    int32_t n_src0, int32_t d, int32_t lds, SpmmOut out, SpmmEpilogue ep)
 {
     static_assert(!EP || (NCH == 1 && GL * VEC <= kNarrow), "epilogue rows are kNarrow wide");
     static_assert(!SL || !EP, "no epilogue on a sliced pass");
     __shared__ float red[kSpmmWaves][NCH * GL * VEC];
     int32_t wb = (int32_t)blockIdx.x;   // work block
-    int32_t lds = d;                    // source row stride
     if constexpr (SL) {
         const int32_t q = (d + kXcds * kSliceFloats - 1) / (kXcds * kSliceFloats);
         const int32_t off = (wb % kXcds + kXcds * ((wb / kXcds) % q)) * kSliceFloats;
@@ -479,6 +498,7 @@ __global__ __launch_bounds__(kSpmmThreads) void k_spmm_narrow(
         if (out.out1)
             out.out1 += off;
         d = min(kSliceFloats, d - off);
+        out.w = d;
     }
     extern __shared__ float ws[];   // EP: w as [k][n2]
     if constexpr (EP) {
@@ -632,6 +652,7 @@ __global__ __launch_bounds__(256) void k_spmm_tier(
             src1 += off;
         out.out0 += off;
         d = min(kSliceFloats, d - off);
+        out.w = d;
     }
     const int lane = threadIdx.x & (kWave - 1);
     const int g = lane / GL, gl = lane % GL;
@@ -1254,8 +1275,9 @@ __global__ __launch_bounds__(256) void k_narrow_k(int32_t M, int32_t N, int32_t 
 __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N,
                                                    const float *__restrict__ H0,
                                                    const float *__restrict__ H1, int32_t ldh,
-                                                   const float *__restrict__ G, int32_t chunk,
-                                                   int32_t splits, float *__restrict__ part)
+                                                   const float *__restrict__ G, int32_t ldg,
+                                                   int32_t chunk, int32_t splits,
+                                                   float *__restrict__ part)
 {
     constexpr int SB = 8;   // MFMA steps (32 rows) per batch of loads
     const int lane = threadIdx.x & (kWave - 1);
@@ -1285,7 +1307,7 @@ __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_
                 av[s][q] = okf ? v : 0.f;
             }
             const bool okg = ok && m < N;
-            const float g = *(okg ? G + (int64_t)r * N + m : G);
+            const float g = *(okg ? G + (int64_t)r * ldg + m : G);
             bv[s] = okg ? g : 0.f;
         }
 #pragma unroll
@@ -1839,7 +1861,7 @@ template <int VEC, int GL, int NCH, bool TWO>
 hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_blocks,
                          const int32_t *rowptr, const int32_t *col, const float *val,
                          const float *src0, const float *src1, int32_t n_src0, int32_t d,
-                         SpmmOut out, const SpmmEpilogue *ep, hipStream_t s)
+                         int32_t lds, SpmmOut out, const SpmmEpilogue *ep, hipStream_t s)
 {
     constexpr int NB = narrow_nb(GL, NCH, VEC);
     const int64_t grid = n_long + ((int64_t)(n_blocks - n_long) + kSpmmWaves - 1) / kSpmmWaves;
@@ -1847,10 +1869,10 @@ hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_bloc
         return hipErrorInvalidConfiguration;
     if constexpr (NCH == 1 && GL * VEC <= kNarrow) {
         if (ep) {
-            const size_t lds = sizeof(float) * (size_t)d * ep->n2;
+            const size_t lds_bytes = sizeof(float) * (size_t)d * ep->n2;
             hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, NCH, NB, TWO, true>), dim3((unsigned)grid),
-                               dim3(kSpmmThreads), lds, s, blocks, n_long, n_blocks, rowptr, col,
-                               val, src0, src1, n_src0, d, out, *ep);
+                               dim3(kSpmmThreads), lds_bytes, s, blocks, n_long, n_blocks, rowptr,
+                               col, val, src0, src1, n_src0, d, lds, out, *ep);
             return hipGetLastError();
         }
     } else {
@@ -1859,17 +1881,17 @@ hipError_t spmm_narrow_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_bloc
     }
     hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, NCH, NB, TWO, false>), dim3((unsigned)grid),
                        dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val, src0,
-                       src1, n_src0, d, out, SpmmEpilogue{});
+                       src1, n_src0, d, lds, out, SpmmEpilogue{});
     return hipGetLastError();
 }
 
 template <int VEC, int GL, int NCH, bool TWO>
 hipError_t spmm_t(const SpmmBlock *blocks, int32_t n_blocks, const int32_t *rowptr,
                   const int32_t *col, const float *val, const float *src0, const float *src1,
-                  int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
+                  int32_t n_src0, int32_t d, int32_t lds, SpmmOut out, hipStream_t s)
 {
     hipLaunchKernelGGL((k_spmm<VEC, GL, NCH, TWO>), dim3((unsigned)n_blocks), dim3(kSpmmThreads),
-                       0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, d, out);
+                       0, s, blocks, rowptr, col, val, src0, src1, n_src0, d, lds, out);
     return hipGetLastError();
 }
 
@@ -1890,16 +1912,17 @@ hipError_t spmm_sliced_t(const SpmmBlock *blocks, int32_t n_long, int32_t n_bloc
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((k_spmm_narrow<VEC, GL, 1, NB, TWO, false, true>), dim3((unsigned)grid),
                        dim3(kSpmmThreads), 0, s, blocks, n_long, n_blocks, rowptr, col, val, src0,
-                       src1, n_src0, d, out, SpmmEpilogue{});
+                       src1, n_src0, d, d, out, SpmmEpilogue{});
     return hipGetLastError();
 }
 
-#define DIGEST_SPMM_ARGS blocks, n_blocks, rowptr, col, val, src0, src1, n_src0, d, out, s
+#define DIGEST_SPMM_ARGS blocks, n_blocks, rowptr, col, val, src0, src1, n_src0, d, lds, out, s
 
 template <int VEC, bool TWO>
 hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
                   const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
-                  const float *src1, int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
+                  const float *src1, int32_t n_src0, int32_t d, int32_t lds, SpmmOut out,
+                  hipStream_t s)
 {
     switch (gl) {
     case 4: return spmm_t<VEC, 4, 1, TWO>(DIGEST_SPMM_ARGS);
@@ -1931,7 +1954,8 @@ hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
 template <bool TWO>
 hipError_t spmm_v(int vec, int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
                   const int32_t *rowptr, const int32_t *col, const float *val, const float *src0,
-                  const float *src1, int32_t n_src0, int32_t d, SpmmOut out, hipStream_t s)
+                  const float *src1, int32_t n_src0, int32_t d, int32_t lds, SpmmOut out,
+                  hipStream_t s)
 {
     switch (vec) {
     case 4: return spmm_g<4, TWO>(gl, nch, DIGEST_SPMM_ARGS);
@@ -2074,7 +2098,7 @@ hipError_t launch_spmm_sliced(const SpmmBlock *blocks, int32_t n_blocks, int32_t
         return hipSuccess;
     if (n_long < 0 || n_long > n_blocks || nnz < 1)
         return hipErrorInvalidValue;   // padding entries reread entry 0
-    const SpmmOut out{out0, nullptr, INT32_MAX, false, SpmmRank1{}, d, acc};
+    const SpmmOut out{out0, nullptr, INT32_MAX, false, SpmmRank1{}, d, acc, d, true};
     // every slice starts on a multiple of kSliceFloats, so the vector width
     // of the whole row is the slices' too
     int vec = pick_vec(d, src0, out0);
@@ -2101,8 +2125,14 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep, float *out1,
-                       int32_t n_out0, bool relu, const SpmmRank1 *r1, bool acc)
+                       int32_t n_out0, bool relu, const SpmmRank1 *r1, bool acc, int32_t lds,
+                       int32_t out_ld, int32_t out_w)
 {
+    lds = lds > 0 ? lds : d;
+    out_ld = out_ld > 0 ? out_ld : d;
+    out_w = out_w > 0 ? out_w : d;
+    if (lds < d || out_w > d || out_ld < out_w)
+        return hipErrorInvalidValue;
     if (ep && (!spmm_epilogue_ok(d, ep->n2, ep->out2) ||
                (ep->out3 && !spmm_epilogue_ok(d, ep->n2, ep->out3))))
         return hipErrorInvalidValue;
@@ -2114,12 +2144,16 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         return hipErrorInvalidValue;   // the epilogue reads the stored row back
     if (r1 && r1->a && (!r1->x || (r1->ny > 0 && !r1->y)))
         return hipErrorInvalidValue;
-    const SpmmOut out{out0, out1, n_out0, relu, r1 ? *r1 : SpmmRank1{}, d, acc};
-    int vec = pick_vec(d, src0, out0);
+    // the gather's vector width follows the sources (width, stride and
+    // alignment); the stores use it where the output's rows allow, else go
+    // column by column
+    int vec = pick_vec(d, src0, nullptr);
+    if (lds % vec)
+        vec = lds % 2 ? 1 : std::min(vec, 2);
     if (src1 && pick_vec(d, src1, nullptr) < vec)
         vec = pick_vec(d, src1, nullptr);
-    if (out1 && pick_vec(d, out1, nullptr) < vec)
-        vec = pick_vec(d, out1, nullptr);
+    const bool vst = out_ld % vec == 0 && pick_vec(vec, out0, out1) >= vec;
+    const SpmmOut out{out0, out1, n_out0, relu, r1 ? *r1 : SpmmRank1{}, out_ld, acc, out_w, vst};
     const int dv = d / vec;
     const int gl = pick_group(dv);
     // rows of at most kNarrowWide floats: the row-per-lane-group kernel, in
@@ -2135,9 +2169,9 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         const int nnch = (dv + ngl - 1) / ngl;
 #define DIGEST_NARROW(V, L, C)                                                                   \
     return src1 ? spmm_narrow_t<V, L, C, true>(blocks, n_long, n_blocks, rowptr, col, val,      \
-                                               src0, src1, n_src0, d, out, ep, s)              \
+                                               src0, src1, n_src0, d, lds, out, ep, s)         \
                 : spmm_narrow_t<V, L, C, false>(blocks, n_long, n_blocks, rowptr, col, val,     \
-                                                src0, src1, n_src0, d, out, ep, s)
+                                                src0, src1, n_src0, d, lds, out, ep, s)
         if (vec == 4) {   // dv <= 16
             if (ngl == 4) DIGEST_NARROW(4, 4, 1);
             if (ngl == 8) DIGEST_NARROW(4, 8, 1);
@@ -2395,15 +2429,15 @@ hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int3
 }
 
 hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
-                            const float *H1, int32_t ldh, const float *G, int32_t chunk,
-                            int32_t splits, float *part, hipStream_t s)
+                            const float *H1, int32_t ldh, const float *G, int32_t ldg,
+                            int32_t chunk, int32_t splits, float *part, hipStream_t s)
 {
     if (F <= 0 || N <= 0)
         return hipSuccess;
     if (N > kNarrow || splits < 1 || chunk < 1)
         return hipErrorInvalidValue;
     const dim3 grid((unsigned)((F + 63) / 64), (unsigned)((splits + 3) / 4));
-    hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, G, chunk,
+    hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, G, ldg, chunk,
                        splits, part);
     return hipGetLastError();
 }

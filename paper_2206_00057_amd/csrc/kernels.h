@@ -66,13 +66,18 @@ struct SpmmRank1 {
 
 // The first n_long blocks are the long-row blocks (nrows == 0), the rest
 // short-row blocks.
-// acc: add each row's sum to what out already holds.
+// acc: add each row's sum to what out already holds.  Rows are gathered d
+// floats wide from sources of row stride lds (0: d) and stored out_w (0: d)
+// floats wide, out_w <= d, into outputs of row stride out_ld (0: d); a
+// gather padded wider than the output lets rows of odd width load whole
+// vectors (the padding columns are summed and not stored).
 hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long,
                        const int32_t *rowptr, const int32_t *col, const float *val,
                        const float *src0, const float *src1, int32_t n_src0, int32_t d,
                        float *out0, hipStream_t s, const SpmmEpilogue *ep = nullptr,
                        float *out1 = nullptr, int32_t n_out0 = INT32_MAX, bool relu = false,
-                       const SpmmRank1 *r1 = nullptr, bool acc = false);
+                       const SpmmRank1 *r1 = nullptr, bool acc = false, int32_t lds = 0,
+                       int32_t out_ld = 0, int32_t out_w = 0);
 
 // The same aggregation (one output, no epilogue) as one pass over column
 // slices of kSliceFloats floats, the slices dealt to the 8 XCDs so that each
@@ -146,10 +151,11 @@ hipError_t launch_times_wt(int32_t M, int32_t N, int32_t K, const float *A, int3
 
 // part[z][f][n] = sum over rows r in [z*chunk, (z+1)*chunk) of H(r)[f] G[r][n]
 // (f < F, n < N <= kNarrow; H(r) from H0 for r < m0 else H1, leading dim
-// ldh; G row-major [R][N]).  Sum the slices with launch_splitk_reduce.
+// ldh; G row-major with leading dim ldg).  Sum the slices with
+// launch_splitk_reduce.
 hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
-                            const float *H1, int32_t ldh, const float *G, int32_t chunk,
-                            int32_t splits, float *part, hipStream_t s);
+                            const float *H1, int32_t ldh, const float *G, int32_t ldg,
+                            int32_t chunk, int32_t splits, float *part, hipStream_t s);
 
 // Row-wise softmax cross entropy (C >= 1): dlogits and the per-block loss
 // sums (softmax_xent_blocks(n, C) floats); launch_loss_mean then writes
