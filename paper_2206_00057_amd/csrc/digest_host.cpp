@@ -60,6 +60,7 @@ enum Kind : int32_t {
     K_GAT_DATT,
     K_GAT_DW,
     K_GAT_DGRAD,
+    K_PAD_ROWS,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
@@ -68,7 +69,7 @@ const char *const kKindNames[K_COUNT] = {
     "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
     "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
     "gat_aggregate_transposed", "gat_score_grad", "gat_score_sums", "gat_datt", "gat_dw",
-    "gat_dgrad"};
+    "gat_dgrad", "pad_rows"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -341,9 +342,10 @@ struct digest_partition {
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
-        std::vector<size_t> halo_buf;   // per level 0..L-1
-        std::vector<size_t> ah;         // per layer 1..L (index 0 unused)
+        std::vector<size_t> halo_buf;   // per level 0..L-1, rows padded_width(d_level) apart
+        std::vector<size_t> ah;         // per layer 1..L (index 0 unused), padded rows
         size_t tmp, tmp_halo, tbuf, gemm_part, loss_part;
+        size_t hpad;                    // a padded copy of h_in for widths not a multiple of 4
         size_t total;
     } lay{};
 
@@ -497,10 +499,15 @@ void plan_layout(digest_partition &p)
     l.blocks_th = take(sizeof(SpmmBlock) * p.blocks_th.size());
     l.halo_buf.assign(p.L, 0);
     for (int32_t lev = 0; lev < p.L; ++lev)
-        l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * p.widths[lev]);
+        l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * padded_width(p.widths[lev]));
     l.ah.assign(p.L + 1, 0);
-    for (int32_t k = 1; k <= p.L; ++k)
-        l.ah[k] = take(sizeof(float) * (size_t)p.n_own * p.widths[k - 1]);
+    int64_t hpad = 0;
+    for (int32_t k = 1; k <= p.L; ++k) {
+        l.ah[k] = take(sizeof(float) * (size_t)p.n_own * padded_width(p.widths[k - 1]));
+        if (p.widths[k - 1] % 4)
+            hpad = std::max<int64_t>(hpad, (int64_t)p.n_own * padded_width(p.widths[k - 1]));
+    }
+    l.hpad = take(sizeof(float) * (size_t)hpad);
     int64_t wmax = 0, gemm_part = 0, tbuf = 0;
     for (int32_t k = 1; k <= p.L; ++k) {
         const int64_t di = p.widths[k - 1], dout = p.widths[k];
@@ -660,7 +667,7 @@ void plan_tiers(digest_partition &p)
         const bool relu = l < p.L;
         if (!relu && p.n_own > 0 && transform_first_cheaper(p, l))
             continue;
-        want(Csr::Fwd, d_in);
+        want(Csr::Fwd, padded_width(d_in));
         if (l > 1)
             want(Csr::InT, (!relu && d_out < d_in) ? d_out : d_in);
     }
@@ -742,7 +749,8 @@ digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     if (narrow_out(d_in, d_out))
         return hip_check(digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out,
-                                                 h_own, halo, d_in, w, T, ldt, false, s),
+                                                 h_own, halo, d_in, w, T, ldt, false, s,
+                                                 padded_width(d_in)),
                          "transform");
     digest::GemmArgs g{};
     g.N = d_out;
@@ -765,6 +773,7 @@ digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_
         g.M = p->n_halo;
         g.tile = gemm_tile_for(g.M, d_out, d_in, false);
         g.A = halo;
+        g.lda = padded_width(d_in);
         g.C = T + (int64_t)p->n_own * ldt;
         if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
             return st;
@@ -1060,11 +1069,12 @@ digest_status digest_partition_read_halo(const digest_partition *p, int32_t leve
         return st;
     if (level < 0 || level >= p->L || !out)
         return fail(DIGEST_EINVAL, "bad level %d or NULL output", level);
-    const size_t bytes = sizeof(float) * (size_t)p->n_halo * p->widths[level];
-    if (!bytes)
+    if (p->n_halo == 0)
         return DIGEST_OK;
-    return hip_check(hipMemcpyAsync(out, p->at<float>(p->lay.halo_buf[level]), bytes,
-                                    hipMemcpyDeviceToDevice, (hipStream_t)hip_stream),
+    const int32_t d = p->widths[level];
+    return hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_halo, d,
+                                              p->at<float>(p->lay.halo_buf[level]), out,
+                                              (hipStream_t)hip_stream, padded_width(d), d),
                      "read halo");
 }
 
@@ -1083,7 +1093,8 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
         digest_status st = hip_check(
             digest::launch_copy_rows(p->at<int32_t>(p->lay.halo_gid), nullptr, p->n_halo,
                                      p->widths[level], store,
-                                     p->at<float>(p->lay.halo_buf[level]), s),
+                                     p->at<float>(p->lay.halo_buf[level]), s, p->widths[level],
+                                     padded_width(p->widths[level])),
             "pull");
         if (st)
             return st;
@@ -1151,13 +1162,27 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             return st;
     } else if (p->n_own > 0) {
         // AH = P_in h_in + P_out halo (kept for the backward), then act(AH W).
+        // Rows whose width is not a multiple of 4 floats are gathered from
+        // padded copies (the halo buffer is padded, h_in is copied), so that
+        // the aggregation loads whole float4 vectors; AH keeps the padding.
         float *ah = p->at<float>(p->lay.ah[layer]);
-        if (digest_status st = run_spmm(p, Csr::Fwd, h_in, halo, p->n_own, d_in, ah, layer, s))
+        const int32_t lh = padded_width(d_in);
+        const float *src0 = h_in;
+        if (lh != d_in) {
+            float *hp = p->at<float>(p->lay.hpad);
+            Timed t(p, K_PAD_ROWS, layer, s);
+            if (digest_status st = hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_own,
+                                                                      d_in, h_in, hp, s, d_in, lh),
+                                             "pad rows"))
+                return st;
+            src0 = hp;
+        }
+        if (digest_status st = run_spmm(p, Csr::Fwd, src0, halo, p->n_own, lh, ah, layer, s))
             return st;
         Timed t(p, K_GEMM_FWD, layer, s);
         if (narrow_out(d_in, d_out)) {
             if (digest_status st = hip_check(
-                    digest::launch_narrow_n(p->n_own, p->n_own, d_in, d_out, ah, nullptr, d_in, w,
+                    digest::launch_narrow_n(p->n_own, p->n_own, d_in, d_out, ah, nullptr, lh, w,
                                             h_out, d_out, act == DIGEST_ACT_RELU, s),
                     "forward transform"))
                 return st;
@@ -1167,7 +1192,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             g.N = d_out;
             g.K = d_in;
             g.A = ah;
-            g.lda = d_in;
+            g.lda = lh;
             g.B = w;
             g.ldb = d_out;
             g.C = h_out;
@@ -1234,7 +1259,8 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
         if (t.valu) {
             if (digest_status st = hip_check(
                     digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
-                                             halo, d_in, G, ldg, t.chunk, t.slices, gpart, s),
+                                             halo, d_in, G, ldg, t.chunk, t.slices, gpart, s,
+                                             padded_width(d_in)),
                     "dW narrow"))
                 return st;
         } else {
@@ -1257,6 +1283,7 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
             if (p->n_halo > 0) {
                 g.K = p->n_halo;
                 g.A = halo;
+                g.lda = padded_width(d_in);
                 g.B = G + (int64_t)p->n_own * ldg;
                 g.splits = t.s_halo;
                 g.kchunk = t.k_halo;
@@ -1346,7 +1373,7 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
     g.N = d_out;
     g.K = p->n_own;
     g.A = ah;
-    g.lda = d_in;
+    g.lda = padded_width(d_in);
     g.a_trans = true;
     g.B = dh_out;
     g.ldb = d_out;
@@ -1932,7 +1959,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
         splitk_plan(d_in, d_out, p.n_own, splits, kchunk);
         pl.dw_slices = splits;
         pl.dgrad_narrow_first = !relu && d_out < d_in;
-        if (const TierPlan *t = find_tiers(p, Csr::Fwd, d_in)) {
+        if (const TierPlan *t = find_tiers(p, Csr::Fwd, padded_width(d_in))) {
             pl.tiers_fwd = t->tiers;
             pl.tier_rows_fwd = t->rows_per_tier;
             pl.tier_entries_fwd = t->tier_entries;
@@ -2024,6 +2051,8 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
             continue;
         }
         put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * di + 4 * n * di, 0.0, p->nnz);
+        if (p->widths[l - 1] % 4)   // the padded copy of h_in
+            put(K_PAD_ROWS, l, 4 * n * (di + padded_width(p->widths[l - 1])));
         put(K_GEMM_FWD, l, 4 * (n * di + di * dout + n * dout), 2 * n * di * dout);
         put(K_GEMM_DW, l, 4 * (n * di + n * dout * (relu ? 2 : 1) + di * dout),
             2 * n * di * dout);

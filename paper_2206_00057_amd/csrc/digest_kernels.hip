@@ -138,8 +138,8 @@ template <int VEC, int GL, int MODE>
 __global__ __launch_bounds__(256) void k_copy_rows(const int32_t *__restrict__ sidx,
                                                    const int32_t *__restrict__ didx,
                                                    int32_t n_rows, int32_t d,
-                                                   float *__restrict__ src,
-                                                   float *__restrict__ dst)
+                                                   float *__restrict__ src, int32_t lds,
+                                                   float *__restrict__ dst, int32_t ldd)
 {
     constexpr int G = kWave / GL;
     const int lane = threadIdx.x & (kWave - 1);
@@ -150,8 +150,8 @@ __global__ __launch_bounds__(256) void k_copy_rows(const int32_t *__restrict__ s
     const int gl = lane % GL;
     const int64_t sr = sidx ? sidx[r] : r;
     const int64_t dr = didx ? didx[r] : r;
-    float *sp = src + sr * d;
-    float *t = dst + dr * d;
+    float *sp = src + sr * lds;
+    float *t = dst + dr * ldd;
     const int dv = d / VEC;
     for (int c = gl; c < dv; c += GL) {
         float x[VEC];
@@ -1061,6 +1061,7 @@ template <bool VEC, int NB>
 __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N,
                                                   const float *__restrict__ A0,
                                                   const float *__restrict__ A1, int32_t lda,
+                                                  int32_t lda1,
                                                   const float *__restrict__ B,
                                                   float *__restrict__ C, int32_t ldc, bool relu)
 {
@@ -1083,7 +1084,7 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
         const int64_t r = row0 + m;
         const bool row_ok = r < M;   // a lane past M loads the first element, stores nothing
         const float *a =
-            !row_ok ? A0 : (r < m0 ? A0 + r * lda : A1 + (r - m0) * (int64_t)lda);
+            !row_ok ? A0 : (r < m0 ? A0 + r * lda : A1 + (r - m0) * (int64_t)lda1);
         floatx4 acc[NB];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
@@ -1275,7 +1276,8 @@ __global__ __launch_bounds__(256) void k_narrow_k(int32_t M, int32_t N, int32_t 
 __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N,
                                                    const float *__restrict__ H0,
                                                    const float *__restrict__ H1, int32_t ldh,
-                                                   const float *__restrict__ G, int32_t ldg,
+                                                   int32_t ldh1, const float *__restrict__ G,
+                                                   int32_t ldg,
                                                    int32_t chunk, int32_t splits,
                                                    float *__restrict__ part)
 {
@@ -1298,7 +1300,7 @@ __global__ __launch_bounds__(256) void k_dw_narrow(int32_t R, int32_t m0, int32_
         for (int s = 0; s < SB; ++s) {
             const int r = r0 + 4 * s + h;
             const bool ok = r < re;
-            const float *hp = r < m0 ? H0 + (int64_t)r * ldh : H1 + (int64_t)(r - m0) * ldh;
+            const float *hp = r < m0 ? H0 + (int64_t)r * ldh : H1 + (int64_t)(r - m0) * ldh1;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int f = f0 + 16 * q + m;
@@ -1819,33 +1821,35 @@ int pick_group(int32_t dv)
 
 template <int VEC, int GL>
 hipError_t copy_rows_t(int mode, const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                       int32_t d, float *src, float *dst, hipStream_t s)
+                       int32_t d, float *src, int32_t lds, float *dst, int32_t ldd,
+                       hipStream_t s)
 {
     constexpr int rows_per_block = 4 * (kWave / GL);
     const int64_t blocks = ((int64_t)n_rows + rows_per_block - 1) / rows_per_block;
     const dim3 grid((unsigned)blocks), block(256);
     if (mode == kAdd)
         hipLaunchKernelGGL((k_copy_rows<VEC, GL, kAdd>), grid, block, 0, s, sidx, didx, n_rows, d,
-                           src, dst);
+                           src, lds, dst, ldd);
     else if (mode == kAddClear)
         hipLaunchKernelGGL((k_copy_rows<VEC, GL, kAddClear>), grid, block, 0, s, sidx, didx,
-                           n_rows, d, src, dst);
+                           n_rows, d, src, lds, dst, ldd);
     else
         hipLaunchKernelGGL((k_copy_rows<VEC, GL, kCopy>), grid, block, 0, s, sidx, didx, n_rows,
-                           d, src, dst);
+                           d, src, lds, dst, ldd);
     return hipGetLastError();
 }
 
 template <int VEC>
 hipError_t copy_rows_v(int gl, int mode, const int32_t *sidx, const int32_t *didx,
-                       int32_t n_rows, int32_t d, float *src, float *dst, hipStream_t s)
+                       int32_t n_rows, int32_t d, float *src, int32_t lds, float *dst,
+                       int32_t ldd, hipStream_t s)
 {
     switch (gl) {
-    case 4: return copy_rows_t<VEC, 4>(mode, sidx, didx, n_rows, d, src, dst, s);
-    case 8: return copy_rows_t<VEC, 8>(mode, sidx, didx, n_rows, d, src, dst, s);
-    case 16: return copy_rows_t<VEC, 16>(mode, sidx, didx, n_rows, d, src, dst, s);
-    case 32: return copy_rows_t<VEC, 32>(mode, sidx, didx, n_rows, d, src, dst, s);
-    default: return copy_rows_t<VEC, 64>(mode, sidx, didx, n_rows, d, src, dst, s);
+    case 4: return copy_rows_t<VEC, 4>(mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    case 8: return copy_rows_t<VEC, 8>(mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    case 16: return copy_rows_t<VEC, 16>(mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    case 32: return copy_rows_t<VEC, 32>(mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    default: return copy_rows_t<VEC, 64>(mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
     }
 }
 
@@ -1932,8 +1936,11 @@ hipError_t spmm_g(int gl, int nch, const SpmmBlock *blocks, int32_t n_blocks,
     default: break;
     }
     if constexpr (VEC == 4) {
-        return nch >= 2 ? spmm_t<4, 64, 2, TWO>(DIGEST_SPMM_ARGS)
-                        : spmm_t<4, 64, 1, TWO>(DIGEST_SPMM_ARGS);
+        switch (nch) {
+        case 1: return spmm_t<4, 64, 1, TWO>(DIGEST_SPMM_ARGS);
+        case 2: return spmm_t<4, 64, 2, TWO>(DIGEST_SPMM_ARGS);
+        default: return spmm_t<4, 64, 3, TWO>(DIGEST_SPMM_ARGS);
+        }
     } else if constexpr (VEC == 2) {
         switch (nch) {
         case 1: return spmm_t<2, 64, 1, TWO>(DIGEST_SPMM_ARGS);
@@ -2015,25 +2022,34 @@ hipError_t gemm_q(const GemmArgs &a, hipStream_t s)
 namespace {
 
 hipError_t move_rows(int mode, const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                     int32_t d, float *src, float *dst, hipStream_t s)
+                     int32_t d, float *src, float *dst, hipStream_t s, int32_t lds = 0,
+                     int32_t ldd = 0)
 {
     if (n_rows <= 0 || d <= 0)
         return hipSuccess;
-    const int vec = pick_vec(d, src, dst);
+    lds = lds > 0 ? lds : d;
+    ldd = ldd > 0 ? ldd : d;
+    if (lds < d || ldd < d)
+        return hipErrorInvalidValue;
+    // the widest vector that the width, both strides and both bases allow
+    int vec = pick_vec(d, src, dst);
+    while (vec > 1 && (lds % vec || ldd % vec))
+        vec /= 2;
     const int gl = pick_group(d / vec);
     switch (vec) {
-    case 4: return copy_rows_v<4>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
-    case 2: return copy_rows_v<2>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
-    default: return copy_rows_v<1>(gl, mode, sidx, didx, n_rows, d, src, dst, s);
+    case 4: return copy_rows_v<4>(gl, mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    case 2: return copy_rows_v<2>(gl, mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
+    default: return copy_rows_v<1>(gl, mode, sidx, didx, n_rows, d, src, lds, dst, ldd, s);
     }
 }
 
 }  // namespace
 
 hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                            int32_t d, const float *src, float *dst, hipStream_t s)
+                            int32_t d, const float *src, float *dst, hipStream_t s,
+                            int32_t lds, int32_t ldd)
 {
-    return move_rows(kCopy, sidx, didx, n_rows, d, const_cast<float *>(src), dst, s);
+    return move_rows(kCopy, sidx, didx, n_rows, d, const_cast<float *>(src), dst, s, lds, ldd);
 }
 
 hipError_t launch_add_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows, int32_t d,
@@ -2191,7 +2207,7 @@ hipError_t launch_spmm(const SpmmBlock *blocks, int32_t n_blocks, int32_t n_long
         }
 #undef DIGEST_NARROW
     }
-    const int max_nch = vec == 4 ? 2 : (vec == 2 ? 5 : 4);
+    const int max_nch = vec == 4 ? 3 : (vec == 2 ? 5 : 4);
     int nch = (dv + kWave - 1) / kWave;
     if (vec == 1 && nch == 3)
         nch = 4;
@@ -2326,20 +2342,21 @@ size_t narrow_n_lds(int32_t K, int32_t N)
 
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
                            const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
-                           bool relu, hipStream_t s)
+                           bool relu, hipStream_t s, int32_t lda1)
 {
     if (M <= 0 || N <= 0)
         return hipSuccess;
     if (N > kNarrowN || K <= 0 || narrow_n_lds(K, N) > kNarrowNLds)
         return hipErrorInvalidValue;
-    const bool v4 = K % 4 == 0 && lda % 4 == 0 && ((uintptr_t)A0 % 16) == 0 &&
+    lda1 = lda1 > 0 ? lda1 : lda;
+    const bool v4 = K % 4 == 0 && lda % 4 == 0 && lda1 % 4 == 0 && ((uintptr_t)A0 % 16) == 0 &&
                     (A1 == nullptr || ((uintptr_t)A1 % 16) == 0);
     const size_t lds = narrow_n_lds(K, N);
     const int64_t blocks = persistent_blocks((((int64_t)M + 15) / 16 + 3) / 4, lds);
     const int nb = (N + 15) / 16;
 #define DIGEST_NN(V, NB)                                                                       \
     hipLaunchKernelGGL((k_narrow_n<V, NB>), dim3((unsigned)blocks), dim3(256), lds, s, M, m0, K, \
-                       N, A0, A1, lda, B, C, ldc, relu)
+                       N, A0, A1, lda, lda1, B, C, ldc, relu)
     if (v4) {
         switch (nb) {
         case 1: DIGEST_NN(true, 1); break;
@@ -2430,14 +2447,17 @@ hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int3
 
 hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
                             const float *H1, int32_t ldh, const float *G, int32_t ldg,
-                            int32_t chunk, int32_t splits, float *part, hipStream_t s)
+                            int32_t chunk, int32_t splits, float *part, hipStream_t s,
+                            int32_t ldh1)
 {
+    ldh1 = ldh1 > 0 ? ldh1 : ldh;
     if (F <= 0 || N <= 0)
         return hipSuccess;
     if (N > kNarrow || splits < 1 || chunk < 1)
         return hipErrorInvalidValue;
     const dim3 grid((unsigned)((F + 63) / 64), (unsigned)((splits + 3) / 4));
-    hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, G, ldg, chunk,
+    hipLaunchKernelGGL(k_dw_narrow, grid, dim3(256), 0, s, R, m0, F, N, H0, H1, ldh, ldh1, G, ldg,
+                       chunk,
                        splits, part);
     return hipGetLastError();
 }

@@ -26,9 +26,11 @@ constexpr int32_t kSpmmLongRow = 64;
 // Rows with more entries than this get a whole block in a sliced pass.
 constexpr int32_t kTierLongRow = 1024;
 
-// dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows.
+// dst[didx ? didx[r] : r, :] = src[sidx ? sidx[r] : r, :] for r < n_rows, d
+// columns of rows with strides lds and ldd (0: d).
 hipError_t launch_copy_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows,
-                            int32_t d, const float *src, float *dst, hipStream_t s);
+                            int32_t d, const float *src, float *dst, hipStream_t s,
+                            int32_t lds = 0, int32_t ldd = 0);
 // The same with dst += src; the listed destination rows must be distinct.
 hipError_t launch_add_rows(const int32_t *sidx, const int32_t *didx, int32_t n_rows, int32_t d,
                            const float *src, float *dst, hipStream_t s);
@@ -128,7 +130,8 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
 // Dense products with one narrow side, bound by streaming the wide operand.
 
 // C[r][n] = sum_k A(r)[k] B[k][n], n < N <= kNarrowN, B row-major [K][N];
-// A(r) is row r of A0 for r < m0, else row r - m0 of A1 (leading dim lda);
+// A(r) is row r of A0 (leading dim lda) for r < m0, else row r - m0 of A1
+// (leading dim lda1, 0: lda);
 // relu: epilogue max(x, 0).  B is held in LDS: needs
 // narrow_n_lds(K, N) <= kNarrowNLds.
 constexpr int kNarrowN = 64;
@@ -136,7 +139,7 @@ constexpr size_t kNarrowNLds = 64 * 1024;
 size_t narrow_n_lds(int32_t K, int32_t N);
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
                            const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
-                           bool relu, hipStream_t s);
+                           bool relu, hipStream_t s, int32_t lda1 = 0);
 
 // C[r][n] = sum_{k < K} A[r][k] W[n][k] with K <= kNarrow, W row-major [N][K].
 hipError_t launch_narrow_k(int32_t M, int32_t N, int32_t K, const float *A, int32_t lda,
@@ -150,12 +153,13 @@ hipError_t launch_times_wt(int32_t M, int32_t N, int32_t K, const float *A, int3
                            const float *W, float *C, int32_t ldc, hipStream_t s);
 
 // part[z][f][n] = sum over rows r in [z*chunk, (z+1)*chunk) of H(r)[f] G[r][n]
-// (f < F, n < N <= kNarrow; H(r) from H0 for r < m0 else H1, leading dim
-// ldh; G row-major with leading dim ldg).  Sum the slices with
-// launch_splitk_reduce.
+// (f < F, n < N <= kNarrow; H(r) from H0 (leading dim ldh) for r < m0 else
+// H1 (leading dim ldh1, 0: ldh); G row-major with leading dim ldg).  Sum the
+// slices with launch_splitk_reduce.
 hipError_t launch_dw_narrow(int32_t R, int32_t m0, int32_t F, int32_t N, const float *H0,
                             const float *H1, int32_t ldh, const float *G, int32_t ldg,
-                            int32_t chunk, int32_t splits, float *part, hipStream_t s);
+                            int32_t chunk, int32_t splits, float *part, hipStream_t s,
+                            int32_t ldh1 = 0);
 
 // Row-wise softmax cross entropy (C >= 1): dlogits and the per-block loss
 // sums (softmax_xent_blocks(n, C) floats); launch_loss_mean then writes
