@@ -617,3 +617,35 @@ def test_tiering_off_gives_one_pass(monkeypatch):
         Dm.digest_layer_forward(c.h, 1, dev(x), dev(W), out, Dm.ACT_RELU)
         outs.append(host(out))
     assert_close(outs[1], outs[0], "tiered vs one pass")
+
+
+# ---------------------------------------------------------------------------
+# tall products (6,000 owned rows): the GEMMs that hold a column block of W
+# in LDS and stream row tiles -- forward (ReLU epilogue), input gradient
+# (masked A, W read transposed), rows padded past an odd K, and the
+# halo-gradient product
+# ---------------------------------------------------------------------------
+
+TALL = [(100, 256, 256, 47), (602, 256, 41), (500, 256, 7), (33, 130, 9, 70)]
+
+
+@pytest.mark.parametrize("widths", TALL, ids=lambda w: "x".join(map(str, w)))
+def test_tall_products(widths):
+    from paper_2206_00057_amd import digest as Dm
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 24000, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=3)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 1), label=f"tall{widths}")
+    assert c.n >= 4096
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+    # the halo gradient of layer 2 (ReLU or identity, as the layer's act)
+    W = synth.weights(cfg)[1]
+    h_in = c.layer_input(2)
+    act = c.act(2)
+    out = torch.empty(c.n, widths[2], device="cuda")
+    Dm.digest_layer_forward(c.h, 2, dev(h_in), dev(W), out, act)
+    h_out = c.op.forward(2, h_in, W, act)
+    dh = c.upstream(2)
+    got = torch.full((c.part.n_halo, widths[1]), float("nan"), device="cuda")
+    Dm.digest_halo_gradient(c.h, 2, dev(h_out), dev(dh), dev(W), got)
+    assert_close(host(got), c.op.halo_gradient(2, W, h_out, dh, act), f"{c.label} halo gradient")
