@@ -377,6 +377,13 @@ struct digest_partition {
         return reinterpret_cast<T *>(gws + off);
     }
 
+    // A second stream of the library for the weight gradient, which runs
+    // concurrently with the input-gradient chain of the same backward call
+    // (forked from and joined back into the caller's stream by events).
+    hipStream_t side = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+    int side_dev = -1;
+
     bool prof = false;
     struct Rec {
         int32_t kind, layer;
@@ -501,11 +508,12 @@ void plan_layout(digest_partition &p)
     for (int32_t lev = 0; lev < p.L; ++lev)
         l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * padded_width(p.widths[lev]));
     l.ah.assign(p.L + 1, 0);
-    int64_t hpad = 0;
+    int64_t hpad = 0;   // padded copies of h_in (odd d_in) or dh_out (odd d_out)
     for (int32_t k = 1; k <= p.L; ++k) {
         l.ah[k] = take(sizeof(float) * (size_t)p.n_own * padded_width(p.widths[k - 1]));
-        if (p.widths[k - 1] % 4)
-            hpad = std::max<int64_t>(hpad, (int64_t)p.n_own * padded_width(p.widths[k - 1]));
+        for (int32_t d : {p.widths[k - 1], p.widths[k]})
+            if (d % 4)
+                hpad = std::max<int64_t>(hpad, (int64_t)p.n_own * padded_width(d));
     }
     l.hpad = take(sizeof(float) * (size_t)hpad);
     int64_t wmax = 0, gemm_part = 0, tbuf = 0;
@@ -623,6 +631,68 @@ digest_status hip_check(hipError_t e, const char *what)
     if (e != hipSuccess)
         return fail(DIGEST_EHIP, "%s: %s", what, hipGetErrorString(e));
     return DIGEST_OK;
+}
+
+// Weight gradients of at least this many flops run on the side stream,
+// concurrently with the input-gradient chain (smaller ones lose more to the
+// fork and join than the overlap gives).  DIGEST_SIDE_STREAM=0 keeps all
+// work on the caller's stream, =2 uses the side stream at any size.
+constexpr double kSideFlops = 8.0e9;
+
+bool side_pays(double flops)
+{
+    const char *v = std::getenv("DIGEST_SIDE_STREAM");
+    if (v && v[0] == '0')
+        return false;
+    if (v && v[0] == '2')
+        return true;
+    return flops >= kSideFlops;
+}
+
+// Start work on the side stream after everything enqueued on s so far; *sw
+// becomes the side stream, or stays s when s belongs to another device than
+// the current one (the side stream is created on the current device).
+digest_status fork_side(digest_partition *p, hipStream_t s, hipStream_t *sw)
+{
+    *sw = s;
+    int dev = -1;
+    if (digest_status st = hip_check(hipGetDevice(&dev), "current device"))
+        return st;
+    if (s) {
+        hipDevice_t sdev = -1;
+        if (digest_status st = hip_check(hipStreamGetDevice(s, &sdev), "stream device"))
+            return st;
+        if (sdev != dev)
+            return DIGEST_OK;
+    }
+    if (!p->side || p->side_dev != dev) {
+        if (p->side)
+            return DIGEST_OK;   // created for another device: stay on s
+        if (digest_status st = hip_check(hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking),
+                                         "side stream"))
+            return st;
+        p->side_dev = dev;
+        if (digest_status st =
+                hip_check(hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming), "event"))
+            return st;
+        if (digest_status st =
+                hip_check(hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming), "event"))
+            return st;
+    }
+    if (digest_status st = hip_check(hipEventRecord(p->ev_fork, s), "fork"))
+        return st;
+    if (digest_status st = hip_check(hipStreamWaitEvent(p->side, p->ev_fork, 0), "fork"))
+        return st;
+    *sw = p->side;
+    return DIGEST_OK;
+}
+
+// Make s wait for everything enqueued on the side stream so far.
+digest_status join_side(digest_partition *p, hipStream_t s)
+{
+    if (digest_status st = hip_check(hipEventRecord(p->ev_join, p->side), "join"))
+        return st;
+    return hip_check(hipStreamWaitEvent(s, p->ev_join, 0), "join");
 }
 
 digest_status need_bound(const digest_partition *p)
@@ -945,6 +1015,12 @@ void digest_partition_destroy(digest_partition *p)
     }
     for (auto e : p->pool)
         (void)hipEventDestroy(e);
+    if (p->side)
+        (void)hipStreamDestroy(p->side);
+    if (p->ev_fork)
+        (void)hipEventDestroy(p->ev_fork);
+    if (p->ev_join)
+        (void)hipEventDestroy(p->ev_join);
     delete p;
 }
 
@@ -1324,10 +1400,29 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                           digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
                           (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
     const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
-    if (digest_status st = run_spmm(p, Csr::FullT, dh_out, nullptr, p->n_own, d_out, G, layer, s,
+    // Without the epilogue (which reads the stored rows back), rows of a
+    // width not a multiple of 4 are gathered from a padded copy of dh_out,
+    // whole float4 vectors wide; G keeps the padding columns (never read).
+    const float *src = dh_out;
+    int32_t dg = d_out;
+    if (!fused_dh && ldg != d_out && p->n_own > 0) {
+        float *dp = p->at<float>(p->lay.hpad);
+        Timed t(p, K_PAD_ROWS, layer, s);
+        if (digest_status st = hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_own,
+                                                                  d_out, dh_out, dp, s, d_out,
+                                                                  ldg),
+                                         "pad rows"))
+            return st;
+        src = dp;
+        dg = ldg;
+    }
+    if (digest_status st = run_spmm(p, Csr::FullT, src, nullptr, p->n_own, dg, G, layer, s,
                                     fused_dh ? &ep : nullptr, -1, nullptr, INT32_MAX, nullptr,
-                                    false, nullptr, d_out, ldg, d_out))
+                                    false, nullptr, dg, ldg, dg))
         return st;
+    // (everything after G is a product bound by the MFMA units, so the
+    // weight gradient stays on s: two such products side by side only
+    // share the units)
     if (digest_status st = weight_grad_rows(p, layer, h_in, halo, G, ldg, gpart, dw, s,
                                             K_GEMM_DW, K_REDUCE_DW))
         return st;
@@ -1367,85 +1462,111 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
     const bool relu = p->act[layer] == DIGEST_ACT_RELU;
     const float *ah = p->at<float>(p->lay.ah[layer]);
 
-    // dW = AH^T D, D = dh_out (masked by h_out > 0 for ReLU), split over rows.
-    digest::GemmArgs g{};
-    g.M = d_in;
-    g.N = d_out;
-    g.K = p->n_own;
-    g.A = ah;
-    g.lda = padded_width(d_in);
-    g.a_trans = true;
-    g.B = dh_out;
-    g.ldb = d_out;
-    g.b_mask = relu ? h_out : nullptr;
-    splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
-    g.tile = gemm_tile_for(d_in, d_out, p->n_own, true);
-    float *gpart = p->at<float>(p->lay.gemm_part);
-    g.C = g.splits > 1 ? gpart : dw;
-    g.ldc = d_out;
-    {
-        Timed t(p, K_GEMM_DW, layer, s);
-        if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
-            return st;
-    }
-    if (g.splits > 1) {
-        Timed t(p, K_REDUCE_DW, layer, s);
-        if (digest_status st = hip_check(
-                digest::launch_splitk_reduce(gpart, g.splits, (int64_t)d_in * d_out, dw, s),
-                "dW reduce"))
-            return st;
-    }
-    if (p->n_own == 0 && dh_halo)
-        // no owned row reads a halo row: the halo gradient is zero
-        return hip_check(digest::launch_fill_zero(dh_halo, (int64_t)p->n_halo * d_in, s),
-                         "zero halo gradient");
-    if (!dh_in || p->n_own == 0)
-        return DIGEST_OK;
-
-    // P_in^T alone, or P_m^T with its halo rows split off
-    const Csr tr = dh_halo ? Csr::FullT : Csr::InT;
-    const int32_t split = dh_halo ? p->n_own : INT32_MAX;
-    float *tmp = p->at<float>(p->lay.tmp);
-    if (!relu && d_out < d_in) {
-        // Narrower output: aggregate D first (width d_out), then times W^T.
-        float *gh = p->at<float>(p->lay.tmp_halo);
-        if (digest_status st = run_spmm(p, tr, dh_out, nullptr, p->n_own, d_out, tmp, layer, s,
-                                        nullptr, -1, dh_halo ? gh : nullptr, split))
-            return st;
+    // dW = AH^T D, D = dh_out (masked by h_out > 0 for ReLU), split over rows,
+    // on stream sw.
+    auto weight_grad = [&](hipStream_t sw) -> digest_status {
+        digest::GemmArgs g{};
+        g.M = d_in;
+        g.N = d_out;
+        g.K = p->n_own;
+        g.A = ah;
+        g.lda = padded_width(d_in);
+        g.a_trans = true;
+        g.B = dh_out;
+        g.ldb = d_out;
+        g.b_mask = relu ? h_out : nullptr;
+        splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
+        g.tile = gemm_tile_for(d_in, d_out, p->n_own, true);
+        float *gpart = p->at<float>(p->lay.gemm_part);
+        g.C = g.splits > 1 ? gpart : dw;
+        g.ldc = d_out;
         {
-            Timed t(p, K_GEMM_DH, layer, s);
-            if (digest_status st = times_wt(p->n_own, d_in, d_out, tmp, d_out, w, dh_in, s))
+            Timed t(p, K_GEMM_DW, layer, sw);
+            if (digest_status st = hip_check(digest::launch_gemm(g, sw), "dW gemm"))
                 return st;
         }
-        if (!dh_halo)
+        if (g.splits <= 1)
             return DIGEST_OK;
-        Timed t(p, K_HALO_GRAD, layer, s);
-        return times_wt(p->n_halo, d_in, d_out, gh, d_out, w, dh_halo, s);
-    }
-    // Otherwise G = D W^T (mask fused into the operand load), then the
-    // transposed aggregation of G.
-    digest::GemmArgs h{};
-    h.M = p->n_own;
-    h.N = d_in;
-    h.K = d_out;
-    h.B = w;
-    h.ldb = d_out;
-    h.b_trans = true;
-    h.ldc = d_in;
-    h.splits = 1;
-    h.kchunk = d_out;
-    h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
-    h.A = dh_out;
-    h.lda = d_out;
-    h.a_mask = relu ? h_out : nullptr;
-    h.C = tmp;
-    {
-        Timed t(p, K_GEMM_DH, layer, s);
-        if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
+        Timed t(p, K_REDUCE_DW, layer, sw);
+        return hip_check(
+            digest::launch_splitk_reduce(gpart, g.splits, (int64_t)d_in * d_out, dw, sw),
+            "dW reduce");
+    };
+    if (!dh_in || p->n_own == 0) {
+        if (digest_status st = weight_grad(s))
             return st;
+        if (p->n_own == 0 && dh_halo)
+            // no owned row reads a halo row: the halo gradient is zero
+            return hip_check(digest::launch_fill_zero(dh_halo, (int64_t)p->n_halo * d_in, s),
+                             "zero halo gradient");
+        return DIGEST_OK;
     }
-    return run_spmm(p, tr, tmp, nullptr, p->n_own, d_in, dh_in, layer, s, nullptr, -1, dh_halo,
-                    split);
+
+    // The input gradient: its transposed aggregation is bound by memory, so
+    // a large weight gradient (bound by the MFMA units) runs next to it on the
+    // side stream, started right before it and joined at the end of the call.
+    hipStream_t sw = s;
+    auto start_weight_grad = [&]() -> digest_status {
+        if (side_pays(2.0 * p->n_own * d_in * d_out))
+            if (digest_status st = fork_side(p, s, &sw))
+                return st;
+        return weight_grad(sw);
+    };
+    const digest_status st_all = [&]() -> digest_status {
+        // P_in^T alone, or P_m^T with its halo rows split off
+        const Csr tr = dh_halo ? Csr::FullT : Csr::InT;
+        const int32_t split = dh_halo ? p->n_own : INT32_MAX;
+        float *tmp = p->at<float>(p->lay.tmp);
+        if (!relu && d_out < d_in) {
+            // Narrower output: aggregate D first (width d_out), then times W^T.
+            float *gh = p->at<float>(p->lay.tmp_halo);
+            if (digest_status st = start_weight_grad())
+                return st;
+            if (digest_status st = run_spmm(p, tr, dh_out, nullptr, p->n_own, d_out, tmp, layer,
+                                            s, nullptr, -1, dh_halo ? gh : nullptr, split))
+                return st;
+            {
+                Timed t(p, K_GEMM_DH, layer, s);
+                if (digest_status st = times_wt(p->n_own, d_in, d_out, tmp, d_out, w, dh_in, s))
+                    return st;
+            }
+            if (!dh_halo)
+                return DIGEST_OK;
+            Timed t(p, K_HALO_GRAD, layer, s);
+            return times_wt(p->n_halo, d_in, d_out, gh, d_out, w, dh_halo, s);
+        }
+        // Otherwise G = D W^T (mask fused into the operand load), then the
+        // transposed aggregation of G.
+        digest::GemmArgs h{};
+        h.M = p->n_own;
+        h.N = d_in;
+        h.K = d_out;
+        h.B = w;
+        h.ldb = d_out;
+        h.b_trans = true;
+        h.ldc = d_in;
+        h.splits = 1;
+        h.kchunk = d_out;
+        h.tile = gemm_tile_for(p->n_own, d_in, d_out, false);
+        h.A = dh_out;
+        h.lda = d_out;
+        h.a_mask = relu ? h_out : nullptr;
+        h.C = tmp;
+        {
+            Timed t(p, K_GEMM_DH, layer, s);
+            if (digest_status st = hip_check(digest::launch_gemm(h, s), "dgrad gemm"))
+                return st;
+        }
+        if (digest_status st = start_weight_grad())
+            return st;
+        return run_spmm(p, tr, tmp, nullptr, p->n_own, d_in, dh_in, layer, s, nullptr, -1,
+                        dh_halo, split);
+    }();
+    if (sw != s) {
+        const digest_status st = join_side(p, s);
+        return st_all ? st_all : st;
+    }
+    return st_all;
 }
 
 // Argument and state checks shared by both backward entry points.
@@ -2044,6 +2165,8 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
                 4 * (R + 1) + 8 * nnz + 4 * n * dout + 4 * R * dout +
                     (pl.dgrad_fused ? 4 * (n * di + di * dout) : 0.0),
                 0.0, p->nnz);
+            if (!pl.dgrad_fused && p->widths[l] % 4)   // the padded copy of dh_out
+                put(K_PAD_ROWS, l, 4 * n * (dout + padded_width(p->widths[l])));
             put(K_GEMM_DW, l, 4 * (R * di + R * dout + di * dout), 2 * R * di * dout);
             put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);
             if (l > 1 && !pl.dgrad_fused)

@@ -649,3 +649,53 @@ def test_tall_products(widths):
     got = torch.full((c.part.n_halo, widths[1]), float("nan"), device="cuda")
     Dm.digest_halo_gradient(c.h, 2, dev(h_out), dev(dh), dev(W), got)
     assert_close(host(got), c.op.halo_gradient(2, W, h_out, dh, act), f"{c.label} halo gradient")
+
+
+# ---------------------------------------------------------------------------
+# the weight gradient on the library's side stream, concurrent with the
+# input-gradient chain (forced at every size here): results, and graph
+# capture with replays, must not change
+# ---------------------------------------------------------------------------
+
+# (widths): layer 2 aggregate-first with ReLU, the weight gradient next to
+# the transposed aggregation of D W^T (24 -> 40 -> 48 -> 7), and an identity
+# layer aggregated at its narrower output width first (24 -> 40 -> 36)
+SIDE = [(24, 40, 48, 7), (24, 40, 36)]
+
+
+@pytest.mark.parametrize("widths", SIDE, ids=lambda w: "x".join(map(str, w)))
+def test_side_stream_backward(widths, monkeypatch):
+    from paper_2206_00057_amd import step
+    monkeypatch.setenv("DIGEST_SIDE_STREAM", "2")
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=4)
+    part = synth.make_partition(cfg, g, 2)
+    c = Case(cfg, g, part, label=f"side{widths}")
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+    # rounds: eager, then captured and replayed (bit for bit)
+    L = cfg.layers
+    X = synth.features(cfg)
+    stores = [dev(X)] + [dev(synth.relu_normal((g.n, cfg.widths[l]), 20 + l))
+                         for l in range(1, L)]
+    Ws = [dev(w) for w in synth.weights(cfg)]
+    y = dev(synth.labels(cfg)[part.owned])
+    x = dev(X[part.owned])
+    gp = step.GpuPartition(g.n, part, cfg.widths)
+    gp.pull_all(stores)
+    K = 2
+    eager = {}
+    for r in (1, 2):
+        gp.round(r, K, x, Ws, stores, y)
+        eager[r] = [host(gp.dW[l]).copy() for l in range(1, L + 1)] + [host(gp.dH[1]).copy()]
+    gp.capture(K, x, Ws, stores, y)
+    for rep in range(3):
+        for r in (1, 2):
+            for l in range(1, L + 1):
+                gp.dW[l].zero_()
+            gp.replay(r, K)
+            torch.cuda.synchronize()
+            _ = torch.ones(1000, device="cuda").sum().item()   # eager work between replays
+            got = [host(gp.dW[l]) for l in range(1, L + 1)] + [host(gp.dH[1])]
+            for i, (a, b) in enumerate(zip(got, eager[r])):
+                assert_bits(a, b, f"replay {rep} round {r} output {i}")
