@@ -388,6 +388,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(d["gbs"] / HBM_PEAK_GBS, 4)}
     traffic, traffic_source = measured_traffic(cfg.name, dom)
+    if traffic:   # the rate at which the kernel moves L2-fabric bytes
+        roof["traffic_rate_gbs"] = round(traffic / (d["avg_us"] * 1e-6) / 1e9, 1)
     roof.update({"traffic": traffic, "traffic_source": traffic_source, "kernel": dom,
                  "algorithmic_bytes_per_launch": b_l, "algorithmic_flops_per_launch": f_l,
                  "avg_launch_us": round(d["avg_us"], 3),

@@ -5,7 +5,9 @@ Kernel durations (from a ``rocprofv3 --kernel-trace --stats`` run):
     python -m paper_2206_00057_amd.pmc stats --csv <dir>/<name>_kernel_stats.csv \\
         --title "..." --command "..." --out profiles/<kernel-or-workload>_kernel_stats.txt
 
-HBM traffic of one kernel, from two counter passes over the same command:
+L2-to-fabric traffic of one kernel (the bytes its L2 misses move between the
+L2s and the memory side, Infinity Cache hits included; not HBM bytes alone),
+from two counter passes over the same command:
 
     python -m paper_2206_00057_amd.pmc traffic \\
         --fetch <fetch-dir>/fetch_counter_collection.csv \\
@@ -144,7 +146,7 @@ def main():
     co.add_argument("--title", required=True)
     co.add_argument("--command", action="append", default=[])
     co.add_argument("--out", required=True)
-    tr = sub.add_parser("traffic", help="HBM bytes per launch of one kernel")
+    tr = sub.add_parser("traffic", help="L2-fabric bytes per launch of one kernel")
     tr.add_argument("--fetch", required=True)
     tr.add_argument("--write", required=True)
     tr.add_argument("--kernel-name", required=True, help="substring of the rocprof kernel name")
@@ -166,9 +168,11 @@ def main():
         lines += counters_table(a.csv, a.kernel_name)
     else:
         s = summarize(a.fetch, a.write, a.kernel_name, a.copy_name, a.copy_bytes)
-        lines = [f"# HBM traffic of one launch of {a.key} on the {a.workload} workload,",
-                 "# from rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by",
-                 "# the counter's reading per byte of a plain device-to-device copy of known size.",
+        lines = [f"# L2-to-fabric traffic of one launch of {a.key} on the {a.workload} workload:",
+                 "# the bytes the L2s of the 8 XCDs request from and write to the memory side",
+                 "# (Infinity Cache hits included, so not HBM bytes alone), from rocprofv3",
+                 "# FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by the counter's",
+                 "# reading per byte of a plain device-to-device copy of known size.",
                  "# commands:"]
         lines += [f"#   {c}" for c in a.command]
         lines += [f"kernel = {a.key}", f"source_sha = {kernel_source_hash()}"]
