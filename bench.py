@@ -60,7 +60,7 @@ def measured_traffic(workload, key):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     from paper_2206_00057_amd.pmc import kernel_source_hash
-    if kv.get("kernel") != key:
+    if key not in [k.strip() for k in kv.get("kernel", "").split(",")]:
         return None, f"{rel} covers {kv.get('kernel')}, not {key}"
     sha = kernel_source_hash()
     if kv.get("source_sha") != sha:
@@ -357,11 +357,22 @@ def main():
     value = edges * args.steps / (ms * 1e-3) / 1e9
     print(f"[bench] timed {args.steps} rounds: {ms:.3f} ms", file=sys.stderr, flush=True)
 
-    # instrumented pass over the same rounds: per-kernel durations from HIP events
+    # instrumented pass over the same rounds: per-kernel durations from HIP
+    # events, with every kernel on the caller's stream (no weight gradient
+    # on the library's side stream), so that each duration is the kernel's
+    # own and not shared with a concurrent one
     D.digest_profile_enable(gp.p, True)
-    for r in rounds:
-        gp.round(r, K, x_own, dWs, stores, dy)
-    prof = D.digest_profile_read(gp.p)
+    side_env = os.environ.get("DIGEST_SIDE_STREAM")
+    os.environ["DIGEST_SIDE_STREAM"] = "0"
+    try:
+        for r in rounds:
+            gp.round(r, K, x_own, dWs, stores, dy)
+        prof = D.digest_profile_read(gp.p)
+    finally:
+        if side_env is None:
+            del os.environ["DIGEST_SIDE_STREAM"]
+        else:
+            os.environ["DIGEST_SIDE_STREAM"] = side_env
     D.digest_profile_enable(gp.p, False)
     # algorithmic bytes / flops / entries of each launch, from the library's plan
     model = D.digest_profile_model(gp.p, D.MODEL_GAT if gat else D.MODEL_GCN)
@@ -425,6 +436,8 @@ def main():
                                       round(edges / ((ms / args.steps - pp_ms) * 1e-3) / 1e9, 4)),
         "roofline": roof,
         "cpu_baseline": cpu,
+        # per (kernel, layer): HIP-event durations of an instrumented eager
+        # pass over the same rounds, every kernel on the caller's stream
         "kernels": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
                         for kk, vv in v.items()} for k, v in kernels.items()},
     }
