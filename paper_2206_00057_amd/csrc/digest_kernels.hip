@@ -764,8 +764,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 // operand's first element instead) so that the number of loads in flight is
 // static; the zero fill and the mask are applied only when the quad is
 // written to LDS, so no wait on the loads sits between fetch and compute.
-// With VEC the contiguous extent is a multiple of 4 and a quad is one
-// aligned 16-byte load.
+// With VEC a quad is one aligned 16-byte load (the row stride is a multiple
+// of 4, so a quad that starts inside a row ends inside its stride); its
+// elements past the extent are zeroed, so padding columns may hold
+// anything, NaN included.
 template <bool VEC, bool MASK>
 struct Quad {
     float v[4];
@@ -791,7 +793,8 @@ struct Quad {
                 m[2] = b.z;
                 m[3] = b.w;
             }
-            ok = in ? 0xFu : 0u;
+            const int left = lim - pos;
+            ok = !in ? 0u : left >= 4 ? 0xFu : (1u << left) - 1u;
         } else {
             ok = 0;
 #pragma unroll

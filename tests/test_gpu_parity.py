@@ -68,7 +68,7 @@ def assert_bits(gpu, ref, name):
 class Case:
     """A partition with its library handle, oracle twin and seeded inputs."""
 
-    def __init__(self, cfg, g, part, label=""):
+    def __init__(self, cfg, g, part, label="", ws_fill=None):
         self.cfg, self.g, self.part = cfg, g, part
         self.label = label or cfg.name
         self.widths = list(cfg.widths)
@@ -77,6 +77,8 @@ class Case:
         self.h = Dm.digest_partition_create(g.n, part.indptr, part.indices, part.values,
                                             part.owned, part.halo, self.widths)
         self.ws = torch.empty(max(self.h.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
+        if ws_fill is not None:   # every workspace byte set before the library writes any
+            self.ws.fill_(ws_fill)
         Dm.digest_partition_bind_workspace(self.h, self.ws)
         self.op = oracle.OraclePartition(g.n, part.indptr, part.indices, part.values,
                                          part.owned, part.halo, self.widths)
@@ -620,9 +622,8 @@ def test_tiering_off_gives_one_pass(monkeypatch):
 
 
 # ---------------------------------------------------------------------------
-# tall products (6,000 owned rows): the GEMMs that hold a column block of W
-# in LDS and stream row tiles -- forward (ReLU epilogue), input gradient
-# (masked A, W read transposed), rows padded past an odd K, and the
+# tall products (6,000 owned rows) -- forward (ReLU epilogue), input
+# gradient (masked A, W read transposed), rows padded past an odd K, and the
 # halo-gradient product
 # ---------------------------------------------------------------------------
 
@@ -649,6 +650,29 @@ def test_tall_products(widths):
     got = torch.full((c.part.n_halo, widths[1]), float("nan"), device="cuda")
     Dm.digest_halo_gradient(c.h, 2, dev(h_out), dev(dh), dev(W), got)
     assert_close(host(got), c.op.halo_gradient(2, W, h_out, dh, act), f"{c.label} halo gradient")
+
+
+# ---------------------------------------------------------------------------
+# padding columns of the library's buffers hold NaN (the workspace is filled
+# with 0xFF bytes before binding): rows of widths that are not a multiple of
+# 4 floats are read as whole vectors, and nothing of the padding may reach
+# an output -- GEMMs over a padded K (30 -> 100, the 70-wide last layer's
+# padded gradient), the narrow products, the aggregations and the halo reads
+# ---------------------------------------------------------------------------
+
+PADDED = [(30, 100, 70), (30, 80, 9), (602, 47, 7), (33, 130, 9, 70)]
+
+
+@pytest.mark.parametrize("widths", PADDED, ids=lambda w: "x".join(map(str, w)))
+def test_nan_padding_never_reaches_outputs(widths):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=6)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 1), label=f"nanpad{widths}", ws_fill=255)
+    for level in range(c.L):
+        check_pull(c, level)
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+    check_loss(c)
 
 
 # ---------------------------------------------------------------------------
