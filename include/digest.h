@@ -450,6 +450,19 @@ const char *digest_profile_kernel_name(int32_t kind);
  *                       cost model picks the tier count, or
  *                       DIGEST_SPMM_TIERS forces one.
  *   tier_entries_fwd, tier_entries_bwd  entries the sliced passes take.
+ *   forward_fused       aggregate-first layers with at least 16,384 owned
+ *                       rows, 129 <= d_layer-1 <= 256 and the MFMA GEMM as their
+ *                       product: 1 if the forward runs as one pass (kernel
+ *                       kind "spmm_gemm_fwd") in which each tile of 32 rows
+ *                       is aggregated into LDS and multiplied by W there,
+ *                       the tiles of other workgroups gathering meanwhile;
+ *                       rows of more than 64 entries are aggregated first
+ *                       by a long-row pass ("spmm_fwd").  AH is still
+ *                       stored for the backward.  The environment variable
+ *                       DIGEST_FUSE=0 turns this off, =2 fuses at any row
+ *                       count; the forward also falls back to two passes
+ *                       when h_in (d_layer-1 a multiple of 4) is not
+ *                       16-byte aligned.
  * Errors: DIGEST_EINVAL (NULL, layer outside 1..L).
  */
 typedef struct {
@@ -464,6 +477,7 @@ typedef struct {
     int32_t tier_rows_bwd;
     int64_t tier_entries_fwd;
     int64_t tier_entries_bwd;
+    int32_t forward_fused;
 } digest_layer_plan;
 
 digest_status digest_partition_plan(const digest_partition *p, int32_t layer,

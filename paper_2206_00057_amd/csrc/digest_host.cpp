@@ -61,6 +61,7 @@ enum Kind : int32_t {
     K_GAT_DW,
     K_GAT_DGRAD,
     K_PAD_ROWS,
+    K_SPMM_GEMM_FWD,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
@@ -69,7 +70,7 @@ const char *const kKindNames[K_COUNT] = {
     "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
     "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
     "gat_aggregate_transposed", "gat_score_grad", "gat_score_sums", "gat_datt", "gat_dw",
-    "gat_dgrad", "pad_rows"};
+    "gat_dgrad", "pad_rows", "spmm_gemm_fwd"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -334,6 +335,13 @@ struct digest_partition {
     // (P_out^T, numbered from 0).
     std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf, blocks_th;
     int32_t long_f = 0, long_t = 0, long_tf = 0, long_th = 0;   // leading long-row blocks
+    // P_m split at kFuseLong entries per row: the long rows (their count and
+    // entries) and the distinct source rows the short and the long rows read
+    int64_t long_rows_f = 0, long_nnz_f = 0, src_short_f = 0, src_long_f = 0;
+    // the fused forward's row order: tile t's rows t kFuseRows + fuse_order[..]
+    // by descending entry count (long rows, read back, last), so that the
+    // rows the waves take last are the short ones
+    std::vector<uint8_t> fuse_order;
 
     // Tiered plans of the aggregations (see TierPlan), at most one per
     // (sparse operand, width).
@@ -342,6 +350,7 @@ struct digest_partition {
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
+        size_t fuse_order;              // per owned row, uint8 (see fuse_order below)
         std::vector<size_t> halo_buf;   // per level 0..L-1, rows padded_width(d_level) apart
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused), padded rows
         size_t tmp, tmp_halo, tbuf, gemm_part, loss_part;
@@ -501,6 +510,7 @@ void plan_layout(digest_partition &p)
     l.bnd_gid = take(sizeof(int32_t) * p.n_bnd);
     l.owned_gid = take(sizeof(int32_t) * p.n_own);
     l.blocks_f = take(sizeof(SpmmBlock) * p.blocks_f.size());
+    l.fuse_order = take(p.fuse_order.size());
     l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
     l.blocks_tf = take(sizeof(SpmmBlock) * p.blocks_tf.size());
     l.blocks_th = take(sizeof(SpmmBlock) * p.blocks_th.size());
@@ -751,6 +761,22 @@ const TierPlan *find_tiers(const digest_partition &p, Csr which, int32_t width)
     return nullptr;
 }
 
+// Aggregate-first forwards of at least this many owned rows run as one pass
+// that multiplies each aggregated row tile by W while other tiles gather
+// (launch_spmm_gemm).  DIGEST_FUSE=0 never fuses, =2 fuses at any size.
+constexpr int64_t kFuseMinRows = 16384;
+
+bool fuse_forward(const digest_partition &p, int32_t layer, bool transform_first)
+{
+    const int32_t d_in = p.widths[layer - 1], d_out = p.widths[layer];
+    const int64_t mode = env_int("DIGEST_FUSE", 1);
+    if (mode == 0 || transform_first || p.n_own <= 0 || narrow_out(d_in, d_out) ||
+        d_in < digest::kFuseMinWidth || d_in > digest::kFuseMaxWidth ||
+        (mode == 1 && p.n_own < kFuseMinRows))
+        return false;
+    return find_tiers(p, Csr::Fwd, padded_width(d_in)) == nullptr;
+}
+
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
                        int32_t n_src0, int32_t d, float *out, int32_t layer, hipStream_t s,
                        const digest::SpmmEpilogue *ep = nullptr, int32_t kind = -1,
@@ -977,6 +1003,37 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
             }
 
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
+        {
+            std::vector<uint8_t> seen((size_t)p->n_own + p->n_halo, 0);
+            for (int32_t i = 0; i < (int32_t)n_owned; ++i) {
+                const int32_t len = p->rowptr[i + 1] - p->rowptr[i];
+                const bool lng = len > digest::kFuseLong;
+                p->long_rows_f += lng;
+                p->long_nnz_f += lng ? len : 0;
+                for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k)
+                    seen[p->col[k]] |= lng ? 2 : 1;
+            }
+            for (const uint8_t v : seen) {
+                p->src_short_f += v & 1;
+                p->src_long_f += v >> 1;
+            }
+            static_assert(digest::kFuseRows <= 256, "tile offsets fit a byte");
+            p->fuse_order.resize(n_owned);
+            for (int64_t t0 = 0; t0 < n_owned; t0 += digest::kFuseRows) {
+                const int32_t nr = (int32_t)std::min<int64_t>(digest::kFuseRows, n_owned - t0);
+                auto work = [&](int32_t i) {
+                    const int32_t len = p->rowptr[t0 + i + 1] - p->rowptr[t0 + i];
+                    return len > digest::kFuseLong ? -1 : len;
+                };
+                std::vector<int32_t> idx(nr);
+                for (int32_t i = 0; i < nr; ++i)
+                    idx[i] = i;
+                std::stable_sort(idx.begin(), idx.end(),
+                                 [&](int32_t a, int32_t b) { return work(a) > work(b); });
+                for (int32_t i = 0; i < nr; ++i)
+                    p->fuse_order[t0 + i] = (uint8_t)idx[i];
+            }
+        }
         p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
         p->long_tf = build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
         {
@@ -1069,6 +1126,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.bnd_gid, p->bnd_gid.data(), sizeof(int32_t) * p->bnd_gid.size()},
         {l.owned_gid, p->owned_gid.data(), sizeof(int32_t) * p->owned_gid.size()},
         {l.blocks_f, p->blocks_f.data(), sizeof(SpmmBlock) * p->blocks_f.size()},
+        {l.fuse_order, p->fuse_order.data(), p->fuse_order.size()},
         {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
         {l.blocks_tf, p->blocks_tf.data(), sizeof(SpmmBlock) * p->blocks_tf.size()},
         {l.blocks_th, p->blocks_th.data(), sizeof(SpmmBlock) * p->blocks_th.size()},
@@ -1252,6 +1310,35 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
                                              "pad rows"))
                 return st;
             src0 = hp;
+        }
+        if (fuse_forward(*p, layer, tf) && digest::spmm_gemm_ok(d_in, lh, lh, src0, halo, ah)) {
+            // the long rows through the ordinary kernel's long-row blocks,
+            // then every row tile aggregated and multiplied by W in one pass
+            const int32_t *rowptr = p->at<int32_t>(p->lay.rowptr);
+            const int32_t *col = p->at<int32_t>(p->lay.col);
+            const float *val = p->at<float>(p->lay.val);
+            if (p->long_f > 0) {
+                Timed t(p, K_SPMM_FWD, layer, s);
+                if (digest_status st = hip_check(
+                        digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_f), p->long_f,
+                                            p->long_f, rowptr, col, val, src0, halo, p->n_own,
+                                            lh, ah, s),
+                        "spmm long rows"))
+                    return st;
+            }
+            Timed t(p, K_SPMM_GEMM_FWD, layer, s);
+            if (digest_status st = hip_check(
+                    digest::launch_spmm_gemm(p->n_own, rowptr, col, val,
+                                             p->at<uint8_t>(p->lay.fuse_order), src0, halo,
+                                             p->n_own, lh, d_in, ah, lh, w, d_out, h_out, d_out,
+                                             act == DIGEST_ACT_RELU, s),
+                    "fused forward"))
+                return st;
+            p->fwd_done[layer] = 1;
+            p->act[layer] = act;
+            p->tf[layer] = tf;
+            p->fwd_gen[layer] = p->pull_gen[layer - 1];
+            return DIGEST_OK;
         }
         if (digest_status st = run_spmm(p, Csr::Fwd, src0, halo, p->n_own, lh, ah, layer, s))
             return st;
@@ -2071,6 +2158,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
     const bool relu = layer < p.L;
     pl.transform_first = !relu && p.n_own > 0 && transform_first_cheaper(p, layer);
     pl.forward_narrow = narrow_out(d_in, d_out);
+    pl.forward_fused = fuse_forward(p, layer, pl.transform_first);
     if (pl.transform_first) {
         pl.dw_slices = tf_plan(p.n_own, p.n_halo, d_in, d_out).slices;
         pl.dgrad_fused = layer > 1 && narrow_valu(d_in, d_out) &&
@@ -2173,10 +2261,24 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
                 put(K_GEMM_DH, l, 4 * (n * dout + di * dout + n * di), 2 * n * di * dout);
             continue;
         }
-        put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * di + 4 * n * di, 0.0, p->nnz);
+        if (pl.forward_fused) {
+            // the long-row pass, then the fused pass: the short rows' entries
+            // and distinct sources, the long rows read back, AH of the short
+            // rows written, W, the output
+            const double nl = (double)p->long_rows_f, el = (double)p->long_nnz_f;
+            if (p->long_f > 0)
+                put(K_SPMM_FWD, l, 4 * 2 * nl + 8 * el + 4 * p->src_long_f * di + 4 * nl * di,
+                    0.0, p->long_nnz_f);
+            put(K_SPMM_GEMM_FWD, l,
+                4 * (n + 1) + 8 * (nnz - el) + 4 * p->src_short_f * di + 4 * nl * di +
+                    4 * (n - nl) * di + 4 * di * dout + 4 * n * dout,
+                2 * n * di * dout, p->nnz - p->long_nnz_f);
+        } else {
+            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * di + 4 * n * di, 0.0, p->nnz);
+            put(K_GEMM_FWD, l, 4 * (n * di + di * dout + n * dout), 2 * n * di * dout);
+        }
         if (p->widths[l - 1] % 4)   // the padded copy of h_in
             put(K_PAD_ROWS, l, 4 * n * (di + padded_width(p->widths[l - 1])));
-        put(K_GEMM_FWD, l, 4 * (n * di + di * dout + n * dout), 2 * n * di * dout);
         put(K_GEMM_DW, l, 4 * (n * di + n * dout * (relu ? 2 : 1) + di * dout),
             2 * n * di * dout);
         if (pl.dw_slices > 1)

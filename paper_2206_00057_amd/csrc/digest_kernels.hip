@@ -989,6 +989,206 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
         }
 }
 
+// ---------------------------------------------------------------------------
+// Aggregate-then-transform forward in one pass
+// ---------------------------------------------------------------------------
+
+// Forward of an aggregate-first layer over tiles of kFuseRows consecutive
+// rows.  The 4 waves of a workgroup aggregate the tile's rows into LDS (one
+// wave per row, the rows dealt to the waves in the order `order` gives,
+// longest first, so that the waves' shares are even; a row's entries added
+// in CSR order as in k_spmm), storing each row to ah as well
+// (the weight gradient's operand); then the tile is multiplied by W on MFMA
+// and act(tile W) is stored to C.  A CU holds four such workgroups: while
+// one multiplies, the others gather, so the product runs in the shadow of
+// the memory-bound aggregation instead of as a second pass that reads AH
+// back.  Rows of more than kFuseLong entries are aggregated beforehand (the
+// long-row blocks of the ordinary kernel write them to ah) and read back.
+// A lane gathers VEC floats of a row (d <= 64 VEC, sources of row stride
+// lds, ah of row stride ld_ah, both multiples of VEC); columns d .. ld_ah of
+// ah are stored as zeros.  In the product, wave w owns the 64-column blocks
+// w, w + 4, ... of C (two 32x32 accumulator chains of
+// v_mfma_f32_32x32x2f32 over the tile's 32 rows).  It reads its columns of
+// W, row-major [d][N], straight from global memory (W stays in L2), one
+// chunk of KS k-steps ahead, in two register sets used in turn.
+template <int VEC, bool TWO>
+__global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(kFuseWavesPerSimd))) void
+k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+            const float *__restrict__ val, const uint8_t *__restrict__ order,
+            const float *__restrict__ src0,
+            const float *__restrict__ src1, int32_t n_src0, int32_t lds, int32_t d,
+            float *__restrict__ ah, int32_t ld_ah, const float *__restrict__ W, int32_t N,
+            float *__restrict__ C, int32_t ldc, bool relu)
+{
+    constexpr int DMAX = kWave * VEC;
+    constexpr int LS = DMAX + 1;   // odd row stride: a column of the tile spans all banks
+    constexpr int U = VEC == 4 ? 16 : 24;   // entries in flight per wave
+    constexpr int KS = 8;                   // k-steps (of 2) per W chunk
+    constexpr int WAVES = kFuseThreads / kWave;
+    __shared__ float tile[kFuseRows * LS];
+
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int64_t r0 = (int64_t)blockIdx.x * kFuseRows;
+    const int nr = (int)min<int64_t>(kFuseRows, n_rows - r0);
+    const bool lane_cols = lane * VEC < d;
+
+    // Wave w takes the tile positions w, w + WAVES, ... of `order` (rows
+    // dealt longest first).  Lane j looks up the pointers of the wave's j-th
+    // row, then the entry ids and weights of all the wave's rows are fetched
+    // at once (a gathered row has at most kFuseLong <= 64 entries, one per
+    // lane), so that no fetch waits between the rows' gathers.
+    constexpr int RPW = kFuseRows / WAVES;
+    static_assert(kFuseLong <= kWave && RPW <= kWave, "one fetch per row");
+    int my_lr = 0, my_kb = 0, my_ke = 0;
+    if (lane < RPW) {
+        const int p = wave + WAVES * lane;
+        my_lr = p < nr ? (int)order[r0 + p] : p;
+        if (p < nr) {
+            my_kb = rowptr[r0 + my_lr];
+            my_ke = rowptr[r0 + my_lr + 1];
+        }
+    }
+    int mcs[RPW];
+    float mvs[RPW];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+        const int kb = readlane_i(my_kb, j), len = readlane_i(my_ke, j) - kb;
+        mcs[j] = 0;
+        mvs[j] = 0.f;
+        if (len <= kFuseLong && lane < len) {
+            mcs[j] = col[kb + lane];
+            mvs[j] = val[kb + lane];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+        const int mcA = mcs[j];
+        const float mvA = mvs[j];
+        const int lrA = readlane_i(my_lr, j);
+        const int kbA = readlane_i(my_kb, j), keA = readlane_i(my_ke, j);
+        float acc[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            acc[v] = 0.f;
+        const int len = keA - kbA;
+        const int64_t r = r0 + lrA;
+        if (len > kFuseLong) {   // aggregated by the long-row pass
+            if (lane_cols)
+                load_vec<VEC>(ah + r * ld_ah + lane * VEC, acc);
+        } else if (len > 0) {
+            for (int s0 = 0; s0 < len; s0 += U) {
+                float x[U][VEC];
+                float a[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = s0 + u;
+                    const int c = readlane_i(mcA, e & (kWave - 1));
+                    a[u] = readlane_f(mvA, e & (kWave - 1));
+                    const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * lds
+                                                           : src0 + (int64_t)c * lds;
+                    if (e < len && lane_cols) {
+                        load_vec<VEC>(sp + lane * VEC, x[u]);
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v)
+                            x[u][v] = 0.f;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        acc[v] = fmaf(a[u], x[u][v], acc[v]);
+            }
+        }
+        if (len <= kFuseLong && lrA < nr && lane * VEC < ld_ah) {
+            float o[VEC];
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                o[v] = lane * VEC + v < d ? acc[v] : 0.f;
+            store_vec<VEC>(ah + r * ld_ah + lane * VEC, o);
+        }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            tile[lrA * LS + lane * VEC + v] = (lrA < nr && lane * VEC + v < d) ? acc[v] : 0.f;
+    }
+    __syncthreads();
+
+    const int half = lane >> 5, l32 = lane & 31;
+    static_assert(kFuseRows == 32, "one 32-row block per tile");
+    constexpr int NB = 256 / 32 / WAVES;   // 32-column blocks per wave and pass
+    static_assert(NB >= 1 && NB * 32 * WAVES == 256, "256 columns per pass");
+    const int n_chunks = (d + 2 * KS - 1) / (2 * KS);   // chunks of 2 KS k
+    for (int n0 = 32 * NB * wave; n0 < N; n0 += 256) {
+        int nc[NB];
+        bool nok[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int n = n0 + 32 * j + l32;
+            nok[j] = n < N;
+            nc[j] = min(n, N - 1);
+        }
+        floatx16 acc[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[j][e] = 0.f;
+        // W fragments of chunk c (rows k = 2 KS c + 2 st + half, the NB
+        // column blocks), loaded from clamped addresses; entries past d or
+        // N are zeroed where they are used
+        auto load_w = [&](int c, float (&b)[KS][NB]) {
+#pragma unroll
+            for (int st = 0; st < KS; ++st) {
+                const int64_t row = (int64_t)min(2 * KS * c + 2 * st + half, d - 1) * N;
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    b[st][j] = W[row + nc[j]];
+            }
+        };
+        auto mul = [&](int c, const float (&b)[KS][NB]) {
+            float a[KS];
+#pragma unroll
+            for (int st = 0; st < KS; ++st)   // k < DMAX: 2 KS c <= DMAX - 2 KS
+                a[st] = tile[l32 * LS + 2 * KS * c + 2 * st + half];
+#pragma unroll
+            for (int st = 0; st < KS; ++st) {
+                const bool kok = 2 * KS * c + 2 * st + half < d;
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    const float bv = (kok && nok[j]) ? b[st][j] : 0.f;
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[st], bv, acc[j], 0, 0, 0);
+                }
+            }
+        };
+        // chunk c in set c % 2; the loads of chunk c + 1 are in flight while
+        // chunk c is multiplied (chunks past the end load row d - 1 again)
+        float b0[KS][NB], b1[KS][NB];
+        load_w(0, b0);
+        for (int c = 0; c < n_chunks; c += 2) {
+            load_w(c + 1, b1);
+            mul(c, b0);
+            load_w(c + 2, b0);
+            if (c + 1 < n_chunks)
+                mul(c + 1, b1);
+        }
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            if (!nok[j])
+                continue;
+            const int n = n0 + 32 * j + l32;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int m = (e >> 2) * 8 + half * 4 + (e & 3);
+                const float v = relu ? fmaxf(acc[j][e], 0.f) : acc[j][e];
+                if (m < nr)
+                    C[(r0 + m) * ldc + n] = v;
+            }
+        }
+    }
+}
+
 // out[e] = sum over z of part[z][e], z ascending: one element per thread,
 // eight slices in flight (many elements, few slices).
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float *__restrict__ part,
@@ -2243,6 +2443,40 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
         return am ? gemm_q<false, true, true, false, false>(a, s)
                   : gemm_q<false, true, false, false, false>(a, s);
     return hipErrorInvalidValue;
+}
+
+bool spmm_gemm_ok(int32_t d, int32_t lds, int32_t ld_ah, const float *src0, const float *src1,
+                 const float *ah)
+{
+    constexpr int vec = 4;
+    auto al = [&](const float *q) { return q == nullptr || ((uintptr_t)q % (4 * vec)) == 0; };
+    return d >= kFuseMinWidth && d <= kFuseMaxWidth && lds >= d && ld_ah >= d &&
+           lds % vec == 0 &&
+           ld_ah % vec == 0 && al(src0) && al(src1) && al(ah);
+}
+
+hipError_t launch_spmm_gemm(int32_t n_rows, const int32_t *rowptr, const int32_t *col,
+                            const float *val, const uint8_t *order, const float *src0,
+                            const float *src1,
+                            int32_t n_src0, int32_t lds, int32_t d, float *ah, int32_t ld_ah,
+                            const float *W, int32_t N, float *C, int32_t ldc, bool relu,
+                            hipStream_t s)
+{
+    if (n_rows <= 0 || N <= 0)
+        return hipSuccess;
+    if (!spmm_gemm_ok(d, lds, ld_ah, src0, src1, ah) || ldc < N)
+        return hipErrorInvalidValue;
+    const bool two = src1 != nullptr;
+    const unsigned grid = (unsigned)((n_rows + kFuseRows - 1) / kFuseRows);
+#define DIGEST_FUSE_ARGS                                                                      \
+    dim3(grid), dim3(kFuseThreads), 0, s, n_rows, rowptr, col, val, order, src0, src1, n_src0, \
+        lds, d, ah, ld_ah, W, N, C, ldc, relu
+    if (two)
+        hipLaunchKernelGGL((k_spmm_gemm<4, true>), DIGEST_FUSE_ARGS);
+    else
+        hipLaunchKernelGGL((k_spmm_gemm<4, false>), DIGEST_FUSE_ARGS);
+#undef DIGEST_FUSE_ARGS
+    return hipGetLastError();
 }
 
 hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count, float *out,

@@ -223,3 +223,49 @@ def test_tier_plan_follows_the_overrides(monkeypatch):
     h0 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, widths)
     assert D.digest_partition_plan(h0, 1)["tiers_fwd"] == 0
     assert h0.workspace_bytes < h.workspace_bytes
+
+
+def test_fused_forward_plan_and_cost_model(monkeypatch):
+    """The fused forward is planned for aggregate-first layers of 129..256
+    input floats whose product is the MFMA GEMM, at 16,384 owned rows or
+    more (DIGEST_FUSE=2: any count, 0: never); its cost model splits the
+    aggregation at 64 entries per row into the long-row pass and the fused
+    pass (entries, distinct sources, the long rows read back, the short
+    rows' AH written, W, the output) and drops the separate GEMM."""
+    widths = [256, 256, 7]
+    cfg = synth.scaled(synth.CONFIGS["large"], 4000, widths=widths, classes=7)
+    g = synth.make_graph(cfg, seed=7)
+    p = synth.make_partition(cfg, g, 1)
+
+    def create():
+        return D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                         widths)
+
+    monkeypatch.delenv("DIGEST_FUSE", raising=False)
+    h = create()
+    assert D.digest_partition_plan(h, 1)["forward_fused"] == 0   # too few rows
+    monkeypatch.setenv("DIGEST_FUSE", "2")
+    assert D.digest_partition_plan(h, 1)["forward_fused"] == 1
+    assert D.digest_partition_plan(h, 2)["forward_fused"] == 0   # 7 outputs: narrow product
+    lens = np.diff(p.indptr)
+    long_rows = lens > 64
+    assert long_rows.any() and (~long_rows).any()
+    rows = np.repeat(np.arange(p.n_own), lens)
+    src_short = np.unique(p.indices[~long_rows[rows]]).size
+    src_long = np.unique(p.indices[long_rows[rows]]).size
+    n, di, do = p.n_own, widths[0], widths[1]
+    nl, el = int(long_rows.sum()), int(lens[long_rows].sum())
+    m = D.digest_profile_model(h, D.MODEL_GCN)
+    assert "gemm_fwd_relu.l1" not in m
+    assert m["spmm_fwd.l1"] == (8 * nl + 8 * el + 4 * src_long * di + 4 * nl * di, 0.0, el)
+    assert m["spmm_gemm_fwd.l1"] == (
+        4 * (n + 1) + 8 * (h.nnz - el) + 4 * src_short * di + 4 * nl * di + 4 * (n - nl) * di +
+        4 * di * do + 4 * n * do, 2.0 * n * di * do, h.nnz - el)
+    monkeypatch.setenv("DIGEST_FUSE", "0")
+    assert D.digest_partition_plan(h, 1)["forward_fused"] == 0
+    assert "gemm_fwd_relu.l1" in D.digest_profile_model(h, D.MODEL_GCN)
+    # rows of 128 floats or fewer gather too little per load to pay
+    monkeypatch.setenv("DIGEST_FUSE", "2")
+    h2 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                   [100, 256, 7])
+    assert D.digest_partition_plan(h2, 1)["forward_fused"] == 0

@@ -653,6 +653,55 @@ def test_tall_products(widths):
 
 
 # ---------------------------------------------------------------------------
+# the fused forward (each 32-row tile aggregated into LDS and multiplied by
+# W there), forced at small sizes: a padded d_in, column counts that leave
+# partial 64-column blocks and a second 256-column pass, two fused layers,
+# rows long enough for the long-row pass (lognormal degrees: all of them;
+# Zipf degrees up to 4,096: a third of the entries); results
+# against the oracle and the two-pass forward,
+# and bit for bit from one fused run to the next (rows are taken by the
+# waves in whatever order, but each row is summed by one wave in CSR order)
+# ---------------------------------------------------------------------------
+
+FUSED = [((256, 256, 256, 47), "tiny", 1200), ((130, 100, 70), "tiny", 1200),
+         ((133, 130, 9, 70), "tiny", 1200), ((256, 300, 7), "tiny", 1200),
+         ((256, 256, 7), "dense", 2000), ((256, 256, 256, 47), "large", 8000)]
+
+
+@pytest.mark.parametrize("widths,base,n", FUSED,
+                         ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else str(v))
+def test_fused_forward(widths, base, n, monkeypatch):
+    Dm = D()
+    cfg = synth.scaled(synth.CONFIGS[base], n, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=7)
+    part = synth.make_partition(cfg, g, 1)
+    monkeypatch.setenv("DIGEST_FUSE", "2")
+    c = Case(cfg, g, part, label=f"fused{widths}")
+    assert Dm.digest_partition_plan(c.h, 1)["forward_fused"] == 1
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+    # the same forward and weight gradient of layer 1, fused and not
+    x = dev(c.layer_input(1))
+    W = dev(synth.weights(cfg)[0])
+    dh = dev(c.upstream(1))
+    Dm.digest_pull(c.h, 0, dev(c.store(0)))
+    got = {}
+    for mode in ("2", "0", "2b"):
+        monkeypatch.setenv("DIGEST_FUSE", mode[0])
+        out = torch.empty(c.n, widths[1], device="cuda")
+        Dm.digest_layer_forward(c.h, 1, x, W, out, Dm.ACT_RELU)
+        dw = torch.empty(W.shape, device="cuda")
+        Dm.digest_layer_backward(c.h, 1, x, out, dh, W, dw, None)
+        got[mode] = (host(out), host(dw))
+    assert_close(got["2"][0], got["0"][0], f"{c.label} fused vs two-pass forward",
+                 rtol=1e-5, atol=1e-6)
+    assert_close(got["2"][1], got["0"][1], f"{c.label} fused vs two-pass dW",
+                 rtol=1e-5, atol=1e-6)
+    assert_bits(got["2"][0], got["2b"][0], f"{c.label} fused forward run twice")
+    assert_bits(got["2"][1], got["2b"][1], f"{c.label} fused dW run twice")
+
+
+# ---------------------------------------------------------------------------
 # padding columns of the library's buffers hold NaN (the workspace is filled
 # with 0xFF bytes before binding): rows of widths that are not a multiple of
 # 4 floats are read as whole vectors, and nothing of the padding may reach
