@@ -463,6 +463,16 @@ const char *digest_profile_kernel_name(int32_t kind);
  *                       count; the forward also falls back to two passes
  *                       when h_in (d_layer-1 a multiple of 4) is not
  *                       16-byte aligned.
+ *   backward_fused      ReLU aggregate-first layers 2..L-1 with at least
+ *                       16,384 owned rows and 129 <= d_layer <= 256, when
+ *                       dh_in is asked for (and no halo gradient): 1 if the
+ *                       input gradient runs as (P_in^T D) W^T in one pass
+ *                       ("spmm_gemm_bwd"), D = dh_out masked by h_out > 0
+ *                       formed once ("relu_mask", also the weight
+ *                       gradient's operand), W^T formed once
+ *                       ("transpose_w"), rows of P_in^T with more than 64
+ *                       entries aggregated first ("spmm_bwd_transposed").
+ *                       The same DIGEST_FUSE switch.
  * Errors: DIGEST_EINVAL (NULL, layer outside 1..L).
  */
 typedef struct {
@@ -478,6 +488,7 @@ typedef struct {
     int64_t tier_entries_fwd;
     int64_t tier_entries_bwd;
     int32_t forward_fused;
+    int32_t backward_fused;
 } digest_layer_plan;
 
 digest_status digest_partition_plan(const digest_partition *p, int32_t layer,

@@ -62,6 +62,9 @@ enum Kind : int32_t {
     K_GAT_DGRAD,
     K_PAD_ROWS,
     K_SPMM_GEMM_FWD,
+    K_SPMM_GEMM_BWD,
+    K_RELU_MASK,
+    K_TRANSPOSE_W,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
@@ -70,7 +73,7 @@ const char *const kKindNames[K_COUNT] = {
     "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
     "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
     "gat_aggregate_transposed", "gat_score_grad", "gat_score_sums", "gat_datt", "gat_dw",
-    "gat_dgrad", "pad_rows", "spmm_gemm_fwd"};
+    "gat_dgrad", "pad_rows", "spmm_gemm_fwd", "spmm_gemm_bwd", "relu_mask", "transpose_w"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -133,6 +136,48 @@ int32_t gemm_tile_for(int64_t M, int64_t N, int64_t K, bool contraction_over_row
     if (contraction_over_rows)
         return 0;
     return (M >= 20000 && N >= 128) ? 3 : 0;
+}
+
+// A CSR's first n_rows rows split at kFuseLong entries, for the fused
+// passes: the long rows (count, entries), the distinct source rows (of
+// n_cols) that the short and the long rows read, and per tile of kFuseRows
+// rows the order in which its waves take the rows: by descending entry
+// count, long rows (read back, cheap) last, so that the waves' shares are
+// even.
+void fuse_stats(const std::vector<int32_t> &rowptr, const std::vector<int32_t> &col,
+                int32_t n_rows, int64_t n_cols, int64_t &long_rows, int64_t &long_nnz,
+                int64_t &src_short, int64_t &src_long, std::vector<uint8_t> &order)
+{
+    long_rows = long_nnz = src_short = src_long = 0;
+    std::vector<uint8_t> seen((size_t)n_cols, 0);
+    for (int32_t i = 0; i < n_rows; ++i) {
+        const int32_t len = rowptr[i + 1] - rowptr[i];
+        const bool lng = len > digest::kFuseLong;
+        long_rows += lng;
+        long_nnz += lng ? len : 0;
+        for (int32_t k = rowptr[i]; k < rowptr[i + 1]; ++k)
+            seen[col[k]] |= lng ? 2 : 1;
+    }
+    for (const uint8_t v : seen) {
+        src_short += v & 1;
+        src_long += v >> 1;
+    }
+    static_assert(digest::kFuseRows <= 256, "tile offsets fit a byte");
+    order.resize(n_rows);
+    for (int32_t t0 = 0; t0 < n_rows; t0 += digest::kFuseRows) {
+        const int32_t nr = std::min(digest::kFuseRows, n_rows - t0);
+        auto work = [&](int32_t i) {
+            const int32_t len = rowptr[t0 + i + 1] - rowptr[t0 + i];
+            return len > digest::kFuseLong ? -1 : len;
+        };
+        std::vector<int32_t> idx(nr);
+        for (int32_t i = 0; i < nr; ++i)
+            idx[i] = i;
+        std::stable_sort(idx.begin(), idx.end(),
+                         [&](int32_t a, int32_t b) { return work(a) > work(b); });
+        for (int32_t i = 0; i < nr; ++i)
+            order[t0 + i] = (uint8_t)idx[i];
+    }
 }
 
 // Aggregation blocks of a CSR: every long row gets a block of its own (those
@@ -342,6 +387,9 @@ struct digest_partition {
     // by descending entry count (long rows, read back, last), so that the
     // rows the waves take last are the short ones
     std::vector<uint8_t> fuse_order;
+    // the same for P_in^T (the input gradient's aggregation)
+    int64_t long_rows_t = 0, long_nnz_t = 0, src_short_t = 0, src_long_t = 0;
+    std::vector<uint8_t> fuse_order_t;
 
     // Tiered plans of the aggregations (see TierPlan), at most one per
     // (sparse operand, width).
@@ -350,7 +398,9 @@ struct digest_partition {
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
-        size_t fuse_order;              // per owned row, uint8 (see fuse_order below)
+        size_t fuse_order, fuse_order_t;   // per owned row, uint8 (see fuse_order below)
+        size_t fz;                      // the fused input gradient's D and long rows
+        size_t wt;                      // W^T of the fused input gradient
         std::vector<size_t> halo_buf;   // per level 0..L-1, rows padded_width(d_level) apart
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused), padded rows
         size_t tmp, tmp_halo, tbuf, gemm_part, loss_part;
@@ -511,6 +561,7 @@ void plan_layout(digest_partition &p)
     l.owned_gid = take(sizeof(int32_t) * p.n_own);
     l.blocks_f = take(sizeof(SpmmBlock) * p.blocks_f.size());
     l.fuse_order = take(p.fuse_order.size());
+    l.fuse_order_t = take(p.fuse_order_t.size());
     l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
     l.blocks_tf = take(sizeof(SpmmBlock) * p.blocks_tf.size());
     l.blocks_th = take(sizeof(SpmmBlock) * p.blocks_th.size());
@@ -540,6 +591,16 @@ void plan_layout(digest_partition &p)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
         }
     }
+    // the fused input gradient's D and long rows (two n_own x padded rows)
+    // and W^T, for every layer whose width allows it
+    int64_t fz = 0, wt = 0;
+    for (int32_t k = 2; k <= p.L; ++k)
+        if (p.widths[k] >= digest::kFuseMinWidth && p.widths[k] <= digest::kFuseMaxWidth) {
+            fz = std::max<int64_t>(fz, 2 * (int64_t)p.n_own * padded_width(p.widths[k]));
+            wt = std::max<int64_t>(wt, (int64_t)p.widths[k - 1] * p.widths[k]);
+        }
+    l.fz = take(sizeof(float) * (size_t)fz);
+    l.wt = take(sizeof(float) * (size_t)wt);
     l.tmp = take(sizeof(float) * (size_t)p.n_own * wmax);
     l.tmp_halo = take(sizeof(float) * (size_t)p.n_halo * wmax);
     l.tbuf = take(sizeof(float) * (size_t)tbuf);
@@ -765,6 +826,21 @@ const TierPlan *find_tiers(const digest_partition &p, Csr which, int32_t width)
 // that multiplies each aggregated row tile by W while other tiles gather
 // (launch_spmm_gemm).  DIGEST_FUSE=0 never fuses, =2 fuses at any size.
 constexpr int64_t kFuseMinRows = 16384;
+
+// The input gradient of a ReLU aggregate-first layer (layer >= 2, 129..256
+// output floats) runs as P_in^T (D W^T) = (P_in^T D) W^T in one pass over
+// D = dh_out masked by the ReLU derivative (launch_spmm_gemm): the same
+// rules and switch as the fused forward.
+bool fuse_backward(const digest_partition &p, int32_t layer, bool transform_first)
+{
+    const int32_t d_out = p.widths[layer];
+    const int64_t mode = env_int("DIGEST_FUSE", 1);
+    if (mode == 0 || transform_first || layer < 2 || layer >= p.L || p.n_own <= 0 ||
+        d_out < digest::kFuseMinWidth || d_out > digest::kFuseMaxWidth ||
+        (mode == 1 && p.n_own < kFuseMinRows))
+        return false;
+    return find_tiers(p, Csr::InT, p.widths[layer - 1]) == nullptr;
+}
 
 bool fuse_forward(const digest_partition &p, int32_t layer, bool transform_first)
 {
@@ -1003,38 +1079,11 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
             }
 
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
-        {
-            std::vector<uint8_t> seen((size_t)p->n_own + p->n_halo, 0);
-            for (int32_t i = 0; i < (int32_t)n_owned; ++i) {
-                const int32_t len = p->rowptr[i + 1] - p->rowptr[i];
-                const bool lng = len > digest::kFuseLong;
-                p->long_rows_f += lng;
-                p->long_nnz_f += lng ? len : 0;
-                for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k)
-                    seen[p->col[k]] |= lng ? 2 : 1;
-            }
-            for (const uint8_t v : seen) {
-                p->src_short_f += v & 1;
-                p->src_long_f += v >> 1;
-            }
-            static_assert(digest::kFuseRows <= 256, "tile offsets fit a byte");
-            p->fuse_order.resize(n_owned);
-            for (int64_t t0 = 0; t0 < n_owned; t0 += digest::kFuseRows) {
-                const int32_t nr = (int32_t)std::min<int64_t>(digest::kFuseRows, n_owned - t0);
-                auto work = [&](int32_t i) {
-                    const int32_t len = p->rowptr[t0 + i + 1] - p->rowptr[t0 + i];
-                    return len > digest::kFuseLong ? -1 : len;
-                };
-                std::vector<int32_t> idx(nr);
-                for (int32_t i = 0; i < nr; ++i)
-                    idx[i] = i;
-                std::stable_sort(idx.begin(), idx.end(),
-                                 [&](int32_t a, int32_t b) { return work(a) > work(b); });
-                for (int32_t i = 0; i < nr; ++i)
-                    p->fuse_order[t0 + i] = (uint8_t)idx[i];
-            }
-        }
+        fuse_stats(p->rowptr, p->col, (int32_t)n_owned, p->n_own + p->n_halo, p->long_rows_f,
+                   p->long_nnz_f, p->src_short_f, p->src_long_f, p->fuse_order);
         p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
+        fuse_stats(p->t_rowptr, p->t_src, (int32_t)n_owned, p->n_own, p->long_rows_t,
+                   p->long_nnz_t, p->src_short_t, p->src_long_t, p->fuse_order_t);
         p->long_tf = build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
         {
             const std::vector<int32_t> halo_rows(p->t_rowptr.begin() + n_owned,
@@ -1127,6 +1176,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.owned_gid, p->owned_gid.data(), sizeof(int32_t) * p->owned_gid.size()},
         {l.blocks_f, p->blocks_f.data(), sizeof(SpmmBlock) * p->blocks_f.size()},
         {l.fuse_order, p->fuse_order.data(), p->fuse_order.size()},
+        {l.fuse_order_t, p->fuse_order_t.data(), p->fuse_order_t.size()},
         {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
         {l.blocks_tf, p->blocks_tf.data(), sizeof(SpmmBlock) * p->blocks_tf.size()},
         {l.blocks_th, p->blocks_th.data(), sizeof(SpmmBlock) * p->blocks_th.size()},
@@ -1311,7 +1361,8 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
                 return st;
             src0 = hp;
         }
-        if (fuse_forward(*p, layer, tf) && digest::spmm_gemm_ok(d_in, lh, lh, src0, halo, ah)) {
+        if (fuse_forward(*p, layer, tf) &&
+            digest::spmm_gemm_ok(d_in, lh, lh, src0, halo, ah, ah)) {
             // the long rows through the ordinary kernel's long-row blocks,
             // then every row tile aggregated and multiplied by W in one pass
             const int32_t *rowptr = p->at<int32_t>(p->lay.rowptr);
@@ -1330,8 +1381,8 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             if (digest_status st = hip_check(
                     digest::launch_spmm_gemm(p->n_own, rowptr, col, val,
                                              p->at<uint8_t>(p->lay.fuse_order), src0, halo,
-                                             p->n_own, lh, d_in, ah, lh, w, d_out, h_out, d_out,
-                                             act == DIGEST_ACT_RELU, s),
+                                             p->n_own, lh, d_in, ah, ah, lh, w, d_out, h_out,
+                                             d_out, act == DIGEST_ACT_RELU, s),
                     "fused forward"))
                 return st;
             p->fwd_done[layer] = 1;
@@ -1548,6 +1599,17 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
         return backward_transform_first(p, layer, h_in, dh_out, w, dw, dh_in, dh_halo, s);
     const bool relu = p->act[layer] == DIGEST_ACT_RELU;
     const float *ah = p->at<float>(p->lay.ah[layer]);
+    // The fused input gradient: D = dh_out masked by the ReLU derivative is
+    // formed once (the weight gradient reads it too), then (P_in^T D) W^T in
+    // one pass after a long-row pass.
+    const int32_t ldz = padded_width(d_out);
+    float *dz = p->at<float>(p->lay.fz);
+    float *zpre = dz + (int64_t)p->n_own * ldz;
+    const bool fused = dh_in && !dh_halo && relu && p->n_own > 0 &&
+                       fuse_backward(*p, layer, false) &&
+                       digest::spmm_gemm_ok(d_out, ldz, ldz, dz, nullptr, nullptr, zpre);
+    const float *gd = fused ? dz : dh_out;   // the weight gradient's D operand
+    const int32_t ldd = fused ? ldz : d_out;
 
     // dW = AH^T D, D = dh_out (masked by h_out > 0 for ReLU), split over rows,
     // on stream sw.
@@ -1559,9 +1621,9 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
         g.A = ah;
         g.lda = padded_width(d_in);
         g.a_trans = true;
-        g.B = dh_out;
-        g.ldb = d_out;
-        g.b_mask = relu ? h_out : nullptr;
+        g.B = gd;
+        g.ldb = ldd;
+        g.b_mask = relu && !fused ? h_out : nullptr;
         splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
         g.tile = gemm_tile_for(d_in, d_out, p->n_own, true);
         float *gpart = p->at<float>(p->lay.gemm_part);
@@ -1600,6 +1662,43 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
         return weight_grad(sw);
     };
     const digest_status st_all = [&]() -> digest_status {
+        if (fused) {
+            {
+                Timed t(p, K_RELU_MASK, layer, s);
+                if (digest_status st = hip_check(digest::launch_relu_mask(p->n_own, d_out, dh_out,
+                                                                          d_out, h_out, d_out,
+                                                                          dz, ldz, s),
+                                                 "relu mask"))
+                    return st;
+            }
+            if (digest_status st = start_weight_grad())
+                return st;
+            float *wt = p->at<float>(p->lay.wt);
+            {
+                Timed t(p, K_TRANSPOSE_W, layer, s);
+                if (digest_status st =
+                        hip_check(digest::launch_transpose(d_in, d_out, w, wt, s), "W^T"))
+                    return st;
+            }
+            const int32_t *trp = p->at<int32_t>(p->lay.t_rowptr);
+            const int32_t *tsrc = p->at<int32_t>(p->lay.t_src);
+            const float *tval = p->at<float>(p->lay.t_val);
+            if (p->long_t > 0) {
+                Timed t(p, K_SPMM_BWD, layer, s);
+                if (digest_status st = hip_check(
+                        digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_t), p->long_t,
+                                            p->long_t, trp, tsrc, tval, dz, nullptr, p->n_own,
+                                            ldz, zpre, s),
+                        "transposed spmm long rows"))
+                    return st;
+            }
+            Timed t(p, K_SPMM_GEMM_BWD, layer, s);
+            return hip_check(digest::launch_spmm_gemm(p->n_own, trp, tsrc, tval,
+                                                      p->at<uint8_t>(p->lay.fuse_order_t), dz,
+                                                      nullptr, p->n_own, ldz, d_out, nullptr,
+                                                      zpre, ldz, wt, d_in, dh_in, d_in, false, s),
+                             "fused input gradient");
+        }
         // P_in^T alone, or P_m^T with its halo rows split off
         const Csr tr = dh_halo ? Csr::FullT : Csr::InT;
         const int32_t split = dh_halo ? p->n_own : INT32_MAX;
@@ -2159,6 +2258,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
     pl.transform_first = !relu && p.n_own > 0 && transform_first_cheaper(p, layer);
     pl.forward_narrow = narrow_out(d_in, d_out);
     pl.forward_fused = fuse_forward(p, layer, pl.transform_first);
+    pl.backward_fused = fuse_backward(p, layer, pl.transform_first);
     if (pl.transform_first) {
         pl.dw_slices = tf_plan(p.n_own, p.n_halo, d_in, d_out).slices;
         pl.dgrad_fused = layer > 1 && narrow_valu(d_in, d_out) &&
@@ -2279,11 +2379,25 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
         }
         if (p->widths[l - 1] % 4)   // the padded copy of h_in
             put(K_PAD_ROWS, l, 4 * n * (di + padded_width(p->widths[l - 1])));
-        put(K_GEMM_DW, l, 4 * (n * di + n * dout * (relu ? 2 : 1) + di * dout),
+        put(K_GEMM_DW, l, 4 * (n * di + n * dout * (relu && !pl.backward_fused ? 2 : 1) + di * dout),
             2 * n * di * dout);
         if (pl.dw_slices > 1)
             put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);
-        if (l > 1) {
+        if (l > 1 && pl.backward_fused) {
+            // D formed once; the long rows of P_in^T over D, then the fused
+            // pass: the short rows' entries and distinct sources, the long
+            // rows read back, W^T, dh_in
+            const double nl = (double)p->long_rows_t, el = (double)p->long_nnz_t;
+            put(K_RELU_MASK, l, 12 * n * dout);
+            put(K_TRANSPOSE_W, l, 8 * di * dout);
+            if (p->long_t > 0)
+                put(K_SPMM_BWD, l, 4 * 2 * nl + 8 * el + 4 * p->src_long_t * dout + 4 * nl * dout,
+                    0.0, p->long_nnz_t);
+            put(K_SPMM_GEMM_BWD, l,
+                4 * (n + 1) + 8 * (nnz_in - el) + 4 * p->src_short_t * dout + 4 * nl * dout +
+                    4 * di * dout + 4 * n * di,
+                2 * n * di * dout, p->nnz_in - p->long_nnz_t);
+        } else if (l > 1) {
             const double w = pl.dgrad_narrow_first ? dout : di;
             put(K_SPMM_BWD, l, 4 * (n + 1) + 8 * nnz_in + 8 * n * w, 0.0, p->nnz_in);
             put(K_GEMM_DH, l,

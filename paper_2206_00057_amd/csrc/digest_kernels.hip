@@ -989,36 +989,80 @@ __global__ __launch_bounds__(256) void k_gemm(int32_t M, int32_t N, int32_t K, i
         }
 }
 
+// out[r][c] = h[r][c] > 0 ? g[r][c] : 0 for r < n, c < d (row strides ldg,
+// ldh, ldo), VEC floats per thread.
+template <int VEC>
+__global__ __launch_bounds__(256) void k_relu_mask(int64_t n, int32_t d, const float *__restrict__ g,
+                                                   int32_t ldg, const float *__restrict__ h,
+                                                   int32_t ldh, float *__restrict__ out,
+                                                   int32_t ldo)
+{
+    const int32_t dv = d / VEC;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n * dv)
+        return;
+    const int64_t r = i / dv;
+    const int32_t c = (int32_t)(i % dv) * VEC;
+    float gv[VEC], hv[VEC];
+    load_vec<VEC>(g + r * ldg + c, gv);
+    load_vec<VEC>(h + r * ldh + c, hv);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v)
+        gv[v] = hv[v] > 0.f ? gv[v] : 0.f;
+    store_vec<VEC>(out + r * ldo + c, gv);
+}
+
+// dst[c][r] = src[r][c] for a rows x cols row-major src: 32x32 tiles through LDS.
+__global__ __launch_bounds__(256) void k_transpose(int32_t rows, int32_t cols,
+                                                   const float *__restrict__ src,
+                                                   float *__restrict__ dst)
+{
+    __shared__ float t[32][33];
+    const int32_t r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+    const int tx = threadIdx.x % 32, ty = threadIdx.x / 32;   // 8 rows of 32
+    for (int y = ty; y < 32; y += 8)
+        if (r0 + y < rows && c0 + tx < cols)
+            t[y][tx] = src[(int64_t)(r0 + y) * cols + c0 + tx];
+    __syncthreads();
+    for (int y = ty; y < 32; y += 8)
+        if (c0 + y < cols && r0 + tx < rows)
+            dst[(int64_t)(c0 + y) * rows + r0 + tx] = t[tx][y];
+}
+
 // ---------------------------------------------------------------------------
-// Aggregate-then-transform forward in one pass
+// An aggregation and a product in one pass
 // ---------------------------------------------------------------------------
 
-// Forward of an aggregate-first layer over tiles of kFuseRows consecutive
-// rows.  The 4 waves of a workgroup aggregate the tile's rows into LDS (one
-// wave per row, the rows dealt to the waves in the order `order` gives,
-// longest first, so that the waves' shares are even; a row's entries added
-// in CSR order as in k_spmm), storing each row to ah as well
-// (the weight gradient's operand); then the tile is multiplied by W on MFMA
-// and act(tile W) is stored to C.  A CU holds four such workgroups: while
-// one multiplies, the others gather, so the product runs in the shadow of
-// the memory-bound aggregation instead of as a second pass that reads AH
-// back.  Rows of more than kFuseLong entries are aggregated beforehand (the
-// long-row blocks of the ordinary kernel write them to ah) and read back.
-// A lane gathers VEC floats of a row (d <= 64 VEC, sources of row stride
-// lds, ah of row stride ld_ah, both multiples of VEC); columns d .. ld_ah of
-// ah are stored as zeros.  In the product, wave w owns the 64-column blocks
-// w, w + 4, ... of C (two 32x32 accumulator chains of
-// v_mfma_f32_32x32x2f32 over the tile's 32 rows).  It reads its columns of
-// W, row-major [d][N], straight from global memory (W stays in L2), one
-// chunk of KS k-steps ahead, in two register sets used in turn.
+// An aggregation and a product in one pass, over tiles of kFuseRows
+// consecutive rows (the forward of an aggregate-first layer, AH and act(AH
+// W); or the input gradient (P_in^T D) W^T).  The 4 waves of a workgroup
+// aggregate the tile's rows into LDS (one wave per row, the rows dealt to
+// the waves in the order `order` gives, longest first, so that the waves'
+// shares are even; a row's entries added in CSR order as in k_spmm),
+// storing each row to ah as well when ah is given (the forward keeps AH for
+// the weight gradient); then the tile is multiplied by W on MFMA and
+// act(tile W) is stored to C.  A CU holds four such workgroups: while one
+// multiplies, the others gather, so the product runs in the shadow of the
+// memory-bound aggregation instead of as a second pass that reads the
+// aggregate back.  Rows of more than kFuseLong entries are aggregated
+// beforehand (the long-row blocks of the ordinary kernel write them to pre)
+// and read back.  A lane gathers VEC floats of a row (d <= 64 VEC, sources
+// of row stride lds, ah and pre of row stride ld_ah, all multiples of VEC);
+// columns d .. ld_ah of ah are stored as zeros.  In the product, each wave
+// owns 256 / WAVES columns of every 256-column pass of C (32-column blocks,
+// one v_mfma_f32_32x32x2f32 accumulator chain each, over the tile's 32
+// rows).  It reads its columns of W, row-major [d][N], straight from global
+// memory (W stays in L2), one chunk of KS k-steps ahead, in two register
+// sets used in turn.
 template <int VEC, bool TWO>
 __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(kFuseWavesPerSimd))) void
 k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
             const float *__restrict__ val, const uint8_t *__restrict__ order,
             const float *__restrict__ src0,
             const float *__restrict__ src1, int32_t n_src0, int32_t lds, int32_t d,
-            float *__restrict__ ah, int32_t ld_ah, const float *__restrict__ W, int32_t N,
-            float *__restrict__ C, int32_t ldc, bool relu)
+            float *__restrict__ ah, const float *__restrict__ pre, int32_t ld_ah,
+            const float *__restrict__ W, int32_t N, float *__restrict__ C, int32_t ldc,
+            bool relu)
 {
     constexpr int DMAX = kWave * VEC;
     constexpr int LS = DMAX + 1;   // odd row stride: a column of the tile spans all banks
@@ -1075,7 +1119,7 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
         const int64_t r = r0 + lrA;
         if (len > kFuseLong) {   // aggregated by the long-row pass
             if (lane_cols)
-                load_vec<VEC>(ah + r * ld_ah + lane * VEC, acc);
+                load_vec<VEC>(pre + r * ld_ah + lane * VEC, acc);
         } else if (len > 0) {
             for (int s0 = 0; s0 < len; s0 += U) {
                 float x[U][VEC];
@@ -1102,7 +1146,7 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
                         acc[v] = fmaf(a[u], x[u][v], acc[v]);
             }
         }
-        if (len <= kFuseLong && lrA < nr && lane * VEC < ld_ah) {
+        if (ah && len <= kFuseLong && lrA < nr && lane * VEC < ld_ah) {
             float o[VEC];
 #pragma unroll
             for (int v = 0; v < VEC; ++v)
@@ -2445,32 +2489,63 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
     return hipErrorInvalidValue;
 }
 
+hipError_t launch_relu_mask(int64_t n, int32_t d, const float *g, int32_t ldg, const float *h,
+                            int32_t ldh, float *out, int32_t ldo, hipStream_t s)
+{
+    if (n <= 0 || d <= 0)
+        return hipSuccess;
+    auto al = [](const void *q) { return ((uintptr_t)q % 16) == 0; };
+    const bool v4 = d % 4 == 0 && ldg % 4 == 0 && ldh % 4 == 0 && ldo % 4 == 0 && al(g) &&
+                    al(h) && al(out);
+    const int64_t items = n * (v4 ? d / 4 : d);
+    const int64_t grid = (items + 255) / 256;
+    if (grid > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    if (v4)
+        hipLaunchKernelGGL((k_relu_mask<4>), dim3((unsigned)grid), dim3(256), 0, s, n, d, g, ldg,
+                           h, ldh, out, ldo);
+    else
+        hipLaunchKernelGGL((k_relu_mask<1>), dim3((unsigned)grid), dim3(256), 0, s, n, d, g, ldg,
+                           h, ldh, out, ldo);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose(int32_t rows, int32_t cols, const float *src, float *dst,
+                            hipStream_t s)
+{
+    if (rows <= 0 || cols <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_transpose,
+                       dim3((unsigned)((cols + 31) / 32), (unsigned)((rows + 31) / 32)),
+                       dim3(256), 0, s, rows, cols, src, dst);
+    return hipGetLastError();
+}
+
 bool spmm_gemm_ok(int32_t d, int32_t lds, int32_t ld_ah, const float *src0, const float *src1,
-                 const float *ah)
+                  const float *ah, const float *pre)
 {
     constexpr int vec = 4;
     auto al = [&](const float *q) { return q == nullptr || ((uintptr_t)q % (4 * vec)) == 0; };
     return d >= kFuseMinWidth && d <= kFuseMaxWidth && lds >= d && ld_ah >= d &&
            lds % vec == 0 &&
-           ld_ah % vec == 0 && al(src0) && al(src1) && al(ah);
+           ld_ah % vec == 0 && al(src0) && al(src1) && al(ah) && al(pre);
 }
 
 hipError_t launch_spmm_gemm(int32_t n_rows, const int32_t *rowptr, const int32_t *col,
                             const float *val, const uint8_t *order, const float *src0,
-                            const float *src1,
-                            int32_t n_src0, int32_t lds, int32_t d, float *ah, int32_t ld_ah,
-                            const float *W, int32_t N, float *C, int32_t ldc, bool relu,
-                            hipStream_t s)
+                            const float *src1, int32_t n_src0, int32_t lds, int32_t d,
+                            float *ah, const float *pre, int32_t ld_ah, const float *W,
+                            int32_t N, float *C, int32_t ldc, bool relu, hipStream_t s)
 {
     if (n_rows <= 0 || N <= 0)
         return hipSuccess;
-    if (!spmm_gemm_ok(d, lds, ld_ah, src0, src1, ah) || ldc < N)
+    if (!pre || !spmm_gemm_ok(d, lds, ld_ah, src0, src1, ah, pre) || ldc < N)
         return hipErrorInvalidValue;
     const bool two = src1 != nullptr;
     const unsigned grid = (unsigned)((n_rows + kFuseRows - 1) / kFuseRows);
 #define DIGEST_FUSE_ARGS                                                                      \
     dim3(grid), dim3(kFuseThreads), 0, s, n_rows, rowptr, col, val, order, src0, src1, n_src0, \
-        lds, d, ah, ld_ah, W, N, C, ldc, relu
+        lds, d, ah, pre, ld_ah, W, N, C, ldc, relu
     if (two)
         hipLaunchKernelGGL((k_spmm_gemm<4, true>), DIGEST_FUSE_ARGS);
     else

@@ -95,16 +95,16 @@ hipError_t launch_spmm_sliced(const SpmmBlock *blocks, int32_t n_blocks, int32_t
                               int64_t nnz, const float *src0, const float *src1, int32_t n_src0,
                               int32_t n_rows, int32_t d, float *out0, bool acc, hipStream_t s);
 
-// Forward of an aggregate-first layer in one pass: AH = the aggregation of
-// rows 0 .. n_rows-1 (as launch_spmm, sources of row stride lds, d floats
-// gathered) is stored to ah (row stride ld_ah, columns d .. ld_ah zero) and
-// C = act(AH W) (W row-major [d][N], C of row stride ldc) is computed from
-// the tiles of AH in LDS.  Rows with more than kFuseLong entries must
-// already be in ah (the long-row blocks of launch_spmm over the same CSR,
-// run before on the same stream); the others are gathered here.  order
-// holds, per tile of kFuseRows rows, a permutation of its row offsets: the
-// order in which the tile's waves take the rows.  Needs
-// spmm_gemm_ok(d, lds, ld_ah, src0, src1, ah).
+// An aggregation and a product in one pass: AH = the aggregation of rows
+// 0 .. n_rows-1 (as launch_spmm, sources of row stride lds, d floats
+// gathered) is stored to ah (row stride ld_ah, columns d .. ld_ah zero; ah
+// may be null) and C = act(AH W) (W row-major [d][N], C of row stride ldc)
+// is computed from the tiles of AH in LDS.  Rows with more than kFuseLong
+// entries must already be in pre (row stride ld_ah; the long-row blocks of
+// launch_spmm over the same CSR, run before on the same stream); the others
+// are gathered here.  order holds, per tile of kFuseRows rows, a
+// permutation of its row offsets: the order in which the tile's waves take
+// the rows.  Needs spmm_gemm_ok(d, lds, ld_ah, src0, src1, ah, pre).
 constexpr int kFuseRows = 32;
 constexpr int kFuseThreads = 256;
 constexpr int kFuseWavesPerSimd = 4;   // workgroups per CU x waves per workgroup / 4
@@ -112,12 +112,19 @@ constexpr int32_t kFuseLong = kSpmmLongRow;
 constexpr int32_t kFuseMaxWidth = 256;
 constexpr int32_t kFuseMinWidth = 129;   // narrower rows gather too few bytes per load
 bool spmm_gemm_ok(int32_t d, int32_t lds, int32_t ld_ah, const float *src0, const float *src1,
-                  const float *ah);
+                  const float *ah, const float *pre);
 hipError_t launch_spmm_gemm(int32_t n_rows, const int32_t *rowptr, const int32_t *col,
                             const float *val, const uint8_t *order, const float *src0,
-                            const float *src1,
-                            int32_t n_src0, int32_t lds, int32_t d, float *ah, int32_t ld_ah,
-                            const float *W, int32_t N, float *C, int32_t ldc, bool relu,
+                            const float *src1, int32_t n_src0, int32_t lds, int32_t d,
+                            float *ah, const float *pre, int32_t ld_ah, const float *W,
+                            int32_t N, float *C, int32_t ldc, bool relu, hipStream_t s);
+
+// out[r][c] = h[r][c] > 0 ? g[r][c] : 0 (the ReLU derivative applied), row
+// strides ldg, ldh, ldo.
+hipError_t launch_relu_mask(int64_t n, int32_t d, const float *g, int32_t ldg, const float *h,
+                            int32_t ldh, float *out, int32_t ldo, hipStream_t s);
+// dst (cols x rows) = src^T for a row-major rows x cols src.
+hipError_t launch_transpose(int32_t rows, int32_t cols, const float *src, float *dst,
                             hipStream_t s);
 
 // C = op(A) op(B) in fp32 on MFMA, K-range split into `splits`

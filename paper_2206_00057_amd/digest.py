@@ -435,7 +435,8 @@ class LayerPlan(ctypes.Structure):
                 ("dgrad_fused", ctypes.c_int32), ("tiers_fwd", ctypes.c_int32),
                 ("tiers_bwd", ctypes.c_int32), ("tier_rows_fwd", ctypes.c_int32),
                 ("tier_rows_bwd", ctypes.c_int32), ("tier_entries_fwd", ctypes.c_int64),
-                ("tier_entries_bwd", ctypes.c_int64), ("forward_fused", ctypes.c_int32)]
+                ("tier_entries_bwd", ctypes.c_int64), ("forward_fused", ctypes.c_int32),
+                ("backward_fused", ctypes.c_int32)]
 
 
 def digest_partition_plan(p, layer):

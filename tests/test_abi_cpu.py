@@ -264,6 +264,47 @@ def test_fused_forward_plan_and_cost_model(monkeypatch):
     monkeypatch.setenv("DIGEST_FUSE", "0")
     assert D.digest_partition_plan(h, 1)["forward_fused"] == 0
     assert "gemm_fwd_relu.l1" in D.digest_profile_model(h, D.MODEL_GCN)
+
+
+def test_fused_input_gradient_plan_and_cost_model(monkeypatch):
+    """The input gradient of a ReLU aggregate-first layer >= 2 with 129..256
+    output floats is planned as one fused pass over P_in^T (rows split at 64
+    entries) after D is formed once; the weight gradient then reads D
+    without the mask, and the separate input-gradient GEMM is gone."""
+    widths = [100, 256, 256, 7]
+    cfg = synth.scaled(synth.CONFIGS["large"], 4000, widths=widths, classes=7)
+    g = synth.make_graph(cfg, seed=7)
+    p = synth.make_partition(cfg, g, 1)
+    monkeypatch.setenv("DIGEST_FUSE", "2")
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, widths)
+    assert D.digest_partition_plan(h, 2)["backward_fused"] == 1
+    assert D.digest_partition_plan(h, 1)["backward_fused"] == 0   # no input gradient
+    assert D.digest_partition_plan(h, 3)["backward_fused"] == 0   # identity layer
+    # P_in^T: the owned-to-owned entries, by source row
+    pos = {int(v): i for i, v in enumerate(p.owned)}
+    rows = np.repeat(np.arange(p.n_own), np.diff(p.indptr))
+    inn = np.array([int(c) in pos for c in p.indices])
+    src = rows[inn]
+    dst = np.array([pos[int(c)] for c in p.indices[inn]])
+    lens = np.bincount(dst, minlength=p.n_own)
+    long_rows = lens > 64
+    assert long_rows.any() and (~long_rows).any()
+    src_short = np.unique(src[~long_rows[dst]]).size
+    src_long = np.unique(src[long_rows[dst]]).size
+    n, di, do = p.n_own, widths[1], widths[2]
+    nl, el = int(long_rows.sum()), int(lens[long_rows].sum())
+    m = D.digest_profile_model(h, D.MODEL_GCN)
+    assert "gemm_dgrad.l2" not in m
+    assert m["relu_mask.l2"][0] == 12 * n * do and m["transpose_w.l2"][0] == 8 * di * do
+    assert m["spmm_bwd_transposed.l2"] == (8 * nl + 8 * el + 4 * src_long * do + 4 * nl * do,
+                                           0.0, el)
+    assert m["spmm_gemm_bwd.l2"] == (
+        4 * (n + 1) + 8 * (h.nnz_in - el) + 4 * src_short * do + 4 * nl * do + 4 * di * do +
+        4 * n * di, 2.0 * n * di * do, h.nnz_in - el)
+    assert m["gemm_dw_splitk.l2"][0] == 4 * (n * di + n * do + di * do)
+    monkeypatch.setenv("DIGEST_FUSE", "0")
+    assert D.digest_partition_plan(h, 2)["backward_fused"] == 0
+    assert "gemm_dgrad.l2" in D.digest_profile_model(h, D.MODEL_GCN)
     # rows of 128 floats or fewer gather too little per load to pay
     monkeypatch.setenv("DIGEST_FUSE", "2")
     h2 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,

@@ -653,8 +653,8 @@ def test_tall_products(widths):
 
 
 # ---------------------------------------------------------------------------
-# the fused forward (each 32-row tile aggregated into LDS and multiplied by
-# W there), forced at small sizes: a padded d_in, column counts that leave
+# the fused forward and input gradient (each 32-row tile aggregated into LDS
+# and multiplied by W or W^T there), forced at small sizes: a padded d_in, column counts that leave
 # partial 64-column blocks and a second 256-column pass, two fused layers,
 # rows long enough for the long-row pass (lognormal degrees: all of them;
 # Zipf degrees up to 4,096: a third of the entries); results
@@ -665,7 +665,8 @@ def test_tall_products(widths):
 
 FUSED = [((256, 256, 256, 47), "tiny", 1200), ((130, 100, 70), "tiny", 1200),
          ((133, 130, 9, 70), "tiny", 1200), ((256, 300, 7), "tiny", 1200),
-         ((256, 256, 7), "dense", 2000), ((256, 256, 256, 47), "large", 8000)]
+         ((256, 256, 7), "dense", 2000), ((256, 256, 256, 47), "large", 8000),
+         ((100, 200, 256, 7), "large", 8000), ((64, 140, 150, 5), "tiny", 1200)]
 
 
 @pytest.mark.parametrize("widths,base,n", FUSED,
@@ -677,9 +678,30 @@ def test_fused_forward(widths, base, n, monkeypatch):
     part = synth.make_partition(cfg, g, 1)
     monkeypatch.setenv("DIGEST_FUSE", "2")
     c = Case(cfg, g, part, label=f"fused{widths}")
-    assert Dm.digest_partition_plan(c.h, 1)["forward_fused"] == 1
+    plans = [Dm.digest_partition_plan(c.h, l) for l in range(1, c.L + 1)]
+    assert any(pl["forward_fused"] or pl["backward_fused"] for pl in plans)
     for layer in range(1, c.L + 1):
         check_layer(c, layer)
+    # the input gradient of layer 2 (ReLU, aggregate first), fused or not
+    if c.L >= 3:
+        x2 = dev(c.layer_input(2))
+        W2 = dev(synth.weights(cfg)[1])
+        dh2 = dev(c.upstream(2))
+        if c.part.n_halo:
+            Dm.digest_pull(c.h, 1, dev(c.store(1)))
+        got2 = {}
+        for mode in ("2", "0", "2b"):
+            monkeypatch.setenv("DIGEST_FUSE", mode[0])
+            out2 = torch.empty(c.n, widths[2], device="cuda")
+            Dm.digest_layer_forward(c.h, 2, x2, W2, out2, Dm.ACT_RELU)
+            dw2 = torch.empty(W2.shape, device="cuda")
+            dhin = torch.empty(c.n, widths[1], device="cuda")
+            Dm.digest_layer_backward(c.h, 2, x2, out2, dh2, W2, dw2, dhin)
+            got2[mode] = (host(dw2), host(dhin))
+        for i, what in enumerate(("dW", "dH_in")):
+            assert_close(got2["2"][i], got2["0"][i], f"{c.label} fused vs two-pass layer-2 {what}",
+                         rtol=1e-5, atol=1e-6)
+            assert_bits(got2["2"][i], got2["2b"][i], f"{c.label} fused layer-2 {what} run twice")
     # the same forward and weight gradient of layer 1, fused and not
     x = dev(c.layer_input(1))
     W = dev(synth.weights(cfg)[0])
