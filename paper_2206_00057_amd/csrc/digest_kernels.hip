@@ -1046,15 +1046,17 @@ __global__ __launch_bounds__(256) void k_transpose(int32_t rows, int32_t cols,
 // memory-bound aggregation instead of as a second pass that reads the
 // aggregate back.  Rows of more than kFuseLong entries are aggregated
 // beforehand (the long-row blocks of the ordinary kernel write them to pre)
-// and read back.  A lane gathers VEC floats of a row (d <= 64 VEC, sources
-// of row stride lds, ah and pre of row stride ld_ah, all multiples of VEC);
+// and read back.  A row is gathered by G groups of 64 / G lanes, which
+// split its entries and add their sums at the end (as in k_spmm); a lane
+// gathers VEC floats (d <= (64 / G) VEC, sources of row stride lds, ah and
+// pre of row stride ld_ah, all multiples of VEC);
 // columns d .. ld_ah of ah are stored as zeros.  In the product, each wave
 // owns 256 / WAVES columns of every 256-column pass of C (32-column blocks,
 // one v_mfma_f32_32x32x2f32 accumulator chain each, over the tile's 32
 // rows).  It reads its columns of W, row-major [d][N], straight from global
 // memory (W stays in L2), one chunk of KS k-steps ahead, in two register
 // sets used in turn.
-template <int VEC, bool TWO>
+template <int VEC, int G, bool TWO>
 __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(kFuseWavesPerSimd))) void
 k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col,
             const float *__restrict__ val, const uint8_t *__restrict__ order,
@@ -1064,9 +1066,10 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
             const float *__restrict__ W, int32_t N, float *__restrict__ C, int32_t ldc,
             bool relu)
 {
-    constexpr int DMAX = kWave * VEC;
+    constexpr int GL = kWave / G;   // lanes per group; the G groups split a row's entries
+    constexpr int DMAX = GL * VEC;
     constexpr int LS = DMAX + 1;   // odd row stride: a column of the tile spans all banks
-    constexpr int U = VEC == 4 ? 16 : 24;   // entries in flight per wave
+    constexpr int U = 16;          // entries in flight per group
     constexpr int KS = 8;                   // k-steps (of 2) per W chunk
     constexpr int WAVES = kFuseThreads / kWave;
     __shared__ float tile[kFuseRows * LS];
@@ -1075,7 +1078,8 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
     const int wave = threadIdx.x / kWave;
     const int64_t r0 = (int64_t)blockIdx.x * kFuseRows;
     const int nr = (int)min<int64_t>(kFuseRows, n_rows - r0);
-    const bool lane_cols = lane * VEC < d;
+    const int g = lane / GL, gl = lane % GL;
+    const bool lane_cols = gl * VEC < d;
 
     // Wave w takes the tile positions w, w + WAVES, ... of `order` (rows
     // dealt longest first).  Lane j looks up the pointers of the wave's j-th
@@ -1118,21 +1122,28 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
         const int len = keA - kbA;
         const int64_t r = r0 + lrA;
         if (len > kFuseLong) {   // aggregated by the long-row pass
-            if (lane_cols)
-                load_vec<VEC>(pre + r * ld_ah + lane * VEC, acc);
+            if (g == 0 && lane_cols)
+                load_vec<VEC>(pre + r * ld_ah + gl * VEC, acc);
         } else if (len > 0) {
-            for (int s0 = 0; s0 < len; s0 += U) {
+            // group g takes the entries g, g + G, ... (slot t: entry G t + g)
+            for (int s0 = 0; s0 * G < len; s0 += U) {
                 float x[U][VEC];
                 float a[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    const int e = s0 + u;
-                    const int c = readlane_i(mcA, e & (kWave - 1));
-                    a[u] = readlane_f(mvA, e & (kWave - 1));
+                    const int e = G * (s0 + u) + g;
+                    int c;
+                    if constexpr (G == 1) {
+                        c = readlane_i(mcA, e & (kWave - 1));
+                        a[u] = readlane_f(mvA, e & (kWave - 1));
+                    } else {
+                        c = __shfl(mcA, e & (kWave - 1));
+                        a[u] = __shfl(mvA, e & (kWave - 1));
+                    }
                     const float *sp = (TWO && c >= n_src0) ? src1 + (int64_t)(c - n_src0) * lds
                                                            : src0 + (int64_t)c * lds;
                     if (e < len && lane_cols) {
-                        load_vec<VEC>(sp + lane * VEC, x[u]);
+                        load_vec<VEC>(sp + gl * VEC, x[u]);
                     } else {
 #pragma unroll
                         for (int v = 0; v < VEC; ++v)
@@ -1145,17 +1156,26 @@ k_spmm_gemm(int32_t n_rows, const int32_t *__restrict__ rowptr, const int32_t *_
                     for (int v = 0; v < VEC; ++v)
                         acc[v] = fmaf(a[u], x[u][v], acc[v]);
             }
+            if constexpr (G > 1) {
+#pragma unroll
+                for (int off = GL; off < kWave; off <<= 1)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        acc[v] += __shfl_xor(acc[v], off);
+            }
         }
-        if (ah && len <= kFuseLong && lrA < nr && lane * VEC < ld_ah) {
+        if (ah && g == 0 && len <= kFuseLong && lrA < nr && gl * VEC < ld_ah) {
             float o[VEC];
 #pragma unroll
             for (int v = 0; v < VEC; ++v)
-                o[v] = lane * VEC + v < d ? acc[v] : 0.f;
-            store_vec<VEC>(ah + r * ld_ah + lane * VEC, o);
+                o[v] = gl * VEC + v < d ? acc[v] : 0.f;
+            store_vec<VEC>(ah + r * ld_ah + gl * VEC, o);
         }
+        if (g == 0) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v)
-            tile[lrA * LS + lane * VEC + v] = (lrA < nr && lane * VEC + v < d) ? acc[v] : 0.f;
+            for (int v = 0; v < VEC; ++v)
+                tile[lrA * LS + gl * VEC + v] = (lrA < nr && gl * VEC + v < d) ? acc[v] : 0.f;
+        }
     }
     __syncthreads();
 
@@ -2546,10 +2566,17 @@ hipError_t launch_spmm_gemm(int32_t n_rows, const int32_t *rowptr, const int32_t
 #define DIGEST_FUSE_ARGS                                                                      \
     dim3(grid), dim3(kFuseThreads), 0, s, n_rows, rowptr, col, val, order, src0, src1, n_src0, \
         lds, d, ah, pre, ld_ah, W, N, C, ldc, relu
-    if (two)
-        hipLaunchKernelGGL((k_spmm_gemm<4, true>), DIGEST_FUSE_ARGS);
-    else
-        hipLaunchKernelGGL((k_spmm_gemm<4, false>), DIGEST_FUSE_ARGS);
+    if (d <= 2 * kWave) {   // two lane groups of 32, float4 each, split each row
+        if (two)
+            hipLaunchKernelGGL((k_spmm_gemm<4, 2, true>), DIGEST_FUSE_ARGS);
+        else
+            hipLaunchKernelGGL((k_spmm_gemm<4, 2, false>), DIGEST_FUSE_ARGS);
+    } else {
+        if (two)
+            hipLaunchKernelGGL((k_spmm_gemm<4, 1, true>), DIGEST_FUSE_ARGS);
+        else
+            hipLaunchKernelGGL((k_spmm_gemm<4, 1, false>), DIGEST_FUSE_ARGS);
+    }
 #undef DIGEST_FUSE_ARGS
     return hipGetLastError();
 }

@@ -110,7 +110,7 @@ constexpr int kFuseThreads = 256;
 constexpr int kFuseWavesPerSimd = 4;   // workgroups per CU x waves per workgroup / 4
 constexpr int32_t kFuseLong = kSpmmLongRow;
 constexpr int32_t kFuseMaxWidth = 256;
-constexpr int32_t kFuseMinWidth = 129;   // narrower rows gather too few bytes per load
+constexpr int32_t kFuseMinWidth = 65;   // narrower rows go to the narrow kernels
 bool spmm_gemm_ok(int32_t d, int32_t lds, int32_t ld_ah, const float *src0, const float *src1,
                   const float *ah, const float *pre);
 hipError_t launch_spmm_gemm(int32_t n_rows, const int32_t *rowptr, const int32_t *col,

@@ -226,7 +226,7 @@ def test_tier_plan_follows_the_overrides(monkeypatch):
 
 
 def test_fused_forward_plan_and_cost_model(monkeypatch):
-    """The fused forward is planned for aggregate-first layers of 129..256
+    """The fused forward is planned for aggregate-first layers of 65..256
     input floats whose product is the MFMA GEMM, at 16,384 owned rows or
     more (DIGEST_FUSE=2: any count, 0: never); its cost model splits the
     aggregation at 64 entries per row into the long-row pass and the fused
@@ -267,7 +267,7 @@ def test_fused_forward_plan_and_cost_model(monkeypatch):
 
 
 def test_fused_input_gradient_plan_and_cost_model(monkeypatch):
-    """The input gradient of a ReLU aggregate-first layer >= 2 with 129..256
+    """The input gradient of a ReLU aggregate-first layer >= 2 with 65..256
     output floats is planned as one fused pass over P_in^T (rows split at 64
     entries) after D is formed once; the weight gradient then reads D
     without the mask, and the separate input-gradient GEMM is gone."""
@@ -305,8 +305,10 @@ def test_fused_input_gradient_plan_and_cost_model(monkeypatch):
     monkeypatch.setenv("DIGEST_FUSE", "0")
     assert D.digest_partition_plan(h, 2)["backward_fused"] == 0
     assert "gemm_dgrad.l2" in D.digest_profile_model(h, D.MODEL_GCN)
-    # rows of 128 floats or fewer gather too little per load to pay
+    # rows of 65..128 floats are fused too (two lane groups per row), rows of
+    # 64 floats or fewer go to the narrow kernels
     monkeypatch.setenv("DIGEST_FUSE", "2")
-    h2 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
-                                   [100, 256, 7])
-    assert D.digest_partition_plan(h2, 1)["forward_fused"] == 0
+    for d_in, fused in ((100, 1), (65, 1), (64, 0)):
+        h2 = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo,
+                                       [d_in, 256, 7])
+        assert D.digest_partition_plan(h2, 1)["forward_fused"] == fused, d_in

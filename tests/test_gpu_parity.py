@@ -654,19 +654,21 @@ def test_tall_products(widths):
 
 # ---------------------------------------------------------------------------
 # the fused forward and input gradient (each 32-row tile aggregated into LDS
-# and multiplied by W or W^T there), forced at small sizes: a padded d_in, column counts that leave
-# partial 64-column blocks and a second 256-column pass, two fused layers,
-# rows long enough for the long-row pass (lognormal degrees: all of them;
-# Zipf degrees up to 4,096: a third of the entries); results
-# against the oracle and the two-pass forward,
-# and bit for bit from one fused run to the next (rows are taken by the
-# waves in whatever order, but each row is summed by one wave in CSR order)
+# and multiplied by W or W^T there), forced at small sizes: rows of 65..128
+# floats (two lane groups per row) and of 129..256, a padded width, column
+# counts that leave partial 64-column blocks and a second 256-column pass,
+# two fused layers, rows long enough for the long-row pass (lognormal
+# degrees: all of them; Zipf degrees up to 4,096: a third of the entries);
+# results against the oracle and the two-pass path, and bit for bit from one
+# fused run to the next (rows are dealt to the waves in a fixed order, each
+# summed by one wave in a fixed order)
 # ---------------------------------------------------------------------------
 
 FUSED = [((256, 256, 256, 47), "tiny", 1200), ((130, 100, 70), "tiny", 1200),
          ((133, 130, 9, 70), "tiny", 1200), ((256, 300, 7), "tiny", 1200),
          ((256, 256, 7), "dense", 2000), ((256, 256, 256, 47), "large", 8000),
-         ((100, 200, 256, 7), "large", 8000), ((64, 140, 150, 5), "tiny", 1200)]
+         ((100, 200, 256, 7), "large", 8000), ((64, 140, 150, 5), "tiny", 1200),
+         ((72, 96, 80, 5), "large", 8000)]
 
 
 @pytest.mark.parametrize("widths,base,n", FUSED,
