@@ -52,17 +52,31 @@ def _rows(path, counter):
     with open(path) as fh:
         for r in csv.DictReader(fh):
             if r.get("Counter_Name", counter) == counter:
-                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+                out.append((r["Kernel_Name"], float(r["Counter_Value"]), int(r["Grid_Size"])))
     return out
 
 
-def summarize(fetch_csv, write_csv, kernel_name, copy_name, copy_bytes):
+def _pick(rows, kernel_name, grid_size=0, largest_grid=False):
+    """Counter values of the dispatches of one kernel: those whose name
+    contains kernel_name, and of those the ones of one launch shape (a grid
+    of grid_size work-items, or the largest grid among them) when asked."""
+    m = [(v, g) for n, v, g in rows if kernel_name in n]
+    if grid_size:
+        m = [(v, g) for v, g in m if g == grid_size]
+    elif largest_grid and m:
+        top = max(g for _, g in m)
+        m = [(v, g) for v, g in m if g == top]
+    return [v for v, _ in m]
+
+
+def summarize(fetch_csv, write_csv, kernel_name, copy_name, copy_bytes, grid_size=0,
+              largest_grid=False):
     f = _rows(fetch_csv, "FETCH_SIZE")
     w = _rows(write_csv, "WRITE_SIZE")
-    kf = [v for n, v in f if kernel_name in n]
-    kw = [v for n, v in w if kernel_name in n]
-    cf = max(v for n, v in f if copy_name in n)
-    cw = max(v for n, v in w if copy_name in n)
+    kf = _pick(f, kernel_name, grid_size, largest_grid)
+    kw = _pick(w, kernel_name, grid_size, largest_grid)
+    cf = max(v for n, v, _ in f if copy_name in n)
+    cw = max(v for n, v, _ in w if copy_name in n)
     if not kf or not kw:
         raise SystemExit(f"no dispatch of {kernel_name!r} in the counter files")
     fetch_kib = sum(kf) / len(kf)
@@ -70,7 +84,7 @@ def summarize(fetch_csv, write_csv, kernel_name, copy_name, copy_bytes):
     fetch_scale = cf * 1024.0 / copy_bytes
     write_scale = cw * 1024.0 / copy_bytes
     traffic = fetch_kib * 1024.0 / fetch_scale + write_kib * 1024.0 / write_scale
-    names = sorted({n for n, _ in f if kernel_name in n})
+    names = sorted({n for n, _, _ in f if kernel_name in n})
     return {
         "rocprof_kernel": names[0] if names else kernel_name,
         "dispatches": len(kf),
@@ -151,6 +165,10 @@ def main():
     tr.add_argument("--write", required=True)
     tr.add_argument("--kernel-name", required=True, help="substring of the rocprof kernel name")
     tr.add_argument("--key", required=True, help="bench.py kernel key, e.g. gemm_dw_splitk.l1")
+    tr.add_argument("--grid-size", type=int, default=0,
+                    help="only the dispatches of this grid (work-items), e.g. one layer's launch")
+    tr.add_argument("--largest-grid", action="store_true",
+                    help="only the dispatches of the largest grid among the matches")
     tr.add_argument("--copy-name", default="copyBuffer")
     tr.add_argument("--copy-bytes", type=int, required=True)
     tr.add_argument("--workload", required=True)
@@ -167,7 +185,8 @@ def main():
                   f"# source_sha = {kernel_source_hash()}", "#"]
         lines += counters_table(a.csv, a.kernel_name)
     else:
-        s = summarize(a.fetch, a.write, a.kernel_name, a.copy_name, a.copy_bytes)
+        s = summarize(a.fetch, a.write, a.kernel_name, a.copy_name, a.copy_bytes, a.grid_size,
+                      a.largest_grid)
         lines = [f"# L2-to-fabric traffic of one launch of {a.key} on the {a.workload} workload:",
                  "# the bytes the L2s of the 8 XCDs request from and write to the memory side",
                  "# (Infinity Cache hits included, so not HBM bytes alone), from rocprofv3",
