@@ -392,12 +392,19 @@ def main():
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
     d = kernels[dom]
     b_l, f_l, _ = model.get(dom, (0.0, 0.0, 0))
-    if f_l and f_l / max(b_l, 1.0) > FP32_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": round(d["tflops"], 3), "peak": FP32_MFMA_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(d["tflops"] / FP32_MFMA_PEAK_TFLOPS, 4)}
-    else:
-        roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
+    mfma_roof = {"bound": "mfma", "achieved": round(d.get("tflops", 0.0), 3),
+                 "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                 "frac": round(d.get("tflops", 0.0) / FP32_MFMA_PEAK_TFLOPS, 4)}
+    hbm_roof = {"bound": "hbm", "achieved": round(d["gbs"], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(d["gbs"] / HBM_PEAK_GBS, 4)}
+    # the bound is the resource whose roofline time is the longer one; a
+    # kernel that both gathers and multiplies (the fused passes) reports the
+    # other as "secondary"
+    mfma_bound = bool(f_l) and f_l / max(b_l, 1.0) > (FP32_MFMA_PEAK_TFLOPS * 1e12 /
+                                                       (HBM_PEAK_GBS * 1e9))
+    roof = dict(mfma_roof if mfma_bound else hbm_roof)
+    if f_l and b_l:
+        roof["secondary"] = hbm_roof if mfma_bound else mfma_roof
     traffic, traffic_source = measured_traffic(cfg.name, dom)
     if traffic:   # the rate at which the kernel moves L2-fabric bytes
         roof["traffic_rate_gbs"] = round(traffic / (d["avg_us"] * 1e-6) / 1e9, 1)
