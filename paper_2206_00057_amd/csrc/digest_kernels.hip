@@ -1315,15 +1315,18 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // C[r][n] = sum_k A(r)[k] B[k][n] for n < N <= 16 NB, on v_mfma_f32_16x16x4f32.
 // Row r of A is row r of A0 (r < m0) or row r - m0 of A1 (leading dim lda).
-// B is staged once per block in LDS, zero-padded to 16 NB columns, its rows
-// 16 NB + 4 floats apart so that the four k rows one MFMA step reads fall in
-// different banks.  The grid is sized to the chip and each wave takes 16-row
-// tiles in turn, so the staging is paid once per block, not per tile.  The
-// contraction order is permuted so that a lane feeds its own 16-byte load:
-// in MFMA step (j, v) lane group h = lane/16 contributes k = 16 j + 4 h + v
-// for row lane%16 (A) and column lane%16 of each column block (B), and every
-// k is covered once.  All A loads of a K chunk are issued before its MFMAs,
-// and the NB column blocks share them.
+// B is staged once per block in LDS transposed, as [n][k] for the 16 NB
+// columns (zero-padded in n and in k up to a multiple of 16), its rows
+// narrow_n_stride(K) floats apart (4 mod 16, so that the 16 rows one read
+// touches start in different bank quads).  The grid is sized to the chip and
+// each wave takes 16-row tiles in turn, so the staging is paid once per
+// block, not per tile.  The contraction order is permuted so that a lane
+// feeds its own 16-byte loads: in MFMA step (j, v) lane group h = lane/16
+// contributes k = 16 j + 4 h + v for row lane%16 (A) and column lane%16 of
+// each column block (B), and every k is covered once; a lane's four k of a
+// step are one 16-byte read of A and one of B per column block.  All A loads
+// of a K chunk are issued before its MFMAs, and the NB column blocks share
+// them.
 template <bool VEC, int NB>
 __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N,
                                                   const float *__restrict__ A0,
@@ -1334,11 +1337,11 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
 {
     constexpr int KC = 256;          // k per chunk
     constexpr int J = KC / 16;       // 16-k steps per chunk
-    constexpr int BS = 16 * NB + 4;  // LDS row stride of B
-    extern __shared__ float Bs[];    // [K][BS]
-    stage_lds(Bs, K * BS, [&](int i) {
-        const int k = i / BS, n = i % BS;
-        return n < N ? B[(int64_t)k * N + n] : 0.f;
+    const int BS = narrow_n_stride(K);   // LDS row stride of B^T
+    extern __shared__ float Bs[];    // [16 NB][BS]
+    stage_lds(Bs, 16 * NB * BS, [&](int i) {
+        const int n = i / BS, k = i % BS;
+        return n < N && k < K ? B[(int64_t)k * N + n] : 0.f;
     });
     __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
@@ -1378,18 +1381,25 @@ __global__ __launch_bounds__(256) void k_narrow_n(int32_t M, int32_t m0, int32_t
                 }
             }
 #pragma unroll
-            for (int j = 0; j < J; ++j)
+            for (int j = 0; j < J; ++j) {
+                // B^T rows 16 b + m, k = kc + 16 j + 4 h .. + 3 (zeros past K,
+                // and the chunk past the padded K reads row 0 and adds zeros)
+                const int k = kc + 16 * j + 4 * h;
+                const int kk = k < BS - 4 ? k : 0;
+                const float4 *Bs4 = reinterpret_cast<const float4 *>(Bs);   // BS % 4 == 0
+                float4 bq[NB];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int k = kc + 16 * j + 4 * h + v;
-                    const float *brow = Bs + (k < K ? k : 0) * BS + m;
+                for (int b = 0; b < NB; ++b)
+                    bq[b] = Bs4[(16 * b + m) * (BS / 4) + kk / 4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
 #pragma unroll
                     for (int b = 0; b < NB; ++b) {
-                        const float bv = k < K ? brow[16 * b] : 0.f;
+                        const float bv = k < BS - 4 ? bq[b][v] : 0.f;
                         acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j][v], bv, acc[b], 0, 0,
                                                                       0);
                     }
-                }
+            }
         }
         // lane holds C[row0 + 4h + i][16 b + m] for i < 4
 #pragma unroll
@@ -2676,7 +2686,7 @@ int64_t persistent_blocks(int64_t tiles_per_block_work, size_t lds)
 size_t narrow_n_lds(int32_t K, int32_t N)
 {
     const int nb = (N + 15) / 16;
-    return sizeof(float) * (size_t)K * (16 * nb + 4);
+    return sizeof(float) * (size_t)16 * nb * narrow_n_stride(K);
 }
 
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,

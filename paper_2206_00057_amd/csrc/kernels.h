@@ -169,6 +169,8 @@ hipError_t launch_splitk_reduce(const float *part, int32_t splits, int64_t count
 constexpr int kNarrowN = 64;
 constexpr size_t kNarrowNLds = 64 * 1024;
 size_t narrow_n_lds(int32_t K, int32_t N);
+// Row stride (floats) of B^T in LDS: K rounded up to 16, plus 4.
+constexpr int32_t narrow_n_stride(int32_t K) { return (K + 15) / 16 * 16 + 4; }
 hipError_t launch_narrow_n(int32_t M, int32_t m0, int32_t K, int32_t N, const float *A0,
                            const float *A1, int32_t lda, const float *B, float *C, int32_t ldc,
                            bool relu, hipStream_t s, int32_t lda1 = 0);
