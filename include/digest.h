@@ -423,7 +423,8 @@ const char *digest_profile_kernel_name(int32_t kind);
  *                       (forward) with G = P_m^T D over every local row
  *                       (backward); 0: (P_m [h_in; halo]) W with AH kept.
  *   forward_narrow      1: the product with W runs on the narrow-output
- *                       kernel (W held in LDS); 0: the MFMA GEMM.
+ *                       kernel (W held in LDS); 0: the MFMA GEMM, or the
+ *                       fused pass when forward_fused is 1.
  *   dw_slices           split-K slices of the weight gradient, summed in
  *                       slice order (1: no split).
  *   dgrad_narrow_first  aggregate-first layers: 1 if the input gradient is
@@ -451,8 +452,9 @@ const char *digest_profile_kernel_name(int32_t kind);
  *                       DIGEST_SPMM_TIERS forces one.
  *   tier_entries_fwd, tier_entries_bwd  entries the sliced passes take.
  *   forward_fused       aggregate-first layers with at least 16,384 owned
- *                       rows, 129 <= d_layer-1 <= 256 and the MFMA GEMM as their
- *                       product: 1 if the forward runs as one pass (kernel
+ *                       rows, 65 <= d_layer-1 <= 256 and the MFMA GEMM as
+ *                       their product: 1 if the forward runs as one pass
+ *                       (kernel
  *                       kind "spmm_gemm_fwd") in which each tile of 32 rows
  *                       is aggregated into LDS and multiplied by W there,
  *                       the tiles of other workgroups gathering meanwhile;
@@ -464,7 +466,7 @@ const char *digest_profile_kernel_name(int32_t kind);
  *                       when h_in (d_layer-1 a multiple of 4) is not
  *                       16-byte aligned.
  *   backward_fused      ReLU aggregate-first layers 2..L-1 with at least
- *                       16,384 owned rows and 129 <= d_layer <= 256, when
+ *                       16,384 owned rows and 65 <= d_layer <= 256, when
  *                       dh_in is asked for (and no halo gradient): 1 if the
  *                       input gradient runs as (P_in^T D) W^T in one pass
  *                       ("spmm_gemm_bwd"), D = dh_out masked by h_out > 0
