@@ -754,20 +754,29 @@ def test_nan_padding_never_reaches_outputs(widths):
 # capture with replays, must not change
 # ---------------------------------------------------------------------------
 
-# (widths): layer 2 aggregate-first with ReLU, the weight gradient next to
-# the transposed aggregation of D W^T (24 -> 40 -> 48 -> 7), and an identity
-# layer aggregated at its narrower output width first (24 -> 40 -> 36)
-SIDE = [(24, 40, 48, 7), (24, 40, 36)]
+# (widths, fuse): layer 2 aggregate-first with ReLU, the weight gradient next
+# to the transposed aggregation of D W^T (24 -> 40 -> 48 -> 7); an identity
+# layer aggregated at its narrower output width first (24 -> 40 -> 36); and
+# the fused passes forced (a ReLU layer of 96 floats fused in both
+# directions, 100 -> 96 -> 96 -> 7), so that the weight gradient's fork sits
+# after the formed D and beside the fused input gradient
+SIDE = [((24, 40, 48, 7), "0"), ((24, 40, 36), "0"), ((100, 96, 96, 7), "2")]
 
 
-@pytest.mark.parametrize("widths", SIDE, ids=lambda w: "x".join(map(str, w)))
-def test_side_stream_backward(widths, monkeypatch):
+@pytest.mark.parametrize("widths,fuse", SIDE,
+                         ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else v)
+def test_side_stream_backward(widths, fuse, monkeypatch):
     from paper_2206_00057_amd import step
     monkeypatch.setenv("DIGEST_SIDE_STREAM", "2")
+    monkeypatch.setenv("DIGEST_FUSE", fuse)
     cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
     g = synth.make_graph(cfg, seed=4)
     part = synth.make_partition(cfg, g, 2)
     c = Case(cfg, g, part, label=f"side{widths}")
+    if fuse == "2":
+        Dm = D()
+        assert Dm.digest_partition_plan(c.h, 2)["forward_fused"] == 1
+        assert Dm.digest_partition_plan(c.h, 2)["backward_fused"] == 1
     for layer in range(1, c.L + 1):
         check_layer(c, layer)
     # rounds: eager, then captured and replayed (bit for bit)
