@@ -65,6 +65,8 @@ enum Kind : int32_t {
     K_SPMM_GEMM_BWD,
     K_RELU_MASK,
     K_TRANSPOSE_W,
+    K_HALO_AGG,
+    K_BND_ROWS,
     K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
@@ -73,7 +75,8 @@ const char *const kKindNames[K_COUNT] = {
     "halo_gradient", "grad_push_add", "grad_pull_add", "gat_transform", "gat_scores",
     "gat_softmax", "gat_aggregate", "gat_edge_grad", "gat_transpose_edges",
     "gat_aggregate_transposed", "gat_score_grad", "gat_score_sums", "gat_datt", "gat_dw",
-    "gat_dgrad", "pad_rows", "spmm_gemm_fwd", "spmm_gemm_bwd", "relu_mask", "transpose_w"};
+    "gat_dgrad", "pad_rows", "spmm_gemm_fwd", "spmm_gemm_bwd", "relu_mask", "transpose_w",
+    "halo_aggregate", "boundary_rows"};
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kMaxWidth = 65536;
@@ -380,7 +383,19 @@ struct digest_partition {
     // (P_out^T, numbered from 0).
     std::vector<SpmmBlock> blocks_f, blocks_t, blocks_tf, blocks_th;
     int32_t long_f = 0, long_t = 0, long_tf = 0, long_th = 0;   // leading long-row blocks
-    // P_m split at kFuseLong entries per row: the long rows (their count and
+    // The GCN forward's operands.  Between two pulls of a level its halo rows
+    // are constants, and so is their share of every owned row's aggregate,
+    // P_out halo.  P_b holds the halo entries of the boundary rows (n_bnd
+    // rows; columns are halo slots), which a pull multiplies into the halo
+    // aggregate S = P_b halo ([n_bnd] rows).  P_s = [P_in | E] holds each
+    // owned row's owned-column entries, then, for boundary row b, one entry
+    // of 1 in column n_own + b, which reads S's row b: P_s [h; S] = P_m [h; halo].
+    int64_t nnz_s = 0, nnz_b = 0;
+    std::vector<int32_t> s_rowptr, s_col, b_rowptr, b_col;
+    std::vector<float> s_val, b_val;
+    std::vector<SpmmBlock> blocks_s, blocks_b;
+    int32_t long_s = 0, long_b = 0;
+    // P_s split at kFuseLong entries per row: the long rows (their count and
     // entries) and the distinct source rows the short and the long rows read
     int64_t long_rows_f = 0, long_nnz_f = 0, src_short_f = 0, src_long_f = 0;
     // the fused forward's row order: tile t's rows t kFuseRows + fuse_order[..]
@@ -398,10 +413,12 @@ struct digest_partition {
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
+        size_t s_rowptr, s_col, s_val, b_rowptr, b_col, b_val, blocks_s, blocks_b;
         size_t fuse_order, fuse_order_t;   // per owned row, uint8 (see fuse_order below)
         size_t fz;                      // the fused input gradient's D and long rows
         size_t wt;                      // W^T of the fused input gradient
         std::vector<size_t> halo_buf;   // per level 0..L-1, rows padded_width(d_level) apart
+        std::vector<size_t> hagg;       // per level 0..L-1: S, n_bnd rows padded like halo_buf
         std::vector<size_t> ah;         // per layer 1..L (index 0 unused), padded rows
         size_t tmp, tmp_halo, tbuf, gemm_part, loss_part;
         size_t hpad;                    // a padded copy of h_in for widths not a multiple of 4
@@ -515,27 +532,28 @@ void narrow_rows_plan(int64_t R, int64_t F, int32_t &chunk, int32_t &slices)
 }
 
 // Split-K slices of the transform-first weight gradient H_mix^T G over the
-// n_own + n_halo rows.  Narrow outputs (<= kNarrow) use the MFMA kernel with
-// `chunk` rows per slice; wider ones use the MFMA GEMM twice (owned rows,
-// then halo rows) with their own split plans.
+// n_own owned rows and n_halo rows of a second block (the halo rows, or the
+// halo aggregate's boundary rows).  Narrow outputs (<= kNarrow) use the MFMA
+// kernel with `chunk` rows per slice; wider ones use the MFMA GEMM twice
+// (owned rows, then the second block) with their own split plans.
 struct TfPlan {
     bool valu;
     int32_t chunk, slices;           // VALU: rows per slice, number of slices
-    int32_t s_own, k_own, s_halo, k_halo;   // MFMA: splits and chunks
+    int32_t s_own, k_own, s_halo, k_halo;   // MFMA: splits and chunks (owned, second block)
 };
 
-TfPlan tf_plan(int64_t n_own, int64_t n_halo, int64_t d_in, int64_t d_out)
+TfPlan tf_plan(int64_t n_own, int64_t n2, int64_t d_in, int64_t d_out)
 {
     TfPlan t{};
-    const int64_t R = n_own + n_halo;
+    const int64_t R = n_own + n2;
     t.valu = d_out <= digest::kNarrow;
     if (t.valu) {
         narrow_rows_plan(R, d_in, t.chunk, t.slices);
     } else {
         splitk_plan(d_in, d_out, n_own, t.s_own, t.k_own);
-        if (n_halo > 0)
-            splitk_plan(d_in, d_out, n_halo, t.s_halo, t.k_halo);
-        t.slices = t.s_own + (n_halo > 0 ? t.s_halo : 0);
+        if (n2 > 0)
+            splitk_plan(d_in, d_out, n2, t.s_halo, t.k_halo);
+        t.slices = t.s_own + (n2 > 0 ? t.s_halo : 0);
     }
     return t;
 }
@@ -565,9 +583,20 @@ void plan_layout(digest_partition &p)
     l.blocks_t = take(sizeof(SpmmBlock) * p.blocks_t.size());
     l.blocks_tf = take(sizeof(SpmmBlock) * p.blocks_tf.size());
     l.blocks_th = take(sizeof(SpmmBlock) * p.blocks_th.size());
+    l.s_rowptr = take(sizeof(int32_t) * p.s_rowptr.size());
+    l.s_col = take(sizeof(int32_t) * p.s_col.size());
+    l.s_val = take(sizeof(float) * p.s_val.size());
+    l.b_rowptr = take(sizeof(int32_t) * p.b_rowptr.size());
+    l.b_col = take(sizeof(int32_t) * p.b_col.size());
+    l.b_val = take(sizeof(float) * p.b_val.size());
+    l.blocks_s = take(sizeof(SpmmBlock) * p.blocks_s.size());
+    l.blocks_b = take(sizeof(SpmmBlock) * p.blocks_b.size());
     l.halo_buf.assign(p.L, 0);
-    for (int32_t lev = 0; lev < p.L; ++lev)
+    l.hagg.assign(p.L, 0);
+    for (int32_t lev = 0; lev < p.L; ++lev) {
         l.halo_buf[lev] = take(sizeof(float) * (size_t)p.n_halo * padded_width(p.widths[lev]));
+        l.hagg[lev] = take(sizeof(float) * (size_t)p.n_bnd * padded_width(p.widths[lev]));
+    }
     l.ah.assign(p.L + 1, 0);
     int64_t hpad = 0;   // padded copies of h_in (odd d_in) or dh_out (odd d_out)
     for (int32_t k = 1; k <= p.L; ++k) {
@@ -586,9 +615,13 @@ void plan_layout(digest_partition &p)
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
         if (transform_first_cheaper(p, k)) {
-            tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + p.n_halo) * padded_width(dout));
-            const TfPlan t = tf_plan(p.n_own, p.n_halo, di, dout);
-            gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
+            // the second block of rows is the halo (with the halo gradient)
+            // or the halo aggregate's boundary rows
+            for (const int64_t n2 : {(int64_t)p.n_halo, (int64_t)p.n_bnd}) {
+                tbuf = std::max<int64_t>(tbuf, ((int64_t)p.n_own + n2) * padded_width(dout));
+                const TfPlan t = tf_plan(p.n_own, n2, di, dout);
+                gemm_part = std::max<int64_t>(gemm_part, (int64_t)t.slices * di * dout);
+            }
         }
     }
     // the fused input gradient's D and long rows (two n_own x padded rows)
@@ -776,13 +809,14 @@ digest_status need_bound(const digest_partition *p)
 }
 
 // Sparse aggregation over the local CSR (P_m), the CSR of P_in^T (the first
-// n_own rows of the transpose), of P_m^T (all of it) or of P_out^T (its
-// n_halo halo rows, numbered from 0).  `val` replaces the matrix's values
-// (edge weights in the same entry order); relu stores max(x, 0).
-enum class Csr { Fwd, InT, FullT, HaloT };
+// n_own rows of the transpose), of P_m^T (all of it), of P_out^T (its
+// n_halo halo rows, numbered from 0) or of P_s (owned columns, then the
+// halo aggregate's).  `val` replaces the matrix's values (edge weights in
+// the same entry order); relu stores max(x, 0).
+enum class Csr { Fwd, InT, FullT, HaloT, InH };
 
 // Tiered plans for the aggregations a standard round runs at widths where
-// slicing applies: the forward's P_m at d_in of every aggregate-first layer
+// slicing applies: the forward's P_s at d_in of every aggregate-first layer
 // and the backward's P_in^T at its width for layers >= 2 (the layer plan's
 // orders, ReLU below the last layer).  Operands or widths that gain nothing
 // get no plan and run as one pass.
@@ -795,9 +829,9 @@ void plan_tiers(digest_partition &p)
             if (tw.first == (int32_t)which && tw.second == w)
                 return;
         tried.push_back({(int32_t)which, w});
-        TierPlan t = which == Csr::Fwd
-                         ? plan_one_tier((int32_t)which, p.rowptr, p.col, p.val, p.n_own,
-                                         (int64_t)p.n_own + p.n_halo, w)
+        TierPlan t = which == Csr::InH
+                         ? plan_one_tier((int32_t)which, p.s_rowptr, p.s_col, p.s_val, p.n_own,
+                                         (int64_t)p.n_own + p.n_bnd, w)
                          : plan_one_tier((int32_t)which, p.t_rowptr, p.t_src, p.t_val, p.n_own,
                                          p.n_own, w);
         if (t.tiers > 0)
@@ -808,7 +842,7 @@ void plan_tiers(digest_partition &p)
         const bool relu = l < p.L;
         if (!relu && p.n_own > 0 && transform_first_cheaper(p, l))
             continue;
-        want(Csr::Fwd, padded_width(d_in));
+        want(Csr::InH, padded_width(d_in));
         if (l > 1)
             want(Csr::InT, (!relu && d_out < d_in) ? d_out : d_in);
     }
@@ -853,7 +887,7 @@ bool fuse_forward(const digest_partition &p, int32_t layer, bool transform_first
         d_in < digest::kFuseMinWidth || d_in > digest::kFuseMaxWidth ||
         (mode == 1 && p.n_own < kFuseMinRows))
         return false;
-    return find_tiers(p, Csr::Fwd, padded_width(d_in)) == nullptr;
+    return find_tiers(p, Csr::InH, padded_width(d_in)) == nullptr;
 }
 
 digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const float *src1,
@@ -868,17 +902,24 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     const std::vector<SpmmBlock> *blocks = &p->blocks_f;
     size_t boff = p->lay.blocks_f;
     int32_t n_long = p->long_f;
-    if (which == Csr::InT) {
+    size_t o_rowptr = fwd ? p->lay.rowptr : p->lay.t_rowptr;
+    size_t o_col = fwd ? p->lay.col : p->lay.t_src;
+    size_t o_val = fwd ? p->lay.val : p->lay.t_val;
+    if (which == Csr::InH) {
+        blocks = &p->blocks_s, boff = p->lay.blocks_s, n_long = p->long_s;
+        o_rowptr = p->lay.s_rowptr, o_col = p->lay.s_col, o_val = p->lay.s_val;
+    } else if (which == Csr::InT) {
         blocks = &p->blocks_t, boff = p->lay.blocks_t, n_long = p->long_t;
     } else if (which == Csr::FullT) {
         blocks = &p->blocks_tf, boff = p->lay.blocks_tf, n_long = p->long_tf;
     } else if (which == Csr::HaloT) {
         blocks = &p->blocks_th, boff = p->lay.blocks_th, n_long = p->long_th;
     }
-    const int32_t *rowptr = p->at<int32_t>(fwd ? p->lay.rowptr : p->lay.t_rowptr);
+    const int32_t *rowptr = p->at<int32_t>(o_rowptr);
     if (which == Csr::HaloT)
         rowptr += p->n_own;
-    Timed t(p, kind >= 0 ? kind : (fwd ? K_SPMM_FWD : K_SPMM_BWD), layer, s);
+    Timed t(p, kind >= 0 ? kind : (fwd || which == Csr::InH ? K_SPMM_FWD : K_SPMM_BWD), layer,
+            s);
     const TierPlan *tp = find_tiers(*p, which, d);
     if (tp && !ep && !val && !relu && !(r1 && r1->a) && n_out0 == INT32_MAX && !out1 &&
         (lds == 0 || lds == d) && (out_ld == 0 || out_ld == d) && (out_w == 0 || out_w == d) &&
@@ -907,24 +948,44 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     }
     return hip_check(
         digest::launch_spmm(p->at<SpmmBlock>(boff), (int32_t)blocks->size(), n_long, rowptr,
-                            p->at<int32_t>(fwd ? p->lay.col : p->lay.t_src),
-                            val ? val : p->at<float>(fwd ? p->lay.val : p->lay.t_val), src0, src1,
+                            p->at<int32_t>(o_col), val ? val : p->at<float>(o_val), src0, src1,
                             n_src0, d, out, s, ep, out1, n_out0, relu, r1, false, lds, out_ld,
                             out_w),
         "spmm");
 }
 
-// T = [h_own; halo] W over the n_own + n_halo local rows (T row-major
-// [n_own + n_halo][d_out]): the narrow-output kernel with W in LDS when the
-// widths allow, else the MFMA GEMM for the owned and for the halo rows.
+// S = P_b halo_buf[level]: the halo aggregate of level `level` (the halo
+// rows' share of each boundary row's aggregate in the forward of layer
+// level + 1), rows padded like the halo buffer.
+digest_status halo_aggregate(digest_partition *p, int32_t level, hipStream_t s)
+{
+    if (p->n_bnd == 0)
+        return DIGEST_OK;
+    const int32_t lw = padded_width(p->widths[level]);
+    Timed t(p, K_HALO_AGG, level, s);
+    return hip_check(digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_b),
+                                         (int32_t)p->blocks_b.size(), p->long_b,
+                                         p->at<int32_t>(p->lay.b_rowptr),
+                                         p->at<int32_t>(p->lay.b_col),
+                                         p->at<float>(p->lay.b_val),
+                                         p->at<float>(p->lay.halo_buf[level]), nullptr,
+                                         p->n_halo, lw, p->at<float>(p->lay.hagg[level]), s),
+                     "halo aggregate");
+}
+
+// T = [h_own; h2] W over the n_own owned rows and the n2 rows of a second
+// block h2 (the halo rows, or the halo aggregate's boundary rows; rows
+// padded_width(d_in) apart), T row-major [n_own + n2][ldt]: the
+// narrow-output kernel with W in LDS when the widths allow, else the MFMA
+// GEMM for the owned and for the second block's rows.
 digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_own,
-                             const float *halo, const float *w, float *T, int32_t ldt,
+                             const float *h2, int32_t n2, const float *w, float *T, int32_t ldt,
                              hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     if (narrow_out(d_in, d_out))
-        return hip_check(digest::launch_narrow_n(p->n_own + p->n_halo, p->n_own, d_in, d_out,
-                                                 h_own, halo, d_in, w, T, ldt, false, s,
+        return hip_check(digest::launch_narrow_n(p->n_own + n2, p->n_own, d_in, d_out, h_own,
+                                                 h2, d_in, w, T, ldt, false, s,
                                                  padded_width(d_in)),
                          "transform");
     digest::GemmArgs g{};
@@ -944,10 +1005,10 @@ digest_status transform_rows(digest_partition *p, int32_t layer, const float *h_
         if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
             return st;
     }
-    if (p->n_halo > 0) {
-        g.M = p->n_halo;
+    if (n2 > 0) {
+        g.M = n2;
         g.tile = gemm_tile_for(g.M, d_out, d_in, false);
-        g.A = halo;
+        g.A = h2;
         g.lda = padded_width(d_in);
         g.C = T + (int64_t)p->n_own * ldt;
         if (digest_status st = hip_check(digest::launch_gemm(g, s), "transform"))
@@ -1081,8 +1142,38 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
                 ++next[c];
             }
 
+        // P_s and P_b (entries in P_m's order within each row)
+        p->nnz_b = nnz - p->nnz_in;
+        p->nnz_s = p->nnz_in + p->n_bnd;
+        p->s_rowptr.assign(n_owned + 1, 0);
+        p->s_col.reserve(p->nnz_s);
+        p->s_val.reserve(p->nnz_s);
+        p->b_rowptr.assign(p->n_bnd + 1, 0);
+        p->b_col.reserve(p->nnz_b);
+        p->b_val.reserve(p->nnz_b);
+        for (int32_t i = 0, b = 0; i < (int32_t)n_owned; ++i) {
+            for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k)
+                if (p->col[k] < n_owned) {
+                    p->s_col.push_back(p->col[k]);
+                    p->s_val.push_back(p->val[k]);
+                }
+            if (b < p->n_bnd && p->bnd_local[b] == i) {
+                for (int32_t k = p->rowptr[i]; k < p->rowptr[i + 1]; ++k)
+                    if (p->col[k] >= n_owned) {
+                        p->b_col.push_back(p->col[k] - (int32_t)n_owned);
+                        p->b_val.push_back(p->val[k]);
+                    }
+                p->b_rowptr[b + 1] = (int32_t)p->b_col.size();
+                p->s_col.push_back((int32_t)n_owned + b);
+                p->s_val.push_back(1.0f);
+                ++b;
+            }
+            p->s_rowptr[i + 1] = (int32_t)p->s_col.size();
+        }
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
-        fuse_stats(p->rowptr, p->col, (int32_t)n_owned, p->n_own + p->n_halo, p->long_rows_f,
+        p->long_s = build_blocks(p->s_rowptr, p->n_own, p->blocks_s);
+        p->long_b = build_blocks(p->b_rowptr, p->n_bnd, p->blocks_b);
+        fuse_stats(p->s_rowptr, p->s_col, (int32_t)n_owned, p->n_own + p->n_bnd, p->long_rows_f,
                    p->long_nnz_f, p->src_short_f, p->src_long_f, p->fuse_order);
         p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
         fuse_stats(p->t_rowptr, p->t_src, (int32_t)n_owned, p->n_own, p->long_rows_t,
@@ -1183,6 +1274,14 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.blocks_t, p->blocks_t.data(), sizeof(SpmmBlock) * p->blocks_t.size()},
         {l.blocks_tf, p->blocks_tf.data(), sizeof(SpmmBlock) * p->blocks_tf.size()},
         {l.blocks_th, p->blocks_th.data(), sizeof(SpmmBlock) * p->blocks_th.size()},
+        {l.s_rowptr, p->s_rowptr.data(), sizeof(int32_t) * p->s_rowptr.size()},
+        {l.s_col, p->s_col.data(), sizeof(int32_t) * p->s_col.size()},
+        {l.s_val, p->s_val.data(), sizeof(float) * p->s_val.size()},
+        {l.b_rowptr, p->b_rowptr.data(), sizeof(int32_t) * p->b_rowptr.size()},
+        {l.b_col, p->b_col.data(), sizeof(int32_t) * p->b_col.size()},
+        {l.b_val, p->b_val.data(), sizeof(float) * p->b_val.size()},
+        {l.blocks_s, p->blocks_s.data(), sizeof(SpmmBlock) * p->blocks_s.size()},
+        {l.blocks_b, p->blocks_b.data(), sizeof(SpmmBlock) * p->blocks_b.size()},
     };
     for (const Up &u : ups) {
         if (!u.bytes)
@@ -1285,6 +1384,11 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
             "pull");
         if (st)
             return st;
+        // the halo aggregate for the next layer's GCN forward (a partition
+        // with a GAT workspace forms it in each GCN forward instead)
+        if (!p->gws)
+            if (digest_status st2 = halo_aggregate(p, level, s))
+                return st2;
     }
     p->pulled[level] = 1;
     p->pull_gen[level] += 1;
@@ -1330,27 +1434,34 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         return fail(DIGEST_ESTATE, "level %d was never pulled", layer - 1);
     hipStream_t s = (hipStream_t)hip_stream;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    // The halo rows enter through their aggregate S = P_out halo (n_bnd rows),
+    // formed by the pull of level layer-1, or here when a GAT workspace is
+    // bound (its pulls skip it).
+    const float *hs = p->n_bnd > 0 ? p->at<float>(p->lay.hagg[layer - 1]) : nullptr;
+    if (p->gws && p->n_own > 0)
+        if (digest_status st = halo_aggregate(p, layer - 1, s))
+            return st;
     const bool tf = act == DIGEST_ACT_IDENTITY && transform_first_cheaper(*p, layer);
     if (p->n_own > 0 && tf) {
-        // T = [h_in; halo] W over all local rows, then h_out = P_m T.
-        // T's rows are padded to a multiple of 4 floats so that the
-        // aggregation gathers whole float4 vectors; it stores d_out columns
+        // T = [h_in; S] W over the owned and the boundary rows, then
+        // h_out = P_s T.  T's rows are padded to a multiple of 4 floats so
+        // that the aggregation gathers whole float4 vectors; it stores d_out
+        // columns
         float *T = p->at<float>(p->lay.tbuf);
         const int32_t ldt = padded_width(d_out);
         {
             Timed t(p, K_GEMM_FWD, layer, s);
-            if (digest_status st = transform_rows(p, layer, h_in, halo, w, T, ldt, s))
+            if (digest_status st = transform_rows(p, layer, h_in, hs, p->n_bnd, w, T, ldt, s))
                 return st;
         }
-        if (digest_status st = run_spmm(p, Csr::Fwd, T, nullptr, p->n_own + p->n_halo, ldt,
+        if (digest_status st = run_spmm(p, Csr::InH, T, nullptr, p->n_own + p->n_bnd, ldt,
                                         h_out, layer, s, nullptr, -1, nullptr, INT32_MAX,
                                         nullptr, false, nullptr, ldt, d_out, d_out))
             return st;
     } else if (p->n_own > 0) {
-        // AH = P_in h_in + P_out halo (kept for the backward), then act(AH W).
-        // Rows whose width is not a multiple of 4 floats are gathered from
-        // padded copies (the halo buffer is padded, h_in is copied), so that
+        // AH = P_s [h_in; S] = P_in h_in + P_out halo (kept for the backward),
+        // then act(AH W).  Rows whose width is not a multiple of 4 floats are
+        // gathered from padded copies (S is padded, h_in is copied), so that
         // the aggregation loads whole float4 vectors; AH keeps the padding.
         float *ah = p->at<float>(p->lay.ah[layer]);
         const int32_t lh = padded_width(d_in);
@@ -1365,17 +1476,17 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             src0 = hp;
         }
         if (fuse_forward(*p, layer, tf) &&
-            digest::spmm_gemm_ok(d_in, lh, lh, src0, halo, ah, ah)) {
+            digest::spmm_gemm_ok(d_in, lh, lh, src0, hs, ah, ah)) {
             // the long rows through the ordinary kernel's long-row blocks,
             // then every row tile aggregated and multiplied by W in one pass
-            const int32_t *rowptr = p->at<int32_t>(p->lay.rowptr);
-            const int32_t *col = p->at<int32_t>(p->lay.col);
-            const float *val = p->at<float>(p->lay.val);
-            if (p->long_f > 0) {
+            const int32_t *rowptr = p->at<int32_t>(p->lay.s_rowptr);
+            const int32_t *col = p->at<int32_t>(p->lay.s_col);
+            const float *val = p->at<float>(p->lay.s_val);
+            if (p->long_s > 0) {
                 Timed t(p, K_SPMM_FWD, layer, s);
                 if (digest_status st = hip_check(
-                        digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_f), p->long_f,
-                                            p->long_f, rowptr, col, val, src0, halo, p->n_own,
+                        digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_s), p->long_s,
+                                            p->long_s, rowptr, col, val, src0, hs, p->n_own,
                                             lh, ah, s),
                         "spmm long rows"))
                     return st;
@@ -1383,7 +1494,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             Timed t(p, K_SPMM_GEMM_FWD, layer, s);
             if (digest_status st = hip_check(
                     digest::launch_spmm_gemm(p->n_own, rowptr, col, val,
-                                             p->at<uint8_t>(p->lay.fuse_order), src0, halo,
+                                             p->at<uint8_t>(p->lay.fuse_order), src0, hs,
                                              p->n_own, lh, d_in, ah, ah, lh, w, d_out, h_out,
                                              d_out, act == DIGEST_ACT_RELU, s),
                     "fused forward"))
@@ -1394,7 +1505,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
             p->fwd_gen[layer] = p->pull_gen[layer - 1];
             return DIGEST_OK;
         }
-        if (digest_status st = run_spmm(p, Csr::Fwd, src0, halo, p->n_own, lh, ah, layer, s))
+        if (digest_status st = run_spmm(p, Csr::InH, src0, hs, p->n_own, lh, ah, layer, s))
             return st;
         Timed t(p, K_GEMM_FWD, layer, s);
         if (narrow_out(d_in, d_out)) {
@@ -1460,23 +1571,25 @@ digest_status times_wt(int32_t rows, int32_t d_in, int32_t d_out, const float *A
     return hip_check(digest::launch_gemm(h, s), "times W^T");
 }
 
-// dw = [h_own; halo]^T G over the n_own + n_halo local rows (G row-major
-// [n_own + n_halo][d_out], leading dim ldg): split-K slices in `part`,
-// summed in slice order.
+// dw = [h_own; h2]^T G over the n_own owned rows and the n2 rows of a
+// second block h2 (the halo rows, or the halo aggregate's boundary rows;
+// rows padded_width(d_in) apart), G row-major [n_own + n2][ldg]: split-K
+// slices in `part`, summed in slice order.
 // Outputs up to kNarrow wide use the narrow MFMA kernel, wider ones the
-// GEMM over the owned rows and over the halo rows.
+// GEMM over the owned rows and over the second block's rows.
 digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *h_in,
-                               const float *halo, const float *G, int32_t ldg, float *gpart,
-                               float *dw, hipStream_t s, int32_t kind_dw, int32_t kind_reduce)
+                               const float *h2, int32_t n2, const float *G, int32_t ldg,
+                               float *gpart, float *dw, hipStream_t s, int32_t kind_dw,
+                               int32_t kind_reduce)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    const TfPlan t = tf_plan(p->n_own, p->n_halo, d_in, d_out);
+    const TfPlan t = tf_plan(p->n_own, n2, d_in, d_out);
     {
         Timed tm(p, kind_dw, layer, s);
         if (t.valu) {
             if (digest_status st = hip_check(
-                    digest::launch_dw_narrow(p->n_own + p->n_halo, p->n_own, d_in, d_out, h_in,
-                                             halo, d_in, G, ldg, t.chunk, t.slices, gpart, s,
+                    digest::launch_dw_narrow(p->n_own + n2, p->n_own, d_in, d_out, h_in, h2,
+                                             d_in, G, ldg, t.chunk, t.slices, gpart, s,
                                              padded_width(d_in)),
                     "dW narrow"))
                 return st;
@@ -1497,9 +1610,9 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
             g.C = gpart;
             if (digest_status st = hip_check(digest::launch_gemm(g, s), "dW gemm"))
                 return st;
-            if (p->n_halo > 0) {
-                g.K = p->n_halo;
-                g.A = halo;
+            if (n2 > 0) {
+                g.K = n2;
+                g.A = h2;
                 g.lda = padded_width(d_in);
                 g.B = G + (int64_t)p->n_own * ldg;
                 g.splits = t.s_halo;
@@ -1521,22 +1634,29 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
     return DIGEST_OK;
 }
 
-// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer, with
-// G = P_m^T D over all local rows.  The halo rows of G feed dW and, when
-// dh_halo is given, the halo gradient G_halo W^T.
+// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer.  With
+// dh_halo, G = P_m^T D over all local rows and H_mix = [h_in; halo]: the
+// halo rows of G feed dW and the halo gradient G_halo W^T.  Without it,
+// G = P_s^T D and H_mix = [h_in; S], the same dW from the owned and the
+// boundary rows: G_own = P_in^T D, and the boundary rows of G are D's rows
+// of the boundary nodes (P_s's halo-aggregate entries are ones).
 digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
                                        const float *dh_out, const float *w, float *dw,
                                        float *dh_in, float *dh_halo, hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
+    const bool via_s = !dh_halo;
+    const float *h2 = via_s ? (p->n_bnd > 0 ? p->at<float>(p->lay.hagg[layer - 1]) : nullptr)
+                            : (p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr);
+    const int32_t n2 = via_s ? p->n_bnd : p->n_halo;
     // G's rows are padded like T's, so that the products that read it load
     // whole vectors
     float *G = p->at<float>(p->lay.tbuf);
     const int32_t ldg = padded_width(d_out);
     float *gpart = p->at<float>(p->lay.gemm_part);
-    // G = P_m^T dh_out over owned and halo rows; when the widths allow, the
-    // same launch also writes dh_in = G_own W^T for the owned rows.
+    // G = P_m^T dh_out over owned and halo rows, or P_in^T dh_out over the
+    // owned rows; when the widths allow, the same launch also writes
+    // dh_in = G_own W^T for the owned rows.
     const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
                           digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
                           (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
@@ -1557,14 +1677,22 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
         src = dp;
         dg = ldg;
     }
-    if (digest_status st = run_spmm(p, Csr::FullT, src, nullptr, p->n_own, dg, G, layer, s,
-                                    fused_dh ? &ep : nullptr, -1, nullptr, INT32_MAX, nullptr,
-                                    false, nullptr, dg, ldg, dg))
+    if (digest_status st = run_spmm(p, via_s ? Csr::InT : Csr::FullT, src, nullptr, p->n_own,
+                                    dg, G, layer, s, fused_dh ? &ep : nullptr, -1, nullptr,
+                                    INT32_MAX, nullptr, false, nullptr, dg, ldg, dg))
         return st;
+    if (via_s && p->n_bnd > 0) {
+        Timed t(p, K_BND_ROWS, layer, s);
+        if (digest_status st = hip_check(
+                digest::launch_copy_rows(p->at<int32_t>(p->lay.bnd_local), nullptr, p->n_bnd, dg,
+                                         src, G + (int64_t)p->n_own * ldg, s, dg, ldg),
+                "boundary rows"))
+            return st;
+    }
     // (everything after G is a product bound by the MFMA units, so the
     // weight gradient stays on s: two such products side by side only
     // share the units)
-    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, G, ldg, gpart, dw, s,
+    if (digest_status st = weight_grad_rows(p, layer, h_in, h2, n2, G, ldg, gpart, dw, s,
                                             K_GEMM_DW, K_REDUCE_DW))
         return st;
     if (fused_dh)
@@ -2057,7 +2185,8 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
     float *alpha = p->gat<float>(p->glay.alpha[layer]);
     {
         Timed t(p, K_GAT_TRANSFORM, layer, s);
-        if (digest_status st = transform_rows(p, layer, h_in, halo, w, Z, p->widths[layer], s))
+        if (digest_status st = transform_rows(p, layer, h_in, halo, p->n_halo, w, Z,
+                                              p->widths[layer], s))
             return st;
     }
     {
@@ -2186,8 +2315,8 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
                 "GAT datt reduce"))
             return st;
     }
-    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, dz, d_out, part, dw, s, K_GAT_DW,
-                                            K_REDUCE_DW))
+    if (digest_status st = weight_grad_rows(p, layer, h_in, halo, p->n_halo, dz, d_out, part, dw,
+                                            s, K_GAT_DW, K_REDUCE_DW))
         return st;
     if (!dh_in || p->n_own == 0)
         return DIGEST_OK;
@@ -2263,7 +2392,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
     pl.forward_fused = fuse_forward(p, layer, pl.transform_first);
     pl.backward_fused = fuse_backward(p, layer, pl.transform_first);
     if (pl.transform_first) {
-        pl.dw_slices = tf_plan(p.n_own, p.n_halo, d_in, d_out).slices;
+        pl.dw_slices = tf_plan(p.n_own, p.n_bnd, d_in, d_out).slices;
         pl.dgrad_fused = layer > 1 && narrow_valu(d_in, d_out) &&
                          digest::spmm_epilogue_ok(d_out, d_in, nullptr);
     } else {
@@ -2271,7 +2400,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
         splitk_plan(d_in, d_out, p.n_own, splits, kchunk);
         pl.dw_slices = splits;
         pl.dgrad_narrow_first = !relu && d_out < d_in;
-        if (const TierPlan *t = find_tiers(p, Csr::Fwd, padded_width(d_in))) {
+        if (const TierPlan *t = find_tiers(p, Csr::InH, padded_width(d_in))) {
             pl.tiers_fwd = t->tiers;
             pl.tier_rows_fwd = t->rows_per_tier;
             pl.tier_entries_fwd = t->tier_entries;
@@ -2320,8 +2449,8 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
         flops[kind * slots + slot] = f;
         entries[kind * slots + slot] = e;
     };
-    const double n = p->n_own, nh = p->n_halo, nb = p->n_bnd, R = n + nh;
-    const double nnz = (double)p->nnz, nnz_in = (double)p->nnz_in;
+    const double n = p->n_own, nh = p->n_halo, nb = p->n_bnd, R = n + nh, Rs = n + nb;
+    const double nnz = (double)p->nnz, nnz_in = (double)p->nnz_in, nnz_s = (double)p->nnz_s;
     const int32_t L = p->L;
     for (int32_t l = 1; l <= L; ++l) {
         const double di = p->widths[l - 1], dout = p->widths[l];
@@ -2350,15 +2479,19 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
         }
         const digest_layer_plan pl = layer_plan(*p, l);
         if (pl.transform_first) {
-            put(K_GEMM_FWD, l, 4 * (R * di + di * dout + R * dout), 2 * R * di * dout);
-            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * dout + 4 * n * dout, 0.0, p->nnz);
+            // over the owned rows and the halo aggregate's boundary rows
+            put(K_GEMM_FWD, l, 4 * (Rs * di + di * dout + Rs * dout), 2 * Rs * di * dout);
+            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz_s + 4 * Rs * dout + 4 * n * dout, 0.0,
+                p->nnz_s);
             put(K_SPMM_BWD, l,
-                4 * (R + 1) + 8 * nnz + 4 * n * dout + 4 * R * dout +
+                4 * (n + 1) + 8 * nnz_in + 8 * n * dout +
                     (pl.dgrad_fused ? 4 * (n * di + di * dout) : 0.0),
-                0.0, p->nnz);
+                0.0, p->nnz_in);
+            if (p->n_bnd > 0)
+                put(K_BND_ROWS, l, 8 * nb * dout + 4 * nb);
             if (!pl.dgrad_fused && p->widths[l] % 4)   // the padded copy of dh_out
                 put(K_PAD_ROWS, l, 4 * n * (dout + padded_width(p->widths[l])));
-            put(K_GEMM_DW, l, 4 * (R * di + R * dout + di * dout), 2 * R * di * dout);
+            put(K_GEMM_DW, l, 4 * (Rs * di + Rs * dout + di * dout), 2 * Rs * di * dout);
             put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);
             if (l > 1 && !pl.dgrad_fused)
                 put(K_GEMM_DH, l, 4 * (n * dout + di * dout + n * di), 2 * n * di * dout);
@@ -2373,11 +2506,12 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
                 put(K_SPMM_FWD, l, 4 * 2 * nl + 8 * el + 4 * p->src_long_f * di + 4 * nl * di,
                     0.0, p->long_nnz_f);
             put(K_SPMM_GEMM_FWD, l,
-                4 * (n + 1) + 8 * (nnz - el) + 4 * p->src_short_f * di + 4 * nl * di +
+                4 * (n + 1) + 8 * (nnz_s - el) + 4 * p->src_short_f * di + 4 * nl * di +
                     4 * (n - nl) * di + 4 * di * dout + 4 * n * dout,
-                2 * n * di * dout, p->nnz - p->long_nnz_f);
+                2 * n * di * dout, p->nnz_s - p->long_nnz_f);
         } else {
-            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz + 4 * R * di + 4 * n * di, 0.0, p->nnz);
+            put(K_SPMM_FWD, l, 4 * (n + 1) + 8 * nnz_s + 4 * Rs * di + 4 * n * di, 0.0,
+                p->nnz_s);
             put(K_GEMM_FWD, l, 4 * (n * di + di * dout + n * dout), 2 * n * di * dout);
         }
         if (p->widths[l - 1] % 4)   // the padded copy of h_in
@@ -2411,8 +2545,15 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
     const double C = p->widths[L];
     put(K_LOSS, L, 4 * (2 * n * C + n));
     put(K_LOSS_MEAN, L, 4.0 * digest::softmax_xent_blocks(p->n_own, p->widths[L]) + 4);
-    for (int32_t lev = 0; lev < L; ++lev)
+    for (int32_t lev = 0; lev < L; ++lev) {
         put(K_PULL, lev, 8 * nh * p->widths[lev] + 4 * nh);
+        // the GCN pull's halo aggregate: P_b's entries, its distinct sources
+        // (at most every halo row), S written
+        if (model == DIGEST_MODEL_GCN && p->n_bnd > 0)
+            put(K_HALO_AGG, lev,
+                4 * (nb + 1) + 8 * (double)p->nnz_b + 4 * (nh + nb) * p->widths[lev], 0.0,
+                p->nnz_b);
+    }
     for (int32_t lev = 1; lev < L; ++lev)
         put(K_PUSH, lev, 8 * nb * p->widths[lev] + 8 * nb);
     return DIGEST_OK;

@@ -183,17 +183,30 @@ def test_launch_plan_and_cost_model():
     with pytest.raises(D.DigestError):
         D.digest_partition_plan(h, cfg.layers + 1)
     n, nh, nb = p.n_own, p.n_halo, h.n_boundary
+    assert 0 < nb < n and h.nnz_in < h.nnz
+    # the forward's operand: the owned-column entries, plus one entry per
+    # boundary row for its halo aggregate; the pull's: the halo entries
+    nnz_s, nnz_b = h.nnz_in + nb, h.nnz - h.nnz_in
     gcn = D.digest_profile_model(h, D.MODEL_GCN)
     assert gcn["pull_gather.l0"][0] == 8 * nh * cfg.widths[0] + 4 * nh
     assert gcn["push_scatter.l1"][0] == 8 * nb * cfg.widths[1] + 8 * nb
-    di = cfg.widths[0]
-    assert gcn["spmm_fwd.l1"] == (4 * (n + 1) + 8 * h.nnz + 4 * (n + nh) * di + 4 * n * di, 0.0,
-                                  h.nnz)
+    di, dh, do = cfg.widths
+    for lev, d in ((0, di), (1, dh)):
+        assert gcn[f"halo_aggregate.l{lev}"] == (
+            4 * (nb + 1) + 8 * nnz_b + 4 * (nh + nb) * d, 0.0, nnz_b)
+    assert gcn["spmm_fwd.l1"] == (4 * (n + 1) + 8 * nnz_s + 4 * (n + nb) * di + 4 * n * di, 0.0,
+                                  nnz_s)
     assert gcn["gemm_fwd_relu.l1"][1] == 2.0 * n * di * cfg.widths[1]
+    # the transform-first layer 2 multiplies the owned and the boundary rows
+    assert gcn["gemm_fwd_relu.l2"][1] == 2.0 * (n + nb) * dh * do
+    assert gcn["gemm_dw_splitk.l2"][1] == 2.0 * (n + nb) * dh * do
+    assert gcn["spmm_bwd_transposed.l2"][2] == h.nnz_in
+    assert gcn["boundary_rows.l2"][0] == 8 * nb * do + 4 * nb
     assert not any(k.startswith("gat_") for k in gcn)
     assert "softmax_xent.l2" in gcn and "loss_mean.l2" in gcn
     gat = D.digest_profile_model(h, D.MODEL_GAT)
     assert gat["gat_aggregate.l2"][2] == h.nnz and "spmm_fwd.l1" not in gat
+    assert not any(k.startswith("halo_aggregate") for k in gat)
     L = D.lib()
     buf = (ctypes.c_double * 1000)()
     cnt = (ctypes.c_int64 * 1000)()
@@ -247,20 +260,31 @@ def test_fused_forward_plan_and_cost_model(monkeypatch):
     monkeypatch.setenv("DIGEST_FUSE", "2")
     assert D.digest_partition_plan(h, 1)["forward_fused"] == 1
     assert D.digest_partition_plan(h, 2)["forward_fused"] == 0   # 7 outputs: narrow product
-    lens = np.diff(p.indptr)
+    # the forward's operand: row i's owned-column entries, then, for a row
+    # with halo entries (boundary row b), one entry reading column n_own + b
+    n = p.n_own
+    pos = {int(v): i for i, v in enumerate(p.owned)}
+    rows = np.repeat(np.arange(n), np.diff(p.indptr))
+    local = np.array([pos.get(int(c), -1) for c in p.indices])
+    inn = local >= 0
+    bnd = np.unique(rows[~inn])
+    s_rows = np.concatenate([rows[inn], bnd])
+    s_cols = np.concatenate([local[inn], n + np.arange(bnd.size)])
+    lens = np.bincount(s_rows, minlength=n)
+    assert lens.sum() == h.nnz_in + h.n_boundary
     long_rows = lens > 64
     assert long_rows.any() and (~long_rows).any()
-    rows = np.repeat(np.arange(p.n_own), lens)
-    src_short = np.unique(p.indices[~long_rows[rows]]).size
-    src_long = np.unique(p.indices[long_rows[rows]]).size
-    n, di, do = p.n_own, widths[0], widths[1]
+    src_short = np.unique(s_cols[~long_rows[s_rows]]).size
+    src_long = np.unique(s_cols[long_rows[s_rows]]).size
+    di, do = widths[0], widths[1]
     nl, el = int(long_rows.sum()), int(lens[long_rows].sum())
+    nnz_s = int(lens.sum())
     m = D.digest_profile_model(h, D.MODEL_GCN)
     assert "gemm_fwd_relu.l1" not in m
     assert m["spmm_fwd.l1"] == (8 * nl + 8 * el + 4 * src_long * di + 4 * nl * di, 0.0, el)
     assert m["spmm_gemm_fwd.l1"] == (
-        4 * (n + 1) + 8 * (h.nnz - el) + 4 * src_short * di + 4 * nl * di + 4 * (n - nl) * di +
-        4 * di * do + 4 * n * do, 2.0 * n * di * do, h.nnz - el)
+        4 * (n + 1) + 8 * (nnz_s - el) + 4 * src_short * di + 4 * nl * di + 4 * (n - nl) * di +
+        4 * di * do + 4 * n * do, 2.0 * n * di * do, nnz_s - el)
     monkeypatch.setenv("DIGEST_FUSE", "0")
     assert D.digest_partition_plan(h, 1)["forward_fused"] == 0
     assert "gemm_fwd_relu.l1" in D.digest_profile_model(h, D.MODEL_GCN)

@@ -296,6 +296,57 @@ def test_single_partition_no_halo():
         check_layer(c, layer)
 
 
+def test_halo_aggregate_follows_pulls():
+    """The halo rows reach the GCN forward through their aggregate, formed
+    when a level is pulled: a second pull from another store changes the
+    next forward and backward, a store written after the pull does not
+    (the rows are stale until the next pull), and a partition with a GAT
+    workspace (whose pulls skip the aggregate) forms it in the forward.
+    Layer 1 aggregates first (ReLU), layer 2 multiplies first (identity)."""
+    Dm = D()
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1500, widths=(36, 40, 12), classes=12)
+    g = synth.make_graph(cfg, seed=9)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 2), label="halo-aggregate", ws_fill=255)
+    assert 0 < c.h.n_boundary < c.n
+    assert Dm.digest_partition_plan(c.h, 1)["transform_first"] == 0
+    assert Dm.digest_partition_plan(c.h, 2)["transform_first"] == 1
+
+    def run(layer, store, label, write_after=None):
+        gstore = dev(store)
+        Dm.digest_pull(c.h, layer - 1, gstore)
+        c.op.pull(layer - 1, store)
+        if write_after is not None:   # the store changes, the pulled rows do not
+            gstore.copy_(dev(write_after))
+        h_in = c.layer_input(layer)
+        W = synth.weights(c.cfg)[layer - 1]
+        act = c.act(layer)
+        out = torch.empty(c.n, c.widths[layer], device="cuda")
+        Dm.digest_layer_forward(c.h, layer, dev(h_in), dev(W), out, act)
+        ref_out = c.op.forward(layer, h_in, W, act)
+        assert_close(host(out), ref_out, f"{label} forward layer {layer}")
+        dh = c.upstream(layer)
+        dw = torch.empty(W.shape, device="cuda")
+        dh_in = torch.empty(c.n, c.widths[layer - 1], device="cuda") if layer > 1 else None
+        Dm.digest_layer_backward(c.h, layer, dev(h_in), dev(ref_out), dev(dh), dev(W), dw,
+                                 dh_in)
+        ref_dw, ref_dh_in = c.op.backward(layer, h_in, W, ref_out, dh, act,
+                                          want_dh_in=layer > 1)
+        assert_close(host(dw), ref_dw, f"{label} dW layer {layer}")
+        if layer > 1:
+            assert_close(host(dh_in), ref_dh_in, f"{label} dH_in layer {layer}")
+
+    for layer in (1, 2):
+        a = synth.relu_normal((g.n, c.widths[layer - 1]), seed=70 + layer)
+        b = synth.relu_normal((g.n, c.widths[layer - 1]), seed=75 + layer) + 0.5
+        run(layer, a, "first pull")
+        run(layer, b, "second pull", write_after=a)
+    gat_ws = torch.empty(max(Dm.digest_gat_query(c.h), 256), dtype=torch.uint8, device="cuda")
+    Dm.digest_gat_bind_workspace(c.h, gat_ws)
+    for layer in (1, 2):
+        a = synth.relu_normal((g.n, c.widths[layer - 1]), seed=80 + layer)
+        run(layer, a, "GAT workspace bound")
+
+
 def test_empty_partition():
     Dm = D()
     h = Dm.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
