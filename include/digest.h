@@ -91,8 +91,10 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
 /* Release a handle (NULL is ignored).  The bound workspace is the caller's. */
 void digest_partition_destroy(digest_partition *p);
 
-/* Sizes: boundary rows, nnz of P_m, nnz of the owned block P_in, and the
- * device workspace bytes the handle needs.  Any output pointer may be NULL. */
+/* Sizes: boundary rows (owned rows with at least one halo column, in
+ * ascending row order: bnd[0..n_boundary)), nnz of P_m, nnz of the owned
+ * block P_in, and the device workspace bytes the handle needs.  Any output
+ * pointer may be NULL. */
 digest_status digest_partition_query(const digest_partition *p, int64_t *n_boundary,
                                      int64_t *nnz, int64_t *nnz_in,
                                      size_t *workspace_bytes);
@@ -101,8 +103,9 @@ digest_status digest_partition_query(const digest_partition *p, int64_t *n_bound
  * Bind caller-allocated device memory (>= workspace_bytes, 256-byte
  * aligned) and upload the partition's index structures into it on
  * hip_stream.  The library owns the layout of this memory (local CSR,
- * P_in^T, id lists, one halo buffer per level, the aggregated input AH of
- * each layer kept for the backward, reduction scratch) until the next bind
+ * P_in^T, id lists, one halo buffer and one halo aggregate per level, the
+ * aggregated input AH of each layer kept for the backward, reduction
+ * scratch) until the next bind
  * or destroy.  Re-binding resets the pull/forward state: every level must
  * be pulled again, and every backward (GCN or GAT) needs a forward after
  * the bind.
@@ -135,6 +138,12 @@ digest_status digest_partition_read_halo(const digest_partition *p, int32_t leve
  * Pull (Sec. 3.2; Algorithm 1 pulls when r mod N == 0): gather the stale
  * rows of the halo nodes of level `level` out of the store into the
  * handle's halo buffer of that level:  halo_buf[j, :] = store[halo[j], :].
+ * The same call forms the halo aggregate of the level, the halo rows'
+ * share of Eq. 5's aggregation for the boundary rows,
+ *   S[b, :] = sum_j P_out[bnd[b], j] halo_buf[j, :]   (n_boundary rows),
+ * which stays constant until the next pull of the level; the GCN forward of
+ * layer level+1 reads it instead of the halo rows (a handle with a GAT
+ * workspace bound skips it here and forms it in each GCN forward).
  *   level  0..L-1 (level 0 = the static features X, pulled once).
  *   store  device [n_global, d_level].
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace bound), DIGEST_EHIP.
@@ -170,15 +179,19 @@ digest_status digest_push(digest_partition *p, int32_t level, const float *h_own
  *   w      device [d_{layer-1}, d_layer].   h_out device [n_owned, d_layer].
  *   act    DIGEST_ACT_RELU or DIGEST_ACT_IDENTITY (the paper uses ReLU on
  *          hidden layers and raw logits at the last layer).
+ * The halo term enters through the level's halo aggregate S (digest_pull):
+ * P_out halo_buf = E S, with E placing S's rows at the boundary rows, so
+ * that h_out = act(P_s [h_in; S] W) with P_s = [P_in | E] (the same result
+ * up to float rounding).
  * Order of the two products (the same result up to float rounding): a
  * layer with the identity activation is computed transform-first,
- * T = [h_in; halo] W over all n_owned + n_halo local rows, then
- * h_out = P_m T, when a cost model of the layer's forward and backward says
- * that is cheaper: it weighs the gathered bytes of the sparse aggregations
- * (nnz rows at width d_out twice, against nnz rows at width d_in plus the
+ * T = [h_in; S] W over the n_owned + n_boundary rows, then h_out = P_s T,
+ * when a cost model of the layer's forward and backward says that is
+ * cheaper: it weighs the gathered bytes of the sparse aggregations (nnz
+ * rows at width d_out twice, against nnz rows at width d_in plus the
  * input-gradient aggregation) and the GEMM flops (over n_owned + n_halo rows
  * against n_owned rows) at measured MI355X rates.  Every other layer
- * aggregates first, AH = P_m [h_in; halo], then h_out = act(AH W), keeping AH
+ * aggregates first, AH = P_s [h_in; S], then h_out = act(AH W), keeping AH
  * in the workspace for the backward.
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace, or level layer-1 never
  * pulled while the partition has halo nodes), DIGEST_EHIP.
@@ -194,6 +207,8 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
  *   dw    = (P_m [h_in; halo])^T D                      (overwritten)
  *   dh_in = P_in^T D W^T           if dh_in != NULL    (overwritten)
  * The stale halo rows are constants of the layer: they get no gradient.
+ * A transform-first layer forms dw as [h_in; S]^T (P_s^T D): the owned
+ * rows' P_in^T D and, for the boundary rows, D's own rows.
  *   h_in   the same device array the forward of this layer read (it must
  *          be unchanged); h_out, dh_out device [n_owned, d_layer];
  *   w device [d_{layer-1}, d_layer];  dw device [d_{layer-1}, d_layer];
