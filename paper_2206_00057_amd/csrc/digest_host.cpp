@@ -478,28 +478,35 @@ struct digest_partition {
 namespace {
 
 // Order of the two products of a layer with the identity activation (the
-// same result, associated the other way).  Aggregate-first gathers nnz rows
-// of width d_in (and, for layers > 1, nnz_in rows of width min(d_in, d_out)
-// for the input gradient) and multiplies the n_own aggregated rows;
-// transform-first, Z = P_m ([H_in; H~_out] W), multiplies all n_own + n_halo
-// local rows and gathers 2 nnz rows of width d_out (P_m and P_m^T).  The
-// rates are those measured for the aggregation kernels (random row gathers)
-// and the fp32 MFMA GEMM on MI355X.
+// same result, associated the other way).  Both read the halo rows through
+// their aggregate S (nb boundary rows, formed at the pull).  Aggregate-first
+// gathers the nnz_s entries of P_s at width d_in (and, for layers > 1,
+// nnz_in entries of width min(d_in, d_out) for the input gradient) and
+// multiplies the n_own aggregated rows; transform-first, Z = P_s ([H_in; S] W),
+// multiplies the n_own + nb rows of [H_in; S] (and its weight gradient runs
+// over them) and gathers nnz_s + nnz_in entries of width d_out (P_s and
+// P_in^T), and copies D's boundary rows (and pads D when d_out is not a
+// multiple of 4).  The rates are those measured for the aggregation kernels
+// (random row gathers), the fp32 MFMA GEMM and row copies on MI355X.
 constexpr double kGatherBytesPerS = 7.0e12;
 constexpr double kGemmFlopsPerS = 80.0e12;
 
 bool transform_first_cheaper(const digest_partition &p, int32_t layer)
 {
     const double di = p.widths[layer - 1], dout = p.widths[layer];
-    const double n = p.n_own, R = (double)p.n_own + (double)p.n_halo;
+    const double n = p.n_own, R = (double)p.n_own + (double)p.n_bnd;
+    const double nnz_s = (double)p.nnz_s, nnz_in = (double)p.nnz_in;
     const bool dgrad = layer > 1;
     const double af =
-        ((double)p.nnz * di + (dgrad ? (double)p.nnz_in * std::min(di, dout) : 0.0)) * 4.0 /
-            kGatherBytesPerS +
+        (nnz_s * di + (dgrad ? nnz_in * std::min(di, dout) : 0.0)) * 4.0 / kGatherBytesPerS +
         2.0 * n * di * dout * (dgrad ? 3.0 : 2.0) / kGemmFlopsPerS;
-    const double tf = 2.0 * (double)p.nnz * dout * 4.0 / kGatherBytesPerS +
+    const double copies = 8.0 * p.n_bnd * dout +
+                          (p.widths[layer] % 4 ? 4.0 * n * (dout + padded_width(p.widths[layer]))
+                                               : 0.0);
+    const double tf = (nnz_s + nnz_in) * dout * 4.0 / kGatherBytesPerS +
                       (4.0 * R * di * dout + (dgrad ? 2.0 * n * di * dout : 0.0)) /
-                          kGemmFlopsPerS;
+                          kGemmFlopsPerS +
+                      copies / kStreamBytesPerS;
     return tf < af;
 }
 
