@@ -1382,20 +1382,22 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
         return fail(DIGEST_EINVAL, "store is NULL");
     hipStream_t s = (hipStream_t)hip_stream;
     if (p->n_halo > 0) {
-        Timed t(p, K_PULL, level, s);
-        digest_status st = hip_check(
-            digest::launch_copy_rows(p->at<int32_t>(p->lay.halo_gid), nullptr, p->n_halo,
-                                     p->widths[level], store,
-                                     p->at<float>(p->lay.halo_buf[level]), s, p->widths[level],
-                                     padded_width(p->widths[level])),
-            "pull");
-        if (st)
-            return st;
+        {
+            Timed t(p, K_PULL, level, s);
+            digest_status st = hip_check(
+                digest::launch_copy_rows(p->at<int32_t>(p->lay.halo_gid), nullptr, p->n_halo,
+                                         p->widths[level], store,
+                                         p->at<float>(p->lay.halo_buf[level]), s,
+                                         p->widths[level], padded_width(p->widths[level])),
+                "pull");
+            if (st)
+                return st;
+        }
         // the halo aggregate for the next layer's GCN forward (a partition
         // with a GAT workspace forms it in each GCN forward instead)
         if (!p->gws)
-            if (digest_status st2 = halo_aggregate(p, level, s))
-                return st2;
+            if (digest_status st = halo_aggregate(p, level, s))
+                return st;
     }
     p->pulled[level] = 1;
     p->pull_gen[level] += 1;
