@@ -1698,23 +1698,37 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                 "boundary rows"))
             return st;
     }
-    // (everything after G is a product bound by the MFMA units, so the
-    // weight gradient stays on s: two such products side by side only
-    // share the units)
-    if (digest_status st = weight_grad_rows(p, layer, h_in, h2, n2, G, ldg, gpart, dw, s,
-                                            K_GEMM_DW, K_REDUCE_DW))
-        return st;
-    if (fused_dh)
-        return DIGEST_OK;
-    if (dh_in) {
-        Timed tm(p, K_GEMM_DH, layer, s);
-        if (digest_status st = times_wt(p->n_own, d_in, d_out, G, ldg, w, dh_in, s))
+    // The weight gradient and the products by W^T both only read G.  A
+    // large weight gradient runs on the side stream next to them (neither
+    // kind keeps the MFMA units busy alone on these narrow shapes), joined
+    // back before the call returns.
+    hipStream_t sw = s;
+    const bool more = !fused_dh && (dh_in || (dh_halo && p->n_halo > 0));
+    if (more && side_pays(2.0 * ((double)p->n_own + n2) * d_in * d_out))
+        if (digest_status st = fork_side(p, s, &sw))
             return st;
+    const digest_status st_all = [&]() -> digest_status {
+        if (digest_status st = weight_grad_rows(p, layer, h_in, h2, n2, G, ldg, gpart, dw, sw,
+                                                K_GEMM_DW, K_REDUCE_DW))
+            return st;
+        if (fused_dh)
+            return DIGEST_OK;
+        if (dh_in) {
+            Timed tm(p, K_GEMM_DH, layer, s);
+            if (digest_status st = times_wt(p->n_own, d_in, d_out, G, ldg, w, dh_in, s))
+                return st;
+        }
+        if (!dh_halo || p->n_halo == 0)
+            return DIGEST_OK;
+        Timed tm(p, K_HALO_GRAD, layer, s);
+        return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * ldg, ldg, w, dh_halo,
+                        s);
+    }();
+    if (sw != s) {
+        const digest_status st = join_side(p, s);
+        return st_all ? st_all : st;
     }
-    if (!dh_halo || p->n_halo == 0)
-        return DIGEST_OK;
-    Timed tm(p, K_HALO_GRAD, layer, s);
-    return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * ldg, ldg, w, dh_halo, s);
+    return st_all;
 }
 
 }  // namespace

@@ -810,8 +810,11 @@ def test_nan_padding_never_reaches_outputs(widths):
 # layer aggregated at its narrower output width first (24 -> 40 -> 36); and
 # the fused passes forced (a ReLU layer of 96 floats fused in both
 # directions, 100 -> 96 -> 96 -> 7), so that the weight gradient's fork sits
-# after the formed D and beside the fused input gradient
-SIDE = [((24, 40, 48, 7), "0"), ((24, 40, 36), "0"), ((100, 96, 96, 7), "2")]
+# after the formed D and beside the fused input gradient; and a
+# transform-first layer 24 floats wide (48 -> 96 -> 24), whose weight
+# gradient runs beside G W^T
+SIDE = [((24, 40, 48, 7), "0"), ((24, 40, 36), "0"), ((100, 96, 96, 7), "2"),
+        ((48, 96, 24), "0")]
 
 
 @pytest.mark.parametrize("widths,fuse", SIDE,
@@ -824,10 +827,13 @@ def test_side_stream_backward(widths, fuse, monkeypatch):
     g = synth.make_graph(cfg, seed=4)
     part = synth.make_partition(cfg, g, 2)
     c = Case(cfg, g, part, label=f"side{widths}")
+    Dm = D()
     if fuse == "2":
-        Dm = D()
         assert Dm.digest_partition_plan(c.h, 2)["forward_fused"] == 1
         assert Dm.digest_partition_plan(c.h, 2)["backward_fused"] == 1
+    if widths == (48, 96, 24):
+        pl = Dm.digest_partition_plan(c.h, 2)
+        assert pl["transform_first"] == 1 and pl["dgrad_fused"] == 0
     for layer in range(1, c.L + 1):
         check_layer(c, layer)
     # rounds: eager, then captured and replayed (bit for bit)
