@@ -48,20 +48,25 @@ def measured_traffic(workload, key):
     summary: L2-to-fabric bytes (rocprofv3 FETCH_SIZE + WRITE_SIZE, each
     scaled by a plain copy kernel of known size; Infinity Cache hits are
     included, so this is not HBM traffic alone).  (None, reason) when there
-    is no summary for this kernel or the kernel sources changed since."""
-    rel = os.path.join("profiles", f"{workload}_hbm_traffic.txt")
-    path = os.path.join(ROOT, rel)
-    if not os.path.exists(path):
-        return None, f"no counter summary for {workload}"
-    kv = {}
-    for line in open(path):
-        line = line.split("#", 1)[0].strip()
-        if "=" in line:
-            k, v = line.split("=", 1)
-            kv[k.strip()] = v.strip()
+    is no summary for this kernel or the kernel sources changed since.
+    The summaries of a workload are profiles/<workload>_*traffic.txt, one
+    kernel (or a list of launches of one kernel) each."""
+    import glob
+    found = None
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", f"{workload}_*traffic.txt"))):
+        kv = {}
+        for line in open(path):
+            line = line.split("#", 1)[0].strip()
+            if "=" in line:
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+        if key in [k.strip() for k in kv.get("kernel", "").split(",")]:
+            found = (os.path.relpath(path, ROOT), kv)
+            break
+    if found is None:
+        return None, f"no counter summary of {key} for {workload}"
+    rel, kv = found
     from paper_2206_00057_amd.pmc import kernel_source_hash
-    if key not in [k.strip() for k in kv.get("kernel", "").split(",")]:
-        return None, f"{rel} covers {kv.get('kernel')}, not {key}"
     sha = kernel_source_hash()
     if kv.get("source_sha") != sha:
         return None, f"{rel} was taken on kernel sources {kv.get('source_sha')}, now {sha}"
