@@ -50,6 +50,7 @@ typedef enum {
 
 enum { DIGEST_ACT_RELU = 0, DIGEST_ACT_IDENTITY = 1 };
 enum { DIGEST_PUSH_BOUNDARY = 0, DIGEST_PUSH_ALL_OWNED = 1 };
+enum { DIGEST_PULL_ROWS = 0, DIGEST_PULL_AGGREGATE = 1 };
 
 /* Message describing the last non-OK status returned on this thread. */
 const char *digest_last_error(void);
@@ -130,9 +131,26 @@ digest_status digest_partition_export_transpose(const digest_partition *p,
 
 /* Test hook: copy the halo buffer of `level` ([n_halo, d_level], filled by
  * digest_pull) into the caller's device array `out` on hip_stream.
- * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace), DIGEST_EHIP. */
+ * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace; pull mode
+ * DIGEST_PULL_AGGREGATE, which keeps no halo rows), DIGEST_EHIP. */
 digest_status digest_partition_read_halo(const digest_partition *p, int32_t level, float *out,
                                          void *hip_stream);
+
+/*
+ * What a pull of this handle keeps (host-side state, no device work):
+ *   DIGEST_PULL_ROWS (the default): the halo rows in the halo buffer, and
+ *     the halo aggregate formed from them (digest_pull).
+ *   DIGEST_PULL_AGGREGATE: the halo aggregate alone, gathered straight from
+ *     the store; the halo buffer is left alone, so a pull moves the halo
+ *     rows once instead of twice.  For callers that use the GCN layer only:
+ *     the calls that read halo rows (the GAT layer, the halo read-back, and
+ *     digest_layer_backward_halo of a transform-first layer) return
+ *     DIGEST_ESTATE while a level pulled this way is in use.
+ * A change of mode marks every level as not pulled.  Callers that capture
+ * graphs set the mode before the capture.
+ * Errors: DIGEST_EINVAL (NULL, unknown mode).
+ */
+digest_status digest_partition_set_pull_mode(digest_partition *p, int32_t mode);
 
 /*
  * Pull (Sec. 3.2; Algorithm 1 pulls when r mod N == 0): gather the stale
@@ -143,7 +161,9 @@ digest_status digest_partition_read_halo(const digest_partition *p, int32_t leve
  *   S[b, :] = sum_j P_out[bnd[b], j] halo_buf[j, :]   (n_boundary rows),
  * which stays constant until the next pull of the level; the GCN forward of
  * layer level+1 reads it instead of the halo rows (a handle with a GAT
- * workspace bound skips it here and forms it in each GCN forward).
+ * workspace bound skips it here and forms it in each GCN forward).  In pull
+ * mode DIGEST_PULL_AGGREGATE the call forms S from the store's rows directly
+ * and leaves the halo buffer as it was.
  *   level  0..L-1 (level 0 = the static features X, pulled once).
  *   store  device [n_global, d_level].
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace bound), DIGEST_EHIP.
@@ -253,7 +273,9 @@ digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const flo
  * Results equal those of the two separate calls up to float32 rounding
  * order.
  * Errors: those of digest_layer_backward; DIGEST_EINVAL for layer 1 or a
- * NULL dh_in / dh_halo.
+ * NULL dh_in / dh_halo; DIGEST_ESTATE for a transform-first layer (its
+ * weight gradient then reads the halo rows) in pull mode
+ * DIGEST_PULL_AGGREGATE.
  */
 digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, const float *h_in,
                                          const float *h_out, const float *dh_out,
@@ -320,7 +342,8 @@ digest_status digest_gat_bind_workspace(digest_partition *p, void *dev_ptr, size
  *   h_out device [n_owned, d_layer];  act DIGEST_ACT_RELU or _IDENTITY.
  *   d_layer <= 512.
  * Errors: DIGEST_EINVAL (range, NULL, width), DIGEST_ESTATE (no workspace
- * or GAT workspace, level layer-1 never pulled), DIGEST_EHIP.
+ * or GAT workspace, level layer-1 never pulled, pull mode
+ * DIGEST_PULL_AGGREGATE with halo nodes), DIGEST_EHIP.
  */
 digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float *h_in,
                                  const float *w, const float *att, float negative_slope,
@@ -341,7 +364,8 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
  * act' is the ReLU mask h_out > 0.  Sums run in a fixed order (no float
  * atomics).
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no GAT forward of the layer since
- * the GAT bind, or level layer-1 pulled again since it), DIGEST_EHIP.
+ * the GAT bind, or level layer-1 pulled again since it, pull mode
+ * DIGEST_PULL_AGGREGATE with halo nodes), DIGEST_EHIP.
  */
 digest_status digest_gat_backward(digest_partition *p, int32_t layer, const float *h_in,
                                   const float *h_out, const float *dh_out, const float *w,

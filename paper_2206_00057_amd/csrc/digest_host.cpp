@@ -392,6 +392,11 @@ struct digest_partition {
     // of 1 in column n_own + b, which reads S's row b: P_s [h; S] = P_m [h; halo].
     int64_t nnz_s = 0, nnz_b = 0;
     std::vector<int32_t> s_rowptr, s_col, b_rowptr, b_col;
+    std::vector<int32_t> b_gcol;   // P_b's columns as global ids (the store's rows)
+    // DIGEST_PULL_ROWS: a pull fills the halo buffer, then S from it;
+    // DIGEST_PULL_AGGREGATE: a pull forms S straight from the store and
+    // leaves the halo buffer alone (the calls that read it refuse).
+    int32_t pull_mode = DIGEST_PULL_ROWS;
     std::vector<float> s_val, b_val;
     std::vector<SpmmBlock> blocks_s, blocks_b;
     int32_t long_s = 0, long_b = 0;
@@ -413,7 +418,7 @@ struct digest_partition {
     struct Layout {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
-        size_t s_rowptr, s_col, s_val, b_rowptr, b_col, b_val, blocks_s, blocks_b;
+        size_t s_rowptr, s_col, s_val, b_rowptr, b_col, b_gcol, b_val, blocks_s, blocks_b;
         size_t fuse_order, fuse_order_t;   // per owned row, uint8 (see fuse_order below)
         size_t fz;                      // the fused input gradient's D and long rows
         size_t wt;                      // W^T of the fused input gradient
@@ -595,6 +600,7 @@ void plan_layout(digest_partition &p)
     l.s_val = take(sizeof(float) * p.s_val.size());
     l.b_rowptr = take(sizeof(int32_t) * p.b_rowptr.size());
     l.b_col = take(sizeof(int32_t) * p.b_col.size());
+    l.b_gcol = take(sizeof(int32_t) * p.b_gcol.size());
     l.b_val = take(sizeof(float) * p.b_val.size());
     l.blocks_s = take(sizeof(SpmmBlock) * p.blocks_s.size());
     l.blocks_b = take(sizeof(SpmmBlock) * p.blocks_b.size());
@@ -963,20 +969,31 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
 
 // S = P_b halo_buf[level]: the halo aggregate of level `level` (the halo
 // rows' share of each boundary row's aggregate in the forward of layer
-// level + 1), rows padded like the halo buffer.
-digest_status halo_aggregate(digest_partition *p, int32_t level, hipStream_t s)
+// level + 1), rows padded like the halo buffer.  With `store` (the level's
+// [n_global, d] rows) the same sum is gathered from the store by global id
+// instead; S then stores the d columns of each row.
+digest_status halo_aggregate(digest_partition *p, int32_t level, hipStream_t s,
+                             const float *store = nullptr)
 {
     if (p->n_bnd == 0)
         return DIGEST_OK;
-    const int32_t lw = padded_width(p->widths[level]);
+    const int32_t d = p->widths[level], lw = padded_width(d);
+    const int32_t *rowptr = p->at<int32_t>(p->lay.b_rowptr);
+    const float *val = p->at<float>(p->lay.b_val);
+    const SpmmBlock *blocks = p->at<SpmmBlock>(p->lay.blocks_b);
+    const int32_t nb = (int32_t)p->blocks_b.size();
+    float *out = p->at<float>(p->lay.hagg[level]);
     Timed t(p, K_HALO_AGG, level, s);
-    return hip_check(digest::launch_spmm(p->at<SpmmBlock>(p->lay.blocks_b),
-                                         (int32_t)p->blocks_b.size(), p->long_b,
-                                         p->at<int32_t>(p->lay.b_rowptr),
-                                         p->at<int32_t>(p->lay.b_col),
-                                         p->at<float>(p->lay.b_val),
+    if (store)
+        return hip_check(digest::launch_spmm(blocks, nb, p->long_b, rowptr,
+                                             p->at<int32_t>(p->lay.b_gcol), val, store, nullptr,
+                                             INT32_MAX, d, out, s, nullptr, nullptr, INT32_MAX,
+                                             false, nullptr, false, d, lw, d),
+                         "halo aggregate");
+    return hip_check(digest::launch_spmm(blocks, nb, p->long_b, rowptr,
+                                         p->at<int32_t>(p->lay.b_col), val,
                                          p->at<float>(p->lay.halo_buf[level]), nullptr,
-                                         p->n_halo, lw, p->at<float>(p->lay.hagg[level]), s),
+                                         p->n_halo, lw, out, s),
                      "halo aggregate");
 }
 
@@ -1177,6 +1194,9 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
             }
             p->s_rowptr[i + 1] = (int32_t)p->s_col.size();
         }
+        p->b_gcol.resize(p->b_col.size());
+        for (size_t k = 0; k < p->b_col.size(); ++k)
+            p->b_gcol[k] = p->halo_gid[p->b_col[k]];
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
         p->long_s = build_blocks(p->s_rowptr, p->n_own, p->blocks_s);
         p->long_b = build_blocks(p->b_rowptr, p->n_bnd, p->blocks_b);
@@ -1286,6 +1306,7 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.s_val, p->s_val.data(), sizeof(float) * p->s_val.size()},
         {l.b_rowptr, p->b_rowptr.data(), sizeof(int32_t) * p->b_rowptr.size()},
         {l.b_col, p->b_col.data(), sizeof(int32_t) * p->b_col.size()},
+        {l.b_gcol, p->b_gcol.data(), sizeof(int32_t) * p->b_gcol.size()},
         {l.b_val, p->b_val.data(), sizeof(float) * p->b_val.size()},
         {l.blocks_s, p->blocks_s.data(), sizeof(SpmmBlock) * p->blocks_s.size()},
         {l.blocks_b, p->blocks_b.data(), sizeof(SpmmBlock) * p->blocks_b.size()},
@@ -1364,11 +1385,25 @@ digest_status digest_partition_read_halo(const digest_partition *p, int32_t leve
         return fail(DIGEST_EINVAL, "bad level %d or NULL output", level);
     if (p->n_halo == 0)
         return DIGEST_OK;
+    if (p->pull_mode != DIGEST_PULL_ROWS)
+        return fail(DIGEST_ESTATE, "the pull mode keeps no halo rows");
     const int32_t d = p->widths[level];
     return hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_halo, d,
                                               p->at<float>(p->lay.halo_buf[level]), out,
                                               (hipStream_t)hip_stream, padded_width(d), d),
                      "read halo");
+}
+
+digest_status digest_partition_set_pull_mode(digest_partition *p, int32_t mode)
+{
+    if (!p)
+        return fail(DIGEST_EINVAL, "NULL partition handle");
+    if (mode != DIGEST_PULL_ROWS && mode != DIGEST_PULL_AGGREGATE)
+        return fail(DIGEST_EINVAL, "unknown pull mode %d", mode);
+    if (mode != p->pull_mode)
+        std::fill(p->pulled.begin(), p->pulled.end(), 0);
+    p->pull_mode = mode;
+    return DIGEST_OK;
 }
 
 digest_status digest_pull(digest_partition *p, int32_t level, const float *store,
@@ -1381,7 +1416,10 @@ digest_status digest_pull(digest_partition *p, int32_t level, const float *store
     if (!store)
         return fail(DIGEST_EINVAL, "store is NULL");
     hipStream_t s = (hipStream_t)hip_stream;
-    if (p->n_halo > 0) {
+    if (p->n_halo > 0 && p->pull_mode == DIGEST_PULL_AGGREGATE) {
+        if (digest_status st = halo_aggregate(p, level, s, store))
+            return st;
+    } else if (p->n_halo > 0) {
         {
             Timed t(p, K_PULL, level, s);
             digest_status st = hip_check(
@@ -1447,7 +1485,7 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
     // formed by the pull of level layer-1, or here when a GAT workspace is
     // bound (its pulls skip it).
     const float *hs = p->n_bnd > 0 ? p->at<float>(p->lay.hagg[layer - 1]) : nullptr;
-    if (p->gws && p->n_own > 0)
+    if (p->gws && p->pull_mode == DIGEST_PULL_ROWS && p->n_own > 0)
         if (digest_status st = halo_aggregate(p, layer - 1, s))
             return st;
     const bool tf = act == DIGEST_ACT_IDENTITY && transform_first_cheaper(*p, layer);
@@ -1957,6 +1995,9 @@ digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, con
         return fail(DIGEST_EINVAL, "NULL dh_in or dh_halo");
     if (digest_status st = check_backward(p, layer, h_in, h_out, dh_out, w, dw))
         return st;
+    if (p->tf[layer] && p->n_own > 0 && p->n_halo > 0 && p->pull_mode != DIGEST_PULL_ROWS)
+        return fail(DIGEST_ESTATE, "the weight gradient of a transform-first layer with the "
+                                   "halo gradient reads halo rows, which the pull mode skips");
     return layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_halo,
                           (hipStream_t)hip_stream);
 }
@@ -2200,6 +2241,8 @@ digest_status digest_gat_forward(digest_partition *p, int32_t layer, const float
         return fail(DIGEST_EINVAL, "NULL h_in, w, att or h_out");
     if (p->n_halo > 0 && !p->pulled[layer - 1])
         return fail(DIGEST_ESTATE, "level %d was never pulled", layer - 1);
+    if (p->n_halo > 0 && p->pull_mode != DIGEST_PULL_ROWS)
+        return fail(DIGEST_ESTATE, "the GAT layer reads halo rows, which the pull mode skips");
     hipStream_t s = (hipStream_t)hip_stream;
     const float *halo = p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr;
     const int32_t R = p->n_own + p->n_halo;
@@ -2262,6 +2305,8 @@ digest_status digest_gat_backward(digest_partition *p, int32_t layer, const floa
         return fail(DIGEST_ESTATE,
                     "level %d was pulled again between the GAT forward and backward of layer %d",
                     layer - 1, layer);
+    if (p->n_halo > 0 && p->pull_mode != DIGEST_PULL_ROWS)
+        return fail(DIGEST_ESTATE, "the GAT layer reads halo rows, which the pull mode skips");
     hipStream_t s = (hipStream_t)hip_stream;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const int32_t R = p->n_own + p->n_halo;
@@ -2568,10 +2613,13 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
     const double C = p->widths[L];
     put(K_LOSS, L, 4 * (2 * n * C + n));
     put(K_LOSS_MEAN, L, 4.0 * digest::softmax_xent_blocks(p->n_own, p->widths[L]) + 4);
+    const bool rows = p->pull_mode == DIGEST_PULL_ROWS;
     for (int32_t lev = 0; lev < L; ++lev) {
-        put(K_PULL, lev, 8 * nh * p->widths[lev] + 4 * nh);
+        if (rows)
+            put(K_PULL, lev, 8 * nh * p->widths[lev] + 4 * nh);
         // the GCN pull's halo aggregate: P_b's entries, its distinct sources
-        // (at most every halo row), S written
+        // (at most every halo row, from the halo buffer or the store), S
+        // written
         if (model == DIGEST_MODEL_GCN && p->n_bnd > 0)
             put(K_HALO_AGG, lev,
                 4 * (nb + 1) + 8 * (double)p->nnz_b + 4 * (nh + nb) * p->widths[lev], 0.0,

@@ -22,6 +22,7 @@ OK, EINVAL, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4
 MODEL_GCN, MODEL_GAT = 0, 1
 ACT_RELU, ACT_IDENTITY = 0, 1
 PUSH_BOUNDARY, PUSH_ALL_OWNED = 0, 1
+PULL_ROWS, PULL_AGGREGATE = 0, 1
 
 _lib = None
 
@@ -52,6 +53,7 @@ def lib():
             "digest_partition_export_transpose": ([P, P, P, P], st),
             "digest_partition_read_halo": ([P, i32, P, P], st),
             "digest_pull": ([P, i32, P, P], st),
+            "digest_partition_set_pull_mode": ([P, i32], st),
             "digest_push": ([P, i32, P, P, i32, P], st),
             "digest_layer_forward": ([P, i32, P, P, P, i32, P], st),
             "digest_layer_backward": ([P, i32, P, P, P, P, P, P, P], st),
@@ -221,6 +223,10 @@ def _check_level(p, level, lo):
 def _check_layer(p, layer):
     if not (1 <= layer <= p.L):
         raise DigestError(EINVAL, f"layer {layer} outside [1, {p.L}]")
+
+
+def digest_partition_set_pull_mode(p, mode):
+    _check(lib().digest_partition_set_pull_mode(p.handle, int(mode)))
 
 
 def digest_pull(p, level, store, stream=None):

@@ -29,9 +29,12 @@ from . import digest as D
 
 class GpuPartition:
     def __init__(self, n_global, part, widths, device="cuda", overlap_io=False, model="gcn",
-                 atts=None):
+                 atts=None, pull_mode=None):
         """model "gcn" (Eq. 5) or "gat" (the attention layer over stale halo
-        rows; atts are its per-layer [d_l, 2] attention matrices)."""
+        rows; atts are its per-layer [d_l, 2] attention matrices).
+        pull_mode: what a pull keeps (D.PULL_ROWS or D.PULL_AGGREGATE); by
+        default the halo aggregate alone for the GCN layer, the halo rows
+        for the GAT layer, which reads them."""
         if model not in ("gcn", "gat"):
             raise ValueError("model is gcn or gat")
         if model == "gat" and (atts is None or len(atts) != len(widths) - 1):
@@ -42,6 +45,9 @@ class GpuPartition:
         self.device = device
         self.p = D.digest_partition_create(n_global, part.indptr, part.indices, part.values,
                                            part.owned, part.halo, self.widths)
+        if pull_mode is None:
+            pull_mode = D.PULL_AGGREGATE if model == "gcn" else D.PULL_ROWS
+        D.digest_partition_set_pull_mode(self.p, pull_mode)
         n = self.p.n_own
         self.n_own = n
         self.workspace = torch.empty(max(self.p.workspace_bytes, 256), dtype=torch.uint8,

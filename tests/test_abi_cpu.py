@@ -214,6 +214,25 @@ def test_launch_plan_and_cost_model():
     assert L.digest_profile_model(h.handle, 0, None, buf, cnt) == D.EINVAL
 
 
+def test_pull_mode_and_its_cost_model():
+    """The aggregate-only pull mode drops the pull's row gather from the cost
+    model (the halo aggregate reads the store instead); unknown modes and a
+    NULL handle are refused."""
+    cfg, g, p = _tiny_partition(0)
+    h = D.digest_partition_create(g.n, p.indptr, p.indices, p.values, p.owned, p.halo, cfg.widths)
+    rows = D.digest_profile_model(h, D.MODEL_GCN)
+    assert "pull_gather.l0" in rows and "halo_aggregate.l0" in rows
+    D.digest_partition_set_pull_mode(h, D.PULL_AGGREGATE)
+    agg = D.digest_profile_model(h, D.MODEL_GCN)
+    assert not any(k.startswith("pull_gather") for k in agg)
+    assert agg["halo_aggregate.l1"] == rows["halo_aggregate.l1"]
+    D.digest_partition_set_pull_mode(h, D.PULL_ROWS)
+    assert "pull_gather.l1" in D.digest_profile_model(h, D.MODEL_GCN)
+    for bad in (-1, 2, 7):
+        expect_status(D.EINVAL, D.digest_partition_set_pull_mode, h, bad)
+    assert D.lib().digest_partition_set_pull_mode(None, D.PULL_ROWS) == D.EINVAL
+
+
 def test_tier_plan_follows_the_overrides(monkeypatch):
     """Tiers are planned at create: a forced count with a small L2 budget
     gives that many tiers of budget / 128 rows (256-wide rows: one 32-float

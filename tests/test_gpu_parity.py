@@ -347,6 +347,64 @@ def test_halo_aggregate_follows_pulls():
         run(layer, a, "GAT workspace bound")
 
 
+def test_pull_aggregate_mode():
+    """In the aggregate-only pull mode a pull forms the halo aggregate from
+    the store's rows (here 42 floats wide, not a multiple of 4) and keeps no
+    halo rows: forward and backward still match the oracle after each pull,
+    the calls that read halo rows refuse, and switching back to the rows
+    mode needs a new pull."""
+    Dm = D()
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1500, widths=(36, 42, 12), classes=12)
+    g = synth.make_graph(cfg, seed=9)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 2), label="pull-aggregate", ws_fill=255)
+    assert 0 < c.h.n_boundary < c.n
+    assert Dm.digest_partition_plan(c.h, 2)["transform_first"] == 1
+    Dm.digest_partition_set_pull_mode(c.h, Dm.PULL_AGGREGATE)
+    for layer in (1, 2):
+        check_layer(c, layer)   # pulls store(layer - 1) first
+        b = synth.relu_normal((g.n, c.widths[layer - 1]), seed=85 + layer) + 0.25
+        Dm.digest_pull(c.h, layer - 1, dev(b))
+        c.op.pull(layer - 1, b)
+        h_in = c.layer_input(layer)
+        W = synth.weights(c.cfg)[layer - 1]
+        out = torch.empty(c.n, c.widths[layer], device="cuda")
+        Dm.digest_layer_forward(c.h, layer, dev(h_in), dev(W), out, c.act(layer))
+        ref = c.op.forward(layer, h_in, W, c.act(layer))
+        assert_close(host(out), ref, f"second pull forward layer {layer}")
+    # the calls that read halo rows refuse
+    with pytest.raises(Dm.DigestError) as e:
+        Dm.digest_partition_read_halo(c.h, 1, torch.empty(c.part.n_halo, c.widths[1],
+                                                           device="cuda"))
+    assert e.value.status == Dm.ESTATE
+    h_in = c.layer_input(2)
+    W = synth.weights(c.cfg)[1]
+    ref = c.op.forward(2, h_in, W, c.act(2))
+    dw = torch.empty(W.shape, device="cuda")
+    dh_in = torch.empty(c.n, c.widths[1], device="cuda")
+    dh_halo = torch.empty(c.part.n_halo, c.widths[1], device="cuda")
+    with pytest.raises(Dm.DigestError) as e:
+        Dm.digest_layer_backward_halo(c.h, 2, dev(h_in), dev(ref), dev(c.upstream(2)), dev(W),
+                                      dw, dh_in, dh_halo)
+    assert e.value.status == Dm.ESTATE
+    gat_ws = torch.empty(max(Dm.digest_gat_query(c.h), 256), dtype=torch.uint8, device="cuda")
+    Dm.digest_gat_bind_workspace(c.h, gat_ws)
+    att = synth.normal((c.widths[1], 2), seed=5)
+    with pytest.raises(Dm.DigestError) as e:
+        Dm.digest_gat_forward(c.h, 1, dev(c.layer_input(1)), dev(synth.weights(c.cfg)[0]),
+                              dev(att), torch.empty(c.n, c.widths[1], device="cuda"),
+                              Dm.ACT_RELU)
+    assert e.value.status == Dm.ESTATE
+    # back to the rows mode: every level must be pulled again
+    Dm.digest_partition_set_pull_mode(c.h, Dm.PULL_ROWS)
+    with pytest.raises(Dm.DigestError) as e:
+        Dm.digest_layer_forward(c.h, 2, dev(h_in), dev(W), torch.empty(c.n, c.widths[2],
+                                                                       device="cuda"),
+                                c.act(2))
+    assert e.value.status == Dm.ESTATE
+    check_pull(c, 1)
+    check_layer(c, 2)
+
+
 def test_empty_partition():
     Dm = D()
     h = Dm.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
@@ -540,7 +598,9 @@ def test_profile_instrumentation(tiny_graph):
     # tiny workload: layer 1 aggregates first; layer 2 (64 -> 16, identity) transforms first
     assert prof["spmm_fwd.l1"][1] == 1 and prof["spmm_fwd.l2"][1] == 1
     assert prof["gemm_fwd_relu.l1"][1] == 1 and prof["gemm_fwd_relu.l2"][1] == 1
-    assert prof["pull_gather.l1"][1] == 1 and prof["push_scatter.l1"][1] == 1
+    # the GCN partition's pulls keep the halo aggregate alone (no row gather)
+    assert prof["halo_aggregate.l1"][1] == 1 and "pull_gather.l1" not in prof
+    assert prof["push_scatter.l1"][1] == 1 and prof["boundary_rows.l2"][1] == 1
     assert prof["softmax_xent.l2"][1] == 1 and prof["loss_mean.l2"][1] == 1
     assert prof["gemm_dw_splitk.l1"][1] == 1 and prof["gemm_dw_splitk.l2"][1] == 1
     assert prof["spmm_bwd_transposed.l2"][1] == 1 and "spmm_bwd_transposed.l1" not in prof
