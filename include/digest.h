@@ -204,15 +204,15 @@ digest_status digest_push(digest_partition *p, int32_t level, const float *h_own
  * that h_out = act(P_s [h_in; S] W) with P_s = [P_in | E] (the same result
  * up to float rounding).
  * Order of the two products (the same result up to float rounding): a
- * layer with the identity activation is computed transform-first,
- * T = [h_in; S] W over the n_owned + n_boundary rows, then h_out = P_s T,
- * when a cost model of the layer's forward and backward says that is
- * cheaper: it weighs the gathered bytes of the sparse aggregations (nnz
- * rows at width d_out twice, against nnz rows at width d_in plus the
- * input-gradient aggregation) and the GEMM flops (over n_owned + n_halo rows
- * against n_owned rows) at measured MI355X rates.  Every other layer
- * aggregates first, AH = P_s [h_in; S], then h_out = act(AH W), keeping AH
- * in the workspace for the backward.
+ * layer is computed transform-first, T = [h_in; S] W over the
+ * n_owned + n_boundary rows, then h_out = act(P_s T), when a cost model of
+ * the layer's forward and backward says that is cheaper: it weighs the
+ * gathered bytes of the sparse aggregations (P_s and P_in^T at width d_out,
+ * against P_s at width d_in plus, above layer 1, the input gradient's
+ * aggregation), the GEMM flops (over n_owned + n_boundary rows against
+ * n_owned rows) and the row copies at measured MI355X rates.  Otherwise the
+ * layer aggregates first, AH = P_s [h_in; S], then h_out = act(AH W),
+ * keeping AH in the workspace for the backward.
  * Errors: DIGEST_EINVAL, DIGEST_ESTATE (no workspace, or level layer-1 never
  * pulled while the partition has halo nodes), DIGEST_EHIP.
  */

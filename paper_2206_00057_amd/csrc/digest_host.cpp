@@ -482,8 +482,9 @@ struct digest_partition {
 
 namespace {
 
-// Order of the two products of a layer with the identity activation (the
-// same result, associated the other way).  Both read the halo rows through
+// Order of the two products of a layer (the same result, associated the
+// other way; a ReLU applies to the aggregated product either way).  Both
+// read the halo rows through
 // their aggregate S (nb boundary rows, formed at the pull).  Aggregate-first
 // gathers the nnz_s entries of P_s at width d_in (and, for layers > 1,
 // nnz_in entries of width min(d_in, d_out) for the input gradient) and
@@ -491,12 +492,13 @@ namespace {
 // multiplies the n_own + nb rows of [H_in; S] (and its weight gradient runs
 // over them) and gathers nnz_s + nnz_in entries of width d_out (P_s and
 // P_in^T), and copies D's boundary rows (and pads D when d_out is not a
-// multiple of 4).  The rates are those measured for the aggregation kernels
-// (random row gathers), the fp32 MFMA GEMM and row copies on MI355X.
+// multiple of 4), and for a ReLU layer forms the masked D once.  The rates
+// are those measured for the aggregation kernels (random row gathers), the
+// fp32 MFMA GEMM and row copies on MI355X.
 constexpr double kGatherBytesPerS = 7.0e12;
 constexpr double kGemmFlopsPerS = 80.0e12;
 
-bool transform_first_cheaper(const digest_partition &p, int32_t layer)
+bool transform_first_cheaper(const digest_partition &p, int32_t layer, bool relu)
 {
     const double di = p.widths[layer - 1], dout = p.widths[layer];
     const double n = p.n_own, R = (double)p.n_own + (double)p.n_bnd;
@@ -506,8 +508,10 @@ bool transform_first_cheaper(const digest_partition &p, int32_t layer)
         (nnz_s * di + (dgrad ? nnz_in * std::min(di, dout) : 0.0)) * 4.0 / kGatherBytesPerS +
         2.0 * n * di * dout * (dgrad ? 3.0 : 2.0) / kGemmFlopsPerS;
     const double copies = 8.0 * p.n_bnd * dout +
-                          (p.widths[layer] % 4 ? 4.0 * n * (dout + padded_width(p.widths[layer]))
-                                               : 0.0);
+                          (relu ? 12.0 * n * dout
+                                : p.widths[layer] % 4
+                                      ? 4.0 * n * (dout + padded_width(p.widths[layer]))
+                                      : 0.0);
     const double tf = (nnz_s + nnz_in) * dout * 4.0 / kGatherBytesPerS +
                       (4.0 * R * di * dout + (dgrad ? 2.0 * n * di * dout : 0.0)) /
                           kGemmFlopsPerS +
@@ -611,12 +615,16 @@ void plan_layout(digest_partition &p)
         l.hagg[lev] = take(sizeof(float) * (size_t)p.n_bnd * padded_width(p.widths[lev]));
     }
     l.ah.assign(p.L + 1, 0);
-    int64_t hpad = 0;   // padded copies of h_in (odd d_in) or dh_out (odd d_out)
+    // padded copies of h_in (odd d_in) or dh_out (odd d_out), and a
+    // transform-first ReLU layer's masked D
+    int64_t hpad = 0;
     for (int32_t k = 1; k <= p.L; ++k) {
         l.ah[k] = take(sizeof(float) * (size_t)p.n_own * padded_width(p.widths[k - 1]));
         for (int32_t d : {p.widths[k - 1], p.widths[k]})
             if (d % 4)
                 hpad = std::max<int64_t>(hpad, (int64_t)p.n_own * padded_width(d));
+        if (transform_first_cheaper(p, k, true))
+            hpad = std::max<int64_t>(hpad, (int64_t)p.n_own * padded_width(p.widths[k]));
     }
     l.hpad = take(sizeof(float) * (size_t)hpad);
     int64_t wmax = 0, gemm_part = 0, tbuf = 0;
@@ -627,7 +635,9 @@ void plan_layout(digest_partition &p)
         splitk_plan(di, dout, p.n_own, splits, kchunk);
         if (splits > 1)
             gemm_part = std::max<int64_t>(gemm_part, (int64_t)splits * di * dout);
-        if (transform_first_cheaper(p, k)) {
+        // (the order depends on the activation the caller passes: room for
+        // either)
+        if (transform_first_cheaper(p, k, false) || transform_first_cheaper(p, k, true)) {
             // the second block of rows is the halo (with the halo gradient)
             // or the halo aggregate's boundary rows
             for (const int64_t n2 : {(int64_t)p.n_halo, (int64_t)p.n_bnd}) {
@@ -853,7 +863,7 @@ void plan_tiers(digest_partition &p)
     for (int32_t l = 1; l <= p.L; ++l) {
         const int32_t d_in = p.widths[l - 1], d_out = p.widths[l];
         const bool relu = l < p.L;
-        if (!relu && p.n_own > 0 && transform_first_cheaper(p, l))
+        if (p.n_own > 0 && transform_first_cheaper(p, l, relu))
             continue;
         want(Csr::InH, padded_width(d_in));
         if (l > 1)
@@ -1488,12 +1498,12 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
     if (p->gws && p->pull_mode == DIGEST_PULL_ROWS && p->n_own > 0)
         if (digest_status st = halo_aggregate(p, layer - 1, s))
             return st;
-    const bool tf = act == DIGEST_ACT_IDENTITY && transform_first_cheaper(*p, layer);
+    const bool tf = transform_first_cheaper(*p, layer, act == DIGEST_ACT_RELU);
     if (p->n_own > 0 && tf) {
         // T = [h_in; S] W over the owned and the boundary rows, then
-        // h_out = P_s T.  T's rows are padded to a multiple of 4 floats so
-        // that the aggregation gathers whole float4 vectors; it stores d_out
-        // columns
+        // h_out = act(P_s T).  T's rows are padded to a multiple of 4 floats
+        // so that the aggregation gathers whole float4 vectors; it stores
+        // d_out columns
         float *T = p->at<float>(p->lay.tbuf);
         const int32_t ldt = padded_width(d_out);
         {
@@ -1503,7 +1513,8 @@ digest_status digest_layer_forward(digest_partition *p, int32_t layer, const flo
         }
         if (digest_status st = run_spmm(p, Csr::InH, T, nullptr, p->n_own + p->n_bnd, ldt,
                                         h_out, layer, s, nullptr, -1, nullptr, INT32_MAX,
-                                        nullptr, false, nullptr, ldt, d_out, d_out))
+                                        nullptr, act == DIGEST_ACT_RELU, nullptr, ldt, d_out,
+                                        d_out))
             return st;
     } else if (p->n_own > 0) {
         // AH = P_s [h_in; S] = P_in h_in + P_out halo (kept for the backward),
@@ -1688,8 +1699,8 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
 // boundary rows: G_own = P_in^T D, and the boundary rows of G are D's rows
 // of the boundary nodes (P_s's halo-aggregate entries are ones).
 digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
-                                       const float *dh_out, const float *w, float *dw,
-                                       float *dh_in, float *dh_halo, hipStream_t s)
+                                       const float *h_out, const float *dh_out, const float *w,
+                                       float *dw, float *dh_in, float *dh_halo, hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     const bool via_s = !dh_halo;
@@ -1708,12 +1719,23 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                           digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
                           (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
     const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
-    // Without the epilogue (which reads the stored rows back), rows of a
+    // A ReLU layer's D is formed once, rows padded like G's.  Otherwise,
+    // without the epilogue (which reads the stored rows back), rows of a
     // width not a multiple of 4 are gathered from a padded copy of dh_out,
     // whole float4 vectors wide; G keeps the padding columns (never read).
     const float *src = dh_out;
-    int32_t dg = d_out;
-    if (!fused_dh && ldg != d_out && p->n_own > 0) {
+    int32_t dg = d_out, lsrc = d_out;   // gathered width, row stride of src
+    if (p->act[layer] == DIGEST_ACT_RELU && p->n_own > 0) {
+        float *dm = p->at<float>(p->lay.hpad);
+        Timed t(p, K_RELU_MASK, layer, s);
+        if (digest_status st = hip_check(digest::launch_relu_mask(p->n_own, d_out, dh_out, d_out,
+                                                                  h_out, d_out, dm, ldg, s),
+                                         "relu mask"))
+            return st;
+        src = dm;
+        lsrc = ldg;
+        dg = fused_dh ? d_out : ldg;   // the epilogue contracts exactly d_out columns
+    } else if (!fused_dh && ldg != d_out && p->n_own > 0) {
         float *dp = p->at<float>(p->lay.hpad);
         Timed t(p, K_PAD_ROWS, layer, s);
         if (digest_status st = hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_own,
@@ -1722,17 +1744,17 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
                                          "pad rows"))
             return st;
         src = dp;
-        dg = ldg;
+        dg = lsrc = ldg;
     }
     if (digest_status st = run_spmm(p, via_s ? Csr::InT : Csr::FullT, src, nullptr, p->n_own,
                                     dg, G, layer, s, fused_dh ? &ep : nullptr, -1, nullptr,
-                                    INT32_MAX, nullptr, false, nullptr, dg, ldg, dg))
+                                    INT32_MAX, nullptr, false, nullptr, lsrc, ldg, dg))
         return st;
     if (via_s && p->n_bnd > 0) {
         Timed t(p, K_BND_ROWS, layer, s);
         if (digest_status st = hip_check(
                 digest::launch_copy_rows(p->at<int32_t>(p->lay.bnd_local), nullptr, p->n_bnd, dg,
-                                         src, G + (int64_t)p->n_own * ldg, s, dg, ldg),
+                                         src, G + (int64_t)p->n_own * ldg, s, lsrc, ldg),
                 "boundary rows"))
             return st;
     }
@@ -1788,7 +1810,8 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
         dh_halo = nullptr;
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
     if (p->tf[layer] && p->n_own > 0)
-        return backward_transform_first(p, layer, h_in, dh_out, w, dw, dh_in, dh_halo, s);
+        return backward_transform_first(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_halo,
+                                        s);
     const bool relu = p->act[layer] == DIGEST_ACT_RELU;
     const float *ah = p->at<float>(p->lay.ah[layer]);
     // The fused input gradient: D = dh_out masked by the ReLU derivative is
@@ -2455,7 +2478,7 @@ digest_layer_plan layer_plan(const digest_partition &p, int32_t layer)
     digest_layer_plan pl{};
     const int32_t d_in = p.widths[layer - 1], d_out = p.widths[layer];
     const bool relu = layer < p.L;
-    pl.transform_first = !relu && p.n_own > 0 && transform_first_cheaper(p, layer);
+    pl.transform_first = p.n_own > 0 && transform_first_cheaper(p, layer, relu);
     pl.forward_narrow = narrow_out(d_in, d_out);
     pl.forward_fused = fuse_forward(p, layer, pl.transform_first);
     pl.backward_fused = fuse_backward(p, layer, pl.transform_first);
@@ -2557,7 +2580,9 @@ digest_status digest_profile_model(const digest_partition *p, int32_t model, dou
                 0.0, p->nnz_in);
             if (p->n_bnd > 0)
                 put(K_BND_ROWS, l, 8 * nb * dout + 4 * nb);
-            if (!pl.dgrad_fused && p->widths[l] % 4)   // the padded copy of dh_out
+            if (relu)   // D formed once
+                put(K_RELU_MASK, l, 12 * n * dout);
+            else if (!pl.dgrad_fused && p->widths[l] % 4)   // the padded copy of dh_out
                 put(K_PAD_ROWS, l, 4 * n * (dout + padded_width(p->widths[l])));
             put(K_GEMM_DW, l, 4 * (Rs * di + Rs * dout + di * dout), 2 * Rs * di * dout);
             put(K_REDUCE_DW, l, 4 * (pl.dw_slices + 1) * di * dout);

@@ -405,6 +405,28 @@ def test_pull_aggregate_mode():
     check_layer(c, 2)
 
 
+# ReLU layers computed transform-first, relu(P_s (H W)), where the output
+# is much narrower than the input: 600 -> 62 (D formed once, padded to 64
+# floats) and 300 -> 11 (the narrow epilogue writes dH_in from the gather of
+# D's 11 columns, rows 12 floats apart)
+RELU_TF = [(24, 600, 62, 7), (24, 300, 11, 5)]
+
+
+@pytest.mark.parametrize("widths", RELU_TF, ids=lambda w: "x".join(map(str, w)))
+def test_relu_transform_first(widths):
+    Dm = D()
+    cfg = synth.scaled(synth.CONFIGS["tiny"], 1500, widths=widths, classes=widths[-1])
+    g = synth.make_graph(cfg, seed=6)
+    c = Case(cfg, g, synth.make_partition(cfg, g, 1), label=f"relu-tf{widths}", ws_fill=255)
+    pl = Dm.digest_partition_plan(c.h, 2)
+    assert pl["transform_first"] == 1 and c.act(2) == oracle.RELU
+    assert pl["dgrad_fused"] == (1 if widths[2] <= 16 else 0)
+    for layer in range(1, c.L + 1):
+        check_layer(c, layer)
+    Dm.digest_partition_set_pull_mode(c.h, Dm.PULL_AGGREGATE)
+    check_layer(c, 2)
+
+
 def test_empty_partition():
     Dm = D()
     h = Dm.digest_partition_create(10, np.array([0]), np.zeros(0), np.zeros(0, np.float32),
