@@ -393,13 +393,13 @@ struct digest_partition {
     int64_t nnz_s = 0, nnz_b = 0;
     std::vector<int32_t> s_rowptr, s_col, b_rowptr, b_col;
     std::vector<int32_t> b_gcol;   // P_b's columns as global ids (the store's rows)
+    std::vector<float> s_val, b_val;
+    std::vector<SpmmBlock> blocks_s, blocks_b;
+    int32_t long_s = 0, long_b = 0;
     // DIGEST_PULL_ROWS: a pull fills the halo buffer, then S from it;
     // DIGEST_PULL_AGGREGATE: a pull forms S straight from the store and
     // leaves the halo buffer alone (the calls that read it refuse).
     int32_t pull_mode = DIGEST_PULL_ROWS;
-    std::vector<float> s_val, b_val;
-    std::vector<SpmmBlock> blocks_s, blocks_b;
-    int32_t long_s = 0, long_b = 0;
     // P_s split at kFuseLong entries per row: the long rows (their count and
     // entries) and the distinct source rows the short and the long rows read
     int64_t long_rows_f = 0, long_nnz_f = 0, src_short_f = 0, src_long_f = 0;
@@ -484,17 +484,16 @@ namespace {
 
 // Order of the two products of a layer (the same result, associated the
 // other way; a ReLU applies to the aggregated product either way).  Both
-// read the halo rows through
-// their aggregate S (nb boundary rows, formed at the pull).  Aggregate-first
-// gathers the nnz_s entries of P_s at width d_in (and, for layers > 1,
-// nnz_in entries of width min(d_in, d_out) for the input gradient) and
-// multiplies the n_own aggregated rows; transform-first, Z = P_s ([H_in; S] W),
-// multiplies the n_own + nb rows of [H_in; S] (and its weight gradient runs
-// over them) and gathers nnz_s + nnz_in entries of width d_out (P_s and
-// P_in^T), and copies D's boundary rows (and pads D when d_out is not a
-// multiple of 4), and for a ReLU layer forms the masked D once.  The rates
-// are those measured for the aggregation kernels (random row gathers), the
-// fp32 MFMA GEMM and row copies on MI355X.
+// orders read the halo rows through their aggregate S (nb boundary rows,
+// formed at the pull).  Aggregate-first gathers the nnz_s entries of P_s at
+// width d_in (and, for layers > 1, nnz_in entries of width min(d_in, d_out)
+// for the input gradient) and multiplies the n_own aggregated rows.
+// Transform-first, Z = P_s ([H_in; S] W), multiplies the n_own + nb rows of
+// [H_in; S] (its weight gradient runs over them too), gathers nnz_s + nnz_in
+// entries of width d_out (P_s and P_in^T) and copies D's boundary rows; a
+// ReLU layer forms the masked D once, an identity layer pads D when d_out
+// is not a multiple of 4.  The rates are those measured for the aggregation
+// kernels (random row gathers), the fp32 MFMA GEMM and row copies on MI355X.
 constexpr double kGatherBytesPerS = 7.0e12;
 constexpr double kGemmFlopsPerS = 80.0e12;
 
