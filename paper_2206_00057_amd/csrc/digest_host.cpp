@@ -184,8 +184,9 @@ void fuse_stats(const std::vector<int32_t> &rowptr, const std::vector<int32_t> &
 }
 
 // Aggregation blocks of a CSR: every long row gets a block of its own (those
-// come first, so they start early); runs of consecutive short rows are
-// packed one per wave.  Returns the number of long-row blocks.
+// come first, longest first, so that the longest start earliest and do not
+// set the launch's tail); runs of consecutive short rows are packed one per
+// wave.  Returns the number of long-row blocks.
 int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
                      std::vector<SpmmBlock> &blocks, int32_t long_row = digest::kSpmmLongRow)
 {
@@ -194,6 +195,9 @@ int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
     for (int32_t r = 0; r < n_rows; ++r)
         if (rowptr[r + 1] - rowptr[r] > long_row)
             blocks.push_back({r, 0, rowptr[r], rowptr[r + 1]});
+    std::stable_sort(blocks.begin(), blocks.end(), [](const SpmmBlock &a, const SpmmBlock &b) {
+        return a.ke - a.kb > b.ke - b.kb;
+    });
     const int32_t n_long = (int32_t)blocks.size();
     int32_t first = -1, count = 0;
     for (int32_t r = 0; r <= n_rows; ++r) {
