@@ -238,7 +238,10 @@ BACKWARD_HALO_CASES = [((24, 40, 6), True), ((24, 42, 6), True), ((24, 200, 48),
                          ids=[f"{w[1]}-{w[2]}" for w, _ in BACKWARD_HALO_CASES])
 def test_layer_backward_halo_matches_oracle(widths, tf):
     """The fused backward gives the separate calls' dw and dh_in and the halo
-    gradient, for ReLU (GEMM-first with the mask) and identity."""
+    gradient, for ReLU and identity.  The cost model picks the product order
+    per activation: the first three cases run transform-first with either
+    (a ReLU layer's masked D formed once), the last two aggregate first
+    (ReLU: GEMM-first with the mask)."""
     from paper_2206_00057_amd import digest as D
     cfg = synth.scaled(synth.CONFIGS["tiny"], 1200, widths=widths, classes=widths[-1])
     g = synth.make_graph(cfg, seed=4)
