@@ -89,21 +89,27 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int32_t padded_width(int32_t d) { return (d + 3) / 4 * 4; }
 
 // Split-K factor for a contraction with an M x N result over K: at least
-// kSplitTarget workgroups in all, at least kSplitMinRows rows of K per split,
+// `target` workgroups in all (kSplitTarget, or kSideSplitTarget on the side
+// stream), at least kSplitMinRows rows of K per split,
 // split starts on GEMM K-tile boundaries.  From that count up to twice it,
 // the split whose workgroups fill whole rounds of the chip's kCUs compute
 // units best is taken (the fewest splits among equals): a round of 800
 // workgroups on 256 CUs leaves most CUs idle for its last quarter.
 constexpr int64_t kSplitTarget = 768;
+// A weight gradient on the side stream runs next to the memory-bound
+// aggregations of the same backward: one workgroup per CU leaves them the
+// rest of each CU (OGB-Products-shaped round 6.82 -> 6.70 ms against 768).
+constexpr int64_t kSideSplitTarget = 256;
 constexpr int64_t kSplitMinRows = 256;
 constexpr int64_t kCUs = 256;
 
-void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchunk)
+void splitk_plan(int64_t M, int64_t N, int64_t K, int32_t &splits, int32_t &kchunk,
+                 int64_t target = kSplitTarget)
 {
     const int64_t tiles = std::max<int64_t>(1, ((M + digest::kGemmBM - 1) / digest::kGemmBM) *
                                                    ((N + digest::kGemmBN - 1) / digest::kGemmBN));
     const int64_t cap = std::min<int64_t>(256, std::max<int64_t>(1, K / kSplitMinRows));
-    const int64_t lo = std::max<int64_t>(1, std::min<int64_t>((kSplitTarget + tiles - 1) / tiles, cap));
+    const int64_t lo = std::max<int64_t>(1, std::min<int64_t>((target + tiles - 1) / tiles, cap));
     // the split count and K-chunk that a requested count rounds to
     auto realise = [&](int64_t want, int64_t &chunk) {
         chunk = (K + want - 1) / want;
@@ -1842,7 +1848,8 @@ digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_
         g.B = gd;
         g.ldb = ldd;
         g.b_mask = relu && !fused ? h_out : nullptr;
-        splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk);
+        splitk_plan(d_in, d_out, p->n_own, g.splits, g.kchunk,
+                    sw != s ? kSideSplitTarget : kSplitTarget);
         g.tile = gemm_tile_for(d_in, d_out, p->n_own, true);
         float *gpart = p->at<float>(p->lay.gemm_part);
         g.C = g.splits > 1 ? gpart : dw;
