@@ -143,9 +143,8 @@ digest_status digest_partition_read_halo(const digest_partition *p, int32_t leve
  *   DIGEST_PULL_AGGREGATE: the halo aggregate alone, gathered straight from
  *     the store; the halo buffer is left alone, so a pull moves the halo
  *     rows once instead of twice.  For callers that use the GCN layer only:
- *     the calls that read halo rows (the GAT layer, the halo read-back, and
- *     digest_layer_backward_halo of a transform-first layer) return
- *     DIGEST_ESTATE while a level pulled this way is in use.
+ *     the calls that read halo rows (the GAT layer and the halo read-back)
+ *     return DIGEST_ESTATE.
  * A change of mode marks every level as not pulled.  Callers that capture
  * graphs set the mode before the capture.
  * Errors: DIGEST_EINVAL (NULL, unknown mode).
@@ -265,17 +264,16 @@ digest_status digest_halo_gradient(digest_partition *p, int32_t layer, const flo
  * Layer backward with the halo gradient (the appendix's DIGEST backward
  * with its stale-gradient term): the outputs of digest_layer_backward
  * (dw, dh_in) and the dh_halo of digest_halo_gradient, from shared
- * products.  The transposed aggregation runs over all of P_m^T, so D W^T
- * (or P_m^T D) is formed once for the owned and the halo rows.
+ * products.  Aggregating first, the transposed aggregation runs over all of
+ * P_m^T, so D W^T is formed once for the owned and the halo rows;
+ * transform-first, P_in^T D and P_out^T D share D (and its ReLU mask).
  *   layer 2..L;  dh_in device [n_owned, d_{layer-1}] (required when
  *   n_owned > 0);  dh_halo device [n_halo, d_{layer-1}] (required when
  *   n_halo > 0); other arguments as for digest_layer_backward.
  * Results equal those of the two separate calls up to float32 rounding
  * order.
  * Errors: those of digest_layer_backward; DIGEST_EINVAL for layer 1 or a
- * NULL dh_in / dh_halo; DIGEST_ESTATE for a transform-first layer (its
- * weight gradient then reads the halo rows) in pull mode
- * DIGEST_PULL_AGGREGATE.
+ * NULL dh_in / dh_halo.
  */
 digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, const float *h_in,
                                          const float *h_out, const float *dh_out,

@@ -1701,40 +1701,40 @@ digest_status weight_grad_rows(digest_partition *p, int32_t layer, const float *
     return DIGEST_OK;
 }
 
-// dW = H_mix^T G and dh_in = G_own W^T for a transform-first layer.  With
-// dh_halo, G = P_m^T D over all local rows and H_mix = [h_in; halo]: the
-// halo rows of G feed dW and the halo gradient G_halo W^T.  Without it,
-// G = P_s^T D and H_mix = [h_in; S], the same dW from the owned and the
-// boundary rows: G_own = P_in^T D, and the boundary rows of G are D's rows
-// of the boundary nodes (P_s's halo-aggregate entries are ones).
+// dW = [h_in; S]^T G and dh_in = G_own W^T for a transform-first layer,
+// with G = P_s^T D: G_own = P_in^T D over the owned rows, and the boundary
+// rows of G are D's rows of the boundary nodes (P_s's halo-aggregate
+// entries are ones), the same dW as [h_in; halo]^T P_m^T D.  With dh_halo,
+// the halo rows' gradient (P_out^T D) W^T comes from one more aggregation
+// over P_out^T, into G's rows past the owned ones before the boundary rows
+// take their place.  D = dh_out, or for a ReLU layer dh_out masked by
+// h_out > 0, formed once (padded rows) before the transposed aggregations.
 digest_status backward_transform_first(digest_partition *p, int32_t layer, const float *h_in,
                                        const float *h_out, const float *dh_out, const float *w,
                                        float *dw, float *dh_in, float *dh_halo, hipStream_t s)
 {
     const int32_t d_in = p->widths[layer - 1], d_out = p->widths[layer];
-    const bool via_s = !dh_halo;
-    const float *h2 = via_s ? (p->n_bnd > 0 ? p->at<float>(p->lay.hagg[layer - 1]) : nullptr)
-                            : (p->n_halo > 0 ? p->at<float>(p->lay.halo_buf[layer - 1]) : nullptr);
-    const int32_t n2 = via_s ? p->n_bnd : p->n_halo;
+    const float *hs = p->n_bnd > 0 ? p->at<float>(p->lay.hagg[layer - 1]) : nullptr;
     // G's rows are padded like T's, so that the products that read it load
     // whole vectors
     float *G = p->at<float>(p->lay.tbuf);
     const int32_t ldg = padded_width(d_out);
+    float *G2 = G + (int64_t)p->n_own * ldg;   // the halo, then the boundary rows
     float *gpart = p->at<float>(p->lay.gemm_part);
-    // G = P_m^T dh_out over owned and halo rows, or P_in^T dh_out over the
-    // owned rows; when the widths allow, the same launch also writes
-    // dh_in = G_own W^T for the owned rows.
+    // When the widths allow, the transposed aggregations also write their
+    // rows times W^T: dh_in for the owned rows, dh_halo for the halo rows.
     const bool fused_dh = dh_in && p->n_own > 0 && narrow_valu(d_in, d_out) &&
                           digest::spmm_epilogue_ok(d_out, d_in, dh_in) &&
                           (!dh_halo || digest::spmm_epilogue_ok(d_out, d_in, dh_halo));
-    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, dh_halo};
+    const digest::SpmmEpilogue ep{w, p->n_own, d_in, dh_in, nullptr};
+    const digest::SpmmEpilogue ep_halo{w, 0, d_in, nullptr, dh_halo};
     // A ReLU layer's D is formed once, rows padded like G's.  Otherwise,
     // without the epilogue (which reads the stored rows back), rows of a
     // width not a multiple of 4 are gathered from a padded copy of dh_out,
     // whole float4 vectors wide; G keeps the padding columns (never read).
     const float *src = dh_out;
     int32_t dg = d_out, lsrc = d_out;   // gathered width, row stride of src
-    if (p->act[layer] == DIGEST_ACT_RELU && p->n_own > 0) {
+    if (p->act[layer] == DIGEST_ACT_RELU) {
         float *dm = p->at<float>(p->lay.hpad);
         Timed t(p, K_RELU_MASK, layer, s);
         if (digest_status st = hip_check(digest::launch_relu_mask(p->n_own, d_out, dh_out, d_out,
@@ -1744,7 +1744,7 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
         src = dm;
         lsrc = ldg;
         dg = fused_dh ? d_out : ldg;   // the epilogue contracts exactly d_out columns
-    } else if (!fused_dh && ldg != d_out && p->n_own > 0) {
+    } else if (!fused_dh && ldg != d_out) {
         float *dp = p->at<float>(p->lay.hpad);
         Timed t(p, K_PAD_ROWS, layer, s);
         if (digest_status st = hip_check(digest::launch_copy_rows(nullptr, nullptr, p->n_own,
@@ -1755,43 +1755,47 @@ digest_status backward_transform_first(digest_partition *p, int32_t layer, const
         src = dp;
         dg = lsrc = ldg;
     }
-    if (digest_status st = run_spmm(p, via_s ? Csr::InT : Csr::FullT, src, nullptr, p->n_own,
-                                    dg, G, layer, s, fused_dh ? &ep : nullptr, -1, nullptr,
-                                    INT32_MAX, nullptr, false, nullptr, lsrc, ldg, dg))
+    if (digest_status st = run_spmm(p, Csr::InT, src, nullptr, p->n_own, dg, G, layer, s,
+                                    fused_dh ? &ep : nullptr, -1, nullptr, INT32_MAX, nullptr,
+                                    false, nullptr, lsrc, ldg, dg))
         return st;
-    if (via_s && p->n_bnd > 0) {
+    if (dh_halo) {
+        // G_halo = P_out^T D; dh_halo = G_halo W^T (in the same launch when
+        // the epilogue applies)
+        if (digest_status st = run_spmm(p, Csr::HaloT, src, nullptr, p->n_own, dg, G2, layer, s,
+                                        fused_dh ? &ep_halo : nullptr, K_HALO_GRAD, nullptr,
+                                        INT32_MAX, nullptr, false, nullptr, lsrc, ldg, dg))
+            return st;
+        if (!fused_dh) {
+            Timed tm(p, K_HALO_GRAD, layer, s);
+            if (digest_status st = times_wt(p->n_halo, d_in, d_out, G2, ldg, w, dh_halo, s))
+                return st;
+        }
+    }
+    if (p->n_bnd > 0) {
         Timed t(p, K_BND_ROWS, layer, s);
         if (digest_status st = hip_check(
                 digest::launch_copy_rows(p->at<int32_t>(p->lay.bnd_local), nullptr, p->n_bnd, dg,
-                                         src, G + (int64_t)p->n_own * ldg, s, lsrc, ldg),
+                                         src, G2, s, lsrc, ldg),
                 "boundary rows"))
             return st;
     }
-    // The weight gradient and the products by W^T both only read G.  A
-    // large weight gradient runs on the side stream next to them (neither
-    // kind keeps the MFMA units busy alone on these narrow shapes), joined
-    // back before the call returns.
+    // The weight gradient and the product by W^T both only read G.  A large
+    // weight gradient runs on the side stream next to it (neither kind keeps
+    // the MFMA units busy alone on these narrow shapes), joined back before
+    // the call returns.
     hipStream_t sw = s;
-    const bool more = !fused_dh && (dh_in || (dh_halo && p->n_halo > 0));
-    if (more && side_pays(2.0 * ((double)p->n_own + n2) * d_in * d_out))
+    if (!fused_dh && dh_in && side_pays(2.0 * ((double)p->n_own + p->n_bnd) * d_in * d_out))
         if (digest_status st = fork_side(p, s, &sw))
             return st;
     const digest_status st_all = [&]() -> digest_status {
-        if (digest_status st = weight_grad_rows(p, layer, h_in, h2, n2, G, ldg, gpart, dw, sw,
-                                                K_GEMM_DW, K_REDUCE_DW))
+        if (digest_status st = weight_grad_rows(p, layer, h_in, hs, p->n_bnd, G, ldg, gpart, dw,
+                                                sw, K_GEMM_DW, K_REDUCE_DW))
             return st;
-        if (fused_dh)
+        if (fused_dh || !dh_in)
             return DIGEST_OK;
-        if (dh_in) {
-            Timed tm(p, K_GEMM_DH, layer, s);
-            if (digest_status st = times_wt(p->n_own, d_in, d_out, G, ldg, w, dh_in, s))
-                return st;
-        }
-        if (!dh_halo || p->n_halo == 0)
-            return DIGEST_OK;
-        Timed tm(p, K_HALO_GRAD, layer, s);
-        return times_wt(p->n_halo, d_in, d_out, G + (int64_t)p->n_own * ldg, ldg, w, dh_halo,
-                        s);
+        Timed tm(p, K_GEMM_DH, layer, s);
+        return times_wt(p->n_own, d_in, d_out, G, ldg, w, dh_in, s);
     }();
     if (sw != s) {
         const digest_status st = join_side(p, s);
@@ -1808,9 +1812,10 @@ namespace {
 
 // The layer backward of both entry points.  With dh_halo (layer >= 2, dh_in
 // given) the halo rows' gradient P_out^T D W^T comes out of the same
-// products: the transposed aggregation runs over all of P_m^T, its owned
-// rows into dh_in and its halo rows into dh_halo (or, aggregating first,
-// into the halo scratch that one more product by W^T finishes).
+// products: aggregating first, the transposed aggregation runs over all of
+// P_m^T, its owned rows into dh_in and its halo rows into dh_halo (or into
+// the halo scratch that one more product by W^T finishes); transform-first,
+// one more aggregation over P_out^T (backward_transform_first).
 digest_status layer_backward(digest_partition *p, int32_t layer, const float *h_in,
                              const float *h_out, const float *dh_out, const float *w, float *dw,
                              float *dh_in, float *dh_halo, hipStream_t s)
@@ -2028,9 +2033,6 @@ digest_status digest_layer_backward_halo(digest_partition *p, int32_t layer, con
         return fail(DIGEST_EINVAL, "NULL dh_in or dh_halo");
     if (digest_status st = check_backward(p, layer, h_in, h_out, dh_out, w, dw))
         return st;
-    if (p->tf[layer] && p->n_own > 0 && p->n_halo > 0 && p->pull_mode != DIGEST_PULL_ROWS)
-        return fail(DIGEST_ESTATE, "the weight gradient of a transform-first layer with the "
-                                   "halo gradient reads halo rows, which the pull mode skips");
     return layer_backward(p, layer, h_in, h_out, dh_out, w, dw, dh_in, dh_halo,
                           (hipStream_t)hip_stream);
 }

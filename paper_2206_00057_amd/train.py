@@ -78,11 +78,10 @@ class DigestTrainer:
         self.n_global = int(n_global)
         self.lr, self.K = float(lr), int(K)
         self.W = weights
-        # the halo-gradient exchange runs the halo variant of the backward,
-        # whose transform-first layers read the halo rows
-        pull_mode = D.PULL_ROWS if grad_exchange != "none" or model == "gat" else D.PULL_AGGREGATE
-        self.gps = [GpuPartition(n_global, p, widths, device=device, model=model, atts=atts,
-                                 pull_mode=pull_mode) for p in parts]
+        # pulls keep the halo aggregate alone for GCN layers, the halo rows
+        # for GAT layers (GpuPartition's default)
+        self.gps = [GpuPartition(n_global, p, widths, device=device, model=model, atts=atts)
+                    for p in parts]
         self.push_mode = boundary_push_mode(self.gps, parts)
         idx = [torch.from_numpy(p.owned).to(device) for p in parts]
         self.x_own = [x.index_select(0, i).contiguous() for i in idx]

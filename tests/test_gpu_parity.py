@@ -350,9 +350,9 @@ def test_halo_aggregate_follows_pulls():
 def test_pull_aggregate_mode():
     """In the aggregate-only pull mode a pull forms the halo aggregate from
     the store's rows (here 42 floats wide, not a multiple of 4) and keeps no
-    halo rows: forward and backward still match the oracle after each pull,
-    the calls that read halo rows refuse, and switching back to the rows
-    mode needs a new pull."""
+    halo rows: forward and backward (with the halo gradient too) still match
+    the oracle after each pull, the calls that read halo rows refuse, and
+    switching back to the rows mode needs a new pull."""
     Dm = D()
     cfg = synth.scaled(synth.CONFIGS["tiny"], 1500, widths=(36, 42, 12), classes=12)
     g = synth.make_graph(cfg, seed=9)
@@ -371,20 +371,25 @@ def test_pull_aggregate_mode():
         Dm.digest_layer_forward(c.h, layer, dev(h_in), dev(W), out, c.act(layer))
         ref = c.op.forward(layer, h_in, W, c.act(layer))
         assert_close(host(out), ref, f"second pull forward layer {layer}")
+    # the halo variant of the (transform-first) backward needs no halo rows
+    h_in = c.layer_input(2)
+    W = synth.weights(c.cfg)[1]
+    ref = c.op.forward(2, h_in, W, c.act(2))
+    dh = c.upstream(2)
+    dw = torch.empty(W.shape, device="cuda")
+    dh_in = torch.empty(c.n, c.widths[1], device="cuda")
+    dh_halo = torch.full((c.part.n_halo, c.widths[1]), float("nan"), device="cuda")
+    Dm.digest_layer_backward_halo(c.h, 2, dev(h_in), dev(ref), dev(dh), dev(W), dw, dh_in,
+                                  dh_halo)
+    ref_dw, ref_dh = c.op.backward(2, h_in, W, ref, dh, c.act(2), want_dh_in=True)
+    assert_close(host(dw), ref_dw, "aggregate mode, halo variant dW")
+    assert_close(host(dh_in), ref_dh, "aggregate mode, halo variant dH_in")
+    assert_close(host(dh_halo), c.op.halo_gradient(2, W, ref, dh, c.act(2)),
+                 "aggregate mode, halo gradient")
     # the calls that read halo rows refuse
     with pytest.raises(Dm.DigestError) as e:
         Dm.digest_partition_read_halo(c.h, 1, torch.empty(c.part.n_halo, c.widths[1],
                                                            device="cuda"))
-    assert e.value.status == Dm.ESTATE
-    h_in = c.layer_input(2)
-    W = synth.weights(c.cfg)[1]
-    ref = c.op.forward(2, h_in, W, c.act(2))
-    dw = torch.empty(W.shape, device="cuda")
-    dh_in = torch.empty(c.n, c.widths[1], device="cuda")
-    dh_halo = torch.empty(c.part.n_halo, c.widths[1], device="cuda")
-    with pytest.raises(Dm.DigestError) as e:
-        Dm.digest_layer_backward_halo(c.h, 2, dev(h_in), dev(ref), dev(c.upstream(2)), dev(W),
-                                      dw, dh_in, dh_halo)
     assert e.value.status == Dm.ESTATE
     gat_ws = torch.empty(max(Dm.digest_gat_query(c.h), 256), dtype=torch.uint8, device="cuda")
     Dm.digest_gat_bind_workspace(c.h, gat_ws)
