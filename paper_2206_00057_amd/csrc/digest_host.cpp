@@ -190,20 +190,24 @@ void fuse_stats(const std::vector<int32_t> &rowptr, const std::vector<int32_t> &
 }
 
 // Aggregation blocks of a CSR: every long row gets a block of its own (those
-// come first, longest first, so that the longest start earliest and do not
-// set the launch's tail); runs of consecutive short rows are packed one per
-// wave.  Returns the number of long-row blocks.
+// come first, by default longest first, so that the longest start earliest
+// and do not set the launch's tail; else in row order); runs of consecutive
+// short rows are packed one per wave.  Returns the number of long-row
+// blocks.
 int32_t build_blocks(const std::vector<int32_t> &rowptr, int32_t n_rows,
-                     std::vector<SpmmBlock> &blocks, int32_t long_row = digest::kSpmmLongRow)
+                     std::vector<SpmmBlock> &blocks, bool longest_first = true,
+                     int32_t long_row = digest::kSpmmLongRow)
 {
     const int32_t waves = digest::kSpmmThreads / 64;
     blocks.clear();
     for (int32_t r = 0; r < n_rows; ++r)
         if (rowptr[r + 1] - rowptr[r] > long_row)
             blocks.push_back({r, 0, rowptr[r], rowptr[r + 1]});
-    std::stable_sort(blocks.begin(), blocks.end(), [](const SpmmBlock &a, const SpmmBlock &b) {
-        return a.ke - a.kb > b.ke - b.kb;
-    });
+    if (longest_first)
+        std::stable_sort(blocks.begin(), blocks.end(),
+                         [](const SpmmBlock &a, const SpmmBlock &b) {
+                             return a.ke - a.kb > b.ke - b.kb;
+                         });
     const int32_t n_long = (int32_t)blocks.size();
     int32_t first = -1, count = 0;
     for (int32_t r = 0; r <= n_rows; ++r) {
@@ -366,8 +370,8 @@ TierPlan plan_one_tier(int32_t which, const std::vector<int32_t> &rowptr,
         std::vector<SpmmBlock> b;
         // the sliced passes' strip kernel takes every row up to
         // kTierLongRow entries; only longer rows get a workgroup each
-        const int32_t n_long = build_blocks(rp, n_rows, b, c < T ? digest::kTierLongRow
-                                                                 : digest::kSpmmLongRow);
+        const int32_t n_long = build_blocks(rp, n_rows, b, true,
+                                            c < T ? digest::kTierLongRow : digest::kSpmmLongRow);
         t.blk_off.push_back((int32_t)t.blocks.size());
         t.blk_cnt.push_back((int32_t)b.size());
         t.blk_long.push_back(n_long);
@@ -406,6 +410,11 @@ struct digest_partition {
     std::vector<float> s_val, b_val;
     std::vector<SpmmBlock> blocks_s, blocks_b;
     int32_t long_s = 0, long_b = 0;
+    // P_s and P_in^T with their long rows in row order, for the aggregations
+    // of rows of at most kNarrowWide floats (whose long rows are short work:
+    // longest first measured 10-13 us slower on the OGB-Products-shaped
+    // 48-float layer)
+    std::vector<SpmmBlock> blocks_s_rows, blocks_t_rows;
     // DIGEST_PULL_ROWS: a pull fills the halo buffer, then S from it;
     // DIGEST_PULL_AGGREGATE: a pull forms S straight from the store and
     // leaves the halo buffer alone (the calls that read it refuse).
@@ -429,6 +438,7 @@ struct digest_partition {
         size_t rowptr, col, val, t_rowptr, t_src, t_val, halo_gid, bnd_local, bnd_gid, owned_gid;
         size_t blocks_f, blocks_t, blocks_tf, blocks_th;
         size_t s_rowptr, s_col, s_val, b_rowptr, b_col, b_gcol, b_val, blocks_s, blocks_b;
+        size_t blocks_s_rows, blocks_t_rows;
         size_t fuse_order, fuse_order_t;   // per owned row, uint8 (see fuse_order below)
         size_t fz;                      // the fused input gradient's D and long rows
         size_t wt;                      // W^T of the fused input gradient
@@ -616,6 +626,8 @@ void plan_layout(digest_partition &p)
     l.b_gcol = take(sizeof(int32_t) * p.b_gcol.size());
     l.b_val = take(sizeof(float) * p.b_val.size());
     l.blocks_s = take(sizeof(SpmmBlock) * p.blocks_s.size());
+    l.blocks_s_rows = take(sizeof(SpmmBlock) * p.blocks_s_rows.size());
+    l.blocks_t_rows = take(sizeof(SpmmBlock) * p.blocks_t_rows.size());
     l.blocks_b = take(sizeof(SpmmBlock) * p.blocks_b.size());
     l.halo_buf.assign(p.L, 0);
     l.hagg.assign(p.L, 0);
@@ -937,11 +949,14 @@ digest_status run_spmm(digest_partition *p, Csr which, const float *src0, const 
     size_t o_rowptr = fwd ? p->lay.rowptr : p->lay.t_rowptr;
     size_t o_col = fwd ? p->lay.col : p->lay.t_src;
     size_t o_val = fwd ? p->lay.val : p->lay.t_val;
+    const bool narrow = d <= digest::kNarrowWide;
     if (which == Csr::InH) {
-        blocks = &p->blocks_s, boff = p->lay.blocks_s, n_long = p->long_s;
+        blocks = &p->blocks_s, boff = narrow ? p->lay.blocks_s_rows : p->lay.blocks_s;
+        n_long = p->long_s;
         o_rowptr = p->lay.s_rowptr, o_col = p->lay.s_col, o_val = p->lay.s_val;
     } else if (which == Csr::InT) {
-        blocks = &p->blocks_t, boff = p->lay.blocks_t, n_long = p->long_t;
+        blocks = &p->blocks_t, boff = narrow ? p->lay.blocks_t_rows : p->lay.blocks_t;
+        n_long = p->long_t;
     } else if (which == Csr::FullT) {
         blocks = &p->blocks_tf, boff = p->lay.blocks_tf, n_long = p->long_tf;
     } else if (which == Csr::HaloT) {
@@ -1218,10 +1233,12 @@ digest_status digest_partition_create(int64_t n_global, const int64_t *indptr,
             p->b_gcol[k] = p->halo_gid[p->b_col[k]];
         p->long_f = build_blocks(p->rowptr, p->n_own, p->blocks_f);
         p->long_s = build_blocks(p->s_rowptr, p->n_own, p->blocks_s);
+        build_blocks(p->s_rowptr, p->n_own, p->blocks_s_rows, false);
         p->long_b = build_blocks(p->b_rowptr, p->n_bnd, p->blocks_b);
         fuse_stats(p->s_rowptr, p->s_col, (int32_t)n_owned, p->n_own + p->n_bnd, p->long_rows_f,
                    p->long_nnz_f, p->src_short_f, p->src_long_f, p->fuse_order);
         p->long_t = build_blocks(p->t_rowptr, p->n_own, p->blocks_t);
+        build_blocks(p->t_rowptr, p->n_own, p->blocks_t_rows, false);
         fuse_stats(p->t_rowptr, p->t_src, (int32_t)n_owned, p->n_own, p->long_rows_t,
                    p->long_nnz_t, p->src_short_t, p->src_long_t, p->fuse_order_t);
         p->long_tf = build_blocks(p->t_rowptr, p->n_own + p->n_halo, p->blocks_tf);
@@ -1328,6 +1345,8 @@ digest_status digest_partition_bind_workspace(digest_partition *p, void *dev_ptr
         {l.b_gcol, p->b_gcol.data(), sizeof(int32_t) * p->b_gcol.size()},
         {l.b_val, p->b_val.data(), sizeof(float) * p->b_val.size()},
         {l.blocks_s, p->blocks_s.data(), sizeof(SpmmBlock) * p->blocks_s.size()},
+        {l.blocks_s_rows, p->blocks_s_rows.data(), sizeof(SpmmBlock) * p->blocks_s_rows.size()},
+        {l.blocks_t_rows, p->blocks_t_rows.data(), sizeof(SpmmBlock) * p->blocks_t_rows.size()},
         {l.blocks_b, p->blocks_b.data(), sizeof(SpmmBlock) * p->blocks_b.size()},
     };
     for (const Up &u : ups) {
